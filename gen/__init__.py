@@ -1,0 +1,230 @@
+"""Seeded synthetic inputs for one TriRoute-routed layer.
+
+This module only draws numbers: shapes, value distributions and routing
+mixes of the five workloads (160M-1.3B-class layers, Table 2 shapes).  It holds
+none of the layer's arithmetic, so both the CPU oracle and the GPU path can
+take their inputs from here.
+
+Every tensor is drawn from its own PCG64 stream keyed by (seed, tensor name,
+optional index), so the draw order never changes a value.  Values are drawn in
+fp32 and rounded once (round-to-nearest-even) to the activation dtype; both
+sides receive exactly those values.
+
+Router head biases are not drawn: they are the per-workload calibrated values
+stored in ``router_bias.json`` (written by the oracle's calibration script),
+so that the hard decisions split as each workload asks.
+"""
+from __future__ import annotations
+
+import json
+import os
+import zlib
+
+import numpy as np
+
+BITS = (2, 4, 8, 16)
+MODES = ("skip", "local", "full")
+D_PSI = 8
+D_ROUTER = 128
+
+# Workload table.  Fractions are listed in the order of the enumerations:
+# modes (skip, local, full), bit widths (2, 4, 8, 16).  ``experts`` is the
+# target share of top-k assignments over the E+1 options (index 0 = null).
+CONFIGS = {
+    "tiny_f32_prefill": dict(
+        kind="prefill", B=1, T=128, d=256, H=4, Hkv=1, dh=64, w=32, E=4, k=1,
+        d_ff=512, G=32, act="f32", seeds=(0,),
+        modes=(0.30, 0.40, 0.30), bits=(0.25, 0.25, 0.25, 0.25),
+        experts="uniform"),
+    "160m_bf16_prefill": dict(
+        kind="prefill", B=8, T=2048, d=768, H=12, Hkv=3, dh=64, w=128, E=8,
+        k=2, d_ff=2048, G=64, act="bf16", seeds=(1, 2, 3),
+        modes=(0.25, 0.45, 0.30), bits=(0.15, 0.35, 0.35, 0.15),
+        experts="uniform"),
+    "410m_bf16_decode": dict(
+        kind="decode", B=64, T=1, ctx=8192, d=1024, H=16, Hkv=4, dh=64, w=256,
+        E=8, k=2, d_ff=2816, G=64, act="bf16", seeds=(103,),
+        modes=(0.25, 0.45, 0.30), bits=(0.20, 0.40, 0.30, 0.10),
+        ctx_bits=(0.20, 0.40, 0.30, 0.10), experts="uniform"),
+    "1p3b_bf16_prefill": dict(
+        kind="prefill", B=4, T=4096, d=2048, H=16, Hkv=4, dh=128, w=512, E=16,
+        k=2, d_ff=5632, G=64, act="bf16", seeds=(104,),
+        modes=(0.20, 0.50, 0.30), bits=(0.15, 0.35, 0.35, 0.15),
+        experts="uniform"),
+    "1p3b_bf16_decode": dict(
+        kind="decode", B=32, T=1, ctx=32768, d=2048, H=16, Hkv=4, dh=128,
+        w=1024, E=16, k=2, d_ff=5632, G=64, act="bf16", seeds=(105,),
+        modes=(0.20, 0.50, 0.30), bits=(0.70, 0.20, 0.0, 0.10),
+        ctx_bits=(0.70, 0.20, 0.0, 0.10), experts="skewed"),
+}
+
+_BIAS_FILE = os.path.join(os.path.dirname(__file__), "router_bias.json")
+
+
+def expert_targets(cfg: dict) -> np.ndarray:
+    """Target share of assignments per option 0..E (0 = null)."""
+    E = cfg["E"]
+    if cfg["experts"] == "uniform":
+        return np.full(E + 1, 1.0 / (E + 1))
+    if cfg["experts"] == "skewed":
+        # two hot experts take 30% each, the null 15%, the rest share 25%
+        t = np.full(E + 1, 0.25 / (E - 2))
+        t[0], t[1], t[2] = 0.15, 0.30, 0.30
+        return t
+    raise ValueError(cfg["experts"])
+
+
+def stream(seed: int, name: str, *index: int) -> np.random.Generator:
+    key = [int(seed), zlib.crc32(name.encode())] + [int(i) for i in index]
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(key)))
+
+
+def round_bf16(a: np.ndarray) -> np.ndarray:
+    """Round fp32 values to the nearest bf16 (ties to even); returns fp32."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    u = a.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32)
+
+
+def to_act(a: np.ndarray, act: str) -> np.ndarray:
+    if act == "bf16":
+        return round_bf16(a)
+    if act == "f32":
+        return np.ascontiguousarray(a, dtype=np.float32)
+    if act == "f64":
+        return np.ascontiguousarray(a, dtype=np.float64)
+    raise ValueError(act)
+
+
+def normal(seed, name, shape, std=1.0, *index):
+    g = stream(seed, name, *index)
+    return (g.standard_normal(shape, dtype=np.float32) * np.float32(std))
+
+
+def load_biases() -> dict:
+    if not os.path.exists(_BIAS_FILE):
+        return {}
+    with open(_BIAS_FILE) as f:
+        return json.load(f)
+
+
+def bias_key(name: str, seed: int) -> str:
+    return f"{name}/seed{seed}"
+
+
+def token_psi(seed: int, n_tok: int, rel_pos: np.ndarray) -> np.ndarray:
+    """Side features: psi_0 = relative position, psi_1..7 ~ N(0, 1)."""
+    psi = np.empty((n_tok, D_PSI), np.float32)
+    psi[:, 0] = rel_pos
+    psi[:, 1:] = normal(seed, "psi", (n_tok, D_PSI - 1))
+    return psi
+
+
+def resample_psi_row(seed: int, token: int, attempt: int) -> np.ndarray:
+    """Fresh psi_1..7 for one token (used to move a token off a routing tie)."""
+    return stream(seed, "psi_resample", token, attempt).standard_normal(
+        D_PSI - 1, dtype=np.float32)
+
+
+def make_layer(name: str, seed: int | None = None, *, act: str | None = None,
+               with_moe: bool = True, biases: dict | None = None) -> dict:
+    """Draw every input of one routed layer for workload ``name``.
+
+    Returns a dict with ``cfg`` (shape fields plus ``name``/``seed``/``act``),
+    the activations ``x`` [N, d] and ``psi`` [N, 8], fp32 router weights, the
+    act-dtype attention / expert weights, and per-token positions.
+    """
+    cfg = dict(CONFIGS[name])
+    seed = cfg["seeds"][0] if seed is None else seed
+    act = act or cfg["act"]
+    cfg.update(name=name, seed=seed, act=act)
+    B, T, d, H, Hkv, dh = (cfg[k] for k in ("B", "T", "d", "H", "Hkv", "dh"))
+    E, dff = cfg["E"], cfg["d_ff"]
+    N = B * T
+    L = {"cfg": cfg}
+    L["x"] = to_act(normal(seed, "x", (N, d)), act)
+    if cfg["kind"] == "prefill":
+        rel = np.tile(np.arange(T, dtype=np.float32) / np.float32(T), B)
+    else:
+        ctx = cfg["ctx"]
+        rel = np.full(N, np.float32(ctx) / np.float32(ctx + 1), np.float32)
+    L["psi"] = token_psi(seed, N, rel)
+    # router (fp32 end to end); whitening and the gradient-balance scale are
+    # already folded into the head weights and biases
+    dr = D_ROUTER
+    L["g1"] = to_act(1.0 + normal(seed, "g1", (d,), 0.02), act)
+    L["W1"] = normal(seed, "W1", (dr, d + D_PSI), 0.02)
+    L["b1"] = normal(seed, "b1", (dr,), 0.02)
+    L["W2"] = normal(seed, "W2", (dr, dr), 0.02)
+    L["b2"] = normal(seed, "b2", (dr,), 0.02)
+    L["gr"] = 1.0 + normal(seed, "gr", (dr,), 0.02)
+    L["Wa"] = normal(seed, "Wa", (3 * H, dr), 0.02)
+    L["We"] = normal(seed, "We", (E + 1, dr), 0.02)
+    L["Wb"] = normal(seed, "Wb", (4, dr), 0.02)
+    biases = load_biases() if biases is None else biases
+    bk = biases.get(bias_key(name, seed))
+    if bk is not None:
+        L["ca"] = np.asarray(bk["ca"], np.float32)
+        L["ce"] = np.asarray(bk["ce"], np.float32)
+        L["cb"] = np.asarray(bk["cb"], np.float32)
+    else:
+        L["ca"] = np.zeros(3 * H, np.float32)
+        L["ce"] = np.zeros(E + 1, np.float32)
+        L["cb"] = np.zeros(4, np.float32)
+    # attention projections and the second norm gain (act dtype)
+    L["Wq"] = to_act(normal(seed, "Wq", (H * dh, d), 0.02), act)
+    L["Wk"] = to_act(normal(seed, "Wk", (Hkv * dh, d), 0.02), act)
+    L["Wv"] = to_act(normal(seed, "Wv", (Hkv * dh, d), 0.02), act)
+    L["Wo"] = to_act(normal(seed, "Wo", (d, H * dh), 0.02), act)
+    L["g2"] = to_act(1.0 + normal(seed, "g2", (d,), 0.02), act)
+    if with_moe:
+        L["Wg"], L["Wu"], L["Wd"] = moe_weights(cfg)
+    return L
+
+
+def moe_weights(cfg: dict):
+    """SwiGLU expert weights: gate/up [E, d_ff, d], down [E, d, d_ff]."""
+    E, d, dff, seed, act = cfg["E"], cfg["d"], cfg["d_ff"], cfg["seed"], cfg["act"]
+    dt = np.float64 if act == "f64" else np.float32
+    Wg = np.empty((E, dff, d), dt)
+    Wu = np.empty((E, dff, d), dt)
+    Wd = np.empty((E, d, dff), dt)
+    for e in range(E):
+        Wg[e] = to_act(normal(seed, "Wg", (dff, d), 0.02, e), act)
+        Wu[e] = to_act(normal(seed, "Wu", (dff, d), 0.02, e), act)
+        Wd[e] = to_act(normal(seed, "Wd", (d, dff), 0.02, e), act)
+    return Wg, Wu, Wd
+
+
+def context_bits(cfg: dict, s: int) -> np.ndarray:
+    """Exact-count, randomly interleaved bit indices (0..3) of one sequence's
+    pre-existing context (decode workloads)."""
+    ctx = cfg["ctx"]
+    frac = np.asarray(cfg["ctx_bits"], np.float64)
+    counts = np.floor(frac * ctx).astype(np.int64)
+    rem = ctx - counts.sum()
+    order = np.argsort(-(frac * ctx - counts), kind="stable")
+    for i in range(rem):
+        counts[order[i % 4]] += 1
+    bits = np.repeat(np.arange(4, dtype=np.uint8), counts)
+    return stream(cfg["seed"], "ctx_bits", s).permutation(bits)
+
+
+def context_kv(cfg: dict, s: int):
+    """Keys (already rotated) and values held in the cache of sequence ``s``
+    before the decode step: [ctx, Hkv, dh], N(0, (0.02 sqrt(d))^2), the
+    statistics of N(0, 1) states projected by N(0, 0.02^2) weights."""
+    ctx, Hkv, dh, d = cfg["ctx"], cfg["Hkv"], cfg["dh"], cfg["d"]
+    std = 0.02 * np.sqrt(d)
+    k = to_act(normal(cfg["seed"], "ctx_k", (ctx, Hkv, dh), std, s), cfg["act"])
+    v = to_act(normal(cfg["seed"], "ctx_v", (ctx, Hkv, dh), std, s), cfg["act"])
+    return k, v
+
+
+def kv_block(seed: int, n: int, Hkv: int, dh: int, act: str, std: float = 1.0,
+             tag: str = "kvblock"):
+    """Stand-alone K/V tensors [n, Hkv, dh] for appending tests."""
+    k = to_act(normal(seed, tag + "_k", (n, Hkv, dh), std), act)
+    v = to_act(normal(seed, tag + "_v", (n, Hkv, dh), std), act)
+    return k, v

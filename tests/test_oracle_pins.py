@@ -1,0 +1,364 @@
+"""Pins for the CPU oracle: closed forms, library routines, brute force on
+tiny inputs and invariants the paper states.  None of these re-types the
+oracle's own formula; each is chosen so that a dropped term, a wrong sign or
+index, or a transposed operand in the oracle fails at least one of them."""
+import json
+import math
+import os
+import struct
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import gen
+import oracle
+from oracle import quant
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ------------------------------------------------------------- elementwise
+def test_rmsnorm_matches_torch_and_is_scale_invariant():
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((7, 48))
+    g = 1.0 + 0.1 * rng.standard_normal(48)
+    ref = F.rms_norm(torch.from_numpy(x), (48,), torch.from_numpy(g), eps=1e-6).numpy()
+    np.testing.assert_allclose(oracle.rmsnorm(x, g), ref, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(oracle.rmsnorm(3.7 * x, g), oracle.rmsnorm(x, g), rtol=1e-6)
+    ones = oracle.rmsnorm(x, np.ones(48), eps=0.0)
+    np.testing.assert_allclose(np.sqrt(np.mean(ones ** 2, axis=1)), 1.0, rtol=1e-12)
+
+
+def test_gelu_silu_softmax_match_torch():
+    y = np.linspace(-6, 6, 241)
+    t = torch.from_numpy(y)
+    np.testing.assert_allclose(oracle.gelu(y), F.gelu(t).numpy(), rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(oracle.silu(y), F.silu(t).numpy(), rtol=1e-12, atol=1e-14)
+    # GELU(x) - GELU(-x) = x (Phi(x) + Phi(-x) = 1)
+    np.testing.assert_allclose(oracle.gelu(y) - oracle.gelu(-y), y, atol=1e-12)
+    z = np.random.default_rng(1).standard_normal((5, 9)) * 4
+    np.testing.assert_allclose(oracle.softmax(z), torch.softmax(torch.from_numpy(z), -1).numpy(),
+                               rtol=1e-12)
+
+
+def test_rope_closed_form():
+    dh = 8
+    pos = np.array([0, 1, 5])
+    for j in range(dh):
+        e = np.zeros((3, 1, dh))
+        e[:, 0, j] = 1.0
+        r = oracle.rope(e, pos)
+        jj = j % (dh // 2)
+        ang = pos * 10000.0 ** (-2.0 * jj / dh)
+        exp = np.zeros((3, dh))
+        if j < dh // 2:      # x_j -> (x_j cos, ..., x_j sin at j + dh/2)
+            exp[:, j] = np.cos(ang)
+            exp[:, j + dh // 2] = np.sin(ang)
+        else:                # x_{j'+dh/2} -> (-sin at j', cos at j)
+            exp[:, jj] = -np.sin(ang)
+            exp[:, j] = np.cos(ang)
+        np.testing.assert_allclose(r[:, 0, :], exp, atol=1e-15)
+
+
+def test_rope_relative_position_property():
+    rng = np.random.default_rng(2)
+    q = rng.standard_normal((1, 1, 64))
+    k = rng.standard_normal((1, 1, 64))
+    dots = []
+    for shift in (0, 3, 100):
+        qr = oracle.rope(q, np.array([7 + shift]))
+        kr = oracle.rope(k, np.array([2 + shift]))
+        dots.append(float((qr * kr).sum()))
+        np.testing.assert_allclose(np.linalg.norm(qr), np.linalg.norm(q), rtol=1e-12)
+    np.testing.assert_allclose(dots, dots[0], rtol=1e-10)
+
+
+# --------------------------------------------------------------- quantizer
+def _fp16_rne(v):
+    return struct.unpack("<e", struct.pack("<e", float(v)))[0]
+
+
+def test_quantizer_golden_cases():
+    data = json.load(open(os.path.join(GOLD, "quant_cases.json")))
+    for c in data["cases"]:
+        x = np.asarray(c["x"], np.float32)[None, :]
+        codes, s, z = quant.quantize(x, c["b"], len(c["x"]))
+        assert codes[0].tolist() == c["codes"], c["name"]
+        assert float(s[0, 0]) == c["scale"], c["name"]
+        assert float(z[0, 0]) == c["zero"], c["name"]
+        xhat = quant.dequantize(codes, s, z, len(c["x"]))
+        assert xhat[0].tolist() == c["xhat"], c["name"]
+
+
+def test_quantizer_properties_random():
+    rng = np.random.default_rng(3)
+    x = (rng.standard_normal((64, 2, 64)) * 0.7).astype(np.float32)
+    G = 32
+    for b in (2, 4, 8):
+        codes, s, z = quant.quantize(x, b, G)
+        assert codes.dtype == np.uint8 and codes.max() <= 2 ** b - 1
+        xg = x.reshape(64, 2, 2, G)
+        cg = codes.reshape(64, 2, 2, G)
+        # scale/zero are fp16 RNE of the fp32 range / levels and the minimum
+        mn, mx = xg.min(-1), xg.max(-1)
+        exp_s = np.vectorize(_fp16_rne)((mx - mn) / np.float32(2 ** b - 1))
+        np.testing.assert_array_equal(s.astype(np.float64), exp_s)
+        np.testing.assert_array_equal(z.astype(np.float64), np.vectorize(_fp16_rne)(mn))
+        # the group minimum maps to code 0 and the maximum to the top code
+        am, ax = xg.argmin(-1), xg.argmax(-1)
+        assert (np.take_along_axis(cg, am[..., None], -1) == 0).all()
+        assert (np.take_along_axis(cg, ax[..., None], -1) == 2 ** b - 1).all()
+        # error bound: half a step plus the zero's fp16 rounding, fp32 slack
+        xhat = quant.dequantize(codes, s, z, G).reshape(64, 2, 2, G)
+        S = s.astype(np.float64)[..., None]
+        bound = S / 2 + np.abs(z.astype(np.float64) - mn)[..., None] + 1e-6
+        assert (np.abs(xhat - xg) <= bound + S * 1e-3).all()
+    # 16-bit keeps the native value exactly
+    np.testing.assert_array_equal(quant.roundtrip(x, 16, G), x.astype(np.float64))
+
+
+# ------------------------------------------------------------ controller
+def test_router_logits_match_torch_modules():
+    L = gen.make_layer("tiny_f32_prefill", act="f64", with_moe=False)
+    cfg = L["cfg"]
+    d, H, E = cfg["d"], cfg["H"], cfg["E"]
+    t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    trunk = torch.nn.Sequential(torch.nn.Linear(d + 8, 128), torch.nn.GELU(),
+                                torch.nn.Linear(128, 128)).double()
+    with torch.no_grad():
+        trunk[0].weight.copy_(t(L["W1"])); trunk[0].bias.copy_(t(L["b1"]))
+        trunk[2].weight.copy_(t(L["W2"])); trunk[2].bias.copy_(t(L["b2"]))
+        n1 = F.rms_norm(t(L["x"]), (d,), t(L["g1"]), eps=1e-6)
+        h = F.rms_norm(trunk(torch.cat([n1, t(L["psi"])], -1)), (128,), t(L["gr"]), eps=1e-6)
+        za = F.linear(h, t(L["Wa"]), t(L["ca"])).view(-1, H, 3)
+        ze = F.linear(h, t(L["We"]), t(L["ce"]))
+        zb = F.linear(h, t(L["Wb"]), t(L["cb"]))
+    n1o, zao, zeo, zbo = oracle.router_logits(L)
+    np.testing.assert_allclose(n1o, n1.numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(zao, za.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(zeo, ze.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(zbo, zb.numpy(), rtol=1e-10, atol=1e-12)
+    assert E + 1 == zeo.shape[1]
+
+
+def test_decisions_brute_force_and_invariants():
+    rng = np.random.default_rng(4)
+    N, H, E, k = 50, 3, 5, 2
+    za = np.round(rng.standard_normal((N, H, 3)), 1)     # rounding makes ties
+    zb = np.round(rng.standard_normal((N, 4)), 1)
+    ze = np.round(rng.standard_normal((N, E + 1)), 1)
+    mode, bit, eidx, egate = oracle.decide(za, ze, zb, k)
+    np.testing.assert_array_equal(mode, np.argmax(za, -1))        # first maximum
+    np.testing.assert_array_equal(bit, np.argmax(zb, -1))
+    p = torch.softmax(torch.from_numpy(ze), -1).numpy()
+    top = np.sort(np.argsort(-p, axis=-1, kind="stable")[:, :k], axis=-1)
+    np.testing.assert_array_equal(eidx, top)
+    sel = np.take_along_axis(p, top, -1)
+    np.testing.assert_allclose(egate, sel / sel.sum(-1, keepdims=True), rtol=1e-12)
+    np.testing.assert_allclose(egate.sum(-1), 1.0, rtol=1e-12)
+    # a positive rescale of every head leaves the hard decisions unchanged
+    m2, b2, e2, _ = oracle.decide(2.5 * za, 2.5 * ze, 2.5 * zb, k)
+    np.testing.assert_array_equal(m2, mode)
+    np.testing.assert_array_equal(b2, bit)
+    np.testing.assert_array_equal(e2, eidx)
+    # k = 1 gives a unit gate; the null's share is dropped, not moved
+    _, _, e1, g1 = oracle.decide(za, ze, zb, 1)
+    np.testing.assert_allclose(g1, 1.0)
+    zn = np.array([[3.0, 2.0, 0.0]])
+    _, _, en, gn = oracle.decide(np.zeros((1, 1, 3)), zn, np.zeros((1, 4)), 2)
+    assert en.tolist() == [[0, 1]]
+    pn = np.exp(zn[0]) / np.exp(zn[0]).sum()
+    np.testing.assert_allclose(gn[0], pn[:2] / pn[:2].sum())
+
+
+def test_compaction_matches_library_partition():
+    rng = np.random.default_rng(5)
+    B, T, H, E, k = 3, 37, 4, 6, 2
+    mode = rng.integers(0, 3, (B * T, H)).astype(np.uint8)
+    eidx = np.sort(np.stack([rng.choice(E + 1, k, replace=False) for _ in range(B * T)]), -1)
+    c = oracle.compact(mode, eidx, B, T, H, E, k)
+    for b in range(B):
+        for h in range(H):
+            for m in (1, 2):
+                s = (b * H + h) * 2 + m - 1
+                ref = np.flatnonzero(mode[b * T:(b + 1) * T, h] == m)
+                assert c["attn_cnt"][s] == len(ref)
+                np.testing.assert_array_equal(c["attn_idx"][s, :len(ref)], ref)
+    cnt = c["attn_cnt"].reshape(B, H, 2).sum(-1)
+    skips = (mode.reshape(B, T, H) == 0).sum(1)
+    np.testing.assert_array_equal(cnt + skips, T)
+    flat = eidx.reshape(-1)
+    assert c["exp_cnt"].sum() == B * T * k
+    np.testing.assert_array_equal(c["exp_cnt"], np.bincount(flat, minlength=E + 1))
+    order = np.argsort(flat, kind="stable")
+    real = order[flat[order] > 0]
+    np.testing.assert_array_equal(c["exp_rows"], real)
+    assert c["exp_off"][-1] == len(real)
+
+
+# --------------------------------------------------------------- attention
+def _brute_attention(q, khat, vhat, modes, w):
+    nq, H, dh = q.shape
+    Hkv = khat.shape[1]
+    out = np.zeros_like(q)
+    for t in range(nq):
+        for h in range(H):
+            g = h // (H // Hkv)
+            m = modes[t, h]
+            if m == 0:
+                continue
+            keys = list(range(max(0, t - w + 1), t + 1)) if m == 1 else list(range(0, t + 1))
+            sc = [sum(q[t, h, c] * khat[j, g, c] for c in range(dh)) / math.sqrt(dh) for j in keys]
+            mx = max(sc)
+            ex = [math.exp(s - mx) for s in sc]
+            tot = sum(ex)
+            for c in range(dh):
+                out[t, h, c] = sum(ex[i] * vhat[j, g, c] for i, j in enumerate(keys)) / tot
+    return out
+
+
+def test_attention_brute_force_tiny():
+    rng = np.random.default_rng(6)
+    T, H, Hkv, dh, w = 9, 4, 2, 4, 3
+    q = rng.standard_normal((T, H, dh))
+    k = rng.standard_normal((T, Hkv, dh))
+    v = rng.standard_normal((T, Hkv, dh))
+    modes = rng.integers(0, 3, (T, H))
+    o = oracle.attention_seq(q, np.arange(T), k, v, modes, w)
+    np.testing.assert_allclose(o, _brute_attention(q, k, v, modes, w), rtol=1e-12, atol=1e-14)
+
+
+def test_attention_full_matches_sdpa_and_special_windows():
+    rng = np.random.default_rng(7)
+    T, H, Hkv, dh = 33, 8, 2, 16
+    q = rng.standard_normal((T, H, dh))
+    k = rng.standard_normal((T, Hkv, dh))
+    v = rng.standard_normal((T, Hkv, dh))
+    full = np.full((T, H), 2)
+    o = oracle.attention_seq(q, np.arange(T), k, v, full, 5)
+    tq = torch.from_numpy(q).permute(1, 0, 2)[None]
+    tk = torch.from_numpy(k).permute(1, 0, 2)[None]
+    tv = torch.from_numpy(v).permute(1, 0, 2)[None]
+    ref = F.scaled_dot_product_attention(tq, tk, tv, is_causal=True, enable_gqa=True)
+    np.testing.assert_allclose(o, ref[0].permute(1, 0, 2).numpy(), rtol=1e-10, atol=1e-12)
+    # a window at least as long as the sequence is full attention
+    loc = np.full((T, H), 1)
+    np.testing.assert_allclose(oracle.attention_seq(q, np.arange(T), k, v, loc, T), o,
+                               rtol=1e-12)
+    # a window of one key returns that token's own value
+    o1 = oracle.attention_seq(q, np.arange(T), k, v, loc, 1)
+    np.testing.assert_allclose(o1, np.repeat(v, H // Hkv, axis=1), rtol=1e-12)
+    # skip returns zero
+    assert not oracle.attention_seq(q, np.arange(T), k, v, np.zeros((T, H), int), 4).any()
+
+
+def test_prefill_equals_token_by_token_decode():
+    rng = np.random.default_rng(8)
+    T, H, Hkv, dh, w = 12, 4, 1, 8, 4
+    q = rng.standard_normal((T, H, dh))
+    k = rng.standard_normal((T, Hkv, dh))
+    v = rng.standard_normal((T, Hkv, dh))
+    modes = rng.integers(0, 3, (T, H))
+    o = oracle.attention_seq(q, np.arange(T), k, v, modes, w)
+    for t in range(T):      # cache holding only positions 0..t
+        ot = oracle.attention_seq(q[t:t + 1], np.array([t]), k[:t + 1], v[:t + 1],
+                                  modes[t:t + 1], w)
+        np.testing.assert_allclose(ot[0], o[t], rtol=1e-12, atol=1e-15)
+
+
+# ------------------------------------------------------------- whole layer
+def _dense_block_torch(L):
+    """Standard pre-norm block from torch library routines (fp64)."""
+    cfg = L["cfg"]
+    d, H, Hkv, dh, T = cfg["d"], cfg["H"], cfg["Hkv"], cfg["dh"], cfg["T"]
+    t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    x = t(L["x"])
+    n1 = F.rms_norm(x, (d,), t(L["g1"]), eps=1e-6)
+    q = F.linear(n1, t(L["Wq"])).view(T, H, dh)
+    k = F.linear(n1, t(L["Wk"])).view(T, Hkv, dh)
+    v = F.linear(n1, t(L["Wv"])).view(T, Hkv, dh)
+    pos = torch.arange(T, dtype=torch.float64)
+    inv = 10000.0 ** (-torch.arange(0, dh, 2, dtype=torch.float64) / dh)
+    ang = pos[:, None] * inv[None]
+    cos = torch.cat([ang.cos(), ang.cos()], -1)[:, None]
+    sin = torch.cat([ang.sin(), ang.sin()], -1)[:, None]
+    rot = lambda u: torch.cat([-u[..., dh // 2:], u[..., :dh // 2]], -1)
+    q = q * cos + rot(q) * sin
+    k = k * cos + rot(k) * sin
+    o = F.scaled_dot_product_attention(q.permute(1, 0, 2)[None], k.permute(1, 0, 2)[None],
+                                       v.permute(1, 0, 2)[None], is_causal=True,
+                                       enable_gqa=True)[0].permute(1, 0, 2)
+    xt = x + F.linear(o.reshape(T, H * dh), t(L["Wo"]))
+    n2 = F.rms_norm(xt, (d,), t(L["g2"]), eps=1e-6)
+    f = F.linear(F.silu(F.linear(n2, t(L["Wg"][0]))) * F.linear(n2, t(L["Wu"][0])),
+                 t(L["Wd"][0]))
+    return xt.numpy(), (xt + f).numpy()
+
+
+def test_dense_special_case_is_a_standard_block():
+    """All-full attention, all 16-bit KV, one expert with k = 1 and the null
+    never chosen: the routed layer is the standard pre-norm block."""
+    L = gen.make_layer("tiny_f32_prefill", act="f64")
+    H, E = L["cfg"]["H"], L["cfg"]["E"]
+    L["ca"] = np.tile([-50.0, -50.0, 50.0], H)
+    L["cb"] = np.array([-50.0, -50.0, -50.0, 50.0])
+    L["ce"] = np.array([-1e4, 50.0] + [-1e4] * (E - 1))
+    r = oracle.layer_prefill(L)
+    assert (r["mode"] == 2).all() and (r["bit"] == 3).all() and (r["eidx"] == 1).all()
+    xt, xout = _dense_block_torch(L)
+    np.testing.assert_allclose(r["xt"], xt, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(r["xout"], xout, rtol=1e-10, atol=1e-12)
+
+
+def test_skip_and_null_tokens_pass_the_residual_unchanged():
+    L = gen.make_layer("tiny_f32_prefill")
+    H, E = L["cfg"]["H"], L["cfg"]["E"]
+    L["ca"] = np.tile([50.0, -50.0, -50.0], H)          # every head skips
+    L["ce"] = np.array([50.0] + [-50.0] * E)            # k = 1 null
+    r = oracle.layer_prefill(L)
+    assert (r["mode"] == 0).all() and (r["eidx"] == 0).all()
+    np.testing.assert_array_equal(r["xt"], L["x"].astype(np.float64))
+    np.testing.assert_array_equal(r["xout"], r["xt"])
+
+
+def test_moe_is_gate_weighted_sum_of_experts():
+    L = gen.make_layer("tiny_f32_prefill", act="f64")
+    rng = np.random.default_rng(9)
+    N, E = 6, L["cfg"]["E"]
+    xt = rng.standard_normal((N, L["cfg"]["d"]))
+    eidx = np.array([[0, 1], [2, 3], [1, 4], [0, 2], [3, 4], [1, 2]])
+    egate = rng.uniform(0.1, 0.9, (N, 2))
+    out, n2, y = oracle.moe(xt, L, eidx, egate)
+    t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    n2t = F.rms_norm(t(xt), (xt.shape[1],), t(L["g2"]), eps=1e-6)
+    ref = t(xt).clone()
+    for i in range(N):
+        for s in range(2):
+            e = int(eidx[i, s])
+            if e == 0:
+                continue
+            u = n2t[i]
+            f = F.linear(F.silu(F.linear(u, t(L["Wg"][e - 1]))) * F.linear(u, t(L["Wu"][e - 1])),
+                         t(L["Wd"][e - 1]))
+            ref[i] += egate[i, s] * f
+    np.testing.assert_allclose(out, ref.numpy(), rtol=1e-10, atol=1e-12)
+
+
+# ------------------------------------------------------------- generator
+def test_generator_bf16_rounding_matches_torch():
+    a = np.random.default_rng(10).standard_normal(10000).astype(np.float32) * 3
+    ref = torch.from_numpy(a).to(torch.bfloat16).to(torch.float32).numpy()
+    np.testing.assert_array_equal(gen.round_bf16(a), ref)
+
+
+def test_generator_is_deterministic_and_hits_mixes():
+    L1 = gen.make_layer("tiny_f32_prefill", with_moe=False)
+    L2 = gen.make_layer("tiny_f32_prefill", with_moe=False)
+    for key in ("x", "psi", "W1", "Wq"):
+        np.testing.assert_array_equal(L1[key], L2[key])
+    cfg = gen.CONFIGS["410m_bf16_decode"] | {"seed": 103}
+    bits = gen.context_bits(cfg, 3)
+    np.testing.assert_array_equal(np.bincount(bits, minlength=4),
+                                  np.round(np.array(cfg["ctx_bits"]) * cfg["ctx"]))

@@ -1,0 +1,319 @@
+/*
+ * triroute.h -- C ABI of an MI355X (gfx950) implementation of the inference
+ * forward of one TriRoute-routed transformer layer.
+ *
+ * The layer (paper Sec. 3.1 block, Sec. 3.2 axes, Sec. 3.3 controller,
+ * Sec. 3.8 inference rule):
+ *   1. a shared controller decides, per token, an attention mode per query
+ *      head (skip / local window / full), a top-k set of SwiGLU experts that
+ *      may include the null expert, and the bit width {2,4,8,16} at which the
+ *      token's own K/V are written to the cache;
+ *   2. tokens are compacted by decision (deterministic prefix sums);
+ *   3. K/V are quantized per token and per group of G channels and appended
+ *      to a bit-packed mixed-width cache; attention reads that cache and
+ *      dequantizes in registers (every read, including a token's own key,
+ *      goes through the cache: append, then attend);
+ *   4. the experts run as a grouped GEMM in which the null expert is the
+ *      identity (never computed).
+ *
+ * Conventions
+ *   - Every pointer is a device pointer unless stated; the caller owns all
+ *     memory.  The library never allocates or frees device memory and keeps
+ *     no pointer past a call.  Calls are asynchronous on the given stream and
+ *     never synchronise it, except triroute_kv_status().
+ *   - Tensors are row-major and contiguous.  A batch of B sequences of T
+ *     tokens is flattened as token i = b*T + t.
+ *   - "act" tensors have the activation dtype of cfg->act: IEEE fp32, or
+ *     bf16 (16-bit storage, round-to-nearest-even on every write).
+ *   - Enumerations: attention mode 0 skip, 1 local, 2 full; bit index 0..3
+ *     means 2, 4, 8, 16 bits; expert id 0 is the null expert, 1..E are real.
+ *   - Errors: every call validates its arguments on the host first; on error
+ *     nothing is launched, outputs are untouched, and the return value is a
+ *     negative TRIROUTE_E_* code (message via triroute_last_error(), kept
+ *     per thread).  Failures that only the device can see (cache capacity)
+ *     set bits of the cache's status word, read with triroute_kv_status().
+ *   - No C++ exception crosses this boundary.
+ */
+#ifndef TRIROUTE_H
+#define TRIROUTE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t *triroute_stream_t; /* a hipStream_t (NULL = default stream) */
+
+enum triroute_status {
+  TRIROUTE_OK = 0,
+  TRIROUTE_E_INVALID = -1,     /* null pointer, bad enum, inconsistent sizes */
+  TRIROUTE_E_UNSUPPORTED = -2, /* a shape or dtype this build does not run */
+  TRIROUTE_E_WORKSPACE = -3,   /* workspace smaller than triroute_workspace_bytes() */
+  TRIROUTE_E_CAPACITY = -4,    /* cache too small for the request (host-visible) */
+  TRIROUTE_E_HIP = -5          /* a HIP runtime call or kernel launch failed */
+};
+
+/* Device-side status bits of a cache (triroute_kv_status). */
+enum triroute_cache_flags {
+  TRIROUTE_CACHE_OVERFLOW = 1, /* an append would have passed the capacity; that row was dropped */
+  TRIROUTE_CACHE_BAD_SEQ = 2   /* a sequence id outside [0, n_seq); that row was dropped */
+};
+
+enum triroute_dtype { TRIROUTE_F32 = 0, TRIROUTE_BF16 = 1 };
+enum triroute_mode { TRIROUTE_SKIP = 0, TRIROUTE_LOCAL = 1, TRIROUTE_FULL = 2 };
+
+/* Layer shape.  Paper notation: d, H, H_kv, d_h, window w, E experts plus
+ * the null, top-k, expert width d_f, quantizer group G, side-feature width
+ * d_psi, router width d_r (Sec. 3.1-3.3, Table 2, Table 6).
+ * Supported: head_dim in {64, 128}; n_heads a multiple of n_kv_heads with
+ * at most 16 query heads per kv head; kv_group in {32, 64} dividing
+ * head_dim; d_router == 128; d_psi <= 32; 1 <= top_k <= n_experts + 1 <= 64;
+ * d_model and d_ff multiples of 64; 3 * n_heads + n_experts + 5 <= 112;
+ * rms_eps > 0. */
+typedef struct triroute_cfg {
+  int32_t d_model;
+  int32_t n_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t window;    /* local mode reads keys [t - window + 1, t] */
+  int32_t n_experts; /* E real experts; the expert head has E + 1 logits */
+  int32_t top_k;
+  int32_t d_ff;
+  int32_t kv_group;  /* G */
+  int32_t d_psi;
+  int32_t d_router;
+  int32_t act;       /* enum triroute_dtype */
+  float rms_eps;     /* all three RMSNorms */
+  float rope_theta;  /* rotate-half RoPE base */
+} triroute_cfg;
+
+/* Controller weights, fp32 (Sec. 3.3 controller equation; trunk = two-layer
+ * GELU MLP, Table 6).  The frozen per-axis whitening and gradient-balance
+ * scales are folded into (W, c) by the caller.
+ *   g1 [d]            first RMSNorm gain, shared with the attention sublayer
+ *   W1 [d_r, d+d_psi] b1 [d_r]      trunk layer 1 (input [n1 ; psi])
+ *   W2 [d_r, d_r]     b2 [d_r]      trunk layer 2
+ *   gr [d_r]          RMSNorm gain of h
+ *   Wa [3H, d_r]      ca [3H]       attention head, logits [H, 3]
+ *   We [E+1, d_r]     ce [E+1]      expert head (index 0 = null)
+ *   Wb [4, d_r]       cb [4]        bit head */
+typedef struct triroute_router_w {
+  const float *g1, *W1, *b1, *W2, *b2, *gr;
+  const float *Wa, *ca, *We, *ce, *Wb, *cb;
+} triroute_router_w;
+
+/* Attention projections and the second norm gain, act dtype.
+ *   Wq [H*dh, d]  Wk [Hkv*dh, d]  Wv [Hkv*dh, d]  Wo [d, H*dh]  g2 [d] */
+typedef struct triroute_dense_w {
+  const void *Wq, *Wk, *Wv, *Wo, *g2;
+} triroute_dense_w;
+
+/* SwiGLU experts, act dtype: f_e(u) = Wdown_e (silu(Wgate_e u) * Wup_e u).
+ *   Wgate [E, d_ff, d]  Wup [E, d_ff, d]  Wdown [E, d, d_ff]
+ * (expert id e >= 1 uses slice e - 1). */
+typedef struct triroute_moe_w {
+  const void *Wgate, *Wup, *Wdown;
+} triroute_moe_w;
+
+/* Compaction produced by triroute_router (all device int32 arrays).
+ *   attn_cnt [B*H*2]      queries per segment s = (b*H + h)*2 + (m - 1),
+ *                         m in {local, full}
+ *   attn_idx [B*H*2, T]   segment s lists its token positions t ascending
+ *                         in attn_idx[s*T .. s*T + attn_cnt[s])
+ *   exp_cnt  [E+1]        assignments per expert id (exp_cnt[0] = nulls)
+ *   exp_off  [E+1]        exp_off[0] = 0, exp_off[e] = exp_off[e-1] + exp_cnt[e]
+ *   exp_rows [B*T*k]      assignment ids a = i*k + slot of real experts,
+ *                         grouped by expert (expert e in
+ *                         [exp_off[e-1], exp_off[e])), ascending within */
+typedef struct triroute_compaction {
+  int32_t *attn_cnt, *attn_idx, *exp_cnt, *exp_off, *exp_rows;
+} triroute_compaction;
+
+/* Mixed-width KV cache (paper Sec. 3.2 (C); per-width grouping of tokens).
+ * One device allocation of triroute_kv_cache_bytes() holds, for each of
+ * n_seq sequences: a length, per width b a pool of `capacity` slots filled
+ * in position order, the position of every slot, and the packed codes.
+ * Fields are filled by triroute_kv_cache_init; treat them as read-only.
+ *
+ * Physical layout of one pool (sequence s, width index bi, kv head g): a run
+ * of tiles of TS = 4096 / head_dim slots.  A tile holds [K codes | V codes |
+ * K scale/zero | V scale/zero] (no scale/zero for 16-bit).  The code block
+ * of a tile is 64 lane records of 8*bp bytes (bp = bits, or 16 / 32 for the
+ * native bf16 / fp32 store); record l holds 64 elements q = f*8 + j, eight
+ * "fields" f of eight elements j:
+ *   K: slot 16*(f / (dh/32)) + (l % 16), channel 32*(f % (dh/32)) + 8*(l / 16) + j
+ *   V: slot 32*(f / (dh/16)) + 8*(l / 16) + j, channel 16*(f % (dh/16)) + (l % 16)
+ * Element q sits in 32-bit word (q/2) / (16/bp) at bit ((q/2) % (16/bp))*bp
+ * + (q % 2)*16 for bp < 32 (one element per word for fp32).  Scale/zero
+ * blocks are [TS slots][dh/G groups][2] fp16 (scale, zero). */
+typedef struct triroute_kv_cache {
+  void *base;
+  int32_t n_seq;
+  int32_t capacity;
+  int32_t tile_slots;
+  int32_t n_tiles;        /* tiles per pool */
+  int64_t off_status;     /* int32 status word */
+  int64_t off_seq_len;    /* int32 [n_seq] */
+  int64_t off_pool_len;   /* int32 [n_seq][4] */
+  int64_t off_pos;        /* int32 [n_seq][4][capacity] */
+  int64_t off_pool[4];    /* first tile of width bi */
+  int64_t tile_bytes[4];  /* bytes per tile of width bi */
+  int64_t total_bytes;
+} triroute_kv_cache;
+
+/* Optional taps of the composite calls: where to also leave intermediates
+ * (any field may be NULL).  Shapes as in the per-stage calls. */
+typedef struct triroute_layer_taps {
+  void *n1;          /* act [N, d] */
+  uint8_t *mode;     /* [N, H] */
+  uint8_t *bit;      /* [N] */
+  int32_t *eidx;     /* [N, k] */
+  float *egate;      /* [N, k] */
+  void *q, *k, *v;   /* act [N, H*dh], [N, Hkv*dh], [N, Hkv*dh] */
+  void *o;           /* act [N, H*dh] */
+  void *xt;          /* act [N, d] */
+} triroute_layer_taps;
+
+enum triroute_op {
+  TRIROUTE_OP_ROUTER = 0,
+  TRIROUTE_OP_QKV = 1,
+  TRIROUTE_OP_KV_APPEND = 2,
+  TRIROUTE_OP_ATTN_PREFILL = 3,
+  TRIROUTE_OP_ATTN_DECODE = 4,
+  TRIROUTE_OP_MOE = 5,
+  TRIROUTE_OP_LAYER_PREFILL = 6,
+  TRIROUTE_OP_LAYER_DECODE = 7
+};
+
+/* ---- configuration, errors, sizes ---------------------------------------- */
+
+/* Checks cfg against the supported set; TRIROUTE_OK or E_INVALID/E_UNSUPPORTED. */
+int triroute_validate(const triroute_cfg *cfg);
+/* Static name of a status code. */
+const char *triroute_status_string(int status);
+/* Message of the calling thread's last failing call ("" if none). */
+const char *triroute_last_error(void);
+/* Workspace bytes op needs for B sequences of T tokens (T = 1 for decode). */
+int triroute_workspace_bytes(const triroute_cfg *cfg, int op, int B, int T, size_t *bytes);
+
+/* ---- KV cache ------------------------------------------------------------- */
+
+/* Bytes of a cache for n_seq sequences of at most `capacity` tokens. */
+int triroute_kv_cache_bytes(const triroute_cfg *cfg, int n_seq, int capacity, size_t *bytes);
+/* Lays out `cache` in the caller's allocation `base` (>= cache_bytes, 256-byte
+ * aligned) and clears it on `stream` (all sequences empty). */
+int triroute_kv_cache_init(const triroute_cfg *cfg, triroute_kv_cache *cache, void *base,
+                           size_t bytes, int n_seq, int capacity, triroute_stream_t stream);
+/* Empties sequence `seq` (clears its pools) on `stream`. */
+int triroute_kv_reset_seq(const triroute_cfg *cfg, const triroute_kv_cache *cache, int seq,
+                          triroute_stream_t stream);
+/* Synchronises `stream` and copies the cache status word to *status (host). */
+int triroute_kv_status(const triroute_kv_cache *cache, int32_t *status, triroute_stream_t stream);
+
+/* Row a4 (Sec. 3.2 (C)): quantize and append T new tokens to each of B cache
+ * sequences.  Row b goes to sequence seq_ids[b] (seq_ids NULL: b); its tokens
+ * take positions seq_len, seq_len + 1, ... in order, and token (b, t) lands in
+ * the pool of width bit[b*T + t] at the next free slot.
+ *   k, v  act [B*T, Hkv*dh] (already rotated keys)   bit uint8 [B*T]
+ * A row that would pass `capacity` is dropped and sets TRIROUTE_CACHE_OVERFLOW.
+ * Quantizer (bit exact): per group of G channels, fp32 mn/mx, s32 = (mx-mn)/(2^b-1),
+ * stored s = fp16(s32), z = fp16(mn) (RNE), code = 0 if s == 0 else
+ * clamp(rint_even((x - z) / s), 0, 2^b - 1) in fp32; 16-bit keeps x verbatim.
+ * Rows must name distinct sequences. */
+int triroute_kv_append(const triroute_cfg *cfg, const triroute_kv_cache *cache, int B, int T,
+                       const int32_t *seq_ids, const void *k, const void *v, const uint8_t *bit,
+                       void *ws, size_t ws_bytes, triroute_stream_t stream);
+
+/* Reads back slots [slot0, slot0 + count) of pool (seq, bi) in logical form:
+ *   k_out, v_out  [count, Hkv, dh]: uint8 codes (bi < 3) or act values (bi == 3)
+ *   k_sz, v_sz    [count, Hkv, dh/G, 2] fp16 bit patterns (scale, zero); unused for bi == 3
+ *   pos_out       int32 [count] token positions
+ * Slots beyond the pool's length read as zero.  (Inspection / tests.) */
+int triroute_kv_export(const triroute_cfg *cfg, const triroute_kv_cache *cache, int seq, int bi,
+                       int slot0, int count, void *k_out, void *v_out, uint16_t *k_sz,
+                       uint16_t *v_sz, int32_t *pos_out, triroute_stream_t stream);
+
+/* ---- per-stage calls ------------------------------------------------------ */
+
+/* Rows a1 + a2 (Sec. 3.3 controller equation, Sec. 3.8 hard decisions):
+ *   n1 = RMSNorm(x; g1) (fp32 inside, act out), u = GELU(W1 [n1; psi] + b1),
+ *   h = W2 u + b2, h^ = RMSNorm(h; gr), z^a = Wa h^ + ca, z^e = We h^ + ce,
+ *   z^b = Wb h^ + cb;  mode[i,h] = argmax_m z^a[h,m] (first maximum),
+ *   bit[i] = argmax z^b, S_i = k largest softmax(z^e) (lower id on ties)
+ *   stored in ascending id, egate = p_j / sum_{S_i} p (the null's share is
+ *   dropped).  Then the compaction `cmp` (see triroute_compaction).
+ *   x act [B*T, d], psi f32 [B*T, d_psi]; outputs n1 act [B*T, d],
+ *   mode u8 [B*T, H], bit u8 [B*T], eidx i32 [B*T, k], egate f32 [B*T, k]. */
+int triroute_router(const triroute_cfg *cfg, int B, int T, const void *x, const float *psi,
+                    const triroute_router_w *w, void *n1, uint8_t *mode, uint8_t *bit,
+                    int32_t *eidx, float *egate, const triroute_compaction *cmp, void *ws,
+                    size_t ws_bytes, triroute_stream_t stream);
+
+/* Row a3: q = Wq n1, k = Wk n1, v = Wv n1 with rotate-half RoPE on q and k
+ * at position pos0[b] + t (pos0 NULL: t); pos0 may point into a cache's
+ * sequence lengths (see triroute_kv_seq_len_ptr).
+ *   n1 act [B*T, d]; q act [B*T, H*dh]; k, v act [B*T, Hkv*dh]. */
+int triroute_qkv(const triroute_cfg *cfg, int B, int T, const void *n1,
+                 const triroute_dense_w *w, const int32_t *pos0, void *q, void *k, void *v,
+                 triroute_stream_t stream);
+
+/* Device pointer to the int32 [n_seq] sequence lengths of a cache. */
+const int32_t *triroute_kv_seq_len_ptr(const triroute_kv_cache *cache);
+
+/* Row a6 (Sec. 3.2 (A)): attention of B*T new queries whose K/V were just
+ * appended (the T tokens of row b occupy the last T positions of sequence
+ * seq_ids[b]).  Query head h of token (b, t) at position P reads kv head
+ * h / (H / Hkv): skip -> zeros, local -> keys [P - w + 1, P], full -> [0, P],
+ * softmax(q k^T / sqrt(dh)) v over the dequantized cache.
+ *   q act [B*T, H*dh]; mode u8 [B*T, H]; cmp from triroute_router; o act [B*T, H*dh]. */
+int triroute_attn_prefill(const triroute_cfg *cfg, int B, int T, const int32_t *seq_ids,
+                          const void *q, const triroute_kv_cache *cache, const uint8_t *mode,
+                          const triroute_compaction *cmp, void *o, void *ws, size_t ws_bytes,
+                          triroute_stream_t stream);
+
+/* Row a7: as triroute_attn_prefill for one new query per sequence (T = 1),
+ * split over KV chunks with a log-sum-exp combine.
+ *   q act [B, H*dh]; mode u8 [B, H]; o act [B, H*dh]. */
+int triroute_attn_decode(const triroute_cfg *cfg, int B, const int32_t *seq_ids, const void *q,
+                         const triroute_kv_cache *cache, const uint8_t *mode, void *o, void *ws,
+                         size_t ws_bytes, triroute_stream_t stream);
+
+/* Row a8 (first residual): xt = x + Wo concat_h(o).  x, xt act [N, d]. */
+int triroute_oproj(const triroute_cfg *cfg, int n_tok, const void *x, const void *o,
+                   const triroute_dense_w *w, void *xt, triroute_stream_t stream);
+
+/* Rows a8 (second norm) + a9 (Sec. 3.2 (B)): n2 = RMSNorm(xt; g2),
+ * x_out = xt + sum over slots with eidx != 0 of egate * f_eidx(n2).
+ * Null slots are never computed.  eidx/egate/cmp as produced by
+ * triroute_router for the same n_tok = B*T tokens. */
+int triroute_moe(const triroute_cfg *cfg, int n_tok, const void *xt, const triroute_dense_w *dw,
+                 const triroute_moe_w *w, const int32_t *eidx, const float *egate,
+                 const triroute_compaction *cmp, void *x_out, void *ws, size_t ws_bytes,
+                 triroute_stream_t stream);
+
+/* ---- composites (no host synchronisation inside) ------------------------- */
+
+/* Whole layer for B sequences of T new tokens: router, compaction, QKV at
+ * positions continuing each sequence, append, attention, O-proj, experts. */
+int triroute_layer_prefill(const triroute_cfg *cfg, int B, int T, const int32_t *seq_ids,
+                           const void *x, const float *psi, const triroute_router_w *rw,
+                           const triroute_dense_w *dw, const triroute_moe_w *mw,
+                           const triroute_kv_cache *cache, void *x_out,
+                           const triroute_layer_taps *taps, void *ws, size_t ws_bytes,
+                           triroute_stream_t stream);
+
+/* One decode step: one new token per sequence (x [B, d], psi [B, d_psi]). */
+int triroute_layer_decode(const triroute_cfg *cfg, int B, const int32_t *seq_ids,
+                          const void *x, const float *psi, const triroute_router_w *rw,
+                          const triroute_dense_w *dw, const triroute_moe_w *mw,
+                          const triroute_kv_cache *cache, void *x_out,
+                          const triroute_layer_taps *taps, void *ws, size_t ws_bytes,
+                          triroute_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TRIROUTE_H */

@@ -1,0 +1,585 @@
+// Host side of libtriroute: argument validation, cache layout, workspace
+// carving and kernel launches on the caller's stream.  No call allocates or
+// frees device memory, and only triroute_kv_status synchronises.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <algorithm>
+#include <string.h>
+
+#include <mutex>
+
+#include "kernels.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+  return fail(TRIROUTE_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define CHECK_HIP(expr, what)                        \
+  do {                                               \
+    hipError_t e_ = (expr);                          \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+#define REQUIRE(cond, code, ...)                 \
+  do {                                           \
+    if (!(cond)) return fail(code, __VA_ARGS__); \
+  } while (0)
+
+int prepare_once() {
+  static std::once_flag once;
+  static hipError_t err = hipSuccess;
+  std::call_once(once, [] { err = tr::router_prepare(); });
+  if (err != hipSuccess) return hip_fail(err, "kernel attribute setup");
+  return TRIROUTE_OK;
+}
+
+int act_bytes(const triroute_cfg &c) { return c.act == TRIROUTE_BF16 ? 2 : 4; }
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Bump allocator over a workspace (or a dry run that only counts bytes).
+struct Carve {
+  uint8_t *base;
+  size_t used = 0;
+  explicit Carve(void *b) : base((uint8_t *)b) {}
+  template <typename T>
+  T *take(size_t count) {
+    T *p = base ? (T *)(base + used) : nullptr;
+    used += align256(count * sizeof(T));
+    return p;
+  }
+};
+
+constexpr int DECODE_MAX_SPLITS = 64;
+
+struct LayerBufs {
+  void *n1, *q, *k, *v, *o, *xt;
+  uint8_t *mode, *bit;
+  int32_t *eidx;
+  float *egate;
+  triroute_compaction cmp;
+};
+
+// --- per-op scratch (the parts a stage needs beyond its outputs)
+struct RouterWs {
+  float *rinv, *u;
+  int32_t *hist;
+};
+RouterWs carve_router(Carve &cv, const triroute_cfg &c, int N) {
+  RouterWs w;
+  w.rinv = cv.take<float>(N);
+  w.u = cv.take<float>(size_t(N) * 128);
+  w.hist = cv.take<int32_t>(tr::compact_hist_ints(N, c.top_k, c.n_experts + 1));
+  return w;
+}
+struct MoeWs {
+  void *n2, *Hm;
+  float *Y;
+};
+MoeWs carve_moe(Carve &cv, const triroute_cfg &c, int N) {
+  MoeWs w;
+  const size_t ab = act_bytes(c);
+  w.n2 = cv.take<uint8_t>(size_t(N) * c.d_model * ab);
+  w.Hm = cv.take<uint8_t>(size_t(N) * c.top_k * c.d_ff * ab);
+  w.Y = cv.take<float>(size_t(N) * c.top_k * c.d_model);
+  return w;
+}
+int32_t *carve_kv(Carve &cv, int N) { return cv.take<int32_t>(N); }
+float *carve_attn_decode(Carve &cv, const triroute_cfg &c, int B) {
+  return cv.take<float>(size_t(B) * c.n_heads * DECODE_MAX_SPLITS * (c.head_dim + 2));
+}
+
+LayerBufs carve_layer(Carve &cv, const triroute_cfg &c, int B, int T) {
+  const int N = B * T, H = c.n_heads;
+  const size_t ab = act_bytes(c);
+  LayerBufs L;
+  L.n1 = cv.take<uint8_t>(size_t(N) * c.d_model * ab);
+  L.mode = cv.take<uint8_t>(size_t(N) * H);
+  L.bit = cv.take<uint8_t>(N);
+  L.eidx = cv.take<int32_t>(size_t(N) * c.top_k);
+  L.egate = cv.take<float>(size_t(N) * c.top_k);
+  L.cmp.attn_cnt = cv.take<int32_t>(size_t(B) * H * 2);
+  L.cmp.attn_idx = cv.take<int32_t>(size_t(B) * H * 2 * T);
+  L.cmp.exp_cnt = cv.take<int32_t>(c.n_experts + 1);
+  L.cmp.exp_off = cv.take<int32_t>(c.n_experts + 1);
+  L.cmp.exp_rows = cv.take<int32_t>(size_t(N) * c.top_k);
+  L.q = cv.take<uint8_t>(size_t(N) * H * c.head_dim * ab);
+  L.k = cv.take<uint8_t>(size_t(N) * c.n_kv_heads * c.head_dim * ab);
+  L.v = cv.take<uint8_t>(size_t(N) * c.n_kv_heads * c.head_dim * ab);
+  L.o = cv.take<uint8_t>(size_t(N) * H * c.head_dim * ab);
+  L.xt = cv.take<uint8_t>(size_t(N) * c.d_model * ab);
+  return L;
+}
+
+size_t op_bytes(const triroute_cfg &c, int op, int B, int T) {
+  Carve cv(nullptr);
+  const int N = B * T;
+  switch (op) {
+    case TRIROUTE_OP_ROUTER: carve_router(cv, c, N); break;
+    case TRIROUTE_OP_QKV: break;
+    case TRIROUTE_OP_KV_APPEND: carve_kv(cv, N); break;
+    case TRIROUTE_OP_ATTN_PREFILL: break;
+    case TRIROUTE_OP_ATTN_DECODE: carve_attn_decode(cv, c, B); break;
+    case TRIROUTE_OP_MOE: carve_moe(cv, c, N); break;
+    case TRIROUTE_OP_LAYER_PREFILL:
+    case TRIROUTE_OP_LAYER_DECODE: {
+      carve_layer(cv, c, B, T);
+      size_t s = 0;
+      s = std::max(s, op_bytes(c, TRIROUTE_OP_ROUTER, B, T));
+      s = std::max(s, op_bytes(c, TRIROUTE_OP_KV_APPEND, B, T));
+      s = std::max(s, op_bytes(c, op == TRIROUTE_OP_LAYER_DECODE ? TRIROUTE_OP_ATTN_DECODE
+                                                                 : TRIROUTE_OP_ATTN_PREFILL,
+                               B, T));
+      s = std::max(s, op_bytes(c, TRIROUTE_OP_MOE, B, T));
+      return cv.used + s;
+    }
+    default: return 0;
+  }
+  return cv.used;
+}
+
+int check_cfg(const triroute_cfg *c) {
+  REQUIRE(c, TRIROUTE_E_INVALID, "cfg is NULL");
+  REQUIRE(c->act == TRIROUTE_F32 || c->act == TRIROUTE_BF16, TRIROUTE_E_INVALID,
+          "act must be TRIROUTE_F32 or TRIROUTE_BF16 (got %d)", c->act);
+  REQUIRE(c->d_model > 0 && c->n_heads > 0 && c->n_kv_heads > 0 && c->head_dim > 0 &&
+              c->window > 0 && c->n_experts > 0 && c->top_k > 0 && c->d_ff > 0 &&
+              c->kv_group > 0 && c->d_psi >= 0 && c->d_router > 0,
+          TRIROUTE_E_INVALID, "cfg has a non-positive size");
+  REQUIRE(c->rms_eps > 0.f && c->rope_theta > 0.f, TRIROUTE_E_INVALID,
+          "rms_eps and rope_theta must be positive");
+  REQUIRE(c->n_heads % c->n_kv_heads == 0, TRIROUTE_E_INVALID,
+          "n_heads (%d) must be a multiple of n_kv_heads (%d)", c->n_heads, c->n_kv_heads);
+  REQUIRE(c->top_k <= c->n_experts + 1, TRIROUTE_E_INVALID, "top_k (%d) > n_experts + 1 (%d)",
+          c->top_k, c->n_experts + 1);
+  REQUIRE(c->head_dim == 64 || c->head_dim == 128, TRIROUTE_E_UNSUPPORTED,
+          "head_dim %d not in {64, 128}", c->head_dim);
+  REQUIRE(c->kv_group == 32 || c->kv_group == 64, TRIROUTE_E_UNSUPPORTED,
+          "kv_group %d not in {32, 64}", c->kv_group);
+  REQUIRE(c->head_dim % c->kv_group == 0, TRIROUTE_E_UNSUPPORTED,
+          "kv_group %d does not divide head_dim %d", c->kv_group, c->head_dim);
+  REQUIRE(c->n_heads / c->n_kv_heads <= 16, TRIROUTE_E_UNSUPPORTED,
+          "more than 16 query heads per kv head");
+  REQUIRE(c->d_router == 128, TRIROUTE_E_UNSUPPORTED, "d_router %d != 128", c->d_router);
+  REQUIRE(c->d_psi <= 32, TRIROUTE_E_UNSUPPORTED, "d_psi %d > 32", c->d_psi);
+  REQUIRE(c->n_experts + 1 <= 64, TRIROUTE_E_UNSUPPORTED, "n_experts + 1 > 64");
+  REQUIRE(3 * c->n_heads + c->n_experts + 5 <= 112, TRIROUTE_E_UNSUPPORTED,
+          "router head count 3H + E + 5 > 112");
+  REQUIRE(c->d_model % 64 == 0 && c->d_ff % 64 == 0, TRIROUTE_E_UNSUPPORTED,
+          "d_model and d_ff must be multiples of 64");
+  return TRIROUTE_OK;
+}
+
+int check_bt(int B, int T) {
+  REQUIRE(B >= 1 && T >= 1, TRIROUTE_E_INVALID, "B (%d) and T (%d) must be >= 1", B, T);
+  REQUIRE(int64_t(B) * T <= (int64_t(1) << 24), TRIROUTE_E_UNSUPPORTED,
+          "B*T = %lld tokens exceeds 2^24", (long long)B * T);
+  return TRIROUTE_OK;
+}
+
+int check_ws(const triroute_cfg &c, int op, int B, int T, const void *ws, size_t ws_bytes) {
+  const size_t need = op_bytes(c, op, B, T);
+  REQUIRE(need == 0 || ws, TRIROUTE_E_INVALID, "workspace is NULL (%zu bytes needed)", need);
+  REQUIRE(ws_bytes >= need, TRIROUTE_E_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes,
+          need);
+  REQUIRE((uintptr_t(ws) & 255) == 0, TRIROUTE_E_INVALID, "workspace must be 256-byte aligned");
+  return TRIROUTE_OK;
+}
+
+int check_cache(const triroute_cfg &c, const triroute_kv_cache *kc, int B, int T) {
+  REQUIRE(kc && kc->base, TRIROUTE_E_INVALID, "cache is NULL or not initialised");
+  REQUIRE(kc->tile_slots == 4096 / c.head_dim, TRIROUTE_E_INVALID,
+          "cache was laid out for another head_dim");
+  REQUIRE(B <= kc->n_seq, TRIROUTE_E_INVALID, "B (%d) > cache sequences (%d)", B, kc->n_seq);
+  REQUIRE(T <= kc->capacity, TRIROUTE_E_CAPACITY, "T (%d) > cache capacity (%d)", T,
+          kc->capacity);
+  return TRIROUTE_OK;
+}
+
+#define TRY(expr)                 \
+  do {                            \
+    int r_ = (expr);              \
+    if (r_ != TRIROUTE_OK) return r_; \
+  } while (0)
+
+void layout_cache(const triroute_cfg &c, int n_seq, int capacity, triroute_kv_cache *kc) {
+  memset(kc, 0, sizeof *kc);
+  const int dh = c.head_dim, G = c.kv_group, ab = act_bytes(c);
+  const int TS = 4096 / dh;
+  kc->n_seq = n_seq;
+  kc->capacity = capacity;
+  kc->tile_slots = TS;
+  kc->n_tiles = (capacity + TS - 1) / TS;
+  size_t off = 0;
+  kc->off_status = off;
+  off += 256;
+  kc->off_seq_len = off;
+  off += align256(size_t(n_seq) * 4);
+  kc->off_pool_len = off;
+  off += align256(size_t(n_seq) * 16);
+  kc->off_pos = off;
+  off += align256(size_t(n_seq) * 4 * capacity * 4);
+  for (int bi = 0; bi < 4; ++bi) {
+    const int bp = tr::pool_bits(bi, ab);
+    kc->tile_bytes[bi] = align256(size_t(1024) * bp + (bi < 3 ? size_t(2) * TS * (dh / G) * 4 : 0));
+    kc->off_pool[bi] = off;
+    off += size_t(n_seq) * c.n_kv_heads * kc->n_tiles * kc->tile_bytes[bi];
+  }
+  kc->total_bytes = off;
+}
+
+}  // namespace
+
+namespace tr {
+CacheView make_view(const triroute_cfg &c, const triroute_kv_cache &k) {
+  CacheView v;
+  v.base = (uint8_t *)k.base;
+  v.status = (int32_t *)(v.base + k.off_status);
+  v.seq_len = (int32_t *)(v.base + k.off_seq_len);
+  v.pool_len = (int32_t *)(v.base + k.off_pool_len);
+  v.pos = (int32_t *)(v.base + k.off_pos);
+  v.n_seq = k.n_seq;
+  v.capacity = k.capacity;
+  v.TS = k.tile_slots;
+  v.n_tiles = k.n_tiles;
+  v.Hkv = c.n_kv_heads;
+  v.dh = c.head_dim;
+  v.G = c.kv_group;
+  v.act_bytes = act_bytes(c);
+  for (int i = 0; i < 4; ++i) {
+    v.off_pool[i] = k.off_pool[i];
+    v.tile_bytes[i] = k.tile_bytes[i];
+  }
+  return v;
+}
+}  // namespace tr
+
+// ======================================================================= ABI
+extern "C" {
+
+const char *triroute_status_string(int s) {
+  switch (s) {
+    case TRIROUTE_OK: return "ok";
+    case TRIROUTE_E_INVALID: return "invalid argument";
+    case TRIROUTE_E_UNSUPPORTED: return "unsupported shape or dtype";
+    case TRIROUTE_E_WORKSPACE: return "workspace too small";
+    case TRIROUTE_E_CAPACITY: return "cache capacity exceeded";
+    case TRIROUTE_E_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char *triroute_last_error(void) { return g_err; }
+
+int triroute_validate(const triroute_cfg *cfg) {
+  g_err[0] = 0;
+  return check_cfg(cfg);
+}
+
+int triroute_workspace_bytes(const triroute_cfg *cfg, int op, int B, int T, size_t *bytes) {
+  TRY(check_cfg(cfg));
+  TRY(check_bt(B, T));
+  REQUIRE(bytes, TRIROUTE_E_INVALID, "bytes is NULL");
+  REQUIRE(op >= TRIROUTE_OP_ROUTER && op <= TRIROUTE_OP_LAYER_DECODE, TRIROUTE_E_INVALID,
+          "unknown op %d", op);
+  *bytes = op_bytes(*cfg, op, B, T);
+  return TRIROUTE_OK;
+}
+
+int triroute_kv_cache_bytes(const triroute_cfg *cfg, int n_seq, int capacity, size_t *bytes) {
+  TRY(check_cfg(cfg));
+  REQUIRE(bytes, TRIROUTE_E_INVALID, "bytes is NULL");
+  REQUIRE(n_seq >= 1 && capacity >= 1, TRIROUTE_E_INVALID, "n_seq and capacity must be >= 1");
+  REQUIRE(int64_t(capacity) <= (int64_t(1) << 28), TRIROUTE_E_UNSUPPORTED, "capacity too large");
+  triroute_kv_cache kc;
+  layout_cache(*cfg, n_seq, capacity, &kc);
+  *bytes = kc.total_bytes;
+  return TRIROUTE_OK;
+}
+
+int triroute_kv_cache_init(const triroute_cfg *cfg, triroute_kv_cache *cache, void *base,
+                           size_t bytes, int n_seq, int capacity, triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  REQUIRE(cache && base, TRIROUTE_E_INVALID, "cache or base is NULL");
+  REQUIRE((uintptr_t(base) & 255) == 0, TRIROUTE_E_INVALID, "cache base must be 256-byte aligned");
+  REQUIRE(n_seq >= 1 && capacity >= 1, TRIROUTE_E_INVALID, "n_seq and capacity must be >= 1");
+  triroute_kv_cache kc;
+  layout_cache(*cfg, n_seq, capacity, &kc);
+  REQUIRE(bytes >= size_t(kc.total_bytes), TRIROUTE_E_CAPACITY,
+          "cache allocation %zu bytes < %lld needed", bytes, (long long)kc.total_bytes);
+  kc.base = base;
+  CHECK_HIP(tr::launch_fill_u32(base, kc.total_bytes / 4, 0u, (hipStream_t)stream), "cache clear");
+  *cache = kc;
+  return TRIROUTE_OK;
+}
+
+int triroute_kv_reset_seq(const triroute_cfg *cfg, const triroute_kv_cache *cache, int seq,
+                          triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  REQUIRE(cache && cache->base, TRIROUTE_E_INVALID, "cache is NULL");
+  REQUIRE(seq >= 0 && seq < cache->n_seq, TRIROUTE_E_INVALID, "seq %d out of range", seq);
+  hipStream_t st = (hipStream_t)stream;
+  uint8_t *b = (uint8_t *)cache->base;
+  CHECK_HIP(tr::launch_fill_u32(b + cache->off_seq_len + 4 * size_t(seq), 1, 0u, st), "reset");
+  CHECK_HIP(tr::launch_fill_u32(b + cache->off_pool_len + 16 * size_t(seq), 4, 0u, st), "reset");
+  CHECK_HIP(tr::launch_fill_u32(b + cache->off_pos + size_t(seq) * 16 * cache->capacity,
+                                int64_t(4) * cache->capacity, 0u, st),
+            "reset");
+  for (int bi = 0; bi < 4; ++bi) {
+    const size_t per_seq = size_t(cfg->n_kv_heads) * cache->n_tiles * cache->tile_bytes[bi];
+    CHECK_HIP(tr::launch_fill_u32(b + cache->off_pool[bi] + per_seq * seq, per_seq / 4, 0u, st),
+              "reset");
+  }
+  return TRIROUTE_OK;
+}
+
+int triroute_kv_status(const triroute_kv_cache *cache, int32_t *status, triroute_stream_t stream) {
+  REQUIRE(cache && cache->base && status, TRIROUTE_E_INVALID, "NULL argument");
+  CHECK_HIP(hipStreamSynchronize((hipStream_t)stream), "stream sync");
+  CHECK_HIP(hipMemcpy(status, (uint8_t *)cache->base + cache->off_status, 4, hipMemcpyDeviceToHost),
+            "status read");
+  return TRIROUTE_OK;
+}
+
+const int32_t *triroute_kv_seq_len_ptr(const triroute_kv_cache *cache) {
+  if (!cache || !cache->base) return nullptr;
+  return (const int32_t *)((uint8_t *)cache->base + cache->off_seq_len);
+}
+
+int triroute_kv_append(const triroute_cfg *cfg, const triroute_kv_cache *cache, int B, int T,
+                       const int32_t *seq_ids, const void *k, const void *v, const uint8_t *bit,
+                       void *ws, size_t ws_bytes, triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  TRY(check_bt(B, T));
+  TRY(check_cache(*cfg, cache, B, T));
+  REQUIRE(k && v && bit, TRIROUTE_E_INVALID, "k, v or bit is NULL");
+  TRY(check_ws(*cfg, TRIROUTE_OP_KV_APPEND, B, T, ws, ws_bytes));
+  Carve cv(ws);
+  int32_t *slots = carve_kv(cv, B * T);
+  CHECK_HIP(tr::launch_kv_append(*cfg, tr::make_view(*cfg, *cache), B, T, seq_ids, k, v, bit, slots,
+                                 (hipStream_t)stream),
+            "kv_append launch");
+  return TRIROUTE_OK;
+}
+
+int triroute_kv_export(const triroute_cfg *cfg, const triroute_kv_cache *cache, int seq, int bi,
+                       int slot0, int count, void *k_out, void *v_out, uint16_t *k_sz,
+                       uint16_t *v_sz, int32_t *pos_out, triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  REQUIRE(cache && cache->base, TRIROUTE_E_INVALID, "cache is NULL");
+  REQUIRE(seq >= 0 && seq < cache->n_seq, TRIROUTE_E_INVALID, "seq out of range");
+  REQUIRE(bi >= 0 && bi < 4, TRIROUTE_E_INVALID, "bit index out of range");
+  REQUIRE(slot0 >= 0 && count >= 1 && int64_t(slot0) + count <= cache->capacity,
+          TRIROUTE_E_INVALID, "slot range outside the capacity");
+  REQUIRE(k_out && v_out, TRIROUTE_E_INVALID, "k_out or v_out is NULL");
+  CHECK_HIP(tr::launch_kv_export(*cfg, tr::make_view(*cfg, *cache), seq, bi, slot0, count, k_out,
+                                 v_out, k_sz, v_sz, pos_out, (hipStream_t)stream),
+            "kv_export launch");
+  return TRIROUTE_OK;
+}
+
+int triroute_router(const triroute_cfg *cfg, int B, int T, const void *x, const float *psi,
+                    const triroute_router_w *w, void *n1, uint8_t *mode, uint8_t *bit,
+                    int32_t *eidx, float *egate, const triroute_compaction *cmp, void *ws,
+                    size_t ws_bytes, triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  TRY(check_bt(B, T));
+  REQUIRE(x && (psi || cfg->d_psi == 0) && w && n1 && mode && bit && eidx && egate && cmp,
+          TRIROUTE_E_INVALID, "NULL argument");
+  REQUIRE(w->g1 && w->W1 && w->b1 && w->W2 && w->b2 && w->gr && w->Wa && w->ca && w->We &&
+              w->ce && w->Wb && w->cb,
+          TRIROUTE_E_INVALID, "NULL router weight");
+  REQUIRE(cmp->attn_cnt && cmp->attn_idx && cmp->exp_cnt && cmp->exp_off && cmp->exp_rows,
+          TRIROUTE_E_INVALID, "NULL compaction array");
+  TRY(check_ws(*cfg, TRIROUTE_OP_ROUTER, B, T, ws, ws_bytes));
+  TRY(prepare_once());
+  Carve cv(ws);
+  RouterWs rw = carve_router(cv, *cfg, B * T);
+  hipStream_t st = (hipStream_t)stream;
+  CHECK_HIP(tr::launch_router(*cfg, B * T, x, psi, *w, n1, mode, bit, eidx, egate, rw.rinv, rw.u, st),
+            "router launch");
+  CHECK_HIP(tr::launch_compact(*cfg, B, T, mode, eidx, *cmp, rw.hist, st), "compaction launch");
+  return TRIROUTE_OK;
+}
+
+int triroute_qkv(const triroute_cfg *cfg, int B, int T, const void *n1, const triroute_dense_w *w,
+                 const int32_t *pos0, void *q, void *k, void *v, triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  TRY(check_bt(B, T));
+  REQUIRE(n1 && w && w->Wq && w->Wk && w->Wv && q && k && v, TRIROUTE_E_INVALID, "NULL argument");
+  CHECK_HIP(tr::launch_qkv(*cfg, B, T, n1, *w, pos0, nullptr, q, k, v, (hipStream_t)stream),
+            "qkv launch");
+  return TRIROUTE_OK;
+}
+
+int triroute_attn_prefill(const triroute_cfg *cfg, int B, int T, const int32_t *seq_ids,
+                          const void *q, const triroute_kv_cache *cache, const uint8_t *mode,
+                          const triroute_compaction *cmp, void *o, void *ws, size_t ws_bytes,
+                          triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  TRY(check_bt(B, T));
+  TRY(check_cache(*cfg, cache, B, T));
+  REQUIRE(q && mode && cmp && cmp->attn_cnt && cmp->attn_idx && o, TRIROUTE_E_INVALID,
+          "NULL argument");
+  TRY(check_ws(*cfg, TRIROUTE_OP_ATTN_PREFILL, B, T, ws, ws_bytes));
+  hipStream_t st = (hipStream_t)stream;
+  const int64_t words = int64_t(B) * T * cfg->n_heads * cfg->head_dim * act_bytes(*cfg) / 4;
+  CHECK_HIP(tr::launch_fill_u32(o, words, 0u, st), "o clear");
+  CHECK_HIP(tr::launch_attn_valu_prefill(*cfg, tr::make_view(*cfg, *cache), B, T, seq_ids, q, *cmp,
+                                         o, st),
+            "attn_prefill launch");
+  return TRIROUTE_OK;
+}
+
+int triroute_attn_decode(const triroute_cfg *cfg, int B, const int32_t *seq_ids, const void *q,
+                         const triroute_kv_cache *cache, const uint8_t *mode, void *o, void *ws,
+                         size_t ws_bytes, triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  TRY(check_bt(B, 1));
+  TRY(check_cache(*cfg, cache, B, 1));
+  REQUIRE(q && mode && o, TRIROUTE_E_INVALID, "NULL argument");
+  TRY(check_ws(*cfg, TRIROUTE_OP_ATTN_DECODE, B, 1, ws, ws_bytes));
+  CHECK_HIP(tr::launch_attn_valu_decode(*cfg, tr::make_view(*cfg, *cache), B, seq_ids, q, mode, o,
+                                        (hipStream_t)stream),
+            "attn_decode launch");
+  return TRIROUTE_OK;
+}
+
+int triroute_oproj(const triroute_cfg *cfg, int n_tok, const void *x, const void *o,
+                   const triroute_dense_w *w, void *xt, triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  TRY(check_bt(n_tok, 1));
+  REQUIRE(x && o && w && w->Wo && xt, TRIROUTE_E_INVALID, "NULL argument");
+  CHECK_HIP(tr::launch_oproj(*cfg, n_tok, x, o, *w, xt, (hipStream_t)stream), "oproj launch");
+  return TRIROUTE_OK;
+}
+
+static int moe_impl(const triroute_cfg *cfg, int n_tok, const void *xt, const triroute_dense_w *dw,
+                    const triroute_moe_w *w, const int32_t *eidx, const float *egate,
+                    const triroute_compaction *cmp, void *x_out, Carve &cv, hipStream_t st) {
+  MoeWs m = carve_moe(cv, *cfg, n_tok);
+  CHECK_HIP(tr::launch_rms_norm2(*cfg, n_tok, xt, dw->g2, m.n2, st), "rms_norm2 launch");
+  CHECK_HIP(tr::launch_moe_gemms(*cfg, n_tok, m.n2, *w, *cmp, m.Hm, m.Y, st), "moe gemm launch");
+  CHECK_HIP(tr::launch_moe_combine(*cfg, n_tok, xt, m.Y, eidx, egate, x_out, st), "combine launch");
+  return TRIROUTE_OK;
+}
+
+int triroute_moe(const triroute_cfg *cfg, int n_tok, const void *xt, const triroute_dense_w *dw,
+                 const triroute_moe_w *w, const int32_t *eidx, const float *egate,
+                 const triroute_compaction *cmp, void *x_out, void *ws, size_t ws_bytes,
+                 triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  TRY(check_bt(n_tok, 1));
+  REQUIRE(xt && dw && dw->g2 && w && w->Wgate && w->Wup && w->Wdown && eidx && egate && cmp &&
+              cmp->exp_cnt && cmp->exp_off && cmp->exp_rows && x_out,
+          TRIROUTE_E_INVALID, "NULL argument");
+  TRY(check_ws(*cfg, TRIROUTE_OP_MOE, n_tok, 1, ws, ws_bytes));
+  Carve cv(ws);
+  return moe_impl(cfg, n_tok, xt, dw, w, eidx, egate, cmp, x_out, cv, (hipStream_t)stream);
+}
+
+static int layer_impl(const triroute_cfg *cfg, int B, int T, bool decode, const int32_t *seq_ids,
+                      const void *x, const float *psi, const triroute_router_w *rw,
+                      const triroute_dense_w *dw, const triroute_moe_w *mw,
+                      const triroute_kv_cache *cache, void *x_out, const triroute_layer_taps *taps,
+                      void *ws, size_t ws_bytes, triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  TRY(check_bt(B, T));
+  TRY(check_cache(*cfg, cache, B, T));
+  REQUIRE(x && (psi || cfg->d_psi == 0) && rw && dw && mw && x_out, TRIROUTE_E_INVALID,
+          "NULL argument");
+  const int op = decode ? TRIROUTE_OP_LAYER_DECODE : TRIROUTE_OP_LAYER_PREFILL;
+  TRY(check_ws(*cfg, op, B, T, ws, ws_bytes));
+  TRY(prepare_once());
+  hipStream_t st = (hipStream_t)stream;
+  Carve cv(ws);
+  LayerBufs L = carve_layer(cv, *cfg, B, T);
+  if (taps) {
+    if (taps->n1) L.n1 = taps->n1;
+    if (taps->mode) L.mode = taps->mode;
+    if (taps->bit) L.bit = taps->bit;
+    if (taps->eidx) L.eidx = taps->eidx;
+    if (taps->egate) L.egate = taps->egate;
+    if (taps->q) L.q = taps->q;
+    if (taps->k) L.k = taps->k;
+    if (taps->v) L.v = taps->v;
+    if (taps->o) L.o = taps->o;
+    if (taps->xt) L.xt = taps->xt;
+  }
+  const size_t scratch_at = cv.used;
+  const int N = B * T;
+  {
+    Carve sc(ws);
+    sc.used = scratch_at;
+    RouterWs r = carve_router(sc, *cfg, N);
+    CHECK_HIP(tr::launch_router(*cfg, N, x, psi, *rw, L.n1, L.mode, L.bit, L.eidx, L.egate, r.rinv,
+                                r.u, st),
+              "router launch");
+    CHECK_HIP(tr::launch_compact(*cfg, B, T, L.mode, L.eidx, L.cmp, r.hist, st), "compaction");
+  }
+  // positions continue each sequence: its current length, read on the device
+  const int32_t *seq_len = triroute_kv_seq_len_ptr(cache);
+  CHECK_HIP(tr::launch_qkv(*cfg, B, T, L.n1, *dw, seq_len, seq_ids, L.q, L.k, L.v, st), "qkv launch");
+  {
+    Carve sc(ws);
+    sc.used = scratch_at;
+    int32_t *slots = carve_kv(sc, N);
+    CHECK_HIP(tr::launch_kv_append(*cfg, tr::make_view(*cfg, *cache), B, T, seq_ids, L.k, L.v, L.bit,
+                                   slots, st),
+              "kv_append launch");
+  }
+  if (decode) {
+    CHECK_HIP(tr::launch_attn_valu_decode(*cfg, tr::make_view(*cfg, *cache), B, seq_ids, L.q, L.mode,
+                                          L.o, st),
+              "attn_decode launch");
+  } else {
+    const int64_t words = int64_t(N) * cfg->n_heads * cfg->head_dim * act_bytes(*cfg) / 4;
+    CHECK_HIP(tr::launch_fill_u32(L.o, words, 0u, st), "o clear");
+    CHECK_HIP(tr::launch_attn_valu_prefill(*cfg, tr::make_view(*cfg, *cache), B, T, seq_ids, L.q,
+                                           L.cmp, L.o, st),
+              "attn_prefill launch");
+  }
+  CHECK_HIP(tr::launch_oproj(*cfg, N, x, L.o, *dw, L.xt, st), "oproj launch");
+  {
+    Carve sc(ws);
+    sc.used = scratch_at;
+    TRY(moe_impl(cfg, N, L.xt, dw, mw, L.eidx, L.egate, &L.cmp, x_out, sc, st));
+  }
+  return TRIROUTE_OK;
+}
+
+int triroute_layer_prefill(const triroute_cfg *cfg, int B, int T, const int32_t *seq_ids,
+                           const void *x, const float *psi, const triroute_router_w *rw,
+                           const triroute_dense_w *dw, const triroute_moe_w *mw,
+                           const triroute_kv_cache *cache, void *x_out,
+                           const triroute_layer_taps *taps, void *ws, size_t ws_bytes,
+                           triroute_stream_t stream) {
+  return layer_impl(cfg, B, T, false, seq_ids, x, psi, rw, dw, mw, cache, x_out, taps, ws, ws_bytes,
+                    stream);
+}
+
+int triroute_layer_decode(const triroute_cfg *cfg, int B, const int32_t *seq_ids, const void *x,
+                          const float *psi, const triroute_router_w *rw, const triroute_dense_w *dw,
+                          const triroute_moe_w *mw, const triroute_kv_cache *cache, void *x_out,
+                          const triroute_layer_taps *taps, void *ws, size_t ws_bytes,
+                          triroute_stream_t stream) {
+  return layer_impl(cfg, B, 1, true, seq_ids, x, psi, rw, dw, mw, cache, x_out, taps, ws, ws_bytes,
+                    stream);
+}
+
+}  // extern "C"

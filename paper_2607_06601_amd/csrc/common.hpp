@@ -1,0 +1,122 @@
+// Internal declarations shared by the HIP sources of libtriroute (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "triroute.h"
+
+namespace tr {
+
+// ------------------------------------------------------------------ dtypes
+typedef uint16_t bf16;  // storage of a bfloat16
+
+__device__ __forceinline__ float bf2f(bf16 v) { return __uint_as_float(uint32_t(v) << 16); }
+
+// Round to nearest even (finite inputs).
+__device__ __forceinline__ bf16 f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return bf16(u >> 16);
+}
+
+template <typename T> struct Act;
+template <> struct Act<float> {
+  static constexpr int bytes = 4;
+  __device__ static float ld(const float *p, int64_t i) { return p[i]; }
+  __device__ static float cvt(float v) { return v; }
+  __device__ static void st(float *p, int64_t i, float v) { p[i] = v; }
+};
+template <> struct Act<bf16> {
+  static constexpr int bytes = 2;
+  __device__ static float ld(const bf16 *p, int64_t i) { return bf2f(p[i]); }
+  __device__ static float cvt(bf16 v) { return bf2f(v); }
+  __device__ static void st(bf16 *p, int64_t i, float v) { p[i] = f2bf(v); }
+};
+
+// --------------------------------------------------------- wave helpers
+constexpr int WAVE = 64;
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, WAVE);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, WAVE));
+  return v;
+}
+// Reductions within aligned lane segments of `seg` lanes (seg a power of 2).
+__device__ __forceinline__ float seg_min(float v, int seg) {
+  for (int m = seg >> 1; m >= 1; m >>= 1) v = fminf(v, __shfl_xor(v, m, WAVE));
+  return v;
+}
+__device__ __forceinline__ float seg_max(float v, int seg) {
+  for (int m = seg >> 1; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, WAVE));
+  return v;
+}
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  int l = __lane_id();
+  return l ? (~0ull >> (64 - l)) : 0ull;
+}
+
+// ------------------------------------------------------------ KV cache view
+// Bits of the physical store of width index bi (bi = 3 keeps the act dtype).
+__host__ __device__ inline int pool_bits(int bi, int act_bytes) {
+  return bi == 0 ? 2 : bi == 1 ? 4 : bi == 2 ? 8 : 8 * act_bytes;
+}
+
+struct CacheView {
+  uint8_t *base;
+  int32_t *status, *seq_len, *pool_len, *pos;
+  int n_seq, capacity, TS, n_tiles;
+  int Hkv, dh, G, act_bytes;
+  int64_t off_pool[4], tile_bytes[4];
+
+  __device__ __forceinline__ uint8_t *tile(int s, int bi, int g, int t) const {
+    return base + off_pool[bi] + ((int64_t(s) * Hkv + g) * n_tiles + t) * tile_bytes[bi];
+  }
+  __device__ __forceinline__ int bits(int bi) const { return pool_bits(bi, act_bytes); }
+  // byte offsets inside a tile
+  __device__ __forceinline__ int v_codes_off(int bi) const { return 512 * bits(bi); }
+  __device__ __forceinline__ int k_sz_off(int bi) const { return 1024 * bits(bi); }
+  __device__ __forceinline__ int v_sz_off(int bi) const {
+    return 1024 * bits(bi) + TS * (dh / G) * 4;
+  }
+};
+
+// Element placement inside a 64-lane record (see triroute.h).
+// K element (slot st in tile, channel c) -> (lane record, element index q).
+__device__ __forceinline__ void k_place(int st, int c, int dh, int &lane, int &q) {
+  int KS = dh >> 5;
+  int blk = st >> 4, n = st & 15;
+  int ks = c >> 5, o = (c >> 3) & 3, j = c & 7;
+  lane = o * 16 + n;
+  q = (blk * KS + ks) * 8 + j;
+}
+// V element (slot st in tile, channel c) -> (lane record, element index q).
+__device__ __forceinline__ void v_place(int st, int c, int dh, int &lane, int &q) {
+  int CB = dh >> 4;
+  int kv = st >> 5, o = (st >> 3) & 3, j = st & 7;
+  int cb = c >> 4, n = c & 15;
+  lane = o * 16 + n;
+  q = (kv * CB + cb) * 8 + j;
+}
+// element index q of a record of bp bits -> (32-bit word, bit offset)
+__device__ __forceinline__ void q_word(int q, int bp, int &word, int &bit) {
+  if (bp == 32) {
+    word = q;
+    bit = 0;
+    return;
+  }
+  int per = 16 / bp;
+  int pr = q >> 1;
+  word = pr / per;
+  bit = (pr % per) * bp + (q & 1) * 16;
+}
+
+// ------------------------------------------------------------ launch helpers
+CacheView make_view(const triroute_cfg &cfg, const triroute_kv_cache &c);
+
+}  // namespace tr

@@ -1,0 +1,140 @@
+// Token compaction by routing decision: deterministic stable partitions by
+// prefix sums (no atomics decide any order).
+//
+//   attention: per (b, h), the ascending t of local and of full queries
+//   experts  : per expert 1..E, the ascending assignment ids a = i*k + slot
+#include "kernels.hpp"
+
+namespace tr {
+
+constexpr int CHUNK = 1024;  // assignments per expert block
+
+// Blocks [0, B*H): attention lists of one (b, h).  Blocks [B*H, +nbe):
+// per-block expert histograms.
+__global__ __launch_bounds__(256) void compact_count_kernel(
+    const uint8_t *__restrict__ mode, const int32_t *__restrict__ eidx, int B, int T, int H,
+    int E1, int Nk, int32_t *__restrict__ attn_cnt, int32_t *__restrict__ attn_idx,
+    int32_t *__restrict__ hist) {
+  __shared__ int wcnt[2][4];
+  __shared__ int lh[64];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int bid = blockIdx.x;
+  if (bid < B * H) {
+    const int b = bid / H, h = bid % H;
+    int base[2] = {0, 0};
+    for (int t0 = 0; t0 < T; t0 += 256) {
+      const int t = t0 + tid;
+      const int m = t < T ? mode[(int64_t(b) * T + t) * H + h] : 0;
+      uint64_t bal[2];
+      bal[0] = __ballot(m == 1);
+      bal[1] = __ballot(m == 2);
+      if (lane == 0) {
+        wcnt[0][w] = __popcll(bal[0]);
+        wcnt[1][w] = __popcll(bal[1]);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int mm = 0; mm < 2; ++mm) {
+        if (m == mm + 1) {
+          int off = base[mm] + __popcll(bal[mm] & lanemask_lt());
+          for (int ww = 0; ww < w; ++ww) off += wcnt[mm][ww];
+          attn_idx[(int64_t(bid) * 2 + mm) * T + off] = t;
+        }
+      }
+#pragma unroll
+      for (int mm = 0; mm < 2; ++mm)
+        base[mm] += wcnt[mm][0] + wcnt[mm][1] + wcnt[mm][2] + wcnt[mm][3];
+      __syncthreads();
+    }
+    if (tid < 2) attn_cnt[bid * 2 + tid] = base[tid];
+    return;
+  }
+  const int j = bid - B * H;
+  for (int e = tid; e < E1; e += 256) lh[e] = 0;
+  __syncthreads();
+  for (int a = j * CHUNK + tid; a < min(Nk, (j + 1) * CHUNK); a += 256) atomicAdd(&lh[eidx[a]], 1);
+  __syncthreads();
+  for (int e = tid; e < E1; e += 256) hist[j * E1 + e] = lh[e];
+}
+
+// One block: expert counts, offsets and each block's first output position.
+__global__ __launch_bounds__(64) void compact_scan_kernel(int32_t *__restrict__ hist, int nbe,
+                                                         int E1, int32_t *__restrict__ exp_cnt,
+                                                         int32_t *__restrict__ exp_off) {
+  __shared__ int cnt[64];
+  const int e = threadIdx.x;
+  if (e < E1) {
+    int run = 0;
+    for (int j = 0; j < nbe; ++j) {
+      int v = hist[j * E1 + e];
+      hist[j * E1 + e] = run;
+      run += v;
+    }
+    cnt[e] = run;
+    exp_cnt[e] = run;
+  }
+  __syncthreads();
+  if (e == 0) {
+    int off = 0;
+    exp_off[0] = 0;
+    for (int ee = 1; ee < E1; ++ee) {
+      off += cnt[ee];
+      exp_off[ee] = off;
+    }
+  }
+  __syncthreads();
+  if (e >= 1 && e < E1) {
+    int start = 0;
+    for (int ee = 1; ee < e; ++ee) start += cnt[ee];
+    for (int j = 0; j < nbe; ++j) hist[j * E1 + e] += start;
+  }
+}
+
+// Stable scatter of assignment ids into per-expert lists.
+__global__ __launch_bounds__(256) void compact_scatter_kernel(const int32_t *__restrict__ eidx,
+                                                              const int32_t *__restrict__ hist,
+                                                              int E1, int Nk,
+                                                              int32_t *__restrict__ rows) {
+  __shared__ int wc[4][64];
+  __shared__ int run[64];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int j = blockIdx.x;
+  for (int e = tid; e < E1; e += 256) run[e] = hist[j * E1 + e];
+  __syncthreads();
+  for (int sub = 0; sub < CHUNK; sub += 256) {
+    const int a = j * CHUNK + sub + tid;
+    const int e = a < Nk ? eidx[a] : -1;
+    int rank = 0;
+    for (int ee = 1; ee < E1; ++ee) {
+      uint64_t bal = __ballot(e == ee);
+      if (e == ee) rank = __popcll(bal & lanemask_lt());
+      if (lane == 0) wc[w][ee] = __popcll(bal);
+    }
+    __syncthreads();
+    if (e >= 1) {
+      int pos = run[e] + rank;
+      for (int ww = 0; ww < w; ++ww) pos += wc[ww][e];
+      rows[pos] = a;
+    }
+    __syncthreads();
+    for (int ee = tid; ee < E1; ee += 256)
+      if (ee >= 1) run[ee] += wc[0][ee] + wc[1][ee] + wc[2][ee] + wc[3][ee];
+    __syncthreads();
+  }
+}
+
+int compact_hist_ints(int N, int k, int E1) { return ((N * k + CHUNK - 1) / CHUNK) * E1; }
+
+hipError_t launch_compact(const triroute_cfg &cfg, int B, int T, const uint8_t *mode,
+                          const int32_t *eidx, const triroute_compaction &c, int32_t *hist,
+                          hipStream_t st) {
+  const int H = cfg.n_heads, E1 = cfg.n_experts + 1, Nk = B * T * cfg.top_k;
+  const int nbe = (Nk + CHUNK - 1) / CHUNK;
+  compact_count_kernel<<<B * H + nbe, 256, 0, st>>>(mode, eidx, B, T, H, E1, Nk, c.attn_cnt,
+                                                    c.attn_idx, hist);
+  compact_scan_kernel<<<1, 64, 0, st>>>(hist, nbe, E1, c.exp_cnt, c.exp_off);
+  compact_scatter_kernel<<<nbe, 256, 0, st>>>(eidx, hist, E1, Nk, c.exp_rows);
+  return hipGetLastError();
+}
+
+}  // namespace tr

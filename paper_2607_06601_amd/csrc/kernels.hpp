@@ -1,0 +1,50 @@
+// Launchers of the device kernels (internal to libtriroute).
+#pragma once
+
+#include "common.hpp"
+
+namespace tr {
+
+// router.hip
+hipError_t router_prepare();
+hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const float *psi,
+                         const triroute_router_w &w, void *n1, uint8_t *mode, uint8_t *bit,
+                         int32_t *eidx, float *egate, float *rinv, float *u, hipStream_t st);
+// compact.hip
+int compact_hist_ints(int N, int k, int E1);
+hipError_t launch_compact(const triroute_cfg &cfg, int B, int T, const uint8_t *mode,
+                          const int32_t *eidx, const triroute_compaction &c, int32_t *hist,
+                          hipStream_t st);
+// kv.hip
+hipError_t launch_fill_u32(void *p, int64_t n_words, uint32_t v, hipStream_t st);
+hipError_t launch_kv_append(const triroute_cfg &cfg, const CacheView &cv, int B, int T,
+                            const int32_t *seq_ids, const void *k, const void *v,
+                            const uint8_t *bit, int32_t *slots, hipStream_t st);
+hipError_t launch_kv_export(const triroute_cfg &cfg, const CacheView &cv, int seq, int bi,
+                            int slot0, int count, void *kout, void *vout, uint16_t *ksz,
+                            uint16_t *vsz, int32_t *pos_out, hipStream_t st);
+// gemm.hip
+// position of token (b, t) = (pos_base ? pos_base[pos_idx ? pos_idx[b] : b] : 0) + t
+hipError_t launch_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
+                      const triroute_dense_w &w, const int32_t *pos_base, const int32_t *pos_idx,
+                      void *q, void *k, void *v, hipStream_t st);
+hipError_t launch_oproj(const triroute_cfg &cfg, int N, const void *x, const void *o,
+                        const triroute_dense_w &w, void *xt, hipStream_t st);
+hipError_t launch_moe_gemms(const triroute_cfg &cfg, int N, const void *n2,
+                            const triroute_moe_w &w, const triroute_compaction &c, void *Hm,
+                            float *Y, hipStream_t st);
+// attn_valu.hip
+hipError_t launch_attn_valu_prefill(const triroute_cfg &cfg, const CacheView &cv, int B, int Tq,
+                                    const int32_t *seq_ids, const void *q,
+                                    const triroute_compaction &c, void *o, hipStream_t st);
+hipError_t launch_attn_valu_decode(const triroute_cfg &cfg, const CacheView &cv, int B,
+                                   const int32_t *seq_ids, const void *q, const uint8_t *mode,
+                                   void *o, hipStream_t st);
+// misc.hip
+hipError_t launch_rms_norm2(const triroute_cfg &cfg, int N, const void *x, const void *g,
+                            void *out, hipStream_t st);
+hipError_t launch_moe_combine(const triroute_cfg &cfg, int N, const void *xt, const float *Y,
+                              const int32_t *eidx, const float *egate, void *xout,
+                              hipStream_t st);
+
+}  // namespace tr

@@ -1,0 +1,271 @@
+// Mixed-width KV cache: layout, append (per-token group quantizer of paper
+// Sec. 3.2 (C)) and read-back.
+//
+// Quantizer (bit exact with the CPU oracle): per group of G channels, fp32
+// mn/mx, s32 = (mx - mn) / (2^b - 1), s = fp16_rne(s32), z = fp16_rne(mn),
+// code = 0 if s == 0 else clamp(rint_even((x - z) / s), 0, 2^b - 1), every
+// step in IEEE fp32.  16-bit stores the activation value verbatim.
+#include "kernels.hpp"
+
+namespace tr {
+
+__global__ void fill_u32_kernel(uint32_t *__restrict__ p, int64_t n, uint32_t v) {
+  for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * blockDim.x)
+    p[i] = v;
+}
+
+hipError_t launch_fill_u32(void *p, int64_t n_words, uint32_t v, hipStream_t st) {
+  if (n_words <= 0) return hipSuccess;
+  int64_t blocks = (n_words + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  fill_u32_kernel<<<dim3(unsigned(blocks)), 256, 0, st>>>((uint32_t *)p, n_words, v);
+  return hipGetLastError();
+}
+
+// Per batch row: slots in each width pool, positions, new lengths.
+__global__ __launch_bounds__(256) void kv_slots_kernel(CacheView cv, int T,
+                                                       const int32_t *__restrict__ seq_ids,
+                                                       const uint8_t *__restrict__ bit,
+                                                       int32_t *__restrict__ slots) {
+  __shared__ int wc[4][4];
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int s = seq_ids ? seq_ids[b] : b;
+  if (s < 0 || s >= cv.n_seq) {
+    if (tid == 0) atomicOr(cv.status, int(TRIROUTE_CACHE_BAD_SEQ));
+    for (int t = tid; t < T; t += 256) slots[int64_t(b) * T + t] = -1;
+    return;
+  }
+  const int len0 = cv.seq_len[s];
+  if (len0 + T > cv.capacity) {
+    if (tid == 0) atomicOr(cv.status, int(TRIROUTE_CACHE_OVERFLOW));
+    for (int t = tid; t < T; t += 256) slots[int64_t(b) * T + t] = -1;
+    return;
+  }
+  int run[4];
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi) run[bi] = cv.pool_len[s * 4 + bi];
+  for (int t0 = 0; t0 < T; t0 += 256) {
+    const int t = t0 + tid;
+    const int bi = t < T ? int(bit[int64_t(b) * T + t]) : -1;
+    uint64_t bal[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) bal[q] = __ballot(bi == q);
+    if (lane == 0)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) wc[q][w] = __popcll(bal[q]);
+    __syncthreads();
+    if (bi >= 0) {
+      int slot = run[bi] + __popcll(bal[bi] & lanemask_lt());
+      for (int ww = 0; ww < w; ++ww) slot += wc[bi][ww];
+      slots[int64_t(b) * T + t] = slot;
+      cv.pos[(int64_t(s) * 4 + bi) * cv.capacity + slot] = len0 + t;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) run[q] += wc[q][0] + wc[q][1] + wc[q][2] + wc[q][3];
+    __syncthreads();
+  }
+  if (tid == 0) {
+#pragma unroll
+    for (int bi = 0; bi < 4; ++bi) cv.pool_len[s * 4 + bi] = run[bi];
+    cv.seq_len[s] = len0 + T;
+  }
+}
+
+// One wave per (token, kv head): quantize K and V, write codes and scales.
+template <typename T>
+__global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int N,
+                                                       const int32_t *__restrict__ seq_ids,
+                                                       const T *__restrict__ kin,
+                                                       const T *__restrict__ vin,
+                                                       const uint8_t *__restrict__ bit,
+                                                       const int32_t *__restrict__ slots) {
+  __shared__ uint32_t el[4][2][128];  // per wave: element value per channel (K, V)
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int item = blockIdx.x * 4 + w;
+  const int Hkv = cv.Hkv, dh = cv.dh, G = cv.G;
+  const int i = item / Hkv, g = item % Hkv;
+  const int slot = item < N * Hkv ? slots[i] : -1;
+  const bool valid = slot >= 0;  // uniform per wave
+  const int b = i / T_;
+  const int s = valid ? (seq_ids ? seq_ids[b] : b) : 0;
+  const int bi = valid ? int(bit[i]) : 0;
+  const int bp = cv.bits(bi);
+  const int tile = valid ? slot / cv.TS : 0, st = valid ? slot % cv.TS : 0;
+  uint8_t *tp = cv.tile(s, bi, g, tile);
+  const int NR = dh >> 6;  // channels per lane: lane + 64 r
+  for (int kvsel = 0; kvsel < 2 && valid; ++kvsel) {
+    const T *src = (kvsel ? vin : kin) + int64_t(i) * Hkv * dh + g * dh;
+    for (int r = 0; r < NR; ++r) {
+      const int c = lane + 64 * r;
+      T raw = src[c];
+      float x = Act<T>::cvt(raw);
+      uint32_t e;
+      if (bi == 3) {
+        if (sizeof(T) == 2)
+          e = uint32_t(*(const uint16_t *)&raw);
+        else
+          e = __float_as_uint(x);
+      } else {
+        const int seg = G < 64 ? G : 64;
+        float mn = seg_min(x, seg), mx = seg_max(x, seg);
+        const float levels = float((1 << bp) - 1);
+        float s32 = __fdiv_rn(mx - mn, levels);
+        _Float16 s16 = (_Float16)s32;
+        _Float16 z16 = (_Float16)mn;
+        float S = (float)s16, Z = (float)z16;
+        float q = 0.f;
+        if (S != 0.f) q = fminf(fmaxf(rintf(__fdiv_rn(x - Z, S)), 0.f), levels);
+        e = uint32_t(q);
+        if ((lane & (seg - 1)) == 0) {
+          const int grp = c / G;
+          const int off = (kvsel ? cv.v_sz_off(bi) : cv.k_sz_off(bi)) + (st * (dh / G) + grp) * 4;
+          uint32_t pk = uint32_t(*(uint16_t *)&s16) | (uint32_t(*(uint16_t *)&z16) << 16);
+          *(uint32_t *)(tp + off) = pk;
+        }
+      }
+      el[w][kvsel][c] = e;
+    }
+  }
+  __syncthreads();
+  if (!valid) return;
+  // ---- K: every 32-bit word touched by this token belongs to it alone
+  {
+    const int KS = dh >> 5;
+    const int blk = st >> 4, n = st & 15;
+    const int per = bp == 32 ? 1 : 32 / bp;         // elements per word
+    const int q0 = blk * KS * 8, nq = KS * 8;        // this token's element range per record
+    const int words_per_rec = (nq + per - 1) / per;
+    for (int wid = lane; wid < 4 * words_per_rec; wid += 64) {
+      const int o = wid / words_per_rec, wr = wid % words_per_rec;
+      const int qa = q0 + wr * per;
+      uint32_t val = 0;
+      int word = 0;
+      for (int qq = qa; qq < qa + per; ++qq) {
+        const int f = qq >> 3, j = qq & 7;
+        const int ks = f % KS;
+        const int c = 32 * ks + 8 * o + j;
+        int wd, bt;
+        q_word(qq, bp, wd, bt);
+        word = wd;
+        val |= el[w][0][c] << bt;
+      }
+      *(uint32_t *)(tp + (o * 16 + n) * (8 * bp) + word * 4) = val;
+    }
+  }
+  // ---- V: words are shared by neighbouring slots
+  {
+    uint8_t *vp = tp + cv.v_codes_off(bi);
+    for (int r = 0; r < NR; ++r) {
+      const int c = lane + 64 * r;
+      int ln, q, wd, bt;
+      v_place(st, c, dh, ln, q);
+      q_word(q, bp, wd, bt);
+      uint8_t *addr = vp + ln * (8 * bp) + wd * 4;
+      const uint32_t e = el[w][1][c];
+      if (bp <= 4)
+        atomicOr((unsigned int *)addr, e << bt);
+      else if (bp == 8)
+        addr[bt >> 3] = uint8_t(e);
+      else if (bp == 16)
+        *(uint16_t *)(addr + (bt >> 3)) = uint16_t(e);
+      else
+        *(uint32_t *)addr = e;
+    }
+  }
+}
+
+// Logical read-back of slots [slot0, slot0 + count) of pool (seq, bi).
+template <typename T>
+__global__ void kv_export_kernel(CacheView cv, int seq, int bi, int slot0, int count,
+                                 uint8_t *__restrict__ kout, uint8_t *__restrict__ vout,
+                                 uint16_t *__restrict__ ksz, uint16_t *__restrict__ vsz,
+                                 int32_t *__restrict__ pos_out) {
+  const int Hkv = cv.Hkv, dh = cv.dh, G = cv.G;
+  const int64_t total = int64_t(count) * Hkv * dh;
+  const int len = cv.pool_len[seq * 4 + bi];
+  const int bp = cv.bits(bi);
+  for (int64_t idx = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; idx < total;
+       idx += int64_t(gridDim.x) * blockDim.x) {
+    const int c = int(idx % dh);
+    const int g = int((idx / dh) % Hkv);
+    const int r = int(idx / (int64_t(dh) * Hkv));
+    const int slot = slot0 + r;
+    const bool live = slot < len;
+    uint32_t ke = 0, ve = 0;
+    uint32_t kszv = 0, vszv = 0;
+    if (live) {
+      const int tile = slot / cv.TS, st = slot % cv.TS;
+      const uint8_t *tp = cv.tile(seq, bi, g, tile);
+      int ln, q, wd, bt;
+      const uint32_t mask = bp == 32 ? 0xFFFFFFFFu : ((1u << bp) - 1u);
+      k_place(st, c, dh, ln, q);
+      q_word(q, bp, wd, bt);
+      ke = (*(const uint32_t *)(tp + ln * 8 * bp + wd * 4) >> bt) & mask;
+      v_place(st, c, dh, ln, q);
+      q_word(q, bp, wd, bt);
+      ve = (*(const uint32_t *)(tp + cv.v_codes_off(bi) + ln * 8 * bp + wd * 4) >> bt) & mask;
+      if (bi < 3 && c % G == 0) {
+        kszv = *(const uint32_t *)(tp + cv.k_sz_off(bi) + (st * (dh / G) + c / G) * 4);
+        vszv = *(const uint32_t *)(tp + cv.v_sz_off(bi) + (st * (dh / G) + c / G) * 4);
+      }
+    }
+    if (bi < 3) {
+      kout[idx] = uint8_t(ke);
+      vout[idx] = uint8_t(ve);
+      if (c % G == 0) {
+        const int64_t so = ((int64_t(r) * Hkv + g) * (dh / G) + c / G) * 2;
+        if (ksz) {
+          ksz[so] = uint16_t(kszv);
+          ksz[so + 1] = uint16_t(kszv >> 16);
+        }
+        if (vsz) {
+          vsz[so] = uint16_t(vszv);
+          vsz[so + 1] = uint16_t(vszv >> 16);
+        }
+      }
+    } else if (sizeof(T) == 2) {
+      ((uint16_t *)kout)[idx] = uint16_t(ke);
+      ((uint16_t *)vout)[idx] = uint16_t(ve);
+    } else {
+      ((uint32_t *)kout)[idx] = ke;
+      ((uint32_t *)vout)[idx] = ve;
+    }
+    if (pos_out && c == 0 && g == 0)
+      pos_out[r] = live ? cv.pos[(int64_t(seq) * 4 + bi) * cv.capacity + slot] : 0;
+  }
+}
+
+hipError_t launch_kv_append(const triroute_cfg &cfg, const CacheView &cv, int B, int T,
+                            const int32_t *seq_ids, const void *k, const void *v,
+                            const uint8_t *bit, int32_t *slots, hipStream_t st) {
+  kv_slots_kernel<<<B, 256, 0, st>>>(cv, T, seq_ids, bit, slots);
+  const int N = B * T;
+  dim3 grid((N * cfg.n_kv_heads + 3) / 4);
+  if (cfg.act == TRIROUTE_BF16)
+    kv_write_kernel<bf16><<<grid, 256, 0, st>>>(cv, T, N, seq_ids, (const bf16 *)k,
+                                                (const bf16 *)v, bit, slots);
+  else
+    kv_write_kernel<float><<<grid, 256, 0, st>>>(cv, T, N, seq_ids, (const float *)k,
+                                                 (const float *)v, bit, slots);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_export(const triroute_cfg &cfg, const CacheView &cv, int seq, int bi,
+                            int slot0, int count, void *kout, void *vout, uint16_t *ksz,
+                            uint16_t *vsz, int32_t *pos_out, hipStream_t st) {
+  int64_t total = int64_t(count) * cv.Hkv * cv.dh;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  if (cfg.act == TRIROUTE_BF16)
+    kv_export_kernel<bf16><<<dim3(unsigned(blocks)), 256, 0, st>>>(
+        cv, seq, bi, slot0, count, (uint8_t *)kout, (uint8_t *)vout, ksz, vsz, pos_out);
+  else
+    kv_export_kernel<float><<<dim3(unsigned(blocks)), 256, 0, st>>>(
+        cv, seq, bi, slot0, count, (uint8_t *)kout, (uint8_t *)vout, ksz, vsz, pos_out);
+  return hipGetLastError();
+}
+
+}  // namespace tr

@@ -1,0 +1,87 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function include/triroute.h declares, and rejects bad arguments with
+the documented status codes before launching anything."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+import paper_2607_06601_amd as tr
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared():
+    text = open(os.path.join(ROOT, "include", "triroute.h")).read()
+    return sorted(set(re.findall(r"\b(triroute_[a-z_0-9]+)\s*\(", text)))
+
+
+def cfg160(**over):
+    c = tr.make_cfg(768, 12, 3, 64, 128, 8, 2, 2048, 64, "bf16")
+    for k, v in over.items():
+        setattr(c, k, v)
+    return c
+
+
+def test_library_exports_every_declared_symbol():
+    lib = tr.lib()
+    names = declared()
+    assert len(names) >= 18
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(tr.EXPORTS)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("head_dim", 96, -2), ("kv_group", 48, -2), ("n_kv_heads", 5, -1), ("top_k", 10, -1),
+    ("act", 7, -1), ("d_router", 64, -2), ("rms_eps", 0.0, -1), ("d_model", 100, -2),
+    ("n_heads", 0, -1)])
+def test_validate_rejects(field, value, code):
+    assert tr.validate(cfg160(**{field: value})) == code
+    assert tr.lib().triroute_last_error()
+
+
+def test_validate_accepts_every_workload():
+    import gen
+    from paper_2607_06601_amd.device import cfg_from
+    for name, shape in gen.CONFIGS.items():
+        assert tr.validate(cfg_from(shape)) == 0, name
+
+
+def test_workspace_and_cache_sizes():
+    c = cfg160()
+    assert tr.workspace_bytes(c, tr.OP_QKV, 8, 2048) == 0
+    assert tr.workspace_bytes(c, tr.OP_KV_APPEND, 8, 2048) == 8 * 2048 * 4
+    lay = tr.workspace_bytes(c, tr.OP_LAYER_PREFILL, 8, 2048)
+    assert lay > tr.workspace_bytes(c, tr.OP_MOE, 8, 2048)
+    n = C.c_size_t()
+    # 1.3B decode: dh 128, G 64: a 32-slot tile of one kv head holds 80/144/272/512 B per slot
+    c5 = tr.make_cfg(2048, 16, 4, 128, 1024, 16, 2, 5632, 64, "bf16")
+    assert tr.lib().triroute_kv_cache_bytes(C.byref(c5), 32, 32784, C.byref(n)) == 0
+    tiles = (32784 + 31) // 32
+    pools = 32 * 4 * tiles * 32 * (80 + 144 + 272 + 512)
+    assert pools < n.value < pools + 32 * 16 * 32784 * 4 + (1 << 20)
+
+
+def test_bad_calls_return_codes_without_launching():
+    lib = tr.lib()
+    c = cfg160()
+    rw, cmp = tr.RouterW(), tr.Compaction()
+    # NULL pointers
+    r = lib.triroute_router(C.byref(c), 8, 2048, None, None, C.byref(rw), None, None, None,
+                            None, None, C.byref(cmp), None, 0, None)
+    assert r == tr.lib().triroute_validate(None) == -1
+    # workspace too small (all pointers non-NULL but never dereferenced on the host)
+    fake = 1 << 40
+    rw = tr.RouterW(*([fake] * 12))
+    cmp = tr.Compaction(*([fake] * 5))
+    r = lib.triroute_router(C.byref(c), 8, 2048, fake, fake, C.byref(rw), fake, fake, fake,
+                            fake, fake, C.byref(cmp), fake, 1024, None)
+    assert r == -3 and b"workspace" in lib.triroute_last_error()
+    # B*T beyond the supported range
+    n = C.c_size_t()
+    assert lib.triroute_workspace_bytes(C.byref(c), 0, 1 << 13, 1 << 12, C.byref(n)) == -2
+    # unknown op
+    assert lib.triroute_workspace_bytes(C.byref(c), 42, 1, 1, C.byref(n)) == -1
+    assert lib.triroute_status_string(-3) == b"workspace too small"

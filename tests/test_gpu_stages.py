@@ -1,0 +1,360 @@
+"""Per-stage parity of the HIP path against the CPU oracle (through the C ABI).
+
+Discrete results (routing decisions, compaction lists, KV codes, scales,
+positions) must be bit exact; activations within the bf16 / fp32 tolerance.
+Every input comes from the seeded generator; the oracle never sees a value
+the GPU produced."""
+import numpy as np
+import pytest
+import torch
+
+import gen
+import oracle
+import paper_2607_06601_amd as tr
+from oracle import quant
+from paper_2607_06601_amd.device import DeviceLayer, cfg_from, to_dev
+
+from _common import assert_close, layer, npy, shape_of, torch_act
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    tr.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+# ------------------------------------------------------------------ router
+def run_router(L):
+    cfg = L["cfg"]
+    D = DeviceLayer(L, moe=False)
+    c = D.cfg
+    B, T, H, k = cfg["B"], cfg["T"], cfg["H"], cfg["k"]
+    N = B * T
+    n1 = torch.empty(N, cfg["d"], dtype=D.act, device=DEV)
+    mode = torch.empty(N, H, dtype=torch.uint8, device=DEV)
+    bit = torch.empty(N, dtype=torch.uint8, device=DEV)
+    eidx = torch.empty(N, k, dtype=torch.int32, device=DEV)
+    egate = torch.empty(N, k, dtype=torch.float32, device=DEV)
+    cmp = tr.CompactionBuffers(c, B, T)
+    ws = tr.workspace(c, tr.OP_ROUTER, B, T)
+    tr.router(c, B, T, D.x, D.psi, D.rw, n1, mode, bit, eidx, egate, cmp.struct, ws)
+    torch.cuda.synchronize()
+    return dict(n1=n1, mode=mode, bit=bit, eidx=eidx, egate=egate, cmp=cmp)
+
+
+@pytest.mark.parametrize("name,seed", [
+    ("tiny_f32_prefill", 0), ("160m_bf16_prefill", 1), ("410m_bf16_decode", 103),
+    ("1p3b_bf16_prefill", 104), ("1p3b_bf16_decode", 105)])
+def test_router_and_compaction_bit_exact(name, seed):
+    L = layer(name, seed, moe=False)
+    cfg = L["cfg"]
+    B, T, H, E, k = cfg["B"], cfg["T"], cfg["H"], cfg["E"], cfg["k"]
+    g = run_router(L)
+    n1, za, ze, zb = oracle.router_logits(L)
+    mode, bit, eidx, egate = oracle.decide(za, ze, zb, k)
+    np.testing.assert_array_equal(npy(g["mode"]), mode)
+    np.testing.assert_array_equal(npy(g["bit"]), bit)
+    np.testing.assert_array_equal(npy(g["eidx"]), eidx)
+    np.testing.assert_allclose(npy(g["egate"]), egate, rtol=2e-5, atol=1e-6)
+    assert_close(npy(g["n1"]), oracle.layer.to_native(n1, cfg["act"]) if cfg["act"] == "f32"
+                 else n1, cfg["act"], "n1")
+    c = oracle.compact(mode, eidx, B, T, H, E, k)
+    cnt = npy(g["cmp"].attn_cnt)
+    np.testing.assert_array_equal(cnt, c["attn_cnt"])
+    idx = npy(g["cmp"].attn_idx).reshape(B * H * 2, T)
+    for s in range(B * H * 2):
+        np.testing.assert_array_equal(idx[s, :cnt[s]], c["attn_idx"][s, :cnt[s]])
+    np.testing.assert_array_equal(npy(g["cmp"].exp_cnt), c["exp_cnt"])
+    np.testing.assert_array_equal(npy(g["cmp"].exp_off), c["exp_off"])
+    nreal = int(c["exp_off"][-1])
+    np.testing.assert_array_equal(npy(g["cmp"].exp_rows)[:nreal], c["exp_rows"])
+
+
+# ------------------------------------------------------------ KV append
+KV_SHAPES = [  # (act, dh, G, Hkv)
+    ("f32", 64, 32, 1), ("bf16", 64, 64, 3), ("bf16", 128, 64, 4), ("bf16", 128, 32, 2)]
+
+
+def kv_cfg(act, dh, G, Hkv):
+    return tr.make_cfg(256, 4 * Hkv, Hkv, dh, 32, 4, 1, 512, G, act)
+
+
+def export_pool(c, cache, s, bi, n, act, Hkv, dh, G):
+    tdt = torch_act(act)
+    if bi < 3:
+        ko = torch.zeros(n, Hkv, dh, dtype=torch.uint8, device=DEV)
+        vo = torch.zeros_like(ko)
+    else:
+        ko = torch.zeros(n, Hkv, dh, dtype=tdt, device=DEV)
+        vo = torch.zeros_like(ko)
+    ks = torch.zeros(n, Hkv, dh // G, 2, dtype=torch.int16, device=DEV)
+    vs = torch.zeros_like(ks)
+    pos = torch.zeros(n, dtype=torch.int32, device=DEV)
+    tr.kv_export(c, cache, s, bi, 0, n, ko, vo, ks, vs, pos)
+    torch.cuda.synchronize()
+    return ko, vo, ks, vs, pos
+
+
+def _f16(bits_i16):
+    return np.asarray(bits_i16).astype(np.int16).view(np.float16)
+
+
+@pytest.mark.parametrize("act,dh,G,Hkv", KV_SHAPES)
+def test_kv_append_codes_bit_exact(act, dh, G, Hkv):
+    B, T1, T2, cap = 3, 37, 58, 200
+    c = kv_cfg(act, dh, G, Hkv)
+    tdt = torch_act(act)
+    k, v = gen.kv_block(11, B * (T1 + T2), Hkv, dh, act, std=0.7)
+    k, v = k.reshape(B, T1 + T2, Hkv, dh), v.reshape(B, T1 + T2, Hkv, dh)
+    bits = gen.stream(11, "kvbits").integers(0, 4, (B, T1 + T2)).astype(np.uint8)
+    cache = tr.KVCache(c, B + 1, cap)
+    for (t0, t1) in ((0, T1), (T1, T1 + T2)):
+        Tn = t1 - t0
+        kd = to_dev(k[:, t0:t1].reshape(B * Tn, Hkv * dh), tdt)
+        vd = to_dev(v[:, t0:t1].reshape(B * Tn, Hkv * dh), tdt)
+        bd = to_dev(bits[:, t0:t1].reshape(-1), torch.uint8)
+        sid = torch.tensor([2, 0, 1], dtype=torch.int32, device=DEV)
+        ws = tr.workspace(c, tr.OP_KV_APPEND, B, Tn)
+        tr.kv_append(c, cache, B, Tn, kd, vd, bd, ws, seq_ids=sid)
+    torch.cuda.synchronize()
+    assert cache.status() == 0
+    seq_of_row = [2, 0, 1]
+    np.testing.assert_array_equal(npy(cache.seq_len())[[2, 0, 1, 3]], [T1 + T2] * 3 + [0])
+    for b in range(B):
+        s = seq_of_row[b]
+        for bi, nb in enumerate(quant.BITS):
+            toks = np.flatnonzero(bits[b] == bi)
+            assert int(npy(cache.pool_len())[s, bi]) == len(toks)
+            if len(toks) == 0:
+                continue
+            ko, vo, ks, vs, pos = export_pool(c, cache, s, bi, len(toks), act, Hkv, dh, G)
+            np.testing.assert_array_equal(npy(pos), toks)
+            for src, out, sz in ((k, ko, ks), (v, vo, vs)):
+                x = src[b, toks]
+                if nb == 16:
+                    np.testing.assert_array_equal(npy(out).astype(np.float32), x)
+                    continue
+                codes, s16, z16 = quant.quantize(x, nb, G)
+                np.testing.assert_array_equal(npy(out), codes)
+                szn = npy(sz)
+                np.testing.assert_array_equal(_f16(szn[..., 0]).view(np.uint16), s16.view(np.uint16))
+                np.testing.assert_array_equal(_f16(szn[..., 1]).view(np.uint16), z16.view(np.uint16))
+
+
+def _host_decode(raw: np.ndarray, desc, c, s, bi, g, slot, ch, isv, act):
+    """Independent reading of the documented physical layout (include/triroute.h)."""
+    dh, Hkv = c.head_dim, c.n_kv_heads
+    bp = [2, 4, 8, 16 if act == "bf16" else 32][bi]
+    TS = 4096 // dh
+    tile, st = divmod(slot, TS)
+    base = desc.off_pool[bi] + ((s * Hkv + g) * desc.n_tiles + tile) * desc.tile_bytes[bi]
+    if isv:
+        base += 512 * bp
+        f = (st // 32) * (dh // 16) + ch // 16
+        lane = ((st % 32) // 8) * 16 + ch % 16
+        j = st % 8
+    else:
+        f = (st // 16) * (dh // 32) + ch // 32
+        lane = ((ch % 32) // 8) * 16 + st % 16
+        j = ch % 8
+    q = f * 8 + j
+    rec = base + lane * 8 * bp
+    if bp == 32:
+        return int(raw[rec + 4 * q: rec + 4 * q + 4].view(np.uint32)[0])
+    per = 16 // bp
+    word, bitpos = (q // 2) // per, ((q // 2) % per) * bp + (q % 2) * 16
+    w = int(raw[rec + 4 * word: rec + 4 * word + 4].view(np.uint32)[0])
+    return (w >> bitpos) & ((1 << bp) - 1)
+
+
+@pytest.mark.parametrize("act,dh,G,Hkv", KV_SHAPES[:3])
+def test_kv_physical_layout_matches_header(act, dh, G, Hkv):
+    c = kv_cfg(act, dh, G, Hkv)
+    n = 70
+    k, v = gen.kv_block(12, n, Hkv, dh, act)
+    bits = gen.stream(12, "kvbits").integers(0, 4, n).astype(np.uint8)
+    cache = tr.KVCache(c, 1, 128)
+    tdt = torch_act(act)
+    tr.kv_append(c, cache, 1, n, to_dev(k.reshape(n, -1), tdt), to_dev(v.reshape(n, -1), tdt),
+                 to_dev(bits, torch.uint8), tr.workspace(c, tr.OP_KV_APPEND, 1, n))
+    torch.cuda.synchronize()
+    raw = cache.buf.cpu().numpy()
+    rng = np.random.default_rng(0)
+    for bi in range(4):
+        m = int((bits == bi).sum())
+        if m == 0:
+            continue
+        ko, vo, _, _, _ = export_pool(c, cache, 0, bi, m, act, Hkv, dh, G)
+        kon, von = npy(ko), npy(vo)
+        if bi == 3:
+            kon = kon.astype(np.float32).view(np.uint32) >> (16 if act == "bf16" else 0)
+            von = von.astype(np.float32).view(np.uint32) >> (16 if act == "bf16" else 0)
+        for _ in range(40):
+            slot, g, ch = int(rng.integers(m)), int(rng.integers(Hkv)), int(rng.integers(dh))
+            assert _host_decode(raw, cache.desc, c, 0, bi, g, slot, ch, False, act) == kon[slot, g, ch]
+            assert _host_decode(raw, cache.desc, c, 0, bi, g, slot, ch, True, act) == von[slot, g, ch]
+
+
+def test_kv_capacity_overflow_sets_flag_and_drops_row():
+    c = kv_cfg("bf16", 64, 64, 1)
+    cache = tr.KVCache(c, 2, 16)
+    k, v = gen.kv_block(13, 2 * 10, 1, 64, "bf16")
+    kd, vd = to_dev(k.reshape(20, -1), torch.bfloat16), to_dev(v.reshape(20, -1), torch.bfloat16)
+    bd = torch.zeros(20, dtype=torch.uint8, device=DEV)
+    ws = tr.workspace(c, tr.OP_KV_APPEND, 2, 10)
+    tr.kv_append(c, cache, 2, 10, kd, vd, bd, ws)
+    assert cache.status() == 0
+    tr.kv_append(c, cache, 2, 10, kd, vd, bd, ws)     # 20 > 16: both rows dropped
+    assert cache.status() == tr.CACHE_OVERFLOW
+    np.testing.assert_array_equal(npy(cache.seq_len()), [10, 10])
+    with pytest.raises(tr.TrirouteError):              # host-visible: T > capacity
+        tr.kv_append(c, cache, 1, 17, kd, vd, bd, tr.workspace(c, tr.OP_KV_APPEND, 1, 17))
+
+
+# ------------------------------------------------------------------- QKV
+@pytest.mark.parametrize("name", ["tiny_f32_prefill", "160m_bf16_prefill", "1p3b_bf16_prefill"])
+def test_qkv_rope(name):
+    L = gen.make_layer(name, with_moe=False)
+    cfg = L["cfg"]
+    act = cfg["act"]
+    B, T = 2, 133                                       # ragged against 64/128-row tiles
+    x = L["x"][:B * T]
+    D = DeviceLayer(L, moe=False)
+    c = D.cfg
+    H, Hkv, dh = cfg["H"], cfg["Hkv"], cfg["dh"]
+    pos0 = np.array([0, 30000], np.int32)               # long positions stress RoPE angles
+    n1 = to_dev(x, D.act)
+    q = torch.empty(B * T, H * dh, dtype=D.act, device=DEV)
+    k = torch.empty(B * T, Hkv * dh, dtype=D.act, device=DEV)
+    v = torch.empty_like(k)
+    tr.qkv(c, B, T, n1, D.dw, q, k, v, pos0=to_dev(pos0, torch.int32))
+    torch.cuda.synchronize()
+    pos = np.concatenate([p + np.arange(T) for p in pos0])
+    qo, ko, vo = oracle.qkv(np.asarray(x, np.float64), L, pos)
+    assert_close(npy(q), qo.reshape(B * T, -1), act, "q")
+    assert_close(npy(k), ko.reshape(B * T, -1), act, "k")
+    assert_close(npy(v), vo.reshape(B * T, -1), act, "v")
+
+
+# ------------------------------------------------------------- attention
+def _fill_cache(c, cache, kk, vv, bits, act, seq_ids=None):
+    B, T = bits.shape
+    tdt = torch_act(act)
+    tr.kv_append(c, cache, B, T, to_dev(kk.reshape(B * T, -1), tdt),
+                 to_dev(vv.reshape(B * T, -1), tdt), to_dev(bits.reshape(-1), torch.uint8),
+                 tr.workspace(c, tr.OP_KV_APPEND, B, T),
+                 seq_ids=None if seq_ids is None else to_dev(np.asarray(seq_ids, np.int32), torch.int32))
+
+
+ATTN_SHAPES = [  # (act, H, Hkv, dh, G, w, B, T)
+    ("f32", 4, 1, 64, 32, 32, 1, 128),
+    ("bf16", 12, 3, 64, 64, 48, 2, 150),
+    ("bf16", 16, 4, 128, 64, 40, 2, 97),
+]
+
+
+@pytest.mark.parametrize("act,H,Hkv,dh,G,w,B,T", ATTN_SHAPES)
+def test_attention_prefill(act, H, Hkv, dh, G, w, B, T):
+    c = tr.make_cfg(256, H, Hkv, dh, w, 4, 1, 512, G, act)
+    std = 0.6
+    kk, vv = gen.kv_block(21, B * T, Hkv, dh, act, std)
+    kk, vv = kk.reshape(B, T, Hkv, dh), vv.reshape(B, T, Hkv, dh)
+    qq = gen.to_act(gen.normal(21, "attn_q", (B, T, H, dh), std), act)
+    rng = gen.stream(21, "attn_modes")
+    modes = rng.choice(3, size=(B * T, H), p=[0.25, 0.45, 0.30]).astype(np.uint8)
+    bits = rng.integers(0, 4, (B, T)).astype(np.uint8)
+    cache = tr.KVCache(c, B, T + 8)
+    _fill_cache(c, cache, kk, vv, bits, act)
+    cm = oracle.compact(modes, np.zeros((B * T, 1), np.int32), B, T, H, 4, 1)
+    cmp = tr.CompactionBuffers(c, B, T)
+    cmp.attn_cnt.copy_(to_dev(cm["attn_cnt"], torch.int32))
+    cmp.attn_idx.copy_(to_dev(np.where(cm["attn_idx"] < 0, 0, cm["attn_idx"]).reshape(-1), torch.int32))
+    o = torch.empty(B * T, H * dh, dtype=torch_act(act), device=DEV)
+    qd = to_dev(qq.reshape(B * T, H * dh), torch_act(act))
+    md = to_dev(modes, torch.uint8)
+    tr.attn_prefill(c, B, T, qd, cache, md, cmp.struct, o,
+                    ws=tr.workspace(c, tr.OP_ATTN_PREFILL, B, T))
+    torch.cuda.synchronize()
+    og = npy(o).reshape(B, T, H, dh)
+    cfgd = dict(G=G)
+    for b in range(B):
+        khat, vhat, _ = oracle.layer.store_kv(kk[b], vv[b], bits[b], cfgd)
+        ref = oracle.attention_seq(np.asarray(qq[b], np.float64), np.arange(T), khat, vhat,
+                                   modes[b * T:(b + 1) * T], w)
+        assert_close(og[b], ref, act, f"o[b={b}]")
+
+
+@pytest.mark.parametrize("act,H,Hkv,dh,G,w,ctx", [
+    ("f32", 4, 1, 64, 32, 32, 300),
+    ("bf16", 16, 4, 64, 64, 256, 1500),
+    ("bf16", 16, 4, 128, 64, 100, 2100),
+])
+def test_attention_decode(act, H, Hkv, dh, G, w, ctx):
+    B = 5
+    c = tr.make_cfg(256, H, Hkv, dh, w, 4, 1, 512, G, act)
+    kk, vv = gen.kv_block(22, B * (ctx + 1), Hkv, dh, act, 0.8)
+    kk, vv = kk.reshape(B, ctx + 1, Hkv, dh), vv.reshape(B, ctx + 1, Hkv, dh)
+    rng = gen.stream(22, "dec")
+    bits = rng.integers(0, 4, (B, ctx + 1)).astype(np.uint8)
+    modes = rng.choice(3, size=(B, H), p=[0.2, 0.4, 0.4]).astype(np.uint8)
+    modes[0] = 0                                          # a sequence whose heads all skip
+    modes[1] = 1                                          # all local
+    qq = gen.to_act(gen.normal(22, "dec_q", (B, H, dh), 0.8), act)
+    cache = tr.KVCache(c, B, ctx + 4)
+    # context in two appends (ragged), then the new token
+    _fill_cache(c, cache, kk[:, :ctx // 2], vv[:, :ctx // 2], bits[:, :ctx // 2], act)
+    _fill_cache(c, cache, kk[:, ctx // 2:ctx], vv[:, ctx // 2:ctx], bits[:, ctx // 2:ctx], act)
+    _fill_cache(c, cache, kk[:, ctx:], vv[:, ctx:], bits[:, ctx:], act)
+    o = torch.empty(B, H * dh, dtype=torch_act(act), device=DEV)
+    tr.attn_decode(c, B, to_dev(qq.reshape(B, -1), torch_act(act)), cache,
+                   to_dev(modes, torch.uint8), o, ws=tr.workspace(c, tr.OP_ATTN_DECODE, B, 1))
+    torch.cuda.synchronize()
+    og = npy(o).reshape(B, H, dh)
+    cfgd = dict(G=G)
+    for b in range(B):
+        khat, vhat, _ = oracle.layer.store_kv(kk[b], vv[b], bits[b], cfgd)
+        ref = oracle.attention_seq(np.asarray(qq[b:b + 1], np.float64), np.array([ctx]), khat,
+                                   vhat, modes[b:b + 1], w)[0]
+        assert_close(og[b], ref, act, f"o[b={b}]")
+    assert not og[0].any()
+
+
+# ------------------------------------------------------------ O-proj, MoE
+@pytest.mark.parametrize("name,n_tok", [("tiny_f32_prefill", 128), ("160m_bf16_prefill", 301),
+                                        ("1p3b_bf16_decode", 32)])
+def test_oproj_and_moe(name, n_tok):
+    L = gen.make_layer(name)
+    cfg = L["cfg"]
+    act, H, dh, d, E, k = cfg["act"], cfg["H"], cfg["dh"], cfg["d"], cfg["E"], cfg["k"]
+    D = DeviceLayer(L)
+    c = D.cfg
+    x = L["x"][:n_tok]
+    o = gen.to_act(gen.normal(31, "o_in", (n_tok, H * dh), 0.5), act)
+    xt = torch.empty(n_tok, d, dtype=D.act, device=DEV)
+    tr.oproj(c, n_tok, to_dev(x, D.act), to_dev(o, D.act), D.dw, xt)
+    torch.cuda.synchronize()
+    ref_xt = oracle.oproj(x, np.asarray(o, np.float64), L["Wo"])
+    assert_close(npy(xt), ref_xt, act, "xt")
+    # experts on a generator-made xt with decisions from random logits
+    xt_in = gen.to_act(gen.normal(32, "xt_in", (n_tok, d)), act)
+    ze = gen.normal(32, "ze", (n_tok, E + 1), 1.5).astype(np.float64)
+    _, _, eidx, egate = oracle.decide(np.zeros((n_tok, 1, 3)), ze, np.zeros((n_tok, 4)), k)
+    cm = oracle.compact(np.zeros((n_tok, 1), np.uint8), eidx, n_tok, 1, 1, E, k)
+    cmp = tr.CompactionBuffers(c, n_tok, 1)
+    cmp.exp_cnt.copy_(to_dev(cm["exp_cnt"], torch.int32))
+    cmp.exp_off.copy_(to_dev(cm["exp_off"], torch.int32))
+    cmp.exp_rows[:len(cm["exp_rows"])].copy_(to_dev(cm["exp_rows"], torch.int32))
+    xo = torch.empty(n_tok, d, dtype=D.act, device=DEV)
+    tr.moe(c, n_tok, to_dev(xt_in, D.act), D.dw, D.mw, to_dev(eidx, torch.int32),
+           to_dev(egate.astype(np.float32), torch.float32), cmp.struct, xo,
+           tr.workspace(c, tr.OP_MOE, n_tok, 1))
+    torch.cuda.synchronize()
+    ref, _, _ = oracle.moe(np.asarray(xt_in, np.float64), L, eidx, egate.astype(np.float32))
+    assert_close(npy(xo), ref, act, "x_out")
+    null_only = np.all(eidx == 0, axis=1)
+    np.testing.assert_array_equal(npy(xo)[null_only], xt_in[null_only])

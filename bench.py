@@ -1,0 +1,282 @@
+"""Benchmark of the TriRoute routed-layer forward on one MI355X.
+
+A step is one full routed-layer prefill (router, compaction, QKV + RoPE,
+KV quantize/append, attention, O-proj, second norm, expert grouped GEMM,
+combine) of the 160M-class workload: batch 8 x 2048 tokens, d 768, 12 x 64
+heads (3 kv heads), window 128, 8 SwiGLU experts (d_ff 2048) + null, top-2,
+KV group 64, bf16, seeded synthetic inputs and random-init weights.  Inputs
+are resident in HBM before timing; every step writes a fresh cache; the
+L2 / Infinity Cache is flushed (1 GiB write) before each timed step.
+
+Also reported: the MoE sublayer's achieved bf16 MFMA rate (roofline), the
+410M-class decode step (64 sequences x 8192 context) and its decode
+attention's achieved HBM bandwidth, and the CPU oracle timed on a bounded
+sample on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFLOPS = 2516.6  # MI355X dense bf16 MFMA, TFLOP/s (256 CU x 2.4 GHz x 4096)
+
+PREFILL = "160m_bf16_prefill"
+DECODE = "410m_bf16_decode"
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-decode", action="store_true")
+    return p.parse_args()
+
+
+def events(torch):
+    return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the routed layer is "
+              "measured on a single MI355X in this build", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import gen
+    import paper_2607_06601_amd as tr
+    from paper_2607_06601_amd.device import DeviceLayer, to_dev
+
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    tr.lib()
+    dev = "cuda"
+    stream = torch.cuda.current_stream()
+
+    # ------------------------------------------------------------ prefill
+    L = gen.make_layer(PREFILL, 1)
+    cfg = L["cfg"]
+    B, T, d, H, dh, E, k, dff = (cfg[x] for x in ("B", "T", "d", "H", "dh", "E", "k", "d_ff"))
+    N = B * T
+    D = DeviceLayer(L)
+    c = D.cfg
+    ws = tr.workspace(c, tr.OP_LAYER_PREFILL, B, T)
+    xo = torch.empty(N, d, dtype=D.act, device=dev)
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    caches = [tr.KVCache(c, B, T) for _ in range(args.steps)]
+    warm = tr.KVCache(c, B, T)
+    eidx_t = torch.empty(N, k, dtype=torch.int32, device=dev)
+    egate_t = torch.empty(N, k, dtype=torch.float32, device=dev)
+    xt_t = torch.empty(N, d, dtype=D.act, device=dev)
+    taps = tr.Taps(eidx=eidx_t.data_ptr(), egate=egate_t.data_ptr(), xt=xt_t.data_ptr())
+    for _ in range(args.warmup):
+        warm.reset_seq(0)
+        for s in range(B):
+            warm.reset_seq(s)
+        tr.layer_prefill(c, B, T, D.x, D.psi, D.rw, D.dw, D.mw, warm, xo, ws, taps=taps)
+    torch.cuda.synchronize()
+    times = []
+    t_wall0 = time.perf_counter()
+    for i in range(args.steps):
+        flush.fill_(i & 0xFF)
+        e0, e1 = events(torch)
+        e0.record(stream)
+        tr.layer_prefill(c, B, T, D.x, D.psi, D.rw, D.dw, D.mw, caches[i], xo, ws, taps=taps)
+        e1.record(stream)
+        times.append((e0, e1))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall0
+    step_ms = [a.elapsed_time(b) for a, b in times]
+    ms = float(np.mean(step_ms))
+    for cc in caches:
+        assert cc.status() == 0
+
+    # MoE sublayer alone on the same routed inputs: achieved MFMA rate
+    eidx_h = eidx_t.cpu().numpy()
+    n_real = int((eidx_h != 0).sum())
+    moe_flops = 6.0 * d * dff * n_real
+    cmp = tr.CompactionBuffers(c, B, T)
+    rw_ws = tr.workspace(c, tr.OP_ROUTER, B, T)
+    n1 = torch.empty(N, d, dtype=D.act, device=dev)
+    mode = torch.empty(N, H, dtype=torch.uint8, device=dev)
+    bit = torch.empty(N, dtype=torch.uint8, device=dev)
+    tr.router(c, B, T, D.x, D.psi, D.rw, n1, mode, bit, eidx_t, egate_t, cmp.struct, rw_ws)
+    moe_ws = tr.workspace(c, tr.OP_MOE, N, 1)
+    for _ in range(3):
+        tr.moe(c, N, xt_t, D.dw, D.mw, eidx_t, egate_t, cmp.struct, xo, moe_ws)
+    moe_ms = []
+    for i in range(args.steps):
+        flush.fill_(i & 0xFF)
+        e0, e1 = events(torch)
+        e0.record(stream)
+        tr.moe(c, N, xt_t, D.dw, D.mw, eidx_t, egate_t, cmp.struct, xo, moe_ws)
+        e1.record(stream)
+        moe_ms.append((e0, e1))
+    torch.cuda.synchronize()
+    moe_avg = float(np.mean([a.elapsed_time(b) for a, b in moe_ms]))
+    moe_tflops = moe_flops / (moe_avg * 1e-3) / 1e12
+    roofline = {"kernel": "triroute_moe (rmsnorm2, grouped GEMM gate/up + SwiGLU, grouped GEMM "
+                          "down, combine)",
+                "bound": "mfma", "achieved": round(moe_tflops, 2),
+                "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(moe_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                "algorithmic": f"6*d*d_ff FLOP x {n_real} real assignments = "
+                               f"{moe_flops / 1e9:.1f} GFLOP per launch",
+                "avg_ms": round(moe_avg, 4)}
+
+    out = {
+        "metric": "routed-layer tokens/s (prefill, decode); decode-attn HBM GB/s; MoE MFMA util",
+        "value": round(N / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded generator, random-init weights)",
+        "config": {"workload": "160M-class TriRoute layer prefill: batch 8 x seq 2048, d 768, "
+                               "12x64 heads (3 kv), window 128, 8 SwiGLU experts d_ff 2048 + "
+                               "null, top-2, KV group 64, bf16",
+                   "global_batch": B, "seq_len": T, "parallelism": "single GPU"},
+        "roofline": roofline,
+        "timing": {"per_step_ms_min": round(min(step_ms), 4),
+                   "per_step_ms_max": round(max(step_ms), 4),
+                   "wall_s_timed_loop": round(wall, 3), "cache_flush_per_step": "1 GiB write"},
+    }
+
+    # ------------------------------------------------------------- decode
+    if not args.no_decode:
+        out["decode"] = bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush)
+
+    # --------------------------------------------------------- CPU oracle
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(np)
+    print(json.dumps(out), flush=True)
+
+
+def decode_attn_bytes(cfg, mode, bits_per_seq):
+    """Algorithmic bytes the routed decode attention must read: per (sequence,
+    kv head), the union of the key ranges its query heads need (full -> all
+    P+1 keys, local -> last w, skip -> none) x packed K+V bytes incl. fp16
+    scale/zero."""
+    import numpy as np
+    H, Hkv, dh, G, w = cfg["H"], cfg["Hkv"], cfg["dh"], cfg["G"], cfg["w"]
+    grp = H // Hkv
+    per_tok = np.array([2 * dh * b / 8 + (2 * (dh // G) * 4 if b < 16 else 0)
+                        for b in (2, 4, 8, 16)])
+    total = 0.0
+    for s, bits in enumerate(bits_per_seq):
+        P1 = len(bits)
+        full_b = per_tok[bits].sum()
+        loc_b = per_tok[bits[max(0, P1 - w):]].sum()
+        for g in range(Hkv):
+            m = mode[s, g * grp:(g + 1) * grp].max()
+            total += full_b if m == 2 else loc_b if m == 1 else 0.0
+    return total
+
+
+def bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush):
+    L = gen.make_layer(DECODE)
+    cfg = L["cfg"]
+    B, ctx, d, H, k = cfg["B"], cfg["ctx"], cfg["d"], cfg["H"], cfg["k"]
+    D = DeviceLayer(L)
+    c = D.cfg
+    dev = "cuda"
+    stream = torch.cuda.current_stream()
+    cap = ctx + args.warmup + args.steps + 1
+    cache = tr.KVCache(c, B, cap)
+    ws_app = tr.workspace(c, tr.OP_KV_APPEND, 1, ctx)
+    bits_all = []
+    for s in range(B):
+        kk, vv = gen.context_kv(cfg, s)
+        bits = gen.context_bits(cfg, s)
+        bits_all.append(bits)
+        tr.kv_append(c, cache, 1, ctx, to_dev(kk.reshape(ctx, -1), D.act),
+                     to_dev(vv.reshape(ctx, -1), D.act), to_dev(bits, torch.uint8), ws_app,
+                     seq_ids=torch.tensor([s], dtype=torch.int32, device=dev))
+    torch.cuda.synchronize()
+    ws = tr.workspace(c, tr.OP_LAYER_DECODE, B, 1)
+    xo = torch.empty(B, d, dtype=D.act, device=dev)
+    mode_t = torch.empty(B, H, dtype=torch.uint8, device=dev)
+    bit_t = torch.empty(B, dtype=torch.uint8, device=dev)
+    q_t = torch.empty(B, H * cfg["dh"], dtype=D.act, device=dev)
+    taps = tr.Taps(mode=mode_t.data_ptr(), bit=bit_t.data_ptr(), q=q_t.data_ptr())
+    for _ in range(args.warmup):
+        tr.layer_decode(c, B, D.x, D.psi, D.rw, D.dw, D.mw, cache, xo, ws, taps=taps)
+    times = []
+    for i in range(args.steps):
+        flush.fill_(i & 0xFF)
+        e0, e1 = events(torch)
+        e0.record(stream)
+        tr.layer_decode(c, B, D.x, D.psi, D.rw, D.dw, D.mw, cache, xo, ws, taps=taps)
+        e1.record(stream)
+        times.append((e0, e1))
+    torch.cuda.synchronize()
+    assert cache.status() == 0
+    step_ms = float(np.mean([a.elapsed_time(b) for a, b in times]))
+    # decode attention alone over the cache as it now stands
+    mode = mode_t.cpu().numpy()
+    seq_len = cache.seq_len().cpu().numpy()
+    # bit widths of every cached token, in position order, per sequence
+    extra = bit_t.cpu().numpy()
+    bits_now = [np.concatenate([bits_all[s], np.full(seq_len[s] - ctx, extra[s], np.uint8)])
+                for s in range(B)]
+    nbytes = decode_attn_bytes(cfg, mode, bits_now)
+    o = torch.empty(B, H * cfg["dh"], dtype=D.act, device=dev)
+    aws = tr.workspace(c, tr.OP_ATTN_DECODE, B, 1)
+    for _ in range(3):
+        tr.attn_decode(c, B, q_t, cache, mode_t, o, aws)
+    at = []
+    for i in range(args.steps):
+        flush.fill_(i & 0xFF)
+        e0, e1 = events(torch)
+        e0.record(stream)
+        tr.attn_decode(c, B, q_t, cache, mode_t, o, aws)
+        e1.record(stream)
+        at.append((e0, e1))
+    torch.cuda.synchronize()
+    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in at]))
+    gbs = nbytes / (attn_ms * 1e-3) / 1e9
+    return {"workload": "410M-class decode step: 64 sequences x 1 new token, context 8192 "
+                        "(bits 20/40/30/10 % for 2/4/8/16), d 1024, 16x64 heads (4 kv), "
+                        "window 256, 8 SwiGLU experts d_ff 2816 + null, top-2",
+            "tokens_per_s": round(B / (step_ms * 1e-3), 1), "ms_per_step": round(step_ms, 4),
+            "attn": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                     "algorithmic_bytes": int(nbytes), "avg_ms": round(attn_ms, 4),
+                     "traffic": None}}
+
+
+def cpu_baseline(np):
+    """The CPU oracle (fp64 numpy) on one of the 8 sequences of the prefill
+    workload (2048 tokens), on the host cores."""
+    import gen
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    L = gen.make_layer(PREFILL, 1)
+    T = L["cfg"]["T"]
+    L["cfg"]["B"] = 1
+    L["x"], L["psi"] = L["x"][:T], L["psi"][:T]
+    t0 = time.perf_counter()
+    oracle.layer_prefill(L)
+    dt = time.perf_counter() - t0
+    return {"value": round(T / dt, 2), "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"full routed-layer prefill of 1 of the 8 sequences ({T} tokens), "
+                      f"{dt:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -206,7 +206,8 @@ int triroute_kv_cache_bytes(const triroute_cfg *cfg, int n_seq, int capacity, si
  * aligned) and clears it on `stream` (all sequences empty). */
 int triroute_kv_cache_init(const triroute_cfg *cfg, triroute_kv_cache *cache, void *base,
                            size_t bytes, int n_seq, int capacity, triroute_stream_t stream);
-/* Empties sequence `seq` (clears its pools) on `stream`. */
+/* Empties sequence `seq` (its length and pool lengths) on `stream`; later
+ * appends overwrite every bit of the slots they take. */
 int triroute_kv_reset_seq(const triroute_cfg *cfg, const triroute_kv_cache *cache, int seq,
                           triroute_stream_t stream);
 /* Synchronises `stream` and copies the cache status word to *status (host). */

@@ -25,6 +25,13 @@ Readings where the paper is silent (each listed in the design notes):
   exact-erf GELU; rotate-half RoPE with theta = 10000 on the cached (rotated)
   keys; every attention read, including a token's own key, goes through the
   quantized cache (append, then attend).
+
+Precision: the paper's models run in bf16 (Sec. 4 Training).  Read as the
+usual mixed-precision contract, every activation tensor handed from one
+operator to the next is held in the activation dtype (n1 into the
+projections, q/k/v, o, x~, n2 and the SwiGLU product H), while each operator
+accumulates in higher precision (here fp64).  ``act = "f64"`` keeps
+everything in fp64 (used by the library-reduction pins).
 """
 from __future__ import annotations
 
@@ -82,7 +89,8 @@ def rope(x, pos, theta=ROPE_THETA):
 
 
 def to_native(a, act):
-    """The activation dtype a stored K/V value keeps ("native precision")."""
+    """Round to the activation dtype: the precision of every tensor handed
+    between operators, and the "native precision" of a 16-bit cache entry."""
     t = torch.from_numpy(np.ascontiguousarray(a, np.float64))
     if act == "bf16":
         return t.to(torch.bfloat16).to(torch.float32).numpy()
@@ -201,14 +209,16 @@ def compact(mode, eidx, B, T, H, E, k):
 
 # ------------------------------------------------------------ attention
 def qkv(n1, L, pos):
-    """q = Wq n1, k = Wk n1, v = Wv n1 per head, RoPE on q and k at ``pos``."""
+    """q = Wq n1, k = Wk n1, v = Wv n1 per head, RoPE on q and k at ``pos``;
+    outputs held in the activation dtype."""
     cfg = L["cfg"]
-    H, Hkv, dh = cfg["H"], cfg["Hkv"], cfg["dh"]
+    H, Hkv, dh, act = cfg["H"], cfg["Hkv"], cfg["dh"], cfg["act"]
     n = len(n1)
     q = (n1 @ np.asarray(L["Wq"], np.float64).T).reshape(n, H, dh)
     k = (n1 @ np.asarray(L["Wk"], np.float64).T).reshape(n, Hkv, dh)
     v = (n1 @ np.asarray(L["Wv"], np.float64).T).reshape(n, Hkv, dh)
-    return rope(q, pos), rope(k, pos), v
+    return (to_native(rope(q, pos), act), to_native(rope(k, pos), act),
+            to_native(v, act))
 
 
 def store_kv(k, v, bit, cfg):
@@ -278,7 +288,8 @@ def moe(xt, L, eidx, egate):
     with SwiGLU experts f_j(u) = W_down,j (silu(W_gate,j u) * W_up,j u).
     The null expert contributes nothing (Sec. 3.2 (B))."""
     cfg = L["cfg"]
-    n2 = rmsnorm(xt, L["g2"])
+    act = cfg["act"]
+    n2 = to_native(rmsnorm(xt, L["g2"]), act)
     y = np.zeros_like(n2)
     k = eidx.shape[1]
     for e in range(1, cfg["E"] + 1):
@@ -290,7 +301,7 @@ def moe(xt, L, eidx, egate):
         Wu = np.asarray(L["Wu"][e - 1], np.float64)
         Wd = np.asarray(L["Wd"][e - 1], np.float64)
         u = n2[rows]
-        hmid = silu(u @ Wg.T) * (u @ Wu.T)
+        hmid = to_native(silu(u @ Wg.T) * (u @ Wu.T), act)
         np.add.at(y, rows, egate[rows, slots][:, None] * (hmid @ Wd.T))
     del k
     return xt + y, n2, y
@@ -315,11 +326,11 @@ def layer_prefill(L, rows=None):
     seqs = sorted(set(int(r) // T for r in rows))
     q_all, k_all, v_all, o_rows = {}, {}, {}, {}
     stored = {}
+    n1a = to_native(n1, act)
     for b in seqs:
         sl = slice(b * T, (b + 1) * T)
         pos = np.arange(T)
-        q, k, v = qkv(n1[sl], L, pos)
-        kn, vn = to_native(k, act), to_native(v, act)
+        q, kn, vn = qkv(n1a[sl], L, pos)
         khat, vhat, st = store_kv(kn, vn, bit[sl], cfg)
         stored[b] = st
         want = [int(r) - b * T for r in rows if int(r) // T == b]
@@ -328,8 +339,8 @@ def layer_prefill(L, rows=None):
         for ti, t in enumerate(want):
             o_rows[b * T + t] = o[ti]
         q_all[b], k_all[b], v_all[b] = q, kn, vn
-    o = np.stack([o_rows[int(r)] for r in rows])
-    xt = oproj(L["x"][rows], o, L["Wo"])
+    o = to_native(np.stack([o_rows[int(r)] for r in rows]), act)
+    xt = to_native(oproj(L["x"][rows], o, L["Wo"]), act)
     xout, n2, y = moe(xt, L, eidx[rows], egate[rows])
     return dict(rows=rows, n1=n1, za=za, ze=ze, zb=zb, mode=mode, bit=bit,
                 eidx=eidx, egate=egate, cmp=cmp, q=q_all, k=k_all, v=v_all,
@@ -359,8 +370,7 @@ def layer_decode(L, seqs=None):
     seqs = list(range(B)) if seqs is None else sorted(set(int(s) for s in seqs))
     rows = np.asarray(seqs)
     pos = np.full(len(rows), ctx)
-    q, k, v = qkv(n1[rows], L, pos)
-    kn, vn = to_native(k, act), to_native(v, act)
+    q, kn, vn = qkv(to_native(n1[rows], act), L, pos)
     o = np.zeros((len(rows), H, cfg["dh"]))
     new_stored = {}
     for ri, s in enumerate(seqs):
@@ -372,7 +382,8 @@ def layer_decode(L, seqs=None):
         o[ri] = attention_seq(q[ri:ri + 1], np.array([ctx]), khat, vhat,
                               mode[s:s + 1], w)[0]
         del khat, vhat
-    xt = oproj(L["x"][rows], o, L["Wo"])
+    o = to_native(o, act)
+    xt = to_native(oproj(L["x"][rows], o, L["Wo"]), act)
     xout, n2, y = moe(xt, L, eidx[rows], egate[rows])
     return dict(rows=rows, n1=n1, za=za, ze=ze, zb=zb, mode=mode, bit=bit,
                 eidx=eidx, egate=egate, cmp=cmp, q=q, k=kn, v=vn,

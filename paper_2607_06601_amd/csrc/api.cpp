@@ -333,18 +333,12 @@ int triroute_kv_reset_seq(const triroute_cfg *cfg, const triroute_kv_cache *cach
   TRY(check_cfg(cfg));
   REQUIRE(cache && cache->base, TRIROUTE_E_INVALID, "cache is NULL");
   REQUIRE(seq >= 0 && seq < cache->n_seq, TRIROUTE_E_INVALID, "seq %d out of range", seq);
+  // Appends overwrite every bit a slot owns, so emptying a sequence only
+  // needs its lengths cleared.
   hipStream_t st = (hipStream_t)stream;
   uint8_t *b = (uint8_t *)cache->base;
   CHECK_HIP(tr::launch_fill_u32(b + cache->off_seq_len + 4 * size_t(seq), 1, 0u, st), "reset");
   CHECK_HIP(tr::launch_fill_u32(b + cache->off_pool_len + 16 * size_t(seq), 4, 0u, st), "reset");
-  CHECK_HIP(tr::launch_fill_u32(b + cache->off_pos + size_t(seq) * 16 * cache->capacity,
-                                int64_t(4) * cache->capacity, 0u, st),
-            "reset");
-  for (int bi = 0; bi < 4; ++bi) {
-    const size_t per_seq = size_t(cfg->n_kv_heads) * cache->n_tiles * cache->tile_bytes[bi];
-    CHECK_HIP(tr::launch_fill_u32(b + cache->off_pool[bi] + per_seq * seq, per_seq / 4, 0u, st),
-              "reset");
-  }
   return TRIROUTE_OK;
 }
 

@@ -154,7 +154,7 @@ __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int
       *(uint32_t *)(tp + (o * 16 + n) * (8 * bp) + word * 4) = val;
     }
   }
-  // ---- V: words are shared by neighbouring slots
+  // ---- V: words are shared by neighbouring slots (other slots' bits untouched)
   {
     uint8_t *vp = tp + cv.v_codes_off(bi);
     for (int r = 0; r < NR; ++r) {
@@ -164,8 +164,10 @@ __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int
       q_word(q, bp, wd, bt);
       uint8_t *addr = vp + ln * (8 * bp) + wd * 4;
       const uint32_t e = el[w][1][c];
-      if (bp <= 4)
+      if (bp <= 4) {  // clear this slot's bits, then set them: correct on a reused slot
+        atomicAnd((unsigned int *)addr, ~(((1u << bp) - 1u) << bt));
         atomicOr((unsigned int *)addr, e << bt);
+      }
       else if (bp == 8)
         addr[bt >> 3] = uint8_t(e);
       else if (bp == 16)

@@ -223,7 +223,7 @@ def test_qkv_rope(name):
     cfg = L["cfg"]
     act = cfg["act"]
     B, T = 2, 133                                       # ragged against 64/128-row tiles
-    x = L["x"][:B * T]
+    x = gen.to_act(gen.normal(41, "qkv_in", (B * T, cfg["d"])), act)
     D = DeviceLayer(L, moe=False)
     c = D.cfg
     H, Hkv, dh = cfg["H"], cfg["Hkv"], cfg["dh"]
@@ -358,3 +358,31 @@ def test_oproj_and_moe(name, n_tok):
     assert_close(npy(xo), ref, act, "x_out")
     null_only = np.all(eidx == 0, axis=1)
     np.testing.assert_array_equal(npy(xo)[null_only], xt_in[null_only])
+
+
+def test_kv_reset_and_reuse_overwrites_slots():
+    """After reset_seq, new appends land on the same slots and fully replace
+    the previous contents (sub-byte V words included)."""
+    act, dh, G, Hkv = "bf16", 64, 64, 2
+    c = kv_cfg(act, dh, G, Hkv)
+    n = 90
+    cache = tr.KVCache(c, 1, 128)
+    bits = gen.stream(14, "kvbits").integers(0, 4, n).astype(np.uint8)
+    for rep, seed in enumerate((14, 15)):
+        if rep:
+            cache.reset_seq(0)
+        k, v = gen.kv_block(seed, n, Hkv, dh, act)
+        tr.kv_append(c, cache, 1, n, to_dev(k.reshape(n, -1), torch.bfloat16),
+                     to_dev(v.reshape(n, -1), torch.bfloat16), to_dev(bits, torch.uint8),
+                     tr.workspace(c, tr.OP_KV_APPEND, 1, n))
+    torch.cuda.synchronize()
+    for bi, nb in enumerate(quant.BITS):
+        toks = np.flatnonzero(bits == bi)
+        if len(toks) == 0:
+            continue
+        ko, vo, _, _, _ = export_pool(c, cache, 0, bi, len(toks), act, Hkv, dh, G)
+        for src, out in ((k, ko), (v, vo)):
+            if nb == 16:
+                np.testing.assert_array_equal(npy(out).astype(np.float32), src[toks])
+            else:
+                np.testing.assert_array_equal(npy(out), quant.quantize(src[toks], nb, G)[0])

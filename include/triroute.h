@@ -144,7 +144,8 @@ typedef struct triroute_compaction {
  * native bf16 / fp32 store); record l holds 64 elements q = f*8 + j, eight
  * "fields" f of eight elements j:
  *   K: slot 16*(f / (dh/32)) + (l % 16), channel 32*(f % (dh/32)) + 8*(l / 16) + j
- *   V: slot 32*(f / (dh/16)) + 8*(l / 16) + j, channel 16*(f % (dh/16)) + (l % 16)
+ *   V: slot 32*(f / (dh/16)) + 16*(j / 4) + 4*(l / 16) + j % 4,
+ *      channel 16*(f % (dh/16)) + (l % 16)
  * Element q sits in 32-bit word (q/2) / (16/bp) at bit ((q/2) % (16/bp))*bp
  * + (q % 2)*16 for bp < 32 (one element per word for fp32).  Scale/zero
  * blocks are [TS slots][dh/G groups][2] fp16 (scale, zero). */

@@ -243,6 +243,25 @@ void layout_cache(const triroute_cfg &c, int n_seq, int capacity, triroute_kv_ca
   kc->total_bytes = off;
 }
 
+hipError_t run_attn_prefill(const triroute_cfg &c, const triroute_kv_cache &kc, int B, int T,
+                            const int32_t *seq_ids, const void *q, const triroute_compaction &cmp,
+                            void *o, hipStream_t st) {
+  const int64_t words = int64_t(B) * T * c.n_heads * c.head_dim * act_bytes(c) / 4;
+  hipError_t e = tr::launch_fill_u32(o, words, 0u, st);
+  if (e != hipSuccess) return e;
+  const tr::CacheView v = tr::make_view(c, kc);
+  return c.act == TRIROUTE_BF16 ? tr::launch_attn_mfma_prefill(c, v, B, T, seq_ids, q, cmp, o, st)
+                                : tr::launch_attn_valu_prefill(c, v, B, T, seq_ids, q, cmp, o, st);
+}
+
+hipError_t run_attn_decode(const triroute_cfg &c, const triroute_kv_cache &kc, int B,
+                           const int32_t *seq_ids, const void *q, const uint8_t *mode, void *o,
+                           float *part, hipStream_t st) {
+  const tr::CacheView v = tr::make_view(c, kc);
+  return c.act == TRIROUTE_BF16 ? tr::launch_attn_mfma_decode(c, v, B, seq_ids, q, mode, o, part, st)
+                                : tr::launch_attn_valu_decode(c, v, B, seq_ids, q, mode, o, st);
+}
+
 }  // namespace
 
 namespace tr {
@@ -431,11 +450,7 @@ int triroute_attn_prefill(const triroute_cfg *cfg, int B, int T, const int32_t *
   REQUIRE(q && mode && cmp && cmp->attn_cnt && cmp->attn_idx && o, TRIROUTE_E_INVALID,
           "NULL argument");
   TRY(check_ws(*cfg, TRIROUTE_OP_ATTN_PREFILL, B, T, ws, ws_bytes));
-  hipStream_t st = (hipStream_t)stream;
-  const int64_t words = int64_t(B) * T * cfg->n_heads * cfg->head_dim * act_bytes(*cfg) / 4;
-  CHECK_HIP(tr::launch_fill_u32(o, words, 0u, st), "o clear");
-  CHECK_HIP(tr::launch_attn_valu_prefill(*cfg, tr::make_view(*cfg, *cache), B, T, seq_ids, q, *cmp,
-                                         o, st),
+  CHECK_HIP(run_attn_prefill(*cfg, *cache, B, T, seq_ids, q, *cmp, o, (hipStream_t)stream),
             "attn_prefill launch");
   return TRIROUTE_OK;
 }
@@ -448,8 +463,9 @@ int triroute_attn_decode(const triroute_cfg *cfg, int B, const int32_t *seq_ids,
   TRY(check_cache(*cfg, cache, B, 1));
   REQUIRE(q && mode && o, TRIROUTE_E_INVALID, "NULL argument");
   TRY(check_ws(*cfg, TRIROUTE_OP_ATTN_DECODE, B, 1, ws, ws_bytes));
-  CHECK_HIP(tr::launch_attn_valu_decode(*cfg, tr::make_view(*cfg, *cache), B, seq_ids, q, mode, o,
-                                        (hipStream_t)stream),
+  Carve cv(ws);
+  float *part = carve_attn_decode(cv, *cfg, B);
+  CHECK_HIP(run_attn_decode(*cfg, *cache, B, seq_ids, q, mode, o, part, (hipStream_t)stream),
             "attn_decode launch");
   return TRIROUTE_OK;
 }
@@ -538,14 +554,13 @@ static int layer_impl(const triroute_cfg *cfg, int B, int T, bool decode, const 
               "kv_append launch");
   }
   if (decode) {
-    CHECK_HIP(tr::launch_attn_valu_decode(*cfg, tr::make_view(*cfg, *cache), B, seq_ids, L.q, L.mode,
-                                          L.o, st),
+    Carve sc(ws);
+    sc.used = scratch_at;
+    float *part = carve_attn_decode(sc, *cfg, B);
+    CHECK_HIP(run_attn_decode(*cfg, *cache, B, seq_ids, L.q, L.mode, L.o, part, st),
               "attn_decode launch");
   } else {
-    const int64_t words = int64_t(N) * cfg->n_heads * cfg->head_dim * act_bytes(*cfg) / 4;
-    CHECK_HIP(tr::launch_fill_u32(L.o, words, 0u, st), "o clear");
-    CHECK_HIP(tr::launch_attn_valu_prefill(*cfg, tr::make_view(*cfg, *cache), B, T, seq_ids, L.q,
-                                           L.cmp, L.o, st),
+    CHECK_HIP(run_attn_prefill(*cfg, *cache, B, T, seq_ids, L.q, L.cmp, L.o, st),
               "attn_prefill launch");
   }
   CHECK_HIP(tr::launch_oproj(*cfg, N, x, L.o, *dw, L.xt, st), "oproj launch");

@@ -1,0 +1,660 @@
+// Routed attention over the mixed-width cache on bf16 MFMA (gfx950).
+//
+// Paper Sec. 3.2 (A): a query head at position P reads kv head h / (H/Hkv):
+// skip -> 0, local -> keys [P - w + 1, P], full -> [0, P]; softmax over
+// q k^T / sqrt(dh) of the dequantized cache (Sec. 3.2 (C)), times v.
+//
+// One wave processes 32/64-slot tiles of one width pool at a time:
+//   S^T = K Q^T   v_mfma_f32_16x16x32_bf16, A = K codes of 16 slots (bf16 of
+//                 128 + code, or the code itself for 8-bit, or the stored bf16),
+//                 B = up to 16 query columns (GQA heads of one token in decode,
+//                 16 tokens of one head in prefill).  The dequantization is
+//                 algebraic: per group, s * (acc - off * sum q) + z * sum q.
+//   O += P' V     A = P' = fp16(p * s_v) straight from the S^T registers (the
+//                 cache stores V in the order that makes this a register
+//                 reuse), B = fp16 codes (v_mfma_f32_16x16x32_f16);
+//                 the z_v and offset terms are accumulated per query column
+//                 and added at the end.  The 16-bit pool multiplies bf16(p)
+//                 by the stored bf16 values.
+// Online softmax in the exp2 domain.  Decode splits each (sequence, kv head)
+// over KV chunks: 4 waves merge in LDS, a second kernel merges the chunks
+// with log-sum-exp.
+#include <limits.h>
+
+#include "kernels.hpp"
+
+namespace tr {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float LOG2E = 1.4426950408889634f;
+
+__device__ __forceinline__ bf16x8 as_op(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ f16x8 as_h(u32x4 v) { return __builtin_bit_cast(f16x8, v); }
+
+// V field of a quantized pool -> fp16 operand holding the code itself:
+// 0x6400 | code is fp16(1024 + code), and a packed fp16 subtraction of 1024
+// is exact.  (A large constant left in the operand would be summed over the
+// whole key range in the fp32 accumulator.)
+template <int BP>
+__device__ __forceinline__ f16x8 vfield_h(const uint32_t *w, int f) {
+  u32x4 r;
+  if constexpr (BP == 2) {
+    const uint32_t x = w[f >> 1] >> ((f & 1) * 8);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) r[p] = ((x >> (2 * p)) & 0x00030003u) | 0x64006400u;
+  } else if constexpr (BP == 4) {
+    const uint32_t x = w[f];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) r[p] = ((x >> (4 * p)) & 0x000F000Fu) | 0x64006400u;
+  } else {
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+      r[p] = ((w[2 * f + (p >> 1)] >> ((p & 1) * 8)) & 0x00FF00FFu) | 0x64006400u;
+  }
+  const f16x8 k1024 = {1024, 1024, 1024, 1024, 1024, 1024, 1024, 1024};
+  return as_h(r) - k1024;
+}
+
+// bf16 pair from two small integer codes held at bits 0 and 16 of x.
+__device__ __forceinline__ uint32_t pair_small(uint32_t x) { return x | 0x43004300u; }
+// exact bf16 pair of two 8-bit codes at bits 0..7 and 16..23
+__device__ __forceinline__ uint32_t pair_byte(uint32_t x) {
+  const float lo = float(x & 0xFFu), hi = float((x >> 16) & 0xFFu);
+  return (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
+}
+
+// Eight elements (field f) of a lane record -> MFMA operand.  Small codes
+// become bf16(128 + code) (the 128 is removed algebraically).
+template <int BP>
+__device__ __forceinline__ bf16x8 field_op(const uint32_t *w, int f) {
+  u32x4 r;
+  if constexpr (BP == 2) {
+    const uint32_t x = w[f >> 1] >> ((f & 1) * 8);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) r[p] = pair_small((x >> (2 * p)) & 0x00030003u);
+  } else if constexpr (BP == 4) {
+    const uint32_t x = w[f];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) r[p] = pair_small((x >> (4 * p)) & 0x000F000Fu);
+  } else if constexpr (BP == 8) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) r[p] = pair_byte((w[2 * f + (p >> 1)] >> ((p & 1) * 8)) & 0x00FF00FFu);
+  } else {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) r[p] = w[4 * f + p];
+  }
+  return as_op(r);
+}
+
+template <int BP> struct PoolTraits {
+  static constexpr int WORDS = 2 * BP;               // 32-bit words per lane record
+  static constexpr float OFF = BP <= 4 ? 128.f : 0.f;  // code offset inside the operand
+  static constexpr bool QUANT = BP < 16;
+};
+
+template <int DH> struct Geo {
+  static constexpr int TS = 4096 / DH;  // slots per tile
+  static constexpr int NB = TS / 16;    // 16-slot blocks per tile
+  static constexpr int KS = DH / 32;    // 32-channel k-steps
+  static constexpr int CB = DH / 16;    // 16-channel output blocks
+  static constexpr int KV = TS / 32;    // 32-slot steps of the P V product
+};
+
+// Per-wave running state of the online softmax for 16 query columns.
+template <int DH>
+struct SoftState {
+  float m;               // running max (log2 domain) of column n16
+  float l;               // partial denominator of column n16 (this lane's slots)
+  float zc[DH / 32];     // partial per-group additive term of column n16
+  f32x4 O[DH / 16];      // rows = columns 4*o4 + i, cols = channel n16 + 16 cb
+};
+
+template <int DH>
+__device__ __forceinline__ void state_init(SoftState<DH> &st) {
+  st.m = -INFINITY;
+  st.l = 0.f;
+#pragma unroll
+  for (int g = 0; g < DH / 32; ++g) st.zc[g] = 0.f;
+#pragma unroll
+  for (int c = 0; c < DH / 16; ++c) st.O[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// Column description: the lane's column n16 takes keys with
+// key_lo <= key <= key_hi (slot indices in decode, positions in prefill).
+struct ColMask {
+  int lo, hi;  // inclusive bounds; lo > hi disables the column
+};
+
+// Process one tile of width BP, one 32-slot step at a time: S^T for two
+// 16-slot blocks, the online-softmax update, then O += P' V for the step.
+// `slot0` = pool slot index of the tile's first slot; `kpos` = key
+// positions (nullptr: keys are compared by slot index).
+template <int DH, int BP, int G>
+__device__ __forceinline__ void process_tile(SoftState<DH> &st, const uint32_t *kw,
+                                             const uint32_t *vw, const uint8_t *tp,
+                                             const CacheView &cv, int slot0,
+                                             const int32_t *kpos, int klen, ColMask cm,
+                                             const bf16x8 *qop, const float *qsum,
+                                             float scale2) {
+  using Gm = Geo<DH>;
+  using PT = PoolTraits<BP>;
+  constexpr int NG = DH / G;    // groups per head vector
+  constexpr int gks = G / 32;   // k-steps per group
+  constexpr int NV = NG;        // 16-byte scale/zero vectors per 4 slots
+  const int lane = threadIdx.x & 63, o4 = lane >> 4;
+  const u32x4 *ksz = (const u32x4 *)(tp + cv.k_sz_off(BP == 2 ? 0 : BP == 4 ? 1 : 2));
+  const u32x4 *vsz = (const u32x4 *)(tp + cv.v_sz_off(BP == 2 ? 0 : BP == 4 ? 1 : 2));
+#pragma unroll
+  for (int kv = 0; kv < Gm::KV; ++kv) {
+    float p[2][4];
+    // ---- S^T = K Q^T for blocks 2 kv, 2 kv + 1, dequantized per group
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb) {
+      const int blk = 2 * kv + hb;
+      f32x4 acc[NG];
+#pragma unroll
+      for (int g = 0; g < NG; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < Gm::KS; ++ks) {
+        const bf16x8 a = field_op<BP>(kw, blk * Gm::KS + ks);
+        acc[ks / gks] =
+            __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qop[ks], acc[ks / gks], 0, 0, 0);
+      }
+      const int stb = blk * 16 + 4 * o4;  // first of this lane's 4 slots in the tile
+      uint32_t kszw[4 * NG];
+      if constexpr (PT::QUANT) {
+#pragma unroll
+        for (int x = 0; x < NV; ++x) {
+          const u32x4 v = ksz[(stb * NG) / 4 + x];
+#pragma unroll
+          for (int y = 0; y < 4; ++y) kszw[4 * x + y] = v[y];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float sv = 0.f;
+        if constexpr (PT::QUANT) {
+#pragma unroll
+          for (int g = 0; g < NG; ++g) {
+            const uint32_t szw = kszw[i * NG + g];
+            const uint16_t sb = uint16_t(szw), zb = uint16_t(szw >> 16);
+            const float S = float(*(const _Float16 *)&sb), Z = float(*(const _Float16 *)&zb);
+            sv = fmaf(S, acc[g][i], sv);
+            sv = fmaf(Z - PT::OFF * S, qsum[g], sv);
+          }
+        } else {
+#pragma unroll
+          for (int g = 0; g < NG; ++g) sv += acc[g][i];
+        }
+        const int slot = slot0 + stb + i;
+        // slots past the pool length hold no token (and may lie past `capacity`)
+        const int key = kpos ? (slot < klen ? kpos[slot] : INT_MAX) : slot;
+        p[hb][i] = (key >= cm.lo && key <= cm.hi) ? sv * scale2 : -INFINITY;
+      }
+    }
+    // ---- online softmax for this lane's column
+    float mt = fmaxf(fmaxf(fmaxf(p[0][0], p[0][1]), fmaxf(p[0][2], p[0][3])),
+                     fmaxf(fmaxf(p[1][0], p[1][1]), fmaxf(p[1][2], p[1][3])));
+    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float mnew = fmaxf(st.m, mt);
+    const bool live = mnew != -INFINITY;
+    const float corr = live ? exp2f(st.m - mnew) : 1.f;
+    float ps = 0.f;
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        p[hb][i] = live ? exp2f(p[hb][i] - mnew) : 0.f;
+        ps += p[hb][i];
+      }
+    st.l = st.l * corr + ps;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) st.zc[g] *= corr;
+    st.m = mnew;
+    // rescale the output rows (column 4 o4 + i lives in lane 4 o4 + i)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float ci = __shfl(corr, 4 * o4 + i, 64);
+#pragma unroll
+      for (int cb = 0; cb < Gm::CB; ++cb) st.O[cb][i] *= ci;
+    }
+    // ---- O += P' V.  Quantized pools: P' = fp16(p * s_v) against fp16
+    // codes; the 16-bit pool: P = bf16(p) against the stored bf16.
+    uint32_t vszw[2][4 * NG];  // this lane's slots of the step: two runs of 4
+    if constexpr (PT::QUANT) {
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+        for (int x = 0; x < NV; ++x) {
+          const u32x4 v = vsz[((32 * kv + 16 * hb + 4 * o4) * NG) / 4 + x];
+#pragma unroll
+          for (int y = 0; y < 4; ++y) vszw[hb][4 * x + y] = v[y];
+        }
+    }
+    u32x4 pk[NG];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+#pragma unroll
+      for (int jp = 0; jp < 4; ++jp) {
+        uint32_t h2[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int j = 2 * jp + h;
+          const float pp = p[j >> 2][j & 3];
+          if constexpr (PT::QUANT) {
+            const uint32_t szw = vszw[j >> 2][(j & 3) * NG + g];
+            const uint16_t sb = uint16_t(szw), zb = uint16_t(szw >> 16);
+            const float S = float(*(const _Float16 *)&sb), Z = float(*(const _Float16 *)&zb);
+            const _Float16 ph = (_Float16)(pp * S);
+            st.zc[g] = fmaf(pp, Z, st.zc[g]);
+            h2[h] = uint32_t(*(const uint16_t *)&ph);
+          } else {
+            h2[h] = uint32_t(f2bf(pp));
+          }
+        }
+        pk[g][jp] = h2[0] | (h2[1] << 16);
+      }
+    }
+#pragma unroll
+    for (int cb = 0; cb < Gm::CB; ++cb) {
+      const int g = (16 * cb) / G;
+      if constexpr (PT::QUANT) {
+        const f16x8 bv = vfield_h<BP>(vw, kv * Gm::CB + cb);
+        st.O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_h(pk[g]), bv, st.O[cb], 0, 0, 0);
+      } else {
+        const bf16x8 bv = field_op<BP>(vw, kv * Gm::CB + cb);
+        st.O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_op(pk[g]), bv, st.O[cb], 0, 0, 0);
+      }
+    }
+  }
+}
+
+// Walk this wave's tiles [t_begin, t_end) (stride `step`) of pool bi.
+// Narrow pools (records of 16-32 B per lane) keep the next tile's records in
+// flight while the current one is processed; wide pools issue 64-128 B per
+// lane per tile and rely on the other waves of the CU to hide latency.
+template <int DH, int BP, int G>
+__device__ void run_pool(SoftState<DH> &st, const CacheView &cv, int s, int bi, int g,
+                         int t_begin, int t_end, int step, const int32_t *kpos, int klen,
+                         ColMask cm, const bf16x8 *qop, const float *qsum, float scale2) {
+  using PT = PoolTraits<BP>;
+  const int lane = threadIdx.x & 63;
+  constexpr int V4 = PT::WORDS / 4;  // 16-byte loads per record
+  constexpr bool PREFETCH = BP <= 4;
+  union Rec {
+    u32x4 v[V4];
+    uint32_t w[PT::WORDS];
+  };
+  auto load = [&](int t, Rec &k, Rec &v) {
+    const uint8_t *tp = cv.tile(s, bi, g, t);
+    const u32x4 *kp = (const u32x4 *)(tp + lane * 8 * BP);
+    const u32x4 *vp = (const u32x4 *)(tp + 512 * BP + lane * 8 * BP);
+#pragma unroll
+    for (int x = 0; x < V4; ++x) {
+      k.v[x] = kp[x];
+      v.v[x] = vp[x];
+    }
+  };
+  if (t_begin >= t_end) return;
+  Rec kr, vr;
+  if constexpr (PREFETCH) {
+    Rec kn, vn;
+    load(t_begin, kr, vr);
+    for (int t = t_begin; t < t_end; t += step) {
+      const bool more = t + step < t_end;
+      if (more) load(t + step, kn, vn);
+      process_tile<DH, BP, G>(st, kr.w, vr.w, cv.tile(s, bi, g, t), cv, t * cv.TS, kpos, klen,
+                              cm, qop, qsum, scale2);
+      if (more) {
+        kr = kn;
+        vr = vn;
+      }
+    }
+  } else {
+    for (int t = t_begin; t < t_end; t += step) {
+      load(t, kr, vr);
+      process_tile<DH, BP, G>(st, kr.w, vr.w, cv.tile(s, bi, g, t), cv, t * cv.TS, kpos, klen,
+                              cm, qop, qsum, scale2);
+    }
+  }
+}
+
+template <int DH, int G>
+__device__ __forceinline__ void run_pool_any(SoftState<DH> &st, const CacheView &cv, int s,
+                                             int bi, int g, int t0, int t1, int step,
+                                             const int32_t *kpos, int klen, ColMask cm,
+                                             const bf16x8 *qop, const float *qsum, float scale2) {
+  switch (bi) {
+    case 0: run_pool<DH, 2, G>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
+    case 1: run_pool<DH, 4, G>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
+    case 2: run_pool<DH, 8, G>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
+    default: run_pool<DH, 16, G>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
+  }
+}
+
+__device__ __forceinline__ int lower_bound_pos(const int32_t *pos, int len, int p) {
+  int lo = 0, hi = len;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (pos[mid] < p)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  return lo;
+}
+
+// Load the query operand of column n16 (a row of q, bf16) and per-group sums.
+template <int DH, int G>
+__device__ __forceinline__ void load_q(const bf16 *qrow, bool valid, bf16x8 *qop, float *qsum) {
+  const int lane = threadIdx.x & 63, o4 = lane >> 4;
+  constexpr int gks = G / 32;
+#pragma unroll
+  for (int g = 0; g < DH / G; ++g) qsum[g] = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < DH / 32; ++ks) {
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (valid) v = *(const u32x4 *)(qrow + 32 * ks + 8 * o4);
+    qop[ks] = as_op(v);
+    float sum = 0.f;
+#pragma unroll
+    for (int y = 0; y < 4; ++y)
+      sum += __uint_as_float(v[y] << 16) + __uint_as_float(v[y] & 0xFFFF0000u);
+    qsum[ks / gks] += sum;
+  }
+#pragma unroll
+  for (int g = 0; g < DH / G; ++g) {
+    qsum[g] += __shfl_xor(qsum[g], 16, 64);
+    qsum[g] += __shfl_xor(qsum[g], 32, 64);
+  }
+}
+
+// Reduce the per-lane partials of every column over the 4 lane groups and
+// fold the additive terms into O.  Afterwards lane (0, n) holds in O[cb][i]
+// the un-normalised output of column i, channel n + 16 cb; m and l are the
+// column's (lane n16 = column).
+template <int DH, int G>
+__device__ __forceinline__ void state_finish(SoftState<DH> &st) {
+  constexpr int NG = DH / G;
+  const int lane = threadIdx.x & 63, o4 = lane >> 4;
+  st.l += __shfl_xor(st.l, 16, 64);
+  st.l += __shfl_xor(st.l, 32, 64);
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    st.zc[g] += __shfl_xor(st.zc[g], 16, 64);
+    st.zc[g] += __shfl_xor(st.zc[g], 32, 64);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int col = 4 * o4 + i;
+#pragma unroll
+    for (int cb = 0; cb < DH / 16; ++cb) {
+      const int g = (16 * cb) / G;
+      st.O[cb][i] += __shfl(st.zc[g], col, 64);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ decode
+struct DecodeArgs {
+  CacheView cv;
+  const bf16 *q;
+  const uint8_t *mode;
+  const int32_t *seq_ids;
+  float *part;  // [B*H][NS][DH + 2]: m, l, O
+  int B, H, R, w, NS;
+  float scale2;
+};
+
+template <int DH, int G>
+__global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(DecodeArgs a) {
+  __shared__ float red[4][16][DH + 2];
+  const CacheView &cv = a.cv;
+  const int Hkv = cv.Hkv;
+  const int b = blockIdx.x / Hkv, g = blockIdx.x % Hkv, split = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, n16 = lane & 15;
+  const int s = a.seq_ids ? a.seq_ids[b] : b;
+  const bool seq_ok = s >= 0 && s < cv.n_seq;
+  const int R = a.R;
+  const int head = g * R + n16;
+  const int hm = (seq_ok && n16 < R) ? int(a.mode[b * a.H + head]) : 0;
+  // union of the group's modes (max over the R heads)
+  int U = hm;
+  for (int x = 1; x < 16; x <<= 1) U = max(U, __shfl_xor(U, x, 16));
+  SoftState<DH> st;
+  state_init(st);
+  if (U > 0) {
+    const int P = cv.seq_len[s] - 1;
+    bf16x8 qop[DH / 32];
+    float qsum[DH / G];
+    load_q<DH, G>(a.q + (int64_t(b) * a.H + head) * DH, n16 < R && hm > 0, qop, qsum);
+    for (int bi = 0; bi < 4; ++bi) {
+      const int len = cv.pool_len[s * 4 + bi];
+      const int32_t *pos = cv.pos + (int64_t(s) * 4 + bi) * cv.capacity;
+      const int lb = lower_bound_pos(pos, len, P - a.w + 1);  // first slot of the window
+      const int lo = U == TRIROUTE_FULL ? 0 : lb;
+      const int t0 = lo / cv.TS, t1 = (len + cv.TS - 1) / cv.TS;
+      const int nt = t1 - t0;
+      const int a0 = t0 + int(int64_t(nt) * split / a.NS);
+      const int a1 = t0 + int(int64_t(nt) * (split + 1) / a.NS);
+      ColMask cm;
+      cm.lo = hm == TRIROUTE_FULL ? 0 : hm == TRIROUTE_LOCAL ? lb : 1;
+      cm.hi = hm == TRIROUTE_SKIP ? 0 : len - 1;
+      run_pool_any<DH, G>(st, cv, s, bi, g, a0 + wave, a1, 4, nullptr, len, cm, qop, qsum, a.scale2);
+    }
+    state_finish<DH, G>(st);
+  }
+  // merge the 4 waves in LDS: red[wave][col][0] = m, [1] = l, [2..] = O
+  if (lane < 16) {
+    red[wave][lane][0] = st.m;
+    red[wave][lane][1] = st.l;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int cb = 0; cb < DH / 16; ++cb)
+      red[wave][4 * (lane >> 4) + i][2 + n16 + 16 * cb] = st.O[cb][i];
+  __syncthreads();
+  // threads: column c = tid / (DH + 2) ... one thread per (column < R, entry)
+  for (int idx = threadIdx.x; idx < R * (DH + 2); idx += 256) {
+    const int col = idx / (DH + 2), e = idx % (DH + 2);
+    float M = -INFINITY;
+#pragma unroll
+    for (int wv = 0; wv < 4; ++wv) M = fmaxf(M, red[wv][col][0]);
+    float val;
+    if (e == 0) {
+      val = M;
+    } else {
+      val = 0.f;
+      if (M != -INFINITY) {
+#pragma unroll
+        for (int wv = 0; wv < 4; ++wv) {
+          const float mw = red[wv][col][0];
+          if (mw != -INFINITY) val += red[wv][col][e] * exp2f(mw - M);
+        }
+      }
+    }
+    const int hh = g * R + col;
+    a.part[((int64_t(b) * a.H + hh) * a.NS + split) * (DH + 2) + e] = val;
+  }
+}
+
+template <int DH>
+__global__ __launch_bounds__(256) void attn_decode_combine_kernel(const float *__restrict__ part,
+                                                                  int BH, int NS,
+                                                                  bf16 *__restrict__ o) {
+  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (item >= BH) return;
+  const float *pp = part + int64_t(item) * NS * (DH + 2);
+  float M = -INFINITY;
+  for (int j = 0; j < NS; ++j) M = fmaxf(M, pp[j * (DH + 2)]);
+  float L = 0.f, acc[DH / 64];
+#pragma unroll
+  for (int r = 0; r < DH / 64; ++r) acc[r] = 0.f;
+  if (M != -INFINITY) {
+    for (int j = 0; j < NS; ++j) {
+      const float mj = pp[j * (DH + 2)];
+      if (mj == -INFINITY) continue;
+      const float wgt = exp2f(mj - M);
+      L += pp[j * (DH + 2) + 1] * wgt;
+#pragma unroll
+      for (int r = 0; r < DH / 64; ++r) acc[r] += pp[j * (DH + 2) + 2 + lane + 64 * r] * wgt;
+    }
+  }
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+#pragma unroll
+  for (int r = 0; r < DH / 64; ++r) o[int64_t(item) * DH + lane + 64 * r] = f2bf(acc[r] * inv);
+}
+
+// ------------------------------------------------------------------ prefill
+struct PrefillArgs {
+  CacheView cv;
+  const bf16 *q;
+  const int32_t *seq_ids, *cnt, *idx;
+  bf16 *o;
+  int B, T, H, R, w, QT;  // QT = 16-query tiles per segment (ceil(T / 16))
+  float scale2;
+};
+
+template <int DH, int G>
+__global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(PrefillArgs a) {
+  const CacheView &cv = a.cv;
+  const int lane = threadIdx.x & 63, n16 = lane & 15, o4 = lane >> 4;
+  const int64_t item = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  const int nseg = a.B * a.H * 2;
+  if (item >= int64_t(nseg) * a.QT) return;
+  // heavy tiles first: full-mode segments, latest query tiles first
+  const int seg_rank = int(item / a.QT), qt = a.QT - 1 - int(item % a.QT);
+  const int half = a.B * a.H;
+  const int seg = seg_rank < half ? 2 * seg_rank + 1 : 2 * (seg_rank - half);
+  const int count = a.cnt[seg];
+  if (qt * 16 >= count) return;
+  const int b = seg / (2 * a.H), h = (seg >> 1) % a.H, m = (seg & 1) + 1;
+  const int g = h / a.R;
+  const int s = a.seq_ids ? a.seq_ids[b] : b;
+  if (s < 0 || s >= cv.n_seq) return;
+  const int base = cv.seq_len[s] - a.T;
+  const int j = qt * 16 + n16;
+  const bool valid = j < count;
+  const int* lst = a.idx + int64_t(seg) * a.T;
+  const int t = valid ? lst[j] : lst[count - 1];
+  const int P = base + t;
+  const int Pmax = base + lst[min(qt * 16 + 15, count - 1)];
+  const int Pmin = base + lst[qt * 16];
+  bf16x8 qop[DH / 32];
+  float qsum[DH / G];
+  load_q<DH, G>(a.q + (int64_t(b * a.T + t) * a.H + h) * DH, valid, qop, qsum);
+  ColMask cm;
+  cm.lo = valid ? (m == TRIROUTE_LOCAL ? P - a.w + 1 : 0) : 1;
+  cm.hi = valid ? P : 0;
+  const int lo_all = m == TRIROUTE_LOCAL ? Pmin - a.w + 1 : 0;
+  SoftState<DH> st;
+  state_init(st);
+  for (int bi = 0; bi < 4; ++bi) {
+    const int len = cv.pool_len[s * 4 + bi];
+    const int32_t *pos = cv.pos + (int64_t(s) * 4 + bi) * cv.capacity;
+    const int sa = lower_bound_pos(pos, len, lo_all);
+    const int sb = lower_bound_pos(pos, len, Pmax + 1);
+    if (sa >= sb) continue;
+    run_pool_any<DH, G>(st, cv, s, bi, g, sa / cv.TS, (sb + cv.TS - 1) / cv.TS, 1, pos, len, cm,
+                     qop, qsum, a.scale2);
+  }
+  state_finish<DH, G>(st);
+  // normalise and write: lane (o4, n) holds column 4 o4 + i, channel n + 16 cb
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int col = 4 * o4 + i;
+    const float lc = __shfl(st.l, col, 64);
+    const int jj = qt * 16 + col;
+    if (jj >= count) continue;
+    const int tt = lst[jj];
+    const float inv = lc > 0.f ? 1.f / lc : 0.f;
+    bf16 *orow = a.o + (int64_t(b * a.T + tt) * a.H + h) * DH;
+#pragma unroll
+    for (int cb = 0; cb < DH / 16; ++cb) orow[n16 + 16 * cb] = f2bf(st.O[cb][i] * inv);
+  }
+}
+
+// ------------------------------------------------------------------ launchers
+int decode_splits(int B, int Hkv, int capacity, int TS) {
+  const int tiles = (capacity + TS - 1) / TS;
+  int ns = (2048 + B * Hkv - 1) / (B * Hkv);
+  ns = min(ns, max(1, tiles / 8));
+  return max(1, min(ns, 64));
+}
+
+hipError_t launch_attn_mfma_decode(const triroute_cfg &cfg, const CacheView &cv, int B,
+                                   const int32_t *seq_ids, const void *q, const uint8_t *mode,
+                                   void *o, float *part, hipStream_t st) {
+  DecodeArgs a;
+  a.cv = cv;
+  a.q = (const bf16 *)q;
+  a.mode = mode;
+  a.seq_ids = seq_ids;
+  a.part = part;
+  a.B = B;
+  a.H = cfg.n_heads;
+  a.R = cfg.n_heads / cfg.n_kv_heads;
+  a.w = cfg.window;
+  a.NS = decode_splits(B, cfg.n_kv_heads, cv.capacity, cv.TS);
+  a.scale2 = LOG2E / sqrtf(float(cfg.head_dim));
+  dim3 grid(B * cfg.n_kv_heads, a.NS);
+  const int BH = B * cfg.n_heads;
+  const int G = cfg.kv_group;
+  if (cfg.head_dim == 64) {
+    if (G == 64)
+      attn_decode_mfma_kernel<64, 64><<<grid, 256, 0, st>>>(a);
+    else
+      attn_decode_mfma_kernel<64, 32><<<grid, 256, 0, st>>>(a);
+    attn_decode_combine_kernel<64><<<(BH + 3) / 4, 256, 0, st>>>(part, BH, a.NS, (bf16 *)o);
+  } else {
+    if (G == 64)
+      attn_decode_mfma_kernel<128, 64><<<grid, 256, 0, st>>>(a);
+    else
+      attn_decode_mfma_kernel<128, 32><<<grid, 256, 0, st>>>(a);
+    attn_decode_combine_kernel<128><<<(BH + 3) / 4, 256, 0, st>>>(part, BH, a.NS, (bf16 *)o);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_mfma_prefill(const triroute_cfg &cfg, const CacheView &cv, int B, int T,
+                                    const int32_t *seq_ids, const void *q,
+                                    const triroute_compaction &c, void *o, hipStream_t st) {
+  PrefillArgs a;
+  a.cv = cv;
+  a.q = (const bf16 *)q;
+  a.seq_ids = seq_ids;
+  a.cnt = c.attn_cnt;
+  a.idx = c.attn_idx;
+  a.o = (bf16 *)o;
+  a.B = B;
+  a.T = T;
+  a.H = cfg.n_heads;
+  a.R = cfg.n_heads / cfg.n_kv_heads;
+  a.w = cfg.window;
+  a.QT = (T + 15) / 16;
+  a.scale2 = LOG2E / sqrtf(float(cfg.head_dim));
+  const int64_t items = int64_t(B) * cfg.n_heads * 2 * a.QT;
+  dim3 grid(unsigned((items + 3) / 4));
+  const int G = cfg.kv_group;
+  if (cfg.head_dim == 64) {
+    if (G == 64)
+      attn_prefill_mfma_kernel<64, 64><<<grid, 256, 0, st>>>(a);
+    else
+      attn_prefill_mfma_kernel<64, 32><<<grid, 256, 0, st>>>(a);
+  } else {
+    if (G == 64)
+      attn_prefill_mfma_kernel<128, 64><<<grid, 256, 0, st>>>(a);
+    else
+      attn_prefill_mfma_kernel<128, 32><<<grid, 256, 0, st>>>(a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace tr

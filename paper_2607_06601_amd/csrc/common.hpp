@@ -96,9 +96,12 @@ __device__ __forceinline__ void k_place(int st, int c, int dh, int &lane, int &q
   q = (blk * KS + ks) * 8 + j;
 }
 // V element (slot st in tile, channel c) -> (lane record, element index q).
+// Within a 32-slot step, element j of lane group o is slot 16*(j/4) + 4*o + j%4:
+// the order in which the K-tile MFMA leaves softmax weights in registers.
 __device__ __forceinline__ void v_place(int st, int c, int dh, int &lane, int &q) {
   int CB = dh >> 4;
-  int kv = st >> 5, o = (st >> 3) & 3, j = st & 7;
+  int kv = st >> 5, r = st & 31;
+  int o = (r >> 2) & 3, j = (r >> 4) * 4 + (r & 3);
   int cb = c >> 4, n = c & 15;
   lane = o * 16 + n;
   q = (kv * CB + cb) * 8 + j;

@@ -40,6 +40,14 @@ hipError_t launch_attn_valu_prefill(const triroute_cfg &cfg, const CacheView &cv
 hipError_t launch_attn_valu_decode(const triroute_cfg &cfg, const CacheView &cv, int B,
                                    const int32_t *seq_ids, const void *q, const uint8_t *mode,
                                    void *o, hipStream_t st);
+// attn_mfma.hip (bf16)
+int decode_splits(int B, int Hkv, int capacity, int TS);
+hipError_t launch_attn_mfma_decode(const triroute_cfg &cfg, const CacheView &cv, int B,
+                                   const int32_t *seq_ids, const void *q, const uint8_t *mode,
+                                   void *o, float *part, hipStream_t st);
+hipError_t launch_attn_mfma_prefill(const triroute_cfg &cfg, const CacheView &cv, int B, int T,
+                                    const int32_t *seq_ids, const void *q,
+                                    const triroute_compaction &c, void *o, hipStream_t st);
 // misc.hip
 hipError_t launch_rms_norm2(const triroute_cfg &cfg, int N, const void *x, const void *g,
                             void *out, hipStream_t st);

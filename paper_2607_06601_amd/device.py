@@ -25,6 +25,10 @@ def to_dev(a, dtype, device="cuda"):
 class DeviceLayer:
     """Device copies of one layer's weights (and optionally its inputs)."""
 
+    @staticmethod
+    def cfg_only(L: dict) -> Cfg:
+        return cfg_from(L["cfg"])
+
     def __init__(self, L: dict, device="cuda", moe: bool = True):
         cfg = L["cfg"]
         self.cfg = cfg_from(cfg)

@@ -31,11 +31,103 @@ def _taps(cfg, N, act_t):
         egate=torch.empty(N, k, dtype=torch.float32, device=DEV),
         o=torch.empty(N, H * dh, dtype=act_t, device=DEV),
         xt=torch.empty(N, d, dtype=act_t, device=DEV),
-        k=torch.empty(N, Hkv * dh, dtype=act_t, device=DEV))
+        q=torch.empty(N, H * dh, dtype=act_t, device=DEV),
+        k=torch.empty(N, Hkv * dh, dtype=act_t, device=DEV),
+        v=torch.empty(N, Hkv * dh, dtype=act_t, device=DEV))
     s = tr.Taps(mode=t["mode"].data_ptr(), bit=t["bit"].data_ptr(), eidx=t["eidx"].data_ptr(),
                 egate=t["egate"].data_ptr(), o=t["o"].data_ptr(), xt=t["xt"].data_ptr(),
-                k=t["k"].data_ptr())
+                q=t["q"].data_ptr(), k=t["k"].data_ptr(), v=t["v"].data_ptr())
     return t, s
+
+
+LOOSE = 8.0   # bound multiplier for outputs downstream of a differing cache entry
+LOOSE_ROW = 3.0  # for x~ / x_out rows whose input differs from the oracle's in a bf16 bit
+
+
+def _cache_diff(c, cache, cfg, r, seqs, only_last=False):
+    """Per sequence, a bool [n_positions, Hkv]: the quantized cache entry of
+    that token / kv head (codes or fp16 scale/zero, K or V) differs between
+    the GPU's cache and the oracle's.  Each side quantized its own K/V, which
+    may legitimately differ in the last bf16 bit (fp32 versus fp64
+    accumulation); such a bit can move a code.  16-bit entries are not
+    flagged: a last-bit difference there is covered by the tolerance."""
+    from test_gpu_stages import export_pool
+    Hkv, dh, G, act = cfg["Hkv"], cfg["dh"], cfg["G"], cfg["act"]
+    out = {}
+    for s_ in seqs:
+        st = r["stored"][s_]
+        npos = 1 if only_last else cfg["T"]
+        d = np.zeros((npos, Hkv), bool)
+        plen = npy(cache.pool_len())[s_]
+        for bi, ent in st.items():
+            if bi == 3:
+                continue
+            n = len(ent["tokens"])
+            first = int(plen[bi]) - n            # the oracle's tokens are the pool's last n
+            ko, vo, ks, vs, _ = export_pool(c, cache, s_, bi, int(plen[bi]), act, Hkv, dh, G)
+            sl = slice(first, first + n)
+            kc, vc = npy(ko)[sl], npy(vo)[sl]
+            ksz = npy(ks)[sl].astype(np.int16).view(np.float16)
+            vsz = npy(vs)[sl].astype(np.int16).view(np.float16)
+            diff = (kc != ent["kc"]).any(-1) | (vc != ent["vc"]).any(-1)
+            diff |= (ksz[..., 0] != ent["ks"]).any(-1) | (ksz[..., 1] != ent["kz"]).any(-1)
+            diff |= (vsz[..., 0] != ent["vs"]).any(-1) | (vsz[..., 1] != ent["vz"]).any(-1)
+            idx = np.zeros(n, int) if only_last else ent["tokens"]
+            d[idx] |= diff
+        out[s_] = d
+    return out
+
+
+def _tainted(cfg, mode, rows, seq_of, qpos_of, diff, first_pos=0):
+    """(row, head) pairs whose key range holds a differing cache entry."""
+    H, Hkv, w = cfg["H"], cfg["Hkv"], cfg["w"]
+    grp = H // Hkv
+    taint = np.zeros((len(rows), H), bool)
+    for ri, row in enumerate(rows):
+        b, P = seq_of(row), qpos_of(row)
+        for h in range(H):
+            m = int(mode[row, h])
+            if m == 0:
+                continue
+            lo = max(0, P - w + 1) if m == 1 else 0
+            keys = diff[b][max(lo - first_pos, 0):P - first_pos + 1, h // grp]
+            taint[ri, h] = bool(keys.any())
+    return taint
+
+
+def _assert_split(gpu, ref, taint_rows, act, name, loose=LOOSE):
+    """Strict tolerance on untainted entries, `loose` x tolerance on the rest."""
+    from _common import BF16_ATOL, BF16_RTOL
+    ok = ~taint_rows
+    if ok.any():
+        assert_close(gpu[ok], ref[ok], act, name)
+    if (~ok).any():
+        err = np.abs(gpu[~ok] - ref[~ok])
+        bound = loose * (BF16_ATOL + BF16_RTOL * np.abs(ref[~ok]))
+        assert (err <= bound).all(), f"{name} (tainted): max abs err {err.max():.3e}"
+
+
+def _row_bits_differ(gpu, ref, act):
+    """Rows where the GPU's stored activation differs from the oracle's
+    rounding of the same quantity in at least one element (both are correct
+    roundings of nearly equal values; the expert block amplifies such a bit,
+    see test_oracle_pins.test_expert_block_sensitivity_to_one_bit)."""
+    if act != "bf16":
+        return np.zeros(len(gpu), bool)
+    return (np.asarray(gpu, np.float32) != np.asarray(ref, np.float32)).any(axis=1)
+
+
+def _check_chain(t, xo, r, rows, taint, act):
+    H = taint.shape[1]
+    og = npy(t["o"])[rows]
+    _assert_split(og.reshape(len(rows), H, -1), r["o"].reshape(len(rows), H, -1), taint, act, "o")
+    trow = taint.any(axis=1)
+    xt_rows = trow | _row_bits_differ(og, r["o"].reshape(len(rows), -1), act)
+    _assert_split(npy(t["xt"])[rows], r["xt"], xt_rows, act, "xt", LOOSE_ROW)
+    xo_rows = xt_rows | _row_bits_differ(npy(t["xt"])[rows], r["xt"], act)
+    print(f"rows held to the {LOOSE_ROW}x bound: x~ {int(xt_rows.sum())}, x_out {int(xo_rows.sum())}"
+          f" of {len(rows)}")
+    _assert_split(npy(xo)[rows], r["xout"], xo_rows, act, "x_out", LOOSE_ROW)
 
 
 def run_prefill(L, D=None):
@@ -68,7 +160,7 @@ def test_layer_prefill(name, seed, nrows):
     L = layer(name, seed)
     cfg = L["cfg"]
     N = cfg["B"] * cfg["T"]
-    xo, t, _ = run_prefill(L)
+    xo, t, cache = run_prefill(L)
     if nrows is None:
         rows = np.arange(N)
     else:
@@ -78,13 +170,15 @@ def test_layer_prefill(name, seed, nrows):
     r = oracle.layer_prefill(L, rows)
     _check_decisions(t, r)
     act = cfg["act"]
-    assert_close(npy(t["o"])[rows], r["o"].reshape(len(rows), -1), act, "o")
-    assert_close(npy(t["xt"])[rows], r["xt"], act, "xt")
-    assert_close(npy(xo)[rows], r["xout"], act, "x_out")
-    # diagnostic: K the GPU stored vs the oracle's native-precision K
-    kg = npy(t["k"]).reshape(cfg["B"], cfg["T"], -1)
-    diff = sum(int((kg[b] != r["k"][b].reshape(cfg["T"], -1)).sum()) for b in r["k"])
-    print(f"{name}: K elements differing in the last bit: {diff}")
+    T, H, dh = cfg["T"], cfg["H"], cfg["dh"]
+    D_cfg = DeviceLayer.cfg_only(L)
+    diff = _cache_diff(D_cfg, cache, cfg, r, sorted(r["stored"]))
+    frac = np.mean([d.mean() for d in diff.values()])
+    taint = _tainted(cfg, npy(t["mode"]), rows, lambda row: row // T, lambda row: row % T, diff)
+    print(f"{name}: quantized cache entries differing: {frac:.2e}; "
+          f"tainted (row, head) pairs: {int(taint.sum())}/{taint.size}")
+    assert frac < 1e-2
+    _check_chain(t, xo, r, rows, taint, act)
 
 
 def test_layer_prefill_deterministic():
@@ -138,6 +232,11 @@ def test_layer_decode(name, nseq):
     r = oracle.layer_decode(L, seqs)
     _check_decisions(t, r)
     act = cfg["act"]
-    assert_close(npy(t["o"])[seqs], r["o"].reshape(len(seqs), -1), act, "o")
-    assert_close(npy(t["xt"])[seqs], r["xt"], act, "xt")
-    assert_close(npy(xo)[seqs], r["xout"], act, "x_out")
+    H, dh = cfg["H"], cfg["dh"]
+    diff = _cache_diff(c, cache, cfg, r, [int(x) for x in seqs], only_last=True)
+    taint = _tainted(cfg, npy(t["mode"]), [int(x) for x in seqs], lambda row: row,
+                     lambda row: ctx, diff, first_pos=ctx)
+    print(f"{name}: new tokens with a differing quantized cache entry: "
+          f"{sum(int(d.any()) for d in diff.values())}/{len(diff)}; "
+          f"tainted (seq, head) pairs: {int(taint.sum())}/{taint.size}")
+    _check_chain(t, xo, r, seqs, taint, act)

@@ -155,9 +155,10 @@ def _host_decode(raw: np.ndarray, desc, c, s, bi, g, slot, ch, isv, act):
     base = desc.off_pool[bi] + ((s * Hkv + g) * desc.n_tiles + tile) * desc.tile_bytes[bi]
     if isv:
         base += 512 * bp
+        r = st % 32
         f = (st // 32) * (dh // 16) + ch // 16
-        lane = ((st % 32) // 8) * 16 + ch % 16
-        j = st % 8
+        lane = ((r % 16) // 4) * 16 + ch % 16
+        j = (r // 16) * 4 + r % 4
     else:
         f = (st // 16) * (dh // 32) + ch // 32
         lane = ((ch % 32) // 8) * 16 + st % 16

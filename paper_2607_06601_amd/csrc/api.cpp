@@ -65,7 +65,7 @@ struct Carve {
   }
 };
 
-constexpr int DECODE_MAX_SPLITS = 64;
+constexpr int DECODE_MAX_SPLITS = 16;
 
 struct LayerBufs {
   void *n1, *q, *k, *v, *o, *xt;

@@ -16,9 +16,11 @@
 //                 the z_v and offset terms are accumulated per query column
 //                 and added at the end.  The 16-bit pool multiplies bf16(p)
 //                 by the stored bf16 values.
-// Online softmax in the exp2 domain.  Decode splits each (sequence, kv head)
-// over KV chunks: 4 waves merge in LDS, a second kernel merges the chunks
-// with log-sum-exp.
+// Online softmax in the exp2 domain.  Decode runs one 8-wave block per
+// (sequence, kv head, chunk); each wave streams its share of every pool's
+// whole tiles into a private LDS ring with direct-to-LDS loads several tiles
+// ahead; the waves merge in LDS and a last kernel merges the chunks with
+// log-sum-exp.
 #include <limits.h>
 
 #include "kernels.hpp"
@@ -129,25 +131,89 @@ struct ColMask {
   int lo, hi;  // inclusive bounds; lo > hi disables the column
 };
 
+// Everything one lane needs of a tile, loaded together so that a tile costs
+// one memory round trip (and narrow pools prefetch the next tile): the K and
+// V lane records, the fp16 scale/zero words of the lane's slots, and, when
+// keys are compared by position, the positions of the lane's slots.
+template <int DH, int BP, int G, bool POS>
+struct TileRegs {
+  using Gm = Geo<DH>;
+  static constexpr int NG = DH / G;
+  static constexpr int W = PoolTraits<BP>::WORDS;
+  static constexpr bool Q = PoolTraits<BP>::QUANT;
+  union {
+    u32x4 v[W / 4];
+    uint32_t w[W];
+  } k, v;
+  uint32_t ksz[Q ? Gm::NB : 1][4 * NG];        // [block][slot i * NG + g]
+  uint32_t vsz[Q ? Gm::KV : 1][2][4 * NG];     // [step][half][slot i * NG + g]
+  int key[POS ? Gm::NB : 1][4];                // key positions (INT_MAX past klen)
+
+  __device__ __forceinline__ void load(const uint8_t *tp, const CacheView &cv, int bi,
+                                       int slot0, const int32_t *kpos, int klen) {
+    const int lane = threadIdx.x & 63, o4 = lane >> 4;
+    const u32x4 *kp = (const u32x4 *)(tp + lane * 8 * BP);
+    const u32x4 *vp = (const u32x4 *)(tp + 512 * BP + lane * 8 * BP);
+#pragma unroll
+    for (int x = 0; x < W / 4; ++x) {
+      k.v[x] = kp[x];
+      v.v[x] = vp[x];
+    }
+    if constexpr (Q) {
+      const u32x4 *ks = (const u32x4 *)(tp + cv.k_sz_off(bi));
+      const u32x4 *vs = (const u32x4 *)(tp + cv.v_sz_off(bi));
+#pragma unroll
+      for (int blk = 0; blk < Gm::NB; ++blk)
+#pragma unroll
+        for (int x = 0; x < NG; ++x) {
+          const u32x4 t = ks[((blk * 16 + 4 * o4) * NG) / 4 + x];
+#pragma unroll
+          for (int y = 0; y < 4; ++y) ksz[blk][4 * x + y] = t[y];
+        }
+#pragma unroll
+      for (int kv = 0; kv < Gm::KV; ++kv)
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+          for (int x = 0; x < NG; ++x) {
+            const u32x4 t = vs[((32 * kv + 16 * hb + 4 * o4) * NG) / 4 + x];
+#pragma unroll
+            for (int y = 0; y < 4; ++y) vsz[kv][hb][4 * x + y] = t[y];
+          }
+    }
+    if constexpr (POS) {
+#pragma unroll
+      for (int blk = 0; blk < Gm::NB; ++blk)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int slot = slot0 + blk * 16 + 4 * o4 + i;
+          // slots past the pool length hold no token (and may lie past `capacity`)
+          key[blk][i] = slot < klen ? kpos[slot] : INT_MAX;
+        }
+    }
+  }
+};
+
+__device__ __forceinline__ void unpack_sz(uint32_t szw, float &S, float &Z) {
+  const uint16_t sb = uint16_t(szw), zb = uint16_t(szw >> 16);
+  S = float(*(const _Float16 *)&sb);
+  Z = float(*(const _Float16 *)&zb);
+}
+
 // Process one tile of width BP, one 32-slot step at a time: S^T for two
 // 16-slot blocks, the online-softmax update, then O += P' V for the step.
-// `slot0` = pool slot index of the tile's first slot; `kpos` = key
-// positions (nullptr: keys are compared by slot index).
-template <int DH, int BP, int G>
-__device__ __forceinline__ void process_tile(SoftState<DH> &st, const uint32_t *kw,
-                                             const uint32_t *vw, const uint8_t *tp,
-                                             const CacheView &cv, int slot0,
-                                             const int32_t *kpos, int klen, ColMask cm,
-                                             const bf16x8 *qop, const float *qsum,
+// `slot0` = pool slot index of the tile's first slot.  Keys are compared
+// with the column's bounds by position (POS) or by slot index.
+template <int DH, int BP, int G, bool POS>
+__device__ __forceinline__ void process_tile(SoftState<DH> &st,
+                                             const TileRegs<DH, BP, G, POS> &tr, int slot0,
+                                             ColMask cm, const bf16x8 *qop, const float *qsum,
                                              float scale2) {
   using Gm = Geo<DH>;
   using PT = PoolTraits<BP>;
   constexpr int NG = DH / G;    // groups per head vector
   constexpr int gks = G / 32;   // k-steps per group
-  constexpr int NV = NG;        // 16-byte scale/zero vectors per 4 slots
   const int lane = threadIdx.x & 63, o4 = lane >> 4;
-  const u32x4 *ksz = (const u32x4 *)(tp + cv.k_sz_off(BP == 2 ? 0 : BP == 4 ? 1 : 2));
-  const u32x4 *vsz = (const u32x4 *)(tp + cv.v_sz_off(BP == 2 ? 0 : BP == 4 ? 1 : 2));
 #pragma unroll
   for (int kv = 0; kv < Gm::KV; ++kv) {
     float p[2][4];
@@ -160,19 +226,9 @@ __device__ __forceinline__ void process_tile(SoftState<DH> &st, const uint32_t *
       for (int g = 0; g < NG; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < Gm::KS; ++ks) {
-        const bf16x8 a = field_op<BP>(kw, blk * Gm::KS + ks);
+        const bf16x8 a = field_op<BP>(tr.k.w, blk * Gm::KS + ks);
         acc[ks / gks] =
             __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qop[ks], acc[ks / gks], 0, 0, 0);
-      }
-      const int stb = blk * 16 + 4 * o4;  // first of this lane's 4 slots in the tile
-      uint32_t kszw[4 * NG];
-      if constexpr (PT::QUANT) {
-#pragma unroll
-        for (int x = 0; x < NV; ++x) {
-          const u32x4 v = ksz[(stb * NG) / 4 + x];
-#pragma unroll
-          for (int y = 0; y < 4; ++y) kszw[4 * x + y] = v[y];
-        }
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -180,9 +236,8 @@ __device__ __forceinline__ void process_tile(SoftState<DH> &st, const uint32_t *
         if constexpr (PT::QUANT) {
 #pragma unroll
           for (int g = 0; g < NG; ++g) {
-            const uint32_t szw = kszw[i * NG + g];
-            const uint16_t sb = uint16_t(szw), zb = uint16_t(szw >> 16);
-            const float S = float(*(const _Float16 *)&sb), Z = float(*(const _Float16 *)&zb);
+            float S, Z;
+            unpack_sz(tr.ksz[blk][i * NG + g], S, Z);
             sv = fmaf(S, acc[g][i], sv);
             sv = fmaf(Z - PT::OFF * S, qsum[g], sv);
           }
@@ -190,9 +245,11 @@ __device__ __forceinline__ void process_tile(SoftState<DH> &st, const uint32_t *
 #pragma unroll
           for (int g = 0; g < NG; ++g) sv += acc[g][i];
         }
-        const int slot = slot0 + stb + i;
-        // slots past the pool length hold no token (and may lie past `capacity`)
-        const int key = kpos ? (slot < klen ? kpos[slot] : INT_MAX) : slot;
+        int key;
+        if constexpr (POS)
+          key = tr.key[blk][i];
+        else
+          key = slot0 + blk * 16 + 4 * o4 + i;
         p[hb][i] = (key >= cm.lo && key <= cm.hi) ? sv * scale2 : -INFINITY;
       }
     }
@@ -225,17 +282,6 @@ __device__ __forceinline__ void process_tile(SoftState<DH> &st, const uint32_t *
     }
     // ---- O += P' V.  Quantized pools: P' = fp16(p * s_v) against fp16
     // codes; the 16-bit pool: P = bf16(p) against the stored bf16.
-    uint32_t vszw[2][4 * NG];  // this lane's slots of the step: two runs of 4
-    if constexpr (PT::QUANT) {
-#pragma unroll
-      for (int hb = 0; hb < 2; ++hb)
-#pragma unroll
-        for (int x = 0; x < NV; ++x) {
-          const u32x4 v = vsz[((32 * kv + 16 * hb + 4 * o4) * NG) / 4 + x];
-#pragma unroll
-          for (int y = 0; y < 4; ++y) vszw[hb][4 * x + y] = v[y];
-        }
-    }
     u32x4 pk[NG];
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
@@ -247,9 +293,8 @@ __device__ __forceinline__ void process_tile(SoftState<DH> &st, const uint32_t *
           const int j = 2 * jp + h;
           const float pp = p[j >> 2][j & 3];
           if constexpr (PT::QUANT) {
-            const uint32_t szw = vszw[j >> 2][(j & 3) * NG + g];
-            const uint16_t sb = uint16_t(szw), zb = uint16_t(szw >> 16);
-            const float S = float(*(const _Float16 *)&sb), Z = float(*(const _Float16 *)&zb);
+            float S, Z;
+            unpack_sz(tr.vsz[kv][j >> 2][(j & 3) * NG + g], S, Z);
             const _Float16 ph = (_Float16)(pp * S);
             st.zc[g] = fmaf(pp, Z, st.zc[g]);
             h2[h] = uint32_t(*(const uint16_t *)&ph);
@@ -264,89 +309,75 @@ __device__ __forceinline__ void process_tile(SoftState<DH> &st, const uint32_t *
     for (int cb = 0; cb < Gm::CB; ++cb) {
       const int g = (16 * cb) / G;
       if constexpr (PT::QUANT) {
-        const f16x8 bv = vfield_h<BP>(vw, kv * Gm::CB + cb);
+        const f16x8 bv = vfield_h<BP>(tr.v.w, kv * Gm::CB + cb);
         st.O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_h(pk[g]), bv, st.O[cb], 0, 0, 0);
       } else {
-        const bf16x8 bv = field_op<BP>(vw, kv * Gm::CB + cb);
+        const bf16x8 bv = field_op<BP>(tr.v.w, kv * Gm::CB + cb);
         st.O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_op(pk[g]), bv, st.O[cb], 0, 0, 0);
       }
     }
   }
 }
 
-// Walk this wave's tiles [t_begin, t_end) (stride `step`) of pool bi.
-// Narrow pools (records of 16-32 B per lane) keep the next tile's records in
-// flight while the current one is processed; wide pools issue 64-128 B per
-// lane per tile and rely on the other waves of the CU to hide latency.
-template <int DH, int BP, int G>
+// Walk this wave's tiles [t_begin, t_end) (stride `step`) of pool bi.  Narrow
+// pools without position keys keep the next tile in flight while the current
+// one is processed; otherwise all of a tile's loads are issued at once.
+template <int DH, int BP, int G, bool POS>
 __device__ void run_pool(SoftState<DH> &st, const CacheView &cv, int s, int bi, int g,
                          int t_begin, int t_end, int step, const int32_t *kpos, int klen,
                          ColMask cm, const bf16x8 *qop, const float *qsum, float scale2) {
-  using PT = PoolTraits<BP>;
-  const int lane = threadIdx.x & 63;
-  constexpr int V4 = PT::WORDS / 4;  // 16-byte loads per record
-  constexpr bool PREFETCH = BP <= 4;
-  union Rec {
-    u32x4 v[V4];
-    uint32_t w[PT::WORDS];
-  };
-  auto load = [&](int t, Rec &k, Rec &v) {
-    const uint8_t *tp = cv.tile(s, bi, g, t);
-    const u32x4 *kp = (const u32x4 *)(tp + lane * 8 * BP);
-    const u32x4 *vp = (const u32x4 *)(tp + 512 * BP + lane * 8 * BP);
-#pragma unroll
-    for (int x = 0; x < V4; ++x) {
-      k.v[x] = kp[x];
-      v.v[x] = vp[x];
-    }
-  };
   if (t_begin >= t_end) return;
-  Rec kr, vr;
-  if constexpr (PREFETCH) {
-    Rec kn, vn;
-    load(t_begin, kr, vr);
+  TileRegs<DH, BP, G, POS> cur;
+  if constexpr (BP <= 4 && !POS) {
+    TileRegs<DH, BP, G, POS> nxt;
+    cur.load(cv.tile(s, bi, g, t_begin), cv, bi, t_begin * cv.TS, kpos, klen);
     for (int t = t_begin; t < t_end; t += step) {
       const bool more = t + step < t_end;
-      if (more) load(t + step, kn, vn);
-      process_tile<DH, BP, G>(st, kr.w, vr.w, cv.tile(s, bi, g, t), cv, t * cv.TS, kpos, klen,
-                              cm, qop, qsum, scale2);
-      if (more) {
-        kr = kn;
-        vr = vn;
-      }
+      if (more) nxt.load(cv.tile(s, bi, g, t + step), cv, bi, (t + step) * cv.TS, kpos, klen);
+      process_tile<DH, BP, G, POS>(st, cur, t * cv.TS, cm, qop, qsum, scale2);
+      if (more) cur = nxt;
     }
   } else {
     for (int t = t_begin; t < t_end; t += step) {
-      load(t, kr, vr);
-      process_tile<DH, BP, G>(st, kr.w, vr.w, cv.tile(s, bi, g, t), cv, t * cv.TS, kpos, klen,
-                              cm, qop, qsum, scale2);
+      cur.load(cv.tile(s, bi, g, t), cv, bi, t * cv.TS, kpos, klen);
+      process_tile<DH, BP, G, POS>(st, cur, t * cv.TS, cm, qop, qsum, scale2);
     }
   }
 }
 
-template <int DH, int G>
+template <int DH, int G, bool POS>
 __device__ __forceinline__ void run_pool_any(SoftState<DH> &st, const CacheView &cv, int s,
                                              int bi, int g, int t0, int t1, int step,
                                              const int32_t *kpos, int klen, ColMask cm,
                                              const bf16x8 *qop, const float *qsum, float scale2) {
   switch (bi) {
-    case 0: run_pool<DH, 2, G>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
-    case 1: run_pool<DH, 4, G>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
-    case 2: run_pool<DH, 8, G>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
-    default: run_pool<DH, 16, G>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
+    case 0: run_pool<DH, 2, G, POS>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
+    case 1: run_pool<DH, 4, G, POS>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
+    case 2: run_pool<DH, 8, G, POS>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
+    default: run_pool<DH, 16, G, POS>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
   }
 }
 
+// First index in [0, len) with pos[index] >= p (pos ascending), searched by
+// the whole wave: each round probes 64 evenly spaced entries and narrows the
+// range 64-fold, so a 32k-entry pool takes two rounds of parallel loads.
+// Must be called by all 64 lanes with wave-uniform arguments.
 __device__ __forceinline__ int lower_bound_pos(const int32_t *pos, int len, int p) {
-  int lo = 0, hi = len;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (pos[mid] < p)
-      lo = mid + 1;
-    else
-      hi = mid;
+  const int lane = threadIdx.x & 63;
+  int lo = 0, hi = len;  // the answer lies in [lo, hi]
+  while (hi - lo > 64) {
+    const int span = hi - lo;
+    const int idx = lo + int(int64_t(span) * (lane + 1) / 64) - 1;
+    const uint64_t below = __ballot(pos[idx] < p);
+    const int c = __popcll(below);  // probes 0 .. c-1 lie below p
+    const int nlo = c > 0 ? lo + int(int64_t(span) * c / 64) : lo;
+    const int nhi = c < 64 ? lo + int(int64_t(span) * (c + 1) / 64) - 1 : hi;
+    lo = nlo;
+    hi = nhi;
   }
-  return lo;
+  const int idx = lo + lane;
+  const uint64_t below = __ballot(idx < hi && pos[idx] < p);
+  return lo + __popcll(below);
 }
 
 // Load the query operand of column n16 (a row of q, bf16) and per-group sums.
@@ -411,10 +442,87 @@ struct DecodeArgs {
   float scale2;
 };
 
+// Geometry of the decode stream for one pool width: tile bytes, 1 KB wave
+// transfers per tile, ring slot size, and ring depth within a wave's
+// share of the block's LDS (8 shares plus a few words fill the 160 KB).
+constexpr int DEC_WAVES = 8;
+constexpr int DEC_RING = 20 * 1024 - 32;
+template <int DH, int G, int BP>
+struct DmaGeo {
+  static constexpr int TS = 4096 / DH;
+  static constexpr int NG = DH / G;
+  static constexpr int TB = 1024 * BP + (BP < 16 ? 2 * TS * NG * 4 : 0);
+  static constexpr int NI = (TB + 1023) / 1024;
+  static constexpr int SLOT = (TB + 255) & ~255;
+  static constexpr int D = DEC_RING / SLOT < 6 ? DEC_RING / SLOT : 6;
+  static_assert(D >= 1 && (D - 1) * NI < 64, "ring depth / vmcnt range");
+};
+
+// s_waitcnt vmcnt(N) with the other counters left free (gfx9 encoding:
+// vmcnt[3:0] at bits 3:0, vmcnt[5:4] at bits 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+template <int NI>
+__device__ __forceinline__ void wait_tiles_ahead(int ahead) {
+  switch (ahead) {
+    case 0: wait_vm<0>(); break;
+    case 1: wait_vm<NI>(); break;
+    case 2: wait_vm<2 * NI>(); break;
+    case 3: wait_vm<3 * NI>(); break;
+    case 4: wait_vm<4 * NI>(); break;
+    default: wait_vm<5 * NI>(); break;
+  }
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Copy one whole tile (codes + scale/zero, contiguous in HBM) into an LDS
+// ring slot with direct-to-LDS loads: each lane moves 16 bytes per 1 KB
+// transfer; lanes past the tile end sit out the last transfer.
+template <int TB, int NI>
+__device__ __forceinline__ void tile_to_lds(const uint8_t *src, uint8_t *dst) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int j = 0; j < NI; ++j) {
+    const int off = j * 1024 + lane * 16;
+    if (off < TB)
+      __builtin_amdgcn_global_load_lds((const void *)(src + off), (lds_void *)(dst + j * 1024), 16,
+                                       0, 0);
+  }
+}
+
+// Stream this wave's tiles [w0, w1) of pool bi through its LDS ring.  On
+// entry no other vector-memory load of the wave may be in flight.
+template <int DH, int G, int BP>
+__device__ void stream_pool(SoftState<DH> &st, const CacheView &cv, int s, int bi, int g,
+                            int w0, int w1, uint8_t *myring, ColMask cm, const bf16x8 *qop,
+                            const float *qsum, float scale2, int len) {
+  using DG = DmaGeo<DH, G, BP>;
+  for (int j = 0; j < DG::D - 1 && w0 + j < w1; ++j)
+    tile_to_lds<DG::TB, DG::NI>(cv.tile(s, bi, g, w0 + j), myring + j * DG::SLOT);
+  for (int t = w0; t < w1; ++t) {
+    const int nx = t + DG::D - 1;
+    if (nx < w1)
+      tile_to_lds<DG::TB, DG::NI>(cv.tile(s, bi, g, nx), myring + ((nx - w0) % DG::D) * DG::SLOT);
+    wait_tiles_ahead<DG::NI>(min(DG::D - 1, w1 - 1 - t));
+    TileRegs<DH, BP, G, false> tr;
+    tr.load(myring + ((t - w0) % DG::D) * DG::SLOT, cv, bi, t * DG::TS, nullptr, len);
+    process_tile<DH, BP, G, false>(st, tr, t * DG::TS, cm, qop, qsum, scale2);
+  }
+}
+
+// One block of 8 waves per (sequence, kv head, chunk): the waves split each
+// pool's tile range of the chunk into contiguous runs and stream them.
 template <int DH, int G>
-__global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(DecodeArgs a) {
-  __shared__ float red[4][16][DH + 2];
+__global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
+  constexpr int RING = DEC_WAVES * DEC_RING;
+  static_assert(RING >= DEC_WAVES * 16 * (DH + 2) * 4, "ring doubles as the merge buffer");
+  __shared__ __align__(16) uint8_t ring[RING];
+  __shared__ int bounds[4][2];  // per pool: first slot of the window, length
   const CacheView &cv = a.cv;
+  constexpr int TS = 4096 / DH;
   const int Hkv = cv.Hkv;
   const int b = blockIdx.x / Hkv, g = blockIdx.x % Hkv, split = blockIdx.y;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, n16 = lane & 15;
@@ -423,33 +531,51 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(DecodeArgs a) 
   const int R = a.R;
   const int head = g * R + n16;
   const int hm = (seq_ok && n16 < R) ? int(a.mode[b * a.H + head]) : 0;
-  // union of the group's modes (max over the R heads)
-  int U = hm;
+  int U = hm;  // union of the group's modes (max over its R heads)
   for (int x = 1; x < 16; x <<= 1) U = max(U, __shfl_xor(U, x, 16));
   SoftState<DH> st;
   state_init(st);
+  const int P = U > 0 ? cv.seq_len[s] - 1 : 0;
+  if (U > 0 && wave < 4) {  // waves 0..3 find the window start of pools 0..3
+    const int bi = wave;
+    const int len = cv.pool_len[s * 4 + bi];
+    const int32_t *pos = cv.pos + (int64_t(s) * 4 + bi) * cv.capacity;
+    const int lb = lower_bound_pos(pos, len, P - a.w + 1);
+    if (lane == 0) {
+      bounds[bi][0] = lb;
+      bounds[bi][1] = len;
+    }
+  }
+  __syncthreads();
   if (U > 0) {
-    const int P = cv.seq_len[s] - 1;
     bf16x8 qop[DH / 32];
     float qsum[DH / G];
     load_q<DH, G>(a.q + (int64_t(b) * a.H + head) * DH, n16 < R && hm > 0, qop, qsum);
+    wait_vm<0>();  // from here on the only vector-memory traffic is the tile stream
+    uint8_t *myring = ring + wave * DEC_RING;
     for (int bi = 0; bi < 4; ++bi) {
-      const int len = cv.pool_len[s * 4 + bi];
-      const int32_t *pos = cv.pos + (int64_t(s) * 4 + bi) * cv.capacity;
-      const int lb = lower_bound_pos(pos, len, P - a.w + 1);  // first slot of the window
+      const int lb = bounds[bi][0], len = bounds[bi][1];
       const int lo = U == TRIROUTE_FULL ? 0 : lb;
-      const int t0 = lo / cv.TS, t1 = (len + cv.TS - 1) / cv.TS;
-      const int nt = t1 - t0;
-      const int a0 = t0 + int(int64_t(nt) * split / a.NS);
-      const int a1 = t0 + int(int64_t(nt) * (split + 1) / a.NS);
+      const int t0 = lo / TS, nt = (len + TS - 1) / TS - t0;
+      const int c0 = t0 + int(int64_t(nt) * split / a.NS);
+      const int c1 = t0 + int(int64_t(nt) * (split + 1) / a.NS);
+      const int w0 = c0 + (c1 - c0) * wave / DEC_WAVES;
+      const int w1 = c0 + (c1 - c0) * (wave + 1) / DEC_WAVES;
       ColMask cm;
       cm.lo = hm == TRIROUTE_FULL ? 0 : hm == TRIROUTE_LOCAL ? lb : 1;
       cm.hi = hm == TRIROUTE_SKIP ? 0 : len - 1;
-      run_pool_any<DH, G>(st, cv, s, bi, g, a0 + wave, a1, 4, nullptr, len, cm, qop, qsum, a.scale2);
+      switch (bi) {
+        case 0: stream_pool<DH, G, 2>(st, cv, s, 0, g, w0, w1, myring, cm, qop, qsum, a.scale2, len); break;
+        case 1: stream_pool<DH, G, 4>(st, cv, s, 1, g, w0, w1, myring, cm, qop, qsum, a.scale2, len); break;
+        case 2: stream_pool<DH, G, 8>(st, cv, s, 2, g, w0, w1, myring, cm, qop, qsum, a.scale2, len); break;
+        default: stream_pool<DH, G, 16>(st, cv, s, 3, g, w0, w1, myring, cm, qop, qsum, a.scale2, len); break;
+      }
     }
     state_finish<DH, G>(st);
   }
-  // merge the 4 waves in LDS: red[wave][col][0] = m, [1] = l, [2..] = O
+  // merge the waves in LDS (the ring is free now): [wave][col][m, l, O]
+  __syncthreads();
+  float(*red)[16][DH + 2] = (float(*)[16][DH + 2])ring;
   if (lane < 16) {
     red[wave][lane][0] = st.m;
     red[wave][lane][1] = st.l;
@@ -460,12 +586,11 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(DecodeArgs a) 
     for (int cb = 0; cb < DH / 16; ++cb)
       red[wave][4 * (lane >> 4) + i][2 + n16 + 16 * cb] = st.O[cb][i];
   __syncthreads();
-  // threads: column c = tid / (DH + 2) ... one thread per (column < R, entry)
-  for (int idx = threadIdx.x; idx < R * (DH + 2); idx += 256) {
+  for (int idx = threadIdx.x; idx < R * (DH + 2); idx += blockDim.x) {
     const int col = idx / (DH + 2), e = idx % (DH + 2);
     float M = -INFINITY;
 #pragma unroll
-    for (int wv = 0; wv < 4; ++wv) M = fmaxf(M, red[wv][col][0]);
+    for (int wv = 0; wv < DEC_WAVES; ++wv) M = fmaxf(M, red[wv][col][0]);
     float val;
     if (e == 0) {
       val = M;
@@ -473,7 +598,7 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(DecodeArgs a) 
       val = 0.f;
       if (M != -INFINITY) {
 #pragma unroll
-        for (int wv = 0; wv < 4; ++wv) {
+        for (int wv = 0; wv < DEC_WAVES; ++wv) {
           const float mw = red[wv][col][0];
           if (mw != -INFINITY) val += red[wv][col][e] * exp2f(mw - M);
         }
@@ -562,8 +687,8 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(PrefillArgs a
     const int sa = lower_bound_pos(pos, len, lo_all);
     const int sb = lower_bound_pos(pos, len, Pmax + 1);
     if (sa >= sb) continue;
-    run_pool_any<DH, G>(st, cv, s, bi, g, sa / cv.TS, (sb + cv.TS - 1) / cv.TS, 1, pos, len, cm,
-                     qop, qsum, a.scale2);
+    run_pool_any<DH, G, true>(st, cv, s, bi, g, sa / cv.TS, (sb + cv.TS - 1) / cv.TS, 1, pos, len,
+                              cm, qop, qsum, a.scale2);
   }
   state_finish<DH, G>(st);
   // normalise and write: lane (o4, n) holds column 4 o4 + i, channel n + 16 cb
@@ -583,10 +708,11 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(PrefillArgs a
 
 // ------------------------------------------------------------------ launchers
 int decode_splits(int B, int Hkv, int capacity, int TS) {
-  const int tiles = (capacity + TS - 1) / TS;
-  int ns = (2048 + B * Hkv - 1) / (B * Hkv);
-  ns = min(ns, max(1, tiles / 8));
-  return max(1, min(ns, 64));
+  (void)capacity;
+  (void)TS;
+  // one 8-wave block per CU: chunks so that the grid covers the 256 CUs
+  const int ns = (256 + B * Hkv - 1) / (B * Hkv);
+  return max(1, min(ns, 16));
 }
 
 hipError_t launch_attn_mfma_decode(const triroute_cfg &cfg, const CacheView &cv, int B,
@@ -607,17 +733,18 @@ hipError_t launch_attn_mfma_decode(const triroute_cfg &cfg, const CacheView &cv,
   dim3 grid(B * cfg.n_kv_heads, a.NS);
   const int BH = B * cfg.n_heads;
   const int G = cfg.kv_group;
+  const int threads = 64 * DEC_WAVES;
   if (cfg.head_dim == 64) {
     if (G == 64)
-      attn_decode_mfma_kernel<64, 64><<<grid, 256, 0, st>>>(a);
+      attn_decode_kernel<64, 64><<<grid, threads, 0, st>>>(a);
     else
-      attn_decode_mfma_kernel<64, 32><<<grid, 256, 0, st>>>(a);
+      attn_decode_kernel<64, 32><<<grid, threads, 0, st>>>(a);
     attn_decode_combine_kernel<64><<<(BH + 3) / 4, 256, 0, st>>>(part, BH, a.NS, (bf16 *)o);
   } else {
     if (G == 64)
-      attn_decode_mfma_kernel<128, 64><<<grid, 256, 0, st>>>(a);
+      attn_decode_kernel<128, 64><<<grid, threads, 0, st>>>(a);
     else
-      attn_decode_mfma_kernel<128, 32><<<grid, 256, 0, st>>>(a);
+      attn_decode_kernel<128, 32><<<grid, threads, 0, st>>>(a);
     attn_decode_combine_kernel<128><<<(BH + 3) / 4, 256, 0, st>>>(part, BH, a.NS, (bf16 *)o);
   }
   return hipGetLastError();

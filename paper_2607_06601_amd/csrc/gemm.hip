@@ -1,12 +1,12 @@
-// Dense and grouped GEMMs of the layer, C = A B^T with both operands
-// K-contiguous, and their fused epilogues:
+// Dense and grouped GEMMs of the layer for the fp32 activation dtype (the bf16
+// path is gemm_mfma.hip), C = A B^T with both operands K-contiguous, and
+// their fused epilogues:
 //   QKV   : [n1] x [Wq;Wk;Wv]^T, rotate-half RoPE on q and k
 //   O-proj: xt = x + o Wo^T
 //   MoE-1 : H = silu(n2 Wgate_e^T) * (n2 Wup_e^T) per expert e, rows gathered
 //           from the expert's assignment list (paper Sec. 3.2 (B), SwiGLU)
 //   MoE-2 : Y[a] = H Wdown_e^T, scattered back to assignment a
-// bf16 runs on MFMA (v_mfma_f32_16x16x32_bf16, fp32 accumulate); fp32 runs a
-// VALU tiled kernel.  Grouped problems map block -> (expert, row tile) from
+// A VALU tiled kernel.  Grouped problems map block -> (expert, row tile) from
 // the device-side expert counts, so no host synchronisation is needed.
 #include <type_traits>
 
@@ -14,8 +14,6 @@
 
 namespace tr {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct Tile {
   int m0, n0, mvalid, e, p0;
@@ -195,101 +193,6 @@ struct Moe2Prob {
   }
 };
 
-// ------------------------------------------------------------- MFMA kernel
-// Block tile 128 x 128, K step 64, 4 waves of 64 x 64.  LDS rows of 128 B
-// (64 bf16) with 16-byte chunk c stored at c ^ (row & 7).
-template <class P>
-__global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(P p) {
-  constexpr int BM = 128, LDC = 132;
-  __shared__ __align__(16) uint8_t smem[65536];
-  Tile tc;
-  if (!p.map(blockIdx.x, blockIdx.y, BM, tc)) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int lr = tid >> 3, lc = tid & 7;
-  const bf16 *ap[4], *bq[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = lr + 32 * i;
-    ap[i] = r < tc.mvalid ? p.a_row(tc, r) : nullptr;
-    bq[i] = p.b_row(tc, r);
-  }
-  uint4 ra[4], rb[4];
-  const uint4 zero = make_uint4(0, 0, 0, 0);
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ra[i] = ap[i] ? *(const uint4 *)(ap[i] + k0 + lc * 8) : zero;
-      rb[i] = bq[i] ? *(const uint4 *)(bq[i] + k0 + lc * 8) : zero;
-    }
-  };
-  auto sstore = [&](int buf) {
-    uint8_t *As = smem + buf * 32768;
-    uint8_t *Bs = As + 16384;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = lr + 32 * i;
-      const int o = r * 128 + ((lc ^ (r & 7)) << 4);
-      *(uint4 *)(As + o) = ra[i];
-      *(uint4 *)(Bs + o) = rb[i];
-    }
-  };
-  f32x4 acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int nk = p.K / 64;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload((kt + 1) * 64);
-    const uint8_t *As = smem + (kt & 1) * 32768;
-    const uint8_t *Bs = As + 16384;
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 a[4], b[4];
-      const int ch = ks * 4 + (lane >> 4);
-#pragma unroll
-      for (int mi = 0; mi < 4; ++mi) {
-        const int r = wm * 64 + mi * 16 + (lane & 15);
-        a[mi] = *(const bf16x8 *)(As + r * 128 + ((ch ^ (r & 7)) << 4));
-      }
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni) {
-        const int n = wn * 64 + ni * 16 + (lane & 15);
-        b[ni] = *(const bf16x8 *)(Bs + n * 128 + ((ch ^ (n & 7)) << 4));
-      }
-#pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], b[ni], acc[mi][ni], 0, 0, 0);
-    }
-    if (kt + 1 < nk) sstore((kt + 1) & 1);
-    __syncthreads();
-  }
-  // epilogue: stage 64 rows at a time as fp32 in LDS
-  float *C = (float *)smem;
-#pragma unroll
-  for (int half = 0; half < 2; ++half) {
-    if (wm == half) {
-#pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            C[(mi * 16 + 4 * (lane >> 4) + i) * LDC + wn * 64 + ni * 16 + (lane & 15)] =
-                acc[mi][ni][i];
-    }
-    __syncthreads();
-    p.epilogue(tc, C, LDC, half * 64, 64, tid);
-    __syncthreads();
-  }
-}
-
 // -------------------------------------------------------------- fp32 kernel
 // Block tile 64 x 128, K step 16, 4 x 8 outputs per thread.
 template <class P>
@@ -342,13 +245,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(P p) {
 
 // ------------------------------------------------------------------ launchers
 template <class P>
-static hipError_t run_gemm(const triroute_cfg &, const P &p, int m_tiles128, int m_tiles64,
-                           int n_tiles, hipStream_t st) {
-  if constexpr (std::is_same<typename P::elem, bf16>::value) {
-    if (m_tiles128 > 0) gemm_mfma_kernel<P><<<dim3(m_tiles128, n_tiles), 256, 0, st>>>(p);
-  } else {
-    if (m_tiles64 > 0) gemm_f32_kernel<P><<<dim3(m_tiles64, n_tiles), 256, 0, st>>>(p);
-  }
+static hipError_t run_gemm(const triroute_cfg &, const P &p, int, int m_tiles64, int n_tiles,
+                           hipStream_t st) {
+  static_assert(std::is_same<typename P::elem, float>::value, "fp32 problems only");
+  if (m_tiles64 > 0) gemm_f32_kernel<P><<<dim3(m_tiles64, n_tiles), 256, 0, st>>>(p);
   return hipGetLastError();
 }
 
@@ -386,7 +286,7 @@ hipError_t launch_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
                       const triroute_dense_w &w, const int32_t *pos_base, const int32_t *pos_idx,
                       void *q, void *k, void *v, hipStream_t st) {
   return cfg.act == TRIROUTE_BF16
-             ? qkv_t<bf16>(cfg, B, Tq, n1, w, pos_base, pos_idx, q, k, v, st)
+             ? mfma_qkv(cfg, B, Tq, n1, w, pos_base, pos_idx, q, k, v, st)
              : qkv_t<float>(cfg, B, Tq, n1, w, pos_base, pos_idx, q, k, v, st);
 }
 
@@ -406,7 +306,7 @@ static hipError_t oproj_t(const triroute_cfg &cfg, int N, const void *x, const v
 
 hipError_t launch_oproj(const triroute_cfg &cfg, int N, const void *x, const void *o,
                         const triroute_dense_w &w, void *xt, hipStream_t st) {
-  return cfg.act == TRIROUTE_BF16 ? oproj_t<bf16>(cfg, N, x, o, w, xt, st)
+  return cfg.act == TRIROUTE_BF16 ? mfma_oproj(cfg, N, x, o, w, xt, st)
                                   : oproj_t<float>(cfg, N, x, o, w, xt, st);
 }
 
@@ -448,7 +348,7 @@ static hipError_t moe_gemms_t(const triroute_cfg &cfg, int N, const void *n2,
 hipError_t launch_moe_gemms(const triroute_cfg &cfg, int N, const void *n2,
                             const triroute_moe_w &w, const triroute_compaction &c, void *Hm,
                             float *Y, hipStream_t st) {
-  return cfg.act == TRIROUTE_BF16 ? moe_gemms_t<bf16>(cfg, N, n2, w, c, Hm, Y, st)
+  return cfg.act == TRIROUTE_BF16 ? mfma_moe(cfg, N, n2, w, c, Hm, Y, st)
                                   : moe_gemms_t<float>(cfg, N, n2, w, c, Hm, Y, st);
 }
 

@@ -33,6 +33,14 @@ hipError_t launch_oproj(const triroute_cfg &cfg, int N, const void *x, const voi
 hipError_t launch_moe_gemms(const triroute_cfg &cfg, int N, const void *n2,
                             const triroute_moe_w &w, const triroute_compaction &c, void *Hm,
                             float *Y, hipStream_t st);
+// gemm_mfma.hip (bf16)
+hipError_t mfma_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
+                    const triroute_dense_w &w, const int32_t *pos_base, const int32_t *pos_idx,
+                    void *q, void *k, void *v, hipStream_t st);
+hipError_t mfma_oproj(const triroute_cfg &cfg, int N, const void *x, const void *o,
+                      const triroute_dense_w &w, void *xt, hipStream_t st);
+hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const triroute_moe_w &w,
+                    const triroute_compaction &c, void *Hm, float *Y, hipStream_t st);
 // attn_valu.hip
 hipError_t launch_attn_valu_prefill(const triroute_cfg &cfg, const CacheView &cv, int B, int Tq,
                                     const int32_t *seq_ids, const void *q,

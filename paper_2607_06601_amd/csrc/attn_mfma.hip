@@ -458,25 +458,17 @@ struct DmaGeo {
   static_assert(D >= 1 && (D - 1) * NI < 64, "ring depth / vmcnt range");
 };
 
-// s_waitcnt vmcnt(N) with the other counters left free (gfx9 encoding:
-// vmcnt[3:0] at bits 3:0, vmcnt[5:4] at bits 15:14, expcnt 6:4, lgkmcnt 11:8).
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-template <int NI>
+// Wait until at most `ahead` tiles of NI transfers each are still in flight
+// (0 <= ahead < D).
+template <int NI, int D>
 __device__ __forceinline__ void wait_tiles_ahead(int ahead) {
-  switch (ahead) {
-    case 0: wait_vm<0>(); break;
-    case 1: wait_vm<NI>(); break;
-    case 2: wait_vm<2 * NI>(); break;
-    case 3: wait_vm<3 * NI>(); break;
-    case 4: wait_vm<4 * NI>(); break;
-    default: wait_vm<5 * NI>(); break;
-  }
+  if constexpr (D > 5) if (ahead >= 5) { wait_vm<5 * NI>(); return; }
+  if constexpr (D > 4) if (ahead == 4) { wait_vm<4 * NI>(); return; }
+  if constexpr (D > 3) if (ahead == 3) { wait_vm<3 * NI>(); return; }
+  if constexpr (D > 2) if (ahead == 2) { wait_vm<2 * NI>(); return; }
+  if constexpr (D > 1) if (ahead == 1) { wait_vm<NI>(); return; }
+  wait_vm<0>();
 }
-
-typedef __attribute__((address_space(3))) void lds_void;
 
 // Copy one whole tile (codes + scale/zero, contiguous in HBM) into an LDS
 // ring slot with direct-to-LDS loads: each lane moves 16 bytes per 1 KB
@@ -484,12 +476,11 @@ typedef __attribute__((address_space(3))) void lds_void;
 template <int TB, int NI>
 __device__ __forceinline__ void tile_to_lds(const uint8_t *src, uint8_t *dst) {
   const int lane = threadIdx.x & 63;
+  const uint32_t d0 = lds_addr(dst);
 #pragma unroll
   for (int j = 0; j < NI; ++j) {
     const int off = j * 1024 + lane * 16;
-    if (off < TB)
-      __builtin_amdgcn_global_load_lds((const void *)(src + off), (lds_void *)(dst + j * 1024), 16,
-                                       0, 0);
+    if (off < TB) dma16(src + off, d0 + j * 1024);
   }
 }
 
@@ -506,7 +497,7 @@ __device__ void stream_pool(SoftState<DH> &st, const CacheView &cv, int s, int b
     const int nx = t + DG::D - 1;
     if (nx < w1)
       tile_to_lds<DG::TB, DG::NI>(cv.tile(s, bi, g, nx), myring + ((nx - w0) % DG::D) * DG::SLOT);
-    wait_tiles_ahead<DG::NI>(min(DG::D - 1, w1 - 1 - t));
+    wait_tiles_ahead<DG::NI, DG::D>(min(DG::D - 1, w1 - 1 - t));
     TileRegs<DH, BP, G, false> tr;
     tr.load(myring + ((t - w0) % DG::D) * DG::SLOT, cv, bi, t * DG::TS, nullptr, len);
     process_tile<DH, BP, G, false>(st, tr, t * DG::TS, cm, qop, qsum, scale2);

@@ -61,6 +61,36 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
   return l ? (~0ull >> (64 - l)) : 0ull;
 }
 
+// ------------------------------------------------------- direct-to-LDS loads
+// LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+  return uint32_t(uintptr_t((const __attribute__((address_space(3))) void *)p));
+}
+
+// One wave-wide direct-to-LDS transfer (global_load_lds_dwordx4): each
+// active lane moves the 16 bytes at src to LDS address lds + 16 * lane.
+// It is issued from inline assembly so that the compiler does not wait for
+// every outstanding transfer before each later LDS read; the caller orders
+// the data with wait_vm counts of its own (vector-memory ops complete in
+// issue order, so a count that ignores other loads is conservative).
+__device__ __forceinline__ void dma16(const void *src, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off"
+      :
+      : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
+      : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(N) with the other counters left free (gfx9 encoding:
+// vmcnt[3:0] at bits 3:0, vmcnt[5:4] at bits 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // ------------------------------------------------------------ KV cache view
 // Bits of the physical store of width index bi (bi = 3 keeps the act dtype).
 __host__ __device__ inline int pool_bits(int bi, int act_bytes) {

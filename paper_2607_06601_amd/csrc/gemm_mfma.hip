@@ -45,6 +45,13 @@ __device__ __forceinline__ bool mmap_grouped(int bx, int BM, const int32_t *cnt,
   return false;
 }
 
+// Row tiles of all experts e = 1..E (the null expert 0 has no GEMM).
+__device__ __forceinline__ int grouped_row_tiles(int BM, const int32_t *cnt, int E) {
+  int n = 0;
+  for (int e = 1; e <= E; ++e) n += (cnt[e] + BM - 1) / BM;
+  return n;
+}
+
 // Physical column n of a BN-wide tile -> (pair index P in the tile, half).
 // Wave slice s = n / 64 holds pairs 32 s .. 32 s + 31: first halves in its
 // columns 0..31, second halves in 32..63.
@@ -54,12 +61,30 @@ __device__ __forceinline__ void col_pair(int n, int &P, int &half) {
 }
 
 // ---------------------------------------------------------------- problems
+// Each problem names its operand rows (a_row, b_row), the LDS column of an
+// accumulator after the register pass (EPI_ROPE / EPI_SWIGLU combine the
+// partner columns first), and a row-wise epilogue that reads the staged fp32
+// tile C (NC columns, row stride LDC) and writes 16-byte chunks.
+enum { EPI_PLAIN = 0, EPI_ROPE = 1, EPI_SWIGLU = 2 };
+
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
+
+__device__ __forceinline__ u32x4_t pack8_bf16(const float *v) {
+  u32x4_t w;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w[i] = uint32_t(f2bf(v[2 * i])) | (uint32_t(f2bf(v[2 * i + 1])) << 16);
+  return w;
+}
+
 struct QkvM {
+  static constexpr int EPI = EPI_ROPE;
   const bf16 *n1, *Wq, *Wk, *Wv;
   bf16 *q, *k, *v;
   const int32_t *pos_base, *pos_idx;
   int N, Tq, d, H, Hkv, dh, Ncols;
   double inv_freq[64];
+  static constexpr int out_cols(int BN) { return BN; }
+  __device__ int tiles(int BM, int ny) const { return (N + BM - 1) / BM * ny; }
   __device__ bool map(int bx, int by, int BM, int BN, MTile &t) const {
     t.m0 = bx * BM;
     t.n0 = by * BN;
@@ -67,15 +92,16 @@ struct QkvM {
     t.e = t.p0 = 0;
     return t.mvalid > 0;
   }
-  __device__ int logical_col(const MTile &t, int P, int half) const {
+  // logical column (within the tile) of half `half` of pair P
+  __device__ int ccol(int P, int half) const {
     const int hd = dh >> 1;
-    return t.n0 + (P / hd) * dh + (P % hd) + half * hd;
+    return (P / hd) * dh + (P % hd) + half * hd;
   }
   __device__ const bf16 *a_row(const MTile &t, int r) const { return n1 + int64_t(t.m0 + r) * d; }
   __device__ const bf16 *b_row(const MTile &t, int n) const {
     int P, half;
     col_pair(n, P, half);
-    int gc = logical_col(t, P, half);
+    int gc = t.n0 + ccol(P, half);
     if (gc >= Ncols) return nullptr;
     const int Hd = H * dh, Kd = Hkv * dh;
     if (gc < Hd) return Wq + int64_t(gc) * d;
@@ -83,48 +109,67 @@ struct QkvM {
     if (gc < Kd) return Wk + int64_t(gc) * d;
     return Wv + int64_t(gc - Kd) * d;
   }
-  // x1 / x2: first / second half of pair P for tile row r
-  __device__ void store_pair(const MTile &t, int r, int P, float x1, float x2) const {
-    if (r >= t.mvalid) return;
-    const int c1 = logical_col(t, P, 0);
-    if (c1 >= Ncols) return;
+  // item = (row, 8 consecutive pairs of one head): rotate-half RoPE on q and
+  // k with the angle taken in fp64 and reduced to [-pi, pi] before an fp32
+  // sincos; v is copied.
+  template <int BM, int NC, int LDC>
+  __device__ void epilogue(const MTile &t, const float *C, int tid) const {
+    constexpr int PC = NC / 16;  // 8-pair chunks per row
     const int Hd = H * dh, Kd = Hkv * dh, hd = dh >> 1;
-    const int row = t.m0 + r;
-    bf16 *out;
-    int ld, col;
-    bool rot = true;
-    if (c1 < Hd) {
-      out = q; ld = Hd; col = c1;
-    } else if (c1 < Hd + Kd) {
-      out = k; ld = Kd; col = c1 - Hd;
-    } else {
-      out = v; ld = Kd; col = c1 - Hd - Kd; rot = false;
+    for (int it = tid; it < BM * PC; it += 512) {
+      const int r = it / PC, P0 = (it % PC) * 8;
+      const int lc1 = (P0 / hd) * dh + (P0 % hd);
+      const int c1 = t.n0 + lc1;
+      if (r >= t.mvalid || c1 >= Ncols) continue;
+      const int row = t.m0 + r;
+      bf16 *out;
+      int ld, col;
+      bool rot = true;
+      if (c1 < Hd) {
+        out = q; ld = Hd; col = c1;
+      } else if (c1 < Hd + Kd) {
+        out = k; ld = Kd; col = c1 - Hd;
+      } else {
+        out = v; ld = Kd; col = c1 - Hd - Kd; rot = false;
+      }
+      float y1[8], y2[8];
+      const float *x1 = C + r * LDC + lc1, *x2 = x1 + hd;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        y1[u] = x1[u];
+        y2[u] = x2[u];
+      }
+      if (rot) {
+        const int b = row / Tq, tt = row - b * Tq;
+        const int pos = (pos_base ? pos_base[pos_idx ? pos_idx[b] : b] : 0) + tt;
+        const int j0 = col % hd;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const double ang = double(pos) * inv_freq[j0 + u];
+          const double kq = rint(ang * 0.15915494309189535);
+          double rr = fma(-kq, 6.283185307179586, ang);
+          rr = fma(-kq, 2.4492935982947064e-16, rr);
+          float sn, cs;
+          sincosf(float(rr), &sn, &cs);
+          const float a1 = y1[u], a2 = y2[u];
+          y1[u] = a1 * cs - a2 * sn;
+          y2[u] = a1 * sn + a2 * cs;
+        }
+      }
+      bf16 *o = out + int64_t(row) * ld + col;
+      *(u32x4_t *)o = pack8_bf16(y1);
+      *(u32x4_t *)(o + hd) = pack8_bf16(y2);
     }
-    float y1 = x1, y2 = x2;
-    if (rot) {
-      const int jj = col % hd;
-      const int b = row / Tq, tt = row - b * Tq;
-      const int pos = (pos_base ? pos_base[pos_idx ? pos_idx[b] : b] : 0) + tt;
-      // angle in fp64, reduced to [-pi, pi], then an accurate fp32 sincos
-      const double ang = double(pos) * inv_freq[jj];
-      const double kq = rint(ang * 0.15915494309189535);
-      double rr = fma(-kq, 6.283185307179586, ang);
-      rr = fma(-kq, 2.4492935982947064e-16, rr);
-      float sn, cs;
-      sincosf(float(rr), &sn, &cs);
-      y1 = x1 * cs - x2 * sn;
-      y2 = x1 * sn + x2 * cs;
-    }
-    bf16 *o = out + int64_t(row) * ld + col;
-    o[0] = f2bf(y1);
-    o[hd] = f2bf(y2);
   }
 };
 
 struct OprojM {
+  static constexpr int EPI = EPI_PLAIN;
   const bf16 *o, *Wo, *x;
   bf16 *xt;
   int N, d, K;
+  static constexpr int out_cols(int BN) { return BN; }
+  __device__ int tiles(int BM, int ny) const { return (N + BM - 1) / BM * ny; }
   __device__ bool map(int bx, int by, int BM, int BN, MTile &t) const {
     t.m0 = bx * BM;
     t.n0 = by * BN;
@@ -136,23 +181,40 @@ struct OprojM {
   __device__ const bf16 *b_row(const MTile &t, int n) const {
     return t.n0 + n < d ? Wo + int64_t(t.n0 + n) * K : nullptr;
   }
-  __device__ void store(const MTile &t, int r, int n, float acc) const {
-    if (r >= t.mvalid || t.n0 + n >= d) return;
-    const int64_t off = int64_t(t.m0 + r) * d + t.n0 + n;
-    xt[off] = f2bf(bf2f(x[off]) + acc);
+  // item = 8 columns of one row: xt = x + o Wo^T
+  template <int BM, int NC, int LDC>
+  __device__ void epilogue(const MTile &t, const float *C, int tid) const {
+    constexpr int CC = NC / 8;
+    for (int it = tid; it < BM * CC; it += 512) {
+      const int r = it / CC, c8 = (it % CC) * 8;
+      if (r >= t.mvalid || t.n0 + c8 >= d) continue;
+      const int64_t off = int64_t(t.m0 + r) * d + t.n0 + c8;
+      const u32x4_t xv = *(const u32x4_t *)(x + off);
+      float y[8];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        y[2 * u] = __uint_as_float(xv[u] << 16) + C[r * LDC + c8 + 2 * u];
+        y[2 * u + 1] = __uint_as_float(xv[u] & 0xFFFF0000u) + C[r * LDC + c8 + 2 * u + 1];
+      }
+      *(u32x4_t *)(xt + off) = pack8_bf16(y);
+    }
   }
 };
 
 struct Moe1M {
+  static constexpr int EPI = EPI_SWIGLU;
   const bf16 *n2, *Wg, *Wu;
   bf16 *Hm;
   const int32_t *cnt, *off, *rows;
   int E, k, d, dff;
+  static constexpr int out_cols(int BN) { return BN / 2; }
+  __device__ int tiles(int BM, int ny) const { return grouped_row_tiles(BM, cnt, E) * ny; }
   __device__ bool map(int bx, int by, int BM, int BN, MTile &t) const {
     if (!mmap_grouped(bx, BM, cnt, off, E, t)) return false;
     t.n0 = by * (BN / 2);  // BN/2 expert units per tile (gate + up columns)
     return true;
   }
+  __device__ int ccol(int P, int) const { return P; }
   __device__ const bf16 *a_row(const MTile &t, int r) const {
     return n2 + int64_t(rows[t.p0 + r] / k) * d;
   }
@@ -163,19 +225,26 @@ struct Moe1M {
     if (f >= dff) return nullptr;
     return (half ? Wu : Wg) + (int64_t(t.e - 1) * dff + f) * d;
   }
-  __device__ void store_pair(const MTile &t, int r, int P, float g, float u) const {
-    const int f = t.n0 + P;
-    if (r >= t.mvalid || f >= dff) return;
-    const float s = g / (1.0f + expf(-g));
-    Hm[int64_t(t.p0 + r) * dff + f] = f2bf(s * u);
+  // item = 8 expert units of one assignment row (C holds silu(g) u)
+  template <int BM, int NC, int LDC>
+  __device__ void epilogue(const MTile &t, const float *C, int tid) const {
+    constexpr int CC = NC / 8;
+    for (int it = tid; it < BM * CC; it += 512) {
+      const int r = it / CC, c8 = (it % CC) * 8;
+      if (r >= t.mvalid || t.n0 + c8 >= dff) continue;
+      *(u32x4_t *)(Hm + int64_t(t.p0 + r) * dff + t.n0 + c8) = pack8_bf16(C + r * LDC + c8);
+    }
   }
 };
 
 struct Moe2M {
+  static constexpr int EPI = EPI_PLAIN;
   const bf16 *Hm, *Wd;
   float *Y;
   const int32_t *cnt, *off, *rows;
   int E, d, dff;
+  static constexpr int out_cols(int BN) { return BN; }
+  __device__ int tiles(int BM, int ny) const { return grouped_row_tiles(BM, cnt, E) * ny; }
   __device__ bool map(int bx, int by, int BM, int BN, MTile &t) const {
     if (!mmap_grouped(bx, BM, cnt, off, E, t)) return false;
     t.n0 = by * BN;
@@ -185,60 +254,74 @@ struct Moe2M {
   __device__ const bf16 *b_row(const MTile &t, int n) const {
     return t.n0 + n < d ? Wd + (int64_t(t.e - 1) * d + t.n0 + n) * dff : nullptr;
   }
-  __device__ void store(const MTile &t, int r, int n, float acc) const {
-    if (r >= t.mvalid || t.n0 + n >= d) return;
-    Y[int64_t(rows[t.p0 + r]) * d + t.n0 + n] = acc;
+  // item = 8 output features of one assignment, scattered to its slot row
+  template <int BM, int NC, int LDC>
+  __device__ void epilogue(const MTile &t, const float *C, int tid) const {
+    constexpr int CC = NC / 8;
+    for (int it = tid; it < BM * CC; it += 512) {
+      const int r = it / CC, c8 = (it % CC) * 8;
+      if (r >= t.mvalid || t.n0 + c8 >= d) continue;
+      float *y = Y + int64_t(rows[t.p0 + r]) * d + t.n0 + c8;
+      const float *c = C + r * LDC + c8;
+      *(float4 *)y = make_float4(c[0], c[1], c[2], c[3]);
+      *(float4 *)(y + 4) = make_float4(c[4], c[5], c[6], c[7]);
+    }
   }
 };
 
-template <class P> struct IsPaired { static constexpr bool value = false; };
-template <> struct IsPaired<QkvM> { static constexpr bool value = true; };
-template <> struct IsPaired<Moe1M> { static constexpr bool value = true; };
-
 // ------------------------------------------------------------------ kernel
-template <class P, int BM, int WM, int WN>
-__global__ __launch_bounds__(512, 1) void gemm_mfma_kernel(P p, int K) {
+// Tiles of the whole problem are handed out XCD by XCD: blocks are issued to
+// the 8 XCDs round-robin, so block L runs on XCD L % 8, and it takes tile
+// number (its XCD's contiguous share) + L / 8.  Tile t covers row tile t / ny
+// and column tile t % ny, so the blocks resident on one XCD share A rows and
+// a few weight tiles in that XCD's L2.
+__device__ __forceinline__ int xcd_tile(int L, int total) {
+  const int per = total >> 3, extra = total & 7, x = L & 7;
+  return x * per + min(x, extra) + (L >> 3);
+}
+
+template <class P, int BM, int WM, int WN, int S>
+__global__ __launch_bounds__(512, 1) void gemm_mfma_kernel(P p, int K, int ny) {
   constexpr int BN = 64 * WN;
-  constexpr int TM = BM / WM;      // wave rows
-  constexpr int MI = TM / 16;      // 16-row MFMA tiles per wave
-  constexpr int LA = BM / 64;      // A chunks per thread per stage
-  constexpr int LB = BN / 64;      // B chunks per thread per stage
-  constexpr int ABYTES = BM * 128, BBYTES = BN * 128, STAGE = ABYTES + BBYTES;
-  __shared__ __align__(16) uint8_t smem[2 * STAGE];
+  constexpr int TM = BM / WM;       // wave rows
+  constexpr int MI = TM / 16;       // 16-row MFMA tiles per wave
+  constexpr int STAGE = (BM + BN) * 128;
+  constexpr int IPW = (BM + BN) / 64;  // 1 KB transfers per wave per stage
+  static_assert(WM * WN == 8 && (BM + BN) % 64 == 0, "8 waves, whole transfers");
+  constexpr int NC = P::out_cols(BN), LDC = NC + 16;  // staged output tile (fp32)
+  constexpr int SMEM = S * STAGE > BM * LDC * 4 ? S * STAGE : BM * LDC * 4;
+  __shared__ __align__(1024) uint8_t smem[SMEM];
+  const int total = p.tiles(BM, ny);
+  if (int(blockIdx.x) >= total) return;
+  const int t = xcd_tile(blockIdx.x, total);
   MTile tc;
-  if (!p.map(blockIdx.x, blockIdx.y, BM, BN, tc)) return;
+  if (!p.map(t / ny, t % ny, BM, BN, tc)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int lr = tid >> 3, lc = tid & 7;
-  const bf16 *ap[LA], *bq[LB];
+  // Transfer j of this wave fills stage rows 8 g .. 8 g + 7 (g = wave IPW + j;
+  // A rows first, then B rows).  Lane l writes LDS chunk l % 8 of row
+  // 8 g + l / 8, which holds source chunk (l % 8) ^ (row & 7).  Rows past the
+  // valid rows (or past the weight's columns) read a valid row instead: their
+  // products land in accumulator rows/columns the epilogue never stores.
+  const uint8_t *src[IPW];
+  const bf16 *b_fallback = p.b_row(tc, 0);
 #pragma unroll
-  for (int i = 0; i < LA; ++i) {
-    const int r = lr + 64 * i;
-    ap[i] = r < tc.mvalid ? p.a_row(tc, r) : nullptr;
+  for (int j = 0; j < IPW; ++j) {
+    const int rr = 8 * (wave * IPW + j) + (lane >> 3);
+    const int c = (lane & 7) ^ (rr & 7);
+    const bf16 *row;
+    if (rr < BM) {
+      row = p.a_row(tc, rr < tc.mvalid ? rr : 0);
+    } else {
+      row = p.b_row(tc, rr - BM);
+      if (!row) row = b_fallback;
+    }
+    src[j] = (const uint8_t *)row + c * 16;
   }
+  const uint32_t sbase = lds_addr(smem) + wave * IPW * 1024;
+  auto issue = [&](int kt, int stage) {
 #pragma unroll
-  for (int i = 0; i < LB; ++i) bq[i] = p.b_row(tc, lr + 64 * i);
-  uint4 ra[LA], rb[LB];
-  const uint4 zero = make_uint4(0, 0, 0, 0);
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < LA; ++i) ra[i] = ap[i] ? *(const uint4 *)(ap[i] + k0 + lc * 8) : zero;
-#pragma unroll
-    for (int i = 0; i < LB; ++i) rb[i] = bq[i] ? *(const uint4 *)(bq[i] + k0 + lc * 8) : zero;
-  };
-  auto sstore = [&](int buf) {
-    uint8_t *As = smem + buf * STAGE;
-    uint8_t *Bs = As + ABYTES;
-#pragma unroll
-    for (int i = 0; i < LA; ++i) {
-      const int r = lr + 64 * i;
-      *(uint4 *)(As + r * 128 + ((lc ^ (r & 7)) << 4)) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < LB; ++i) {
-      const int r = lr + 64 * i;
-      *(uint4 *)(Bs + r * 128 + ((lc ^ (r & 7)) << 4)) = rb[i];
-    }
+    for (int j = 0; j < IPW; ++j) dma16(src[j] + kt * 128, sbase + stage * STAGE + j * 1024);
   };
   f32x4_t acc[MI][4];
 #pragma unroll
@@ -246,13 +329,20 @@ __global__ __launch_bounds__(512, 1) void gemm_mfma_kernel(P p, int K) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   const int nk = K / 64;
-  gload(0);
-  sstore(0);
-  __syncthreads();
+#pragma unroll
+  for (int s0 = 0; s0 < S - 1; ++s0)
+    if (s0 < nk) issue(s0, s0);
   for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload((kt + 1) * 64);
-    const uint8_t *As = smem + (kt & 1) * STAGE;
-    const uint8_t *Bs = As + ABYTES;
+    // stage kt has landed once at most the later stages' transfers are out
+    if constexpr (S >= 3) {
+      if (kt + 1 < nk) wait_vm<IPW>(); else wait_vm<0>();
+    } else {
+      wait_vm<0>();
+    }
+    __syncthreads();  // every wave's part of stage kt is in; stage kt-1 is free
+    if (kt + S - 1 < nk) issue(kt + S - 1, (kt + S - 1) % S);
+    const uint8_t *As = smem + (kt % S) * STAGE;
+    const uint8_t *Bs = As + BM * 128;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       const int ch = ks * 4 + (lane >> 4);
@@ -271,35 +361,46 @@ __global__ __launch_bounds__(512, 1) void gemm_mfma_kernel(P p, int K) {
           acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[ni], acc[mi][ni], 0, 0, 0);
       }
     }
-    if (kt + 1 < nk) sstore((kt + 1) & 1);
-    __syncthreads();
   }
-  // epilogue from registers: lane holds rows 4 (lane/16) + i of each 16-row
-  // tile, column (lane % 16) of each 16-column block
+  // Epilogue.  Register pass: lane holds rows 4 (lane/16) + i of each 16-row
+  // tile and column (lane % 16) of each 16-column block; partner columns
+  // (ni, ni + 2) are combined for SwiGLU and kept apart for RoPE.  Then the
+  // problem's row-wise pass reads the staged tile.
+  __syncthreads();  // every wave is done with the operand stages
+  float *C = (float *)smem;
 #pragma unroll
   for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = wm * TM + mi * 16 + 4 * (lane >> 4) + i;
-      if constexpr (IsPaired<P>::value) {
+      if constexpr (P::EPI == EPI_PLAIN) {
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni) C[r * LDC + wn * 64 + ni * 16 + (lane & 15)] = acc[mi][ni][i];
+      } else {
 #pragma unroll
         for (int ni = 0; ni < 2; ++ni) {
           const int Pp = wn * 32 + ni * 16 + (lane & 15);
-          p.store_pair(tc, r, Pp, acc[mi][ni][i], acc[mi][ni + 2][i]);
+          const float g = acc[mi][ni][i], u = acc[mi][ni + 2][i];
+          if constexpr (P::EPI == EPI_SWIGLU) {
+            C[r * LDC + Pp] = g / (1.0f + expf(-g)) * u;
+          } else {
+            C[r * LDC + p.ccol(Pp, 0)] = g;
+            C[r * LDC + p.ccol(Pp, 1)] = u;
+          }
         }
-      } else {
-#pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
-          p.store(tc, r, wn * 64 + ni * 16 + (lane & 15), acc[mi][ni][i]);
       }
     }
+  __syncthreads();
+  p.template epilogue<BM, NC, LDC>(tc, C, tid);
 }
 
 // ------------------------------------------------------------------ launchers
-template <class P, int BM, int WM, int WN>
+// m_tiles bounds the row tiles (for grouped problems: the most any routing
+// can need); the kernel takes the actual count from the problem.
+template <class P, int BM, int WM, int WN, int S>
 static hipError_t launch(const P &p, int K, int m_tiles, int n_tiles, hipStream_t st) {
   if (m_tiles > 0 && n_tiles > 0)
-    gemm_mfma_kernel<P, BM, WM, WN><<<dim3(m_tiles, n_tiles), 512, 0, st>>>(p, K);
+    gemm_mfma_kernel<P, BM, WM, WN, S><<<m_tiles * n_tiles, 512, 0, st>>>(p, K, n_tiles);
   return hipGetLastError();
 }
 
@@ -327,7 +428,7 @@ hipError_t mfma_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
     p.inv_freq[j] = j < cfg.head_dim / 2
                         ? pow(double(cfg.rope_theta), -2.0 * j / double(cfg.head_dim))
                         : 0.0;
-  return launch<QkvM, 256, 4, 2>(p, cfg.d_model, (p.N + 255) / 256, (p.Ncols + 127) / 128, st);
+  return launch<QkvM, 256, 4, 2, 3>(p, cfg.d_model, (p.N + 255) / 256, (p.Ncols + 127) / 128, st);
 }
 
 hipError_t mfma_oproj(const triroute_cfg &cfg, int N, const void *x, const void *o,
@@ -340,7 +441,7 @@ hipError_t mfma_oproj(const triroute_cfg &cfg, int N, const void *x, const void 
   p.N = N;
   p.d = cfg.d_model;
   p.K = cfg.n_heads * cfg.head_dim;
-  return launch<OprojM, 256, 4, 2>(p, p.K, (N + 255) / 256, (p.d + 127) / 128, st);
+  return launch<OprojM, 256, 4, 2, 3>(p, p.K, (N + 255) / 256, (p.d + 127) / 128, st);
 }
 
 hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const triroute_moe_w &w,
@@ -359,7 +460,7 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
   p1.k = k;
   p1.d = d;
   p1.dff = dff;
-  hipError_t err = launch<Moe1M, 256, 2, 4>(p1, d, Nk / 256 + E, (dff + 127) / 128, st);
+  hipError_t err = launch<Moe1M, 256, 2, 4, 2>(p1, d, Nk / 256 + E, (dff + 127) / 128, st);
   if (err != hipSuccess) return err;
   Moe2M p2;
   p2.Hm = (const bf16 *)Hm;
@@ -371,7 +472,7 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
   p2.E = E;
   p2.d = d;
   p2.dff = dff;
-  return launch<Moe2M, 256, 4, 2>(p2, dff, Nk / 256 + E, (d + 127) / 128, st);
+  return launch<Moe2M, 256, 4, 2, 3>(p2, dff, Nk / 256 + E, (d + 127) / 128, st);
 }
 
 }  // namespace tr

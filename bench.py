@@ -6,7 +6,9 @@ combine) of the 160M-class workload: batch 8 x 2048 tokens, d 768, 12 x 64
 heads (3 kv heads), window 128, 8 SwiGLU experts (d_ff 2048) + null, top-2,
 KV group 64, bf16, seeded synthetic inputs and random-init weights.  Inputs
 are resident in HBM before timing; every step writes a fresh cache; the
-L2 / Infinity Cache is flushed (1 GiB write) before each timed step.
+L2 / Infinity Cache is flushed before each timed step by reading a 1 GiB
+buffer (a read, so that no dirty lines are left whose write-back would land
+in the timed region).
 
 Also reported: the MoE sublayer's achieved bf16 MFMA rate (roofline), the
 410M-class decode step (64 sequences x 8192 context) and its decode
@@ -38,9 +40,25 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true")
-    p.add_argument("--only", choices=("prefill", "decode"), default=None,
-                   help="profile one workload alone (prints its section only)")
+    p.add_argument("--only", choices=("prefill", "decode", "moe"), default=None,
+                   help="profile one workload alone (prints its section only); 'moe' times "
+                        "the MoE sublayer and then runs a 256 MiB copy for counter calibration")
+    p.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "KERNEL_REGEX"),
+                   default=None,
+                   help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; csv output) "
+                        "into per-launch HBM bytes of the kernels matching KERNEL_REGEX, "
+                        "scaled by the 256 MiB copy in the same runs")
     return p.parse_args()
+
+
+class CacheFlush:
+    """Evicts L2 and the Infinity Cache by reading a 1 GiB buffer."""
+
+    def __init__(self, torch, dev):
+        self.buf = torch.ones(1 << 28, dtype=torch.int32, device=dev)
+
+    def __call__(self):
+        self.buf.sum()
 
 
 def events(torch):
@@ -53,6 +71,9 @@ def main():
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the routed layer is "
               "measured on a single MI355X in this build", file=sys.stderr)
         sys.exit(2)
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc)
+        return
     import numpy as np
     import torch
 
@@ -65,9 +86,10 @@ def main():
     dev = "cuda"
     stream = torch.cuda.current_stream()
     if args.only == "decode":
-        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        print(json.dumps({"decode": bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev,
-                                                 flush)}), flush=True)
+        flush = CacheFlush(torch, dev)
+        res = bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush)
+        copy_calibration(torch)
+        print(json.dumps({"decode": res}), flush=True)
         return
 
     # ------------------------------------------------------------ prefill
@@ -79,7 +101,7 @@ def main():
     c = D.cfg
     ws = tr.workspace(c, tr.OP_LAYER_PREFILL, B, T)
     xo = torch.empty(N, d, dtype=D.act, device=dev)
-    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    flush = CacheFlush(torch, dev)
     caches = [tr.KVCache(c, B, T) for _ in range(args.steps)]
     warm = tr.KVCache(c, B, T)
     eidx_t = torch.empty(N, k, dtype=torch.int32, device=dev)
@@ -95,7 +117,7 @@ def main():
     times = []
     t_wall0 = time.perf_counter()
     for i in range(args.steps):
-        flush.fill_(i & 0xFF)
+        flush()
         e0, e1 = events(torch)
         e0.record(stream)
         tr.layer_prefill(c, B, T, D.x, D.psi, D.rw, D.dw, D.mw, caches[i], xo, ws, taps=taps)
@@ -108,38 +130,11 @@ def main():
     for cc in caches:
         assert cc.status() == 0
 
-    # MoE sublayer alone on the same routed inputs: achieved MFMA rate
-    eidx_h = eidx_t.cpu().numpy()
-    n_real = int((eidx_h != 0).sum())
-    moe_flops = 6.0 * d * dff * n_real
-    cmp = tr.CompactionBuffers(c, B, T)
-    rw_ws = tr.workspace(c, tr.OP_ROUTER, B, T)
-    n1 = torch.empty(N, d, dtype=D.act, device=dev)
-    mode = torch.empty(N, H, dtype=torch.uint8, device=dev)
-    bit = torch.empty(N, dtype=torch.uint8, device=dev)
-    tr.router(c, B, T, D.x, D.psi, D.rw, n1, mode, bit, eidx_t, egate_t, cmp.struct, rw_ws)
-    moe_ws = tr.workspace(c, tr.OP_MOE, N, 1)
-    for _ in range(3):
-        tr.moe(c, N, xt_t, D.dw, D.mw, eidx_t, egate_t, cmp.struct, xo, moe_ws)
-    moe_ms = []
-    for i in range(args.steps):
-        flush.fill_(i & 0xFF)
-        e0, e1 = events(torch)
-        e0.record(stream)
-        tr.moe(c, N, xt_t, D.dw, D.mw, eidx_t, egate_t, cmp.struct, xo, moe_ws)
-        e1.record(stream)
-        moe_ms.append((e0, e1))
-    torch.cuda.synchronize()
-    moe_avg = float(np.mean([a.elapsed_time(b) for a, b in moe_ms]))
-    moe_tflops = moe_flops / (moe_avg * 1e-3) / 1e12
-    roofline = {"kernel": "triroute_moe (rmsnorm2, grouped GEMM gate/up + SwiGLU, grouped GEMM "
-                          "down, combine)",
-                "bound": "mfma", "achieved": round(moe_tflops, 2),
-                "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(moe_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
-                "algorithmic": f"6*d*d_ff FLOP x {n_real} real assignments = "
-                               f"{moe_flops / 1e9:.1f} GFLOP per launch",
-                "avg_ms": round(moe_avg, 4)}
+    roofline = bench_moe(args, torch, np, tr, D, c, B, T, flush, eidx_t, egate_t, xt_t, xo)
+    if args.only == "moe":
+        copy_calibration(torch)
+        print(json.dumps({"moe": roofline}), flush=True)
+        return
 
     out = {
         "metric": "routed-layer tokens/s (prefill, decode); decode-attn HBM GB/s; MoE MFMA util",
@@ -156,7 +151,7 @@ def main():
         "roofline": roofline,
         "timing": {"per_step_ms_min": round(min(step_ms), 4),
                    "per_step_ms_max": round(max(step_ms), 4),
-                   "wall_s_timed_loop": round(wall, 3), "cache_flush_per_step": "1 GiB write"},
+                   "wall_s_timed_loop": round(wall, 3), "cache_flush_per_step": "1 GiB read"},
     }
 
     # ------------------------------------------------------------- decode
@@ -167,6 +162,96 @@ def main():
     if not args.no_cpu_baseline and args.only is None:
         out["cpu_baseline"] = cpu_baseline(np)
     print(json.dumps(out), flush=True)
+
+
+def source_digest(*names):
+    """sha256 over kernel sources (package csrc/), to tell whether stored
+    counter readings still describe the kernels as built."""
+    import hashlib
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2607_06601_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+MOE_SOURCES = ("gemm_mfma.hip", "misc.hip", "common.hpp", "kernels.hpp", "api.cpp")
+DECODE_ATTN_SOURCES = ("attn_mfma.hip", "common.hpp", "kernels.hpp", "api.cpp")
+
+
+def stored_traffic(name, sources):
+    """HBM bytes per launch from a committed counter summary under profiles/
+    (FETCH_SIZE + WRITE_SIZE, scaled by the plain-copy calibration), or None
+    when it is missing or was taken from other kernel sources."""
+    path = os.path.join(ROOT, "profiles", name)
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_digest") != source_digest(*sources):
+        return None
+    try:
+        return int(float(kv["hbm_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
+
+
+def bench_moe(args, torch, np, tr, D, c, B, T, flush, eidx_t, egate_t, xt_t, xo):
+    """The MoE sublayer (triroute_moe: rmsnorm2, grouped GEMM gate/up + SwiGLU,
+    grouped GEMM down, combine) alone on the routed inputs of the last prefill
+    step: achieved bf16 MFMA rate of the expert FLOPs."""
+    dev = "cuda"
+    stream = torch.cuda.current_stream()
+    d, dff = c.d_model, c.d_ff
+    N = B * T
+    eidx_h = eidx_t.cpu().numpy()
+    n_real = int((eidx_h != 0).sum())
+    moe_flops = 6.0 * d * dff * n_real
+    cmp = tr.CompactionBuffers(c, B, T)
+    rw_ws = tr.workspace(c, tr.OP_ROUTER, B, T)
+    n1 = torch.empty(N, d, dtype=D.act, device=dev)
+    mode = torch.empty(N, c.n_heads, dtype=torch.uint8, device=dev)
+    bit = torch.empty(N, dtype=torch.uint8, device=dev)
+    tr.router(c, B, T, D.x, D.psi, D.rw, n1, mode, bit, eidx_t, egate_t, cmp.struct, rw_ws)
+    moe_ws = tr.workspace(c, tr.OP_MOE, N, 1)
+    for _ in range(3):
+        tr.moe(c, N, xt_t, D.dw, D.mw, eidx_t, egate_t, cmp.struct, xo, moe_ws)
+    moe_ms = []
+    for i in range(args.steps):
+        flush()
+        e0, e1 = events(torch)
+        e0.record(stream)
+        tr.moe(c, N, xt_t, D.dw, D.mw, eidx_t, egate_t, cmp.struct, xo, moe_ws)
+        e1.record(stream)
+        moe_ms.append((e0, e1))
+    torch.cuda.synchronize()
+    moe_avg = float(np.mean([a.elapsed_time(b) for a, b in moe_ms]))
+    moe_tflops = moe_flops / (moe_avg * 1e-3) / 1e12
+    return {"kernel": "triroute_moe (rmsnorm2, grouped GEMM gate/up + SwiGLU, grouped GEMM "
+                      "down, combine)",
+            "bound": "mfma", "achieved": round(moe_tflops, 2),
+            "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(moe_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+            "traffic": stored_traffic("moe_160m_prefill_traffic.txt", MOE_SOURCES),
+            "algorithmic": f"6*d*d_ff FLOP x {n_real} real assignments = "
+                           f"{moe_flops / 1e9:.1f} GFLOP per launch",
+            "avg_ms": round(moe_avg, 4)}
+
+
+def copy_calibration(torch):
+    """A plain device copy of 256 MiB: the reference reading for the FETCH_SIZE
+    / WRITE_SIZE counters (kernel name contains 'copy' or 'elementwise')."""
+    n = 256 << 20
+    src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    return n
 
 
 def decode_attn_bytes(cfg, mode, bits_per_seq):
@@ -220,7 +305,7 @@ def bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush):
         tr.layer_decode(c, B, D.x, D.psi, D.rw, D.dw, D.mw, cache, xo, ws, taps=taps)
     times = []
     for i in range(args.steps):
-        flush.fill_(i & 0xFF)
+        flush()
         e0, e1 = events(torch)
         e0.record(stream)
         tr.layer_decode(c, B, D.x, D.psi, D.rw, D.dw, D.mw, cache, xo, ws, taps=taps)
@@ -243,7 +328,7 @@ def bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush):
         tr.attn_decode(c, B, q_t, cache, mode_t, o, aws)
     at = []
     for i in range(args.steps):
-        flush.fill_(i & 0xFF)
+        flush()
         e0, e1 = events(torch)
         e0.record(stream)
         tr.attn_decode(c, B, q_t, cache, mode_t, o, aws)
@@ -259,7 +344,53 @@ def bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush):
             "attn": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                      "algorithmic_bytes": int(nbytes), "avg_ms": round(attn_ms, 4),
-                     "traffic": None}}
+                     "traffic": stored_traffic("attn_decode_410m_traffic.txt",
+                                                DECODE_ATTN_SOURCES)}}
+
+
+def summarize_pmc(fetch_dir, write_dir, regex):
+    """Per-launch HBM bytes of the kernels matching `regex` from two rocprofv3
+    counter runs, each scaled by what the same counter reads for the 256 MiB
+    copy of copy_calibration() (the copy reads and writes 256 MiB)."""
+    import csv
+    import glob
+    import re
+
+    pat = re.compile(regex)
+
+    def read(d, counter):
+        rows = []
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(f) as fh:
+                for r in csv.DictReader(fh):
+                    if r.get("Counter_Name") == counter:
+                        rows.append((r["Kernel_Name"], int(r.get("Dispatch_Id", 0)),
+                                     float(r["Counter_Value"])))
+        return rows
+
+    out = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = read(d, counter)
+        copy = [v for n, _, v in rows if ("copy" in n.lower() or "elementwise" in n.lower())
+                and v > 0.5 * (256 << 10)]
+        ref = (256 << 10) / max(copy) if copy else float("nan")
+        per_kernel = {}
+        for n, _, v in rows:
+            if pat.search(n):
+                per_kernel.setdefault(n, []).append(v)
+        out[counter] = (ref, {n: sum(v) / len(v) for n, v in per_kernel.items()},
+                        {n: len(v) for n, v in per_kernel.items()})
+    fr, fk, fc = out["FETCH_SIZE"]
+    wr, wk, _ = out["WRITE_SIZE"]
+    total = 0.0
+    print(f"calibration: copy of 256 MiB reads FETCH x {fr:.4f}, WRITE x {wr:.4f}")
+    for n in sorted(fk):
+        fb = fk[n] * fr * 1024
+        wb = wk.get(n, 0.0) * wr * 1024
+        total += fb + wb
+        print(f"kernel: {n[:100]} | dispatches {fc[n]} | FETCH_SIZE {fk[n]:.0f} KiB | "
+              f"WRITE_SIZE {wk.get(n, 0.0):.0f} KiB | HBM bytes {fb + wb:.0f}")
+    print(f"hbm_bytes_per_launch: {total:.0f}")
 
 
 def cpu_baseline(np):

@@ -22,7 +22,10 @@
  *     no pointer past a call.  Calls are asynchronous on the given stream and
  *     never synchronise it, except triroute_kv_status().
  *   - Tensors are row-major and contiguous.  A batch of B sequences of T
- *     tokens is flattened as token i = b*T + t.
+ *     tokens is flattened as token i = b*T + t.  Every activation tensor and
+ *     weight (everything but index / decision arrays and psi) must be 16-byte
+ *     aligned: the kernels move 16-byte pieces.  A misaligned pointer is
+ *     rejected with TRIROUTE_E_INVALID.
  *   - "act" tensors have the activation dtype of cfg->act: IEEE fp32, or
  *     bf16 (16-bit storage, round-to-nearest-even on every write).
  *   - Enumerations: attention mode 0 skip, 1 local, 2 full; bit index 0..3

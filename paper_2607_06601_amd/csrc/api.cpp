@@ -10,6 +10,8 @@
 
 #include <mutex>
 
+#include <initializer_list>
+
 #include "kernels.hpp"
 
 namespace {
@@ -83,7 +85,9 @@ struct RouterWs {
 RouterWs carve_router(Carve &cv, const triroute_cfg &c, int N) {
   RouterWs w;
   w.rinv = cv.take<float>(N);
-  w.u = cv.take<float>(size_t(N) * 128);
+  int ks, kchunk;
+  tr::router_split(N, c.d_model + c.d_psi, ks, kchunk);
+  w.u = cv.take<float>(size_t(ks) * N * 128);
   w.hist = cv.take<int32_t>(tr::compact_hist_ints(N, c.top_k, c.n_experts + 1));
   return w;
 }
@@ -182,6 +186,16 @@ int check_cfg(const triroute_cfg *c) {
           "router head count 3H + E + 5 > 112");
   REQUIRE(c->d_model % 64 == 0 && c->d_ff % 64 == 0, TRIROUTE_E_UNSUPPORTED,
           "d_model and d_ff must be multiples of 64");
+  return TRIROUTE_OK;
+}
+
+// Every tensor the kernels read or write in 16-byte pieces must be 16-byte
+// aligned (NULL entries are skipped: optional arguments are checked where
+// they are required).
+int check_aligned(std::initializer_list<const void *> ptrs) {
+  for (const void *p : ptrs)
+    REQUIRE((uintptr_t(p) & 15) == 0, TRIROUTE_E_INVALID,
+            "tensor pointer %p is not 16-byte aligned", p);
   return TRIROUTE_OK;
 }
 
@@ -381,6 +395,7 @@ int triroute_kv_append(const triroute_cfg *cfg, const triroute_kv_cache *cache, 
   TRY(check_bt(B, T));
   TRY(check_cache(*cfg, cache, B, T));
   REQUIRE(k && v && bit, TRIROUTE_E_INVALID, "k, v or bit is NULL");
+  TRY(check_aligned({k, v}));
   TRY(check_ws(*cfg, TRIROUTE_OP_KV_APPEND, B, T, ws, ws_bytes));
   Carve cv(ws);
   int32_t *slots = carve_kv(cv, B * T);
@@ -419,6 +434,7 @@ int triroute_router(const triroute_cfg *cfg, int B, int T, const void *x, const 
           TRIROUTE_E_INVALID, "NULL router weight");
   REQUIRE(cmp->attn_cnt && cmp->attn_idx && cmp->exp_cnt && cmp->exp_off && cmp->exp_rows,
           TRIROUTE_E_INVALID, "NULL compaction array");
+  TRY(check_aligned({x, n1, w->g1, w->W1, w->W2, w->Wa, w->We, w->Wb}));
   TRY(check_ws(*cfg, TRIROUTE_OP_ROUTER, B, T, ws, ws_bytes));
   TRY(prepare_once());
   Carve cv(ws);
@@ -435,6 +451,7 @@ int triroute_qkv(const triroute_cfg *cfg, int B, int T, const void *n1, const tr
   TRY(check_cfg(cfg));
   TRY(check_bt(B, T));
   REQUIRE(n1 && w && w->Wq && w->Wk && w->Wv && q && k && v, TRIROUTE_E_INVALID, "NULL argument");
+  TRY(check_aligned({n1, w->Wq, w->Wk, w->Wv, q, k, v}));
   CHECK_HIP(tr::launch_qkv(*cfg, B, T, n1, *w, pos0, nullptr, q, k, v, (hipStream_t)stream),
             "qkv launch");
   return TRIROUTE_OK;
@@ -449,6 +466,7 @@ int triroute_attn_prefill(const triroute_cfg *cfg, int B, int T, const int32_t *
   TRY(check_cache(*cfg, cache, B, T));
   REQUIRE(q && mode && cmp && cmp->attn_cnt && cmp->attn_idx && o, TRIROUTE_E_INVALID,
           "NULL argument");
+  TRY(check_aligned({q, o}));
   TRY(check_ws(*cfg, TRIROUTE_OP_ATTN_PREFILL, B, T, ws, ws_bytes));
   CHECK_HIP(run_attn_prefill(*cfg, *cache, B, T, seq_ids, q, *cmp, o, (hipStream_t)stream),
             "attn_prefill launch");
@@ -462,6 +480,7 @@ int triroute_attn_decode(const triroute_cfg *cfg, int B, const int32_t *seq_ids,
   TRY(check_bt(B, 1));
   TRY(check_cache(*cfg, cache, B, 1));
   REQUIRE(q && mode && o, TRIROUTE_E_INVALID, "NULL argument");
+  TRY(check_aligned({q, o}));
   TRY(check_ws(*cfg, TRIROUTE_OP_ATTN_DECODE, B, 1, ws, ws_bytes));
   Carve cv(ws);
   float *part = carve_attn_decode(cv, *cfg, B);
@@ -475,6 +494,7 @@ int triroute_oproj(const triroute_cfg *cfg, int n_tok, const void *x, const void
   TRY(check_cfg(cfg));
   TRY(check_bt(n_tok, 1));
   REQUIRE(x && o && w && w->Wo && xt, TRIROUTE_E_INVALID, "NULL argument");
+  TRY(check_aligned({x, o, w->Wo, xt}));
   CHECK_HIP(tr::launch_oproj(*cfg, n_tok, x, o, *w, xt, (hipStream_t)stream), "oproj launch");
   return TRIROUTE_OK;
 }
@@ -498,6 +518,7 @@ int triroute_moe(const triroute_cfg *cfg, int n_tok, const void *xt, const triro
   REQUIRE(xt && dw && dw->g2 && w && w->Wgate && w->Wup && w->Wdown && eidx && egate && cmp &&
               cmp->exp_cnt && cmp->exp_off && cmp->exp_rows && x_out,
           TRIROUTE_E_INVALID, "NULL argument");
+  TRY(check_aligned({xt, dw->g2, w->Wgate, w->Wup, w->Wdown, x_out}));
   TRY(check_ws(*cfg, TRIROUTE_OP_MOE, n_tok, 1, ws, ws_bytes));
   Carve cv(ws);
   return moe_impl(cfg, n_tok, xt, dw, w, eidx, egate, cmp, x_out, cv, (hipStream_t)stream);
@@ -513,6 +534,9 @@ static int layer_impl(const triroute_cfg *cfg, int B, int T, bool decode, const 
   TRY(check_cache(*cfg, cache, B, T));
   REQUIRE(x && (psi || cfg->d_psi == 0) && rw && dw && mw && x_out, TRIROUTE_E_INVALID,
           "NULL argument");
+  TRY(check_aligned({x, x_out, rw->g1, rw->W1, rw->W2, rw->Wa, rw->We, rw->Wb, dw->Wq, dw->Wk,
+                     dw->Wv, dw->Wo, dw->g2, mw->Wgate, mw->Wup, mw->Wdown}));
+  if (taps) TRY(check_aligned({taps->n1, taps->q, taps->k, taps->v, taps->o, taps->xt}));
   const int op = decode ? TRIROUTE_OP_LAYER_DECODE : TRIROUTE_OP_LAYER_PREFILL;
   TRY(check_ws(*cfg, op, B, T, ws, ws_bytes));
   TRY(prepare_once());

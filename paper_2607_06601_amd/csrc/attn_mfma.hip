@@ -18,9 +18,9 @@
 //                 by the stored bf16 values.
 // Online softmax in the exp2 domain.  Decode runs one 8-wave block per
 // (sequence, kv head, chunk); each wave streams its share of every pool's
-// whole tiles into a private LDS ring with direct-to-LDS loads several tiles
-// ahead; the waves merge in LDS and a last kernel merges the chunks with
-// log-sum-exp.
+// whole tiles through a private LDS byte FIFO with direct-to-LDS loads issued
+// as far ahead as the FIFO allows; the waves merge in LDS and, when a
+// sequence is split into chunks, a last kernel merges them with log-sum-exp.
 #include <limits.h>
 
 #include "kernels.hpp"
@@ -437,86 +437,119 @@ struct DecodeArgs {
   const bf16 *q;
   const uint8_t *mode;
   const int32_t *seq_ids;
-  float *part;  // [B*H][NS][DH + 2]: m, l, O
+  float *part;  // [B*H][NS][DH + 2]: m, l, O (NS > 1)
+  bf16 *o;      // [B][H][DH] (NS == 1)
   int B, H, R, w, NS;
   float scale2;
 };
 
-// Geometry of the decode stream for one pool width: tile bytes, 1 KB wave
-// transfers per tile, ring slot size, and ring depth within a wave's
-// share of the block's LDS (8 shares plus a few words fill the 160 KB).
+// Decode streams every pool's tiles through a per-wave LDS ring used as a
+// byte FIFO: tiles of different widths are placed back to back (wrapping to
+// the ring start when one does not fit before the end), and the wave keeps
+// issuing tiles, across pool boundaries, for as long as free ring space
+// allows.  The block's 8 rings plus a few words fill the 160 KB of LDS.
 constexpr int DEC_WAVES = 8;
 constexpr int DEC_RING = 20 * 1024 - 32;
-template <int DH, int G, int BP>
-struct DmaGeo {
+
+// Per pool width index bi (2, 4, 8, 16 bits): tile bytes (codes + fp16
+// scale/zero), 1 KB wave transfers per tile, ring footprint.
+template <int DH, int G>
+struct DecGeo {
   static constexpr int TS = 4096 / DH;
   static constexpr int NG = DH / G;
-  static constexpr int TB = 1024 * BP + (BP < 16 ? 2 * TS * NG * 4 : 0);
-  static constexpr int NI = (TB + 1023) / 1024;
-  static constexpr int SLOT = (TB + 255) & ~255;
-  static constexpr int D = DEC_RING / SLOT < 6 ? DEC_RING / SLOT : 6;
-  static_assert(D >= 1 && (D - 1) * NI < 64, "ring depth / vmcnt range");
+  __device__ static constexpr int tb(int bi) {
+    return 1024 * (2 << bi) + (bi < 3 ? 2 * TS * NG * 4 : 0);
+  }
+  __device__ static constexpr int ni(int bi) { return (tb(bi) + 1023) / 1024; }
+  __device__ static constexpr int foot(int bi) { return (tb(bi) + 255) & ~255; }
+  static_assert(((1024 * 16 + 255) & ~255) <= DEC_RING, "a 16-bit tile fits the ring");
 };
 
-// Wait until at most `ahead` tiles of NI transfers each are still in flight
-// (0 <= ahead < D).
-template <int NI, int D>
-__device__ __forceinline__ void wait_tiles_ahead(int ahead) {
-  if constexpr (D > 5) if (ahead >= 5) { wait_vm<5 * NI>(); return; }
-  if constexpr (D > 4) if (ahead == 4) { wait_vm<4 * NI>(); return; }
-  if constexpr (D > 3) if (ahead == 3) { wait_vm<3 * NI>(); return; }
-  if constexpr (D > 2) if (ahead == 2) { wait_vm<2 * NI>(); return; }
-  if constexpr (D > 1) if (ahead == 1) { wait_vm<NI>(); return; }
-  wait_vm<0>();
-}
-
-// Copy one whole tile (codes + scale/zero, contiguous in HBM) into an LDS
-// ring slot with direct-to-LDS loads: each lane moves 16 bytes per 1 KB
-// transfer; lanes past the tile end sit out the last transfer.
-template <int TB, int NI>
-__device__ __forceinline__ void tile_to_lds(const uint8_t *src, uint8_t *dst) {
-  const int lane = threadIdx.x & 63;
-  const uint32_t d0 = lds_addr(dst);
-#pragma unroll
-  for (int j = 0; j < NI; ++j) {
-    const int off = j * 1024 + lane * 16;
-    if (off < TB) dma16(src + off, d0 + j * 1024);
+// s_waitcnt vmcnt(n) for a run-time n, rounded down to a value the switch
+// covers (waiting for fewer outstanding transfers is always safe).
+__device__ __forceinline__ void wait_vm_le(int n) {
+  switch (n < 0 ? 0 : n) {
+    case 0: wait_vm<0>(); break;
+    case 1: wait_vm<1>(); break;
+    case 2: wait_vm<2>(); break;
+    case 3: wait_vm<3>(); break;
+    case 4: wait_vm<4>(); break;
+    case 5: wait_vm<5>(); break;
+    case 6: wait_vm<6>(); break;
+    case 7: wait_vm<7>(); break;
+    case 8: wait_vm<8>(); break;
+    case 9: wait_vm<9>(); break;
+    case 10: wait_vm<10>(); break;
+    case 11: wait_vm<11>(); break;
+    case 12: wait_vm<12>(); break;
+    case 13: wait_vm<13>(); break;
+    case 14: wait_vm<14>(); break;
+    case 15: wait_vm<15>(); break;
+    case 16: case 17: wait_vm<16>(); break;
+    case 18: case 19: wait_vm<18>(); break;
+    case 20: case 21: wait_vm<20>(); break;
+    case 22: case 23: wait_vm<22>(); break;
+    default: wait_vm<24>(); break;
   }
 }
 
-// Stream this wave's tiles [w0, w1) of pool bi through its LDS ring.  On
-// entry no other vector-memory load of the wave may be in flight.
-template <int DH, int G, int BP>
-__device__ void stream_pool(SoftState<DH> &st, const CacheView &cv, int s, int bi, int g,
-                            int w0, int w1, uint8_t *myring, ColMask cm, const bf16x8 *qop,
-                            const float *qsum, float scale2, int len) {
-  using DG = DmaGeo<DH, G, BP>;
-  for (int j = 0; j < DG::D - 1 && w0 + j < w1; ++j)
-    tile_to_lds<DG::TB, DG::NI>(cv.tile(s, bi, g, w0 + j), myring + j * DG::SLOT);
-  for (int t = w0; t < w1; ++t) {
-    const int nx = t + DG::D - 1;
-    if (nx < w1)
-      tile_to_lds<DG::TB, DG::NI>(cv.tile(s, bi, g, nx), myring + ((nx - w0) % DG::D) * DG::SLOT);
-    wait_tiles_ahead<DG::NI, DG::D>(min(DG::D - 1, w1 - 1 - t));
-    TileRegs<DH, BP, G, false> tr;
-    tr.load(myring + ((t - w0) % DG::D) * DG::SLOT, cv, bi, t * DG::TS, nullptr, len);
-    process_tile<DH, BP, G, false>(st, tr, t * DG::TS, cm, qop, qsum, scale2);
+// Copy one whole tile (codes + scale/zero, contiguous in HBM) to LDS address
+// dst with direct-to-LDS loads: each lane moves 16 bytes per 1 KB transfer;
+// lanes past the tile end sit out the last transfer.
+__device__ __forceinline__ void tile_to_lds(const uint8_t *src, uint32_t dst, int tb, int ni) {
+  const int lane = threadIdx.x & 63;
+  for (int j = 0; j < ni; ++j) {
+    const int off = j * 1024 + lane * 16;
+    if (off < tb) dma16(src + off, dst + j * 1024);
+  }
+}
+
+// 4 wave-uniform ints picked by a run-time index without a private array.
+struct Int4 {
+  int v0, v1, v2, v3;
+  __device__ __forceinline__ int operator[](int i) const {
+    return i == 0 ? v0 : i == 1 ? v1 : i == 2 ? v2 : v3;
+  }
+  __device__ __forceinline__ void set(int i, int x) {
+    if (i == 0) v0 = x; else if (i == 1) v1 = x; else if (i == 2) v2 = x; else v3 = x;
+  }
+};
+
+// Consume tile t of pool bi from LDS.
+template <int DH, int G>
+__device__ __forceinline__ void decode_tile(SoftState<DH> &st, const CacheView &cv, int bi, int t,
+                                            const uint8_t *tp, ColMask cm, const bf16x8 *qop,
+                                            const float *qsum, float scale2) {
+  constexpr int TS = 4096 / DH;
+  switch (bi) {
+    case 0: { TileRegs<DH, 2, G, false> r; r.load(tp, cv, 0, t * TS, nullptr, 0);
+              process_tile<DH, 2, G, false>(st, r, t * TS, cm, qop, qsum, scale2); } break;
+    case 1: { TileRegs<DH, 4, G, false> r; r.load(tp, cv, 1, t * TS, nullptr, 0);
+              process_tile<DH, 4, G, false>(st, r, t * TS, cm, qop, qsum, scale2); } break;
+    case 2: { TileRegs<DH, 8, G, false> r; r.load(tp, cv, 2, t * TS, nullptr, 0);
+              process_tile<DH, 8, G, false>(st, r, t * TS, cm, qop, qsum, scale2); } break;
+    default: { TileRegs<DH, 16, G, false> r; r.load(tp, cv, 3, t * TS, nullptr, 0);
+               process_tile<DH, 16, G, false>(st, r, t * TS, cm, qop, qsum, scale2); } break;
   }
 }
 
 // One block of 8 waves per (sequence, kv head, chunk): the waves split each
-// pool's tile range of the chunk into contiguous runs and stream them.
+// pool's tile range of the chunk into contiguous runs; each wave streams its
+// runs of all four pools through its ring.  With one chunk the block writes
+// the normalised output itself; otherwise it leaves (m, l, O) partials.
 template <int DH, int G>
 __global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
+  using DG = DecGeo<DH, G>;
   constexpr int RING = DEC_WAVES * DEC_RING;
   static_assert(RING >= DEC_WAVES * 16 * (DH + 2) * 4, "ring doubles as the merge buffer");
-  __shared__ __align__(16) uint8_t ring[RING];
+  __shared__ __align__(1024) uint8_t ring[RING];
   __shared__ int bounds[4][2];  // per pool: first slot of the window, length
   const CacheView &cv = a.cv;
   constexpr int TS = 4096 / DH;
   const int Hkv = cv.Hkv;
   const int b = blockIdx.x / Hkv, g = blockIdx.x % Hkv, split = blockIdx.y;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, n16 = lane & 15;
+  const int lane = threadIdx.x & 63, n16 = lane & 15;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int s = a.seq_ids ? a.seq_ids[b] : b;
   const bool seq_ok = s >= 0 && s < cv.n_seq;
   const int R = a.R;
@@ -524,6 +557,7 @@ __global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
   const int hm = (seq_ok && n16 < R) ? int(a.mode[b * a.H + head]) : 0;
   int U = hm;  // union of the group's modes (max over its R heads)
   for (int x = 1; x < 16; x <<= 1) U = max(U, __shfl_xor(U, x, 16));
+  U = __builtin_amdgcn_readfirstlane(U);
   SoftState<DH> st;
   state_init(st);
   const int P = U > 0 ? cv.seq_len[s] - 1 : 0;
@@ -543,28 +577,59 @@ __global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
     float qsum[DH / G];
     load_q<DH, G>(a.q + (int64_t(b) * a.H + head) * DH, n16 < R && hm > 0, qop, qsum);
     wait_vm<0>();  // from here on the only vector-memory traffic is the tile stream
-    uint8_t *myring = ring + wave * DEC_RING;
+    Int4 w0, w1;
     for (int bi = 0; bi < 4; ++bi) {
       const int lb = bounds[bi][0], len = bounds[bi][1];
       const int lo = U == TRIROUTE_FULL ? 0 : lb;
       const int t0 = lo / TS, nt = (len + TS - 1) / TS - t0;
       const int c0 = t0 + int(int64_t(nt) * split / a.NS);
       const int c1 = t0 + int(int64_t(nt) * (split + 1) / a.NS);
-      const int w0 = c0 + (c1 - c0) * wave / DEC_WAVES;
-      const int w1 = c0 + (c1 - c0) * (wave + 1) / DEC_WAVES;
+      w0.set(bi, __builtin_amdgcn_readfirstlane(c0 + (c1 - c0) * wave / DEC_WAVES));
+      w1.set(bi, __builtin_amdgcn_readfirstlane(c0 + (c1 - c0) * (wave + 1) / DEC_WAVES));
+    }
+    const uint32_t rbase = lds_addr(ring) + wave * DEC_RING;
+    const uint8_t *rptr = ring + wave * DEC_RING;
+    // producer: next tile (pb, pt) to issue; consumer: next tile (cb, ct)
+    int pb = 0, pt = w0[0];
+    while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
+    int cb = pb, ct = pt;
+    int phead = 0, nin = 0, issued = 0;  // ring end of the newest tile, tiles and transfers out
+    int cpos = 0, consumed = 0;          // ring offset of tile (cb, ct), transfers consumed
+    while (cb < 4) {
+      while (pb < 4) {
+        const int sz = DG::foot(pb);
+        const int pos = phead + sz <= DEC_RING ? phead : 0;
+        bool ok = true;
+        if (nin > 0) {
+          if (cpos < phead)
+            ok = pos == phead || sz <= cpos;
+          else
+            ok = pos == phead && phead + sz <= cpos;
+        }
+        if (!ok) break;
+        tile_to_lds(cv.tile(s, pb, g, pt), rbase + pos, DG::tb(pb), DG::ni(pb));
+        phead = pos + sz;
+        issued += DG::ni(pb);
+        ++nin;
+        ++pt;
+        while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
+      }
+      consumed += DG::ni(cb);
+      wait_vm_le(issued - consumed);
+      const int lb = bounds[cb][0], len = bounds[cb][1];
       ColMask cm;
       cm.lo = hm == TRIROUTE_FULL ? 0 : hm == TRIROUTE_LOCAL ? lb : 1;
       cm.hi = hm == TRIROUTE_SKIP ? 0 : len - 1;
-      switch (bi) {
-        case 0: stream_pool<DH, G, 2>(st, cv, s, 0, g, w0, w1, myring, cm, qop, qsum, a.scale2, len); break;
-        case 1: stream_pool<DH, G, 4>(st, cv, s, 1, g, w0, w1, myring, cm, qop, qsum, a.scale2, len); break;
-        case 2: stream_pool<DH, G, 8>(st, cv, s, 2, g, w0, w1, myring, cm, qop, qsum, a.scale2, len); break;
-        default: stream_pool<DH, G, 16>(st, cv, s, 3, g, w0, w1, myring, cm, qop, qsum, a.scale2, len); break;
-      }
+      decode_tile<DH, G>(st, cv, cb, ct, rptr + cpos, cm, qop, qsum, a.scale2);
+      --nin;
+      const int chead = cpos + DG::foot(cb);
+      ++ct;
+      while (cb < 4 && ct >= w1[cb]) { ++cb; if (cb < 4) ct = w0[cb]; }
+      if (cb < 4) cpos = chead + DG::foot(cb) <= DEC_RING ? chead : 0;
     }
     state_finish<DH, G>(st);
   }
-  // merge the waves in LDS (the ring is free now): [wave][col][m, l, O]
+  // merge the waves in LDS (the rings are drained): [wave][col][m, l, O]
   __syncthreads();
   float(*red)[16][DH + 2] = (float(*)[16][DH + 2])ring;
   if (lane < 16) {
@@ -577,26 +642,33 @@ __global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
     for (int cb = 0; cb < DH / 16; ++cb)
       red[wave][4 * (lane >> 4) + i][2 + n16 + 16 * cb] = st.O[cb][i];
   __syncthreads();
-  for (int idx = threadIdx.x; idx < R * (DH + 2); idx += blockDim.x) {
-    const int col = idx / (DH + 2), e = idx % (DH + 2);
+  for (int idx = threadIdx.x; idx < R * DH; idx += blockDim.x) {
+    const int col = idx / DH, c = idx % DH;
     float M = -INFINITY;
 #pragma unroll
     for (int wv = 0; wv < DEC_WAVES; ++wv) M = fmaxf(M, red[wv][col][0]);
-    float val;
-    if (e == 0) {
-      val = M;
-    } else {
-      val = 0.f;
-      if (M != -INFINITY) {
+    float L = 0.f, O = 0.f;
+    if (M != -INFINITY) {
 #pragma unroll
-        for (int wv = 0; wv < DEC_WAVES; ++wv) {
-          const float mw = red[wv][col][0];
-          if (mw != -INFINITY) val += red[wv][col][e] * exp2f(mw - M);
-        }
+      for (int wv = 0; wv < DEC_WAVES; ++wv) {
+        const float mw = red[wv][col][0];
+        if (mw == -INFINITY) continue;
+        const float f = exp2f(mw - M);
+        L += red[wv][col][1] * f;
+        O += red[wv][col][2 + c] * f;
       }
     }
     const int hh = g * R + col;
-    a.part[((int64_t(b) * a.H + hh) * a.NS + split) * (DH + 2) + e] = val;
+    if (a.NS == 1) {
+      a.o[(int64_t(b) * a.H + hh) * DH + c] = f2bf(L > 0.f ? O * (1.f / L) : 0.f);
+    } else {
+      float *pp = a.part + ((int64_t(b) * a.H + hh) * a.NS + split) * (DH + 2);
+      pp[2 + c] = O;
+      if (c == 0) {
+        pp[0] = M;
+        pp[1] = L;
+      }
+    }
   }
 }
 
@@ -715,6 +787,7 @@ hipError_t launch_attn_mfma_decode(const triroute_cfg &cfg, const CacheView &cv,
   a.mode = mode;
   a.seq_ids = seq_ids;
   a.part = part;
+  a.o = (bf16 *)o;
   a.B = B;
   a.H = cfg.n_heads;
   a.R = cfg.n_heads / cfg.n_kv_heads;
@@ -730,13 +803,15 @@ hipError_t launch_attn_mfma_decode(const triroute_cfg &cfg, const CacheView &cv,
       attn_decode_kernel<64, 64><<<grid, threads, 0, st>>>(a);
     else
       attn_decode_kernel<64, 32><<<grid, threads, 0, st>>>(a);
-    attn_decode_combine_kernel<64><<<(BH + 3) / 4, 256, 0, st>>>(part, BH, a.NS, (bf16 *)o);
+    if (a.NS > 1)
+      attn_decode_combine_kernel<64><<<(BH + 3) / 4, 256, 0, st>>>(part, BH, a.NS, (bf16 *)o);
   } else {
     if (G == 64)
       attn_decode_kernel<128, 64><<<grid, threads, 0, st>>>(a);
     else
       attn_decode_kernel<128, 32><<<grid, threads, 0, st>>>(a);
-    attn_decode_combine_kernel<128><<<(BH + 3) / 4, 256, 0, st>>>(part, BH, a.NS, (bf16 *)o);
+    if (a.NS > 1)
+      attn_decode_combine_kernel<128><<<(BH + 3) / 4, 256, 0, st>>>(part, BH, a.NS, (bf16 *)o);
   }
   return hipGetLastError();
 }

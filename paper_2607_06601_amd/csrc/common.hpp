@@ -34,6 +34,35 @@ template <> struct Act<bf16> {
   __device__ static void st(bf16 *p, int64_t i, float v) { p[i] = f2bf(v); }
 };
 
+// 8 consecutive elements <-> fp32 (16-byte bf16 / two 16-byte fp32 accesses;
+// the address must be aligned to 8 elements).
+__device__ __forceinline__ void load8(const bf16 *p, float *v) {
+  const uint4 w = *(const uint4 *)p;
+  const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(u[i] << 16);
+    v[2 * i + 1] = __uint_as_float(u[i] & 0xFFFF0000u);
+  }
+}
+__device__ __forceinline__ void load8(const float *p, float *v) {
+  const float4 a = *(const float4 *)p, b = *(const float4 *)(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ __forceinline__ void store8(bf16 *p, const float *v) {
+  uint4 w;
+  w.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);
+  w.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);
+  w.z = uint32_t(f2bf(v[4])) | (uint32_t(f2bf(v[5])) << 16);
+  w.w = uint32_t(f2bf(v[6])) | (uint32_t(f2bf(v[7])) << 16);
+  *(uint4 *)p = w;
+}
+__device__ __forceinline__ void store8(float *p, const float *v) {
+  *(float4 *)p = make_float4(v[0], v[1], v[2], v[3]);
+  *(float4 *)(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+
 // --------------------------------------------------------- wave helpers
 constexpr int WAVE = 64;
 

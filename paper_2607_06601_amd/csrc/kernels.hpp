@@ -7,6 +7,9 @@ namespace tr {
 
 // router.hip
 hipError_t router_prepare();
+// trunk K split: ks chunks of kchunk inputs; the trunk partials take
+// ks * N * 128 floats of scratch
+void router_split(int N, int K, int &ks, int &kchunk);
 hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const float *psi,
                          const triroute_router_w &w, void *n1, uint8_t *mode, uint8_t *bit,
                          int32_t *eidx, float *egate, float *rinv, float *u, hipStream_t st);

@@ -6,6 +6,7 @@
 
 namespace tr {
 
+// One wave per row, 8 consecutive elements per lane access (d % 64 == 0).
 template <typename T>
 __global__ __launch_bounds__(256) void rms_norm2_kernel(const T *__restrict__ x,
                                                         const T *__restrict__ g,
@@ -16,16 +17,26 @@ __global__ __launch_bounds__(256) void rms_norm2_kernel(const T *__restrict__ x,
   if (row >= N) return;
   const T *xr = x + int64_t(row) * d;
   float ss = 0.f;
-  for (int c = lane; c < d; c += 64) {
-    const float v = Act<T>::ld(xr, c);
-    ss = fmaf(v, v, ss);
+  for (int c = lane * 8; c < d; c += 512) {
+    float v[8];
+    load8(xr + c, v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss = fmaf(v[i], v[i], ss);
   }
   ss = wave_sum(ss);
   const float r = 1.0f / sqrtf(ss / float(d) + eps);
   T *orow = out + int64_t(row) * d;
-  for (int c = lane; c < d; c += 64) Act<T>::st(orow, c, (Act<T>::ld(xr, c) * r) * Act<T>::ld(g, c));
+  for (int c = lane * 8; c < d; c += 512) {
+    float v[8], gv[8];
+    load8(xr + c, v);
+    load8(g + c, gv);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = (v[i] * r) * gv[i];
+    store8(orow + c, v);
+  }
 }
 
+// One thread per 8 consecutive features of a token.
 template <typename T>
 __global__ __launch_bounds__(256) void moe_combine_kernel(const T *__restrict__ xt,
                                                           const float *__restrict__ Y,
@@ -33,20 +44,30 @@ __global__ __launch_bounds__(256) void moe_combine_kernel(const T *__restrict__ 
                                                           const float *__restrict__ egate,
                                                           T *__restrict__ xout, int N, int d,
                                                           int k) {
-  const int64_t total = int64_t(N) * d;
-  for (int64_t idx = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; idx < total;
-       idx += int64_t(gridDim.x) * blockDim.x) {
-    const int i = int(idx / d), c = int(idx % d);
-    float acc = Act<T>::ld(xt, idx);
-    float y = 0.f;
+  const int d8 = d >> 3;
+  const int64_t total = int64_t(N) * d8;
+  for (int64_t it = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; it < total;
+       it += int64_t(gridDim.x) * blockDim.x) {
+    const int i = int(it / d8), c = int(it % d8) * 8;
+    float acc[8], y[8];
+    load8(xt + int64_t(i) * d + c, acc);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) y[u] = 0.f;
     bool any = false;
     for (int s = 0; s < k; ++s) {
       if (eidx[int64_t(i) * k + s] == 0) continue;
-      y = fmaf(egate[int64_t(i) * k + s], Y[(int64_t(i) * k + s) * d + c], y);
+      const float gt = egate[int64_t(i) * k + s];
+      float ys[8];
+      load8(Y + (int64_t(i) * k + s) * d + c, ys);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) y[u] = fmaf(gt, ys[u], y[u]);
       any = true;
     }
-    if (any) acc += y;
-    Act<T>::st(xout, idx, acc);
+    if (any) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc[u] += y[u];
+    }
+    store8(xout + int64_t(i) * d + c, acc);
   }
 }
 
@@ -65,7 +86,7 @@ hipError_t launch_rms_norm2(const triroute_cfg &cfg, int N, const void *x, const
 hipError_t launch_moe_combine(const triroute_cfg &cfg, int N, const void *xt, const float *Y,
                               const int32_t *eidx, const float *egate, void *xout,
                               hipStream_t st) {
-  int64_t total = int64_t(N) * cfg.d_model;
+  int64_t total = int64_t(N) * (cfg.d_model / 8);
   int64_t blocks = (total + 255) / 256;
   if (blocks > 8192) blocks = 8192;
   if (cfg.act == TRIROUTE_BF16)

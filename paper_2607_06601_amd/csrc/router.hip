@@ -2,14 +2,14 @@
 // decisions (Sec. 3.8), fp32 end to end.
 //
 //   rms_norm1   : r_i = 1/sqrt(mean(x_i^2) + eps); n1 = x r g1 (act out, for QKV)
-//   trunk1      : u = GELU(W1 [x r g1 ; psi] + b1)        fp32 tiled GEMM, N x 128
-//   tail        : h = W2 u + b2, h^ = RMSNorm(h) gr, z = W_{a,e,b} h^ + c,
-//                 argmax / top-k decisions and gates
+//   trunk1      : partial W1 [x r g1 ; psi] over K chunks    fp32 MFMA, N x 128
+//   tail        : u = GELU(sum + b1), h = W2 u + b2, h^ = RMSNorm(h) gr,
+//                 z = W_{a,e,b} h^ + c, argmax / top-k decisions and gates
 #include "kernels.hpp"
 
 namespace tr {
 
-// One wave per token row.
+// One wave per token row, 8 consecutive elements per lane access.
 template <typename T>
 __global__ __launch_bounds__(256) void rms_norm1_kernel(const T *__restrict__ x,
                                                         const float *__restrict__ g,
@@ -21,181 +21,210 @@ __global__ __launch_bounds__(256) void rms_norm1_kernel(const T *__restrict__ x,
   if (row >= N) return;
   const T *xr = x + int64_t(row) * d;
   float ss = 0.f;
-  for (int c = lane; c < d; c += 64) {
-    float v = Act<T>::ld(xr, c);
-    ss = fmaf(v, v, ss);
+  for (int c = lane * 8; c < d; c += 512) {
+    float v[8];
+    load8(xr + c, v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss = fmaf(v[i], v[i], ss);
   }
   ss = wave_sum(ss);
   float r = 1.0f / sqrtf(ss / float(d) + eps);
   if (lane == 0) rinv[row] = r;
   if (n1) {
     T *nr = n1 + int64_t(row) * d;
-    for (int c = lane; c < d; c += 64) Act<T>::st(nr, c, (Act<T>::ld(xr, c) * r) * g[c]);
+    for (int c = lane * 8; c < d; c += 512) {
+      float v[8], gv[8];
+      load8(xr + c, v);
+      load8(g + c, gv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = (v[i] * r) * gv[i];
+      store8(nr + c, v);
+    }
   }
 }
 
-// u[N][128] = GELU([n1 ; psi] W1^T + b1), n1 = x * r * g1 formed on load.
-// Block: 64 rows x 128 outputs, 256 threads, 4x8 outputs per thread.
+typedef float f32x4r __attribute__((ext_vector_type(4)));
+
+// Split of the trunk's K = d + d_psi inputs over blocks, so that a small
+// batch (decode) still spreads over the chip: K chunks are multiples of 32.
+void router_split(int N, int K, int &ks, int &kchunk) {
+  const int mt = (N + 63) / 64;
+  int want = (512 + mt - 1) / mt;
+  const int kmax = (K + 63) / 64;
+  want = want < 1 ? 1 : want > kmax ? kmax : want;
+  kchunk = ((K + want - 1) / want + 31) / 32 * 32;
+  ks = (K + kchunk - 1) / kchunk;
+}
+
+// Partial trunk pre-activations upart[ks][N][128] = [n1 ; psi] W1^T over the
+// block's K chunk, with n1 = x r g1 formed on load (fp32 MFMA 16x16x4).
+// Block: 64 rows x 128 outputs, 4 waves of 16 rows; the next K step is
+// fetched into registers while the current one is multiplied from LDS.
 template <typename T>
 __global__ __launch_bounds__(256) void trunk1_kernel(const T *__restrict__ x,
                                                      const float *__restrict__ rinv,
                                                      const float *__restrict__ g1,
                                                      const float *__restrict__ psi,
                                                      const float *__restrict__ W1,
-                                                     const float *__restrict__ b1,
-                                                     float *__restrict__ u, int N, int d,
-                                                     int dpsi) {
-  constexpr int BM = 64, BN = 128, BK = 16;
-  __shared__ __align__(16) float As[BK][BM + 4];
-  __shared__ __align__(16) float Bs[BK][BN + 4];
+                                                     float *__restrict__ upart, int N, int d,
+                                                     int dpsi, int kchunk) {
+  constexpr int BM = 64, BK = 32, LD = BK + 1;
+  __shared__ float As[2][BM][LD];
+  __shared__ float Bs[2][128][LD];
   const int K = d + dpsi;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int m0 = blockIdx.x * BM;
-  const int tr = tid >> 4, tc = tid & 15;
-  float acc[4][8];
+  const int kb = blockIdx.y * kchunk, ke = min(K, kb + kchunk);
+  f32x4r acc[8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = 0.f;
-  // loaders: A 64x16 (4 per thread), B 128x16 (8 per thread)
-  const int ar = tid >> 2, ak = (tid & 3) * 4;
-  const int bn = tid >> 1, bk = (tid & 1) * 8;
+  for (int j = 0; j < 8; ++j) acc[j] = f32x4r{0.f, 0.f, 0.f, 0.f};
+  const int ar = tid >> 2, ak = (tid & 3) * 8;
+  const int br = tid >> 1, bk = (tid & 1) * 16;
   const int arow = m0 + ar;
   const float rr = arow < N ? rinv[arow] : 0.f;
-  for (int k0 = 0; k0 < K; k0 += BK) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int k = k0 + ak + i;
-      float v = 0.f;
-      if (arow < N && k < K) {
-        if (k < d)
-          v = (Act<T>::ld(x, int64_t(arow) * d + k) * rr) * g1[k];
-        else
-          v = psi[int64_t(arow) * dpsi + (k - d)];
-      }
-      As[ak + i][ar] = v;
-    }
+  float ra[8], rb[16];
+  auto fetch = [&](int k0) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      int k = k0 + bk + i;
-      Bs[bk + i][bn] = k < K ? W1[int64_t(bn) * K + k] : 0.f;
+      const int k = k0 + ak + i;
+      float v = 0.f;
+      if (arow < N && k < ke)
+        v = k < d ? (Act<T>::ld(x, int64_t(arow) * d + k) * rr) * g1[k]
+                  : psi[int64_t(arow) * dpsi + (k - d)];
+      ra[i] = v;
     }
-    __syncthreads();
 #pragma unroll
-    for (int kk = 0; kk < BK; ++kk) {
-      float a[4], b[8];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = As[kk][tr * 4 + i];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) b[j] = Bs[kk][tc * 8 + j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    for (int i = 0; i < 16; ++i) {
+      const int k = k0 + bk + i;
+      rb[i] = k < ke ? W1[int64_t(br) * K + k] : 0.f;
     }
+  };
+  auto put = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) As[buf][ar][ak + i] = ra[i];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) Bs[buf][br][bk + i] = rb[i];
+  };
+  fetch(kb);
+  put(0);
+  __syncthreads();
+  int buf = 0;
+  for (int k0 = kb; k0 < ke; k0 += BK) {
+    const bool more = k0 + BK < ke;
+    if (more) fetch(k0 + BK);
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 4) {
+      const float av = As[buf][16 * wave + (lane & 15)][kk + (lane >> 4)];
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+            av, Bs[buf][16 * j + (lane & 15)][kk + (lane >> 4)], acc[j], 0, 0, 0);
+    }
+    if (more) put(buf ^ 1);
     __syncthreads();
+    buf ^= 1;
   }
+  float *out = upart + int64_t(blockIdx.y) * N * 128;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int row = m0 + tr * 4 + i;
+  for (int r = 0; r < 4; ++r) {
+    const int row = m0 + 16 * wave + 4 * (lane >> 4) + r;
     if (row >= N) continue;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      int col = tc * 8 + j;
-      float y = acc[i][j] + b1[col];
-      u[int64_t(row) * BN + col] = 0.5f * y * (1.0f + erff(y * 0.70710678118654752f));
-    }
+    for (int j = 0; j < 8; ++j) out[int64_t(row) * 128 + 16 * j + (lane & 15)] = acc[j][r];
   }
 }
 
-// Tail: 32 tokens per block, weights staged through LDS in two halves of
-// the 128-wide router dimension.  LDS: weights [max(128, NZ)][65],
-// activations [32][128], logits [32][NZ] (NZ = 3H + E + 5 <= 112: < 64 KB).
+// Tail, 16 tokens per block (4 waves, fp32 MFMA 16x16x4), with W2 and the
+// head weights staged in LDS by coalesced loads:
+//   u = GELU(sum of trunk partials + b1); h = W2 u + b2; h^ = RMSNorm(h) gr;
+//   z = [Wa; We; Wb] h^ + [ca; ce; cb]; argmax / top-k decisions and gates.
+constexpr int RT_TB = 16, RT_DR = 128, RT_LD = RT_DR + 4, RT_NZ = 112;
+constexpr size_t RT_LDS = sizeof(float) * (size_t(RT_DR + RT_NZ + 2 * RT_TB) * RT_LD);
+
 __global__ __launch_bounds__(256) void router_tail_kernel(
-    const float *__restrict__ u, const float *__restrict__ W2, const float *__restrict__ b2,
-    const float *__restrict__ gr, const float *__restrict__ Wa, const float *__restrict__ ca,
-    const float *__restrict__ We, const float *__restrict__ ce, const float *__restrict__ Wb,
-    const float *__restrict__ cb, uint8_t *__restrict__ mode, uint8_t *__restrict__ bit,
-    int32_t *__restrict__ eidx, float *__restrict__ egate, int N, int H, int E1, int k,
-    float eps) {
-  constexpr int DR = 128, TB = 32, HALF = 64, LDW = HALF + 1;
-  extern __shared__ __align__(16) float lds[];
+    const float *__restrict__ upart, int KS, const float *__restrict__ b1,
+    const float *__restrict__ W2, const float *__restrict__ b2, const float *__restrict__ gr,
+    const float *__restrict__ Wa, const float *__restrict__ ca, const float *__restrict__ We,
+    const float *__restrict__ ce, const float *__restrict__ Wb, const float *__restrict__ cb,
+    uint8_t *__restrict__ mode, uint8_t *__restrict__ bit, int32_t *__restrict__ eidx,
+    float *__restrict__ egate, int N, int H, int E1, int k, float eps) {
+  constexpr int TB = RT_TB, DR = RT_DR, LD = RT_LD;
+  extern __shared__ __align__(16) float rt_lds[];
+  float(*W2s)[LD] = (float(*)[LD])rt_lds;              // [128][LD]
+  float(*Wzs)[LD] = (float(*)[LD])(rt_lds + DR * LD);  // [NZ][LD]
+  float(*Us)[LD] = (float(*)[LD])(rt_lds + (DR + RT_NZ) * LD);
+  float(*Zs)[LD] = (float(*)[LD])(rt_lds + (DR + RT_NZ + TB) * LD);
   const int NZ = 3 * H + E1 + 4;
-  const int wrows = NZ > DR ? NZ : DR;
-  float *Ws = lds;                   // [wrows][LDW]
-  float *Hs = Ws + wrows * LDW;      // [TB][DR]
-  float *Zs = Hs + TB * DR;          // [TB][NZ]
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int t0 = blockIdx.x * TB;
+  for (int i = tid; i < DR * DR / 4; i += 256) {
+    const int r = i / (DR / 4), c4 = (i % (DR / 4)) * 4;
+    const float4 v = *(const float4 *)(W2 + r * DR + c4);
+    W2s[r][c4] = v.x; W2s[r][c4 + 1] = v.y; W2s[r][c4 + 2] = v.z; W2s[r][c4 + 3] = v.w;
+  }
+  for (int i = tid; i < NZ * DR / 4; i += 256) {
+    const int z = i / (DR / 4), c4 = (i % (DR / 4)) * 4;
+    const float *wz = z < 3 * H ? Wa + z * DR
+                      : z < 3 * H + E1 ? We + (z - 3 * H) * DR : Wb + (z - 3 * H - E1) * DR;
+    const float4 v = *(const float4 *)(wz + c4);
+    Wzs[z][c4] = v.x; Wzs[z][c4 + 1] = v.y; Wzs[z][c4 + 2] = v.z; Wzs[z][c4 + 3] = v.w;
+  }
   for (int idx = tid; idx < TB * DR; idx += 256) {
-    int t = t0 + idx / DR;
-    Hs[idx] = t < N ? u[int64_t(t) * DR + idx % DR] : 0.f;
-  }
-  // h = W2 u + b2 ; thread: column c, tokens tg, tg + 2, ...
-  const int c = tid & (DR - 1), tg = tid >> 7;
-  float h[TB / 2];
-#pragma unroll
-  for (int j = 0; j < TB / 2; ++j) h[j] = b2[c];
-  for (int half = 0; half < 2; ++half) {
-    __syncthreads();
-    for (int idx = tid; idx < DR * HALF; idx += 256)
-      Ws[(idx / HALF) * LDW + idx % HALF] = W2[(idx / HALF) * DR + half * HALF + idx % HALF];
-    __syncthreads();
-    for (int kk = 0; kk < HALF; ++kk) {
-      const float wv = Ws[c * LDW + kk];
-#pragma unroll
-      for (int j = 0; j < TB / 2; ++j)
-        h[j] = fmaf(wv, Hs[(tg + 2 * j) * DR + half * HALF + kk], h[j]);
+    const int t = idx / DR, c = idx % DR;
+    float y = 0.f;
+    if (t0 + t < N) {
+      float sacc = 0.f;
+      for (int s = 0; s < KS; ++s) sacc += upart[(int64_t(s) * N + t0 + t) * DR + c];
+      y = sacc + b1[c];
+      y = 0.5f * y * (1.0f + erff(y * 0.70710678118654752f));
     }
+    Us[t][c] = y;
+  }
+  __syncthreads();
+  // h: wave w computes columns 32 w .. 32 w + 31
+  f32x4r hacc[2] = {f32x4r{0.f, 0.f, 0.f, 0.f}, f32x4r{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll 8
+  for (int kk = 0; kk < DR; kk += 4) {
+    const float av = Us[lane & 15][kk + (lane >> 4)];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      hacc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+          av, W2s[32 * wave + 16 * j + (lane & 15)][kk + (lane >> 4)], hacc[j], 0, 0, 0);
   }
   __syncthreads();
 #pragma unroll
-  for (int j = 0; j < TB / 2; ++j) Hs[(tg + 2 * j) * DR + c] = h[j];
-  __syncthreads();
-  // RMSNorm of h per token (wave w handles tokens w, w + 4, ...)
-  {
-    const int lane = tid & 63, w = tid >> 6;
-    for (int t = w; t < TB; t += 4) {
-      const float a = Hs[t * DR + lane], b = Hs[t * DR + lane + 64];
-      const float ss = wave_sum(a * a + b * b);
-      const float r = 1.0f / sqrtf(ss / float(DR) + eps);
-      Hs[t * DR + lane] = (a * r) * gr[lane];
-      Hs[t * DR + lane + 64] = (b * r) * gr[lane + 64];
-    }
-  }
-  // logits, the head weights staged in two halves as well
-  for (int half = 0; half < 2; ++half) {
-    __syncthreads();
-    for (int idx = tid; idx < NZ * HALF; idx += 256) {
-      const int z = idx / HALF, kk = half * HALF + idx % HALF;
-      float wv;
-      if (z < 3 * H)
-        wv = Wa[z * DR + kk];
-      else if (z < 3 * H + E1)
-        wv = We[(z - 3 * H) * DR + kk];
-      else
-        wv = Wb[(z - 3 * H - E1) * DR + kk];
-      Ws[z * LDW + idx % HALF] = wv;
-    }
-    __syncthreads();
-    for (int idx = tid; idx < TB * NZ; idx += 256) {
-      const int t = idx / NZ, z = idx % NZ;
-      float acc = half ? Zs[t * NZ + z] : 0.f;
-      for (int kk = 0; kk < HALF; ++kk)
-        acc = fmaf(Ws[z * LDW + kk], Hs[t * DR + half * HALF + kk], acc);
-      Zs[t * NZ + z] = acc;
-    }
+  for (int j = 0; j < 2; ++j) {
+    const int n = 32 * wave + 16 * j + (lane & 15);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Us[4 * (lane >> 4) + r][n] = hacc[j][r] + b2[n];
   }
   __syncthreads();
-  for (int idx = tid; idx < TB * NZ; idx += 256) {
-    const int z = idx % NZ;
-    const float bias = z < 3 * H ? ca[z] : z < 3 * H + E1 ? ce[z - 3 * H] : cb[z - 3 * H - E1];
-    Zs[idx] += bias;
+  for (int t = wave; t < TB; t += 4) {
+    const float a = Us[t][lane], b = Us[t][lane + 64];
+    const float ss = wave_sum(a * a + b * b);
+    const float r = 1.0f / sqrtf(ss / float(DR) + eps);
+    Us[t][lane] = (a * r) * gr[lane];
+    Us[t][lane + 64] = (b * r) * gr[lane + 64];
+  }
+  __syncthreads();
+  for (int nt = wave; nt * 16 < NZ; nt += 4) {
+    const int z = nt * 16 + (lane & 15);
+    const int zr = z < NZ ? z : NZ - 1;
+    f32x4r zacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+    for (int kk = 0; kk < DR; kk += 4)
+      zacc = __builtin_amdgcn_mfma_f32_16x16x4f32(Us[lane & 15][kk + (lane >> 4)],
+                                                  Wzs[zr][kk + (lane >> 4)], zacc, 0, 0, 0);
+    if (z < NZ) {
+      const float bias = z < 3 * H ? ca[z] : z < 3 * H + E1 ? ce[z - 3 * H] : cb[z - 3 * H - E1];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) Zs[4 * (lane >> 4) + r][z] = zacc[r] + bias;
+    }
   }
   __syncthreads();
   if (tid < TB && t0 + tid < N) {
     const int t = t0 + tid;
-    const float *z = Zs + tid * NZ;
+    const float *z = Zs[tid];
     for (int hh = 0; hh < H; ++hh) {
       const float *za = z + 3 * hh;
       int best = 0;
@@ -233,34 +262,29 @@ __global__ __launch_bounds__(256) void router_tail_kernel(
   }
 }
 
-size_t router_tail_lds(int H, int E1) {
-  const int NZ = 3 * H + E1 + 4;
-  const int wrows = NZ > 128 ? NZ : 128;
-  return sizeof(float) * (size_t(wrows) * 65 + 32 * 128 + 32 * size_t(NZ));
-}
-
 hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const float *psi,
                          const triroute_router_w &w, void *n1, uint8_t *mode, uint8_t *bit,
                          int32_t *eidx, float *egate, float *rinv, float *u,
                          hipStream_t st) {
   const int d = cfg.d_model;
+  int ks, kchunk;
+  router_split(N, d + cfg.d_psi, ks, kchunk);
   dim3 g1((N + 3) / 4);
-  dim3 g2((N + 63) / 64);
+  dim3 g2((N + 63) / 64, ks);
   if (cfg.act == TRIROUTE_BF16) {
     rms_norm1_kernel<bf16><<<g1, 256, 0, st>>>((const bf16 *)x, w.g1, rinv, (bf16 *)n1, N, d,
                                                cfg.rms_eps);
-    trunk1_kernel<bf16><<<g2, 256, 0, st>>>((const bf16 *)x, rinv, w.g1, psi, w.W1, w.b1, u,
-                                            N, d, cfg.d_psi);
+    trunk1_kernel<bf16><<<g2, 256, 0, st>>>((const bf16 *)x, rinv, w.g1, psi, w.W1, u, N, d,
+                                            cfg.d_psi, kchunk);
   } else {
     rms_norm1_kernel<float><<<g1, 256, 0, st>>>((const float *)x, w.g1, rinv, (float *)n1, N, d,
                                                 cfg.rms_eps);
-    trunk1_kernel<float><<<g2, 256, 0, st>>>((const float *)x, rinv, w.g1, psi, w.W1, w.b1, u,
-                                             N, d, cfg.d_psi);
+    trunk1_kernel<float><<<g2, 256, 0, st>>>((const float *)x, rinv, w.g1, psi, w.W1, u, N, d,
+                                             cfg.d_psi, kchunk);
   }
-  size_t lds = router_tail_lds(cfg.n_heads, cfg.n_experts + 1);
-  router_tail_kernel<<<dim3((N + 31) / 32), 256, lds, st>>>(u, w.W2, w.b2, w.gr, w.Wa, w.ca, w.We, w.ce, w.Wb,
-                                           w.cb, mode, bit, eidx, egate, N, cfg.n_heads,
-                                           cfg.n_experts + 1, cfg.top_k, cfg.rms_eps);
+  router_tail_kernel<<<dim3((N + RT_TB - 1) / RT_TB), 256, RT_LDS, st>>>(
+      u, ks, w.b1, w.W2, w.b2, w.gr, w.Wa, w.ca, w.We, w.ce, w.Wb, w.cb, mode, bit, eidx, egate, N,
+      cfg.n_heads, cfg.n_experts + 1, cfg.top_k, cfg.rms_eps);
   return hipGetLastError();
 }
 

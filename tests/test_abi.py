@@ -79,6 +79,13 @@ def test_bad_calls_return_codes_without_launching():
     r = lib.triroute_router(C.byref(c), 8, 2048, fake, fake, C.byref(rw), fake, fake, fake,
                             fake, fake, C.byref(cmp), fake, 1024, None)
     assert r == -3 and b"workspace" in lib.triroute_last_error()
+    # a tensor pointer off 16-byte alignment
+    r = lib.triroute_router(C.byref(c), 8, 2048, fake + 8, fake, C.byref(rw), fake, fake, fake,
+                            fake, fake, C.byref(cmp), fake, 1 << 40, None)
+    assert r == -1 and b"aligned" in lib.triroute_last_error()
+    dw = tr.DenseW(*([fake] * 5))
+    r = lib.triroute_oproj(C.byref(c), 16, fake, fake + 2, C.byref(dw), fake, None)
+    assert r == -1 and b"aligned" in lib.triroute_last_error()
     # B*T beyond the supported range
     n = C.c_size_t()
     assert lib.triroute_workspace_bytes(C.byref(c), 0, 1 << 13, 1 << 12, C.byref(n)) == -2

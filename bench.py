@@ -55,7 +55,8 @@ class CacheFlush:
     """Evicts L2 and the Infinity Cache by reading a 1 GiB buffer."""
 
     def __init__(self, torch, dev):
-        self.buf = torch.ones(1 << 28, dtype=torch.int32, device=dev)
+        # fp32, so that the reduction reads the buffer as it is (no widening copy)
+        self.buf = torch.ones(1 << 28, dtype=torch.float32, device=dev)
 
     def __call__(self):
         self.buf.sum()
@@ -349,9 +350,10 @@ def bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush):
 
 
 def summarize_pmc(fetch_dir, write_dir, regex):
-    """Per-launch HBM bytes of the kernels matching `regex` from two rocprofv3
-    counter runs, each scaled by what the same counter reads for the 256 MiB
-    copy of copy_calibration() (the copy reads and writes 256 MiB)."""
+    """Per-launch HBM bytes of the kernels matching `regex` (one dispatch of
+    each per launch) from two rocprofv3 counter runs, each counter scaled by
+    what it reads for the 256 MiB copy of copy_calibration(), which reads and
+    writes 256 MiB."""
     import csv
     import glob
     import re
@@ -371,9 +373,9 @@ def summarize_pmc(fetch_dir, write_dir, regex):
     out = {}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         rows = read(d, counter)
-        copy = [v for n, _, v in rows if ("copy" in n.lower() or "elementwise" in n.lower())
-                and v > 0.5 * (256 << 10)]
-        ref = (256 << 10) / max(copy) if copy else float("nan")
+        # the 256 MiB device copy (hipMemcpy D2D kernel) reads and writes 256 MiB
+        copy = sorted(v for n, _, v in rows if "copyBuffer" in n and v > 0.25 * (256 << 10))
+        ref = (256 << 10) / copy[len(copy) // 2] if copy else float("nan")
         per_kernel = {}
         for n, _, v in rows:
             if pat.search(n):

@@ -161,7 +161,7 @@ typedef struct triroute_kv_cache {
   int64_t off_status;     /* int32 status word */
   int64_t off_seq_len;    /* int32 [n_seq] */
   int64_t off_pool_len;   /* int32 [n_seq][4] */
-  int64_t off_pos;        /* int32 [n_seq][4][capacity] */
+  int64_t off_pos;        /* int32 [n_seq][4][n_tiles * tile_slots] */
   int64_t off_pool[4];    /* first tile of width bi */
   int64_t tile_bytes[4];  /* bytes per tile of width bi */
   int64_t total_bytes;

@@ -247,7 +247,7 @@ void layout_cache(const triroute_cfg &c, int n_seq, int capacity, triroute_kv_ca
   kc->off_pool_len = off;
   off += align256(size_t(n_seq) * 16);
   kc->off_pos = off;
-  off += align256(size_t(n_seq) * 4 * capacity * 4);
+  off += align256(size_t(n_seq) * 4 * kc->n_tiles * TS * 4);
   for (int bi = 0; bi < 4; ++bi) {
     const int bp = tr::pool_bits(bi, ab);
     kc->tile_bytes[bi] = align256(size_t(1024) * bp + (bi < 3 ? size_t(2) * TS * (dh / G) * 4 : 0));

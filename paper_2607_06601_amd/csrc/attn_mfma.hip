@@ -23,6 +23,8 @@
 // sequence is split into chunks, a last kernel merges them with log-sum-exp.
 #include <limits.h>
 
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace tr {
@@ -149,6 +151,9 @@ struct TileRegs {
   uint32_t vsz[Q ? Gm::KV : 1][2][4 * NG];     // [step][half][slot i * NG + g]
   int key[POS ? Gm::NB : 1][4];                // key positions (INT_MAX past klen)
 
+  // tp: the tile; kpos: positions of the tile's slots (POS only); slot0:
+  // pool slot of the tile's first slot; klen: pool length.
+
   __device__ __forceinline__ void load(const uint8_t *tp, const CacheView &cv, int bi,
                                        int slot0, const int32_t *kpos, int klen) {
     const int lane = threadIdx.x & 63, o4 = lane >> 4;
@@ -186,9 +191,9 @@ struct TileRegs {
       for (int blk = 0; blk < Gm::NB; ++blk)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int slot = slot0 + blk * 16 + 4 * o4 + i;
-          // slots past the pool length hold no token (and may lie past `capacity`)
-          key[blk][i] = slot < klen ? kpos[slot] : INT_MAX;
+          const int r = blk * 16 + 4 * o4 + i;
+          // slots past the pool length hold no token
+          key[blk][i] = slot0 + r < klen ? kpos[r] : INT_MAX;
         }
     }
   }
@@ -319,7 +324,8 @@ __device__ __forceinline__ void process_tile(SoftState<DH> &st,
   }
 }
 
-// Walk this wave's tiles [t_begin, t_end) (stride `step`) of pool bi.  Narrow
+// Walk this wave's tiles [t_begin, t_end) (stride `step`) of pool bi, loading
+// each straight from HBM into registers (kpos: the pool's slot positions).  Narrow
 // pools without position keys keep the next tile in flight while the current
 // one is processed; otherwise all of a tile's loads are issued at once.
 template <int DH, int BP, int G, bool POS>
@@ -330,16 +336,16 @@ __device__ void run_pool(SoftState<DH> &st, const CacheView &cv, int s, int bi, 
   TileRegs<DH, BP, G, POS> cur;
   if constexpr (BP <= 4 && !POS) {
     TileRegs<DH, BP, G, POS> nxt;
-    cur.load(cv.tile(s, bi, g, t_begin), cv, bi, t_begin * cv.TS, kpos, klen);
+    cur.load(cv.tile(s, bi, g, t_begin), cv, bi, t_begin * cv.TS, kpos + t_begin * cv.TS, klen);
     for (int t = t_begin; t < t_end; t += step) {
       const bool more = t + step < t_end;
-      if (more) nxt.load(cv.tile(s, bi, g, t + step), cv, bi, (t + step) * cv.TS, kpos, klen);
+      if (more) nxt.load(cv.tile(s, bi, g, t + step), cv, bi, (t + step) * cv.TS, kpos + (t + step) * cv.TS, klen);
       process_tile<DH, BP, G, POS>(st, cur, t * cv.TS, cm, qop, qsum, scale2);
       if (more) cur = nxt;
     }
   } else {
     for (int t = t_begin; t < t_end; t += step) {
-      cur.load(cv.tile(s, bi, g, t), cv, bi, t * cv.TS, kpos, klen);
+      cur.load(cv.tile(s, bi, g, t), cv, bi, t * cv.TS, kpos ? kpos + t * cv.TS : nullptr, klen);
       process_tile<DH, BP, G, POS>(st, cur, t * cv.TS, cm, qop, qsum, scale2);
     }
   }
@@ -454,7 +460,7 @@ constexpr int DEC_RING = 20 * 1024 - 32;
 // Per pool width index bi (2, 4, 8, 16 bits): tile bytes (codes + fp16
 // scale/zero), 1 KB wave transfers per tile, ring footprint.
 template <int DH, int G>
-struct DecGeo {
+struct StreamGeo {
   static constexpr int TS = 4096 / DH;
   static constexpr int NG = DH / G;
   __device__ static constexpr int tb(int bi) {
@@ -515,11 +521,279 @@ struct Int4 {
   }
 };
 
-// Consume tile t of pool bi from LDS.
+// Stream this wave's tiles [w0[bi], w1[bi]) of the four pools, pools in
+// order, through its LDS ring (DEC_RING bytes at rptr / LDS address rbase)
+// used as a byte FIFO: tiles are placed back to back, wrapping to the ring
+// start when one does not fit before the end, and the wave keeps issuing
+// tiles, across pool boundaries, while free space allows.  Each tile, once
+// resident, goes to fold(bi, t, lds_pointer).  On entry no other
+// vector-memory load of the wave may be in flight.
+template <int DH, int G, class Fold>
+__device__ void stream_tiles(const CacheView &cv, int s, int g, Int4 w0, Int4 w1,
+                             const uint8_t *rptr, uint32_t rbase, Fold &&fold) {
+  using SG = StreamGeo<DH, G>;
+  int pb = 0, pt = w0[0];  // producer: next tile to issue
+  while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
+  int cb = pb, ct = pt;    // consumer: next tile to fold
+  int phead = 0, nin = 0, issued = 0;  // ring end of the newest tile, tiles and transfers out
+  int cpos = 0, consumed = 0;          // ring offset of tile (cb, ct), transfers consumed
+  while (cb < 4) {
+    while (pb < 4) {
+      const int sz = SG::foot(pb);
+      const int pos = phead + sz <= DEC_RING ? phead : 0;
+      bool ok = true;
+      if (nin > 0) {
+        if (cpos < phead)
+          ok = pos == phead || sz <= cpos;
+        else
+          ok = pos == phead && phead + sz <= cpos;
+      }
+      if (!ok) break;
+      tile_to_lds(cv.tile(s, pb, g, pt), rbase + pos, SG::tb(pb), SG::ni(pb));
+      phead = pos + sz;
+      issued += SG::ni(pb);
+      ++nin;
+      ++pt;
+      while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
+    }
+    consumed += SG::ni(cb);
+    wait_vm_le(issued - consumed);
+    fold(cb, ct, rptr + cpos);
+    --nin;
+    const int chead = cpos + SG::foot(cb);
+    ++ct;
+    while (cb < 4 && ct >= w1[cb]) { ++cb; if (cb < 4) ct = w0[cb]; }
+    if (cb < 4) cpos = chead + SG::foot(cb) <= DEC_RING ? chead : 0;
+  }
+}
+
+// ---- decode with head-packed columns (at most 4 query heads per kv head)
+//
+// The 16 columns of the S^T = K Q^T product are 4 groups of 4 heads; group
+// c multiplies key block c of the tile (its Q operand is zero in the other
+// groups' columns), so one accumulator holds every score of the tile with no
+// idle column: lane (o4, n16) has head n16 % 4 against slots
+// 16 (n16 / 4) + 4 o4 + i.  The softmax state is kept per head (a max over
+// the lanes of one head), and P V runs with these 16 "virtual columns" (head,
+// key block) as rows: the lane's own probabilities are already in the A
+// operand order of the V layout, zero outside its block.  The virtual rows
+// of a head are summed once at the end.
+template <int DH>
+struct DecState {
+  float m;             // running max (log2 domain) of the lane's head
+  float l;             // partial denominator (this lane's keys)
+  float zc[DH / 32];   // partial additive term per channel group
+  f32x4 O[DH / 16];    // rows: virtual columns (key block o4, head i); cols: channel n16 + 16 cb
+};
+
+template <int DH>
+__device__ __forceinline__ void dec_init(DecState<DH> &st) {
+  st.m = -INFINITY;
+  st.l = 0.f;
+#pragma unroll
+  for (int g = 0; g < DH / 32; ++g) st.zc[g] = 0.f;
+#pragma unroll
+  for (int c = 0; c < DH / 16; ++c) st.O[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// A tile's K / V lane records and the scale/zero words of the lane's 4 slots.
+template <int DH, int BP, int G>
+struct DecRegs {
+  using Gm = Geo<DH>;
+  static constexpr int NG = DH / G;
+  static constexpr int W = PoolTraits<BP>::WORDS;
+  static constexpr bool Q = PoolTraits<BP>::QUANT;
+  union {
+    u32x4 v[W / 4];
+    uint32_t w[W];
+  } k, v;
+  uint32_t ksz[Q ? 4 * NG : 1], vsz[Q ? 4 * NG : 1];  // [slot i * NG + g]
+
+  __device__ __forceinline__ void load(const uint8_t *tp, const CacheView &cv, int bi) {
+    const int lane = threadIdx.x & 63, o4 = lane >> 4;
+    const int blk = min((lane & 15) >> 2, Gm::NB - 1);
+    const u32x4 *kp = (const u32x4 *)(tp + lane * 8 * BP);
+    const u32x4 *vp = (const u32x4 *)(tp + 512 * BP + lane * 8 * BP);
+#pragma unroll
+    for (int x = 0; x < W / 4; ++x) {
+      k.v[x] = kp[x];
+      v.v[x] = vp[x];
+    }
+    if constexpr (Q) {
+      const int st0 = 16 * blk + 4 * o4;
+      const u32x4 *ks = (const u32x4 *)(tp + cv.k_sz_off(bi) + st0 * NG * 4);
+      const u32x4 *vs = (const u32x4 *)(tp + cv.v_sz_off(bi) + st0 * NG * 4);
+#pragma unroll
+      for (int x = 0; x < NG; ++x) {
+        const u32x4 a = ks[x], b = vs[x];
+#pragma unroll
+        for (int y = 0; y < 4; ++y) {
+          ksz[4 * x + y] = a[y];
+          vsz[4 * x + y] = b[y];
+        }
+      }
+    }
+  }
+};
+
+template <int DH, int BP, int G>
+__device__ __forceinline__ void fold_dec(DecState<DH> &st, const DecRegs<DH, BP, G> &tr,
+                                         int slot0, ColMask cm, const bf16x8 *qopm,
+                                         const float *qsum, float scale2) {
+  using Gm = Geo<DH>;
+  using PT = PoolTraits<BP>;
+  constexpr int NG = DH / G;
+  constexpr int gks = G / 32;
+  const int lane = threadIdx.x & 63, o4 = lane >> 4, c = (lane & 15) >> 2;
+  // ---- scores of the lane's head against slots 16 c + 4 o4 + i
+  f32x4 acc[NG];
+#pragma unroll
+  for (int g = 0; g < NG; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int blk = 0; blk < Gm::NB; ++blk)
+#pragma unroll
+    for (int ks = 0; ks < Gm::KS; ++ks)
+      acc[ks / gks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+          field_op<BP>(tr.k.w, blk * Gm::KS + ks), qopm[blk * Gm::KS + ks], acc[ks / gks], 0, 0,
+          0);
+  float p[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float sv = 0.f;
+    if constexpr (PT::QUANT) {
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        float S, Z;
+        unpack_sz(tr.ksz[i * NG + g], S, Z);
+        sv = fmaf(S, acc[g][i], sv);
+        sv = fmaf(Z - PT::OFF * S, qsum[g], sv);
+      }
+    } else {
+#pragma unroll
+      for (int g = 0; g < NG; ++g) sv += acc[g][i];
+    }
+    const int key = slot0 + 16 * c + 4 * o4 + i;
+    p[i] = (c < Gm::NB && key >= cm.lo && key <= cm.hi) ? sv * scale2 : -INFINITY;
+  }
+  // ---- online softmax per head (lanes of one head: equal lane % 4)
+  float mt = fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3]));
+  mt = fmaxf(mt, __shfl_xor(mt, 4, 64));
+  mt = fmaxf(mt, __shfl_xor(mt, 8, 64));
+  mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+  mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+  const float mnew = fmaxf(st.m, mt);
+  const bool live = mnew != -INFINITY;
+  const float corr = live ? exp2f(st.m - mnew) : 1.f;
+  float ps = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    p[i] = live ? exp2f(p[i] - mnew) : 0.f;
+    ps += p[i];
+  }
+  st.l = st.l * corr + ps;
+#pragma unroll
+  for (int g = 0; g < NG; ++g) st.zc[g] *= corr;
+  st.m = mnew;
+  // output rows of head i take head i's factor (lane i holds head i)
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float ci = __shfl(corr, i, 64);
+#pragma unroll
+    for (int cb = 0; cb < Gm::CB; ++cb) st.O[cb][i] *= ci;
+  }
+  // ---- P' (fp16 p * s_v, or bf16 p for the 16-bit pool), two packed pairs per group
+  uint32_t ph[NG][2];
+#pragma unroll
+  for (int g = 0; g < NG; ++g)
+#pragma unroll
+    for (int jp = 0; jp < 2; ++jp) {
+      uint32_t h2[2];
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int i = 2 * jp + hh;
+        if constexpr (PT::QUANT) {
+          float S, Z;
+          unpack_sz(tr.vsz[i * NG + g], S, Z);
+          const _Float16 h = (_Float16)(p[i] * S);
+          st.zc[g] = fmaf(p[i], Z, st.zc[g]);
+          h2[hh] = uint32_t(*(const uint16_t *)&h);
+        } else {
+          h2[hh] = uint32_t(f2bf(p[i]));
+        }
+      }
+      ph[g][jp] = h2[0] | (h2[1] << 16);
+    }
+  // ---- O += P' V, one 32-slot step (key blocks 2 kv, 2 kv + 1) at a time
+#pragma unroll
+  for (int kv = 0; kv < Gm::KV; ++kv) {
+    const bool s0 = c == 2 * kv, s1 = c == 2 * kv + 1;
+    u32x4 pk[NG];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      pk[g][0] = s0 ? ph[g][0] : 0u;
+      pk[g][1] = s0 ? ph[g][1] : 0u;
+      pk[g][2] = s1 ? ph[g][0] : 0u;
+      pk[g][3] = s1 ? ph[g][1] : 0u;
+    }
+#pragma unroll
+    for (int cb = 0; cb < Gm::CB; ++cb) {
+      const int g = (16 * cb) / G;
+      if constexpr (PT::QUANT) {
+        const f16x8 bv = vfield_h<BP>(tr.v.w, kv * Gm::CB + cb);
+        st.O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_h(pk[g]), bv, st.O[cb], 0, 0, 0);
+      } else {
+        const bf16x8 bv = field_op<BP>(tr.v.w, kv * Gm::CB + cb);
+        st.O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_op(pk[g]), bv, st.O[cb], 0, 0, 0);
+      }
+    }
+  }
+}
+
+// Sum the per-lane partials of each head and its virtual output rows.
+// Afterwards lane (o4, n) holds in O[cb][i] the un-normalised output of head
+// i, channel n + 16 cb; lanes 0..3 hold m and l of heads 0..3.
 template <int DH, int G>
-__device__ __forceinline__ void decode_tile(SoftState<DH> &st, const CacheView &cv, int bi, int t,
-                                            const uint8_t *tp, ColMask cm, const bf16x8 *qop,
-                                            const float *qsum, float scale2) {
+__device__ __forceinline__ void dec_finish(DecState<DH> &st) {
+  constexpr int NG = DH / G;
+#pragma unroll
+  for (int x = 4; x < 64; x <<= 1) {
+    st.l += __shfl_xor(st.l, x, 64);
+#pragma unroll
+    for (int g = 0; g < NG; ++g) st.zc[g] += __shfl_xor(st.zc[g], x, 64);
+  }
+#pragma unroll
+  for (int cb = 0; cb < DH / 16; ++cb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float v = st.O[cb][i];
+      v += __shfl_xor(v, 16, 64);
+      v += __shfl_xor(v, 32, 64);
+      st.O[cb][i] = v + __shfl(st.zc[(16 * cb) / G], i, 64);
+    }
+}
+
+template <int DH, int G>
+__device__ __forceinline__ void fold_dec_any(DecState<DH> &st, const CacheView &cv, int bi, int t,
+                                             const uint8_t *tp, ColMask cm, const bf16x8 *qopm,
+                                             const float *qsum, float scale2) {
+  constexpr int TS = 4096 / DH;
+  switch (bi) {
+    case 0: { DecRegs<DH, 2, G> r; r.load(tp, cv, 0);
+              fold_dec<DH, 2, G>(st, r, t * TS, cm, qopm, qsum, scale2); } break;
+    case 1: { DecRegs<DH, 4, G> r; r.load(tp, cv, 1);
+              fold_dec<DH, 4, G>(st, r, t * TS, cm, qopm, qsum, scale2); } break;
+    case 2: { DecRegs<DH, 8, G> r; r.load(tp, cv, 2);
+              fold_dec<DH, 8, G>(st, r, t * TS, cm, qopm, qsum, scale2); } break;
+    default: { DecRegs<DH, 16, G> r; r.load(tp, cv, 3);
+               fold_dec<DH, 16, G>(st, r, t * TS, cm, qopm, qsum, scale2); } break;
+  }
+}
+
+// Fold tile t of pool bi, resident in LDS at tp, into a one-head-per-column state.
+template <int DH, int G>
+__device__ __forceinline__ void fold_tile(SoftState<DH> &st, const CacheView &cv, int bi, int t,
+                                          const uint8_t *tp, ColMask cm, const bf16x8 *qop,
+                                          const float *qsum, float scale2) {
   constexpr int TS = 4096 / DH;
   switch (bi) {
     case 0: { TileRegs<DH, 2, G, false> r; r.load(tp, cv, 0, t * TS, nullptr, 0);
@@ -535,11 +809,12 @@ __device__ __forceinline__ void decode_tile(SoftState<DH> &st, const CacheView &
 
 // One block of 8 waves per (sequence, kv head, chunk): the waves split each
 // pool's tile range of the chunk into contiguous runs; each wave streams its
-// runs of all four pools through its ring.  With one chunk the block writes
-// the normalised output itself; otherwise it leaves (m, l, O) partials.
-template <int DH, int G>
+// runs of all four pools through its ring.  PACKED (at most 4 query heads per
+// kv head): head-packed columns; otherwise one head per column.  With one
+// chunk the block writes the normalised output itself; otherwise it leaves
+// (m, l, O) partials.
+template <int DH, int G, bool PACKED>
 __global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
-  using DG = DecGeo<DH, G>;
   constexpr int RING = DEC_WAVES * DEC_RING;
   static_assert(RING >= DEC_WAVES * 16 * (DH + 2) * 4, "ring doubles as the merge buffer");
   __shared__ __align__(1024) uint8_t ring[RING];
@@ -553,19 +828,20 @@ __global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
   const int s = a.seq_ids ? a.seq_ids[b] : b;
   const bool seq_ok = s >= 0 && s < cv.n_seq;
   const int R = a.R;
-  const int head = g * R + n16;
-  const int hm = (seq_ok && n16 < R) ? int(a.mode[b * a.H + head]) : 0;
+  const int hl = PACKED ? (n16 & 3) : n16;  // the lane's query head within the group
+  const int head = g * R + hl;
+  const int hm = (seq_ok && hl < R) ? int(a.mode[b * a.H + head]) : 0;
   int U = hm;  // union of the group's modes (max over its R heads)
   for (int x = 1; x < 16; x <<= 1) U = max(U, __shfl_xor(U, x, 16));
   U = __builtin_amdgcn_readfirstlane(U);
-  SoftState<DH> st;
-  state_init(st);
+  using State = typename std::conditional<PACKED, DecState<DH>, SoftState<DH>>::type;
+  State st;
+  if constexpr (PACKED) dec_init(st); else state_init(st);
   const int P = U > 0 ? cv.seq_len[s] - 1 : 0;
   if (U > 0 && wave < 4) {  // waves 0..3 find the window start of pools 0..3
     const int bi = wave;
     const int len = cv.pool_len[s * 4 + bi];
-    const int32_t *pos = cv.pos + (int64_t(s) * 4 + bi) * cv.capacity;
-    const int lb = lower_bound_pos(pos, len, P - a.w + 1);
+    const int lb = lower_bound_pos(cv.pos_of(s, bi), len, P - a.w + 1);
     if (lane == 0) {
       bounds[bi][0] = lb;
       bounds[bi][1] = len;
@@ -575,9 +851,9 @@ __global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
   if (U > 0) {
     bf16x8 qop[DH / 32];
     float qsum[DH / G];
-    load_q<DH, G>(a.q + (int64_t(b) * a.H + head) * DH, n16 < R && hm > 0, qop, qsum);
+    load_q<DH, G>(a.q + (int64_t(b) * a.H + head) * DH, hl < R && hm > 0, qop, qsum);
     wait_vm<0>();  // from here on the only vector-memory traffic is the tile stream
-    Int4 w0, w1;
+    Int4 w0, w1, lbs, lens;
     for (int bi = 0; bi < 4; ++bi) {
       const int lb = bounds[bi][0], len = bounds[bi][1];
       const int lo = U == TRIROUTE_FULL ? 0 : lb;
@@ -586,48 +862,36 @@ __global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
       const int c1 = t0 + int(int64_t(nt) * (split + 1) / a.NS);
       w0.set(bi, __builtin_amdgcn_readfirstlane(c0 + (c1 - c0) * wave / DEC_WAVES));
       w1.set(bi, __builtin_amdgcn_readfirstlane(c0 + (c1 - c0) * (wave + 1) / DEC_WAVES));
+      lbs.set(bi, lb);
+      lens.set(bi, len);
     }
-    const uint32_t rbase = lds_addr(ring) + wave * DEC_RING;
-    const uint8_t *rptr = ring + wave * DEC_RING;
-    // producer: next tile (pb, pt) to issue; consumer: next tile (cb, ct)
-    int pb = 0, pt = w0[0];
-    while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
-    int cb = pb, ct = pt;
-    int phead = 0, nin = 0, issued = 0;  // ring end of the newest tile, tiles and transfers out
-    int cpos = 0, consumed = 0;          // ring offset of tile (cb, ct), transfers consumed
-    while (cb < 4) {
-      while (pb < 4) {
-        const int sz = DG::foot(pb);
-        const int pos = phead + sz <= DEC_RING ? phead : 0;
-        bool ok = true;
-        if (nin > 0) {
-          if (cpos < phead)
-            ok = pos == phead || sz <= cpos;
-          else
-            ok = pos == phead && phead + sz <= cpos;
-        }
-        if (!ok) break;
-        tile_to_lds(cv.tile(s, pb, g, pt), rbase + pos, DG::tb(pb), DG::ni(pb));
-        phead = pos + sz;
-        issued += DG::ni(pb);
-        ++nin;
-        ++pt;
-        while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
-      }
-      consumed += DG::ni(cb);
-      wait_vm_le(issued - consumed);
-      const int lb = bounds[cb][0], len = bounds[cb][1];
+    auto mask = [&](int bi) {
       ColMask cm;
-      cm.lo = hm == TRIROUTE_FULL ? 0 : hm == TRIROUTE_LOCAL ? lb : 1;
-      cm.hi = hm == TRIROUTE_SKIP ? 0 : len - 1;
-      decode_tile<DH, G>(st, cv, cb, ct, rptr + cpos, cm, qop, qsum, a.scale2);
-      --nin;
-      const int chead = cpos + DG::foot(cb);
-      ++ct;
-      while (cb < 4 && ct >= w1[cb]) { ++cb; if (cb < 4) ct = w0[cb]; }
-      if (cb < 4) cpos = chead + DG::foot(cb) <= DEC_RING ? chead : 0;
+      cm.lo = hm == TRIROUTE_FULL ? 0 : hm == TRIROUTE_LOCAL ? lbs[bi] : 1;
+      cm.hi = hm == TRIROUTE_SKIP ? 0 : lens[bi] - 1;
+      return cm;
+    };
+    const uint8_t *rptr = ring + wave * DEC_RING;
+    const uint32_t rbase = lds_addr(ring) + wave * DEC_RING;
+    if constexpr (PACKED) {
+      // the lane's Q operand, kept only in the columns of key block blk
+      constexpr int NB = TS / 16, KS = DH / 32;
+      bf16x8 qopm[NB * KS];
+      const bf16x8 zero = as_op(u32x4{0u, 0u, 0u, 0u});
+#pragma unroll
+      for (int blk = 0; blk < NB; ++blk)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) qopm[blk * KS + ks] = (n16 >> 2) == blk ? qop[ks] : zero;
+      stream_tiles<DH, G>(cv, s, g, w0, w1, rptr, rbase, [&](int bi, int t, const uint8_t *tp) {
+        fold_dec_any<DH, G>(st, cv, bi, t, tp, mask(bi), qopm, qsum, a.scale2);
+      });
+      dec_finish<DH, G>(st);
+    } else {
+      stream_tiles<DH, G>(cv, s, g, w0, w1, rptr, rbase, [&](int bi, int t, const uint8_t *tp) {
+        fold_tile<DH, G>(st, cv, bi, t, tp, mask(bi), qop, qsum, a.scale2);
+      });
+      state_finish<DH, G>(st);
     }
-    state_finish<DH, G>(st);
   }
   // merge the waves in LDS (the rings are drained): [wave][col][m, l, O]
   __syncthreads();
@@ -710,6 +974,8 @@ struct PrefillArgs {
   float scale2;
 };
 
+// One wave per 16 compacted queries of a (sequence, head, mode) segment; it
+// walks the key range its queries need in every pool, tile by tile.
 template <int DH, int G>
 __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(PrefillArgs a) {
   const CacheView &cv = a.cv;
@@ -746,7 +1012,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(PrefillArgs a
   state_init(st);
   for (int bi = 0; bi < 4; ++bi) {
     const int len = cv.pool_len[s * 4 + bi];
-    const int32_t *pos = cv.pos + (int64_t(s) * 4 + bi) * cv.capacity;
+    const int32_t *pos = cv.pos_of(s, bi);
     const int sa = lower_bound_pos(pos, len, lo_all);
     const int sb = lower_bound_pos(pos, len, Pmax + 1);
     if (sa >= sb) continue;
@@ -798,21 +1064,20 @@ hipError_t launch_attn_mfma_decode(const triroute_cfg &cfg, const CacheView &cv,
   const int BH = B * cfg.n_heads;
   const int G = cfg.kv_group;
   const int threads = 64 * DEC_WAVES;
+  const bool packed = a.R <= 4;
+#define DEC_LAUNCH(DH_, G_)                                                  \
+  (packed ? attn_decode_kernel<DH_, G_, true><<<grid, threads, 0, st>>>(a)   \
+          : attn_decode_kernel<DH_, G_, false><<<grid, threads, 0, st>>>(a))
   if (cfg.head_dim == 64) {
-    if (G == 64)
-      attn_decode_kernel<64, 64><<<grid, threads, 0, st>>>(a);
-    else
-      attn_decode_kernel<64, 32><<<grid, threads, 0, st>>>(a);
+    if (G == 64) DEC_LAUNCH(64, 64); else DEC_LAUNCH(64, 32);
     if (a.NS > 1)
       attn_decode_combine_kernel<64><<<(BH + 3) / 4, 256, 0, st>>>(part, BH, a.NS, (bf16 *)o);
   } else {
-    if (G == 64)
-      attn_decode_kernel<128, 64><<<grid, threads, 0, st>>>(a);
-    else
-      attn_decode_kernel<128, 32><<<grid, threads, 0, st>>>(a);
+    if (G == 64) DEC_LAUNCH(128, 64); else DEC_LAUNCH(128, 32);
     if (a.NS > 1)
       attn_decode_combine_kernel<128><<<(BH + 3) / 4, 256, 0, st>>>(part, BH, a.NS, (bf16 *)o);
   }
+#undef DEC_LAUNCH
   return hipGetLastError();
 }
 

@@ -10,7 +10,7 @@ namespace tr {
 // First slot of pool (s, bi) whose position is >= p (positions ascend).
 __device__ __forceinline__ int pool_lower_bound(const CacheView &cv, int s, int bi, int len,
                                                 int p) {
-  const int32_t *pos = cv.pos + (int64_t(s) * 4 + bi) * cv.capacity;
+  const int32_t *pos = cv.pos_of(s, bi);
   int lo = 0, hi = len;
   while (lo < hi) {
     const int mid = (lo + hi) >> 1;

@@ -133,6 +133,10 @@ struct CacheView {
   int Hkv, dh, G, act_bytes;
   int64_t off_pool[4], tile_bytes[4];
 
+  // positions of pool (s, bi): one int32 per slot, n_tiles * TS slots per pool
+  __device__ __forceinline__ int32_t *pos_of(int s, int bi) const {
+    return pos + (int64_t(s) * 4 + bi) * (int64_t(n_tiles) * TS);
+  }
   __device__ __forceinline__ uint8_t *tile(int s, int bi, int g, int t) const {
     return base + off_pool[bi] + ((int64_t(s) * Hkv + g) * n_tiles + t) * tile_bytes[bi];
   }

@@ -60,7 +60,7 @@ __global__ __launch_bounds__(256) void kv_slots_kernel(CacheView cv, int T,
       int slot = run[bi] + __popcll(bal[bi] & lanemask_lt());
       for (int ww = 0; ww < w; ++ww) slot += wc[bi][ww];
       slots[int64_t(b) * T + t] = slot;
-      cv.pos[(int64_t(s) * 4 + bi) * cv.capacity + slot] = len0 + t;
+      cv.pos_of(s, bi)[slot] = len0 + t;
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) run[q] += wc[q][0] + wc[q][1] + wc[q][2] + wc[q][3];
@@ -235,7 +235,7 @@ __global__ void kv_export_kernel(CacheView cv, int seq, int bi, int slot0, int c
       ((uint32_t *)vout)[idx] = ve;
     }
     if (pos_out && c == 0 && g == 0)
-      pos_out[r] = live ? cv.pos[(int64_t(seq) * 4 + bi) * cv.capacity + slot] : 0;
+      pos_out[r] = live ? cv.pos_of(seq, bi)[slot] : 0;
   }
 }
 

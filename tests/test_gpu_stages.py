@@ -290,13 +290,15 @@ def test_attention_prefill(act, H, Hkv, dh, G, w, B, T):
         assert_close(og[b], ref, act, f"o[b={b}]")
 
 
-@pytest.mark.parametrize("act,H,Hkv,dh,G,w,ctx", [
-    ("f32", 4, 1, 64, 32, 32, 300),
-    ("bf16", 16, 4, 64, 64, 256, 1500),
-    ("bf16", 16, 4, 128, 64, 100, 2100),
+@pytest.mark.parametrize("act,H,Hkv,dh,G,w,ctx,B", [
+    ("f32", 4, 1, 64, 32, 32, 300, 5),
+    ("bf16", 16, 4, 64, 64, 256, 1500, 5),        # 4 heads per kv head, split into chunks
+    ("bf16", 16, 4, 128, 64, 100, 2100, 5),
+    ("bf16", 16, 2, 64, 32, 64, 700, 5),          # 8 heads per kv head: one head per column
+    ("bf16", 6, 3, 128, 32, 50, 900, 5),          # 2 heads per kv head
+    ("bf16", 8, 4, 64, 64, 96, 260, 64),          # one chunk per (sequence, kv head)
 ])
-def test_attention_decode(act, H, Hkv, dh, G, w, ctx):
-    B = 5
+def test_attention_decode(act, H, Hkv, dh, G, w, ctx, B):
     c = tr.make_cfg(256, H, Hkv, dh, w, 4, 1, 512, G, act)
     kk, vv = gen.kv_block(22, B * (ctx + 1), Hkv, dh, act, 0.8)
     kk, vv = kk.reshape(B, ctx + 1, Hkv, dh), vv.reshape(B, ctx + 1, Hkv, dh)
@@ -305,6 +307,8 @@ def test_attention_decode(act, H, Hkv, dh, G, w, ctx):
     modes = rng.choice(3, size=(B, H), p=[0.2, 0.4, 0.4]).astype(np.uint8)
     modes[0] = 0                                          # a sequence whose heads all skip
     modes[1] = 1                                          # all local
+    modes[2, 0] = 2                                       # mixed modes within a kv head
+    modes[2, 1:] = 0
     qq = gen.to_act(gen.normal(22, "dec_q", (B, H, dh), 0.8), act)
     cache = tr.KVCache(c, B, ctx + 4)
     # context in two appends (ragged), then the new token

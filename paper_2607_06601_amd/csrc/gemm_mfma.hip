@@ -26,30 +26,43 @@ struct MTile {
   int m0, n0, mvalid, e, p0;
 };
 
-// Map a linear row-tile index to (expert e >= 1, tile within e).
-__device__ __forceinline__ bool mmap_grouped(int bx, int BM, const int32_t *cnt,
-                                             const int32_t *off, int E, MTile &t) {
-  int rem = bx;
-  for (int e = 1; e <= E; ++e) {
-    const int c = cnt[e];
-    const int nt = (c + BM - 1) / BM;
-    if (rem < nt) {
-      t.e = e;
-      t.p0 = off[e - 1] + rem * BM;
-      t.mvalid = min(BM, c - rem * BM);
-      t.m0 = 0;
-      return true;
-    }
-    rem -= nt;
+// Row tiles of the grouped problems: lane e - 1 of every wave holds expert
+// e's row count and tile count, and an inclusive scan over the lanes gives
+// the tiles of experts 1..e, so the mapping costs one parallel load instead
+// of a chain of E dependent ones (E <= 63).
+struct GroupScan {
+  int c = 0, nt = 0, incl = 0, total = 0;
+};
+
+__device__ __forceinline__ GroupScan group_scan(int BM, const int32_t *cnt, int E) {
+  const int lane = threadIdx.x & 63;
+  GroupScan g;
+  g.c = lane < E ? cnt[lane + 1] : 0;
+  g.nt = (g.c + BM - 1) / BM;
+  int x = g.nt;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
   }
-  return false;
+  g.incl = x;
+  g.total = __shfl(x, 63, 64);
+  return g;
 }
 
-// Row tiles of all experts e = 1..E (the null expert 0 has no GEMM).
-__device__ __forceinline__ int grouped_row_tiles(int BM, const int32_t *cnt, int E) {
-  int n = 0;
-  for (int e = 1; e <= E; ++e) n += (cnt[e] + BM - 1) / BM;
-  return n;
+// Map a linear row-tile index to (expert e >= 1, tile within e).
+__device__ __forceinline__ bool mmap_grouped(int bx, int BM, const GroupScan &gs,
+                                             const int32_t *off, MTile &t) {
+  const uint64_t m = __ballot(gs.incl > bx);
+  if (!m) return false;
+  const int l = __ffsll((unsigned long long)m) - 1;
+  const int incl = __shfl(gs.incl, l, 64), nt = __shfl(gs.nt, l, 64), c = __shfl(gs.c, l, 64);
+  const int rem = bx - (incl - nt);
+  t.e = l + 1;
+  t.p0 = off[l] + rem * BM;
+  t.mvalid = min(BM, c - rem * BM);
+  t.m0 = 0;
+  return true;
 }
 
 // Physical column n of a BN-wide tile -> (pair index P in the tile, half).
@@ -84,8 +97,9 @@ struct QkvM {
   int N, Tq, d, H, Hkv, dh, Ncols;
   double inv_freq[64];
   static constexpr int out_cols(int BN) { return BN; }
-  __device__ int tiles(int BM, int ny) const { return (N + BM - 1) / BM * ny; }
-  __device__ bool map(int bx, int by, int BM, int BN, MTile &t) const {
+  static constexpr bool GROUPED = false;
+  __device__ int tiles(int BM, int ny, const GroupScan &) const { return (N + BM - 1) / BM * ny; }
+  __device__ bool map(int bx, int by, int BM, int BN, MTile &t, const GroupScan &) const {
     t.m0 = bx * BM;
     t.n0 = by * BN;
     t.mvalid = min(BM, N - t.m0);
@@ -112,11 +126,11 @@ struct QkvM {
   // item = (row, 8 consecutive pairs of one head): rotate-half RoPE on q and
   // k with the angle taken in fp64 and reduced to [-pi, pi] before an fp32
   // sincos; v is copied.
-  template <int BM, int NC, int LDC>
+  template <int BM, int NC, int LDC, int NT>
   __device__ void epilogue(const MTile &t, const float *C, int tid) const {
     constexpr int PC = NC / 16;  // 8-pair chunks per row
     const int Hd = H * dh, Kd = Hkv * dh, hd = dh >> 1;
-    for (int it = tid; it < BM * PC; it += 512) {
+    for (int it = tid; it < BM * PC; it += NT) {
       const int r = it / PC, P0 = (it % PC) * 8;
       const int lc1 = (P0 / hd) * dh + (P0 % hd);
       const int c1 = t.n0 + lc1;
@@ -169,8 +183,9 @@ struct OprojM {
   bf16 *xt;
   int N, d, K;
   static constexpr int out_cols(int BN) { return BN; }
-  __device__ int tiles(int BM, int ny) const { return (N + BM - 1) / BM * ny; }
-  __device__ bool map(int bx, int by, int BM, int BN, MTile &t) const {
+  static constexpr bool GROUPED = false;
+  __device__ int tiles(int BM, int ny, const GroupScan &) const { return (N + BM - 1) / BM * ny; }
+  __device__ bool map(int bx, int by, int BM, int BN, MTile &t, const GroupScan &) const {
     t.m0 = bx * BM;
     t.n0 = by * BN;
     t.mvalid = min(BM, N - t.m0);
@@ -182,10 +197,10 @@ struct OprojM {
     return t.n0 + n < d ? Wo + int64_t(t.n0 + n) * K : nullptr;
   }
   // item = 8 columns of one row: xt = x + o Wo^T
-  template <int BM, int NC, int LDC>
+  template <int BM, int NC, int LDC, int NT>
   __device__ void epilogue(const MTile &t, const float *C, int tid) const {
     constexpr int CC = NC / 8;
-    for (int it = tid; it < BM * CC; it += 512) {
+    for (int it = tid; it < BM * CC; it += NT) {
       const int r = it / CC, c8 = (it % CC) * 8;
       if (r >= t.mvalid || t.n0 + c8 >= d) continue;
       const int64_t off = int64_t(t.m0 + r) * d + t.n0 + c8;
@@ -208,9 +223,10 @@ struct Moe1M {
   const int32_t *cnt, *off, *rows;
   int E, k, d, dff;
   static constexpr int out_cols(int BN) { return BN / 2; }
-  __device__ int tiles(int BM, int ny) const { return grouped_row_tiles(BM, cnt, E) * ny; }
-  __device__ bool map(int bx, int by, int BM, int BN, MTile &t) const {
-    if (!mmap_grouped(bx, BM, cnt, off, E, t)) return false;
+  static constexpr bool GROUPED = true;
+  __device__ int tiles(int BM, int ny, const GroupScan &gs) const { return gs.total * ny; }
+  __device__ bool map(int bx, int by, int BM, int BN, MTile &t, const GroupScan &gs) const {
+    if (!mmap_grouped(bx, BM, gs, off, t)) return false;
     t.n0 = by * (BN / 2);  // BN/2 expert units per tile (gate + up columns)
     return true;
   }
@@ -226,10 +242,10 @@ struct Moe1M {
     return (half ? Wu : Wg) + (int64_t(t.e - 1) * dff + f) * d;
   }
   // item = 8 expert units of one assignment row (C holds silu(g) u)
-  template <int BM, int NC, int LDC>
+  template <int BM, int NC, int LDC, int NT>
   __device__ void epilogue(const MTile &t, const float *C, int tid) const {
     constexpr int CC = NC / 8;
-    for (int it = tid; it < BM * CC; it += 512) {
+    for (int it = tid; it < BM * CC; it += NT) {
       const int r = it / CC, c8 = (it % CC) * 8;
       if (r >= t.mvalid || t.n0 + c8 >= dff) continue;
       *(u32x4_t *)(Hm + int64_t(t.p0 + r) * dff + t.n0 + c8) = pack8_bf16(C + r * LDC + c8);
@@ -244,9 +260,10 @@ struct Moe2M {
   const int32_t *cnt, *off, *rows;
   int E, d, dff;
   static constexpr int out_cols(int BN) { return BN; }
-  __device__ int tiles(int BM, int ny) const { return grouped_row_tiles(BM, cnt, E) * ny; }
-  __device__ bool map(int bx, int by, int BM, int BN, MTile &t) const {
-    if (!mmap_grouped(bx, BM, cnt, off, E, t)) return false;
+  static constexpr bool GROUPED = true;
+  __device__ int tiles(int BM, int ny, const GroupScan &gs) const { return gs.total * ny; }
+  __device__ bool map(int bx, int by, int BM, int BN, MTile &t, const GroupScan &gs) const {
+    if (!mmap_grouped(bx, BM, gs, off, t)) return false;
     t.n0 = by * BN;
     return true;
   }
@@ -255,10 +272,10 @@ struct Moe2M {
     return t.n0 + n < d ? Wd + (int64_t(t.e - 1) * d + t.n0 + n) * dff : nullptr;
   }
   // item = 8 output features of one assignment, scattered to its slot row
-  template <int BM, int NC, int LDC>
+  template <int BM, int NC, int LDC, int NT>
   __device__ void epilogue(const MTile &t, const float *C, int tid) const {
     constexpr int CC = NC / 8;
-    for (int it = tid; it < BM * CC; it += 512) {
+    for (int it = tid; it < BM * CC; it += NT) {
       const int r = it / CC, c8 = (it % CC) * 8;
       if (r >= t.mvalid || t.n0 + c8 >= d) continue;
       float *y = Y + int64_t(rows[t.p0 + r]) * d + t.n0 + c8;
@@ -280,35 +297,64 @@ __device__ __forceinline__ int xcd_tile(int L, int total) {
   return x * per + min(x, extra) + (L >> 3);
 }
 
-template <class P, int BM, int WM, int WN, int S>
-__global__ __launch_bounds__(512, 1) void gemm_mfma_kernel(P p, int K, int ny) {
-  constexpr int BN = 64 * WN;
-  constexpr int TM = BM / WM;       // wave rows
-  constexpr int MI = TM / 16;       // 16-row MFMA tiles per wave
-  constexpr int STAGE = (BM + BN) * 128;
-  constexpr int IPW = (BM + BN) / 64;  // 1 KB transfers per wave per stage
-  static_assert(WM * WN == 8 && (BM + BN) % 64 == 0, "8 waves, whole transfers");
+// LDS chunk (16 bytes) of chunk c of operand row r in a stage whose rows are
+// CPR chunks long: a XOR with the row's position in its 256-byte bank span
+// makes the 16 rows read by one 16-lane phase (same c) hit 16 distinct
+// 16-byte bank groups.
+template <int CPR>
+__device__ __forceinline__ int swz(int r, int c) {
+  if constexpr (CPR == 8)
+    return c ^ ((r >> 1) & 7);  // 2 rows per 256-byte span
+  else
+    return c ^ ((r >> 2) & 3);  // 4 rows per span
+}
+
+// vmcnt(n * N) for the run-time n of stages still allowed in flight, n < S - 1
+template <int N, int S>
+__device__ __forceinline__ void wait_stages(int n) {
+  if constexpr (S > 5) if (n >= 4) { wait_vm<4 * N>(); return; }
+  if constexpr (S > 4) if (n == 3) { wait_vm<3 * N>(); return; }
+  if constexpr (S > 3) if (n == 2) { wait_vm<2 * N>(); return; }
+  if constexpr (S > 2) if (n == 1) { wait_vm<N>(); return; }
+  wait_vm<0>();
+}
+
+template <class P, int BM, int BN, int WM, int WN, int BK, int S>
+__global__ __launch_bounds__(64 * WM * WN, 1) void gemm_mfma_kernel(P p, int K, int ny) {
+  constexpr int NW = WM * WN, NT = 64 * NW;  // waves, threads
+  constexpr int TM = BM / WM, TN = BN / WN;  // wave tile
+  constexpr int MI = TM / 16, NI = TN / 16;  // 16 x 16 MFMA tiles per wave
+  constexpr int RB = BK * 2;                 // bytes per operand row per K step
+  constexpr int CPR = RB / 16;               // 16-byte chunks per row
+  constexpr int RPT = 1024 / RB;             // rows per 1 KB transfer
+  constexpr int STAGE = (BM + BN) * RB;
+  constexpr int IPW = STAGE / 1024 / NW;     // 1 KB transfers per wave per stage
+  static_assert(STAGE % (1024 * NW) == 0 && TN % 64 == 0, "whole transfers, 64-column slices");
+  static_assert(S >= 2 && S <= 6 && (BK == 32 || BK == 64), "pipeline shape");
   constexpr int NC = P::out_cols(BN), LDC = NC + 16;  // staged output tile (fp32)
   constexpr int SMEM = S * STAGE > BM * LDC * 4 ? S * STAGE : BM * LDC * 4;
   __shared__ __align__(1024) uint8_t smem[SMEM];
-  const int total = p.tiles(BM, ny);
+  GroupScan gs;
+  if constexpr (P::GROUPED) gs = group_scan(BM, p.cnt, p.E);
+  const int total = p.tiles(BM, ny, gs);
   if (int(blockIdx.x) >= total) return;
   const int t = xcd_tile(blockIdx.x, total);
   MTile tc;
-  if (!p.map(t / ny, t % ny, BM, BN, tc)) return;
+  if (!p.map(t / ny, t % ny, BM, BN, tc, gs)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  // Transfer j of this wave fills stage rows 8 g .. 8 g + 7 (g = wave IPW + j;
-  // A rows first, then B rows).  Lane l writes LDS chunk l % 8 of row
-  // 8 g + l / 8, which holds source chunk (l % 8) ^ (row & 7).  Rows past the
-  // valid rows (or past the weight's columns) read a valid row instead: their
-  // products land in accumulator rows/columns the epilogue never stores.
+  // Transfer j of this wave fills stage rows RPT g .. RPT g + RPT - 1
+  // (g = wave IPW + j; A rows first, then B rows).  Lane l writes LDS chunk
+  // l % CPR of row RPT g + l / CPR, which holds the source chunk that swz
+  // maps there.  Rows past the valid rows (or past the weight's columns)
+  // read a valid row instead: their products land in accumulator rows /
+  // columns the epilogue never stores.
   const uint8_t *src[IPW];
   const bf16 *b_fallback = p.b_row(tc, 0);
 #pragma unroll
   for (int j = 0; j < IPW; ++j) {
-    const int rr = 8 * (wave * IPW + j) + (lane >> 3);
-    const int c = (lane & 7) ^ (rr & 7);
+    const int rr = RPT * (wave * IPW + j) + lane / CPR;
+    const int c = swz<CPR>(rr, lane % CPR);  // swz is an involution in c
     const bf16 *row;
     if (rr < BM) {
       row = p.a_row(tc, rr < tc.mvalid ? rr : 0);
@@ -321,51 +367,47 @@ __global__ __launch_bounds__(512, 1) void gemm_mfma_kernel(P p, int K, int ny) {
   const uint32_t sbase = lds_addr(smem) + wave * IPW * 1024;
   auto issue = [&](int kt, int stage) {
 #pragma unroll
-    for (int j = 0; j < IPW; ++j) dma16(src[j] + kt * 128, sbase + stage * STAGE + j * 1024);
+    for (int j = 0; j < IPW; ++j) dma16(src[j] + kt * RB, sbase + stage * STAGE + j * 1024);
   };
-  f32x4_t acc[MI][4];
+  f32x4_t acc[MI][NI];
 #pragma unroll
   for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  const int nk = K / 64;
+    for (int j = 0; j < NI; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int nk = K / BK;
 #pragma unroll
   for (int s0 = 0; s0 < S - 1; ++s0)
     if (s0 < nk) issue(s0, s0);
   for (int kt = 0; kt < nk; ++kt) {
     // stage kt has landed once at most the later stages' transfers are out
-    if constexpr (S >= 3) {
-      if (kt + 1 < nk) wait_vm<IPW>(); else wait_vm<0>();
-    } else {
-      wait_vm<0>();
-    }
+    wait_stages<IPW, S>(min(S - 2, nk - 1 - kt));
     __syncthreads();  // every wave's part of stage kt is in; stage kt-1 is free
     if (kt + S - 1 < nk) issue(kt + S - 1, (kt + S - 1) % S);
     const uint8_t *As = smem + (kt % S) * STAGE;
-    const uint8_t *Bs = As + BM * 128;
+    const uint8_t *Bs = As + BM * RB;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int ks = 0; ks < BK / 32; ++ks) {
       const int ch = ks * 4 + (lane >> 4);
-      bf16x8_t b[4];
+      bf16x8_t b[NI];
 #pragma unroll
-      for (int ni = 0; ni < 4; ++ni) {
-        const int n = wn * 64 + ni * 16 + (lane & 15);
-        b[ni] = *(const bf16x8_t *)(Bs + n * 128 + ((ch ^ (n & 7)) << 4));
+      for (int ni = 0; ni < NI; ++ni) {
+        const int n = wn * TN + ni * 16 + (lane & 15);
+        b[ni] = *(const bf16x8_t *)(Bs + n * RB + (swz<CPR>(n, ch) << 4));
       }
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi) {
         const int r = wm * TM + mi * 16 + (lane & 15);
-        const bf16x8_t a = *(const bf16x8_t *)(As + r * 128 + ((ch ^ (r & 7)) << 4));
+        const bf16x8_t a = *(const bf16x8_t *)(As + r * RB + (swz<CPR>(r, ch) << 4));
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
+        for (int ni = 0; ni < NI; ++ni)
           acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[ni], acc[mi][ni], 0, 0, 0);
       }
     }
   }
   // Epilogue.  Register pass: lane holds rows 4 (lane/16) + i of each 16-row
-  // tile and column (lane % 16) of each 16-column block; partner columns
-  // (ni, ni + 2) are combined for SwiGLU and kept apart for RoPE.  Then the
-  // problem's row-wise pass reads the staged tile.
+  // tile and column (lane % 16) of each 16-column block; in each 64-column
+  // slice the partner columns (ni, ni + 2) are combined for SwiGLU and kept
+  // apart for RoPE.  Then the problem's row-wise pass reads the staged tile.
   __syncthreads();  // every wave is done with the operand stages
   float *C = (float *)smem;
 #pragma unroll
@@ -375,11 +417,14 @@ __global__ __launch_bounds__(512, 1) void gemm_mfma_kernel(P p, int K, int ny) {
       const int r = wm * TM + mi * 16 + 4 * (lane >> 4) + i;
       if constexpr (P::EPI == EPI_PLAIN) {
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni) C[r * LDC + wn * 64 + ni * 16 + (lane & 15)] = acc[mi][ni][i];
+        for (int ni = 0; ni < NI; ++ni)
+          C[r * LDC + wn * TN + ni * 16 + (lane & 15)] = acc[mi][ni][i];
       } else {
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni) {
-          const int Pp = wn * 32 + ni * 16 + (lane & 15);
+        for (int ni = 0; ni < NI; ++ni) {
+          if ((ni & 3) >= 2) continue;
+          int Pp, half;
+          col_pair(wn * TN + ni * 16 + (lane & 15), Pp, half);
           const float g = acc[mi][ni][i], u = acc[mi][ni + 2][i];
           if constexpr (P::EPI == EPI_SWIGLU) {
             C[r * LDC + Pp] = g / (1.0f + expf(-g)) * u;
@@ -391,16 +436,17 @@ __global__ __launch_bounds__(512, 1) void gemm_mfma_kernel(P p, int K, int ny) {
       }
     }
   __syncthreads();
-  p.template epilogue<BM, NC, LDC>(tc, C, tid);
+  p.template epilogue<BM, NC, LDC, NT>(tc, C, tid);
 }
 
 // ------------------------------------------------------------------ launchers
 // m_tiles bounds the row tiles (for grouped problems: the most any routing
 // can need); the kernel takes the actual count from the problem.
-template <class P, int BM, int WM, int WN, int S>
+template <class P, int BM, int BN, int WM, int WN, int BK, int S>
 static hipError_t launch(const P &p, int K, int m_tiles, int n_tiles, hipStream_t st) {
   if (m_tiles > 0 && n_tiles > 0)
-    gemm_mfma_kernel<P, BM, WM, WN, S><<<m_tiles * n_tiles, 512, 0, st>>>(p, K, n_tiles);
+    gemm_mfma_kernel<P, BM, BN, WM, WN, BK, S>
+        <<<m_tiles * n_tiles, 64 * WM * WN, 0, st>>>(p, K, n_tiles);
   return hipGetLastError();
 }
 
@@ -428,7 +474,7 @@ hipError_t mfma_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
     p.inv_freq[j] = j < cfg.head_dim / 2
                         ? pow(double(cfg.rope_theta), -2.0 * j / double(cfg.head_dim))
                         : 0.0;
-  return launch<QkvM, 256, 4, 2, 3>(p, cfg.d_model, (p.N + 255) / 256, (p.Ncols + 127) / 128, st);
+  return launch<QkvM, 256, 128, 4, 2, 64, 3>(p, cfg.d_model, (p.N + 255) / 256, (p.Ncols + 127) / 128, st);
 }
 
 hipError_t mfma_oproj(const triroute_cfg &cfg, int N, const void *x, const void *o,
@@ -441,7 +487,7 @@ hipError_t mfma_oproj(const triroute_cfg &cfg, int N, const void *x, const void 
   p.N = N;
   p.d = cfg.d_model;
   p.K = cfg.n_heads * cfg.head_dim;
-  return launch<OprojM, 256, 4, 2, 3>(p, p.K, (N + 255) / 256, (p.d + 127) / 128, st);
+  return launch<OprojM, 256, 128, 4, 2, 64, 3>(p, p.K, (N + 255) / 256, (p.d + 127) / 128, st);
 }
 
 hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const triroute_moe_w &w,
@@ -460,7 +506,7 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
   p1.k = k;
   p1.d = d;
   p1.dff = dff;
-  hipError_t err = launch<Moe1M, 256, 2, 4, 2>(p1, d, Nk / 256 + E, (dff + 127) / 128, st);
+  hipError_t err = launch<Moe1M, 256, 256, 2, 4, 64, 2>(p1, d, Nk / 256 + E, (dff + 127) / 128, st);
   if (err != hipSuccess) return err;
   Moe2M p2;
   p2.Hm = (const bf16 *)Hm;
@@ -472,7 +518,7 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
   p2.E = E;
   p2.d = d;
   p2.dff = dff;
-  return launch<Moe2M, 256, 4, 2, 3>(p2, dff, Nk / 256 + E, (d + 127) / 128, st);
+  return launch<Moe2M, 256, 128, 4, 2, 64, 3>(p2, dff, Nk / 256 + E, (d + 127) / 128, st);
 }
 
 }  // namespace tr

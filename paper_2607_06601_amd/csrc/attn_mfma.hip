@@ -324,46 +324,6 @@ __device__ __forceinline__ void process_tile(SoftState<DH> &st,
   }
 }
 
-// Walk this wave's tiles [t_begin, t_end) (stride `step`) of pool bi, loading
-// each straight from HBM into registers (kpos: the pool's slot positions).  Narrow
-// pools without position keys keep the next tile in flight while the current
-// one is processed; otherwise all of a tile's loads are issued at once.
-template <int DH, int BP, int G, bool POS>
-__device__ void run_pool(SoftState<DH> &st, const CacheView &cv, int s, int bi, int g,
-                         int t_begin, int t_end, int step, const int32_t *kpos, int klen,
-                         ColMask cm, const bf16x8 *qop, const float *qsum, float scale2) {
-  if (t_begin >= t_end) return;
-  TileRegs<DH, BP, G, POS> cur;
-  if constexpr (BP <= 4 && !POS) {
-    TileRegs<DH, BP, G, POS> nxt;
-    cur.load(cv.tile(s, bi, g, t_begin), cv, bi, t_begin * cv.TS, kpos + t_begin * cv.TS, klen);
-    for (int t = t_begin; t < t_end; t += step) {
-      const bool more = t + step < t_end;
-      if (more) nxt.load(cv.tile(s, bi, g, t + step), cv, bi, (t + step) * cv.TS, kpos + (t + step) * cv.TS, klen);
-      process_tile<DH, BP, G, POS>(st, cur, t * cv.TS, cm, qop, qsum, scale2);
-      if (more) cur = nxt;
-    }
-  } else {
-    for (int t = t_begin; t < t_end; t += step) {
-      cur.load(cv.tile(s, bi, g, t), cv, bi, t * cv.TS, kpos ? kpos + t * cv.TS : nullptr, klen);
-      process_tile<DH, BP, G, POS>(st, cur, t * cv.TS, cm, qop, qsum, scale2);
-    }
-  }
-}
-
-template <int DH, int G, bool POS>
-__device__ __forceinline__ void run_pool_any(SoftState<DH> &st, const CacheView &cv, int s,
-                                             int bi, int g, int t0, int t1, int step,
-                                             const int32_t *kpos, int klen, ColMask cm,
-                                             const bf16x8 *qop, const float *qsum, float scale2) {
-  switch (bi) {
-    case 0: run_pool<DH, 2, G, POS>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
-    case 1: run_pool<DH, 4, G, POS>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
-    case 2: run_pool<DH, 8, G, POS>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
-    default: run_pool<DH, 16, G, POS>(st, cv, s, bi, g, t0, t1, step, kpos, klen, cm, qop, qsum, scale2); break;
-  }
-}
-
 // First index in [0, len) with pos[index] >= p (pos ascending), searched by
 // the whole wave: each round probes 64 evenly spaced entries and narrows the
 // range 64-fold, so a 32k-entry pool takes two rounds of parallel loads.
@@ -970,55 +930,141 @@ struct PrefillArgs {
   const bf16 *q;
   const int32_t *seq_ids, *cnt, *idx;
   bf16 *o;
-  int B, T, H, R, w, QT;  // QT = 16-query tiles per segment (ceil(T / 16))
+  int B, T, H, Hkv, R, NQ, w, QT;  // NQ = head quartets per kv head, QT = ceil(T / 16)
   float scale2;
 };
 
-// One wave per 16 compacted queries of a (sequence, head, mode) segment; it
-// walks the key range its queries need in every pool, tile by tile.
+// Prefill: one block of 4 waves per (sequence, kv head, head quartet, mode,
+// query tile qt): wave i takes the qt-th 16 compacted queries of head
+// 4 quartet + i of the kv head.  Those queries sit at similar positions, so
+// the block streams the union of their key ranges from every pool once,
+// tile by tile, through a shared LDS ring (each tile with its slots' key
+// positions; direct-to-LDS transfers split over the waves, D - 1 tiles
+// ahead) and every wave folds every tile with its own position masks.
+constexpr int PF_WAVES = 4;
+constexpr int PF_D = 4;  // ring slots
+
 template <int DH, int G>
 __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(PrefillArgs a) {
+  using SG = StreamGeo<DH, G>;
+  constexpr int TS = 4096 / DH;
+  constexpr int SLOT = (1024 * 16 + 4 * TS + 255) & ~255;  // widest tile + its positions
+  __shared__ __align__(1024) uint8_t ring[PF_D * SLOT];
+  __shared__ int bounds[4][3];  // per pool: first tile, end tile, length
   const CacheView &cv = a.cv;
   const int lane = threadIdx.x & 63, n16 = lane & 15, o4 = lane >> 4;
-  const int64_t item = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  const int nseg = a.B * a.H * 2;
-  if (item >= int64_t(nseg) * a.QT) return;
-  // heavy tiles first: full-mode segments, latest query tiles first
-  const int seg_rank = int(item / a.QT), qt = a.QT - 1 - int(item % a.QT);
-  const int half = a.B * a.H;
-  const int seg = seg_rank < half ? 2 * seg_rank + 1 : 2 * (seg_rank - half);
-  const int count = a.cnt[seg];
-  if (qt * 16 >= count) return;
-  const int b = seg / (2 * a.H), h = (seg >> 1) % a.H, m = (seg & 1) + 1;
-  const int g = h / a.R;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // heavy blocks first: full mode, latest query tiles first
+  const int per_mode = a.B * a.Hkv * a.NQ * a.QT;
+  const int m = int(blockIdx.x) < per_mode ? TRIROUTE_FULL : TRIROUTE_LOCAL;
+  int r = int(blockIdx.x) % per_mode;
+  const int qt = a.QT - 1 - r % a.QT;
+  r /= a.QT;
+  const int quart = r % a.NQ;
+  r /= a.NQ;
+  const int g = r % a.Hkv, b = r / a.Hkv;
   const int s = a.seq_ids ? a.seq_ids[b] : b;
   if (s < 0 || s >= cv.n_seq) return;
   const int base = cv.seq_len[s] - a.T;
+  // union of the quartet's key ranges (every wave computes it; block-uniform)
+  int lo_u = INT_MAX, hi_u = -1;
+  for (int k = 0; k < PF_WAVES && quart * PF_WAVES + k < a.R; ++k) {
+    const int sg = (b * a.H + g * a.R + quart * PF_WAVES + k) * 2 + (m - 1);
+    const int ck = a.cnt[sg];
+    if (qt * 16 >= ck) continue;
+    const int32_t *lk = a.idx + int64_t(sg) * a.T;
+    const int pmin = base + lk[qt * 16], pmax = base + lk[min(qt * 16 + 15, ck - 1)];
+    lo_u = min(lo_u, m == TRIROUTE_LOCAL ? pmin - a.w + 1 : 0);
+    hi_u = max(hi_u, pmax);
+  }
+  lo_u = __builtin_amdgcn_readfirstlane(lo_u);
+  hi_u = __builtin_amdgcn_readfirstlane(hi_u);
+  if (hi_u < 0) return;
+  {  // wave w finds the tile range of pool w
+    const int bi = wave;
+    const int len = cv.pool_len[s * 4 + bi];
+    const int32_t *pos = cv.pos_of(s, bi);
+    const int sa = lower_bound_pos(pos, len, lo_u);
+    const int sb = lower_bound_pos(pos, len, hi_u + 1);
+    if (lane == 0) {
+      bounds[bi][0] = sa < sb ? sa / TS : 0;
+      bounds[bi][1] = sa < sb ? (sb + TS - 1) / TS : 0;
+      bounds[bi][2] = len;
+    }
+  }
+  // this wave's queries
+  const int hr = quart * PF_WAVES + wave;
+  const int h = g * a.R + hr;
+  const int seg = (b * a.H + h) * 2 + (m - 1);
+  const int count = hr < a.R ? a.cnt[seg] : 0;
+  const bool wv = qt * 16 < count;  // wave-uniform
   const int j = qt * 16 + n16;
-  const bool valid = j < count;
-  const int* lst = a.idx + int64_t(seg) * a.T;
-  const int t = valid ? lst[j] : lst[count - 1];
+  const bool valid = wv && j < count;
+  const int32_t *lst = a.idx + int64_t(seg) * a.T;
+  const int t = valid ? lst[j] : (wv ? lst[count - 1] : 0);
   const int P = base + t;
-  const int Pmax = base + lst[min(qt * 16 + 15, count - 1)];
-  const int Pmin = base + lst[qt * 16];
   bf16x8 qop[DH / 32];
   float qsum[DH / G];
-  load_q<DH, G>(a.q + (int64_t(b * a.T + t) * a.H + h) * DH, valid, qop, qsum);
+  load_q<DH, G>(a.q + (int64_t(b * a.T + t) * a.H + (hr < a.R ? h : 0)) * DH, valid, qop, qsum);
   ColMask cm;
   cm.lo = valid ? (m == TRIROUTE_LOCAL ? P - a.w + 1 : 0) : 1;
   cm.hi = valid ? P : 0;
-  const int lo_all = m == TRIROUTE_LOCAL ? Pmin - a.w + 1 : 0;
   SoftState<DH> st;
   state_init(st);
+  wait_vm<0>();  // from here on the only vector-memory traffic is the tile stream
+  __syncthreads();
+  Int4 w0, w1, lens;
+  int n = 0;
   for (int bi = 0; bi < 4; ++bi) {
-    const int len = cv.pool_len[s * 4 + bi];
-    const int32_t *pos = cv.pos_of(s, bi);
-    const int sa = lower_bound_pos(pos, len, lo_all);
-    const int sb = lower_bound_pos(pos, len, Pmax + 1);
-    if (sa >= sb) continue;
-    run_pool_any<DH, G, true>(st, cv, s, bi, g, sa / cv.TS, (sb + cv.TS - 1) / cv.TS, 1, pos, len,
-                              cm, qop, qsum, a.scale2);
+    w0.set(bi, bounds[bi][0]);
+    w1.set(bi, bounds[bi][1]);
+    lens.set(bi, bounds[bi][2]);
+    n += bounds[bi][1] - bounds[bi][0];
   }
+  // transfers of a width-bi tile: ni(bi) code/scale blocks + 1 for the positions;
+  // transfer x is issued by wave x % PF_WAVES
+  auto own = [&](int bi) { return max(0, (SG::ni(bi) + 1 - wave + PF_WAVES - 1) / PF_WAVES); };
+  const uint32_t rbase = lds_addr(ring);
+  int pb = 0, pt = w0[0];  // next tile to issue
+  while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
+  int cb = pb, ct = pt;    // next tile to fold
+  int issued = 0, consumed = 0;  // this wave's transfers
+  auto issue = [&](int slot) {
+    const uint8_t *src = cv.tile(s, pb, g, pt);
+    const uint32_t dst = rbase + slot * SLOT;
+    const int tb = SG::tb(pb), ni = SG::ni(pb);
+    for (int x = wave; x < ni; x += PF_WAVES)
+      if (x * 1024 + lane * 16 < tb) dma16(src + x * 1024 + lane * 16, dst + x * 1024);
+    if (ni % PF_WAVES == wave && lane < TS / 4)
+      dma16(cv.pos_of(s, pb) + pt * TS + 4 * lane, dst + tb);
+    issued += own(pb);
+    ++pt;
+    while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
+  };
+  for (int i = 0; i < PF_D - 1 && i < n; ++i) issue(i);
+  for (int i = 0; i < n; ++i) {
+    consumed += own(cb);
+    wait_vm_le(issued - consumed);
+    __syncthreads();  // tile i is in from every wave; slot (i - 1) % D is free
+    if (i + PF_D - 1 < n) issue((i + PF_D - 1) % PF_D);
+    if (wv) {
+      const uint8_t *tp = ring + (i % PF_D) * SLOT;
+      const int32_t *kp = (const int32_t *)(tp + SG::tb(cb));
+      switch (cb) {
+        case 0: { TileRegs<DH, 2, G, true> rg; rg.load(tp, cv, 0, ct * TS, kp, lens[0]);
+                  process_tile<DH, 2, G, true>(st, rg, ct * TS, cm, qop, qsum, a.scale2); } break;
+        case 1: { TileRegs<DH, 4, G, true> rg; rg.load(tp, cv, 1, ct * TS, kp, lens[1]);
+                  process_tile<DH, 4, G, true>(st, rg, ct * TS, cm, qop, qsum, a.scale2); } break;
+        case 2: { TileRegs<DH, 8, G, true> rg; rg.load(tp, cv, 2, ct * TS, kp, lens[2]);
+                  process_tile<DH, 8, G, true>(st, rg, ct * TS, cm, qop, qsum, a.scale2); } break;
+        default: { TileRegs<DH, 16, G, true> rg; rg.load(tp, cv, 3, ct * TS, kp, lens[3]);
+                   process_tile<DH, 16, G, true>(st, rg, ct * TS, cm, qop, qsum, a.scale2); } break;
+      }
+    }
+    ++ct;
+    while (cb < 4 && ct >= w1[cb]) { ++cb; if (cb < 4) ct = w0[cb]; }
+  }
+  if (!wv) return;
   state_finish<DH, G>(st);
   // normalise and write: lane (o4, n) holds column 4 o4 + i, channel n + 16 cb
 #pragma unroll
@@ -1031,7 +1077,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(PrefillArgs a
     const float inv = lc > 0.f ? 1.f / lc : 0.f;
     bf16 *orow = a.o + (int64_t(b * a.T + tt) * a.H + h) * DH;
 #pragma unroll
-    for (int cb = 0; cb < DH / 16; ++cb) orow[n16 + 16 * cb] = f2bf(st.O[cb][i] * inv);
+    for (int cbk = 0; cbk < DH / 16; ++cbk) orow[n16 + 16 * cbk] = f2bf(st.O[cbk][i] * inv);
   }
 }
 
@@ -1097,20 +1143,22 @@ hipError_t launch_attn_mfma_prefill(const triroute_cfg &cfg, const CacheView &cv
   a.R = cfg.n_heads / cfg.n_kv_heads;
   a.w = cfg.window;
   a.QT = (T + 15) / 16;
+  a.Hkv = cfg.n_kv_heads;
+  a.NQ = (a.R + PF_WAVES - 1) / PF_WAVES;
   a.scale2 = LOG2E / sqrtf(float(cfg.head_dim));
-  const int64_t items = int64_t(B) * cfg.n_heads * 2 * a.QT;
-  dim3 grid(unsigned((items + 3) / 4));
+  const int64_t blocks = int64_t(B) * a.Hkv * a.NQ * 2 * a.QT;
+  const dim3 grid{unsigned(blocks)};
   const int G = cfg.kv_group;
   if (cfg.head_dim == 64) {
     if (G == 64)
-      attn_prefill_mfma_kernel<64, 64><<<grid, 256, 0, st>>>(a);
+      attn_prefill_mfma_kernel<64, 64><<<grid, 64 * PF_WAVES, 0, st>>>(a);
     else
-      attn_prefill_mfma_kernel<64, 32><<<grid, 256, 0, st>>>(a);
+      attn_prefill_mfma_kernel<64, 32><<<grid, 64 * PF_WAVES, 0, st>>>(a);
   } else {
     if (G == 64)
-      attn_prefill_mfma_kernel<128, 64><<<grid, 256, 0, st>>>(a);
+      attn_prefill_mfma_kernel<128, 64><<<grid, 64 * PF_WAVES, 0, st>>>(a);
     else
-      attn_prefill_mfma_kernel<128, 32><<<grid, 256, 0, st>>>(a);
+      attn_prefill_mfma_kernel<128, 32><<<grid, 64 * PF_WAVES, 0, st>>>(a);
   }
   return hipGetLastError();
 }

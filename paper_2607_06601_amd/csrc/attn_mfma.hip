@@ -39,64 +39,98 @@ constexpr float LOG2E = 1.4426950408889634f;
 __device__ __forceinline__ bf16x8 as_op(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 __device__ __forceinline__ f16x8 as_h(u32x4 v) { return __builtin_bit_cast(f16x8, v); }
 
-// V field of a quantized pool -> fp16 operand holding the code itself:
-// 0x6400 | code is fp16(1024 + code), and a packed fp16 subtraction of 1024
-// is exact.  (A large constant left in the operand would be summed over the
-// whole key range in the fp32 accumulator.)
+// Code fields -> MFMA operands.  A code c below 2^7 becomes bf16 128 + c as
+// the 16-bit pattern [c, 0x43] (low byte first); a code below 2^8 becomes
+// fp16 1024 + c as [c, 0x64].  Codes are first spread one per byte, then one
+// byte permute (v_perm_b32) per operand pair places two codes beside the
+// constant bytes.  Selectors: result bytes 0..3 take bytes (0|1, 4, 2|3, 4)
+// of (codes, constant): 0x04020400 pairs bytes 0 and 2, 0x04030401 bytes 1
+// and 3.
+constexpr uint32_t SEL02 = 0x04020400u, SEL13 = 0x04030401u;
+constexpr uint32_t BF16_128 = 0x43434343u, F16_1024 = 0x64646464u;
+
+// Eight codes of field f of a lane record (2, 4 or 8 bits) as four operand
+// pairs with constant byte K (the BF16_128 or F16_1024 pattern).  Element q
+// of a record sits in word (q/2) / (16/bp) at bit ((q/2) % (16/bp)) bp +
+// (q % 2) 16, so pair p of field f is at bits s and 16 + s of one word.
 template <int BP>
-__device__ __forceinline__ f16x8 vfield_h(const uint32_t *w, int f) {
+__device__ __forceinline__ u32x4 code_pairs(const uint32_t *w, int f, uint32_t K) {
   u32x4 r;
   if constexpr (BP == 2) {
-    const uint32_t x = w[f >> 1] >> ((f & 1) * 8);
+    // word f/2 holds fields f & ~1 (bytes 0, 2) and f | 1 (bytes 1, 3)
+    const uint32_t x = w[f >> 1];
+    const uint32_t sel = (f & 1) ? SEL13 : SEL02;
 #pragma unroll
-    for (int p = 0; p < 4; ++p) r[p] = ((x >> (2 * p)) & 0x00030003u) | 0x64006400u;
+    for (int p = 0; p < 4; ++p) r[p] = __builtin_amdgcn_perm(K, (x >> (2 * p)) & 0x03030303u, sel);
   } else if constexpr (BP == 4) {
     const uint32_t x = w[f];
-#pragma unroll
-    for (int p = 0; p < 4; ++p) r[p] = ((x >> (4 * p)) & 0x000F000Fu) | 0x64006400u;
+    const uint32_t lo = x & 0x0F0F0F0Fu, hi = (x >> 4) & 0x0F0F0F0Fu;
+    r[0] = __builtin_amdgcn_perm(K, lo, SEL02);
+    r[1] = __builtin_amdgcn_perm(K, hi, SEL02);
+    r[2] = __builtin_amdgcn_perm(K, lo, SEL13);
+    r[3] = __builtin_amdgcn_perm(K, hi, SEL13);
   } else {
 #pragma unroll
     for (int p = 0; p < 4; ++p)
-      r[p] = ((w[2 * f + (p >> 1)] >> ((p & 1) * 8)) & 0x00FF00FFu) | 0x64006400u;
+      r[p] = __builtin_amdgcn_perm(K, w[2 * f + (p >> 1)], (p & 1) ? SEL13 : SEL02);
   }
-  const f16x8 k1024 = {1024, 1024, 1024, 1024, 1024, 1024, 1024, 1024};
-  return as_h(r) - k1024;
+  return r;
 }
 
-// bf16 pair from two small integer codes held at bits 0 and 16 of x.
-__device__ __forceinline__ uint32_t pair_small(uint32_t x) { return x | 0x43004300u; }
+// V field of a quantized pool -> fp16 operand holding the code itself: the
+// packed fp16 subtraction of 1024 is exact.  (A large constant left in the
+// operand would be summed over the whole key range in the fp32 accumulator.)
+template <int BP>
+__device__ __forceinline__ f16x8 vfield_h(const uint32_t *w, int f) {
+  const f16x8 k1024 = {1024, 1024, 1024, 1024, 1024, 1024, 1024, 1024};
+  return as_h(code_pairs<BP>(w, f, F16_1024)) - k1024;
+}
+
 // exact bf16 pair of two 8-bit codes at bits 0..7 and 16..23
 __device__ __forceinline__ uint32_t pair_byte(uint32_t x) {
   const float lo = float(x & 0xFFu), hi = float((x >> 16) & 0xFFu);
   return (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
 }
 
-// Eight elements (field f) of a lane record -> MFMA operand.  Small codes
-// become bf16(128 + code) (the 128 is removed algebraically).
+// K field -> bf16 operand of S^T = K Q^T.  2- and 4-bit codes: 128 + code
+// (the offset is removed algebraically with the Q sums); 8-bit codes: the
+// code itself; 16-bit: the stored values.
 template <int BP>
-__device__ __forceinline__ bf16x8 field_op(const uint32_t *w, int f) {
-  u32x4 r;
-  if constexpr (BP == 2) {
-    const uint32_t x = w[f >> 1] >> ((f & 1) * 8);
-#pragma unroll
-    for (int p = 0; p < 4; ++p) r[p] = pair_small((x >> (2 * p)) & 0x00030003u);
-  } else if constexpr (BP == 4) {
-    const uint32_t x = w[f];
-#pragma unroll
-    for (int p = 0; p < 4; ++p) r[p] = pair_small((x >> (4 * p)) & 0x000F000Fu);
+__device__ __forceinline__ u32x4 kfield(const uint32_t *w, int f) {
+  if constexpr (BP <= 4) {
+    return code_pairs<BP>(w, f, BF16_128);
   } else if constexpr (BP == 8) {
+    u32x4 r;
 #pragma unroll
-    for (int p = 0; p < 4; ++p) r[p] = pair_byte((w[2 * f + (p >> 1)] >> ((p & 1) * 8)) & 0x00FF00FFu);
+    for (int p = 0; p < 4; ++p)
+      r[p] = pair_byte((w[2 * f + (p >> 1)] >> ((p & 1) * 8)) & 0x00FF00FFu);
+    return r;
   } else {
+    u32x4 r;
 #pragma unroll
     for (int p = 0; p < 4; ++p) r[p] = w[4 * f + p];
+    return r;
   }
+}
+
+// 16-bit pool V field: the stored bf16 values.
+__device__ __forceinline__ bf16x8 field16(const uint32_t *w, int f) {
+  u32x4 r;
+#pragma unroll
+  for (int p = 0; p < 4; ++p) r[p] = w[4 * f + p];
   return as_op(r);
+}
+
+// One K-field product into acc.
+template <int BP>
+__device__ __forceinline__ f32x4 kmfma(const uint32_t *w, int f, const bf16x8 &q, f32x4 acc) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_op(kfield<BP>(w, f)), q, acc, 0, 0, 0);
 }
 
 template <int BP> struct PoolTraits {
   static constexpr int WORDS = 2 * BP;               // 32-bit words per lane record
-  static constexpr float OFF = BP <= 4 ? 128.f : 0.f;  // code offset inside the operand
+  // code offset inside the K operand (bf16 128 + c for 2 and 4 bits)
+  static constexpr float OFF = BP <= 4 ? 128.f : 0.f;
   static constexpr bool QUANT = BP < 16;
 };
 
@@ -231,9 +265,7 @@ __device__ __forceinline__ void process_tile(SoftState<DH> &st,
       for (int g = 0; g < NG; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < Gm::KS; ++ks) {
-        const bf16x8 a = field_op<BP>(tr.k.w, blk * Gm::KS + ks);
-        acc[ks / gks] =
-            __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qop[ks], acc[ks / gks], 0, 0, 0);
+        acc[ks / gks] = kmfma<BP>(tr.k.w, blk * Gm::KS + ks, qop[ks], acc[ks / gks]);
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -317,7 +349,7 @@ __device__ __forceinline__ void process_tile(SoftState<DH> &st,
         const f16x8 bv = vfield_h<BP>(tr.v.w, kv * Gm::CB + cb);
         st.O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_h(pk[g]), bv, st.O[cb], 0, 0, 0);
       } else {
-        const bf16x8 bv = field_op<BP>(tr.v.w, kv * Gm::CB + cb);
+        const bf16x8 bv = field16(tr.v.w, kv * Gm::CB + cb);
         st.O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_op(pk[g]), bv, st.O[cb], 0, 0, 0);
       }
     }
@@ -360,8 +392,9 @@ __device__ __forceinline__ void load_q(const bf16 *qrow, bool valid, bf16x8 *qop
     qop[ks] = as_op(v);
     float sum = 0.f;
 #pragma unroll
-    for (int y = 0; y < 4; ++y)
+    for (int y = 0; y < 4; ++y) {
       sum += __uint_as_float(v[y] << 16) + __uint_as_float(v[y] & 0xFFFF0000u);
+    }
     qsum[ks / gks] += sum;
   }
 #pragma unroll
@@ -613,9 +646,7 @@ __device__ __forceinline__ void fold_dec(DecState<DH> &st, const DecRegs<DH, BP,
   for (int blk = 0; blk < Gm::NB; ++blk)
 #pragma unroll
     for (int ks = 0; ks < Gm::KS; ++ks)
-      acc[ks / gks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-          field_op<BP>(tr.k.w, blk * Gm::KS + ks), qopm[blk * Gm::KS + ks], acc[ks / gks], 0, 0,
-          0);
+      acc[ks / gks] = kmfma<BP>(tr.k.w, blk * Gm::KS + ks, qopm[blk * Gm::KS + ks], acc[ks / gks]);
   float p[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -702,7 +733,7 @@ __device__ __forceinline__ void fold_dec(DecState<DH> &st, const DecRegs<DH, BP,
         const f16x8 bv = vfield_h<BP>(tr.v.w, kv * Gm::CB + cb);
         st.O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_h(pk[g]), bv, st.O[cb], 0, 0, 0);
       } else {
-        const bf16x8 bv = field_op<BP>(tr.v.w, kv * Gm::CB + cb);
+        const bf16x8 bv = field16(tr.v.w, kv * Gm::CB + cb);
         st.O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_op(pk[g]), bv, st.O[cb], 0, 0, 0);
       }
     }

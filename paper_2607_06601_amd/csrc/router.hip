@@ -169,16 +169,39 @@ __global__ __launch_bounds__(256) void router_tail_kernel(
     const float4 v = *(const float4 *)(wz + c4);
     Wzs[z][c4] = v.x; Wzs[z][c4 + 1] = v.y; Wzs[z][c4 + 2] = v.z; Wzs[z][c4 + 3] = v.w;
   }
-  for (int idx = tid; idx < TB * DR; idx += 256) {
-    const int t = idx / DR, c = idx % DR;
-    float y = 0.f;
-    if (t0 + t < N) {
-      float sacc = 0.f;
-      for (int s = 0; s < KS; ++s) sacc += upart[(int64_t(s) * N + t0 + t) * DR + c];
-      y = sacc + b1[c];
-      y = 0.5f * y * (1.0f + erff(y * 0.70710678118654752f));
+  {
+    // u = GELU(sum of the KS trunk partials + b1): thread tid owns elements
+    // tid + 256 e of the block's 16 x 128; partials are summed in chunk order,
+    // four chunks' loads in flight at a time
+    constexpr int EPT = TB * DR / 256;
+    float sacc[EPT];
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) sacc[e] = 0.f;
+    for (int s0 = 0; s0 < KS; s0 += 4) {
+      float v[4][EPT];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+          const int idx = tid + 256 * e, t = idx / DR, c = idx % DR;
+          v[j][e] = (s0 + j < KS && t0 + t < N)
+                        ? upart[(int64_t(s0 + j) * N + t0 + t) * DR + c] : 0.f;
+        }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) sacc[e] += v[j][e];
     }
-    Us[t][c] = y;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const int idx = tid + 256 * e, t = idx / DR, c = idx % DR;
+      float y = 0.f;
+      if (t0 + t < N) {
+        y = sacc[e] + b1[c];
+        y = 0.5f * y * (1.0f + erff(y * 0.70710678118654752f));
+      }
+      Us[t][c] = y;
+    }
   }
   __syncthreads();
   // h: wave w computes columns 32 w .. 32 w + 31

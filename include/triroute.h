@@ -72,7 +72,8 @@ enum triroute_mode { TRIROUTE_SKIP = 0, TRIROUTE_LOCAL = 1, TRIROUTE_FULL = 2 };
  * d_psi, router width d_r (Sec. 3.1-3.3, Table 2, Table 6).
  * Supported: head_dim in {64, 128}; n_heads a multiple of n_kv_heads with
  * at most 16 query heads per kv head; kv_group in {32, 64} dividing
- * head_dim; d_router == 128; d_psi <= 32; 1 <= top_k <= n_experts + 1 <= 64;
+ * head_dim; d_router == 128; d_psi <= 32 and a multiple of 4 (W1 rows stay
+ * 16-byte aligned); 1 <= top_k <= n_experts + 1 <= 64;
  * d_model and d_ff multiples of 64; 3 * n_heads + n_experts + 5 <= 112;
  * rms_eps > 0. */
 typedef struct triroute_cfg {

@@ -103,7 +103,13 @@ MoeWs carve_moe(Carve &cv, const triroute_cfg &c, int N) {
   w.Y = cv.take<float>(size_t(N) * c.top_k * c.d_model);
   return w;
 }
-int32_t *carve_kv(Carve &cv, int N) { return cv.take<int32_t>(N); }
+tr::KvWs carve_kv(Carve &cv, const triroute_cfg &c, int B, int T) {
+  tr::KvWs w;
+  w.slots = cv.take<int32_t>(size_t(B) * T);
+  w.old_len = cv.take<int32_t>(size_t(B) * 4);
+  w.vstage = cv.take<uint8_t>(size_t(B) * T * c.n_kv_heads * c.head_dim);
+  return w;
+}
 float *carve_attn_decode(Carve &cv, const triroute_cfg &c, int B) {
   return cv.take<float>(size_t(B) * c.n_heads * DECODE_MAX_SPLITS * (c.head_dim + 2));
 }
@@ -136,7 +142,7 @@ size_t op_bytes(const triroute_cfg &c, int op, int B, int T) {
   switch (op) {
     case TRIROUTE_OP_ROUTER: carve_router(cv, c, N); break;
     case TRIROUTE_OP_QKV: break;
-    case TRIROUTE_OP_KV_APPEND: carve_kv(cv, N); break;
+    case TRIROUTE_OP_KV_APPEND: carve_kv(cv, c, B, T); break;
     case TRIROUTE_OP_ATTN_PREFILL: break;
     case TRIROUTE_OP_ATTN_DECODE: carve_attn_decode(cv, c, B); break;
     case TRIROUTE_OP_MOE: carve_moe(cv, c, N); break;
@@ -180,7 +186,8 @@ int check_cfg(const triroute_cfg *c) {
   REQUIRE(c->n_heads / c->n_kv_heads <= 16, TRIROUTE_E_UNSUPPORTED,
           "more than 16 query heads per kv head");
   REQUIRE(c->d_router == 128, TRIROUTE_E_UNSUPPORTED, "d_router %d != 128", c->d_router);
-  REQUIRE(c->d_psi <= 32, TRIROUTE_E_UNSUPPORTED, "d_psi %d > 32", c->d_psi);
+  REQUIRE(c->d_psi <= 32 && c->d_psi % 4 == 0, TRIROUTE_E_UNSUPPORTED,
+          "d_psi %d: must be a multiple of 4, at most 32", c->d_psi);
   REQUIRE(c->n_experts + 1 <= 64, TRIROUTE_E_UNSUPPORTED, "n_experts + 1 > 64");
   REQUIRE(3 * c->n_heads + c->n_experts + 5 <= 112, TRIROUTE_E_UNSUPPORTED,
           "router head count 3H + E + 5 > 112");
@@ -398,8 +405,8 @@ int triroute_kv_append(const triroute_cfg *cfg, const triroute_kv_cache *cache, 
   TRY(check_aligned({k, v}));
   TRY(check_ws(*cfg, TRIROUTE_OP_KV_APPEND, B, T, ws, ws_bytes));
   Carve cv(ws);
-  int32_t *slots = carve_kv(cv, B * T);
-  CHECK_HIP(tr::launch_kv_append(*cfg, tr::make_view(*cfg, *cache), B, T, seq_ids, k, v, bit, slots,
+  const tr::KvWs kw = carve_kv(cv, *cfg, B, T);
+  CHECK_HIP(tr::launch_kv_append(*cfg, tr::make_view(*cfg, *cache), B, T, seq_ids, k, v, bit, kw,
                                  (hipStream_t)stream),
             "kv_append launch");
   return TRIROUTE_OK;
@@ -572,9 +579,9 @@ static int layer_impl(const triroute_cfg *cfg, int B, int T, bool decode, const 
   {
     Carve sc(ws);
     sc.used = scratch_at;
-    int32_t *slots = carve_kv(sc, N);
+    const tr::KvWs kw = carve_kv(sc, *cfg, B, T);
     CHECK_HIP(tr::launch_kv_append(*cfg, tr::make_view(*cfg, *cache), B, T, seq_ids, L.k, L.v, L.bit,
-                                   slots, st),
+                                   kw, st),
               "kv_append launch");
   }
   if (decode) {

@@ -27,25 +27,29 @@ hipError_t launch_fill_u32(void *p, int64_t n_words, uint32_t v, hipStream_t st)
 __global__ __launch_bounds__(256) void kv_slots_kernel(CacheView cv, int T,
                                                        const int32_t *__restrict__ seq_ids,
                                                        const uint8_t *__restrict__ bit,
-                                                       int32_t *__restrict__ slots) {
+                                                       int32_t *__restrict__ slots,
+                                                       int32_t *__restrict__ old_len) {
   __shared__ int wc[4][4];
   const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int s = seq_ids ? seq_ids[b] : b;
   if (s < 0 || s >= cv.n_seq) {
     if (tid == 0) atomicOr(cv.status, int(TRIROUTE_CACHE_BAD_SEQ));
+    if (tid < 4) old_len[b * 4 + tid] = -1;
     for (int t = tid; t < T; t += 256) slots[int64_t(b) * T + t] = -1;
     return;
   }
   const int len0 = cv.seq_len[s];
   if (len0 + T > cv.capacity) {
     if (tid == 0) atomicOr(cv.status, int(TRIROUTE_CACHE_OVERFLOW));
+    if (tid < 4) old_len[b * 4 + tid] = -1;
     for (int t = tid; t < T; t += 256) slots[int64_t(b) * T + t] = -1;
     return;
   }
   int run[4];
 #pragma unroll
   for (int bi = 0; bi < 4; ++bi) run[bi] = cv.pool_len[s * 4 + bi];
+  if (tid < 4) old_len[b * 4 + tid] = run[tid];
   for (int t0 = 0; t0 < T; t0 += 256) {
     const int t = t0 + tid;
     const int bi = t < T ? int(bit[int64_t(b) * T + t]) : -1;
@@ -73,14 +77,19 @@ __global__ __launch_bounds__(256) void kv_slots_kernel(CacheView cv, int T,
   }
 }
 
-// One wave per (token, kv head): quantize K and V, write codes and scales.
+// One wave per (token, kv head): quantize K and V, write K codes (every
+// 32-bit word of a K record belongs to one slot), scales and 8/16-bit V
+// codes (byte and half-word stores); 2- and 4-bit V codes share words with
+// neighbouring slots and go to vstage, one byte per element, for
+// kv_vpack_kernel.
 template <typename T>
 __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int N,
                                                        const int32_t *__restrict__ seq_ids,
                                                        const T *__restrict__ kin,
                                                        const T *__restrict__ vin,
                                                        const uint8_t *__restrict__ bit,
-                                                       const int32_t *__restrict__ slots) {
+                                                       const int32_t *__restrict__ slots,
+                                                       uint8_t *__restrict__ vstage) {
   __shared__ uint32_t el[4][2][128];  // per wave: element value per channel (K, V)
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int item = blockIdx.x * 4 + w;
@@ -154,7 +163,7 @@ __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int
       *(uint32_t *)(tp + (o * 16 + n) * (8 * bp) + word * 4) = val;
     }
   }
-  // ---- V: words are shared by neighbouring slots (other slots' bits untouched)
+  // ---- V: words are shared by neighbouring slots
   {
     uint8_t *vp = tp + cv.v_codes_off(bi);
     for (int r = 0; r < NR; ++r) {
@@ -164,10 +173,8 @@ __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int
       q_word(q, bp, wd, bt);
       uint8_t *addr = vp + ln * (8 * bp) + wd * 4;
       const uint32_t e = el[w][1][c];
-      if (bp <= 4) {  // clear this slot's bits, then set them: correct on a reused slot
-        atomicAnd((unsigned int *)addr, ~(((1u << bp) - 1u) << bt));
-        atomicOr((unsigned int *)addr, e << bt);
-      }
+      if (bp <= 4)
+        vstage[(int64_t(i) * Hkv + g) * dh + c] = uint8_t(e);
       else if (bp == 8)
         addr[bt >> 3] = uint8_t(e);
       else if (bp == 16)
@@ -175,6 +182,57 @@ __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int
       else
         *(uint32_t *)addr = e;
     }
+  }
+}
+
+// 2- and 4-bit V words: one wave per (batch row, pool, kv head, 32-slot
+// step of the appended range).  A step's words hold only that step's slots,
+// so the wave owns them: lane l builds the words of its record l from the
+// staged codes of the new slots and keeps the bits of slots appended before.
+__global__ __launch_bounds__(256) void kv_vpack_kernel(CacheView cv, int B, int T, int JS,
+                                                       const int32_t *__restrict__ seq_ids,
+                                                       const int32_t *__restrict__ old_len,
+                                                       const uint8_t *__restrict__ vstage) {
+  const int lane = threadIdx.x & 63;
+  int u = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int j = u % JS;
+  u /= JS;
+  const int g = u % cv.Hkv;
+  u /= cv.Hkv;
+  const int bi = u % 2, b = u / 2;
+  if (b >= B) return;
+  const int s = seq_ids ? seq_ids[b] : b;
+  const int old = old_len[b * 4 + bi];
+  if (old < 0) return;  // row dropped (bad sequence or capacity)
+  const int nlen = cv.pool_len[s * 4 + bi];
+  const int step = old / 32 + j;
+  if (step * 32 >= nlen) return;
+  const int bp = 2 << bi, dh = cv.dh, TS = cv.TS, CB = dh / 16;
+  const int len0 = cv.seq_len[s] - T;
+  const int32_t *pos = cv.pos_of(s, bi);
+  // token of each slot of the step (lanes 0..31), shuffled to the elements
+  const int sl = step * 32 + (lane & 31);
+  const int tok = (sl >= old && sl < nlen) ? b * T + (pos[sl] - len0) : -1;
+  const int tile = step * 32 / TS, kv = (step * 32 % TS) / 32;
+  uint32_t *rec = (uint32_t *)(cv.tile(s, bi, g, tile) + cv.v_codes_off(bi) + lane * 8 * bp);
+  const int per = 16 / bp;  // element pairs per word
+  const int w0 = kv * CB * 8 / (2 * per), w1 = (kv + 1) * CB * 8 / (2 * per);
+  for (int wd = w0; wd < w1; ++wd) {
+    uint32_t word = 0, keep = 0;
+    for (int h = 0; h < 2 * per; ++h) {
+      const int q = 2 * (wd * per + (h >> 1)) + (h & 1);
+      const int f = q >> 3, jj = q & 7;
+      const int sis = 16 * (jj >> 2) + 4 * (lane >> 4) + (jj & 3);  // slot within the step
+      const int ch = 16 * (f % CB) + (lane & 15);
+      const int bt = ((q >> 1) % per) * bp + (q & 1) * 16;
+      const int slot = step * 32 + sis;
+      const int t = __shfl(tok, sis, 64);
+      if (slot < old)
+        keep |= ((1u << bp) - 1u) << bt;
+      else if (t >= 0)
+        word |= uint32_t(vstage[(int64_t(t) * cv.Hkv + g) * dh + ch]) << bt;
+    }
+    rec[wd] = keep ? (rec[wd] & keep) | word : word;
   }
 }
 
@@ -241,16 +299,22 @@ __global__ void kv_export_kernel(CacheView cv, int seq, int bi, int slot0, int c
 
 hipError_t launch_kv_append(const triroute_cfg &cfg, const CacheView &cv, int B, int T,
                             const int32_t *seq_ids, const void *k, const void *v,
-                            const uint8_t *bit, int32_t *slots, hipStream_t st) {
-  kv_slots_kernel<<<B, 256, 0, st>>>(cv, T, seq_ids, bit, slots);
+                            const uint8_t *bit, const KvWs &ws, hipStream_t st) {
+  kv_slots_kernel<<<B, 256, 0, st>>>(cv, T, seq_ids, bit, ws.slots, ws.old_len);
   const int N = B * T;
   dim3 grid((N * cfg.n_kv_heads + 3) / 4);
   if (cfg.act == TRIROUTE_BF16)
     kv_write_kernel<bf16><<<grid, 256, 0, st>>>(cv, T, N, seq_ids, (const bf16 *)k,
-                                                (const bf16 *)v, bit, slots);
+                                                (const bf16 *)v, bit, ws.slots, ws.vstage);
   else
     kv_write_kernel<float><<<grid, 256, 0, st>>>(cv, T, N, seq_ids, (const float *)k,
-                                                 (const float *)v, bit, slots);
+                                                 (const float *)v, bit, ws.slots, ws.vstage);
+  // 32-slot steps an append can touch in one pool: all T tokens, plus the
+  // partly filled step it starts in
+  const int JS = (T + 31) / 32 + 1;
+  const int64_t units = int64_t(B) * 2 * cfg.n_kv_heads * JS;
+  kv_vpack_kernel<<<dim3(unsigned((units + 3) / 4)), 256, 0, st>>>(cv, B, T, JS, seq_ids,
+                                                                    ws.old_len, ws.vstage);
   return hipGetLastError();
 }
 

@@ -84,19 +84,40 @@ __global__ __launch_bounds__(256) void trunk1_kernel(const T *__restrict__ x,
   const float rr = arow < N ? rinv[arow] : 0.f;
   float ra[8], rb[16];
   auto fetch = [&](int k0) {
+    // A: 8 consecutive inputs of row arow; whole 8-runs inside x use one
+    // 16-byte load (d % 64 == 0, so a run never straddles x and psi)
+    const int ka = k0 + ak;
+    if (arow < N && ka + 8 <= ke && ka + 8 <= d) {
+      float xv[8], gv[8];
+      load8(x + int64_t(arow) * d + ka, xv);
+      load8(g1 + ka, gv);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int k = k0 + ak + i;
-      float v = 0.f;
-      if (arow < N && k < ke)
-        v = k < d ? (Act<T>::ld(x, int64_t(arow) * d + k) * rr) * g1[k]
-                  : psi[int64_t(arow) * dpsi + (k - d)];
-      ra[i] = v;
+      for (int i = 0; i < 8; ++i) ra[i] = (xv[i] * rr) * gv[i];
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int k = ka + i;
+        float v = 0.f;
+        if (arow < N && k < ke)
+          v = k < d ? (Act<T>::ld(x, int64_t(arow) * d + k) * rr) * g1[k]
+                    : psi[int64_t(arow) * dpsi + (k - d)];
+        ra[i] = v;
+      }
     }
+    // B: 16 consecutive inputs of W1 row br (K % 4 == 0: 16-byte aligned)
+    const int kb0 = k0 + bk;
+    if (kb0 + 16 <= ke) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int k = k0 + bk + i;
-      rb[i] = k < ke ? W1[int64_t(br) * K + k] : 0.f;
+      for (int i = 0; i < 4; ++i) {
+        const float4 w = *(const float4 *)(W1 + int64_t(br) * K + kb0 + 4 * i);
+        rb[4 * i] = w.x; rb[4 * i + 1] = w.y; rb[4 * i + 2] = w.z; rb[4 * i + 3] = w.w;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int k = kb0 + i;
+        rb[i] = k < ke ? W1[int64_t(br) * K + k] : 0.f;
+      }
     }
   };
   auto put = [&](int buf) {

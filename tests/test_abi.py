@@ -36,7 +36,7 @@ def test_library_exports_every_declared_symbol():
 @pytest.mark.parametrize("field,value,code", [
     ("head_dim", 96, -2), ("kv_group", 48, -2), ("n_kv_heads", 5, -1), ("top_k", 10, -1),
     ("act", 7, -1), ("d_router", 64, -2), ("rms_eps", 0.0, -1), ("d_model", 100, -2),
-    ("n_heads", 0, -1)])
+    ("n_heads", 0, -1), ("d_psi", 6, -2), ("d_psi", 36, -2)])
 def test_validate_rejects(field, value, code):
     assert tr.validate(cfg160(**{field: value})) == code
     assert tr.lib().triroute_last_error()
@@ -52,7 +52,8 @@ def test_validate_accepts_every_workload():
 def test_workspace_and_cache_sizes():
     c = cfg160()
     assert tr.workspace_bytes(c, tr.OP_QKV, 8, 2048) == 0
-    assert tr.workspace_bytes(c, tr.OP_KV_APPEND, 8, 2048) == 8 * 2048 * 4
+    # slots, per-row pool lengths (rounded to 256 B), staged 2/4-bit V codes (3 heads x 64)
+    assert tr.workspace_bytes(c, tr.OP_KV_APPEND, 8, 2048) == 8 * 2048 * 4 + 256 + 8 * 2048 * 192
     lay = tr.workspace_bytes(c, tr.OP_LAYER_PREFILL, 8, 2048)
     assert lay > tr.workspace_bytes(c, tr.OP_MOE, 8, 2048)
     n = C.c_size_t()

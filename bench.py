@@ -40,7 +40,10 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true")
-    p.add_argument("--only", choices=("prefill", "decode", "moe"), default=None,
+    p.add_argument("--no-wide", action="store_true",
+                   help="leave out the 1.3B-class prefill and long-context decode legs")
+    p.add_argument("--only", choices=("prefill", "decode", "moe", "prefill_1p3b", "decode_1p3b"),
+                   default=None,
                    help="profile one workload alone (prints its section only); 'moe' times "
                         "the MoE sublayer and then runs a 256 MiB copy for counter calibration")
     p.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "KERNEL_REGEX"),
@@ -86,56 +89,25 @@ def main():
     tr.lib()
     dev = "cuda"
     stream = torch.cuda.current_stream()
+    flush = CacheFlush(torch, dev)
     if args.only == "decode":
-        flush = CacheFlush(torch, dev)
-        res = bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush)
+        res = bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush, DECODE)
         copy_calibration(torch)
         print(json.dumps({"decode": res}), flush=True)
         return
+    if args.only in ("prefill_1p3b", "decode_1p3b"):
+        res = run_wide(args, torch, np, gen, tr, DeviceLayer, to_dev, flush, args.only)
+        print(json.dumps({args.only: res}), flush=True)
+        return
 
-    # ------------------------------------------------------------ prefill
-    L = gen.make_layer(PREFILL, 1)
-    cfg = L["cfg"]
-    B, T, d, H, dh, E, k, dff = (cfg[x] for x in ("B", "T", "d", "H", "dh", "E", "k", "d_ff"))
-    N = B * T
-    D = DeviceLayer(L)
-    c = D.cfg
-    ws = tr.workspace(c, tr.OP_LAYER_PREFILL, B, T)
-    xo = torch.empty(N, d, dtype=D.act, device=dev)
-    flush = CacheFlush(torch, dev)
-    caches = [tr.KVCache(c, B, T) for _ in range(args.steps)]
-    warm = tr.KVCache(c, B, T)
-    eidx_t = torch.empty(N, k, dtype=torch.int32, device=dev)
-    egate_t = torch.empty(N, k, dtype=torch.float32, device=dev)
-    xt_t = torch.empty(N, d, dtype=D.act, device=dev)
-    taps = tr.Taps(eidx=eidx_t.data_ptr(), egate=egate_t.data_ptr(), xt=xt_t.data_ptr())
-    for _ in range(args.warmup):
-        warm.reset_seq(0)
-        for s in range(B):
-            warm.reset_seq(s)
-        tr.layer_prefill(c, B, T, D.x, D.psi, D.rw, D.dw, D.mw, warm, xo, ws, taps=taps)
-    torch.cuda.synchronize()
-    times = []
-    t_wall0 = time.perf_counter()
-    for i in range(args.steps):
-        flush()
-        e0, e1 = events(torch)
-        e0.record(stream)
-        tr.layer_prefill(c, B, T, D.x, D.psi, D.rw, D.dw, D.mw, caches[i], xo, ws, taps=taps)
-        e1.record(stream)
-        times.append((e0, e1))
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_wall0
-    step_ms = [a.elapsed_time(b) for a, b in times]
-    ms = float(np.mean(step_ms))
-    for cc in caches:
-        assert cc.status() == 0
-
-    roofline = bench_moe(args, torch, np, tr, D, c, B, T, flush, eidx_t, egate_t, xt_t, xo)
+    res = bench_prefill(args, torch, np, gen, tr, DeviceLayer, flush, PREFILL, 1)
     if args.only == "moe":
         copy_calibration(torch)
-        print(json.dumps({"moe": roofline}), flush=True)
+        print(json.dumps({"moe": res["roofline"]}), flush=True)
         return
+    B, T, ms, step_ms, wall = (res[x] for x in ("B", "T", "ms", "step_ms", "wall"))
+    N = B * T
+    roofline = res["roofline"]
 
     out = {
         "metric": "routed-layer tokens/s (prefill, decode); decode-attn HBM GB/s; MoE MFMA util",
@@ -157,12 +129,92 @@ def main():
 
     # ------------------------------------------------------------- decode
     if not args.no_decode and args.only is None:
-        out["decode"] = bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush)
+        out["decode"] = bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush, DECODE)
+
+    # ---------------------------------- the 1.3B-class workloads (context)
+    if not args.no_wide and args.only is None:
+        for leg in ("prefill_1p3b", "decode_1p3b"):
+            out[leg] = run_wide(args, torch, np, gen, tr, DeviceLayer, to_dev, flush, leg)
 
     # --------------------------------------------------------- CPU oracle
     if not args.no_cpu_baseline and args.only is None:
         out["cpu_baseline"] = cpu_baseline(np)
     print(json.dumps(out), flush=True)
+
+
+def describe(cfg):
+    """The workload's sizes in words."""
+    if cfg["kind"] == "prefill":
+        head = f"layer prefill: batch {cfg['B']} x seq {cfg['T']}"
+    else:
+        head = (f"decode step: {cfg['B']} sequences x 1 new token, context {cfg['ctx']} (bits "
+                + "/".join(f"{round(100 * f)}" for f in cfg["ctx_bits"]) + " % for 2/4/8/16)")
+    ex = "skewed" if cfg["experts"] == "skewed" else "uniform"
+    return (f"{head}, d {cfg['d']}, {cfg['H']}x{cfg['dh']} heads ({cfg['Hkv']} kv), window "
+            f"{cfg['w']}, {cfg['E']} SwiGLU experts d_ff {cfg['d_ff']} + null, top-{cfg['k']} "
+            f"({ex} routing), KV group {cfg['G']}, {cfg['act']}")
+
+
+def run_wide(args, torch, np, gen, tr, DeviceLayer, to_dev, flush, leg):
+    """The 1.3B-class prefill (step + MoE sublayer) or long-context decode
+    (step + decode attention), with at most 10 timed steps."""
+    import copy
+    a = copy.copy(args)
+    a.steps, a.warmup = min(args.steps, 10), min(args.warmup, 3)
+    if leg == "prefill_1p3b":
+        name = "1p3b_bf16_prefill"
+        r = bench_prefill(a, torch, np, gen, tr, DeviceLayer, flush, name, None)
+        N = r["B"] * r["T"]
+        return {"workload": "1.3B-class " + describe(gen.CONFIGS[name]),
+                "tokens_per_s": round(N / (r["ms"] * 1e-3), 1), "ms_per_step": round(r["ms"], 4),
+                "steps": a.steps, "moe": r["roofline"]}
+    return bench_decode(a, torch, np, gen, tr, DeviceLayer, to_dev, flush, "1p3b_bf16_decode")
+
+
+def bench_prefill(args, torch, np, gen, tr, DeviceLayer, flush, name, seed):
+    """Timed triroute_layer_prefill steps of one prefill workload, then its
+    MoE sublayer alone on the same routed inputs."""
+    L = gen.make_layer(name, seed)
+    cfg = L["cfg"]
+    B, T, d, k = (cfg[x] for x in ("B", "T", "d", "k"))
+    N = B * T
+    D = DeviceLayer(L)
+    del L
+    c = D.cfg
+    dev = "cuda"
+    stream = torch.cuda.current_stream()
+    ws = tr.workspace(c, tr.OP_LAYER_PREFILL, B, T)
+    xo = torch.empty(N, d, dtype=D.act, device=dev)
+    caches = [tr.KVCache(c, B, T) for _ in range(args.steps)]
+    warm = tr.KVCache(c, B, T)
+    eidx_t = torch.empty(N, k, dtype=torch.int32, device=dev)
+    egate_t = torch.empty(N, k, dtype=torch.float32, device=dev)
+    xt_t = torch.empty(N, d, dtype=D.act, device=dev)
+    taps = tr.Taps(eidx=eidx_t.data_ptr(), egate=egate_t.data_ptr(), xt=xt_t.data_ptr())
+    for _ in range(args.warmup):
+        for s in range(B):
+            warm.reset_seq(s)
+        tr.layer_prefill(c, B, T, D.x, D.psi, D.rw, D.dw, D.mw, warm, xo, ws, taps=taps)
+    torch.cuda.synchronize()
+    times = []
+    t_wall0 = time.perf_counter()
+    for i in range(args.steps):
+        flush()
+        e0, e1 = events(torch)
+        e0.record(stream)
+        tr.layer_prefill(c, B, T, D.x, D.psi, D.rw, D.dw, D.mw, caches[i], xo, ws, taps=taps)
+        e1.record(stream)
+        times.append((e0, e1))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall0
+    step_ms = [a.elapsed_time(b) for a, b in times]
+    for cc in caches:
+        assert cc.status() == 0
+    del caches, warm
+    roofline = bench_moe(args, torch, np, tr, D, c, B, T, flush, eidx_t, egate_t, xt_t, xo,
+                         name)
+    return {"B": B, "T": T, "ms": float(np.mean(step_ms)), "step_ms": step_ms, "wall": wall,
+            "roofline": roofline}
 
 
 def source_digest(*names):
@@ -201,7 +253,7 @@ def stored_traffic(name, sources):
         return None
 
 
-def bench_moe(args, torch, np, tr, D, c, B, T, flush, eidx_t, egate_t, xt_t, xo):
+def bench_moe(args, torch, np, tr, D, c, B, T, flush, eidx_t, egate_t, xt_t, xo, name):
     """The MoE sublayer (triroute_moe: rmsnorm2, grouped GEMM gate/up + SwiGLU,
     grouped GEMM down, combine) alone on the routed inputs of the last prefill
     step: achieved bf16 MFMA rate of the expert FLOPs."""
@@ -237,7 +289,8 @@ def bench_moe(args, torch, np, tr, D, c, B, T, flush, eidx_t, egate_t, xt_t, xo)
             "bound": "mfma", "achieved": round(moe_tflops, 2),
             "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
             "frac": round(moe_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
-            "traffic": stored_traffic("moe_160m_prefill_traffic.txt", MOE_SOURCES),
+            "traffic": (stored_traffic("moe_160m_prefill_traffic.txt", MOE_SOURCES)
+                        if name == PREFILL else None),
             "algorithmic": f"6*d*d_ff FLOP x {n_real} real assignments = "
                            f"{moe_flops / 1e9:.1f} GFLOP per launch",
             "avg_ms": round(moe_avg, 4)}
@@ -276,8 +329,8 @@ def decode_attn_bytes(cfg, mode, bits_per_seq):
     return total
 
 
-def bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush):
-    L = gen.make_layer(DECODE)
+def bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush, name):
+    L = gen.make_layer(name)
     cfg = L["cfg"]
     B, ctx, d, H, k = cfg["B"], cfg["ctx"], cfg["d"], cfg["H"], cfg["k"]
     D = DeviceLayer(L)
@@ -338,15 +391,14 @@ def bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush):
     torch.cuda.synchronize()
     attn_ms = float(np.mean([a.elapsed_time(b) for a, b in at]))
     gbs = nbytes / (attn_ms * 1e-3) / 1e9
-    return {"workload": "410M-class decode step: 64 sequences x 1 new token, context 8192 "
-                        "(bits 20/40/30/10 % for 2/4/8/16), d 1024, 16x64 heads (4 kv), "
-                        "window 256, 8 SwiGLU experts d_ff 2816 + null, top-2",
+    cls = "410M" if name == DECODE else "1.3B"
+    return {"workload": f"{cls}-class " + describe(cfg),
             "tokens_per_s": round(B / (step_ms * 1e-3), 1), "ms_per_step": round(step_ms, 4),
             "attn": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                      "algorithmic_bytes": int(nbytes), "avg_ms": round(attn_ms, 4),
-                     "traffic": stored_traffic("attn_decode_410m_traffic.txt",
-                                                DECODE_ATTN_SOURCES)}}
+                     "traffic": (stored_traffic("attn_decode_410m_traffic.txt",
+                                                 DECODE_ATTN_SOURCES) if name == DECODE else None)}}
 
 
 def summarize_pmc(fetch_dir, write_dir, regex):

@@ -378,6 +378,32 @@ __device__ __forceinline__ int lower_bound_pos(const int32_t *pos, int len, int 
   return lo + __popcll(below);
 }
 
+// The query operand of column n16 (a row of q, bf16, zero when !valid) and
+// its per-group sums, from the raw 16-byte pieces loaded by the caller.
+template <int DH, int G>
+__device__ __forceinline__ void q_operand(const u32x4 *raw, bool valid, bf16x8 *qop, float *qsum) {
+  constexpr int gks = G / 32;
+#pragma unroll
+  for (int g = 0; g < DH / G; ++g) qsum[g] = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < DH / 32; ++ks) {
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    const u32x4 v = valid ? raw[ks] : zero;
+    qop[ks] = as_op(v);
+    float sum = 0.f;
+#pragma unroll
+    for (int y = 0; y < 4; ++y) {
+      sum += __uint_as_float(v[y] << 16) + __uint_as_float(v[y] & 0xFFFF0000u);
+    }
+    qsum[ks / gks] += sum;
+  }
+#pragma unroll
+  for (int g = 0; g < DH / G; ++g) {
+    qsum[g] += __shfl_xor(qsum[g], 16, 64);
+    qsum[g] += __shfl_xor(qsum[g], 32, 64);
+  }
+}
+
 // Load the query operand of column n16 (a row of q, bf16) and per-group sums.
 template <int DH, int G>
 __device__ __forceinline__ void load_q(const bf16 *qrow, bool valid, bf16x8 *qop, float *qsum) {
@@ -518,28 +544,30 @@ struct Int4 {
 // order, through its LDS ring (DEC_RING bytes at rptr / LDS address rbase)
 // used as a byte FIFO: tiles are placed back to back, wrapping to the ring
 // start when one does not fit before the end, and the wave keeps issuing
-// tiles, across pool boundaries, while free space allows.  Each tile, once
-// resident, goes to fold(bi, t, lds_pointer).  On entry no other
-// vector-memory load of the wave may be in flight.
+// tiles, across pool boundaries, while free space allows.  The consumer
+// walks the pools in the same order with the pool index known at compile
+// time: each resident tile goes to fold(BI, t, lds_pointer), BI an
+// std::integral_constant.  On entry no other vector-memory load of the wave
+// may be in flight.
 template <int DH, int G, class Fold>
-__device__ void stream_tiles(const CacheView &cv, int s, int g, Int4 w0, Int4 w1,
-                             const uint8_t *rptr, uint32_t rbase, Fold &&fold) {
+__device__ __forceinline__ void stream_tiles(const CacheView &cv, int s, int g, Int4 w0, Int4 w1,
+                                             const uint8_t *rptr, uint32_t rbase, Fold &&fold) {
   using SG = StreamGeo<DH, G>;
   int pb = 0, pt = w0[0];  // producer: next tile to issue
   while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
-  int cb = pb, ct = pt;    // consumer: next tile to fold
-  int phead = 0, nin = 0, issued = 0;  // ring end of the newest tile, tiles and transfers out
-  int cpos = 0, consumed = 0;          // ring offset of tile (cb, ct), transfers consumed
-  while (cb < 4) {
+  int phead = 0, pfree = 0;  // ring end of the newest tile; start of the oldest resident tile
+  int nin = 0, issued = 0, consumed = 0;  // tiles resident or in flight; transfers out / used
+  int chead = 0;                          // ring end of the last consumed tile
+  auto produce = [&]() {
     while (pb < 4) {
       const int sz = SG::foot(pb);
       const int pos = phead + sz <= DEC_RING ? phead : 0;
       bool ok = true;
       if (nin > 0) {
-        if (cpos < phead)
-          ok = pos == phead || sz <= cpos;
+        if (pfree < phead)
+          ok = pos == phead || sz <= pfree;
         else
-          ok = pos == phead && phead + sz <= cpos;
+          ok = pos == phead && phead + sz <= pfree;
       }
       if (!ok) break;
       tile_to_lds(cv.tile(s, pb, g, pt), rbase + pos, SG::tb(pb), SG::ni(pb));
@@ -549,15 +577,43 @@ __device__ void stream_tiles(const CacheView &cv, int s, int g, Int4 w0, Int4 w1
       ++pt;
       while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
     }
-    consumed += SG::ni(cb);
-    wait_vm_le(issued - consumed);
-    fold(cb, ct, rptr + cpos);
-    --nin;
-    const int chead = cpos + SG::foot(cb);
-    ++ct;
-    while (cb < 4 && ct >= w1[cb]) { ++cb; if (cb < 4) ct = w0[cb]; }
-    if (cb < 4) cpos = chead + SG::foot(cb) <= DEC_RING ? chead : 0;
-  }
+  };
+  auto pool = [&](auto BI) {
+    constexpr int bi = decltype(BI)::value;
+    constexpr int sz = SG::foot(bi);
+    const int t1 = w1[bi];
+    for (int t = w0[bi]; t < t1; ++t) {
+      produce();
+      const int cpos = chead + sz <= DEC_RING ? chead : 0;  // the producer's placement rule
+      consumed += SG::ni(bi);
+      wait_vm_le(issued - consumed);
+      fold(BI, t, rptr + cpos);
+      chead = cpos + sz;
+      --nin;
+      pfree = chead;  // oldest resident tile now starts where this one ended (or the ring wraps)
+    }
+  };
+  pool(std::integral_constant<int, 0>{});
+  pool(std::integral_constant<int, 1>{});
+  pool(std::integral_constant<int, 2>{});
+  pool(std::integral_constant<int, 3>{});
+}
+
+// Max over the lanes n16 = h, h + 4, h + 8, h + 12 of each 16-lane row
+// (row rotations by 4 and 8), then over the four rows (row-pair and
+// half-wave swaps): afterwards every lane holds the maximum over all lanes
+// with its lane % 4.
+__device__ __forceinline__ float max_lane_mod4(float x) {
+  x = fmaxf(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), 0x124, 0xF,
+                                                            0xF, false)));
+  x = fmaxf(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), 0x128, 0xF,
+                                                            0xF, false)));
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+  x = fmaxf(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+  const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+  return fmaxf(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
 }
 
 // ---- decode with head-packed columns (at most 4 query heads per kv head)
@@ -571,6 +627,12 @@ __device__ void stream_tiles(const CacheView &cv, int s, int g, Int4 w0, Int4 w1
 // key block) as rows: the lane's own probabilities are already in the A
 // operand order of the V layout, zero outside its block.  The virtual rows
 // of a head are summed once at the end.
+//
+// The running max starts at a large finite negative value instead of -inf,
+// so that exp2(score - m) of a masked score (-inf) is 0 without a test; a
+// head that sees no key keeps l = 0 and yields a zero output.
+constexpr float DEC_M0 = -1.0e30f;
+
 template <int DH>
 struct DecState {
   float m;             // running max (log2 domain) of the lane's head
@@ -581,7 +643,7 @@ struct DecState {
 
 template <int DH>
 __device__ __forceinline__ void dec_init(DecState<DH> &st) {
-  st.m = -INFINITY;
+  st.m = DEC_M0;
   st.l = 0.f;
 #pragma unroll
   for (int g = 0; g < DH / 32; ++g) st.zc[g] = 0.f;
@@ -629,9 +691,19 @@ struct DecRegs {
   }
 };
 
+// Key bounds of the lane's head in one pool, relative to a tile: slot
+// 16 c + 4 o4 + i of the tile is a key of the head when lo <= it <= hi.
+struct TileMask {
+  int lo, hi;
+};
+
+// Fold one tile: S^T for its key blocks, the online-softmax update (the
+// output rows are rescaled only when some head's running max grows), then
+// O += P' V.  `dead`: the lane's key block lies past the tile (d_h 128 has
+// two 16-slot blocks per tile, so columns of blocks 2 and 3 are idle).
 template <int DH, int BP, int G>
 __device__ __forceinline__ void fold_dec(DecState<DH> &st, const DecRegs<DH, BP, G> &tr,
-                                         int slot0, ColMask cm, const bf16x8 *qopm,
+                                         TileMask tm, bool dead, const bf16x8 *qopm,
                                          const float *qsum, float scale2) {
   using Gm = Geo<DH>;
   using PT = PoolTraits<BP>;
@@ -663,35 +735,46 @@ __device__ __forceinline__ void fold_dec(DecState<DH> &st, const DecRegs<DH, BP,
 #pragma unroll
       for (int g = 0; g < NG; ++g) sv += acc[g][i];
     }
-    const int key = slot0 + 16 * c + 4 * o4 + i;
-    p[i] = (c < Gm::NB && key >= cm.lo && key <= cm.hi) ? sv * scale2 : -INFINITY;
+    p[i] = sv * scale2;
+  }
+  // keys outside the head's range.  Per lane the tile holds all, none or
+  // part of the head's keys; the per-key test runs only when some lane has
+  // a part (a tile with a window start or the pool's end).
+  const int k0 = 16 * c + 4 * o4;
+  const bool none = dead || tm.hi < 0 || tm.lo > Gm::TS - 1 || tm.lo > tm.hi;
+  const bool all = tm.lo <= 0 && tm.hi >= Gm::TS - 1;
+  if (!__builtin_amdgcn_ballot_w64(!none && !all)) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p[i] = none ? -INFINITY : p[i];
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      p[i] = (!dead && k0 + i >= tm.lo && k0 + i <= tm.hi) ? p[i] : -INFINITY;
   }
   // ---- online softmax per head (lanes of one head: equal lane % 4)
-  float mt = fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3]));
-  mt = fmaxf(mt, __shfl_xor(mt, 4, 64));
-  mt = fmaxf(mt, __shfl_xor(mt, 8, 64));
-  mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-  mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-  const float mnew = fmaxf(st.m, mt);
-  const bool live = mnew != -INFINITY;
-  const float corr = live ? exp2f(st.m - mnew) : 1.f;
+  const float mt = max_lane_mod4(fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3])));
+  if (__builtin_amdgcn_ballot_w64(mt > st.m)) {
+    const float mnew = fmaxf(st.m, mt);
+    const float corr = __builtin_amdgcn_exp2f(st.m - mnew);
+    st.l *= corr;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) st.zc[g] *= corr;
+    st.m = mnew;
+    // output rows of head i take head i's factor (lane i holds head i)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float ci = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(corr), i));
+#pragma unroll
+      for (int cb = 0; cb < Gm::CB; ++cb) st.O[cb][i] *= ci;
+    }
+  }
   float ps = 0.f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    p[i] = live ? exp2f(p[i] - mnew) : 0.f;
+    p[i] = __builtin_amdgcn_exp2f(p[i] - st.m);
     ps += p[i];
   }
-  st.l = st.l * corr + ps;
-#pragma unroll
-  for (int g = 0; g < NG; ++g) st.zc[g] *= corr;
-  st.m = mnew;
-  // output rows of head i take head i's factor (lane i holds head i)
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const float ci = __shfl(corr, i, 64);
-#pragma unroll
-    for (int cb = 0; cb < Gm::CB; ++cb) st.O[cb][i] *= ci;
-  }
+  st.l += ps;
   // ---- P' (fp16 p * s_v, or bf16 p for the 16-bit pool), two packed pairs per group
   uint32_t ph[NG][2];
 #pragma unroll
@@ -763,39 +846,15 @@ __device__ __forceinline__ void dec_finish(DecState<DH> &st) {
     }
 }
 
-template <int DH, int G>
-__device__ __forceinline__ void fold_dec_any(DecState<DH> &st, const CacheView &cv, int bi, int t,
-                                             const uint8_t *tp, ColMask cm, const bf16x8 *qopm,
-                                             const float *qsum, float scale2) {
-  constexpr int TS = 4096 / DH;
-  switch (bi) {
-    case 0: { DecRegs<DH, 2, G> r; r.load(tp, cv, 0);
-              fold_dec<DH, 2, G>(st, r, t * TS, cm, qopm, qsum, scale2); } break;
-    case 1: { DecRegs<DH, 4, G> r; r.load(tp, cv, 1);
-              fold_dec<DH, 4, G>(st, r, t * TS, cm, qopm, qsum, scale2); } break;
-    case 2: { DecRegs<DH, 8, G> r; r.load(tp, cv, 2);
-              fold_dec<DH, 8, G>(st, r, t * TS, cm, qopm, qsum, scale2); } break;
-    default: { DecRegs<DH, 16, G> r; r.load(tp, cv, 3);
-               fold_dec<DH, 16, G>(st, r, t * TS, cm, qopm, qsum, scale2); } break;
-  }
-}
-
-// Fold tile t of pool bi, resident in LDS at tp, into a one-head-per-column state.
-template <int DH, int G>
-__device__ __forceinline__ void fold_tile(SoftState<DH> &st, const CacheView &cv, int bi, int t,
+// Fold tile t of pool BI, resident in LDS at tp, into a one-head-per-column state.
+template <int DH, int G, int BI>
+__device__ __forceinline__ void fold_tile(SoftState<DH> &st, const CacheView &cv, int t,
                                           const uint8_t *tp, ColMask cm, const bf16x8 *qop,
                                           const float *qsum, float scale2) {
-  constexpr int TS = 4096 / DH;
-  switch (bi) {
-    case 0: { TileRegs<DH, 2, G, false> r; r.load(tp, cv, 0, t * TS, nullptr, 0);
-              process_tile<DH, 2, G, false>(st, r, t * TS, cm, qop, qsum, scale2); } break;
-    case 1: { TileRegs<DH, 4, G, false> r; r.load(tp, cv, 1, t * TS, nullptr, 0);
-              process_tile<DH, 4, G, false>(st, r, t * TS, cm, qop, qsum, scale2); } break;
-    case 2: { TileRegs<DH, 8, G, false> r; r.load(tp, cv, 2, t * TS, nullptr, 0);
-              process_tile<DH, 8, G, false>(st, r, t * TS, cm, qop, qsum, scale2); } break;
-    default: { TileRegs<DH, 16, G, false> r; r.load(tp, cv, 3, t * TS, nullptr, 0);
-               process_tile<DH, 16, G, false>(st, r, t * TS, cm, qop, qsum, scale2); } break;
-  }
+  constexpr int TS = 4096 / DH, BP = 2 << BI;
+  TileRegs<DH, BP, G, false> r;
+  r.load(tp, cv, BI, t * TS, nullptr, 0);
+  process_tile<DH, BP, G, false>(st, r, t * TS, cm, qop, qsum, scale2);
 }
 
 // One block of 8 waves per (sequence, kv head, chunk): the waves split each
@@ -805,7 +864,7 @@ __device__ __forceinline__ void fold_tile(SoftState<DH> &st, const CacheView &cv
 // chunk the block writes the normalised output itself; otherwise it leaves
 // (m, l, O) partials.
 template <int DH, int G, bool PACKED>
-__global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(512, 1) void attn_decode_kernel(DecodeArgs a) {
   constexpr int RING = DEC_WAVES * DEC_RING;
   static_assert(RING >= DEC_WAVES * 16 * (DH + 2) * 4, "ring doubles as the merge buffer");
   __shared__ __align__(1024) uint8_t ring[RING];
@@ -816,11 +875,18 @@ __global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
   const int b = blockIdx.x / Hkv, g = blockIdx.x % Hkv, split = blockIdx.y;
   const int lane = threadIdx.x & 63, n16 = lane & 15;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int s = a.seq_ids ? a.seq_ids[b] : b;
-  const bool seq_ok = s >= 0 && s < cv.n_seq;
   const int R = a.R;
   const int hl = PACKED ? (n16 & 3) : n16;  // the lane's query head within the group
   const int head = g * R + hl;
+  // independent loads first: the query row, the sequence id and the modes
+  u32x4 qraw[DH / 32];
+  {
+    const bf16 *qrow = a.q + (int64_t(b) * a.H + g * R + (hl < R ? hl : 0)) * DH + 8 * (lane >> 4);
+#pragma unroll
+    for (int ks = 0; ks < DH / 32; ++ks) qraw[ks] = *(const u32x4 *)(qrow + 32 * ks);
+  }
+  const int s = a.seq_ids ? a.seq_ids[b] : b;
+  const bool seq_ok = s >= 0 && s < cv.n_seq;
   const int hm = (seq_ok && hl < R) ? int(a.mode[b * a.H + head]) : 0;
   int U = hm;  // union of the group's modes (max over its R heads)
   for (int x = 1; x < 16; x <<= 1) U = max(U, __shfl_xor(U, x, 16));
@@ -828,11 +894,13 @@ __global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
   using State = typename std::conditional<PACKED, DecState<DH>, SoftState<DH>>::type;
   State st;
   if constexpr (PACKED) dec_init(st); else state_init(st);
-  const int P = U > 0 ? cv.seq_len[s] - 1 : 0;
   if (U > 0 && wave < 4) {  // waves 0..3 find the window start of pools 0..3
     const int bi = wave;
+    const int P = cv.seq_len[s] - 1;
     const int len = cv.pool_len[s * 4 + bi];
-    const int lb = lower_bound_pos(cv.pos_of(s, bi), len, P - a.w + 1);
+    // the window start matters only to local heads
+    const bool any_local = __builtin_amdgcn_ballot_w64(hm == TRIROUTE_LOCAL) != 0;
+    const int lb = any_local ? lower_bound_pos(cv.pos_of(s, bi), len, P - a.w + 1) : 0;
     if (lane == 0) {
       bounds[bi][0] = lb;
       bounds[bi][1] = len;
@@ -842,9 +910,12 @@ __global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
   if (U > 0) {
     bf16x8 qop[DH / 32];
     float qsum[DH / G];
-    load_q<DH, G>(a.q + (int64_t(b) * a.H + head) * DH, hl < R && hm > 0, qop, qsum);
+    q_operand<DH, G>(qraw, hl < R, qop, qsum);
     wait_vm<0>();  // from here on the only vector-memory traffic is the tile stream
-    Int4 w0, w1, lbs, lens;
+    Int4 w0, w1;
+    TileMask tm0[4];  // the lane's key bounds per pool, in pool slots
+    int mlo[4], mhi[4];
+#pragma unroll
     for (int bi = 0; bi < 4; ++bi) {
       const int lb = bounds[bi][0], len = bounds[bi][1];
       const int lo = U == TRIROUTE_FULL ? 0 : lb;
@@ -853,15 +924,10 @@ __global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
       const int c1 = t0 + int(int64_t(nt) * (split + 1) / a.NS);
       w0.set(bi, __builtin_amdgcn_readfirstlane(c0 + (c1 - c0) * wave / DEC_WAVES));
       w1.set(bi, __builtin_amdgcn_readfirstlane(c0 + (c1 - c0) * (wave + 1) / DEC_WAVES));
-      lbs.set(bi, lb);
-      lens.set(bi, len);
+      mlo[bi] = hm == TRIROUTE_FULL ? 0 : hm == TRIROUTE_LOCAL ? lb : 1;
+      mhi[bi] = hm == TRIROUTE_SKIP ? 0 : len - 1;
+      tm0[bi] = TileMask{mlo[bi], mhi[bi]};
     }
-    auto mask = [&](int bi) {
-      ColMask cm;
-      cm.lo = hm == TRIROUTE_FULL ? 0 : hm == TRIROUTE_LOCAL ? lbs[bi] : 1;
-      cm.hi = hm == TRIROUTE_SKIP ? 0 : lens[bi] - 1;
-      return cm;
-    };
     const uint8_t *rptr = ring + wave * DEC_RING;
     const uint32_t rbase = lds_addr(ring) + wave * DEC_RING;
     if constexpr (PACKED) {
@@ -873,13 +939,19 @@ __global__ __launch_bounds__(512, 2) void attn_decode_kernel(DecodeArgs a) {
       for (int blk = 0; blk < NB; ++blk)
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) qopm[blk * KS + ks] = (n16 >> 2) == blk ? qop[ks] : zero;
-      stream_tiles<DH, G>(cv, s, g, w0, w1, rptr, rbase, [&](int bi, int t, const uint8_t *tp) {
-        fold_dec_any<DH, G>(st, cv, bi, t, tp, mask(bi), qopm, qsum, a.scale2);
+      const bool dead = (n16 >> 2) >= NB;
+      stream_tiles<DH, G>(cv, s, g, w0, w1, rptr, rbase, [&](auto BI, int t, const uint8_t *tp) {
+        constexpr int bi = decltype(BI)::value;
+        DecRegs<DH, 2 << bi, G> r;
+        r.load(tp, cv, bi);
+        const TileMask tm{tm0[bi].lo - t * TS, tm0[bi].hi - t * TS};
+        fold_dec<DH, 2 << bi, G>(st, r, tm, dead, qopm, qsum, a.scale2);
       });
       dec_finish<DH, G>(st);
     } else {
-      stream_tiles<DH, G>(cv, s, g, w0, w1, rptr, rbase, [&](int bi, int t, const uint8_t *tp) {
-        fold_tile<DH, G>(st, cv, bi, t, tp, mask(bi), qop, qsum, a.scale2);
+      stream_tiles<DH, G>(cv, s, g, w0, w1, rptr, rbase, [&](auto BI, int t, const uint8_t *tp) {
+        constexpr int bi = decltype(BI)::value;
+        fold_tile<DH, G, bi>(st, cv, t, tp, ColMask{mlo[bi], mhi[bi]}, qop, qsum, a.scale2);
       });
       state_finish<DH, G>(st);
     }

@@ -36,6 +36,16 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float LOG2E = 1.4426950408889634f;
 
+// Sum over the lanes n, n ^ 16, n ^ 32, n ^ 48 (row-pair and half-wave swaps).
+__device__ __forceinline__ float sum_rows(float x) {
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+  x = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+  return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
+}
+
 __device__ __forceinline__ bf16x8 as_op(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 __device__ __forceinline__ f16x8 as_h(u32x4 v) { return __builtin_bit_cast(f16x8, v); }
 
@@ -398,10 +408,7 @@ __device__ __forceinline__ void q_operand(const u32x4 *raw, bool valid, bf16x8 *
     qsum[ks / gks] += sum;
   }
 #pragma unroll
-  for (int g = 0; g < DH / G; ++g) {
-    qsum[g] += __shfl_xor(qsum[g], 16, 64);
-    qsum[g] += __shfl_xor(qsum[g], 32, 64);
-  }
+  for (int g = 0; g < DH / G; ++g) qsum[g] = sum_rows(qsum[g]);
 }
 
 // Load the query operand of column n16 (a row of q, bf16) and per-group sums.
@@ -529,6 +536,20 @@ __device__ __forceinline__ void tile_to_lds(const uint8_t *src, uint32_t dst, in
   }
 }
 
+// tile_to_lds for a tile of pool BI (size known at compile time) from a
+// wave-uniform address: the transfers are unrolled, only the last one can be
+// partial.
+template <int DH, int G, int BI>
+__device__ __forceinline__ void issue_tile(const uint8_t *src, uint32_t dst) {
+  constexpr int TB = StreamGeo<DH, G>::tb(BI), NI = StreamGeo<DH, G>::ni(BI);
+  const uint32_t off = (threadIdx.x & 63) * 16;
+#pragma unroll
+  for (int j = 0; j < NI; ++j) {
+    if ((j + 1) * 1024 <= TB || off < uint32_t(TB - j * 1024))
+      dma16_s(src + j * 1024, off, dst + j * 1024);
+  }
+}
+
 // 4 wave-uniform ints picked by a run-time index without a private array.
 struct Int4 {
   int v0, v1, v2, v3;
@@ -570,7 +591,12 @@ __device__ __forceinline__ void stream_tiles(const CacheView &cv, int s, int g, 
           ok = pos == phead && phead + sz <= pfree;
       }
       if (!ok) break;
-      tile_to_lds(cv.tile(s, pb, g, pt), rbase + pos, SG::tb(pb), SG::ni(pb));
+      switch (pb) {
+        case 0: issue_tile<DH, G, 0>(cv.tile(s, 0, g, pt), rbase + pos); break;
+        case 1: issue_tile<DH, G, 1>(cv.tile(s, 1, g, pt), rbase + pos); break;
+        case 2: issue_tile<DH, G, 2>(cv.tile(s, 2, g, pt), rbase + pos); break;
+        default: issue_tile<DH, G, 3>(cv.tile(s, 3, g, pt), rbase + pos); break;
+      }
       phead = pos + sz;
       issued += SG::ni(pb);
       ++nin;
@@ -888,9 +914,10 @@ __global__ __launch_bounds__(512, 1) void attn_decode_kernel(DecodeArgs a) {
   const int s = a.seq_ids ? a.seq_ids[b] : b;
   const bool seq_ok = s >= 0 && s < cv.n_seq;
   const int hm = (seq_ok && hl < R) ? int(a.mode[b * a.H + head]) : 0;
-  int U = hm;  // union of the group's modes (max over its R heads)
-  for (int x = 1; x < 16; x <<= 1) U = max(U, __shfl_xor(U, x, 16));
-  U = __builtin_amdgcn_readfirstlane(U);
+  // union of the group's modes (every lane holds one of the R heads)
+  const bool any_full = __builtin_amdgcn_ballot_w64(hm == TRIROUTE_FULL) != 0;
+  const bool any_local = __builtin_amdgcn_ballot_w64(hm == TRIROUTE_LOCAL) != 0;
+  const int U = any_full ? TRIROUTE_FULL : any_local ? TRIROUTE_LOCAL : TRIROUTE_SKIP;
   using State = typename std::conditional<PACKED, DecState<DH>, SoftState<DH>>::type;
   State st;
   if constexpr (PACKED) dec_init(st); else state_init(st);
@@ -899,7 +926,6 @@ __global__ __launch_bounds__(512, 1) void attn_decode_kernel(DecodeArgs a) {
     const int P = cv.seq_len[s] - 1;
     const int len = cv.pool_len[s * 4 + bi];
     // the window start matters only to local heads
-    const bool any_local = __builtin_amdgcn_ballot_w64(hm == TRIROUTE_LOCAL) != 0;
     const int lb = any_local ? lower_bound_pos(cv.pos_of(s, bi), len, P - a.w + 1) : 0;
     if (lane == 0) {
       bounds[bi][0] = lb;
@@ -920,8 +946,9 @@ __global__ __launch_bounds__(512, 1) void attn_decode_kernel(DecodeArgs a) {
       const int lb = bounds[bi][0], len = bounds[bi][1];
       const int lo = U == TRIROUTE_FULL ? 0 : lb;
       const int t0 = lo / TS, nt = (len + TS - 1) / TS - t0;
-      const int c0 = t0 + int(int64_t(nt) * split / a.NS);
-      const int c1 = t0 + int(int64_t(nt) * (split + 1) / a.NS);
+      // nt * NS stays far below 2^31 (capacity / TS tiles, at most 16 chunks)
+      const int c0 = t0 + nt * split / a.NS;
+      const int c1 = t0 + nt * (split + 1) / a.NS;
       w0.set(bi, __builtin_amdgcn_readfirstlane(c0 + (c1 - c0) * wave / DEC_WAVES));
       w1.set(bi, __builtin_amdgcn_readfirstlane(c0 + (c1 - c0) * (wave + 1) / DEC_WAVES));
       mlo[bi] = hm == TRIROUTE_FULL ? 0 : hm == TRIROUTE_LOCAL ? lb : 1;

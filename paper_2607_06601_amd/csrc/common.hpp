@@ -112,6 +112,18 @@ __device__ __forceinline__ void dma16(const void *src, uint32_t lds) {
       : "memory", "m0");
 }
 
+// The same transfer from a wave-uniform base (scalar registers) plus the
+// lane's byte offset voff: no per-lane 64-bit address arithmetic.
+__device__ __forceinline__ void dma16_s(const void *sbase, uint32_t voff, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, %1"
+      :
+      : "v"(voff), "s"(sbase), "s"(__builtin_amdgcn_readfirstlane(lds))
+      : "memory", "m0");
+}
+
 // s_waitcnt vmcnt(N) with the other counters left free (gfx9 encoding:
 // vmcnt[3:0] at bits 3:0, vmcnt[5:4] at bits 15:14, expcnt 6:4, lgkmcnt 11:8).
 template <int N>

@@ -150,9 +150,12 @@ typedef struct triroute_compaction {
  *   K: slot 16*(f / (dh/32)) + (l % 16), channel 32*(f % (dh/32)) + 8*(l / 16) + j
  *   V: slot 32*(f / (dh/16)) + 16*(j / 4) + 4*(l / 16) + j % 4,
  *      channel 16*(f % (dh/16)) + (l % 16)
- * Element q sits in 32-bit word (q/2) / (16/bp) at bit ((q/2) % (16/bp))*bp
- * + (q % 2)*16 for bp < 32 (one element per word for fp32).  Scale/zero
- * blocks are [TS slots][dh/G groups][2] fp16 (scale, zero). */
+ * Bit position of element q (f = q / 8, j = q % 8) in the record's 32-bit words:
+ *   bp = 2:      word q / 16, bit 4*j + 2*(f % 2)
+ *   bp = 4:      word q / 8,  bit 8*(j % 4) + 4*(j / 4)
+ *   bp = 8, 16:  word (q/2) / (16/bp), bit ((q/2) % (16/bp))*bp + (q % 2)*16
+ *   bp = 32:     word q (one element per word)
+ * Scale/zero blocks are [TS slots][dh/G groups][2] fp16 (scale, zero). */
 typedef struct triroute_kv_cache {
   void *base;
   int32_t n_seq;

@@ -49,51 +49,63 @@ __device__ __forceinline__ float sum_rows(float x) {
 __device__ __forceinline__ bf16x8 as_op(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 __device__ __forceinline__ f16x8 as_h(u32x4 v) { return __builtin_bit_cast(f16x8, v); }
 
-// Code fields -> MFMA operands.  A code c below 2^7 becomes bf16 128 + c as
-// the 16-bit pattern [c, 0x43] (low byte first); a code below 2^8 becomes
-// fp16 1024 + c as [c, 0x64].  Codes are first spread one per byte, then one
-// byte permute (v_perm_b32) per operand pair places two codes beside the
-// constant bytes.  Selectors: result bytes 0..3 take bytes (0|1, 4, 2|3, 4)
-// of (codes, constant): 0x04020400 pairs bytes 0 and 2, 0x04030401 bytes 1
-// and 3.
+// Code fields -> MFMA operands.
+//
+// 2- and 4-bit fields are laid out so that one mask turns a word into small
+// floats of the gfx950 conversion instructions: a 2-bit code sits alone in a
+// nibble (fp4 e2m1: code / 2), a 4-bit code alone in a byte (fp8 e4m3:
+// code / 512; codes below 16 are the linear subnormal and first normal
+// range).  The scaled conversions (power-of-two scale 2 or 512) then give
+// the codes themselves as exact fp16 / bf16 pairs, two per instruction.
+//
+// An 8-bit code c becomes fp16 1024 + c as the 16-bit pattern [c, 0x64]
+// (low byte first) by one byte permute (v_perm_b32) per pair; the packed
+// fp16 subtraction of 1024 is exact.  Selectors: result bytes 0..3 take
+// bytes (0|1, 4, 2|3, 4) of (codes, constant): 0x04020400 pairs bytes 0 and
+// 2, 0x04030401 bytes 1 and 3.
 constexpr uint32_t SEL02 = 0x04020400u, SEL13 = 0x04030401u;
-constexpr uint32_t BF16_128 = 0x43434343u, F16_1024 = 0x64646464u;
+constexpr uint32_t F16_1024 = 0x64646464u;
 
-// Eight codes of field f of a lane record (2, 4 or 8 bits) as four operand
-// pairs with constant byte K (the BF16_128 or F16_1024 pattern).  Element q
-// of a record sits in word (q/2) / (16/bp) at bit ((q/2) % (16/bp)) bp +
-// (q % 2) 16, so pair p of field f is at bits s and 16 + s of one word.
+// the 32 bits of a packed pair returned by a conversion builtin
+template <class V>
+__device__ __forceinline__ uint32_t u32_of(V v) {
+  static_assert(sizeof(V) == 4, "a packed pair of 16-bit values");
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// field f of a 2-bit record: its eight codes, one per nibble
+__device__ __forceinline__ uint32_t nibbles2(const uint32_t *w, int f) {
+  const uint32_t x = w[f >> 1];
+  return ((f & 1) ? x >> 2 : x) & 0x33333333u;
+}
+
+// V field of a quantized pool -> fp16 operand holding the codes themselves.
+// (A constant left in the operand would be summed over the whole key range
+// in the fp32 accumulator.)
 template <int BP>
-__device__ __forceinline__ u32x4 code_pairs(const uint32_t *w, int f, uint32_t K) {
+__device__ __forceinline__ f16x8 vfield_h(const uint32_t *w, int f) {
   u32x4 r;
   if constexpr (BP == 2) {
-    // word f/2 holds fields f & ~1 (bytes 0, 2) and f | 1 (bytes 1, 3)
-    const uint32_t x = w[f >> 1];
-    const uint32_t sel = (f & 1) ? SEL13 : SEL02;
-#pragma unroll
-    for (int p = 0; p < 4; ++p) r[p] = __builtin_amdgcn_perm(K, (x >> (2 * p)) & 0x03030303u, sel);
+    const uint32_t y = nibbles2(w, f);
+    r[0] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(y, 2.f, 0));
+    r[1] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(y, 2.f, 1));
+    r[2] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(y, 2.f, 2));
+    r[3] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(y, 2.f, 3));
+    return as_h(r);
   } else if constexpr (BP == 4) {
-    const uint32_t x = w[f];
-    const uint32_t lo = x & 0x0F0F0F0Fu, hi = (x >> 4) & 0x0F0F0F0Fu;
-    r[0] = __builtin_amdgcn_perm(K, lo, SEL02);
-    r[1] = __builtin_amdgcn_perm(K, hi, SEL02);
-    r[2] = __builtin_amdgcn_perm(K, lo, SEL13);
-    r[3] = __builtin_amdgcn_perm(K, hi, SEL13);
+    const uint32_t lo = w[f] & 0x0F0F0F0Fu, hi = (w[f] >> 4) & 0x0F0F0F0Fu;
+    r[0] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(lo, 512.f, false));
+    r[1] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(lo, 512.f, true));
+    r[2] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(hi, 512.f, false));
+    r[3] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(hi, 512.f, true));
+    return as_h(r);
   } else {
 #pragma unroll
     for (int p = 0; p < 4; ++p)
-      r[p] = __builtin_amdgcn_perm(K, w[2 * f + (p >> 1)], (p & 1) ? SEL13 : SEL02);
+      r[p] = __builtin_amdgcn_perm(F16_1024, w[2 * f + (p >> 1)], (p & 1) ? SEL13 : SEL02);
+    const f16x8 k1024 = {1024, 1024, 1024, 1024, 1024, 1024, 1024, 1024};
+    return as_h(r) - k1024;
   }
-  return r;
-}
-
-// V field of a quantized pool -> fp16 operand holding the code itself: the
-// packed fp16 subtraction of 1024 is exact.  (A large constant left in the
-// operand would be summed over the whole key range in the fp32 accumulator.)
-template <int BP>
-__device__ __forceinline__ f16x8 vfield_h(const uint32_t *w, int f) {
-  const f16x8 k1024 = {1024, 1024, 1024, 1024, 1024, 1024, 1024, 1024};
-  return as_h(code_pairs<BP>(w, f, F16_1024)) - k1024;
 }
 
 // exact bf16 pair of two 8-bit codes at bits 0..7 and 16..23
@@ -102,25 +114,32 @@ __device__ __forceinline__ uint32_t pair_byte(uint32_t x) {
   return (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
 }
 
-// K field -> bf16 operand of S^T = K Q^T.  2- and 4-bit codes: 128 + code
-// (the offset is removed algebraically with the Q sums); 8-bit codes: the
-// code itself; 16-bit: the stored values.
+// K field -> bf16 operand of S^T = K Q^T: the codes themselves (2, 4 and 8
+// bits), or the stored values (16 bits).
 template <int BP>
 __device__ __forceinline__ u32x4 kfield(const uint32_t *w, int f) {
-  if constexpr (BP <= 4) {
-    return code_pairs<BP>(w, f, BF16_128);
+  u32x4 r;
+  if constexpr (BP == 2) {
+    const uint32_t y = nibbles2(w, f);
+    r[0] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(y, 2.f, 0));
+    r[1] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(y, 2.f, 1));
+    r[2] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(y, 2.f, 2));
+    r[3] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(y, 2.f, 3));
+  } else if constexpr (BP == 4) {
+    const uint32_t lo = w[f] & 0x0F0F0F0Fu, hi = (w[f] >> 4) & 0x0F0F0F0Fu;
+    r[0] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(lo, 512.f, false));
+    r[1] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(lo, 512.f, true));
+    r[2] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(hi, 512.f, false));
+    r[3] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(hi, 512.f, true));
   } else if constexpr (BP == 8) {
-    u32x4 r;
 #pragma unroll
     for (int p = 0; p < 4; ++p)
       r[p] = pair_byte((w[2 * f + (p >> 1)] >> ((p & 1) * 8)) & 0x00FF00FFu);
-    return r;
   } else {
-    u32x4 r;
 #pragma unroll
     for (int p = 0; p < 4; ++p) r[p] = w[4 * f + p];
-    return r;
   }
+  return r;
 }
 
 // 16-bit pool V field: the stored bf16 values.
@@ -139,8 +158,6 @@ __device__ __forceinline__ f32x4 kmfma(const uint32_t *w, int f, const bf16x8 &q
 
 template <int BP> struct PoolTraits {
   static constexpr int WORDS = 2 * BP;               // 32-bit words per lane record
-  // code offset inside the K operand (bf16 128 + c for 2 and 4 bits)
-  static constexpr float OFF = BP <= 4 ? 128.f : 0.f;
   static constexpr bool QUANT = BP < 16;
 };
 
@@ -286,7 +303,7 @@ __device__ __forceinline__ void process_tile(SoftState<DH> &st,
             float S, Z;
             unpack_sz(tr.ksz[blk][i * NG + g], S, Z);
             sv = fmaf(S, acc[g][i], sv);
-            sv = fmaf(Z - PT::OFF * S, qsum[g], sv);
+            sv = fmaf(Z, qsum[g], sv);
           }
         } else {
 #pragma unroll
@@ -755,7 +772,7 @@ __device__ __forceinline__ void fold_dec(DecState<DH> &st, const DecRegs<DH, BP,
         float S, Z;
         unpack_sz(tr.ksz[i * NG + g], S, Z);
         sv = fmaf(S, acc[g][i], sv);
-        sv = fmaf(Z - PT::OFF * S, qsum[g], sv);
+        sv = fmaf(Z, qsum[g], sv);
       }
     } else {
 #pragma unroll

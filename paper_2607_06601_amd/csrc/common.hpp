@@ -181,17 +181,31 @@ __device__ __forceinline__ void v_place(int st, int c, int dh, int &lane, int &q
   lane = o * 16 + n;
   q = (kv * CB + cb) * 8 + j;
 }
-// element index q of a record of bp bits -> (32-bit word, bit offset)
+// element index q = 8 f + j of a record of bp bits -> (32-bit word, bit offset).
+//   2 bits: word q / 16 holds fields 2w (element j at bit 4 j) and 2w + 1
+//           (bit 4 j + 2): masking the word with 0x33333333 leaves one code
+//           per nibble, an fp4 (e2m1) number worth code / 2;
+//   4 bits: word q / 8 holds field f, element j at bit 8 (j % 4) + 4 (j / 4):
+//           masking with 0x0F0F0F0F leaves one code per byte, an fp8 (e4m3)
+//           number worth code / 512;
+//   8 and 16 bits: pairs 16 bits apart, element q at bit
+//           ((q / 2) % (16 / bp)) bp + (q % 2) 16 of word (q / 2) / (16 / bp);
+//   32 bits: one element per word.
 __device__ __forceinline__ void q_word(int q, int bp, int &word, int &bit) {
-  if (bp == 32) {
+  if (bp == 2) {
+    word = q >> 4;
+    bit = 4 * (q & 7) + 2 * ((q >> 3) & 1);
+  } else if (bp == 4) {
+    word = q >> 3;
+    bit = 8 * (q & 3) + 4 * ((q >> 2) & 1);
+  } else if (bp == 32) {
     word = q;
     bit = 0;
-    return;
+  } else {
+    const int per = 16 / bp, pr = q >> 1;
+    word = pr / per;
+    bit = (pr % per) * bp + (q & 1) * 16;
   }
-  int per = 16 / bp;
-  int pr = q >> 1;
-  word = pr / per;
-  bit = (pr % per) * bp + (q & 1) * 16;
 }
 
 // ------------------------------------------------------------ launch helpers

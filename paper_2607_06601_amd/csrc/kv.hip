@@ -224,7 +224,8 @@ __global__ __launch_bounds__(256) void kv_vpack_kernel(CacheView cv, int B, int 
       const int f = q >> 3, jj = q & 7;
       const int sis = 16 * (jj >> 2) + 4 * (lane >> 4) + (jj & 3);  // slot within the step
       const int ch = 16 * (f % CB) + (lane & 15);
-      const int bt = ((q >> 1) % per) * bp + (q & 1) * 16;
+      int wq, bt;
+      q_word(q, bp, wq, bt);
       const int slot = step * 32 + sis;
       const int t = __shfl(tok, sis, 64);
       if (slot < old)

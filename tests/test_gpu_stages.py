@@ -167,8 +167,14 @@ def _host_decode(raw: np.ndarray, desc, c, s, bi, g, slot, ch, isv, act):
     rec = base + lane * 8 * bp
     if bp == 32:
         return int(raw[rec + 4 * q: rec + 4 * q + 4].view(np.uint32)[0])
-    per = 16 // bp
-    word, bitpos = (q // 2) // per, ((q // 2) % per) * bp + (q % 2) * 16
+    f, j = q // 8, q % 8
+    if bp == 2:
+        word, bitpos = q // 16, 4 * j + 2 * (f % 2)
+    elif bp == 4:
+        word, bitpos = q // 8, 8 * (j % 4) + 4 * (j // 4)
+    else:
+        per = 16 // bp
+        word, bitpos = (q // 2) // per, ((q // 2) % per) * bp + (q % 2) * 16
     w = int(raw[rec + 4 * word: rec + 4 * word + 4].view(np.uint32)[0])
     return (w >> bitpos) & ((1 << bp) - 1)
 

@@ -498,6 +498,9 @@ struct DecodeArgs {
 // issuing tiles, across pool boundaries, for as long as free ring space
 // allows.  The block's 8 rings plus a few words fill the 160 KB of LDS.
 constexpr int DEC_WAVES = 8;
+// Relative cost of a tile of width index bi in the wave split (bytes moved
+// plus dequantisation work, 2 / 4 / 8 / 16 bits).
+__device__ constexpr int DEC_COST[4] = {4, 6, 9, 13};
 constexpr int DEC_RING = 20 * 1024 - 32;
 
 // Per pool width index bi (2, 4, 8, 16 bits): tile bytes (codes + fp16
@@ -514,31 +517,22 @@ struct StreamGeo {
   static_assert(((1024 * 16 + 255) & ~255) <= DEC_RING, "a 16-bit tile fits the ring");
 };
 
-// s_waitcnt vmcnt(n) for a run-time n, rounded down to a value the switch
-// covers (waiting for fewer outstanding transfers is always safe).
+// s_waitcnt vmcnt(n) for a run-time n, rounded down to a value the tree
+// covers (waiting for fewer outstanding transfers is always safe): exact
+// below 4, then multiples of 4 up to 24.
 __device__ __forceinline__ void wait_vm_le(int n) {
-  switch (n < 0 ? 0 : n) {
-    case 0: wait_vm<0>(); break;
-    case 1: wait_vm<1>(); break;
-    case 2: wait_vm<2>(); break;
-    case 3: wait_vm<3>(); break;
-    case 4: wait_vm<4>(); break;
-    case 5: wait_vm<5>(); break;
-    case 6: wait_vm<6>(); break;
-    case 7: wait_vm<7>(); break;
-    case 8: wait_vm<8>(); break;
-    case 9: wait_vm<9>(); break;
-    case 10: wait_vm<10>(); break;
-    case 11: wait_vm<11>(); break;
-    case 12: wait_vm<12>(); break;
-    case 13: wait_vm<13>(); break;
-    case 14: wait_vm<14>(); break;
-    case 15: wait_vm<15>(); break;
-    case 16: case 17: wait_vm<16>(); break;
-    case 18: case 19: wait_vm<18>(); break;
-    case 20: case 21: wait_vm<20>(); break;
-    case 22: case 23: wait_vm<22>(); break;
-    default: wait_vm<24>(); break;
+  if (n >= 12) {
+    if (n >= 20) {
+      if (n >= 24) wait_vm<24>(); else wait_vm<20>();
+    } else {
+      if (n >= 16) wait_vm<16>(); else wait_vm<12>();
+    }
+  } else if (n >= 4) {
+    if (n >= 8) wait_vm<8>(); else wait_vm<4>();
+  } else if (n >= 2) {
+    if (n >= 3) wait_vm<3>(); else wait_vm<2>();
+  } else {
+    if (n >= 1) wait_vm<1>(); else wait_vm<0>();
   }
 }
 
@@ -591,14 +585,20 @@ template <int DH, int G, class Fold>
 __device__ __forceinline__ void stream_tiles(const CacheView &cv, int s, int g, Int4 w0, Int4 w1,
                                              const uint8_t *rptr, uint32_t rbase, Fold &&fold) {
   using SG = StreamGeo<DH, G>;
-  int pb = 0, pt = w0[0];  // producer: next tile to issue
-  while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
+  // The producer walks the concatenation of the four ranges with one index
+  // kp; pool and tile follow from the range ends without branches.
+  const int e1 = w1[0] - w0[0], e2 = e1 + w1[1] - w0[1], e3 = e2 + w1[2] - w0[2];
+  const int ktot = e3 + w1[3] - w0[3];
+  const int d0 = w0[0], d1 = w0[1] - e1, d2 = w0[2] - e2, d3 = w0[3] - e3;
+  int kp = 0;
   int phead = 0, pfree = 0;  // ring end of the newest tile; start of the oldest resident tile
   int nin = 0, issued = 0, consumed = 0;  // tiles resident or in flight; transfers out / used
   int chead = 0;                          // ring end of the last consumed tile
   auto produce = [&]() {
-    while (pb < 4) {
-      const int sz = SG::foot(pb);
+    while (kp < ktot) {
+      const int pb = (kp >= e1) + (kp >= e2) + (kp >= e3);
+      const int tb = (1024 << (pb + 1)) + (pb < 3 ? SG::tb(0) - 2048 : 0);
+      const int sz = (tb + 255) & ~255;
       const int pos = phead + sz <= DEC_RING ? phead : 0;
       bool ok = true;
       if (nin > 0) {
@@ -608,6 +608,7 @@ __device__ __forceinline__ void stream_tiles(const CacheView &cv, int s, int g, 
           ok = pos == phead && phead + sz <= pfree;
       }
       if (!ok) break;
+      const int pt = kp + (pb == 0 ? d0 : pb == 1 ? d1 : pb == 2 ? d2 : d3);
       switch (pb) {
         case 0: issue_tile<DH, G, 0>(cv.tile(s, 0, g, pt), rbase + pos); break;
         case 1: issue_tile<DH, G, 1>(cv.tile(s, 1, g, pt), rbase + pos); break;
@@ -615,10 +616,9 @@ __device__ __forceinline__ void stream_tiles(const CacheView &cv, int s, int g, 
         default: issue_tile<DH, G, 3>(cv.tile(s, 3, g, pt), rbase + pos); break;
       }
       phead = pos + sz;
-      issued += SG::ni(pb);
+      issued += (tb + 1023) >> 10;
       ++nin;
-      ++pt;
-      while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
+      ++kp;
     }
   };
   auto pool = [&](auto BI) {
@@ -958,19 +958,38 @@ __global__ __launch_bounds__(512, 1) void attn_decode_kernel(DecodeArgs a) {
     Int4 w0, w1;
     TileMask tm0[4];  // the lane's key bounds per pool, in pool slots
     int mlo[4], mhi[4];
+    // The chunk's tiles of the four pools, taken as one list in pool order,
+    // are cut into DEC_WAVES contiguous runs of about equal cost (a tile of
+    // width bi costs DEC_COST[bi]: its bytes and its dequantisation work);
+    // a tile goes to the run that holds its midpoint.
+    int c0[4], nc[4], wsum = 0;
 #pragma unroll
     for (int bi = 0; bi < 4; ++bi) {
       const int lb = bounds[bi][0], len = bounds[bi][1];
       const int lo = U == TRIROUTE_FULL ? 0 : lb;
       const int t0 = lo / TS, nt = (len + TS - 1) / TS - t0;
       // nt * NS stays far below 2^31 (capacity / TS tiles, at most 16 chunks)
-      const int c0 = t0 + nt * split / a.NS;
-      const int c1 = t0 + nt * (split + 1) / a.NS;
-      w0.set(bi, __builtin_amdgcn_readfirstlane(c0 + (c1 - c0) * wave / DEC_WAVES));
-      w1.set(bi, __builtin_amdgcn_readfirstlane(c0 + (c1 - c0) * (wave + 1) / DEC_WAVES));
+      c0[bi] = t0 + nt * split / a.NS;
+      nc[bi] = t0 + nt * (split + 1) / a.NS - c0[bi];
+      wsum += nc[bi] * DEC_COST[bi];
       mlo[bi] = hm == TRIROUTE_FULL ? 0 : hm == TRIROUTE_LOCAL ? lb : 1;
       mhi[bi] = hm == TRIROUTE_SKIP ? 0 : len - 1;
       tm0[bi] = TileMask{mlo[bi], mhi[bi]};
+    }
+    int pre = 0;  // cost of the earlier pools' tiles
+#pragma unroll
+    for (int bi = 0; bi < 4; ++bi) {
+      // first tile i of run r: DEC_WAVES (2 pre + (2 i + 1) c) >= 2 wsum r
+      const int c = DEC_COST[bi];
+      auto first = [&](int r) {
+        const int num = 2 * wsum * r - DEC_WAVES * (2 * pre + c);
+        const int den = 2 * DEC_WAVES * c;
+        const int i = num <= 0 ? 0 : (num + den - 1) / den;
+        return min(i, nc[bi]);
+      };
+      w0.set(bi, __builtin_amdgcn_readfirstlane(c0[bi] + first(wave)));
+      w1.set(bi, __builtin_amdgcn_readfirstlane(c0[bi] + first(wave + 1)));
+      pre += nc[bi] * c;
     }
     const uint8_t *rptr = ring + wave * DEC_RING;
     const uint32_t rbase = lds_addr(ring) + wave * DEC_RING;

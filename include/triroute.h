@@ -153,7 +153,8 @@ typedef struct triroute_compaction {
  * Bit position of element q (f = q / 8, j = q % 8) in the record's 32-bit words:
  *   bp = 2:      word q / 16, bit 4*j + 2*(f % 2)
  *   bp = 4:      word q / 8,  bit 8*(j % 4) + 4*(j / 4)
- *   bp = 8, 16:  word (q/2) / (16/bp), bit ((q/2) % (16/bp))*bp + (q % 2)*16
+ *   bp = 8:      word q / 4,  bit 8*(q % 4)
+ *   bp = 16:     word q / 2,  bit 16*(q % 2)
  *   bp = 32:     word q (one element per word)
  * Scale/zero blocks are [TS slots][dh/G groups][2] fp16 (scale, zero). */
 typedef struct triroute_kv_cache {

@@ -61,9 +61,9 @@ __device__ __forceinline__ f16x8 as_h(u32x4 v) { return __builtin_bit_cast(f16x8
 // An 8-bit code c becomes fp16 1024 + c as the 16-bit pattern [c, 0x64]
 // (low byte first) by one byte permute (v_perm_b32) per pair; the packed
 // fp16 subtraction of 1024 is exact.  Selectors: result bytes 0..3 take
-// bytes (0|1, 4, 2|3, 4) of (codes, constant): 0x04020400 pairs bytes 0 and
-// 2, 0x04030401 bytes 1 and 3.
-constexpr uint32_t SEL02 = 0x04020400u, SEL13 = 0x04030401u;
+// bytes (0|2, 4, 1|3, 4) of (codes, constant): 0x04010400 pairs bytes 0 and
+// 1, 0x04030402 bytes 2 and 3.
+constexpr uint32_t SEL01 = 0x04010400u, SEL23 = 0x04030402u;
 constexpr uint32_t F16_1024 = 0x64646464u;
 
 // the 32 bits of a packed pair returned by a conversion builtin
@@ -102,16 +102,10 @@ __device__ __forceinline__ f16x8 vfield_h(const uint32_t *w, int f) {
   } else {
 #pragma unroll
     for (int p = 0; p < 4; ++p)
-      r[p] = __builtin_amdgcn_perm(F16_1024, w[2 * f + (p >> 1)], (p & 1) ? SEL13 : SEL02);
+      r[p] = __builtin_amdgcn_perm(F16_1024, w[2 * f + (p >> 1)], (p & 1) ? SEL23 : SEL01);
     const f16x8 k1024 = {1024, 1024, 1024, 1024, 1024, 1024, 1024, 1024};
     return as_h(r) - k1024;
   }
-}
-
-// exact bf16 pair of two 8-bit codes at bits 0..7 and 16..23
-__device__ __forceinline__ uint32_t pair_byte(uint32_t x) {
-  const float lo = float(x & 0xFFu), hi = float((x >> 16) & 0xFFu);
-  return (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
 }
 
 // K field -> bf16 operand of S^T = K Q^T: the codes themselves (2, 4 and 8
@@ -132,9 +126,14 @@ __device__ __forceinline__ u32x4 kfield(const uint32_t *w, int f) {
     r[2] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(hi, 512.f, false));
     r[3] = u32_of(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(hi, 512.f, true));
   } else if constexpr (BP == 8) {
+    // byte -> fp32 (exact), whose upper half is the exact bf16
 #pragma unroll
-    for (int p = 0; p < 4; ++p)
-      r[p] = pair_byte((w[2 * f + (p >> 1)] >> ((p & 1) * 8)) & 0x00FF00FFu);
+    for (int p = 0; p < 4; ++p) {
+      const uint32_t x = w[2 * f + (p >> 1)];
+      const float lo = float((x >> (16 * (p & 1))) & 0xFFu);
+      const float hi = float((x >> (16 * (p & 1) + 8)) & 0xFFu);
+      r[p] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
+    }
   } else {
 #pragma unroll
     for (int p = 0; p < 4; ++p) r[p] = w[4 * f + p];

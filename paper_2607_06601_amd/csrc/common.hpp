@@ -188,8 +188,8 @@ __device__ __forceinline__ void v_place(int st, int c, int dh, int &lane, int &q
 //   4 bits: word q / 8 holds field f, element j at bit 8 (j % 4) + 4 (j / 4):
 //           masking with 0x0F0F0F0F leaves one code per byte, an fp8 (e4m3)
 //           number worth code / 512;
-//   8 and 16 bits: pairs 16 bits apart, element q at bit
-//           ((q / 2) % (16 / bp)) bp + (q % 2) 16 of word (q / 2) / (16 / bp);
+//   8 bits: word q / 4, element q at byte q % 4;
+//   16 bits: word q / 2, element q at bit 16 (q % 2);
 //   32 bits: one element per word.
 __device__ __forceinline__ void q_word(int q, int bp, int &word, int &bit) {
   if (bp == 2) {
@@ -198,13 +198,15 @@ __device__ __forceinline__ void q_word(int q, int bp, int &word, int &bit) {
   } else if (bp == 4) {
     word = q >> 3;
     bit = 8 * (q & 3) + 4 * ((q >> 2) & 1);
-  } else if (bp == 32) {
+  } else if (bp == 8) {
+    word = q >> 2;
+    bit = 8 * (q & 3);
+  } else if (bp == 16) {
+    word = q >> 1;
+    bit = 16 * (q & 1);
+  } else {
     word = q;
     bit = 0;
-  } else {
-    const int per = 16 / bp, pr = q >> 1;
-    word = pr / per;
-    bit = (pr % per) * bp + (q & 1) * 16;
   }
 }
 

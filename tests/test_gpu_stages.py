@@ -172,9 +172,10 @@ def _host_decode(raw: np.ndarray, desc, c, s, bi, g, slot, ch, isv, act):
         word, bitpos = q // 16, 4 * j + 2 * (f % 2)
     elif bp == 4:
         word, bitpos = q // 8, 8 * (j % 4) + 4 * (j // 4)
+    elif bp == 8:
+        word, bitpos = q // 4, 8 * (q % 4)
     else:
-        per = 16 // bp
-        word, bitpos = (q // 2) // per, ((q // 2) % per) * bp + (q % 2) * 16
+        word, bitpos = q // 2, 16 * (q % 2)
     w = int(raw[rec + 4 * word: rec + 4 * word + 4].view(np.uint32)[0])
     return (w >> bitpos) & ((1 << bp) - 1)
 

@@ -36,6 +36,16 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float LOG2E = 1.4426950408889634f;
 
+// Max over the lanes n, n ^ 16, n ^ 32, n ^ 48 (row-pair and half-wave swaps).
+__device__ __forceinline__ float max_rows(float x) {
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+  x = fmaxf(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+  const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+  return fmaxf(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
+}
+
 // Sum over the lanes n, n ^ 16, n ^ 32, n ^ 48 (row-pair and half-wave swaps).
 __device__ __forceinline__ float sum_rows(float x) {
   const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
@@ -177,9 +187,14 @@ struct SoftState {
   f32x4 O[DH / 16];      // rows = columns 4*o4 + i, cols = channel n16 + 16 cb
 };
 
+// The running max starts at a large finite negative value instead of -inf,
+// so that exp2(score - m) of a masked score (-inf) is 0 without a test; a
+// column that sees no key keeps l = 0 and yields a zero output.
+constexpr float M0 = -1.0e30f;
+
 template <int DH>
 __device__ __forceinline__ void state_init(SoftState<DH> &st) {
-  st.m = -INFINITY;
+  st.m = M0;
   st.l = 0.f;
 #pragma unroll
   for (int g = 0; g < DH / 32; ++g) st.zc[g] = 0.f;
@@ -210,6 +225,8 @@ struct TileRegs {
   uint32_t ksz[Q ? Gm::NB : 1][4 * NG];        // [block][slot i * NG + g]
   uint32_t vsz[Q ? Gm::KV : 1][2][4 * NG];     // [step][half][slot i * NG + g]
   int key[POS ? Gm::NB : 1][4];                // key positions (INT_MAX past klen)
+  int kfirst, klast;  // POS: positions of the tile's first and last slot (klast: INT_MAX if
+                      // the tile runs past the pool length)
 
   // tp: the tile; kpos: positions of the tile's slots (POS only); slot0:
   // pool slot of the tile's first slot; klen: pool length.
@@ -247,6 +264,8 @@ struct TileRegs {
           }
     }
     if constexpr (POS) {
+      kfirst = kpos[0];
+      klast = slot0 + Gm::TS <= klen ? kpos[Gm::TS - 1] : INT_MAX;
 #pragma unroll
       for (int blk = 0; blk < Gm::NB; ++blk)
 #pragma unroll
@@ -308,41 +327,72 @@ __device__ __forceinline__ void process_tile(SoftState<DH> &st,
 #pragma unroll
           for (int g = 0; g < NG; ++g) sv += acc[g][i];
         }
-        int key;
-        if constexpr (POS)
-          key = tr.key[blk][i];
-        else
-          key = slot0 + blk * 16 + 4 * o4 + i;
-        p[hb][i] = (key >= cm.lo && key <= cm.hi) ? sv * scale2 : -INFINITY;
+        p[hb][i] = sv * scale2;
       }
     }
-    // ---- online softmax for this lane's column
+    // keys outside the column's range: per-key tests only when some lane's
+    // range cuts through the tile
+    {
+      int first, last;
+      if constexpr (POS) {
+        first = tr.kfirst;
+        last = tr.klast;
+      } else {
+        first = slot0;
+        last = slot0 + Gm::TS - 1;
+      }
+      const bool none = cm.lo > cm.hi || last < cm.lo || first > cm.hi;
+      const bool all = first >= cm.lo && last <= cm.hi;
+      if (!__builtin_amdgcn_ballot_w64(!none && !all)) {
+        if (__builtin_amdgcn_ballot_w64(none)) {
+#pragma unroll
+          for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) p[hb][i] = none ? -INFINITY : p[hb][i];
+        }
+      } else {
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            int key;
+            if constexpr (POS)
+              key = tr.key[2 * kv + hb][i];
+            else
+              key = slot0 + (2 * kv + hb) * 16 + 4 * o4 + i;
+            p[hb][i] = (key >= cm.lo && key <= cm.hi) ? p[hb][i] : -INFINITY;
+          }
+      }
+    }
+    // ---- online softmax for this lane's column (lanes n16 + 16 k); the
+    // output rows are rescaled only when some column's running max grows
     float mt = fmaxf(fmaxf(fmaxf(p[0][0], p[0][1]), fmaxf(p[0][2], p[0][3])),
                      fmaxf(fmaxf(p[1][0], p[1][1]), fmaxf(p[1][2], p[1][3])));
-    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float mnew = fmaxf(st.m, mt);
-    const bool live = mnew != -INFINITY;
-    const float corr = live ? exp2f(st.m - mnew) : 1.f;
+    mt = max_rows(mt);
+    if (__builtin_amdgcn_ballot_w64(mt > st.m)) {
+      const float mnew = fmaxf(st.m, mt);
+      const float corr = __builtin_amdgcn_exp2f(st.m - mnew);
+      st.l *= corr;
+#pragma unroll
+      for (int g = 0; g < NG; ++g) st.zc[g] *= corr;
+      st.m = mnew;
+      // column 4 o4 + i lives in lane 4 o4 + i
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float ci = __shfl(corr, 4 * o4 + i, 64);
+#pragma unroll
+        for (int cb = 0; cb < Gm::CB; ++cb) st.O[cb][i] *= ci;
+      }
+    }
     float ps = 0.f;
 #pragma unroll
     for (int hb = 0; hb < 2; ++hb)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        p[hb][i] = live ? exp2f(p[hb][i] - mnew) : 0.f;
+        p[hb][i] = __builtin_amdgcn_exp2f(p[hb][i] - st.m);
         ps += p[hb][i];
       }
-    st.l = st.l * corr + ps;
-#pragma unroll
-    for (int g = 0; g < NG; ++g) st.zc[g] *= corr;
-    st.m = mnew;
-    // rescale the output rows (column 4 o4 + i lives in lane 4 o4 + i)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float ci = __shfl(corr, 4 * o4 + i, 64);
-#pragma unroll
-      for (int cb = 0; cb < Gm::CB; ++cb) st.O[cb][i] *= ci;
-    }
+    st.l += ps;
     // ---- O += P' V.  Quantized pools: P' = fp16(p * s_v) against fp16
     // codes; the 16-bit pool: P = bf16(p) against the stored bf16.
     u32x4 pk[NG];
@@ -670,10 +720,7 @@ __device__ __forceinline__ float max_lane_mod4(float x) {
 // operand order of the V layout, zero outside its block.  The virtual rows
 // of a head are summed once at the end.
 //
-// The running max starts at a large finite negative value instead of -inf,
-// so that exp2(score - m) of a masked score (-inf) is 0 without a test; a
-// head that sees no key keeps l = 0 and yields a zero output.
-constexpr float DEC_M0 = -1.0e30f;
+// The running max starts at M0 (see state_init).
 
 template <int DH>
 struct DecState {
@@ -685,7 +732,7 @@ struct DecState {
 
 template <int DH>
 __device__ __forceinline__ void dec_init(DecState<DH> &st) {
-  st.m = DEC_M0;
+  st.m = M0;
   st.l = 0.f;
 #pragma unroll
   for (int g = 0; g < DH / 32; ++g) st.zc[g] = 0.f;

@@ -77,14 +77,37 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 // Reductions within aligned lane segments of `seg` lanes (seg a power of 2).
-__device__ __forceinline__ float seg_min(float v, int seg) {
-  for (int m = seg >> 1; m >= 1; m >>= 1) v = fminf(v, __shfl_xor(v, m, WAVE));
+// min / max over aligned segments of `seg` lanes (seg a power of two <= 64,
+// wave-uniform).  Segments of 16 or more lanes reduce within 16-lane rows by
+// row rotations (DPP) and across rows by row-pair and half-wave swaps, with
+// no trip through LDS; smaller segments use lane shuffles.
+template <bool MAX>
+__device__ __forceinline__ float seg_reduce(float v, int seg) {
+  auto op = [](float a, float b) { return MAX ? fmaxf(a, b) : fminf(a, b); };
+  if (seg >= 16) {
+#define TR_ROR(n) __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x120 + (n), 0xF, 0xF, false))
+    v = op(v, TR_ROR(1));
+    v = op(v, TR_ROR(2));
+    v = op(v, TR_ROR(4));
+    v = op(v, TR_ROR(8));
+#undef TR_ROR
+    if (seg >= 32) {
+      const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                      false);
+      v = op(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    }
+    if (seg >= 64) {
+      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                      false);
+      v = op(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    }
+    return v;
+  }
+  for (int m = seg >> 1; m >= 1; m >>= 1) v = op(v, __shfl_xor(v, m, WAVE));
   return v;
 }
-__device__ __forceinline__ float seg_max(float v, int seg) {
-  for (int m = seg >> 1; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, WAVE));
-  return v;
-}
+__device__ __forceinline__ float seg_min(float v, int seg) { return seg_reduce<false>(v, seg); }
+__device__ __forceinline__ float seg_max(float v, int seg) { return seg_reduce<true>(v, seg); }
 __device__ __forceinline__ uint64_t lanemask_lt() {
   int l = __lane_id();
   return l ? (~0ull >> (64 - l)) : 0ull;

@@ -81,7 +81,8 @@ __global__ __launch_bounds__(256) void kv_slots_kernel(CacheView cv, int T,
 // 32-bit word of a K record belongs to one slot), scales and 8/16-bit V
 // codes (byte and half-word stores); 2- and 4-bit V codes share words with
 // neighbouring slots and go to vstage, one byte per element, for
-// kv_vpack_kernel.
+// kv_vpack_kernel.  The K words of the token are assembled in LDS: each lane
+// ORs its element into its word, then one lane per word stores it.
 template <typename T>
 __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int N,
                                                        const int32_t *__restrict__ seq_ids,
@@ -90,26 +91,45 @@ __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int
                                                        const uint8_t *__restrict__ bit,
                                                        const int32_t *__restrict__ slots,
                                                        uint8_t *__restrict__ vstage) {
-  __shared__ uint32_t el[4][2][128];  // per wave: element value per channel (K, V)
+  __shared__ uint32_t kw[4][128];  // per wave: the token's K words (at most 4 dh bits... / 32)
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int item = blockIdx.x * 4 + w;
   const int Hkv = cv.Hkv, dh = cv.dh, G = cv.G;
   const int i = item / Hkv, g = item % Hkv;
   const int slot = item < N * Hkv ? slots[i] : -1;
-  const bool valid = slot >= 0;  // uniform per wave
+  if (slot < 0) return;  // wave-uniform: nothing of this wave touches LDS or a barrier
   const int b = i / T_;
-  const int s = valid ? (seq_ids ? seq_ids[b] : b) : 0;
-  const int bi = valid ? int(bit[i]) : 0;
+  const int s = seq_ids ? seq_ids[b] : b;
+  const int bi = int(bit[i]);
   const int bp = cv.bits(bi);
-  const int tile = valid ? slot / cv.TS : 0, st = valid ? slot % cv.TS : 0;
+  const int tile = slot / cv.TS, st = slot % cv.TS;
   uint8_t *tp = cv.tile(s, bi, g, tile);
   const int NR = dh >> 6;  // channels per lane: lane + 64 r
-  for (int kvsel = 0; kvsel < 2 && valid; ++kvsel) {
-    const T *src = (kvsel ? vin : kin) + int64_t(i) * Hkv * dh + g * dh;
-    for (int r = 0; r < NR; ++r) {
+  // both rows first, so that the two loads are in flight together
+  T kr[2], vr[2];
+  const int64_t row = int64_t(i) * Hkv * dh + g * dh;
+#pragma unroll
+  for (int r = 0; r < 2; ++r)
+    if (r < NR) {
+      kr[r] = kin[row + lane + 64 * r];
+      vr[r] = vin[row + lane + 64 * r];
+    }
+  const int KS = dh >> 5;
+  const int blk = st >> 4, n = st & 15;
+  const int per = bp == 32 ? 1 : 32 / bp;                 // elements per word
+  const int q0 = blk * KS * 8, nq = KS * 8;                // this token's elements per record
+  const int wpr = (nq + per - 1) / per;                    // its words per record
+  const int nw = 4 * wpr;                                  // K words of the token
+  for (int x = lane; x < nw; x += 64) kw[w][x] = 0u;
+  uint8_t *vp = tp + cv.v_codes_off(bi);
+#pragma unroll
+  for (int kvsel = 0; kvsel < 2; ++kvsel) {
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      if (r >= NR) break;
       const int c = lane + 64 * r;
-      T raw = src[c];
-      float x = Act<T>::cvt(raw);
+      const T raw = kvsel ? vr[r] : kr[r];
+      const float x = Act<T>::cvt(raw);
       uint32_t e;
       if (bi == 3) {
         if (sizeof(T) == 2)
@@ -118,70 +138,56 @@ __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int
           e = __float_as_uint(x);
       } else {
         const int seg = G < 64 ? G : 64;
-        float mn = seg_min(x, seg), mx = seg_max(x, seg);
+        const float mn = seg_min(x, seg), mx = seg_max(x, seg);
         const float levels = float((1 << bp) - 1);
-        float s32 = __fdiv_rn(mx - mn, levels);
-        _Float16 s16 = (_Float16)s32;
-        _Float16 z16 = (_Float16)mn;
-        float S = (float)s16, Z = (float)z16;
+        const float s32 = __fdiv_rn(mx - mn, levels);
+        const _Float16 s16 = (_Float16)s32;
+        const _Float16 z16 = (_Float16)mn;
+        const float S = (float)s16, Z = (float)z16;
         float q = 0.f;
         if (S != 0.f) q = fminf(fmaxf(rintf(__fdiv_rn(x - Z, S)), 0.f), levels);
         e = uint32_t(q);
         if ((lane & (seg - 1)) == 0) {
           const int grp = c / G;
           const int off = (kvsel ? cv.v_sz_off(bi) : cv.k_sz_off(bi)) + (st * (dh / G) + grp) * 4;
-          uint32_t pk = uint32_t(*(uint16_t *)&s16) | (uint32_t(*(uint16_t *)&z16) << 16);
+          const uint32_t pk = uint32_t(*(const uint16_t *)&s16) | (uint32_t(*(const uint16_t *)&z16) << 16);
           *(uint32_t *)(tp + off) = pk;
         }
       }
-      el[w][kvsel][c] = e;
-    }
-  }
-  __syncthreads();
-  if (!valid) return;
-  // ---- K: every 32-bit word touched by this token belongs to it alone
-  {
-    const int KS = dh >> 5;
-    const int blk = st >> 4, n = st & 15;
-    const int per = bp == 32 ? 1 : 32 / bp;         // elements per word
-    const int q0 = blk * KS * 8, nq = KS * 8;        // this token's element range per record
-    const int words_per_rec = (nq + per - 1) / per;
-    for (int wid = lane; wid < 4 * words_per_rec; wid += 64) {
-      const int o = wid / words_per_rec, wr = wid % words_per_rec;
-      const int qa = q0 + wr * per;
-      uint32_t val = 0;
-      int word = 0;
-      for (int qq = qa; qq < qa + per; ++qq) {
-        const int f = qq >> 3, j = qq & 7;
-        const int ks = f % KS;
-        const int c = 32 * ks + 8 * o + j;
+      if (kvsel == 0) {
+        // K element (slot st, channel c): record o, element q = f * 8 + j
+        const int ks = c >> 5, o = (c >> 3) & 3, j = c & 7;
+        const int q = (blk * KS + ks) * 8 + j;
         int wd, bt;
-        q_word(qq, bp, wd, bt);
-        word = wd;
-        val |= el[w][0][c] << bt;
+        q_word(q, bp, wd, bt);
+        if (bp == 32)
+          kw[w][o * wpr + (wd - q0)] = e;
+        else
+          atomicOr(&kw[w][o * wpr + (wd - q0 / per)], e << bt);
+      } else {
+        int ln, q, wd, bt;
+        v_place(st, c, dh, ln, q);
+        q_word(q, bp, wd, bt);
+        uint8_t *addr = vp + ln * (8 * bp) + wd * 4;
+        if (bp <= 4)
+          vstage[(int64_t(i) * Hkv + g) * dh + c] = uint8_t(e);
+        else if (bp == 8)
+          addr[bt >> 3] = uint8_t(e);
+        else if (bp == 16)
+          *(uint16_t *)(addr + (bt >> 3)) = uint16_t(e);
+        else
+          *(uint32_t *)addr = e;
       }
-      *(uint32_t *)(tp + (o * 16 + n) * (8 * bp) + word * 4) = val;
     }
   }
-  // ---- V: words are shared by neighbouring slots
-  {
-    uint8_t *vp = tp + cv.v_codes_off(bi);
-    for (int r = 0; r < NR; ++r) {
-      const int c = lane + 64 * r;
-      int ln, q, wd, bt;
-      v_place(st, c, dh, ln, q);
-      q_word(q, bp, wd, bt);
-      uint8_t *addr = vp + ln * (8 * bp) + wd * 4;
-      const uint32_t e = el[w][1][c];
-      if (bp <= 4)
-        vstage[(int64_t(i) * Hkv + g) * dh + c] = uint8_t(e);
-      else if (bp == 8)
-        addr[bt >> 3] = uint8_t(e);
-      else if (bp == 16)
-        *(uint16_t *)(addr + (bt >> 3)) = uint16_t(e);
-      else
-        *(uint32_t *)addr = e;
-    }
+  // the wave's own LDS words: order its ORs before its reads (no other wave
+  // touches them, so no block barrier)
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_wave_barrier();
+  for (int x = lane; x < nw; x += 64) {
+    const int o = x / wpr, wr = x % wpr;
+    const int wd = q0 / per + wr;
+    *(uint32_t *)(tp + (o * 16 + n) * (8 * bp) + wd * 4) = kw[w][x];
   }
 }
 

@@ -1154,10 +1154,10 @@ struct PrefillArgs {
 // positions; direct-to-LDS transfers split over the waves, D - 1 tiles
 // ahead) and every wave folds every tile with its own position masks.
 constexpr int PF_WAVES = 4;
-constexpr int PF_D = 4;  // ring slots
+constexpr int PF_D = 3;  // ring slots
 
 template <int DH, int G>
-__global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(256, 3) void attn_prefill_mfma_kernel(PrefillArgs a) {
   using SG = StreamGeo<DH, G>;
   constexpr int TS = 4096 / DH;
   constexpr int SLOT = (1024 * 16 + 4 * TS + 255) & ~255;  // widest tile + its positions

@@ -107,6 +107,26 @@ __device__ __forceinline__ float seg_reduce(float v, int seg) {
   return v;
 }
 __device__ __forceinline__ float seg_min(float v, int seg) { return seg_reduce<false>(v, seg); }
+// sum over aligned segments of 16, 32 or 64 lanes (same lane pattern)
+__device__ __forceinline__ float seg_sum(float v, int seg) {
+#define TR_ROR(n) __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x120 + (n), 0xF, 0xF, false))
+  v += TR_ROR(1);
+  v += TR_ROR(2);
+  v += TR_ROR(4);
+  v += TR_ROR(8);
+#undef TR_ROR
+  if (seg >= 32) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                    false);
+    v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+  if (seg >= 64) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                    false);
+    v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+  return v;
+}
 __device__ __forceinline__ float seg_max(float v, int seg) { return seg_reduce<true>(v, seg); }
 __device__ __forceinline__ uint64_t lanemask_lt() {
   int l = __lane_id();

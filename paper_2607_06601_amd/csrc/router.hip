@@ -177,7 +177,6 @@ __global__ __launch_bounds__(256) void router_tail_kernel(
   float(*Zs)[LD] = (float(*)[LD])(rt_lds + (DR + RT_NZ + TB) * LD);
   const int NZ = 3 * H + E1 + 4;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int t0 = blockIdx.x * TB;
   for (int i = tid; i < DR * DR / 4; i += 256) {
     const int r = i / (DR / 4), c4 = (i % (DR / 4)) * 4;
     const float4 v = *(const float4 *)(W2 + r * DR + c4);
@@ -190,28 +189,45 @@ __global__ __launch_bounds__(256) void router_tail_kernel(
     const float4 v = *(const float4 *)(wz + c4);
     Wzs[z][c4] = v.x; Wzs[z][c4 + 1] = v.y; Wzs[z][c4 + 2] = v.z; Wzs[z][c4 + 3] = v.w;
   }
+  // the weights stay in LDS while the block walks its token tiles; with at
+  // most 4 trunk chunks the next tile's partials are loaded while the
+  // current tile is computed
+  constexpr int EPT = TB * DR / 256;
+  float pre[4][EPT];
+  auto load_parts = [&](int tt0, int s0, float (*v)[EPT]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        const int idx = tid + 256 * e, t = idx / DR, c = idx % DR;
+        v[j][e] = (s0 + j < KS && tt0 + t < N)
+                      ? upart[(int64_t(s0 + j) * N + tt0 + t) * DR + c] : 0.f;
+      }
+  };
+  const bool prefetch = KS <= 4;
+  if (prefetch) load_parts(blockIdx.x * TB, 0, pre);
+  for (int t0 = blockIdx.x * TB; t0 < N; t0 += gridDim.x * TB) {
   {
     // u = GELU(sum of the KS trunk partials + b1): thread tid owns elements
-    // tid + 256 e of the block's 16 x 128; partials are summed in chunk order,
-    // four chunks' loads in flight at a time
-    constexpr int EPT = TB * DR / 256;
+    // tid + 256 e of the block's 16 x 128; partials are summed in chunk order
     float sacc[EPT];
 #pragma unroll
     for (int e = 0; e < EPT; ++e) sacc[e] = 0.f;
-    for (int s0 = 0; s0 < KS; s0 += 4) {
-      float v[4][EPT];
+    if (prefetch) {
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int e = 0; e < EPT; ++e) {
-          const int idx = tid + 256 * e, t = idx / DR, c = idx % DR;
-          v[j][e] = (s0 + j < KS && t0 + t < N)
-                        ? upart[(int64_t(s0 + j) * N + t0 + t) * DR + c] : 0.f;
-        }
+        for (int e = 0; e < EPT; ++e) sacc[e] += pre[j][e];
+      if (t0 + gridDim.x * TB < N) load_parts(t0 + gridDim.x * TB, 0, pre);
+    } else {
+      for (int s0 = 0; s0 < KS; s0 += 4) {
+        float v[4][EPT];
+        load_parts(t0, s0, v);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int e = 0; e < EPT; ++e) sacc[e] += v[j][e];
+          for (int e = 0; e < EPT; ++e) sacc[e] += v[j][e];
+      }
     }
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
@@ -225,84 +241,107 @@ __global__ __launch_bounds__(256) void router_tail_kernel(
     }
   }
   __syncthreads();
-  // h: wave w computes columns 32 w .. 32 w + 31
-  f32x4r hacc[2] = {f32x4r{0.f, 0.f, 0.f, 0.f}, f32x4r{0.f, 0.f, 0.f, 0.f}};
+  // h: wave w computes columns 32 w .. 32 w + 31 (two accumulators per
+  // column tile, even and odd K steps, so that two MFMA chains interleave)
+  f32x4r hacc[2][2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) hacc[j][0] = hacc[j][1] = f32x4r{0.f, 0.f, 0.f, 0.f};
 #pragma unroll 8
   for (int kk = 0; kk < DR; kk += 4) {
     const float av = Us[lane & 15][kk + (lane >> 4)];
 #pragma unroll
     for (int j = 0; j < 2; ++j)
-      hacc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-          av, W2s[32 * wave + 16 * j + (lane & 15)][kk + (lane >> 4)], hacc[j], 0, 0, 0);
+      hacc[j][(kk >> 2) & 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+          av, W2s[32 * wave + 16 * j + (lane & 15)][kk + (lane >> 4)], hacc[j][(kk >> 2) & 1], 0,
+          0, 0);
   }
   __syncthreads();
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int n = 32 * wave + 16 * j + (lane & 15);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) Us[4 * (lane >> 4) + r][n] = hacc[j][r] + b2[n];
+    for (int r = 0; r < 4; ++r) Us[4 * (lane >> 4) + r][n] = (hacc[j][0][r] + hacc[j][1][r]) + b2[n];
   }
   __syncthreads();
-  for (int t = wave; t < TB; t += 4) {
-    const float a = Us[t][lane], b = Us[t][lane + 64];
-    const float ss = wave_sum(a * a + b * b);
-    const float r = 1.0f / sqrtf(ss / float(DR) + eps);
-    Us[t][lane] = (a * r) * gr[lane];
-    Us[t][lane + 64] = (b * r) * gr[lane + 64];
+  {
+    // RMSNorm of h: wave w takes tokens w, w + 4, w + 8, w + 12 together
+    constexpr int TPW = TB / 4;
+    float av[TPW], bv[TPW], ss[TPW];
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) {
+      av[j] = Us[wave + 4 * j][lane];
+      bv[j] = Us[wave + 4 * j][lane + 64];
+      ss[j] = av[j] * av[j] + bv[j] * bv[j];
+    }
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) ss[j] = seg_sum(ss[j], 64);
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) {
+      const float r = 1.0f / sqrtf(ss[j] / float(DR) + eps);
+      Us[wave + 4 * j][lane] = (av[j] * r) * gr[lane];
+      Us[wave + 4 * j][lane + 64] = (bv[j] * r) * gr[lane + 64];
+    }
   }
   __syncthreads();
   for (int nt = wave; nt * 16 < NZ; nt += 4) {
     const int z = nt * 16 + (lane & 15);
     const int zr = z < NZ ? z : NZ - 1;
-    f32x4r zacc = {0.f, 0.f, 0.f, 0.f};
+    f32x4r zacc[2] = {f32x4r{0.f, 0.f, 0.f, 0.f}, f32x4r{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll 8
     for (int kk = 0; kk < DR; kk += 4)
-      zacc = __builtin_amdgcn_mfma_f32_16x16x4f32(Us[lane & 15][kk + (lane >> 4)],
-                                                  Wzs[zr][kk + (lane >> 4)], zacc, 0, 0, 0);
+      zacc[(kk >> 2) & 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+          Us[lane & 15][kk + (lane >> 4)], Wzs[zr][kk + (lane >> 4)], zacc[(kk >> 2) & 1], 0, 0, 0);
     if (z < NZ) {
       const float bias = z < 3 * H ? ca[z] : z < 3 * H + E1 ? ce[z - 3 * H] : cb[z - 3 * H - E1];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) Zs[4 * (lane >> 4) + r][z] = zacc[r] + bias;
+      for (int r = 0; r < 4; ++r) Zs[4 * (lane >> 4) + r][z] = (zacc[0][r] + zacc[1][r]) + bias;
     }
   }
   __syncthreads();
-  if (tid < TB && t0 + tid < N) {
-    const int t = t0 + tid;
-    const float *z = Zs[tid];
-    for (int hh = 0; hh < H; ++hh) {
-      const float *za = z + 3 * hh;
-      int best = 0;
-      if (za[1] > za[best]) best = 1;
-      if (za[2] > za[best]) best = 2;
-      mode[int64_t(t) * H + hh] = uint8_t(best);
+  // modes: one thread per (token, head); argmax, first maximum on ties
+  for (int it = tid; it < TB * H; it += 256) {
+    const int tt = it / H, hh = it - tt * H;
+    if (t0 + tt >= N) continue;
+    const float *za = Zs[tt] + 3 * hh;
+    int best = 0;
+    if (za[1] > za[best]) best = 1;
+    if (za[2] > za[best]) best = 2;
+    mode[int64_t(t0 + tt) * H + hh] = uint8_t(best);
+  }
+  // bit width and experts: wave w takes tokens w, w + 4, ...; lane j holds
+  // expert logit j (E + 1 <= 64)
+  for (int tt = wave; tt < TB; tt += 4) {
+    const int t = t0 + tt;
+    if (t >= N) break;  // wave-uniform
+    const float *z = Zs[tt];
+    if (lane == 0) {
+      const float *zb = z + 3 * H + E1;
+      int bb = 0;
+      for (int j = 1; j < 4; ++j)
+        if (zb[j] > zb[bb]) bb = j;
+      bit[t] = uint8_t(bb);
     }
-    const float *zb = z + 3 * H + E1;
-    int bb = 0;
-    for (int j = 1; j < 4; ++j)
-      if (zb[j] > zb[bb]) bb = j;
-    bit[t] = uint8_t(bb);
-    const float *ze = z + 3 * H;
-    // top-k by logit (softmax is monotone); ties go to the lower id
+    // top-k by logit (softmax is monotone), ties to the lower id; the gate
+    // renormalises over the selected set, null included
+    const float zj = lane < E1 ? z[3 * H + lane] : -INFINITY;
+    const float zmax = seg_max(zj, 64);
     uint64_t taken = 0;
-    float zmax = ze[0];
-    for (int j = 1; j < E1; ++j) zmax = fmaxf(zmax, ze[j]);
     float tot = 0.f;
-    for (int s = 0; s < k; ++s) {
-      int best = -1;
-      for (int j = 0; j < E1; ++j) {
-        if (taken >> j & 1) continue;
-        if (best < 0 || ze[j] > ze[best]) best = j;
-      }
+    for (int sl = 0; sl < k; ++sl) {
+      const float cand = (lane < E1 && !(taken >> lane & 1)) ? zj : -INFINITY;
+      const float m = seg_max(cand, 64);
+      const uint64_t hit = __ballot(lane < E1 && !(taken >> lane & 1) && cand == m);
+      const int best = __ffsll((unsigned long long)hit) - 1;
       taken |= 1ull << best;
-      tot += expf(ze[best] - zmax);
+      tot += expf(m - zmax);
     }
-    int s = 0;
-    for (int j = 0; j < E1; ++j) {
-      if (!(taken >> j & 1)) continue;
-      eidx[int64_t(t) * k + s] = j;
-      egate[int64_t(t) * k + s] = expf(ze[j] - zmax) / tot;
-      ++s;
+    if (taken >> lane & 1) {
+      const int sl = __popcll(taken & lanemask_lt());
+      eidx[int64_t(t) * k + sl] = lane;
+      egate[int64_t(t) * k + sl] = expf(zj - zmax) / tot;
     }
+  }
+  __syncthreads();  // Us / Zs are reused by the next tile
   }
 }
 
@@ -326,7 +365,10 @@ hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const fl
     trunk1_kernel<float><<<g2, 256, 0, st>>>((const float *)x, rinv, w.g1, psi, w.W1, u, N, d,
                                              cfg.d_psi, kchunk);
   }
-  router_tail_kernel<<<dim3((N + RT_TB - 1) / RT_TB), 256, RT_LDS, st>>>(
+  // one block per CU at most (the weights fill most of its LDS), each
+  // loading them once and then taking every 256th token tile
+  const int tiles = (N + RT_TB - 1) / RT_TB;
+  router_tail_kernel<<<dim3(tiles < 256 ? tiles : 256), 256, RT_LDS, st>>>(
       u, ks, w.b1, w.W2, w.b2, w.gr, w.Wa, w.ca, w.We, w.ce, w.Wb, w.cb, mode, bit, eidx, egate, N,
       cfg.n_heads, cfg.n_experts + 1, cfg.top_k, cfg.rms_eps);
   return hipGetLastError();

@@ -20,6 +20,14 @@ __device__ __forceinline__ bf16 f2bf(float f) {
   return bf16(u >> 16);
 }
 
+// Two floats -> packed bf16 pair (lo in bits 0..15), round to nearest even
+// (one v_cvt_pk_bf16_f32; the same bits as f2bf for finite values).
+__device__ __forceinline__ uint32_t pk_bf16(float lo, float hi) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
 template <typename T> struct Act;
 template <> struct Act<float> {
   static constexpr int bytes = 4;

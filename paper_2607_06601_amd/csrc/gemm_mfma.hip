@@ -15,6 +15,9 @@
 //   O-proj: xt = x + o Wo^T
 //   MoE-1 : H = silu(n2 Wgate_e^T) * (n2 Wup_e^T) per expert (paper Sec. 3.2 (B))
 //   MoE-2 : Y[a] = H Wdown_e^T, scattered back to assignment a
+#include <algorithm>
+#include <initializer_list>
+
 #include "kernels.hpp"
 
 namespace tr {
@@ -85,13 +88,14 @@ typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 __device__ __forceinline__ u32x4_t pack8_bf16(const float *v) {
   u32x4_t w;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) w[i] = uint32_t(f2bf(v[2 * i])) | (uint32_t(f2bf(v[2 * i + 1])) << 16);
+  for (int i = 0; i < 4; ++i) w[i] = pk_bf16(v[2 * i], v[2 * i + 1]);
   return w;
 }
 
 struct QkvM {
+  static constexpr bool DIRECT_W4 = false;
   static constexpr int EPI = EPI_ROPE;
-  const bf16 *n1, *Wq, *Wk, *Wv;
+  const bf16 *n1, *Wq, *Wk, *Wv, *Wlo;  // Wlo: the lowest of Wq, Wk, Wv
   bf16 *q, *k, *v;
   const int32_t *pos_base, *pos_idx;
   int N, Tq, d, H, Hkv, dh, Ncols;
@@ -111,6 +115,8 @@ struct QkvM {
     const int hd = dh >> 1;
     return (P / hd) * dh + (P % hd) + half * hd;
   }
+  __device__ const bf16 *a_base() const { return n1; }
+  __device__ const bf16 *b_base() const { return Wlo; }
   __device__ const bf16 *a_row(const MTile &t, int r) const { return n1 + int64_t(t.m0 + r) * d; }
   __device__ const bf16 *b_row(const MTile &t, int n) const {
     int P, half;
@@ -178,6 +184,7 @@ struct QkvM {
 };
 
 struct OprojM {
+  static constexpr bool DIRECT_W4 = false;
   static constexpr int EPI = EPI_PLAIN;
   const bf16 *o, *Wo, *x;
   bf16 *xt;
@@ -192,6 +199,8 @@ struct OprojM {
     t.e = t.p0 = 0;
     return t.mvalid > 0;
   }
+  __device__ const bf16 *a_base() const { return o; }
+  __device__ const bf16 *b_base() const { return Wo; }
   __device__ const bf16 *a_row(const MTile &t, int r) const { return o + int64_t(t.m0 + r) * K; }
   __device__ const bf16 *b_row(const MTile &t, int n) const {
     return t.n0 + n < d ? Wo + int64_t(t.n0 + n) * K : nullptr;
@@ -218,7 +227,7 @@ struct OprojM {
 
 struct Moe1M {
   static constexpr int EPI = EPI_SWIGLU;
-  const bf16 *n2, *Wg, *Wu;
+  const bf16 *n2, *Wg, *Wu, *Wlo;  // Wlo: the lower of Wg, Wu
   bf16 *Hm;
   const int32_t *cnt, *off, *rows;
   int E, k, d, dff;
@@ -231,6 +240,8 @@ struct Moe1M {
     return true;
   }
   __device__ int ccol(int P, int) const { return P; }
+  __device__ const bf16 *a_base() const { return n2; }
+  __device__ const bf16 *b_base() const { return Wlo; }
   __device__ const bf16 *a_row(const MTile &t, int r) const {
     return n2 + int64_t(rows[t.p0 + r] / k) * d;
   }
@@ -240,6 +251,46 @@ struct Moe1M {
     const int f = t.n0 + P;
     if (f >= dff) return nullptr;
     return (half ? Wu : Wg) + (int64_t(t.e - 1) * dff + f) * d;
+  }
+  // Four-wave kernel (256 x 256 tile, wave tiles 128 x 128): physical column
+  // n = 128 wn + 16 ni + c of the tile (wave column wn, MFMA block ni, lane
+  // column c) holds expert unit 64 wn + 4 c + ni / 2 of the tile, gate for
+  // even ni and up for odd, so each lane ends with both halves of 4
+  // consecutive units and writes them as one 8-byte piece per row.
+  static constexpr bool DIRECT_W4 = true;
+  __device__ const bf16 *b_row_w4(const MTile &t, int n) const {
+    const int wn = n >> 7, ni = (n >> 4) & 7, c = n & 15;
+    const int f = t.n0 + wn * 64 + c * 4 + (ni >> 1);
+    if (f >= dff) return nullptr;
+    return ((ni & 1) ? Wu : Wg) + (int64_t(t.e - 1) * dff + f) * d;
+  }
+  template <int MI, int NI>
+  __device__ void store_w4(const MTile &t, const f32x4_t (&acc)[MI][NI], int wm, int wn, int lane) const {
+    static_assert(NI == 8, "wave tiles 128 columns wide");
+    const int f = t.n0 + wn * 64 + (lane & 15) * 4;
+    if (f >= dff) return;  // d_ff is a multiple of 4: a lane's units are all in or all out
+    // SwiGLU of every value first (independent chains for the VALU to
+    // overlap), then the stores of the valid rows
+    uint32_t w[MI][4][2];
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const float g0 = acc[mi][4 * u][i], u0 = acc[mi][4 * u + 1][i];
+          const float g1 = acc[mi][4 * u + 2][i], u1 = acc[mi][4 * u + 3][i];
+          w[mi][i][u] = pk_bf16(g0 * __builtin_amdgcn_rcpf(1.0f + __expf(-g0)) * u0,
+                                g1 * __builtin_amdgcn_rcpf(1.0f + __expf(-g1)) * u1);
+        }
+    bf16 *out = Hm + int64_t(t.p0) * dff + f;
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = wm * MI * 16 + mi * 16 + 4 * (lane >> 4) + i;
+        if (r < t.mvalid) *(uint2 *)(out + r * dff) = make_uint2(w[mi][i][0], w[mi][i][1]);
+      }
   }
   // item = 8 expert units of one assignment row (C holds silu(g) u)
   template <int BM, int NC, int LDC, int NT>
@@ -254,6 +305,7 @@ struct Moe1M {
 };
 
 struct Moe2M {
+  static constexpr bool DIRECT_W4 = false;
   static constexpr int EPI = EPI_PLAIN;
   const bf16 *Hm, *Wd;
   float *Y;
@@ -267,6 +319,8 @@ struct Moe2M {
     t.n0 = by * BN;
     return true;
   }
+  __device__ const bf16 *a_base() const { return Hm; }
+  __device__ const bf16 *b_base() const { return Wd; }
   __device__ const bf16 *a_row(const MTile &t, int r) const { return Hm + int64_t(t.p0 + r) * dff; }
   __device__ const bf16 *b_row(const MTile &t, int n) const {
     return t.n0 + n < d ? Wd + (int64_t(t.e - 1) * d + t.n0 + n) * dff : nullptr;
@@ -317,6 +371,40 @@ __device__ __forceinline__ void wait_stages(int n) {
   if constexpr (S > 3) if (n == 2) { wait_vm<2 * N>(); return; }
   if constexpr (S > 2) if (n == 1) { wait_vm<N>(); return; }
   wait_vm<0>();
+}
+
+// Epilogue register pass: lane holds rows 4 (lane/16) + i of each 16-row tile
+// and column (lane % 16) of each 16-column block; in each 64-column slice the
+// partner columns (ni, ni + 2) are combined for SwiGLU and kept apart for
+// RoPE.  The problem's row-wise pass then reads the staged fp32 tile C.
+template <class P, int MI, int NI, int TM, int TN, int LDC>
+__device__ __forceinline__ void store_acc(const P &p, float *C, const f32x4_t (&acc)[MI][NI],
+                                          int wm, int wn, int lane) {
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = wm * TM + mi * 16 + 4 * (lane >> 4) + i;
+      if constexpr (P::EPI == EPI_PLAIN) {
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+          C[r * LDC + wn * TN + ni * 16 + (lane & 15)] = acc[mi][ni][i];
+      } else {
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) {
+          if ((ni & 3) >= 2) continue;
+          int Pp, half;
+          col_pair(wn * TN + ni * 16 + (lane & 15), Pp, half);
+          const float g = acc[mi][ni][i], u = acc[mi][ni + 2][i];
+          if constexpr (P::EPI == EPI_SWIGLU) {
+            C[r * LDC + Pp] = g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
+          } else {
+            C[r * LDC + p.ccol(Pp, 0)] = g;
+            C[r * LDC + p.ccol(Pp, 1)] = u;
+          }
+        }
+      }
+    }
 }
 
 template <class P, int BM, int BN, int WM, int WN, int BK, int S>
@@ -404,39 +492,174 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_mfma_kernel(P p, int K, 
       }
     }
   }
-  // Epilogue.  Register pass: lane holds rows 4 (lane/16) + i of each 16-row
-  // tile and column (lane % 16) of each 16-column block; in each 64-column
-  // slice the partner columns (ni, ni + 2) are combined for SwiGLU and kept
-  // apart for RoPE.  Then the problem's row-wise pass reads the staged tile.
   __syncthreads();  // every wave is done with the operand stages
   float *C = (float *)smem;
-#pragma unroll
-  for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = wm * TM + mi * 16 + 4 * (lane >> 4) + i;
-      if constexpr (P::EPI == EPI_PLAIN) {
-#pragma unroll
-        for (int ni = 0; ni < NI; ++ni)
-          C[r * LDC + wn * TN + ni * 16 + (lane & 15)] = acc[mi][ni][i];
-      } else {
-#pragma unroll
-        for (int ni = 0; ni < NI; ++ni) {
-          if ((ni & 3) >= 2) continue;
-          int Pp, half;
-          col_pair(wn * TN + ni * 16 + (lane & 15), Pp, half);
-          const float g = acc[mi][ni][i], u = acc[mi][ni + 2][i];
-          if constexpr (P::EPI == EPI_SWIGLU) {
-            C[r * LDC + Pp] = g / (1.0f + expf(-g)) * u;
-          } else {
-            C[r * LDC + p.ccol(Pp, 0)] = g;
-            C[r * LDC + p.ccol(Pp, 1)] = u;
-          }
-        }
-      }
-    }
+  store_acc<P, MI, NI, TM, TN, LDC>(p, C, acc, wm, wn, lane);
   __syncthreads();
   p.template epilogue<BM, NC, LDC, NT>(tc, C, tid);
+}
+
+// ------------------------------------------------------- four-wave kernel
+// One wave per SIMD, each wave a (BM/2) x (BN/2) sub-tile: every operand byte
+// read from LDS feeds twice the MFMAs of the eight-wave kernel above (per K
+// step and CU, 128 KB of fragment reads against 256 MFMAs per SIMD).  With
+// no second wave on its SIMD to switch to, a wave hides LDS latency itself:
+// the fragments of the next 32-wide K slice are read into a second register
+// set while the current slice's MFMAs issue, the reads slotted between the
+// first MFMAs.  Stages are double-buffered (BK = 64): stage kt + 2 is issued
+// into the buffer of stage kt right after the barrier that also publishes
+// stage kt + 1, half-way through step kt.
+// acc += a b on the accumulator registers (AGPRs).  With 256 accumulators
+// per lane the register allocator, left to itself, parks some of them in
+// VGPRs and copies them around every MFMA; pinning them to AGPRs keeps the
+// loop free of copies.  As a volatile asm statement it also keeps its place
+// relative to the LDS reads and transfers written around it, so the program
+// order below is the issue order.
+__device__ __forceinline__ void mfma_agpr(f32x4_t &acc, const bf16x8_t &a, const bf16x8_t &b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+
+template <class P, int BM, int BN>
+__global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
+  constexpr int NW = 4, NT = 256, WN = 2;
+  constexpr int TM = BM / 2, TN = BN / 2;    // wave tile
+  constexpr int MI = TM / 16, NI = TN / 16;  // 16 x 16 MFMA tiles per wave
+  constexpr int BK = 64, RB = 128, CPR = 8, RPT = 8;
+  constexpr int STAGE = (BM + BN) * RB;
+  constexpr int IPW = STAGE / 1024 / NW;  // 1 KB transfers per wave per stage
+  constexpr int NF = MI + NI;             // fragment reads per K slice
+  constexpr int NM = MI * NI;             // MFMAs per K slice
+  static_assert(STAGE % (1024 * NW) == 0 && TN % 64 == 0, "whole transfers, 64-column slices");
+  constexpr int DMA_GAP = 3;
+  static_assert(NM >= 32 + NF && NM >= 16 + DMA_GAP * (IPW - 1) + 1, "room for the reads and transfers");
+  constexpr int NC = P::out_cols(BN), LDC = NC + 16;
+  constexpr int SMEM = 2 * STAGE > BM * LDC * 4 ? 2 * STAGE : BM * LDC * 4;
+  __shared__ __align__(1024) uint8_t smem[SMEM];
+  GroupScan gs;
+  if constexpr (P::GROUPED) gs = group_scan(BM, p.cnt, p.E);
+  const int total = p.tiles(BM, ny, gs);
+  if (int(blockIdx.x) >= total) return;
+  const int t = xcd_tile(blockIdx.x, total);
+  MTile tc;
+  if (!p.map(t / ny, t % ny, BM, BN, tc, gs)) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, in SGPRs
+  const int wm = wave / WN, wn = wave % WN;
+  // Transfer j of this wave fills stage rows RPT (wave IPW + j) .. + RPT - 1
+  // as in the eight-wave kernel; a wave's transfers are all A rows or all B
+  // rows (IPW RPT divides BM), so each lane keeps one 32-bit byte offset per
+  // transfer from the operand's base (the host checks that every operand row
+  // lies within 4 GB of it), and the base moves on by 128 B per K step.
+  static_assert(BM % (IPW * RPT) == 0, "a wave's transfers stay within one operand");
+  const bool wave_a = wave * IPW * RPT < BM;
+  const uint8_t *gbase = (const uint8_t *)(wave_a ? p.a_base() : p.b_base());
+  uint32_t voff[IPW];
+  if (wave_a) {
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      const int rr = RPT * (wave * IPW + j) + lane / CPR;
+      const bf16 *row = p.a_row(tc, rr < tc.mvalid ? rr : 0);
+      voff[j] = uint32_t((const uint8_t *)row - gbase) + swz<CPR>(rr, lane % CPR) * 16;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      const int rr = RPT * (wave * IPW + j) + lane / CPR;
+      const bf16 *row;
+      if constexpr (P::DIRECT_W4)
+        row = p.b_row_w4(tc, rr - BM);
+      else
+        row = p.b_row(tc, rr - BM);
+      if (!row) row = p.b_base();
+      voff[j] = uint32_t((const uint8_t *)row - gbase) + swz<CPR>(rr, lane % CPR) * 16;
+    }
+  }
+  const uint32_t sbase = lds_addr(smem) + wave * IPW * 1024;
+  // Fragment addresses: row r = (wave row) + 16 i + lane % 16 reads chunk
+  // (4 ks + lane / 16) ^ ((r >> 1) & 7); the XOR term depends on the lane only.
+  const int l15 = lane & 15, x7 = (lane >> 1) & 7;
+  const uint8_t *fa0 = smem + (wm * TM + l15) * RB;
+  const uint8_t *fb0 = smem + BM * RB + (wn * TN + l15) * RB;
+  int coff[2];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) coff[ks] = (((ks * 4 + (lane >> 4)) ^ x7) << 4);
+
+  bf16x8_t fa[2][MI], fb[2][NI];
+  // piece q of slice ks in buffer buf: q = 0 is A0, 1..NI the B pieces, then A1..
+  auto read_piece = [&](int set, int buf, int q) {
+    if (q == 0) {
+      fa[set][0] = *(const bf16x8_t *)(fa0 + buf * STAGE + coff[set]);
+    } else if (q <= NI) {
+      fb[set][q - 1] = *(const bf16x8_t *)(fb0 + buf * STAGE + (q - 1) * 16 * RB + coff[set]);
+    } else {
+      const int mi = q - NI;
+      fa[set][mi] = *(const bf16x8_t *)(fa0 + buf * STAGE + mi * 16 * RB + coff[set]);
+    }
+  };
+  f32x4_t acc[MI][NI];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NI; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  auto mma = [&](int set, int j) {
+    mfma_agpr(acc[j / NI][j % NI], fa[set][j / NI], fb[set][j % NI]);
+  };
+
+  const int nk = K / BK;
+#pragma unroll
+  for (int j = 0; j < IPW; ++j) dma16_s(gbase, voff[j], sbase + j * 1024);
+  if (nk > 1) {
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) dma16_s(gbase + RB, voff[j], sbase + STAGE + j * 1024);
+    wait_vm<IPW>();
+  } else {
+    wait_vm<0>();
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < NF; ++q) read_piece(0, 0, q);
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    // slice 0 of stage kt: MFMAs on set 0, with the reads of slice 1 into
+    // set 1 after the first NF of them
+#pragma unroll
+    for (int j = 0; j < NM; ++j) {
+      mma(0, j);
+      if (j < NF) read_piece(1, buf, j);
+    }
+    // slice 1: sixteen MFMAs cover the barrier after which buffer buf is free
+    // (every wave has its set-1 reads in) and stage kt + 1 is published
+#pragma unroll
+    for (int j = 0; j < 16; ++j) mma(1, j);
+    wait_vm<0>();
+    __syncthreads();
+    // Stage kt + 2 into buffer buf, one transfer every DMA_GAP MFMAs (bunched
+    // together the CU's transfers queue at its address unit and stall the
+    // issuing waves), and from MFMA 32 on the reads of stage kt + 1, slice 0,
+    // into set 0.  Near the end the last stage is fetched again and the reads
+    // land unused, which keeps the loop free of branches.
+    const int kn = min(kt + 2, nk - 1);
+#pragma unroll
+    for (int j = 16; j < NM; ++j) {
+      mma(1, j);
+      if ((j - 16) % DMA_GAP == 0 && (j - 16) / DMA_GAP < IPW)
+        dma16_s(gbase + kn * RB, voff[(j - 16) / DMA_GAP], sbase + buf * STAGE + (j - 16) / DMA_GAP * 1024);
+      if (j >= 32 && j - 32 < NF) read_piece(0, buf ^ 1, j - 32);
+    }
+  }
+  // the last MFMAs' results are read below: let them drain first
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+  wait_vm<0>();
+  if constexpr (P::DIRECT_W4) {
+    p.store_w4(tc, acc, wm, wn, lane);
+  } else {
+    __syncthreads();  // every wave is done with the operand stages
+    float *C = (float *)smem;
+    store_acc<P, MI, NI, TM, TN, LDC>(p, C, acc, wm, wn, lane);
+    __syncthreads();
+    p.template epilogue<BM, NC, LDC, NT>(tc, C, tid);
+  }
 }
 
 // ------------------------------------------------------------------ launchers
@@ -450,6 +673,30 @@ static hipError_t launch(const P &p, int K, int m_tiles, int n_tiles, hipStream_
   return hipGetLastError();
 }
 
+template <class P, int BM, int BN>
+static hipError_t launch_w4(const P &p, int K, int m_tiles, int n_tiles, hipStream_t st) {
+  if (m_tiles > 0 && n_tiles > 0)
+    gemm_w4_kernel<P, BM, BN><<<m_tiles * n_tiles, 256, 0, st>>>(p, K, n_tiles);
+  return hipGetLastError();
+}
+
+// The four-wave kernel addresses operand rows by 32-bit byte offsets from the
+// lowest of an operand's matrices: *lo gets that pointer, and the result says
+// whether every matrix ends within 4 GB of it.
+struct Span {
+  const void *p;
+  size_t bytes;
+};
+static bool span32(std::initializer_list<Span> ms, const bf16 **lo) {
+  uintptr_t a = UINTPTR_MAX, b = 0;
+  for (const Span &m : ms) {
+    a = std::min(a, uintptr_t(m.p));
+    b = std::max(b, uintptr_t(m.p) + m.bytes);
+  }
+  *lo = (const bf16 *)a;
+  return b - a < (uintptr_t(1) << 32);
+}
+
 hipError_t mfma_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
                     const triroute_dense_w &w, const int32_t *pos_base, const int32_t *pos_idx,
                     void *q, void *k, void *v, hipStream_t st) {
@@ -458,6 +705,7 @@ hipError_t mfma_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
   p.Wq = (const bf16 *)w.Wq;
   p.Wk = (const bf16 *)w.Wk;
   p.Wv = (const bf16 *)w.Wv;
+  p.Wlo = std::min(p.Wq, std::min(p.Wk, p.Wv));
   p.q = (bf16 *)q;
   p.k = (bf16 *)k;
   p.v = (bf16 *)v;
@@ -506,7 +754,12 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
   p1.k = k;
   p1.d = d;
   p1.dff = dff;
-  hipError_t err = launch<Moe1M, 256, 256, 2, 4, 64, 2>(p1, d, Nk / 256 + E, (dff + 127) / 128, st);
+  const size_t wb = size_t(E) * dff * d * sizeof(bf16);
+  const bf16 *alo;
+  const bool w4 = span32({{p1.Wg, wb}, {p1.Wu, wb}}, &p1.Wlo) &&
+                  span32({{p1.n2, size_t(N) * d * sizeof(bf16)}}, &alo);
+  hipError_t err = w4 ? launch_w4<Moe1M, 256, 256>(p1, d, Nk / 256 + E, (dff + 127) / 128, st)
+                      : launch<Moe1M, 256, 256, 2, 4, 64, 2>(p1, d, Nk / 256 + E, (dff + 127) / 128, st);
   if (err != hipSuccess) return err;
   Moe2M p2;
   p2.Hm = (const bf16 *)Hm;

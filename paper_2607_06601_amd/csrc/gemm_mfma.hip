@@ -252,22 +252,21 @@ struct Moe1M {
     if (f >= dff) return nullptr;
     return (half ? Wu : Wg) + (int64_t(t.e - 1) * dff + f) * d;
   }
-  // Four-wave kernel (256 x 256 tile, wave tiles 128 x 128): physical column
-  // n = 128 wn + 16 ni + c of the tile (wave column wn, MFMA block ni, lane
-  // column c) holds expert unit 64 wn + 4 c + ni / 2 of the tile, gate for
-  // even ni and up for odd, so each lane ends with both halves of 4
-  // consecutive units and writes them as one 8-byte piece per row.
+  // Four-wave kernel: in wave column wn, MFMA block ni, lane column c
+  // holds expert unit (NI / 2) (16 wn + c) + ni / 2 of the tile, gate for
+  // even ni and up for odd, so each lane ends with both halves of NI / 2
+  // consecutive units and writes them as one piece per row.
   static constexpr bool DIRECT_W4 = true;
-  __device__ const bf16 *b_row_w4(const MTile &t, int n) const {
-    const int wn = n >> 7, ni = (n >> 4) & 7, c = n & 15;
-    const int f = t.n0 + wn * 64 + c * 4 + (ni >> 1);
+  template <int NI>
+  __device__ const bf16 *b_row_w4(const MTile &t, int wn, int ni, int c) const {
+    const int f = t.n0 + (NI / 2) * (16 * wn + c) + (ni >> 1);
     if (f >= dff) return nullptr;
     return ((ni & 1) ? Wu : Wg) + (int64_t(t.e - 1) * dff + f) * d;
   }
   template <int MI, int NI>
   __device__ void store_w4(const MTile &t, const f32x4_t (&acc)[MI][NI], int wm, int wn, int lane) const {
-    static_assert(NI == 8, "wave tiles 128 columns wide");
-    const int f = t.n0 + wn * 64 + (lane & 15) * 4;
+    static_assert(NI == 8, "4 units per lane, one 8-byte piece per row");
+    const int f = t.n0 + (NI / 2) * (16 * wn + (lane & 15));
     if (f >= dff) return;  // d_ff is a multiple of 4: a lane's units are all in or all out
     // SwiGLU of every value first (independent chains for the VALU to
     // overlap), then the stores of the valid rows
@@ -305,7 +304,7 @@ struct Moe1M {
 };
 
 struct Moe2M {
-  static constexpr bool DIRECT_W4 = false;
+  static constexpr bool DIRECT_W4 = true;
   static constexpr int EPI = EPI_PLAIN;
   const bf16 *Hm, *Wd;
   float *Y;
@@ -324,6 +323,37 @@ struct Moe2M {
   __device__ const bf16 *a_row(const MTile &t, int r) const { return Hm + int64_t(t.p0 + r) * dff; }
   __device__ const bf16 *b_row(const MTile &t, int n) const {
     return t.n0 + n < d ? Wd + (int64_t(t.e - 1) * d + t.n0 + n) * dff : nullptr;
+  }
+  // Four-wave kernel: in wave column wn, MFMA block ni, lane column c
+  // holds output feature NI (16 wn + c) + ni of the tile, so each lane ends
+  // with NI consecutive features of each of its rows.
+  template <int NI>
+  __device__ const bf16 *b_row_w4(const MTile &t, int wn, int ni, int c) const {
+    const int f = t.n0 + NI * (16 * wn + c) + ni;
+    return f < d ? Wd + (int64_t(t.e - 1) * d + f) * dff : nullptr;
+  }
+  template <int MI, int NI>
+  __device__ void store_w4(const MTile &t, const f32x4_t (&acc)[MI][NI], int wm, int wn, int lane) const {
+    static_assert(NI % 2 == 0, "whole 8-byte pieces");
+    const int f = t.n0 + NI * (16 * wn + (lane & 15));
+    if (f >= d) return;  // d is a multiple of NI: a lane's features are all in or all out
+    int slot[MI][4];  // destination rows first, so their loads overlap
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = wm * MI * 16 + mi * 16 + 4 * (lane >> 4) + i;
+        slot[mi][i] = r < t.mvalid ? rows[t.p0 + r] : -1;
+      }
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (slot[mi][i] < 0) continue;
+        float *y = Y + int64_t(slot[mi][i]) * d + f;
+#pragma unroll
+        for (int ni = 0; ni < NI; ni += 2) *(float2 *)(y + ni) = make_float2(acc[mi][ni][i], acc[mi][ni + 1][i]);
+      }
   }
   // item = 8 output features of one assignment, scattered to its slot row
   template <int BM, int NC, int LDC, int NT>
@@ -529,11 +559,14 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
   constexpr int IPW = STAGE / 1024 / NW;  // 1 KB transfers per wave per stage
   constexpr int NF = MI + NI;             // fragment reads per K slice
   constexpr int NM = MI * NI;             // MFMAs per K slice
-  static_assert(STAGE % (1024 * NW) == 0 && TN % 64 == 0, "whole transfers, 64-column slices");
-  constexpr int DMA_GAP = 3;
-  static_assert(NM >= 32 + NF && NM >= 16 + DMA_GAP * (IPW - 1) + 1, "room for the reads and transfers");
+  static_assert(STAGE % (1024 * NW) == 0 && (TN % 64 == 0 || P::DIRECT_W4), "whole transfers, 64-column slices");
+  // slice 1 schedule: 16 MFMAs, the barrier, then a transfer every DMA_GAP
+  // MFMAs and the next slice's reads from MFMA RS on
+  constexpr int DMA_GAP = (NM - 17) / (IPW - 1) < 3 ? (NM - 17) / (IPW - 1) : 3;
+  constexpr int RS = NM - NF < 32 ? NM - NF : 32;
+  static_assert(DMA_GAP >= 1 && RS >= 16, "room for the reads and transfers");
   constexpr int NC = P::out_cols(BN), LDC = NC + 16;
-  constexpr int SMEM = 2 * STAGE > BM * LDC * 4 ? 2 * STAGE : BM * LDC * 4;
+  constexpr int SMEM = P::DIRECT_W4 || 2 * STAGE > BM * LDC * 4 ? 2 * STAGE : BM * LDC * 4;
   __shared__ __align__(1024) uint8_t smem[SMEM];
   GroupScan gs;
   if constexpr (P::GROUPED) gs = group_scan(BM, p.cnt, p.E);
@@ -546,33 +579,28 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, in SGPRs
   const int wm = wave / WN, wn = wave % WN;
   // Transfer j of this wave fills stage rows RPT (wave IPW + j) .. + RPT - 1
-  // as in the eight-wave kernel; a wave's transfers are all A rows or all B
-  // rows (IPW RPT divides BM), so each lane keeps one 32-bit byte offset per
-  // transfer from the operand's base (the host checks that every operand row
-  // lies within 4 GB of it), and the base moves on by 128 B per K step.
-  static_assert(BM % (IPW * RPT) == 0, "a wave's transfers stay within one operand");
-  const bool wave_a = wave * IPW * RPT < BM;
-  const uint8_t *gbase = (const uint8_t *)(wave_a ? p.a_base() : p.b_base());
+  // as in the eight-wave kernel.  A transfer's rows are all A rows or all B
+  // rows (RPT divides BM), so each lane keeps one 32-bit byte offset per
+  // transfer from that operand's base (the host checks that every operand
+  // row lies within 4 GB of it); the base moves on by 128 B per K step.
+  static_assert(BM % RPT == 0, "a transfer stays within one operand");
+  auto is_a = [&](int j) { return RPT * (wave * IPW + j) < BM; };  // wave-uniform
+  auto gbase = [&](int j) { return (const uint8_t *)(is_a(j) ? p.a_base() : p.b_base()); };
   uint32_t voff[IPW];
-  if (wave_a) {
 #pragma unroll
-    for (int j = 0; j < IPW; ++j) {
-      const int rr = RPT * (wave * IPW + j) + lane / CPR;
-      const bf16 *row = p.a_row(tc, rr < tc.mvalid ? rr : 0);
-      voff[j] = uint32_t((const uint8_t *)row - gbase) + swz<CPR>(rr, lane % CPR) * 16;
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < IPW; ++j) {
-      const int rr = RPT * (wave * IPW + j) + lane / CPR;
-      const bf16 *row;
+  for (int j = 0; j < IPW; ++j) {
+    const int rr = RPT * (wave * IPW + j) + lane / CPR;
+    const bf16 *row;
+    if (is_a(j)) {
+      row = p.a_row(tc, rr < tc.mvalid ? rr : 0);
+    } else {
       if constexpr (P::DIRECT_W4)
-        row = p.b_row_w4(tc, rr - BM);
+        row = p.template b_row_w4<NI>(tc, (rr - BM) / TN, ((rr - BM) % TN) >> 4, (rr - BM) & 15);
       else
         row = p.b_row(tc, rr - BM);
       if (!row) row = p.b_base();
-      voff[j] = uint32_t((const uint8_t *)row - gbase) + swz<CPR>(rr, lane % CPR) * 16;
     }
+    voff[j] = uint32_t((const uint8_t *)row - gbase(j)) + swz<CPR>(rr, lane % CPR) * 16;
   }
   const uint32_t sbase = lds_addr(smem) + wave * IPW * 1024;
   // Fragment addresses: row r = (wave row) + 16 i + lane % 16 reads chunk
@@ -607,10 +635,10 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
 
   const int nk = K / BK;
 #pragma unroll
-  for (int j = 0; j < IPW; ++j) dma16_s(gbase, voff[j], sbase + j * 1024);
+  for (int j = 0; j < IPW; ++j) dma16_s(gbase(j), voff[j], sbase + j * 1024);
   if (nk > 1) {
 #pragma unroll
-    for (int j = 0; j < IPW; ++j) dma16_s(gbase + RB, voff[j], sbase + STAGE + j * 1024);
+    for (int j = 0; j < IPW; ++j) dma16_s(gbase(j) + RB, voff[j], sbase + STAGE + j * 1024);
     wait_vm<IPW>();
   } else {
     wait_vm<0>();
@@ -636,7 +664,7 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
     __syncthreads();
     // Stage kt + 2 into buffer buf, one transfer every DMA_GAP MFMAs (bunched
     // together the CU's transfers queue at its address unit and stall the
-    // issuing waves), and from MFMA 32 on the reads of stage kt + 1, slice 0,
+    // issuing waves), and from MFMA RS on the reads of stage kt + 1, slice 0,
     // into set 0.  Near the end the last stage is fetched again and the reads
     // land unused, which keeps the loop free of branches.
     const int kn = min(kt + 2, nk - 1);
@@ -644,8 +672,9 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
     for (int j = 16; j < NM; ++j) {
       mma(1, j);
       if ((j - 16) % DMA_GAP == 0 && (j - 16) / DMA_GAP < IPW)
-        dma16_s(gbase + kn * RB, voff[(j - 16) / DMA_GAP], sbase + buf * STAGE + (j - 16) / DMA_GAP * 1024);
-      if (j >= 32 && j - 32 < NF) read_piece(0, buf ^ 1, j - 32);
+        dma16_s(gbase((j - 16) / DMA_GAP) + kn * RB, voff[(j - 16) / DMA_GAP],
+                sbase + buf * STAGE + (j - 16) / DMA_GAP * 1024);
+      if (j >= RS && j - RS < NF) read_piece(0, buf ^ 1, j - RS);
     }
   }
   // the last MFMAs' results are read below: let them drain first
@@ -771,7 +800,10 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
   p2.E = E;
   p2.d = d;
   p2.dff = dff;
-  return launch<Moe2M, 256, 128, 4, 2, 64, 3>(p2, dff, Nk / 256 + E, (d + 127) / 128, st);
+  const bool w4b = dff >= 128 && d % 192 == 0 && span32({{p2.Wd, wb}}, &alo) &&
+                   span32({{p2.Hm, size_t(Nk) * dff * sizeof(bf16)}}, &alo);
+  return w4b ? launch_w4<Moe2M, 256, 192>(p2, dff, Nk / 256 + E, d / 192, st)
+             : launch<Moe2M, 256, 128, 4, 2, 64, 3>(p2, dff, Nk / 256 + E, (d + 127) / 128, st);
 }
 
 }  // namespace tr

@@ -92,15 +92,18 @@ __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int
                                                        const int32_t *__restrict__ slots,
                                                        uint8_t *__restrict__ vstage) {
   __shared__ uint32_t kw[4][128];  // per wave: the token's K words (at most 4 dh bits... / 32)
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  // the wave index, and all that follows from it, in scalar registers: the
+  // per-(token, head) bookkeeping (divisions, addresses) runs on the scalar
+  // unit and the branches on the width are scalar branches
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int item = blockIdx.x * 4 + w;
   const int Hkv = cv.Hkv, dh = cv.dh, G = cv.G;
   const int i = item / Hkv, g = item % Hkv;
-  const int slot = item < N * Hkv ? slots[i] : -1;
+  const int slot = item < N * Hkv ? __builtin_amdgcn_readfirstlane(slots[i]) : -1;
   if (slot < 0) return;  // wave-uniform: nothing of this wave touches LDS or a barrier
   const int b = i / T_;
-  const int s = seq_ids ? seq_ids[b] : b;
-  const int bi = int(bit[i]);
+  const int s = seq_ids ? __builtin_amdgcn_readfirstlane(seq_ids[b]) : b;
+  const int bi = __builtin_amdgcn_readfirstlane(int(bit[i]));
   const int bp = cv.bits(bi);
   const int tile = slot / cv.TS, st = slot % cv.TS;
   uint8_t *tp = cv.tile(s, bi, g, tile);
@@ -200,7 +203,7 @@ __global__ __launch_bounds__(256) void kv_vpack_kernel(CacheView cv, int B, int 
                                                        const int32_t *__restrict__ old_len,
                                                        const uint8_t *__restrict__ vstage) {
   const int lane = threadIdx.x & 63;
-  int u = blockIdx.x * 4 + (threadIdx.x >> 6);
+  int u = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // scalar bookkeeping
   const int j = u % JS;
   u /= JS;
   const int g = u % cv.Hkv;

@@ -1166,12 +1166,14 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_mfma_kernel(PrefillArgs a
   const CacheView &cv = a.cv;
   const int lane = threadIdx.x & 63, n16 = lane & 15, o4 = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  // heavy blocks first: full mode, latest query tiles first
-  const int per_mode = a.B * a.Hkv * a.NQ * a.QT;
+  // heavy blocks first: full mode, and within a mode the query tiles from
+  // the latest down, each across all (sequence, kv head, quartet), so that
+  // blocks start in decreasing order of their key range
+  const int per_qt = a.B * a.Hkv * a.NQ, per_mode = per_qt * a.QT;
   const int m = int(blockIdx.x) < per_mode ? TRIROUTE_FULL : TRIROUTE_LOCAL;
   int r = int(blockIdx.x) % per_mode;
-  const int qt = a.QT - 1 - r % a.QT;
-  r /= a.QT;
+  const int qt = a.QT - 1 - r / per_qt;
+  r %= per_qt;
   const int quart = r % a.NQ;
   r /= a.NQ;
   const int g = r % a.Hkv, b = r / a.Hkv;

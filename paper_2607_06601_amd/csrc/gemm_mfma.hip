@@ -536,9 +536,8 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_mfma_kernel(P p, int K, 
 // no second wave on its SIMD to switch to, a wave hides LDS latency itself:
 // the fragments of the next 32-wide K slice are read into a second register
 // set while the current slice's MFMAs issue, the reads slotted between the
-// first MFMAs.  Stages are double-buffered (BK = 64): stage kt + 2 is issued
-// into the buffer of stage kt right after the barrier that also publishes
-// stage kt + 1, half-way through step kt.
+// MFMAs.  Stages are double-buffered (BK = 64); stage kt + 2 goes into the
+// buffer of stage kt as soon as every wave has read it (schedule below).
 // acc += a b on the accumulator registers (AGPRs).  With 256 accumulators
 // per lane the register allocator, left to itself, parks some of them in
 // VGPRs and copies them around every MFMA; pinning them to AGPRs keeps the
@@ -562,9 +561,22 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
   static_assert(STAGE % (1024 * NW) == 0 && (TN % 64 == 0 || P::DIRECT_W4), "whole transfers, 64-column slices");
   // slice 1 schedule: 16 MFMAs, the barrier, then a transfer every DMA_GAP
   // MFMAs and the next slice's reads from MFMA RS on
-  constexpr int DMA_GAP = (NM - 17) / (IPW - 1) < 3 ? (NM - 17) / (IPW - 1) : 3;
+  // K step schedule.  Long steps (NM = 64: 128 MFMAs per wave) take one
+  // barrier, 16 MFMAs into slice 1: it frees the buffer of stage kt and
+  // publishes stage kt + 1; the transfers of stage kt + 2 follow one every
+  // GAP1 MFMAs.  Shorter steps cannot cover the transfer latency that way
+  // and take two: the first, after MFMA B1J of slice 0 (its reads of set 1
+  // are in), frees the buffer; the transfers go out one every GAP MFMAs
+  // until MFMA RS of slice 1, where the second barrier publishes stage
+  // kt + 1 (at most this step's IPW transfers still out) for the reads of
+  // set 0, so stage kt + 2 has from slice 0 of step kt to slice 1 of kt + 1.
+  constexpr bool TWO = NM < 64;
   constexpr int RS = NM - NF < 32 ? NM - NF : 32;
-  static_assert(DMA_GAP >= 1 && RS >= 16, "room for the reads and transfers");
+  constexpr int GAP1 = (NM - 17) / (IPW - 1) < 3 ? (NM - 17) / (IPW - 1) : 3;
+  constexpr int B1J = NF + 4;
+  constexpr int NSLOT = (NM - 1 - B1J) + RS;  // slice 0 after B1J, then slice 1 before RS
+  constexpr int GAP = NSLOT / IPW < 4 ? NSLOT / IPW : 4;
+  static_assert(B1J < NM && RS >= 16 && (TWO ? GAP >= 1 : GAP1 >= 1), "room for the reads and transfers");
   constexpr int NC = P::out_cols(BN), LDC = NC + 16;
   constexpr int SMEM = P::DIRECT_W4 || 2 * STAGE > BM * LDC * 4 ? 2 * STAGE : BM * LDC * 4;
   __shared__ __align__(1024) uint8_t smem[SMEM];
@@ -649,31 +661,46 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
 
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    // slice 0 of stage kt: MFMAs on set 0, with the reads of slice 1 into
-    // set 1 after the first NF of them
+    // stage kt + 2 (near the end the last stage again, unused: no branch)
+    const int kn = min(kt + 2, nk - 1);
+    auto dma_slot = [&](int pos) {  // transfer pos / GAP at slot pos
+      if (pos >= 0 && pos % GAP == 0 && pos / GAP < IPW) {
+        const int j = pos / GAP;
+        dma16_s(gbase(j) + kn * RB, voff[j], sbase + buf * STAGE + j * 1024);
+      }
+    };
+    // slice 0: MFMAs on set 0, the reads of slice 1 into set 1 after the
+    // first NF of them (TWO: the first barrier after MFMA B1J)
 #pragma unroll
     for (int j = 0; j < NM; ++j) {
       mma(0, j);
       if (j < NF) read_piece(1, buf, j);
+      if constexpr (TWO) {
+        if (j == B1J) __syncthreads();  // every wave's reads of stage kt are in
+        if (j > B1J) dma_slot(j - B1J - 1);
+      }
     }
-    // slice 1: sixteen MFMAs cover the barrier after which buffer buf is free
-    // (every wave has its set-1 reads in) and stage kt + 1 is published
+    // slice 1: MFMAs on set 1, the barrier, then the reads of stage kt + 1,
+    // slice 0, into set 0 (unused in the last step)
 #pragma unroll
-    for (int j = 0; j < 16; ++j) mma(1, j);
-    wait_vm<0>();
-    __syncthreads();
-    // Stage kt + 2 into buffer buf, one transfer every DMA_GAP MFMAs (bunched
-    // together the CU's transfers queue at its address unit and stall the
-    // issuing waves), and from MFMA RS on the reads of stage kt + 1, slice 0,
-    // into set 0.  Near the end the last stage is fetched again and the reads
-    // land unused, which keeps the loop free of branches.
-    const int kn = min(kt + 2, nk - 1);
-#pragma unroll
-    for (int j = 16; j < NM; ++j) {
+    for (int j = 0; j < NM; ++j) {
+      if constexpr (TWO) {
+        if (j == RS) {
+          wait_vm<IPW>();   // stage kt + 1 has landed (in order: only stage kt + 2 may be out)
+          __syncthreads();  // ... in every wave's part
+        }
+      } else {
+        if (j == 16) {
+          wait_vm<0>();
+          __syncthreads();  // buffer buf is free, stage kt + 1 is in
+        }
+      }
       mma(1, j);
-      if ((j - 16) % DMA_GAP == 0 && (j - 16) / DMA_GAP < IPW)
-        dma16_s(gbase((j - 16) / DMA_GAP) + kn * RB, voff[(j - 16) / DMA_GAP],
-                sbase + buf * STAGE + (j - 16) / DMA_GAP * 1024);
+      if constexpr (TWO) {
+        if (j < RS) dma_slot(NM - 1 - B1J + j);
+      } else {
+        if (j >= 16 && (j - 16) % GAP1 == 0 && (j - 16) / GAP1 < IPW) dma_slot((j - 16) / GAP1 * GAP);
+      }
       if (j >= RS && j - RS < NF) read_piece(0, buf ^ 1, j - RS);
     }
   }

@@ -184,7 +184,7 @@ struct QkvM {
 };
 
 struct OprojM {
-  static constexpr bool DIRECT_W4 = false;
+  static constexpr bool DIRECT_W4 = true;
   static constexpr int EPI = EPI_PLAIN;
   const bf16 *o, *Wo, *x;
   bf16 *xt;
@@ -204,6 +204,45 @@ struct OprojM {
   __device__ const bf16 *a_row(const MTile &t, int r) const { return o + int64_t(t.m0 + r) * K; }
   __device__ const bf16 *b_row(const MTile &t, int n) const {
     return t.n0 + n < d ? Wo + int64_t(t.n0 + n) * K : nullptr;
+  }
+  // Four-wave kernel: in wave column wn, MFMA block ni, lane column c holds
+  // output column NI (16 wn + c) + ni of the tile, so each lane ends with NI
+  // consecutive columns of each of its rows: xt = x + o Wo^T in pieces of
+  // NI / 2 words.
+  template <int NI>
+  __device__ const bf16 *b_row_w4(const MTile &t, int wn, int ni, int c) const {
+    const int f = t.n0 + NI * (16 * wn + c) + ni;
+    return f < d ? Wo + int64_t(f) * K : nullptr;
+  }
+  template <int MI, int NI>
+  __device__ void store_w4(const MTile &t, const f32x4_t (&acc)[MI][NI], int wm, int wn, int lane) const {
+    static_assert(NI % 2 == 0, "whole words");
+    const int f = t.n0 + NI * (16 * wn + (lane & 15));
+    if (f >= d) return;  // d is a multiple of NI: a lane's columns are all in or all out
+    uint32_t xv[MI][4][NI / 2];  // the residual rows first, so their loads overlap
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = wm * MI * 16 + mi * 16 + 4 * (lane >> 4) + i;
+        const uint32_t *xr = (const uint32_t *)(x + int64_t(t.m0 + (r < t.mvalid ? r : 0)) * d + f);
+#pragma unroll
+        for (int u = 0; u < NI / 2; ++u) xv[mi][i][u] = xr[u];
+      }
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = wm * MI * 16 + mi * 16 + 4 * (lane >> 4) + i;
+        if (r >= t.mvalid) continue;
+        uint32_t *yr = (uint32_t *)(xt + int64_t(t.m0 + r) * d + f);
+#pragma unroll
+        for (int u = 0; u < NI / 2; ++u) {
+          const uint32_t w = xv[mi][i][u];
+          yr[u] = pk_bf16(__uint_as_float(w << 16) + acc[mi][2 * u][i],
+                          __uint_as_float(w & 0xFFFF0000u) + acc[mi][2 * u + 1][i]);
+        }
+      }
   }
   // item = 8 columns of one row: xt = x + o Wo^T
   template <int BM, int NC, int LDC, int NT>
@@ -729,6 +768,20 @@ static hipError_t launch(const P &p, int K, int m_tiles, int n_tiles, hipStream_
   return hipGetLastError();
 }
 
+// CUs of the current device (the tile-shape choice counts rounds of them).
+static int cu_count() {
+  static int n = 0;
+  if (n == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      n = v;
+    else
+      n = 256;
+  }
+  return n;
+}
+
 template <class P, int BM, int BN>
 static hipError_t launch_w4(const P &p, int K, int m_tiles, int n_tiles, hipStream_t st) {
   if (m_tiles > 0 && n_tiles > 0)
@@ -791,6 +844,17 @@ hipError_t mfma_oproj(const triroute_cfg &cfg, int N, const void *x, const void 
   p.N = N;
   p.d = cfg.d_model;
   p.K = cfg.n_heads * cfg.head_dim;
+  const bf16 *lo;
+  const bool w4 = p.K >= 128 && span32({{p.o, size_t(N) * p.K * sizeof(bf16)}}, &lo) &&
+                  span32({{p.Wo, size_t(p.d) * p.K * sizeof(bf16)}}, &lo);
+  if (w4) {  // 192- or 256-wide tiles: whichever fills the CUs in fewer rounds of shorter steps
+    const int mt = (N + 255) / 256, cu = cu_count();
+    const int r192 = p.d % 192 == 0 ? (mt * (p.d / 192) + cu - 1) / cu : 0;
+    const int r256 = p.d % 256 == 0 ? (mt * (p.d / 256) + cu - 1) / cu : 0;
+    if (r192 > 0 && (r256 == 0 || 3 * r192 <= 4 * r256))
+      return launch_w4<OprojM, 256, 192>(p, p.K, mt, p.d / 192, st);
+    if (r256 > 0) return launch_w4<OprojM, 256, 256>(p, p.K, mt, p.d / 256, st);
+  }
   return launch<OprojM, 256, 128, 4, 2, 64, 3>(p, p.K, (N + 255) / 256, (p.d + 127) / 128, st);
 }
 

@@ -831,6 +831,14 @@ hipError_t mfma_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
     p.inv_freq[j] = j < cfg.head_dim / 2
                         ? pow(double(cfg.rope_theta), -2.0 * j / double(cfg.head_dim))
                         : 0.0;
+  // Few tokens (decode): the product streams the weights; 32-row tiles one
+  // head wide put one block on every head and row tile.
+  if (p.N <= 2048) {
+    if (p.dh == 64)
+      return launch<QkvM, 32, 64, 2, 1, 64, 4>(p, cfg.d_model, (p.N + 31) / 32, (p.Ncols + 63) / 64, st);
+    if (p.dh == 128)
+      return launch<QkvM, 32, 128, 2, 2, 64, 4>(p, cfg.d_model, (p.N + 31) / 32, (p.Ncols + 127) / 128, st);
+  }
   return launch<QkvM, 256, 128, 4, 2, 64, 3>(p, cfg.d_model, (p.N + 255) / 256, (p.Ncols + 127) / 128, st);
 }
 
@@ -845,6 +853,8 @@ hipError_t mfma_oproj(const triroute_cfg &cfg, int N, const void *x, const void 
   p.d = cfg.d_model;
   p.K = cfg.n_heads * cfg.head_dim;
   const bf16 *lo;
+  if (N <= 2048)  // few tokens: weight streaming, narrow tiles as for QKV
+    return launch<OprojM, 32, 64, 2, 1, 64, 4>(p, p.K, (N + 31) / 32, (p.d + 63) / 64, st);
   const bool w4 = p.K >= 128 && span32({{p.o, size_t(N) * p.K * sizeof(bf16)}}, &lo) &&
                   span32({{p.Wo, size_t(p.d) * p.K * sizeof(bf16)}}, &lo);
   if (w4) {  // 192- or 256-wide tiles: whichever fills the CUs in fewer rounds of shorter steps
@@ -876,10 +886,16 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
   p1.dff = dff;
   const size_t wb = size_t(E) * dff * d * sizeof(bf16);
   const bf16 *alo;
+  // Few assignments (decode): each expert's rows fit a 32-row tile and the
+  // work is streaming the expert weights, so narrow 32 x 64 tiles (two
+  // waves, four stages) put every CU on its own slice of the weights.
+  const bool small = Nk <= 2048;
   const bool w4 = span32({{p1.Wg, wb}, {p1.Wu, wb}}, &p1.Wlo) &&
                   span32({{p1.n2, size_t(N) * d * sizeof(bf16)}}, &alo);
-  hipError_t err = w4 ? launch_w4<Moe1M, 256, 256>(p1, d, Nk / 256 + E, (dff + 127) / 128, st)
-                      : launch<Moe1M, 256, 256, 2, 4, 64, 2>(p1, d, Nk / 256 + E, (dff + 127) / 128, st);
+  hipError_t err =
+      small ? launch<Moe1M, 32, 64, 2, 1, 64, 4>(p1, d, Nk / 32 + E, (dff + 31) / 32, st)
+      : w4  ? launch_w4<Moe1M, 256, 256>(p1, d, Nk / 256 + E, (dff + 127) / 128, st)
+            : launch<Moe1M, 256, 256, 2, 4, 64, 2>(p1, d, Nk / 256 + E, (dff + 127) / 128, st);
   if (err != hipSuccess) return err;
   Moe2M p2;
   p2.Hm = (const bf16 *)Hm;
@@ -891,6 +907,7 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
   p2.E = E;
   p2.d = d;
   p2.dff = dff;
+  if (small) return launch<Moe2M, 32, 64, 2, 1, 64, 4>(p2, dff, Nk / 32 + E, (d + 63) / 64, st);
   const bool w4b = dff >= 128 && d % 192 == 0 && span32({{p2.Wd, wb}}, &alo) &&
                    span32({{p2.Hm, size_t(Nk) * dff * sizeof(bf16)}}, &alo);
   return w4b ? launch_w4<Moe2M, 256, 192>(p2, dff, Nk / 256 + E, d / 192, st)

@@ -81,8 +81,9 @@ __global__ __launch_bounds__(256) void kv_slots_kernel(CacheView cv, int T,
 // 32-bit word of a K record belongs to one slot), scales and 8/16-bit V
 // codes (byte and half-word stores); 2- and 4-bit V codes share words with
 // neighbouring slots and go to vstage, one byte per element, for
-// kv_vpack_kernel.  The K words of the token are assembled in LDS: each lane
-// ORs its element into its word, then one lane per word stores it.
+// kv_vpack_kernel (single-token rows: in place, by word atomics).  The K
+// words of the token are assembled in LDS: each lane ORs its element into
+// its word, then one lane per word stores it.
 template <typename T>
 __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int N,
                                                        const int32_t *__restrict__ seq_ids,
@@ -172,9 +173,18 @@ __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int
         v_place(st, c, dh, ln, q);
         q_word(q, bp, wd, bt);
         uint8_t *addr = vp + ln * (8 * bp) + wd * 4;
-        if (bp <= 4)
-          vstage[(int64_t(i) * Hkv + g) * dh + c] = uint8_t(e);
-        else if (bp == 8)
+        if (bp <= 4) {
+          if (T_ == 1) {
+            // one new token per row: its bits of the shared word are cleared
+            // and set in place (another row's token of the same word, if
+            // any, touches other bits), and kv_vpack is not needed
+            const uint32_t m = ((1u << bp) - 1u) << bt;
+            atomicAnd((uint32_t *)addr, ~m);
+            atomicOr((uint32_t *)addr, e << bt);
+          } else {
+            vstage[(int64_t(i) * Hkv + g) * dh + c] = uint8_t(e);
+          }
+        } else if (bp == 8)
           addr[bt >> 3] = uint8_t(e);
         else if (bp == 16)
           *(uint16_t *)(addr + (bt >> 3)) = uint16_t(e);
@@ -323,8 +333,9 @@ hipError_t launch_kv_append(const triroute_cfg &cfg, const CacheView &cv, int B,
   // partly filled step it starts in
   const int JS = (T + 31) / 32 + 1;
   const int64_t units = int64_t(B) * 2 * cfg.n_kv_heads * JS;
-  kv_vpack_kernel<<<dim3(unsigned((units + 3) / 4)), 256, 0, st>>>(cv, B, T, JS, seq_ids,
-                                                                    ws.old_len, ws.vstage);
+  if (T > 1)  // single-token rows wrote their 2- and 4-bit V codes in place
+    kv_vpack_kernel<<<dim3(unsigned((units + 3) / 4)), 256, 0, st>>>(cv, B, T, JS, seq_ids,
+                                                                      ws.old_len, ws.vstage);
   return hipGetLastError();
 }
 

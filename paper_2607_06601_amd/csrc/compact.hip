@@ -57,49 +57,40 @@ __global__ __launch_bounds__(256) void compact_count_kernel(
   for (int e = tid; e < E1; e += 256) hist[j * E1 + e] = lh[e];
 }
 
-// One block: expert counts, offsets and each block's first output position.
-__global__ __launch_bounds__(64) void compact_scan_kernel(int32_t *__restrict__ hist, int nbe,
-                                                         int E1, int32_t *__restrict__ exp_cnt,
-                                                         int32_t *__restrict__ exp_off) {
-  __shared__ int cnt[64];
-  const int e = threadIdx.x;
-  if (e < E1) {
-    int run = 0;
-    for (int j = 0; j < nbe; ++j) {
-      int v = hist[j * E1 + e];
-      hist[j * E1 + e] = run;
-      run += v;
-    }
-    cnt[e] = run;
-    exp_cnt[e] = run;
-  }
-  __syncthreads();
-  if (e == 0) {
-    int off = 0;
-    exp_off[0] = 0;
-    for (int ee = 1; ee < E1; ++ee) {
-      off += cnt[ee];
-      exp_off[ee] = off;
-    }
-  }
-  __syncthreads();
-  if (e >= 1 && e < E1) {
-    int start = 0;
-    for (int ee = 1; ee < e; ++ee) start += cnt[ee];
-    for (int j = 0; j < nbe; ++j) hist[j * E1 + e] += start;
-  }
-}
-
-// Stable scatter of assignment ids into per-expert lists.
+// Stable scatter of assignment ids into per-expert lists.  Block j first
+// forms each expert's first output position for its chunk from the chunk
+// histograms (all chunks' totals give the expert offsets; block 0 also
+// writes the counts and offsets).
 __global__ __launch_bounds__(256) void compact_scatter_kernel(const int32_t *__restrict__ eidx,
                                                               const int32_t *__restrict__ hist,
-                                                              int E1, int Nk,
-                                                              int32_t *__restrict__ rows) {
+                                                              int nbe, int E1, int Nk,
+                                                              int32_t *__restrict__ rows,
+                                                              int32_t *__restrict__ exp_cnt,
+                                                              int32_t *__restrict__ exp_off) {
   __shared__ int wc[4][64];
-  __shared__ int run[64];
+  __shared__ int run[64], tot[64];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int j = blockIdx.x;
-  for (int e = tid; e < E1; e += 256) run[e] = hist[j * E1 + e];
+  if (tid < E1) {
+    int before = 0, all = 0;
+    for (int jj = 0; jj < nbe; ++jj) {
+      const int v = hist[jj * E1 + tid];
+      if (jj < j) before += v;
+      all += v;
+    }
+    run[tid] = before;
+    tot[tid] = all;
+  }
+  __syncthreads();
+  if (tid < E1) {
+    int start = 0;  // lists of experts 1 .. tid - 1 come first
+    for (int ee = 1; ee < tid; ++ee) start += tot[ee];
+    if (tid >= 1) run[tid] += start;
+    if (j == 0) {
+      exp_cnt[tid] = tot[tid];
+      exp_off[tid] = tid == 0 ? 0 : start + tot[tid];
+    }
+  }
   __syncthreads();
   for (int sub = 0; sub < CHUNK; sub += 256) {
     const int a = j * CHUNK + sub + tid;
@@ -132,8 +123,8 @@ hipError_t launch_compact(const triroute_cfg &cfg, int B, int T, const uint8_t *
   const int nbe = (Nk + CHUNK - 1) / CHUNK;
   compact_count_kernel<<<B * H + nbe, 256, 0, st>>>(mode, eidx, B, T, H, E1, Nk, c.attn_cnt,
                                                     c.attn_idx, hist);
-  compact_scan_kernel<<<1, 64, 0, st>>>(hist, nbe, E1, c.exp_cnt, c.exp_off);
-  compact_scatter_kernel<<<nbe, 256, 0, st>>>(eidx, hist, E1, Nk, c.exp_rows);
+  compact_scatter_kernel<<<nbe, 256, 0, st>>>(eidx, hist, nbe, E1, Nk, c.exp_rows, c.exp_cnt,
+                                               c.exp_off);
   return hipGetLastError();
 }
 

@@ -92,15 +92,17 @@ RouterWs carve_router(Carve &cv, const triroute_cfg &c, int N) {
   return w;
 }
 struct MoeWs {
-  void *n2, *Hm;
+  void *n2, *Hm;  // one row per expert-list entry (at most N k)
   float *Y;
+  int32_t *slot_of;  // list entry of each assignment
 };
 MoeWs carve_moe(Carve &cv, const triroute_cfg &c, int N) {
   MoeWs w;
   const size_t ab = act_bytes(c);
-  w.n2 = cv.take<uint8_t>(size_t(N) * c.d_model * ab);
+  w.n2 = cv.take<uint8_t>(size_t(N) * c.top_k * c.d_model * ab);
   w.Hm = cv.take<uint8_t>(size_t(N) * c.top_k * c.d_ff * ab);
   w.Y = cv.take<float>(size_t(N) * c.top_k * c.d_model);
+  w.slot_of = cv.take<int32_t>(size_t(N) * c.top_k);
   return w;
 }
 tr::KvWs carve_kv(Carve &cv, const triroute_cfg &c, int B, int T) {
@@ -510,9 +512,11 @@ static int moe_impl(const triroute_cfg *cfg, int n_tok, const void *xt, const tr
                     const triroute_moe_w *w, const int32_t *eidx, const float *egate,
                     const triroute_compaction *cmp, void *x_out, Carve &cv, hipStream_t st) {
   MoeWs m = carve_moe(cv, *cfg, n_tok);
-  CHECK_HIP(tr::launch_rms_norm2(*cfg, n_tok, xt, dw->g2, m.n2, st), "rms_norm2 launch");
+  CHECK_HIP(tr::launch_moe_norm_rows(*cfg, n_tok, xt, dw->g2, *cmp, m.n2, m.slot_of, st),
+            "moe_norm_rows launch");
   CHECK_HIP(tr::launch_moe_gemms(*cfg, n_tok, m.n2, *w, *cmp, m.Hm, m.Y, st), "moe gemm launch");
-  CHECK_HIP(tr::launch_moe_combine(*cfg, n_tok, xt, m.Y, eidx, egate, x_out, st), "combine launch");
+  CHECK_HIP(tr::launch_moe_combine(*cfg, n_tok, xt, m.Y, m.slot_of, eidx, egate, x_out, st),
+            "combine launch");
   return TRIROUTE_OK;
 }
 

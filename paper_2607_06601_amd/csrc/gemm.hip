@@ -3,9 +3,10 @@
 // their fused epilogues:
 //   QKV   : [n1] x [Wq;Wk;Wv]^T, rotate-half RoPE on q and k
 //   O-proj: xt = x + o Wo^T
-//   MoE-1 : H = silu(n2 Wgate_e^T) * (n2 Wup_e^T) per expert e, rows gathered
-//           from the expert's assignment list (paper Sec. 3.2 (B), SwiGLU)
-//   MoE-2 : Y[a] = H Wdown_e^T, scattered back to assignment a
+//   MoE-1 : H = silu(n2 Wgate_e^T) * (n2 Wup_e^T) per expert e (paper Sec.
+//           3.2 (B), SwiGLU); n2, H and Y hold one row per entry of the
+//           expert lists, in list order (the lists lie back to back)
+//   MoE-2 : Y = H Wdown_e^T
 // A VALU tiled kernel.  Grouped problems map block -> (expert, row tile) from
 // the device-side expert counts, so no host synchronisation is needed.
 #include <type_traits>
@@ -140,15 +141,15 @@ struct Moe1Prob {
   typedef T elem;
   const T *n2, *Wg, *Wu;
   T *Hm;
-  const int32_t *cnt, *off, *rows;
-  int E, k, d, dff, K;
+  const int32_t *cnt, *off;
+  int E, d, dff, K;
   __device__ bool map(int bx, int by, int BM, Tile &t) const {
     if (!map_grouped(bx, BM, cnt, off, E, t)) return false;
     t.n0 = by * 64;
     return true;
   }
   __device__ const T *a_row(const Tile &t, int r) const {
-    return n2 + int64_t(rows[t.p0 + r] / k) * d;
+    return n2 + int64_t(t.p0 + r) * d;
   }
   __device__ const T *b_row(const Tile &t, int n) const {
     const int64_t f = int64_t(t.e - 1) * dff + t.n0 + (n & 63);
@@ -171,7 +172,7 @@ struct Moe2Prob {
   typedef T elem;
   const T *Hm, *Wd;
   float *Y;
-  const int32_t *cnt, *off, *rows;
+  const int32_t *cnt, *off;
   int E, d, dff, K;
   __device__ bool map(int bx, int by, int BM, Tile &t) const {
     if (!map_grouped(bx, BM, cnt, off, E, t)) return false;
@@ -187,8 +188,7 @@ struct Moe2Prob {
     for (int idx = tid; idx < nr * 128; idx += 256) {
       const int r = idx >> 7, c = idx & 127;
       if (r0 + r >= t.mvalid || t.n0 + c >= d) continue;
-      const int a = rows[t.p0 + r0 + r];
-      Y[int64_t(a) * d + t.n0 + c] = C[r * ldc + c];
+      Y[int64_t(t.p0 + r0 + r) * d + t.n0 + c] = C[r * ldc + c];
     }
   }
 };
@@ -323,9 +323,7 @@ static hipError_t moe_gemms_t(const triroute_cfg &cfg, int N, const void *n2,
   p1.Hm = (T *)Hm;
   p1.cnt = c.exp_cnt;
   p1.off = c.exp_off;
-  p1.rows = c.exp_rows;
   p1.E = E;
-  p1.k = k;
   p1.d = d;
   p1.dff = dff;
   p1.K = d;
@@ -337,7 +335,6 @@ static hipError_t moe_gemms_t(const triroute_cfg &cfg, int N, const void *n2,
   p2.Y = Y;
   p2.cnt = c.exp_cnt;
   p2.off = c.exp_off;
-  p2.rows = c.exp_rows;
   p2.E = E;
   p2.d = d;
   p2.dff = dff;

@@ -14,7 +14,9 @@
 //   QKV   : [n1] x [Wq;Wk;Wv]^T, rotate-half RoPE on q and k
 //   O-proj: xt = x + o Wo^T
 //   MoE-1 : H = silu(n2 Wgate_e^T) * (n2 Wup_e^T) per expert (paper Sec. 3.2 (B))
-//   MoE-2 : Y[a] = H Wdown_e^T, scattered back to assignment a
+//   MoE-2 : Y = H Wdown_e^T
+// n2, H and Y of the experts hold one row per entry of the expert lists, in
+// list order (the lists lie back to back), so a tile's rows are contiguous.
 #include <algorithm>
 #include <initializer_list>
 
@@ -34,7 +36,7 @@ struct MTile {
 // the tiles of experts 1..e, so the mapping costs one parallel load instead
 // of a chain of E dependent ones (E <= 63).
 struct GroupScan {
-  int c = 0, nt = 0, incl = 0, total = 0;
+  int c = 0, nt = 0, incl = 0, total = 0, start = 0;
 };
 
 __device__ __forceinline__ GroupScan group_scan(int BM, const int32_t *cnt, int E) {
@@ -50,19 +52,27 @@ __device__ __forceinline__ GroupScan group_scan(int BM, const int32_t *cnt, int 
   }
   g.incl = x;
   g.total = __shfl(x, 63, 64);
+  // first list position of expert lane + 1: the lists lie back to back in
+  // expert order, so it is the sum of the counts before it
+  int s = g.c;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int y = __shfl_up(s, d, 64);
+    if (lane >= d) s += y;
+  }
+  g.start = s - g.c;
   return g;
 }
 
 // Map a linear row-tile index to (expert e >= 1, tile within e).
-__device__ __forceinline__ bool mmap_grouped(int bx, int BM, const GroupScan &gs,
-                                             const int32_t *off, MTile &t) {
+__device__ __forceinline__ bool mmap_grouped(int bx, int BM, const GroupScan &gs, MTile &t) {
   const uint64_t m = __ballot(gs.incl > bx);
   if (!m) return false;
   const int l = __ffsll((unsigned long long)m) - 1;
   const int incl = __shfl(gs.incl, l, 64), nt = __shfl(gs.nt, l, 64), c = __shfl(gs.c, l, 64);
   const int rem = bx - (incl - nt);
   t.e = l + 1;
-  t.p0 = off[l] + rem * BM;
+  t.p0 = __shfl(gs.start, l, 64) + rem * BM;
   t.mvalid = min(BM, c - rem * BM);
   t.m0 = 0;
   return true;
@@ -266,24 +276,22 @@ struct OprojM {
 
 struct Moe1M {
   static constexpr int EPI = EPI_SWIGLU;
-  const bf16 *n2, *Wg, *Wu, *Wlo;  // Wlo: the lower of Wg, Wu
+  const bf16 *n2, *Wg, *Wu, *Wlo;  // n2: normalised rows in list order; Wlo: the lower of Wg, Wu
   bf16 *Hm;
-  const int32_t *cnt, *off, *rows;
-  int E, k, d, dff;
+  const int32_t *cnt;
+  int E, d, dff;
   static constexpr int out_cols(int BN) { return BN / 2; }
   static constexpr bool GROUPED = true;
   __device__ int tiles(int BM, int ny, const GroupScan &gs) const { return gs.total * ny; }
   __device__ bool map(int bx, int by, int BM, int BN, MTile &t, const GroupScan &gs) const {
-    if (!mmap_grouped(bx, BM, gs, off, t)) return false;
+    if (!mmap_grouped(bx, BM, gs, t)) return false;
     t.n0 = by * (BN / 2);  // BN/2 expert units per tile (gate + up columns)
     return true;
   }
   __device__ int ccol(int P, int) const { return P; }
   __device__ const bf16 *a_base() const { return n2; }
   __device__ const bf16 *b_base() const { return Wlo; }
-  __device__ const bf16 *a_row(const MTile &t, int r) const {
-    return n2 + int64_t(rows[t.p0 + r] / k) * d;
-  }
+  __device__ const bf16 *a_row(const MTile &t, int r) const { return n2 + int64_t(t.p0 + r) * d; }
   __device__ const bf16 *b_row(const MTile &t, int n) const {
     int P, half;
     col_pair(n, P, half);
@@ -346,14 +354,14 @@ struct Moe2M {
   static constexpr bool DIRECT_W4 = true;
   static constexpr int EPI = EPI_PLAIN;
   const bf16 *Hm, *Wd;
-  float *Y;
-  const int32_t *cnt, *off, *rows;
+  float *Y;  // rows in list order
+  const int32_t *cnt;
   int E, d, dff;
   static constexpr int out_cols(int BN) { return BN; }
   static constexpr bool GROUPED = true;
   __device__ int tiles(int BM, int ny, const GroupScan &gs) const { return gs.total * ny; }
   __device__ bool map(int bx, int by, int BM, int BN, MTile &t, const GroupScan &gs) const {
-    if (!mmap_grouped(bx, BM, gs, off, t)) return false;
+    if (!mmap_grouped(bx, BM, gs, t)) return false;
     t.n0 = by * BN;
     return true;
   }
@@ -376,32 +384,25 @@ struct Moe2M {
     static_assert(NI % 2 == 0, "whole 8-byte pieces");
     const int f = t.n0 + NI * (16 * wn + (lane & 15));
     if (f >= d) return;  // d is a multiple of NI: a lane's features are all in or all out
-    int slot[MI][4];  // destination rows first, so their loads overlap
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = wm * MI * 16 + mi * 16 + 4 * (lane >> 4) + i;
-        slot[mi][i] = r < t.mvalid ? rows[t.p0 + r] : -1;
-      }
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (slot[mi][i] < 0) continue;
-        float *y = Y + int64_t(slot[mi][i]) * d + f;
+        if (r >= t.mvalid) continue;
+        float *y = Y + int64_t(t.p0 + r) * d + f;
 #pragma unroll
         for (int ni = 0; ni < NI; ni += 2) *(float2 *)(y + ni) = make_float2(acc[mi][ni][i], acc[mi][ni + 1][i]);
       }
   }
-  // item = 8 output features of one assignment, scattered to its slot row
+  // item = 8 output features of one list row
   template <int BM, int NC, int LDC, int NT>
   __device__ void epilogue(const MTile &t, const float *C, int tid) const {
     constexpr int CC = NC / 8;
     for (int it = tid; it < BM * CC; it += NT) {
       const int r = it / CC, c8 = (it % CC) * 8;
       if (r >= t.mvalid || t.n0 + c8 >= d) continue;
-      float *y = Y + int64_t(rows[t.p0 + r]) * d + t.n0 + c8;
+      float *y = Y + int64_t(t.p0 + r) * d + t.n0 + c8;
       const float *c = C + r * LDC + c8;
       *(float4 *)y = make_float4(c[0], c[1], c[2], c[3]);
       *(float4 *)(y + 4) = make_float4(c[4], c[5], c[6], c[7]);
@@ -878,10 +879,7 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
   p1.Wu = (const bf16 *)w.Wup;
   p1.Hm = (bf16 *)Hm;
   p1.cnt = c.exp_cnt;
-  p1.off = c.exp_off;
-  p1.rows = c.exp_rows;
   p1.E = E;
-  p1.k = k;
   p1.d = d;
   p1.dff = dff;
   const size_t wb = size_t(E) * dff * d * sizeof(bf16);
@@ -891,7 +889,7 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
   // waves, four stages) put every CU on its own slice of the weights.
   const bool small = Nk <= 2048;
   const bool w4 = span32({{p1.Wg, wb}, {p1.Wu, wb}}, &p1.Wlo) &&
-                  span32({{p1.n2, size_t(N) * d * sizeof(bf16)}}, &alo);
+                  span32({{p1.n2, size_t(Nk) * d * sizeof(bf16)}}, &alo);
   hipError_t err =
       small ? launch<Moe1M, 32, 64, 2, 1, 64, 4>(p1, d, Nk / 32 + E, (dff + 31) / 32, st)
       : w4  ? launch_w4<Moe1M, 256, 256>(p1, d, Nk / 256 + E, (dff + 127) / 128, st)
@@ -902,8 +900,6 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
   p2.Wd = (const bf16 *)w.Wdown;
   p2.Y = Y;
   p2.cnt = c.exp_cnt;
-  p2.off = c.exp_off;
-  p2.rows = c.exp_rows;
   p2.E = E;
   p2.d = d;
   p2.dff = dff;

@@ -67,10 +67,11 @@ hipError_t launch_attn_mfma_prefill(const triroute_cfg &cfg, const CacheView &cv
                                     const int32_t *seq_ids, const void *q,
                                     const triroute_compaction &c, void *o, hipStream_t st);
 // misc.hip
-hipError_t launch_rms_norm2(const triroute_cfg &cfg, int N, const void *x, const void *g,
-                            void *out, hipStream_t st);
+hipError_t launch_moe_norm_rows(const triroute_cfg &cfg, int N, const void *x, const void *g,
+                                const triroute_compaction &c, void *out, int32_t *slot_of,
+                                hipStream_t st);
 hipError_t launch_moe_combine(const triroute_cfg &cfg, int N, const void *xt, const float *Y,
-                              const int32_t *eidx, const float *egate, void *xout,
-                              hipStream_t st);
+                              const int32_t *slot_of, const int32_t *eidx, const float *egate,
+                              void *xout, hipStream_t st);
 
 }  // namespace tr

@@ -1,21 +1,27 @@
 // Second RMSNorm and the expert combine of paper Sec. 3.1 / 3.2 (B):
 //   n2 = RMSNorm(xt; g2);  x_out = xt + sum_{slot: e != 0} gate * Y[i*k + slot]
 // Slots are summed in slot order (deterministic); a token whose every slot is
-// the null expert gets x_out = xt exactly.
+// the null expert gets x_out = xt exactly.  The expert GEMMs take n2 and give
+// Y in list order (one row per entry of the expert lists, lists back to
+// back), so the normalisation writes the rows of each list entry and records
+// where each assignment's row went.
 #include "kernels.hpp"
 
 namespace tr {
 
-// One wave per row, 8 consecutive elements per lane access (d % 64 == 0).
+// One wave per list entry pos (8 consecutive elements per lane access,
+// d % 64 == 0): token a / k of assignment a = rows[pos], normalised, to row
+// pos; slot_of[a] = pos.  Entries past the lists' total do nothing.
 template <typename T>
-__global__ __launch_bounds__(256) void rms_norm2_kernel(const T *__restrict__ x,
-                                                        const T *__restrict__ g,
-                                                        T *__restrict__ out, int N, int d,
-                                                        float eps) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+__global__ __launch_bounds__(256) void moe_norm_rows_kernel(
+    const T *__restrict__ x, const T *__restrict__ g, const int32_t *__restrict__ rows,
+    const int32_t *__restrict__ off, int E, int k, int Nk, T *__restrict__ out,
+    int32_t *__restrict__ slot_of, int d, float eps) {
+  const int pos = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
   const int lane = threadIdx.x & 63;
-  if (row >= N) return;
-  const T *xr = x + int64_t(row) * d;
+  if (pos >= Nk || pos >= off[E]) return;  // off[E]: end of the last list
+  const int a = rows[pos];
+  const T *xr = x + int64_t(a / k) * d;
   float ss = 0.f;
   for (int c = lane * 8; c < d; c += 512) {
     float v[8];
@@ -25,7 +31,7 @@ __global__ __launch_bounds__(256) void rms_norm2_kernel(const T *__restrict__ x,
   }
   ss = wave_sum(ss);
   const float r = 1.0f / sqrtf(ss / float(d) + eps);
-  T *orow = out + int64_t(row) * d;
+  T *orow = out + int64_t(pos) * d;
   for (int c = lane * 8; c < d; c += 512) {
     float v[8], gv[8];
     load8(xr + c, v);
@@ -34,12 +40,14 @@ __global__ __launch_bounds__(256) void rms_norm2_kernel(const T *__restrict__ x,
     for (int i = 0; i < 8; ++i) v[i] = (v[i] * r) * gv[i];
     store8(orow + c, v);
   }
+  if (lane == 0) slot_of[a] = pos;
 }
 
 // One thread per 8 consecutive features of a token.
 template <typename T>
 __global__ __launch_bounds__(256) void moe_combine_kernel(const T *__restrict__ xt,
                                                           const float *__restrict__ Y,
+                                                          const int32_t *__restrict__ slot_of,
                                                           const int32_t *__restrict__ eidx,
                                                           const float *__restrict__ egate,
                                                           T *__restrict__ xout, int N, int d,
@@ -58,7 +66,7 @@ __global__ __launch_bounds__(256) void moe_combine_kernel(const T *__restrict__ 
       if (eidx[int64_t(i) * k + s] == 0) continue;
       const float gt = egate[int64_t(i) * k + s];
       float ys[8];
-      load8(Y + (int64_t(i) * k + s) * d + c, ys);
+      load8(Y + int64_t(slot_of[int64_t(i) * k + s]) * d + c, ys);
 #pragma unroll
       for (int u = 0; u < 8; ++u) y[u] = fmaf(gt, ys[u], y[u]);
       any = true;
@@ -71,30 +79,35 @@ __global__ __launch_bounds__(256) void moe_combine_kernel(const T *__restrict__ 
   }
 }
 
-hipError_t launch_rms_norm2(const triroute_cfg &cfg, int N, const void *x, const void *g,
-                            void *out, hipStream_t st) {
-  dim3 grid((N + 3) / 4);
+hipError_t launch_moe_norm_rows(const triroute_cfg &cfg, int N, const void *x, const void *g,
+                                const triroute_compaction &c, void *out, int32_t *slot_of,
+                                hipStream_t st) {
+  const int k = cfg.top_k, Nk = N * k, E = cfg.n_experts;
+  dim3 grid((Nk + 3) / 4);
   if (cfg.act == TRIROUTE_BF16)
-    rms_norm2_kernel<bf16><<<grid, 256, 0, st>>>((const bf16 *)x, (const bf16 *)g, (bf16 *)out, N,
-                                                 cfg.d_model, cfg.rms_eps);
+    moe_norm_rows_kernel<bf16><<<grid, 256, 0, st>>>((const bf16 *)x, (const bf16 *)g, c.exp_rows,
+                                                     c.exp_off, E, k, Nk, (bf16 *)out, slot_of,
+                                                     cfg.d_model, cfg.rms_eps);
   else
-    rms_norm2_kernel<float><<<grid, 256, 0, st>>>((const float *)x, (const float *)g,
-                                                  (float *)out, N, cfg.d_model, cfg.rms_eps);
+    moe_norm_rows_kernel<float><<<grid, 256, 0, st>>>((const float *)x, (const float *)g,
+                                                      c.exp_rows, c.exp_off, E, k, Nk,
+                                                      (float *)out, slot_of, cfg.d_model,
+                                                      cfg.rms_eps);
   return hipGetLastError();
 }
 
 hipError_t launch_moe_combine(const triroute_cfg &cfg, int N, const void *xt, const float *Y,
-                              const int32_t *eidx, const float *egate, void *xout,
+                              const int32_t *slot_of, const int32_t *eidx, const float *egate, void *xout,
                               hipStream_t st) {
   int64_t total = int64_t(N) * (cfg.d_model / 8);
   int64_t blocks = (total + 255) / 256;
   if (blocks > 8192) blocks = 8192;
   if (cfg.act == TRIROUTE_BF16)
     moe_combine_kernel<bf16><<<dim3(unsigned(blocks)), 256, 0, st>>>(
-        (const bf16 *)xt, Y, eidx, egate, (bf16 *)xout, N, cfg.d_model, cfg.top_k);
+        (const bf16 *)xt, Y, slot_of, eidx, egate, (bf16 *)xout, N, cfg.d_model, cfg.top_k);
   else
     moe_combine_kernel<float><<<dim3(unsigned(blocks)), 256, 0, st>>>(
-        (const float *)xt, Y, eidx, egate, (float *)xout, N, cfg.d_model, cfg.top_k);
+        (const float *)xt, Y, slot_of, eidx, egate, (float *)xout, N, cfg.d_model, cfg.top_k);
   return hipGetLastError();
 }
 

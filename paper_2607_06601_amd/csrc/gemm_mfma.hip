@@ -220,10 +220,11 @@ struct OprojM {
   // consecutive columns of each of its rows: xt = x + o Wo^T in pieces of
   // NI / 2 words.
   template <int NI>
-  __device__ const bf16 *b_row_w4(const MTile &t, int wn, int ni, int c) const {
+  __device__ uint32_t b_off_w4(const MTile &t, int wn, int ni, int c) const {
     const int f = t.n0 + NI * (16 * wn + c) + ni;
-    return f < d ? Wo + int64_t(f) * K : nullptr;
+    return f < d ? uint32_t(f) * uint32_t(2 * K) : 0u;
   }
+  __device__ uint32_t a_off(const MTile &t, int r) const { return uint32_t(t.m0 + r) * uint32_t(2 * K); }
   template <int MI, int NI>
   __device__ void store_w4(const MTile &t, const f32x4_t (&acc)[MI][NI], int wm, int wn, int lane) const {
     static_assert(NI % 2 == 0, "whole words");
@@ -304,11 +305,15 @@ struct Moe1M {
   // even ni and up for odd, so each lane ends with both halves of NI / 2
   // consecutive units and writes them as one piece per row.
   static constexpr bool DIRECT_W4 = true;
+  // Byte offsets from a_base / b_base (32 bits: the host checks the spans).
+  // Units past d_ff read unit 0 of the lower matrix instead.
+  __device__ uint32_t a_off(const MTile &t, int r) const { return uint32_t(t.p0 + r) * uint32_t(2 * d); }
   template <int NI>
-  __device__ const bf16 *b_row_w4(const MTile &t, int wn, int ni, int c) const {
+  __device__ uint32_t b_off_w4(const MTile &t, int wn, int ni, int c) const {
     const int f = t.n0 + (NI / 2) * (16 * wn + c) + (ni >> 1);
-    if (f >= dff) return nullptr;
-    return ((ni & 1) ? Wu : Wg) + (int64_t(t.e - 1) * dff + f) * d;
+    if (f >= dff) return 0u;
+    const uint32_t m = uint32_t(((ni & 1) ? Wu : Wg) - Wlo) * 2u;
+    return m + uint32_t((t.e - 1) * dff + f) * uint32_t(2 * d);
   }
   template <int MI, int NI>
   __device__ void store_w4(const MTile &t, const f32x4_t (&acc)[MI][NI], int wm, int wn, int lane) const {
@@ -375,10 +380,11 @@ struct Moe2M {
   // holds output feature NI (16 wn + c) + ni of the tile, so each lane ends
   // with NI consecutive features of each of its rows.
   template <int NI>
-  __device__ const bf16 *b_row_w4(const MTile &t, int wn, int ni, int c) const {
+  __device__ uint32_t b_off_w4(const MTile &t, int wn, int ni, int c) const {
     const int f = t.n0 + NI * (16 * wn + c) + ni;
-    return f < d ? Wd + (int64_t(t.e - 1) * d + f) * dff : nullptr;
+    return f < d ? uint32_t((t.e - 1) * d + f) * uint32_t(2 * dff) : 0u;
   }
+  __device__ uint32_t a_off(const MTile &t, int r) const { return uint32_t(t.p0 + r) * uint32_t(2 * dff); }
   template <int MI, int NI>
   __device__ void store_w4(const MTile &t, const f32x4_t (&acc)[MI][NI], int wm, int wn, int lane) const {
     static_assert(NI % 2 == 0, "whole 8-byte pieces");
@@ -588,6 +594,21 @@ __device__ __forceinline__ void mfma_agpr(f32x4_t &acc, const bf16x8_t &a, const
   asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
 
+// The compiler does not see the MFMAs inside the asm statements, so it does
+// not keep its own accesses of the accumulators clear of their hazards.
+// Each row of accumulators passes through an asm statement that starts with
+// `nops` wait states: accesses after it are ordered after the wait, and
+// writes before it (zeroing) before the wait.
+template <int NI>
+__device__ __forceinline__ void acc_fence_row(f32x4_t (&a)[NI]) {
+  static_assert(NI == 6 || NI == 8, "accumulator row widths in use");
+  if constexpr (NI == 8)
+    asm volatile("s_nop 4" : "+a"(a[0]), "+a"(a[1]), "+a"(a[2]), "+a"(a[3]), "+a"(a[4]), "+a"(a[5]),
+                 "+a"(a[6]), "+a"(a[7]));
+  else
+    asm volatile("s_nop 4" : "+a"(a[0]), "+a"(a[1]), "+a"(a[2]), "+a"(a[3]), "+a"(a[4]), "+a"(a[5]));
+}
+
 template <class P, int BM, int BN>
 __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
   constexpr int NW = 4, NT = 256, WN = 2;
@@ -617,16 +638,29 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
   constexpr int NSLOT = (NM - 1 - B1J) + RS;  // slice 0 after B1J, then slice 1 before RS
   constexpr int GAP = NSLOT / IPW < 4 ? NSLOT / IPW : 4;
   static_assert(B1J < NM && RS >= 16 && (TWO ? GAP >= 1 : GAP1 >= 1), "room for the reads and transfers");
-  constexpr int NC = P::out_cols(BN), LDC = NC + 16;
-  constexpr int SMEM = P::DIRECT_W4 || 2 * STAGE > BM * LDC * 4 ? 2 * STAGE : BM * LDC * 4;
-  __shared__ __align__(1024) uint8_t smem[SMEM];
+  static_assert(P::DIRECT_W4, "results are written from the accumulators");
+  __shared__ __align__(1024) uint8_t smem[2 * STAGE];
+  // Persistent: block b takes tiles b, b + gridDim.x, ... (one block per CU).
+  // The operand stream runs on across tiles: the last two K steps of a tile
+  // fetch the first two stages of the block's next tile, so its transfers
+  // are in flight while this one's results are written.
   GroupScan gs;
   if constexpr (P::GROUPED) gs = group_scan(BM, p.cnt, p.E);
-  const int total = p.tiles(BM, ny, gs);
-  if (int(blockIdx.x) >= total) return;
-  const int t = xcd_tile(blockIdx.x, total);
-  MTile tc;
-  if (!p.map(t / ny, t % ny, BM, BN, tc, gs)) return;
+  const int total = __builtin_amdgcn_readfirstlane(p.tiles(BM, ny, gs));
+  int L = blockIdx.x;
+  if (L >= total) return;
+  auto tile = [&](int l) {  // a tile's fields are wave-uniform: kept in SGPRs
+    MTile t;
+    const int x = xcd_tile(l, total);
+    p.map(x / ny, x % ny, BM, BN, t, gs);  // every index below total maps to a tile
+    t.m0 = __builtin_amdgcn_readfirstlane(t.m0);
+    t.n0 = __builtin_amdgcn_readfirstlane(t.n0);
+    t.mvalid = __builtin_amdgcn_readfirstlane(t.mvalid);
+    t.e = __builtin_amdgcn_readfirstlane(t.e);
+    t.p0 = __builtin_amdgcn_readfirstlane(t.p0);
+    return t;
+  };
+  MTile tc = tile(L);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, in SGPRs
   const int wm = wave / WN, wn = wave % WN;
@@ -635,24 +669,38 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
   // rows (RPT divides BM), so each lane keeps one 32-bit byte offset per
   // transfer from that operand's base (the host checks that every operand
   // row lies within 4 GB of it); the base moves on by 128 B per K step.
+  // Rows past the valid ones read a valid row instead: their products land
+  // in accumulators that are never stored.
   static_assert(BM % RPT == 0, "a transfer stays within one operand");
   auto is_a = [&](int j) { return RPT * (wave * IPW + j) < BM; };  // wave-uniform
   auto gbase = [&](int j) { return (const uint8_t *)(is_a(j) ? p.a_base() : p.b_base()); };
-  uint32_t voff[IPW];
+  // (lane-derived terms of the per-tile address arithmetic start from an
+  // opaque copy of the lane: hoisted out of the tile loop they would hold
+  // registers through the K loop)
+  auto pinned_lane = [&]() {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    return ln;
+  };
+  auto offsets = [&](const MTile &t, uint32_t(&o)[IPW]) {
+    const int ln = pinned_lane();
 #pragma unroll
-  for (int j = 0; j < IPW; ++j) {
-    const int rr = RPT * (wave * IPW + j) + lane / CPR;
-    const bf16 *row;
-    if (is_a(j)) {
-      row = p.a_row(tc, rr < tc.mvalid ? rr : 0);
-    } else {
-      if constexpr (P::DIRECT_W4)
-        row = p.template b_row_w4<NI>(tc, (rr - BM) / TN, ((rr - BM) % TN) >> 4, (rr - BM) & 15);
+    for (int j = 0; j < IPW; ++j) {
+      const int rr = RPT * (wave * IPW + j) + ln / CPR;
+      const uint32_t c16 = swz<CPR>(rr, ln % CPR) * 16;
+      if (is_a(j))
+        o[j] = p.a_off(t, rr < t.mvalid ? rr : 0) + c16;
       else
-        row = p.b_row(tc, rr - BM);
-      if (!row) row = p.b_base();
+        o[j] = p.template b_off_w4<NI>(t, (rr - BM) / TN, ((rr - BM) % TN) >> 4, (rr - BM) & 15) + c16;
     }
-    voff[j] = uint32_t((const uint8_t *)row - gbase(j)) + swz<CPR>(rr, lane % CPR) * 16;
+  };
+  uint32_t voff[IPW], vnx[IPW];
+  offsets(tc, voff);
+  int Ln = L + int(gridDim.x);
+  MTile tn = tc;
+  if (Ln < total) {
+    tn = tile(Ln);
+    offsets(tn, vnx);
   }
   const uint32_t sbase = lds_addr(smem) + wave * IPW * 1024;
   // Fragment addresses: row r = (wave row) + 16 i + lane % 16 reads chunk
@@ -677,84 +725,98 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
     }
   };
   f32x4_t acc[MI][NI];
-#pragma unroll
-  for (int i = 0; i < MI; ++i)
-#pragma unroll
-    for (int j = 0; j < NI; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   auto mma = [&](int set, int j) {
     mfma_agpr(acc[j / NI][j % NI], fa[set][j / NI], fb[set][j % NI]);
   };
 
-  const int nk = K / BK;
+  const int nk = K / BK;  // >= 2 (host)
 #pragma unroll
   for (int j = 0; j < IPW; ++j) dma16_s(gbase(j), voff[j], sbase + j * 1024);
-  if (nk > 1) {
 #pragma unroll
-    for (int j = 0; j < IPW; ++j) dma16_s(gbase(j) + RB, voff[j], sbase + STAGE + j * 1024);
-    wait_vm<IPW>();
-  } else {
-    wait_vm<0>();
-  }
+  for (int j = 0; j < IPW; ++j) dma16_s(gbase(j) + RB, voff[j], sbase + STAGE + j * 1024);
+  wait_vm<IPW>();
   __syncthreads();
 #pragma unroll
   for (int q = 0; q < NF; ++q) read_piece(0, 0, q);
 
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    // stage kt + 2 (near the end the last stage again, unused: no branch)
-    const int kn = min(kt + 2, nk - 1);
-    auto dma_slot = [&](int pos) {  // transfer pos / GAP at slot pos
-      if (pos >= 0 && pos % GAP == 0 && pos / GAP < IPW) {
-        const int j = pos / GAP;
-        dma16_s(gbase(j) + kn * RB, voff[j], sbase + buf * STAGE + j * 1024);
-      }
-    };
-    // slice 0: MFMAs on set 0, the reads of slice 1 into set 1 after the
-    // first NF of them (TWO: the first barrier after MFMA B1J)
+  int ph = 0;  // buffer of the tile's stage 0
+  for (;;) {
 #pragma unroll
-    for (int j = 0; j < NM; ++j) {
-      mma(0, j);
-      if (j < NF) read_piece(1, buf, j);
-      if constexpr (TWO) {
-        if (j == B1J) __syncthreads();  // every wave's reads of stage kt are in
-        if (j > B1J) dma_slot(j - B1J - 1);
-      }
+    for (int i = 0; i < MI; ++i) {
+#pragma unroll
+      for (int j = 0; j < NI; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      acc_fence_row<NI>(acc[i]);
     }
-    // slice 1: MFMAs on set 1, the barrier, then the reads of stage kt + 1,
-    // slice 0, into set 0 (unused in the last step)
-#pragma unroll
-    for (int j = 0; j < NM; ++j) {
-      if constexpr (TWO) {
-        if (j == RS) {
-          wait_vm<IPW>();   // stage kt + 1 has landed (in order: only stage kt + 2 may be out)
-          __syncthreads();  // ... in every wave's part
+    const bool more = Ln < total;
+    for (int kt = 0; kt < nk; ++kt) {
+      const int buf = (kt + ph) & 1;
+      // stage kt + 2: of this tile, else the next tile's stage kt + 2 - nk,
+      // else (the block's last tile) this tile's last stage again, unused
+      const bool nxt = kt + 2 >= nk && more;
+      const int kn = kt + 2 < nk ? kt + 2 : more ? kt + 2 - nk : nk - 1;
+      auto dma_slot = [&](int pos) {  // transfer pos / GAP at slot pos
+        if (pos >= 0 && pos % GAP == 0 && pos / GAP < IPW) {
+          const int j = pos / GAP;
+          dma16_s(gbase(j) + kn * RB, nxt ? vnx[j] : voff[j], sbase + buf * STAGE + j * 1024);
         }
-      } else {
-        if (j == 16) {
-          wait_vm<0>();
-          __syncthreads();  // buffer buf is free, stage kt + 1 is in
+      };
+      // slice 0: MFMAs on set 0, the reads of slice 1 into set 1 after the
+      // first NF of them (TWO: the first barrier after MFMA B1J)
+#pragma unroll
+      for (int j = 0; j < NM; ++j) {
+        mma(0, j);
+        if (j < NF) read_piece(1, buf, j);
+        if constexpr (TWO) {
+          if (j == B1J) __syncthreads();  // every wave's reads of stage kt are in
+          if (j > B1J) dma_slot(j - B1J - 1);
         }
       }
-      mma(1, j);
-      if constexpr (TWO) {
-        if (j < RS) dma_slot(NM - 1 - B1J + j);
-      } else {
-        if (j >= 16 && (j - 16) % GAP1 == 0 && (j - 16) / GAP1 < IPW) dma_slot((j - 16) / GAP1 * GAP);
+      // slice 1: MFMAs on set 1, the barrier, then the reads of stage
+      // kt + 1, slice 0, into set 0 (unused in the last step: the registers
+      // are free while the results are written, and read again after)
+#pragma unroll
+      for (int j = 0; j < NM; ++j) {
+        if constexpr (TWO) {
+          if (j == RS) {
+            // stage kt + 1 has landed: loads complete in issue order and only
+            // stage kt + 2 may be out (stores in between do not matter)
+            wait_vm<IPW>();
+            __syncthreads();  // ... in every wave's part
+          }
+        } else {
+          if (j == 16) {
+            wait_vm<0>();
+            __syncthreads();  // buffer buf is free, stage kt + 1 is in
+          }
+        }
+        mma(1, j);
+        if constexpr (TWO) {
+          if (j < RS) dma_slot(NM - 1 - B1J + j);
+        } else {
+          if (j >= 16 && (j - 16) % GAP1 == 0 && (j - 16) / GAP1 < IPW) dma_slot((j - 16) / GAP1 * GAP);
+        }
+        if (j >= RS && j - RS < NF) read_piece(0, buf ^ 1, j - RS);
       }
-      if (j >= RS && j - RS < NF) read_piece(0, buf ^ 1, j - RS);
     }
-  }
-  // the last MFMAs' results are read below: let them drain first
-  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
-  wait_vm<0>();
-  if constexpr (P::DIRECT_W4) {
-    p.store_w4(tc, acc, wm, wn, lane);
-  } else {
-    __syncthreads();  // every wave is done with the operand stages
-    float *C = (float *)smem;
-    store_acc<P, MI, NI, TM, TN, LDC>(p, C, acc, wm, wn, lane);
-    __syncthreads();
-    p.template epilogue<BM, NC, LDC, NT>(tc, C, tid);
+    // the last MFMAs' results are read below: let them drain first
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+#pragma unroll
+    for (int i = 0; i < MI; ++i) acc_fence_row<NI>(acc[i]);
+    p.store_w4(tc, acc, wm, wn, pinned_lane());
+    if (!more) break;
+    ph ^= nk & 1;
+    // the next tile's stage 0 is in buffer ph (published by the last step's barrier)
+#pragma unroll
+    for (int q = 0; q < NF; ++q) read_piece(0, ph, q);
+    L = Ln;
+    tc = tn;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) voff[j] = vnx[j];
+    Ln = L + int(gridDim.x);
+    if (Ln < total) {
+      tn = tile(Ln);
+      offsets(tn, vnx);
+    }
   }
 }
 
@@ -783,10 +845,13 @@ static int cu_count() {
   return n;
 }
 
+// One block per CU at most (a block holds 128 KB of LDS), each walking its
+// share of the tiles.
 template <class P, int BM, int BN>
 static hipError_t launch_w4(const P &p, int K, int m_tiles, int n_tiles, hipStream_t st) {
+  const int cu = cu_count();
   if (m_tiles > 0 && n_tiles > 0)
-    gemm_w4_kernel<P, BM, BN><<<m_tiles * n_tiles, 256, 0, st>>>(p, K, n_tiles);
+    gemm_w4_kernel<P, BM, BN><<<std::min(m_tiles * n_tiles, cu), 256, 0, st>>>(p, K, n_tiles);
   return hipGetLastError();
 }
 
@@ -892,7 +957,7 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
                   span32({{p1.n2, size_t(Nk) * d * sizeof(bf16)}}, &alo);
   hipError_t err =
       small ? launch<Moe1M, 32, 64, 2, 1, 64, 4>(p1, d, Nk / 32 + E, (dff + 31) / 32, st)
-      : w4  ? launch_w4<Moe1M, 256, 256>(p1, d, Nk / 256 + E, (dff + 127) / 128, st)
+      : w4 && d >= 128 ? launch_w4<Moe1M, 256, 256>(p1, d, Nk / 256 + E, (dff + 127) / 128, st)
             : launch<Moe1M, 256, 256, 2, 4, 64, 2>(p1, d, Nk / 256 + E, (dff + 127) / 128, st);
   if (err != hipSuccess) return err;
   Moe2M p2;

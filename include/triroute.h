@@ -264,10 +264,12 @@ int triroute_router(const triroute_cfg *cfg, int B, int T, const void *x, const 
 /* Row a3: q = Wq n1, k = Wk n1, v = Wv n1 with rotate-half RoPE on q and k
  * at position pos0[b] + t (pos0 NULL: t); pos0 may point into a cache's
  * sequence lengths (see triroute_kv_seq_len_ptr).
- *   n1 act [B*T, d]; q act [B*T, H*dh]; k, v act [B*T, Hkv*dh]. */
+ *   n1 act [B*T, d]; q act [B*T, H*dh]; k, v act [B*T, Hkv*dh].
+ * ws: device scratch of triroute_workspace_bytes(cfg, TRIROUTE_OP_QKV, B, T)
+ * bytes (the per-token rotation table); a shorter one is TRIROUTE_E_WORKSPACE. */
 int triroute_qkv(const triroute_cfg *cfg, int B, int T, const void *n1,
                  const triroute_dense_w *w, const int32_t *pos0, void *q, void *k, void *v,
-                 triroute_stream_t stream);
+                 void *ws, size_t ws_bytes, triroute_stream_t stream);
 
 /* Device pointer to the int32 [n_seq] sequence lengths of a cache. */
 const int32_t *triroute_kv_seq_len_ptr(const triroute_kv_cache *cache);

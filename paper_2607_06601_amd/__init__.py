@@ -105,7 +105,7 @@ def lib():
             "triroute_kv_append": [P, P, i32, i32, P, P, P, P, P, sz, P],
             "triroute_kv_export": [P, P, i32, i32, i32, i32, P, P, P, P, P, P],
             "triroute_router": [P, i32, i32, P, P, P, P, P, P, P, P, P, P, sz, P],
-            "triroute_qkv": [P, i32, i32, P, P, P, P, P, P, P],
+            "triroute_qkv": [P, i32, i32, P, P, P, P, P, P, P, sz, P],
             "triroute_attn_prefill": [P, i32, i32, P, P, P, P, P, P, P, sz, P],
             "triroute_attn_decode": [P, i32, P, P, P, P, P, P, sz, P],
             "triroute_oproj": [P, i32, P, P, P, P, P],
@@ -233,9 +233,9 @@ def router(cfg, B, T, x, psi, rw: RouterW, n1, mode, bit, eidx, egate, cmp: Comp
                                  ws.numel(), _stream(stream)))
 
 
-def qkv(cfg, B, T, n1, dw: DenseW, q, k, v, pos0=None, stream=None):
+def qkv(cfg, B, T, n1, dw: DenseW, q, k, v, ws, pos0=None, stream=None):
     _check(lib().triroute_qkv(C.byref(cfg), B, T, _p(n1), C.byref(dw), _p(pos0), _p(q), _p(k),
-                              _p(v), _stream(stream)))
+                              _p(v), _p(ws), ws.numel(), _stream(stream)))
 
 
 def attn_prefill(cfg, B, T, q, cache: KVCache, mode, cmp: Compaction, o, ws=None,

@@ -138,12 +138,16 @@ LayerBufs carve_layer(Carve &cv, const triroute_cfg &c, int B, int T) {
   return L;
 }
 
+float *carve_qkv(Carve &cv, const triroute_cfg &c, int N) {
+  return cv.take<float>(tr::qkv_rope_floats(c, N));
+}
+
 size_t op_bytes(const triroute_cfg &c, int op, int B, int T) {
   Carve cv(nullptr);
   const int N = B * T;
   switch (op) {
     case TRIROUTE_OP_ROUTER: carve_router(cv, c, N); break;
-    case TRIROUTE_OP_QKV: break;
+    case TRIROUTE_OP_QKV: carve_qkv(cv, c, N); break;
     case TRIROUTE_OP_KV_APPEND: carve_kv(cv, c, B, T); break;
     case TRIROUTE_OP_ATTN_PREFILL: break;
     case TRIROUTE_OP_ATTN_DECODE: carve_attn_decode(cv, c, B); break;
@@ -153,6 +157,7 @@ size_t op_bytes(const triroute_cfg &c, int op, int B, int T) {
       carve_layer(cv, c, B, T);
       size_t s = 0;
       s = std::max(s, op_bytes(c, TRIROUTE_OP_ROUTER, B, T));
+      s = std::max(s, op_bytes(c, TRIROUTE_OP_QKV, B, T));
       s = std::max(s, op_bytes(c, TRIROUTE_OP_KV_APPEND, B, T));
       s = std::max(s, op_bytes(c, op == TRIROUTE_OP_LAYER_DECODE ? TRIROUTE_OP_ATTN_DECODE
                                                                  : TRIROUTE_OP_ATTN_PREFILL,
@@ -456,12 +461,16 @@ int triroute_router(const triroute_cfg *cfg, int B, int T, const void *x, const 
 }
 
 int triroute_qkv(const triroute_cfg *cfg, int B, int T, const void *n1, const triroute_dense_w *w,
-                 const int32_t *pos0, void *q, void *k, void *v, triroute_stream_t stream) {
+                 const int32_t *pos0, void *q, void *k, void *v, void *ws, size_t ws_bytes,
+                 triroute_stream_t stream) {
   TRY(check_cfg(cfg));
   TRY(check_bt(B, T));
   REQUIRE(n1 && w && w->Wq && w->Wk && w->Wv && q && k && v, TRIROUTE_E_INVALID, "NULL argument");
   TRY(check_aligned({n1, w->Wq, w->Wk, w->Wv, q, k, v}));
-  CHECK_HIP(tr::launch_qkv(*cfg, B, T, n1, *w, pos0, nullptr, q, k, v, (hipStream_t)stream),
+  TRY(check_ws(*cfg, TRIROUTE_OP_QKV, B, T, ws, ws_bytes));
+  Carve cv(ws);
+  float *rope = carve_qkv(cv, *cfg, B * T);
+  CHECK_HIP(tr::launch_qkv(*cfg, B, T, n1, *w, pos0, nullptr, q, k, v, rope, (hipStream_t)stream),
             "qkv launch");
   return TRIROUTE_OK;
 }
@@ -579,7 +588,13 @@ static int layer_impl(const triroute_cfg *cfg, int B, int T, bool decode, const 
   }
   // positions continue each sequence: its current length, read on the device
   const int32_t *seq_len = triroute_kv_seq_len_ptr(cache);
-  CHECK_HIP(tr::launch_qkv(*cfg, B, T, L.n1, *dw, seq_len, seq_ids, L.q, L.k, L.v, st), "qkv launch");
+  {
+    Carve sc(ws);
+    sc.used = scratch_at;
+    float *rope = carve_qkv(sc, *cfg, N);
+    CHECK_HIP(tr::launch_qkv(*cfg, B, T, L.n1, *dw, seq_len, seq_ids, L.q, L.k, L.v, rope, st),
+              "qkv launch");
+  }
   {
     Carve sc(ws);
     sc.used = scratch_at;

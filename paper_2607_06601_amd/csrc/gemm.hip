@@ -26,9 +26,8 @@ struct QkvProb {
   typedef T elem;
   const T *n1, *Wq, *Wk, *Wv;
   T *q, *k, *v;
-  const int32_t *pos_base, *pos_idx;
-  int N, Tq, d, H, Hkv, dh, K, Ncols;
-  double inv_freq[64];
+  const float2 *rope;  // (cos, sin) of token row, pair j at row * dh / 2 + j
+  int N, d, H, Hkv, dh, K, Ncols;
   __device__ bool map(int bx, int by, int BM, Tile &t) const {
     t.m0 = bx * BM;
     t.n0 = by * 128;
@@ -71,15 +70,8 @@ struct QkvProb {
       if (rot) {
         const int j = col % dh, jj = j % half;
         const float xp = C[r * ldc + (j < half ? c + half : c - half)];
-        const int b = row / Tq, tt = row - b * Tq;
-        const int pos = (pos_base ? pos_base[pos_idx ? pos_idx[b] : b] : 0) + tt;
-        // angle in fp64, reduced to [-pi, pi], then an accurate fp32 sincos
-        const double ang = double(pos) * inv_freq[jj];
-        const double kq = rint(ang * 0.15915494309189535);
-        double rr = fma(-kq, 6.283185307179586, ang);
-        rr = fma(-kq, 2.4492935982947064e-16, rr);
-        float sn, cs;
-        sincosf(float(rr), &sn, &cs);
+        const float2 a = rope[int64_t(row) * half + jj];
+        const float cs = a.x, sn = a.y;
         y = j < half ? x * cs - xp * sn : xp * sn + x * cs;
       }
       Act<T>::st(out, int64_t(row) * ld + col, y);
@@ -252,10 +244,37 @@ static hipError_t run_gemm(const triroute_cfg &, const P &p, int, int m_tiles64,
   return hipGetLastError();
 }
 
+// Rotation table of paper Sec. 3.1 (rotate-half RoPE): per token row and
+// pair j < dh/2 the cosine and sine of pos * theta^(-2j/dh), the angle taken
+// in fp64 and reduced to [-pi, pi] before an accurate fp32 sincos.  One
+// entry serves every q and k head of the token.
+struct RopeFreq {
+  double inv_freq[64];
+};
+__global__ __launch_bounds__(256) void rope_table_kernel(int N, int Tq, int hd,
+                                                         const int32_t *__restrict__ pos_base,
+                                                         const int32_t *__restrict__ pos_idx,
+                                                         RopeFreq f, float2 *__restrict__ tab) {
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= int64_t(N) * hd) return;
+  const int row = int(i / hd), j = int(i % hd);
+  const int b = row / Tq, tt = row - b * Tq;
+  const int pos = (pos_base ? pos_base[pos_idx ? pos_idx[b] : b] : 0) + tt;
+  const double ang = double(pos) * f.inv_freq[j];
+  const double kq = rint(ang * 0.15915494309189535);
+  double rr = fma(-kq, 6.283185307179586, ang);
+  rr = fma(-kq, 2.4492935982947064e-16, rr);
+  float sn, cs;
+  sincosf(float(rr), &sn, &cs);
+  tab[i] = make_float2(cs, sn);
+}
+
+size_t qkv_rope_floats(const triroute_cfg &cfg, int N) { return size_t(N) * cfg.head_dim; }
+
 template <typename T>
 static hipError_t qkv_t(const triroute_cfg &cfg, int B, int Tq, const void *n1,
-                        const triroute_dense_w &w, const int32_t *pos_base,
-                        const int32_t *pos_idx, void *q, void *k, void *v, hipStream_t st) {
+                        const triroute_dense_w &w, const float *rope, void *q, void *k, void *v,
+                        hipStream_t st) {
   QkvProb<T> p;
   p.n1 = (const T *)n1;
   p.Wq = (const T *)w.Wq;
@@ -264,30 +283,30 @@ static hipError_t qkv_t(const triroute_cfg &cfg, int B, int Tq, const void *n1,
   p.q = (T *)q;
   p.k = (T *)k;
   p.v = (T *)v;
-  p.pos_base = pos_base;
-  p.pos_idx = pos_idx;
+  p.rope = (const float2 *)rope;
   p.N = B * Tq;
-  p.Tq = Tq;
   p.d = cfg.d_model;
   p.H = cfg.n_heads;
   p.Hkv = cfg.n_kv_heads;
   p.dh = cfg.head_dim;
   p.K = cfg.d_model;
   p.Ncols = (cfg.n_heads + 2 * cfg.n_kv_heads) * cfg.head_dim;
-  for (int j = 0; j < 64; ++j)
-    p.inv_freq[j] = j < cfg.head_dim / 2
-                        ? pow(double(cfg.rope_theta), -2.0 * j / double(cfg.head_dim))
-                        : 0.0;
   const int N = p.N;
   return run_gemm(cfg, p, (N + 127) / 128, (N + 63) / 64, (p.Ncols + 127) / 128, st);
 }
 
 hipError_t launch_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
                       const triroute_dense_w &w, const int32_t *pos_base, const int32_t *pos_idx,
-                      void *q, void *k, void *v, hipStream_t st) {
-  return cfg.act == TRIROUTE_BF16
-             ? mfma_qkv(cfg, B, Tq, n1, w, pos_base, pos_idx, q, k, v, st)
-             : qkv_t<float>(cfg, B, Tq, n1, w, pos_base, pos_idx, q, k, v, st);
+                      void *q, void *k, void *v, float *rope, hipStream_t st) {
+  const int N = B * Tq, hd = cfg.head_dim / 2;
+  RopeFreq f;
+  for (int j = 0; j < 64; ++j)
+    f.inv_freq[j] = j < hd ? pow(double(cfg.rope_theta), -2.0 * j / double(cfg.head_dim)) : 0.0;
+  const int64_t n = int64_t(N) * hd;
+  rope_table_kernel<<<dim3(unsigned((n + 255) / 256)), 256, 0, st>>>(N, Tq, hd, pos_base, pos_idx,
+                                                                      f, (float2 *)rope);
+  return cfg.act == TRIROUTE_BF16 ? mfma_qkv(cfg, B, Tq, n1, w, rope, q, k, v, st)
+                                  : qkv_t<float>(cfg, B, Tq, n1, w, rope, q, k, v, st);
 }
 
 template <typename T>

@@ -103,13 +103,12 @@ __device__ __forceinline__ u32x4_t pack8_bf16(const float *v) {
 }
 
 struct QkvM {
-  static constexpr bool DIRECT_W4 = false;
+  static constexpr bool DIRECT_W4 = true;
   static constexpr int EPI = EPI_ROPE;
   const bf16 *n1, *Wq, *Wk, *Wv, *Wlo;  // Wlo: the lowest of Wq, Wk, Wv
   bf16 *q, *k, *v;
-  const int32_t *pos_base, *pos_idx;
-  int N, Tq, d, H, Hkv, dh, Ncols;
-  double inv_freq[64];
+  const float2 *rope;  // (cos, sin) of token row, pair j at row * dh / 2 + j
+  int N, d, H, Hkv, dh, Ncols;
   static constexpr int out_cols(int BN) { return BN; }
   static constexpr bool GROUPED = false;
   __device__ int tiles(int BM, int ny, const GroupScan &) const { return (N + BM - 1) / BM * ny; }
@@ -139,9 +138,82 @@ struct QkvM {
     if (gc < Kd) return Wk + int64_t(gc) * d;
     return Wv + int64_t(gc - Kd) * d;
   }
+  // Four-wave kernel (128-column tiles, d_h 64 or 128): wave column wn
+  // holds pairs j = jw + 2 c + (ni >> 1) of one head, the first half of the
+  // pair in block ni even and the second (j + d_h / 2) in ni odd, where
+  // d_h 64: the tile's head wn, jw = 0; d_h 128: the tile's one head, jw = 32 wn.
+  // Each lane thus holds both halves of pairs 2 c, 2 c + 1 of its rows.
+  __device__ void w4_head(const MTile &t, int wn, int &hcol, int &jw) const {
+    hcol = t.n0 + (dh == 64 ? 64 * wn : 0);  // first column of the head
+    jw = dh == 64 ? 0 : 32 * wn;
+  }
+  __device__ uint32_t a_off(const MTile &t, int r) const { return uint32_t(t.m0 + r) * uint32_t(2 * d); }
+  template <int NI>
+  __device__ uint32_t b_off_w4(const MTile &t, int wn, int ni, int c) const {
+    int hcol, jw;
+    w4_head(t, wn, hcol, jw);
+    int gc = hcol + jw + 2 * c + (ni >> 1) + (ni & 1) * (dh >> 1);
+    if (gc >= Ncols) return 0u;
+    const int Hd = H * dh, Kd = Hkv * dh;
+    const bf16 *W = Wq;
+    if (gc >= Hd + Kd) {
+      W = Wv;
+      gc -= Hd + Kd;
+    } else if (gc >= Hd) {
+      W = Wk;
+      gc -= Hd;
+    }
+    return uint32_t(W - Wlo) * 2u + uint32_t(gc) * uint32_t(2 * d);
+  }
+  template <int MI, int NI>
+  __device__ void store_w4(const MTile &t, const f32x4_t (&acc)[MI][NI], int wm, int wn, int lane) const {
+    static_assert(NI == 4, "two pairs per lane");
+    int hcol, jw;
+    w4_head(t, wn, hcol, jw);
+    if (hcol >= Ncols) return;
+    const int Hd = H * dh, Kd = Hkv * dh, hd = dh >> 1;
+    bf16 *out = q;
+    int ld = Hd, col = hcol;
+    bool rot = true;
+    if (hcol >= Hd + Kd) {
+      out = v; ld = Kd; col = hcol - Hd - Kd; rot = false;
+    } else if (hcol >= Hd) {
+      out = k; ld = Kd; col = hcol - Hd;
+    }
+    const int j = jw + 2 * (lane & 15);
+    // the rows' rotation entries first, so their loads overlap
+    float4 cs[MI][4];
+    if (rot) {
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = wm * MI * 16 + mi * 16 + 4 * (lane >> 4) + i;
+          cs[mi][i] = *(const float4 *)(rope + int64_t(t.m0 + (r < t.mvalid ? r : 0)) * hd + j);
+        }
+    }
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = wm * MI * 16 + mi * 16 + 4 * (lane >> 4) + i;
+        if (r >= t.mvalid) continue;
+        const float a10 = acc[mi][0][i], a20 = acc[mi][1][i], a11 = acc[mi][2][i], a21 = acc[mi][3][i];
+        float y10 = a10, y20 = a20, y11 = a11, y21 = a21;
+        if (rot) {
+          const float4 c4 = cs[mi][i];  // (cos, sin) of pairs j and j + 1
+          y10 = a10 * c4.x - a20 * c4.y;
+          y20 = a10 * c4.y + a20 * c4.x;
+          y11 = a11 * c4.z - a21 * c4.w;
+          y21 = a11 * c4.w + a21 * c4.z;
+        }
+        bf16 *o = out + int64_t(t.m0 + r) * ld + col + j;
+        *(uint32_t *)o = pk_bf16(y10, y11);
+        *(uint32_t *)(o + hd) = pk_bf16(y20, y21);
+      }
+  }
   // item = (row, 8 consecutive pairs of one head): rotate-half RoPE on q and
-  // k with the angle taken in fp64 and reduced to [-pi, pi] before an fp32
-  // sincos; v is copied.
+  // k from the token's rotation table; v is copied.
   template <int BM, int NC, int LDC, int NT>
   __device__ void epilogue(const MTile &t, const float *C, int tid) const {
     constexpr int PC = NC / 16;  // 8-pair chunks per row
@@ -170,20 +242,18 @@ struct QkvM {
         y2[u] = x2[u];
       }
       if (rot) {
-        const int b = row / Tq, tt = row - b * Tq;
-        const int pos = (pos_base ? pos_base[pos_idx ? pos_idx[b] : b] : 0) + tt;
-        const int j0 = col % hd;
+        const float4 *tb = (const float4 *)(rope + int64_t(row) * hd + col % hd);
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const double ang = double(pos) * inv_freq[j0 + u];
-          const double kq = rint(ang * 0.15915494309189535);
-          double rr = fma(-kq, 6.283185307179586, ang);
-          rr = fma(-kq, 2.4492935982947064e-16, rr);
-          float sn, cs;
-          sincosf(float(rr), &sn, &cs);
-          const float a1 = y1[u], a2 = y2[u];
-          y1[u] = a1 * cs - a2 * sn;
-          y2[u] = a1 * sn + a2 * cs;
+        for (int u2 = 0; u2 < 4; ++u2) {
+          const float4 cs2 = tb[u2];  // pairs 2 u2 and 2 u2 + 1
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int u = 2 * u2 + h;
+            const float cs = h ? cs2.z : cs2.x, sn = h ? cs2.w : cs2.y;
+            const float a1 = y1[u], a2 = y2[u];
+            y1[u] = a1 * cs - a2 * sn;
+            y2[u] = a1 * sn + a2 * cs;
+          }
         }
       }
       bf16 *o = out + int64_t(row) * ld + col;
@@ -601,8 +671,10 @@ __device__ __forceinline__ void mfma_agpr(f32x4_t &acc, const bf16x8_t &a, const
 // writes before it (zeroing) before the wait.
 template <int NI>
 __device__ __forceinline__ void acc_fence_row(f32x4_t (&a)[NI]) {
-  static_assert(NI == 6 || NI == 8, "accumulator row widths in use");
-  if constexpr (NI == 8)
+  static_assert(NI == 4 || NI == 6 || NI == 8, "accumulator row widths in use");
+  if constexpr (NI == 4)
+    asm volatile("s_nop 4" : "+a"(a[0]), "+a"(a[1]), "+a"(a[2]), "+a"(a[3]));
+  else if constexpr (NI == 8)
     asm volatile("s_nop 4" : "+a"(a[0]), "+a"(a[1]), "+a"(a[2]), "+a"(a[3]), "+a"(a[4]), "+a"(a[5]),
                  "+a"(a[6]), "+a"(a[7]));
   else
@@ -873,8 +945,8 @@ static bool span32(std::initializer_list<Span> ms, const bf16 **lo) {
 }
 
 hipError_t mfma_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
-                    const triroute_dense_w &w, const int32_t *pos_base, const int32_t *pos_idx,
-                    void *q, void *k, void *v, hipStream_t st) {
+                    const triroute_dense_w &w, const float *rope, void *q, void *k, void *v,
+                    hipStream_t st) {
   QkvM p;
   p.n1 = (const bf16 *)n1;
   p.Wq = (const bf16 *)w.Wq;
@@ -884,19 +956,13 @@ hipError_t mfma_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
   p.q = (bf16 *)q;
   p.k = (bf16 *)k;
   p.v = (bf16 *)v;
-  p.pos_base = pos_base;
-  p.pos_idx = pos_idx;
+  p.rope = (const float2 *)rope;
   p.N = B * Tq;
-  p.Tq = Tq;
   p.d = cfg.d_model;
   p.H = cfg.n_heads;
   p.Hkv = cfg.n_kv_heads;
   p.dh = cfg.head_dim;
   p.Ncols = (cfg.n_heads + 2 * cfg.n_kv_heads) * cfg.head_dim;
-  for (int j = 0; j < 64; ++j)
-    p.inv_freq[j] = j < cfg.head_dim / 2
-                        ? pow(double(cfg.rope_theta), -2.0 * j / double(cfg.head_dim))
-                        : 0.0;
   // Few tokens (decode): the product streams the weights; 32-row tiles one
   // head wide put one block on every head and row tile.
   if (p.N <= 2048) {
@@ -905,6 +971,13 @@ hipError_t mfma_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
     if (p.dh == 128)
       return launch<QkvM, 32, 128, 2, 2, 64, 4>(p, cfg.d_model, (p.N + 31) / 32, (p.Ncols + 127) / 128, st);
   }
+  const bf16 *lo;
+  const bool w4 = (p.dh == 64 || p.dh == 128) && p.Ncols % 128 == 0 && p.d >= 128 &&
+                  span32({{p.Wq, size_t(p.H) * p.dh * p.d * sizeof(bf16)},
+                          {p.Wk, size_t(p.Hkv) * p.dh * p.d * sizeof(bf16)},
+                          {p.Wv, size_t(p.Hkv) * p.dh * p.d * sizeof(bf16)}}, &lo) &&
+                  span32({{p.n1, size_t(p.N) * p.d * sizeof(bf16)}}, &lo);
+  if (w4) return launch_w4<QkvM, 256, 128>(p, cfg.d_model, (p.N + 255) / 256, p.Ncols / 128, st);
   return launch<QkvM, 256, 128, 4, 2, 64, 3>(p, cfg.d_model, (p.N + 255) / 256, (p.Ncols + 127) / 128, st);
 }
 

@@ -34,10 +34,12 @@ hipError_t launch_kv_export(const triroute_cfg &cfg, const CacheView &cv, int se
                             int slot0, int count, void *kout, void *vout, uint16_t *ksz,
                             uint16_t *vsz, int32_t *pos_out, hipStream_t st);
 // gemm.hip
-// position of token (b, t) = (pos_base ? pos_base[pos_idx ? pos_idx[b] : b] : 0) + t
+// position of token (b, t) = (pos_base ? pos_base[pos_idx ? pos_idx[b] : b] : 0) + t;
+// rope: scratch of qkv_rope_floats(cfg, B * Tq) floats (the rotation table)
+size_t qkv_rope_floats(const triroute_cfg &cfg, int N);
 hipError_t launch_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
                       const triroute_dense_w &w, const int32_t *pos_base, const int32_t *pos_idx,
-                      void *q, void *k, void *v, hipStream_t st);
+                      void *q, void *k, void *v, float *rope, hipStream_t st);
 hipError_t launch_oproj(const triroute_cfg &cfg, int N, const void *x, const void *o,
                         const triroute_dense_w &w, void *xt, hipStream_t st);
 hipError_t launch_moe_gemms(const triroute_cfg &cfg, int N, const void *n2,
@@ -45,8 +47,8 @@ hipError_t launch_moe_gemms(const triroute_cfg &cfg, int N, const void *n2,
                             float *Y, hipStream_t st);
 // gemm_mfma.hip (bf16)
 hipError_t mfma_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
-                    const triroute_dense_w &w, const int32_t *pos_base, const int32_t *pos_idx,
-                    void *q, void *k, void *v, hipStream_t st);
+                    const triroute_dense_w &w, const float *rope, void *q, void *k, void *v,
+                    hipStream_t st);
 hipError_t mfma_oproj(const triroute_cfg &cfg, int N, const void *x, const void *o,
                       const triroute_dense_w &w, void *xt, hipStream_t st);
 hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const triroute_moe_w &w,

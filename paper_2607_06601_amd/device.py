@@ -39,7 +39,17 @@ class DeviceLayer:
             self.t[name] = to_dev(np.asarray(L[name], np.float32), f32, device)
         self.rw = RouterW(*(self.t[n].data_ptr() for n in (
             "g1", "W1", "b1", "W2", "b2", "gr", "Wa", "ca", "We", "ce", "Wb", "cb")))
-        for name in ("Wq", "Wk", "Wv", "Wo", "g2"):
+        # Wq, Wk, Wv back to back in one buffer: the many-token QKV kernel
+        # addresses all three from one base (within 4 GB of it)
+        qkv = [to_dev(L[n], self.act, device) for n in ("Wq", "Wk", "Wv")]
+        flat = torch.empty(sum(w.numel() for w in qkv), dtype=self.act, device=device)
+        off = 0
+        for name, w in zip(("Wq", "Wk", "Wv"), qkv):
+            self.t[name] = flat[off:off + w.numel()].view(w.shape)
+            self.t[name].copy_(w)
+            off += w.numel()
+        del qkv
+        for name in ("Wo", "g2"):
             self.t[name] = to_dev(L[name], self.act, device)
         self.dw = DenseW(*(self.t[n].data_ptr() for n in ("Wq", "Wk", "Wv", "Wo", "g2")))
         self.mw = None

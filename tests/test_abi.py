@@ -51,7 +51,8 @@ def test_validate_accepts_every_workload():
 
 def test_workspace_and_cache_sizes():
     c = cfg160()
-    assert tr.workspace_bytes(c, tr.OP_QKV, 8, 2048) == 0
+    # rotation table: (cos, sin) fp32 per token and pair (d_h / 2 = 32 pairs)
+    assert tr.workspace_bytes(c, tr.OP_QKV, 8, 2048) == 8 * 2048 * 32 * 8
     # slots, per-row pool lengths (rounded to 256 B), staged 2/4-bit V codes (3 heads x 64)
     assert tr.workspace_bytes(c, tr.OP_KV_APPEND, 8, 2048) == 8 * 2048 * 4 + 256 + 8 * 2048 * 192
     lay = tr.workspace_bytes(c, tr.OP_LAYER_PREFILL, 8, 2048)

@@ -225,12 +225,16 @@ def test_kv_capacity_overflow_sets_flag_and_drops_row():
 
 
 # ------------------------------------------------------------------- QKV
-@pytest.mark.parametrize("name", ["tiny_f32_prefill", "160m_bf16_prefill", "1p3b_bf16_prefill"])
-def test_qkv_rope(name):
+# T 133: few-token tiles (ragged against 32-row tiles); T 1500 / 1100: the
+# many-token four-wave path (ragged against 256-row tiles)
+@pytest.mark.parametrize("name,T", [("tiny_f32_prefill", 133), ("160m_bf16_prefill", 133),
+                                    ("1p3b_bf16_prefill", 133), ("160m_bf16_prefill", 1500),
+                                    ("1p3b_bf16_prefill", 1100)])
+def test_qkv_rope(name, T):
     L = gen.make_layer(name, with_moe=False)
     cfg = L["cfg"]
     act = cfg["act"]
-    B, T = 2, 133                                       # ragged against 64/128-row tiles
+    B = 2
     x = gen.to_act(gen.normal(41, "qkv_in", (B * T, cfg["d"])), act)
     D = DeviceLayer(L, moe=False)
     c = D.cfg
@@ -240,7 +244,8 @@ def test_qkv_rope(name):
     q = torch.empty(B * T, H * dh, dtype=D.act, device=DEV)
     k = torch.empty(B * T, Hkv * dh, dtype=D.act, device=DEV)
     v = torch.empty_like(k)
-    tr.qkv(c, B, T, n1, D.dw, q, k, v, pos0=to_dev(pos0, torch.int32))
+    ws = tr.workspace(c, tr.OP_QKV, B, T)
+    tr.qkv(c, B, T, n1, D.dw, q, k, v, ws, pos0=to_dev(pos0, torch.int32))
     torch.cuda.synchronize()
     pos = np.concatenate([p + np.arange(T) for p in pos0])
     qo, ko, vo = oracle.qkv(np.asarray(x, np.float64), L, pos)

@@ -109,6 +109,10 @@ struct QkvM {
   bf16 *q, *k, *v;
   const float2 *rope;  // (cos, sin) of token row, pair j at row * dh / 2 + j
   int N, d, H, Hkv, dh, Ncols;
+  // four-wave kernel: byte offsets of Wq, Wk, Wv from Wlo less the first
+  // column of their range times the row pitch, and the range ends
+  uint32_t wq_o, wk_o, wv_o;
+  int Hd, HKd;
   static constexpr int out_cols(int BN) { return BN; }
   static constexpr bool GROUPED = false;
   __device__ int tiles(int BM, int ny, const GroupScan &) const { return (N + BM - 1) / BM * ny; }
@@ -152,18 +156,11 @@ struct QkvM {
   __device__ uint32_t b_off_w4(const MTile &t, int wn, int ni, int c) const {
     int hcol, jw;
     w4_head(t, wn, hcol, jw);
-    int gc = hcol + jw + 2 * c + (ni >> 1) + (ni & 1) * (dh >> 1);
-    if (gc >= Ncols) return 0u;
-    const int Hd = H * dh, Kd = Hkv * dh;
-    const bf16 *W = Wq;
-    if (gc >= Hd + Kd) {
-      W = Wv;
-      gc -= Hd + Kd;
-    } else if (gc >= Hd) {
-      W = Wk;
-      gc -= Hd;
-    }
-    return uint32_t(W - Wlo) * 2u + uint32_t(gc) * uint32_t(2 * d);
+    const int gc = hcol + jw + 2 * c + (ni >> 1) + (ni & 1) * (dh >> 1);
+    // (arithmetic on the field values: a select of fields by a lane-varying
+    // condition becomes a per-lane load from the kernel arguments)
+    const uint32_t base = wq_o + uint32_t(gc >= Hd) * (wk_o - wq_o) + uint32_t(gc >= HKd) * (wv_o - wk_o);
+    return gc < Ncols ? base + uint32_t(gc) * uint32_t(2 * d) : 0u;
   }
   template <int MI, int NI>
   __device__ void store_w4(const MTile &t, const f32x4_t (&acc)[MI][NI], int wm, int wn, int lane) const {
@@ -768,12 +765,6 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
   };
   uint32_t voff[IPW], vnx[IPW];
   offsets(tc, voff);
-  int Ln = L + int(gridDim.x);
-  MTile tn = tc;
-  if (Ln < total) {
-    tn = tile(Ln);
-    offsets(tn, vnx);
-  }
   const uint32_t sbase = lds_addr(smem) + wave * IPW * 1024;
   // Fragment addresses: row r = (wave row) + 16 i + lane % 16 reads chunk
   // (4 ks + lane / 16) ^ ((r >> 1) & 7); the XOR term depends on the lane only.
@@ -806,6 +797,13 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
   for (int j = 0; j < IPW; ++j) dma16_s(gbase(j), voff[j], sbase + j * 1024);
 #pragma unroll
   for (int j = 0; j < IPW; ++j) dma16_s(gbase(j) + RB, voff[j], sbase + STAGE + j * 1024);
+  // the next tile's offsets while stage 0 lands (needed from step nk - 2 on)
+  int Ln = L + int(gridDim.x);
+  MTile tn = tc;
+  if (Ln < total) {
+    tn = tile(Ln);
+    offsets(tn, vnx);
+  }
   wait_vm<IPW>();
   __syncthreads();
 #pragma unroll
@@ -977,7 +975,15 @@ hipError_t mfma_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
                           {p.Wk, size_t(p.Hkv) * p.dh * p.d * sizeof(bf16)},
                           {p.Wv, size_t(p.Hkv) * p.dh * p.d * sizeof(bf16)}}, &lo) &&
                   span32({{p.n1, size_t(p.N) * p.d * sizeof(bf16)}}, &lo);
-  if (w4) return launch_w4<QkvM, 256, 128>(p, cfg.d_model, (p.N + 255) / 256, p.Ncols / 128, st);
+  if (w4) {
+    const uint32_t pitch = 2u * uint32_t(p.d);
+    p.Hd = p.H * p.dh;
+    p.HKd = p.Hd + p.Hkv * p.dh;
+    p.wq_o = uint32_t((const uint8_t *)p.Wq - (const uint8_t *)p.Wlo);
+    p.wk_o = uint32_t((const uint8_t *)p.Wk - (const uint8_t *)p.Wlo) - uint32_t(p.Hd) * pitch;
+    p.wv_o = uint32_t((const uint8_t *)p.Wv - (const uint8_t *)p.Wlo) - uint32_t(p.HKd) * pitch;
+    return launch_w4<QkvM, 256, 128>(p, cfg.d_model, (p.N + 255) / 256, p.Ncols / 128, st);
+  }
   return launch<QkvM, 256, 128, 4, 2, 64, 3>(p, cfg.d_model, (p.N + 255) / 256, (p.Ncols + 127) / 128, st);
 }
 

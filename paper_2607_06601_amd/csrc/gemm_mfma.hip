@@ -297,30 +297,38 @@ struct OprojM {
     static_assert(NI % 2 == 0, "whole words");
     const int f = t.n0 + NI * (16 * wn + (lane & 15));
     if (f >= d) return;  // d is a multiple of NI: a lane's columns are all in or all out
-    uint32_t xv[MI][4][NI / 2];  // the residual rows first, so their loads overlap
+    // in halves of the rows (MI / 2 row blocks): each half's residual rows
+    // are loaded first, so their loads overlap (all at once would hold 4 MI
+    // (NI / 2) registers)
+    constexpr int MH = MI / 2;
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
+    for (int h = 0; h < 2; ++h) {
+      uint32_t xv[MH][4][NI / 2];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = wm * MI * 16 + mi * 16 + 4 * (lane >> 4) + i;
-        const uint32_t *xr = (const uint32_t *)(x + int64_t(t.m0 + (r < t.mvalid ? r : 0)) * d + f);
+      for (int m = 0; m < MH; ++m)
 #pragma unroll
-        for (int u = 0; u < NI / 2; ++u) xv[mi][i][u] = xr[u];
-      }
+        for (int i = 0; i < 4; ++i) {
+          const int r = wm * MI * 16 + (h * MH + m) * 16 + 4 * (lane >> 4) + i;
+          const uint32_t *xr = (const uint32_t *)(x + int64_t(t.m0 + (r < t.mvalid ? r : 0)) * d + f);
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = wm * MI * 16 + mi * 16 + 4 * (lane >> 4) + i;
-        if (r >= t.mvalid) continue;
-        uint32_t *yr = (uint32_t *)(xt + int64_t(t.m0 + r) * d + f);
-#pragma unroll
-        for (int u = 0; u < NI / 2; ++u) {
-          const uint32_t w = xv[mi][i][u];
-          yr[u] = pk_bf16(__uint_as_float(w << 16) + acc[mi][2 * u][i],
-                          __uint_as_float(w & 0xFFFF0000u) + acc[mi][2 * u + 1][i]);
+          for (int u = 0; u < NI / 2; ++u) xv[m][i][u] = xr[u];
         }
-      }
+#pragma unroll
+      for (int m = 0; m < MH; ++m)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int mi = h * MH + m;
+          const int r = wm * MI * 16 + mi * 16 + 4 * (lane >> 4) + i;
+          if (r >= t.mvalid) continue;
+          uint32_t *yr = (uint32_t *)(xt + int64_t(t.m0 + r) * d + f);
+#pragma unroll
+          for (int u = 0; u < NI / 2; ++u) {
+            const uint32_t w = xv[m][i][u];
+            yr[u] = pk_bf16(__uint_as_float(w << 16) + acc[mi][2 * u][i],
+                            __uint_as_float(w & 0xFFFF0000u) + acc[mi][2 * u + 1][i]);
+          }
+        }
+    }
   }
   // item = 8 columns of one row: xt = x + o Wo^T
   template <int BM, int NC, int LDC, int NT>

@@ -345,6 +345,116 @@ __global__ __launch_bounds__(256) void router_tail_kernel(
   }
 }
 
+// The same tail for few tokens (decode): one wave per token, so every
+// token's chain runs on its own SIMD instead of 16 tokens sharing one block.
+// The weights are read from global memory (cache-resident: every wave reads
+// the same 120 KB); all trunk chunks are loaded at once.  The products are
+// summed in a different order than the MFMA tail (fp32 either way; the
+// decisions do not depend on it above the routing margin).
+constexpr int RT1_MAXKS = 32;
+__global__ __launch_bounds__(256) void router_tail_tok_kernel(
+    const float *__restrict__ upart, int KS, const float *__restrict__ b1,
+    const float *__restrict__ W2, const float *__restrict__ b2, const float *__restrict__ gr,
+    const float *__restrict__ Wa, const float *__restrict__ ca, const float *__restrict__ We,
+    const float *__restrict__ ce, const float *__restrict__ Wb, const float *__restrict__ cb,
+    uint8_t *__restrict__ mode, uint8_t *__restrict__ bit, int32_t *__restrict__ eidx,
+    float *__restrict__ egate, int N, int H, int E1, int k, float eps) {
+  constexpr int DR = RT_DR;
+  __shared__ __align__(16) float vs[4][2][DR];  // per wave: u, then h^; z
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int t = blockIdx.x * 4 + wave;
+  if (t >= N) return;  // wave-uniform; no barrier below
+  float *us = vs[wave][0], *zs = vs[wave][1];
+  const int NZ = 3 * H + E1 + 4;
+  // u = GELU(sum of the KS trunk partials + b1), chunks summed in order
+  float p0[RT1_MAXKS], p1[RT1_MAXKS];
+#pragma unroll
+  for (int s = 0; s < RT1_MAXKS; ++s)
+    if (s < KS) {
+      p0[s] = upart[(int64_t(s) * N + t) * DR + lane];
+      p1[s] = upart[(int64_t(s) * N + t) * DR + lane + 64];
+    }
+  float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+  for (int s = 0; s < RT1_MAXKS; ++s)
+    if (s < KS) {
+      a0 += p0[s];
+      a1 += p1[s];
+    }
+  a0 += b1[lane];
+  a1 += b1[lane + 64];
+  us[lane] = 0.5f * a0 * (1.0f + erff(a0 * 0.70710678118654752f));
+  us[lane + 64] = 0.5f * a1 * (1.0f + erff(a1 * 0.70710678118654752f));
+  __builtin_amdgcn_wave_barrier();
+  // h = W2 u + b2: lane n owns rows n and n + 64
+  float h0 = 0.f, h1 = 0.f;
+  const float4 *w0 = (const float4 *)(W2 + lane * DR), *w1 = (const float4 *)(W2 + (lane + 64) * DR);
+#pragma unroll 8
+  for (int c4 = 0; c4 < DR / 4; ++c4) {
+    const float4 x = w0[c4], y = w1[c4];
+    const float4 u = *(const float4 *)(us + 4 * c4);
+    h0 = fmaf(x.x, u.x, h0); h0 = fmaf(x.y, u.y, h0); h0 = fmaf(x.z, u.z, h0); h0 = fmaf(x.w, u.w, h0);
+    h1 = fmaf(y.x, u.x, h1); h1 = fmaf(y.y, u.y, h1); h1 = fmaf(y.z, u.z, h1); h1 = fmaf(y.w, u.w, h1);
+  }
+  h0 += b2[lane];
+  h1 += b2[lane + 64];
+  // h^ = RMSNorm(h) gr
+  const float ss = seg_sum(h0 * h0 + h1 * h1, 64);
+  const float r = 1.0f / sqrtf(ss / float(DR) + eps);
+  __builtin_amdgcn_wave_barrier();  // every lane is done reading u
+  us[lane] = (h0 * r) * gr[lane];
+  us[lane + 64] = (h1 * r) * gr[lane + 64];
+  __builtin_amdgcn_wave_barrier();
+  // z = [Wa; We; Wb] h^ + [ca; ce; cb]: lane j owns logits j and j + 64
+  for (int z = lane; z < NZ; z += 64) {
+    const float *wz = z < 3 * H ? Wa + z * DR : z < 3 * H + E1 ? We + (z - 3 * H) * DR
+                                                                : Wb + (z - 3 * H - E1) * DR;
+    float acc = 0.f;
+#pragma unroll 8
+    for (int c4 = 0; c4 < DR / 4; ++c4) {
+      const float4 x = ((const float4 *)wz)[c4];
+      const float4 u = *(const float4 *)(us + 4 * c4);
+      acc = fmaf(x.x, u.x, acc); acc = fmaf(x.y, u.y, acc); acc = fmaf(x.z, u.z, acc); acc = fmaf(x.w, u.w, acc);
+    }
+    const float bias = z < 3 * H ? ca[z] : z < 3 * H + E1 ? ce[z - 3 * H] : cb[z - 3 * H - E1];
+    zs[z] = acc + bias;
+  }
+  __builtin_amdgcn_wave_barrier();
+  // modes: lane h takes head h; argmax, first maximum on ties
+  for (int hh = lane; hh < H; hh += 64) {
+    const float *za = zs + 3 * hh;
+    int best = 0;
+    if (za[1] > za[best]) best = 1;
+    if (za[2] > za[best]) best = 2;
+    mode[int64_t(t) * H + hh] = uint8_t(best);
+  }
+  if (lane == 0) {
+    const float *zb = zs + 3 * H + E1;
+    int bb = 0;
+    for (int j = 1; j < 4; ++j)
+      if (zb[j] > zb[bb]) bb = j;
+    bit[t] = uint8_t(bb);
+  }
+  // top-k by logit, ties to the lower id; gates renormalised over the set
+  const float zj = lane < E1 ? zs[3 * H + lane] : -INFINITY;
+  const float zmax = seg_max(zj, 64);
+  uint64_t taken = 0;
+  float tot = 0.f;
+  for (int sl = 0; sl < k; ++sl) {
+    const float cand = (lane < E1 && !(taken >> lane & 1)) ? zj : -INFINITY;
+    const float m = seg_max(cand, 64);
+    const uint64_t hit = __ballot(lane < E1 && !(taken >> lane & 1) && cand == m);
+    const int best = __ffsll((unsigned long long)hit) - 1;
+    taken |= 1ull << best;
+    tot += expf(m - zmax);
+  }
+  if (taken >> lane & 1) {
+    const int sl = __popcll(taken & lanemask_lt());
+    eidx[int64_t(t) * k + sl] = lane;
+    egate[int64_t(t) * k + sl] = expf(zj - zmax) / tot;
+  }
+}
+
 hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const float *psi,
                          const triroute_router_w &w, void *n1, uint8_t *mode, uint8_t *bit,
                          int32_t *eidx, float *egate, float *rinv, float *u,
@@ -364,6 +474,12 @@ hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const fl
                                                 cfg.rms_eps);
     trunk1_kernel<float><<<g2, 256, 0, st>>>((const float *)x, rinv, w.g1, psi, w.W1, u, N, d,
                                              cfg.d_psi, kchunk);
+  }
+  if (N <= 256 && ks <= RT1_MAXKS) {  // few tokens: one wave per token
+    router_tail_tok_kernel<<<dim3((N + 3) / 4), 256, 0, st>>>(
+        u, ks, w.b1, w.W2, w.b2, w.gr, w.Wa, w.ca, w.We, w.ce, w.Wb, w.cb, mode, bit, eidx, egate,
+        N, cfg.n_heads, cfg.n_experts + 1, cfg.top_k, cfg.rms_eps);
+    return hipGetLastError();
   }
   // one block per CU at most (the weights fill most of its LDS), each
   // loading them once and then taking every 256th token tile

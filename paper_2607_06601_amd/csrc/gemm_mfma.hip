@@ -19,6 +19,7 @@
 // list order (the lists lie back to back), so a tile's rows are contiguous.
 #include <algorithm>
 #include <initializer_list>
+#include <type_traits>
 
 #include "kernels.hpp"
 
@@ -668,6 +669,10 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_mfma_kernel(P p, int K, 
 __device__ __forceinline__ void mfma_agpr(f32x4_t &acc, const bf16x8_t &a, const bf16x8_t &b) {
   asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
+// acc = a b (the first product of a tile: no zeroing of the accumulators)
+__device__ __forceinline__ void mfma_agpr_first(f32x4_t &acc, const bf16x8_t &a, const bf16x8_t &b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=a"(acc) : "v"(a), "v"(b));
+}
 
 // The compiler does not see the MFMAs inside the asm statements, so it does
 // not keep its own accesses of the accumulators clear of their hazards.
@@ -799,6 +804,9 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
   auto mma = [&](int set, int j) {
     mfma_agpr(acc[j / NI][j % NI], fa[set][j / NI], fb[set][j % NI]);
   };
+  auto mma_first = [&](int set, int j) {
+    mfma_agpr_first(acc[j / NI][j % NI], fa[set][j / NI], fb[set][j % NI]);
+  };
 
   const int nk = K / BK;  // >= 2 (host)
 #pragma unroll
@@ -819,14 +827,11 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
 
   int ph = 0;  // buffer of the tile's stage 0
   for (;;) {
-#pragma unroll
-    for (int i = 0; i < MI; ++i) {
-#pragma unroll
-      for (int j = 0; j < NI; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      acc_fence_row<NI>(acc[i]);
-    }
     const bool more = Ln < total;
-    for (int kt = 0; kt < nk; ++kt) {
+    // one K step; in the tile's first (FIRST) the slice-0 products start the
+    // accumulators
+    auto kstep = [&](int kt, auto first) {
+      constexpr bool FIRST = decltype(first)::value;
       const int buf = (kt + ph) & 1;
       // stage kt + 2: of this tile, else the next tile's stage kt + 2 - nk,
       // else (the block's last tile) this tile's last stage again, unused
@@ -842,7 +847,10 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
       // first NF of them (TWO: the first barrier after MFMA B1J)
 #pragma unroll
       for (int j = 0; j < NM; ++j) {
-        mma(0, j);
+        if constexpr (FIRST)
+          mma_first(0, j);
+        else
+          mma(0, j);
         if (j < NF) read_piece(1, buf, j);
         if constexpr (TWO) {
           if (j == B1J) __syncthreads();  // every wave's reads of stage kt are in
@@ -875,7 +883,9 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
         }
         if (j >= RS && j - RS < NF) read_piece(0, buf ^ 1, j - RS);
       }
-    }
+    };
+    kstep(0, std::true_type{});
+    for (int kt = 1; kt < nk; ++kt) kstep(kt, std::false_type{});
     // the last MFMAs' results are read below: let them drain first
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
 #pragma unroll

@@ -156,8 +156,8 @@ size_t op_bytes(const triroute_cfg &c, int op, int B, int T) {
     case TRIROUTE_OP_LAYER_DECODE: {
       carve_layer(cv, c, B, T);
       size_t s = 0;
-      s = std::max(s, op_bytes(c, TRIROUTE_OP_ROUTER, B, T));
-      s = std::max(s, op_bytes(c, TRIROUTE_OP_QKV, B, T));
+      // router scratch and rotation table together (the table outlives the router)
+      s = std::max(s, op_bytes(c, TRIROUTE_OP_ROUTER, B, T) + op_bytes(c, TRIROUTE_OP_QKV, B, T));
       s = std::max(s, op_bytes(c, TRIROUTE_OP_KV_APPEND, B, T));
       s = std::max(s, op_bytes(c, op == TRIROUTE_OP_LAYER_DECODE ? TRIROUTE_OP_ATTN_DECODE
                                                                  : TRIROUTE_OP_ATTN_PREFILL,
@@ -454,7 +454,8 @@ int triroute_router(const triroute_cfg *cfg, int B, int T, const void *x, const 
   Carve cv(ws);
   RouterWs rw = carve_router(cv, *cfg, B * T);
   hipStream_t st = (hipStream_t)stream;
-  CHECK_HIP(tr::launch_router(*cfg, B * T, x, psi, *w, n1, mode, bit, eidx, egate, rw.rinv, rw.u, st),
+  CHECK_HIP(tr::launch_router(*cfg, B * T, x, psi, *w, n1, mode, bit, eidx, egate, rw.rinv, rw.u,
+                              nullptr, st),
             "router launch");
   CHECK_HIP(tr::launch_compact(*cfg, B, T, mode, eidx, *cmp, rw.hist, st), "compaction launch");
   return TRIROUTE_OK;
@@ -470,7 +471,8 @@ int triroute_qkv(const triroute_cfg *cfg, int B, int T, const void *n1, const tr
   TRY(check_ws(*cfg, TRIROUTE_OP_QKV, B, T, ws, ws_bytes));
   Carve cv(ws);
   float *rope = carve_qkv(cv, *cfg, B * T);
-  CHECK_HIP(tr::launch_qkv(*cfg, B, T, n1, *w, pos0, nullptr, q, k, v, rope, (hipStream_t)stream),
+  CHECK_HIP(tr::launch_qkv(*cfg, B, T, n1, *w, pos0, nullptr, q, k, v, rope, false,
+                           (hipStream_t)stream),
             "qkv launch");
   return TRIROUTE_OK;
 }
@@ -577,22 +579,21 @@ static int layer_impl(const triroute_cfg *cfg, int B, int T, bool decode, const 
   }
   const size_t scratch_at = cv.used;
   const int N = B * T;
-  {
-    Carve sc(ws);
-    sc.used = scratch_at;
-    RouterWs r = carve_router(sc, *cfg, N);
-    CHECK_HIP(tr::launch_router(*cfg, N, x, psi, *rw, L.n1, L.mode, L.bit, L.eidx, L.egate, r.rinv,
-                                r.u, st),
-              "router launch");
-    CHECK_HIP(tr::launch_compact(*cfg, B, T, L.mode, L.eidx, L.cmp, r.hist, st), "compaction");
-  }
   // positions continue each sequence: its current length, read on the device
   const int32_t *seq_len = triroute_kv_seq_len_ptr(cache);
   {
+    // the router's scratch, then the rotation table: the first RMSNorm
+    // writes the table, the QKV epilogue reads it
     Carve sc(ws);
     sc.used = scratch_at;
+    RouterWs r = carve_router(sc, *cfg, N);
     float *rope = carve_qkv(sc, *cfg, N);
-    CHECK_HIP(tr::launch_qkv(*cfg, B, T, L.n1, *dw, seq_len, seq_ids, L.q, L.k, L.v, rope, st),
+    const tr::RopeJob job = tr::make_rope_job(*cfg, T, seq_len, seq_ids, rope);
+    CHECK_HIP(tr::launch_router(*cfg, N, x, psi, *rw, L.n1, L.mode, L.bit, L.eidx, L.egate, r.rinv,
+                                r.u, &job, st),
+              "router launch");
+    CHECK_HIP(tr::launch_compact(*cfg, B, T, L.mode, L.eidx, L.cmp, r.hist, st), "compaction");
+    CHECK_HIP(tr::launch_qkv(*cfg, B, T, L.n1, *dw, seq_len, seq_ids, L.q, L.k, L.v, rope, true, st),
               "qkv launch");
   }
   {

@@ -244,29 +244,25 @@ static hipError_t run_gemm(const triroute_cfg &, const P &p, int, int m_tiles64,
   return hipGetLastError();
 }
 
-// Rotation table of paper Sec. 3.1 (rotate-half RoPE): per token row and
-// pair j < dh/2 the cosine and sine of pos * theta^(-2j/dh), the angle taken
-// in fp64 and reduced to [-pi, pi] before an accurate fp32 sincos.  One
-// entry serves every q and k head of the token.
-struct RopeFreq {
-  double inv_freq[64];
-};
-__global__ __launch_bounds__(256) void rope_table_kernel(int N, int Tq, int hd,
-                                                         const int32_t *__restrict__ pos_base,
-                                                         const int32_t *__restrict__ pos_idx,
-                                                         RopeFreq f, float2 *__restrict__ tab) {
+// The rotation table (one entry per token and pair serves every q and k
+// head of the token), when the first RMSNorm did not already write it.
+__global__ __launch_bounds__(256) void rope_table_kernel(int N, const RopeJob r) {
   const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (i >= int64_t(N) * hd) return;
-  const int row = int(i / hd), j = int(i % hd);
-  const int b = row / Tq, tt = row - b * Tq;
-  const int pos = (pos_base ? pos_base[pos_idx ? pos_idx[b] : b] : 0) + tt;
-  const double ang = double(pos) * f.inv_freq[j];
-  const double kq = rint(ang * 0.15915494309189535);
-  double rr = fma(-kq, 6.283185307179586, ang);
-  rr = fma(-kq, 2.4492935982947064e-16, rr);
-  float sn, cs;
-  sincosf(float(rr), &sn, &cs);
-  tab[i] = make_float2(cs, sn);
+  if (i >= int64_t(N) * r.hd) return;
+  r.tab[i] = rope_entry(r, int(i / r.hd), int(i % r.hd));
+}
+
+RopeJob make_rope_job(const triroute_cfg &cfg, int Tq, const int32_t *pos_base,
+                      const int32_t *pos_idx, float *tab) {
+  RopeJob r;
+  r.pos_base = pos_base;
+  r.pos_idx = pos_idx;
+  r.Tq = Tq;
+  r.hd = cfg.head_dim / 2;
+  r.tab = (float2 *)tab;
+  for (int j = 0; j < 64; ++j)
+    r.inv_freq[j] = j < r.hd ? pow(double(cfg.rope_theta), -2.0 * j / double(cfg.head_dim)) : 0.0;
+  return r;
 }
 
 size_t qkv_rope_floats(const triroute_cfg &cfg, int N) { return size_t(N) * cfg.head_dim; }
@@ -297,14 +293,13 @@ static hipError_t qkv_t(const triroute_cfg &cfg, int B, int Tq, const void *n1,
 
 hipError_t launch_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
                       const triroute_dense_w &w, const int32_t *pos_base, const int32_t *pos_idx,
-                      void *q, void *k, void *v, float *rope, hipStream_t st) {
-  const int N = B * Tq, hd = cfg.head_dim / 2;
-  RopeFreq f;
-  for (int j = 0; j < 64; ++j)
-    f.inv_freq[j] = j < hd ? pow(double(cfg.rope_theta), -2.0 * j / double(cfg.head_dim)) : 0.0;
-  const int64_t n = int64_t(N) * hd;
-  rope_table_kernel<<<dim3(unsigned((n + 255) / 256)), 256, 0, st>>>(N, Tq, hd, pos_base, pos_idx,
-                                                                      f, (float2 *)rope);
+                      void *q, void *k, void *v, float *rope, bool rope_ready, hipStream_t st) {
+  const int N = B * Tq;
+  if (!rope_ready) {
+    const RopeJob r = make_rope_job(cfg, Tq, pos_base, pos_idx, rope);
+    const int64_t n = int64_t(N) * r.hd;
+    rope_table_kernel<<<dim3(unsigned((n + 255) / 256)), 256, 0, st>>>(N, r);
+  }
   return cfg.act == TRIROUTE_BF16 ? mfma_qkv(cfg, B, Tq, n1, w, rope, q, k, v, st)
                                   : qkv_t<float>(cfg, B, Tq, n1, w, rope, q, k, v, st);
 }

@@ -10,9 +10,34 @@ hipError_t router_prepare();
 // trunk K split: ks chunks of kchunk inputs; the trunk partials take
 // ks * N * 128 floats of scratch
 void router_split(int N, int K, int &ks, int &kchunk);
+// Rotation table of rotate-half RoPE (paper Sec. 3.1): for token row i of a
+// [B, Tq] batch and pair j < d_h / 2, (cos, sin) of pos * theta^(-2j/d_h) at
+// pos = (pos_base ? pos_base[pos_idx ? pos_idx[b] : b] : 0) + t; the angle is
+// taken in fp64 and reduced to [-pi, pi] before an accurate fp32 sincos.
+struct RopeJob {
+  const int32_t *pos_base, *pos_idx;
+  int Tq, hd;
+  float2 *tab;  // [N][hd]
+  double inv_freq[64];
+};
+RopeJob make_rope_job(const triroute_cfg &cfg, int Tq, const int32_t *pos_base,
+                      const int32_t *pos_idx, float *tab);
+__device__ __forceinline__ float2 rope_entry(const RopeJob &r, int row, int j) {
+  const int b = row / r.Tq, tt = row - b * r.Tq;
+  const int pos = (r.pos_base ? r.pos_base[r.pos_idx ? r.pos_idx[b] : b] : 0) + tt;
+  const double ang = double(pos) * r.inv_freq[j];
+  const double kq = rint(ang * 0.15915494309189535);
+  double rr = fma(-kq, 6.283185307179586, ang);
+  rr = fma(-kq, 2.4492935982947064e-16, rr);
+  float sn, cs;
+  sincosf(float(rr), &sn, &cs);
+  return make_float2(cs, sn);
+}
+// rope (optional): the first RMSNorm also writes that rotation table
 hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const float *psi,
                          const triroute_router_w &w, void *n1, uint8_t *mode, uint8_t *bit,
-                         int32_t *eidx, float *egate, float *rinv, float *u, hipStream_t st);
+                         int32_t *eidx, float *egate, float *rinv, float *u, const RopeJob *rope,
+                         hipStream_t st);
 // compact.hip
 int compact_hist_ints(int N, int k, int E1);
 hipError_t launch_compact(const triroute_cfg &cfg, int B, int T, const uint8_t *mode,
@@ -39,7 +64,7 @@ hipError_t launch_kv_export(const triroute_cfg &cfg, const CacheView &cv, int se
 size_t qkv_rope_floats(const triroute_cfg &cfg, int N);
 hipError_t launch_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
                       const triroute_dense_w &w, const int32_t *pos_base, const int32_t *pos_idx,
-                      void *q, void *k, void *v, float *rope, hipStream_t st);
+                      void *q, void *k, void *v, float *rope, bool rope_ready, hipStream_t st);
 hipError_t launch_oproj(const triroute_cfg &cfg, int N, const void *x, const void *o,
                         const triroute_dense_w &w, void *xt, hipStream_t st);
 hipError_t launch_moe_gemms(const triroute_cfg &cfg, int N, const void *n2,

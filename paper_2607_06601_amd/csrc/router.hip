@@ -15,10 +15,12 @@ __global__ __launch_bounds__(256) void rms_norm1_kernel(const T *__restrict__ x,
                                                         const float *__restrict__ g,
                                                         float *__restrict__ rinv,
                                                         T *__restrict__ n1, int N, int d,
-                                                        float eps) {
+                                                        float eps, const RopeJob rj) {
   int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   int lane = threadIdx.x & 63;
   if (row >= N) return;
+  if (rj.tab)  // the token's rotation table entries (one lane per pair)
+    for (int j = lane; j < rj.hd; j += 64) rj.tab[int64_t(row) * rj.hd + j] = rope_entry(rj, row, j);
   const T *xr = x + int64_t(row) * d;
   float ss = 0.f;
   for (int c = lane * 8; c < d; c += 512) {
@@ -457,8 +459,10 @@ __global__ __launch_bounds__(256) void router_tail_tok_kernel(
 
 hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const float *psi,
                          const triroute_router_w &w, void *n1, uint8_t *mode, uint8_t *bit,
-                         int32_t *eidx, float *egate, float *rinv, float *u,
+                         int32_t *eidx, float *egate, float *rinv, float *u, const RopeJob *rope,
                          hipStream_t st) {
+  RopeJob rj{};
+  if (rope) rj = *rope;
   const int d = cfg.d_model;
   int ks, kchunk;
   router_split(N, d + cfg.d_psi, ks, kchunk);
@@ -466,12 +470,12 @@ hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const fl
   dim3 g2((N + 63) / 64, ks);
   if (cfg.act == TRIROUTE_BF16) {
     rms_norm1_kernel<bf16><<<g1, 256, 0, st>>>((const bf16 *)x, w.g1, rinv, (bf16 *)n1, N, d,
-                                               cfg.rms_eps);
+                                               cfg.rms_eps, rj);
     trunk1_kernel<bf16><<<g2, 256, 0, st>>>((const bf16 *)x, rinv, w.g1, psi, w.W1, u, N, d,
                                             cfg.d_psi, kchunk);
   } else {
     rms_norm1_kernel<float><<<g1, 256, 0, st>>>((const float *)x, w.g1, rinv, (float *)n1, N, d,
-                                                cfg.rms_eps);
+                                                cfg.rms_eps, rj);
     trunk1_kernel<float><<<g2, 256, 0, st>>>((const float *)x, rinv, w.g1, psi, w.W1, u, N, d,
                                              cfg.d_psi, kchunk);
   }

@@ -157,14 +157,16 @@ __global__ __launch_bounds__(256) void trunk1_kernel(const T *__restrict__ x,
   }
 }
 
-// Tail, 16 tokens per block (4 waves, fp32 MFMA 16x16x4), with W2 and the
-// head weights staged in LDS by coalesced loads:
+// Tail in 16-token tiles (4 waves per tile, fp32 MFMA 16x16x4), two tiles
+// at a time per block (8 waves: two per SIMD, so one tile's latencies hide
+// behind the other's work), with W2 and the head weights staged in LDS once
+// by coalesced loads:
 //   u = GELU(sum of trunk partials + b1); h = W2 u + b2; h^ = RMSNorm(h) gr;
 //   z = [Wa; We; Wb] h^ + [ca; ce; cb]; argmax / top-k decisions and gates.
-constexpr int RT_TB = 16, RT_DR = 128, RT_LD = RT_DR + 4, RT_NZ = 112;
-constexpr size_t RT_LDS = sizeof(float) * (size_t(RT_DR + RT_NZ + 2 * RT_TB) * RT_LD);
+constexpr int RT_TB = 16, RT_DR = 128, RT_LD = RT_DR + 1, RT_NZ = 112;
+constexpr size_t RT_LDS = sizeof(float) * (size_t(RT_DR + RT_NZ + 4 * RT_TB) * RT_LD);
 
-__global__ __launch_bounds__(256) void router_tail_kernel(
+__global__ __launch_bounds__(512) void router_tail_kernel(
     const float *__restrict__ upart, int KS, const float *__restrict__ b1,
     const float *__restrict__ W2, const float *__restrict__ b2, const float *__restrict__ gr,
     const float *__restrict__ Wa, const float *__restrict__ ca, const float *__restrict__ We,
@@ -175,16 +177,17 @@ __global__ __launch_bounds__(256) void router_tail_kernel(
   extern __shared__ __align__(16) float rt_lds[];
   float(*W2s)[LD] = (float(*)[LD])rt_lds;              // [128][LD]
   float(*Wzs)[LD] = (float(*)[LD])(rt_lds + DR * LD);  // [NZ][LD]
-  float(*Us)[LD] = (float(*)[LD])(rt_lds + (DR + RT_NZ) * LD);
-  float(*Zs)[LD] = (float(*)[LD])(rt_lds + (DR + RT_NZ + TB) * LD);
+  // group g of 4 waves works on its own tile with its own Us / Zs
+  const int g = threadIdx.x >> 8, tid = threadIdx.x & 255, lane = tid & 63, wave = tid >> 6;
+  float(*Us)[LD] = (float(*)[LD])(rt_lds + (DR + RT_NZ + 2 * TB * g) * LD);
+  float(*Zs)[LD] = (float(*)[LD])(rt_lds + (DR + RT_NZ + 2 * TB * g + TB) * LD);
   const int NZ = 3 * H + E1 + 4;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int i = tid; i < DR * DR / 4; i += 256) {
+  for (int i = threadIdx.x; i < DR * DR / 4; i += 512) {
     const int r = i / (DR / 4), c4 = (i % (DR / 4)) * 4;
     const float4 v = *(const float4 *)(W2 + r * DR + c4);
     W2s[r][c4] = v.x; W2s[r][c4 + 1] = v.y; W2s[r][c4 + 2] = v.z; W2s[r][c4 + 3] = v.w;
   }
-  for (int i = tid; i < NZ * DR / 4; i += 256) {
+  for (int i = threadIdx.x; i < NZ * DR / 4; i += 512) {
     const int z = i / (DR / 4), c4 = (i % (DR / 4)) * 4;
     const float *wz = z < 3 * H ? Wa + z * DR
                       : z < 3 * H + E1 ? We + (z - 3 * H) * DR : Wb + (z - 3 * H - E1) * DR;
@@ -207,8 +210,12 @@ __global__ __launch_bounds__(256) void router_tail_kernel(
       }
   };
   const bool prefetch = KS <= 4;
-  if (prefetch) load_parts(blockIdx.x * TB, 0, pre);
-  for (int t0 = blockIdx.x * TB; t0 < N; t0 += gridDim.x * TB) {
+  // both groups run every round (a group past the last token masks its
+  // work), so the block's barriers stay matched
+  const int stride = gridDim.x * 2 * TB;
+  if (prefetch) load_parts(blockIdx.x * 2 * TB + g * TB, 0, pre);
+  for (int base = blockIdx.x * 2 * TB; base < N; base += stride) {
+  const int t0 = base + g * TB;
   {
     // u = GELU(sum of the KS trunk partials + b1): thread tid owns elements
     // tid + 256 e of the block's 16 x 128; partials are summed in chunk order
@@ -220,7 +227,7 @@ __global__ __launch_bounds__(256) void router_tail_kernel(
       for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int e = 0; e < EPT; ++e) sacc[e] += pre[j][e];
-      if (t0 + gridDim.x * TB < N) load_parts(t0 + gridDim.x * TB, 0, pre);
+      if (t0 + stride < N) load_parts(t0 + stride, 0, pre);
     } else {
       for (int s0 = 0; s0 < KS; s0 += 4) {
         float v[4][EPT];
@@ -487,8 +494,8 @@ hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const fl
   }
   // one block per CU at most (the weights fill most of its LDS), each
   // loading them once and then taking every 256th token tile
-  const int tiles = (N + RT_TB - 1) / RT_TB;
-  router_tail_kernel<<<dim3(tiles < 256 ? tiles : 256), 256, RT_LDS, st>>>(
+  const int pairs = ((N + RT_TB - 1) / RT_TB + 1) / 2;
+  router_tail_kernel<<<dim3(pairs < 256 ? pairs : 256), 512, RT_LDS, st>>>(
       u, ks, w.b1, w.W2, w.b2, w.gr, w.Wa, w.ca, w.We, w.ce, w.Wb, w.cb, mode, bit, eidx, egate, N,
       cfg.n_heads, cfg.n_experts + 1, cfg.top_k, cfg.rms_eps);
   return hipGetLastError();

@@ -92,7 +92,9 @@ __global__ __launch_bounds__(256) void compact_scatter_kernel(const int32_t *__r
     }
   }
   __syncthreads();
-  for (int sub = 0; sub < CHUNK; sub += 256) {
+  // (sub rounds past the last assignment are skipped: the bound is uniform
+  // over the block, so every barrier below is still reached by all threads)
+  for (int sub = 0; sub < CHUNK && j * CHUNK + sub < Nk; sub += 256) {
     const int a = j * CHUNK + sub + tid;
     const int e = a < Nk ? eidx[a] : -1;
     int rank = 0;

@@ -22,23 +22,52 @@ __global__ __launch_bounds__(256) void moe_norm_rows_kernel(
   if (pos >= Nk || pos >= off[E]) return;  // off[E]: end of the last list
   const int a = rows[pos];
   const T *xr = x + int64_t(a / k) * d;
+  // rows of up to 1024 elements stay in registers between the two passes
+  constexpr int RR = 2;
+  float v[RR][8];
   float ss = 0.f;
-  for (int c = lane * 8; c < d; c += 512) {
-    float v[8];
-    load8(xr + c, v);
+  if (d <= 512 * RR) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) ss = fmaf(v[i], v[i], ss);
+    for (int q = 0; q < RR; ++q) {
+      const int c = lane * 8 + 512 * q;
+      if (c < d) {
+        load8(xr + c, v[q]);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) ss = fmaf(v[q][i], v[q][i], ss);
+      }
+    }
+  } else {
+    for (int c = lane * 8; c < d; c += 512) {
+      float w[8];
+      load8(xr + c, w);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ss = fmaf(w[i], w[i], ss);
+    }
   }
   ss = wave_sum(ss);
   const float r = 1.0f / sqrtf(ss / float(d) + eps);
   T *orow = out + int64_t(pos) * d;
-  for (int c = lane * 8; c < d; c += 512) {
-    float v[8], gv[8];
-    load8(xr + c, v);
-    load8(g + c, gv);
+  if (d <= 512 * RR) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) v[i] = (v[i] * r) * gv[i];
-    store8(orow + c, v);
+    for (int q = 0; q < RR; ++q) {
+      const int c = lane * 8 + 512 * q;
+      if (c < d) {
+        float gv[8];
+        load8(g + c, gv);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[q][i] = (v[q][i] * r) * gv[i];
+        store8(orow + c, v[q]);
+      }
+    }
+  } else {
+    for (int c = lane * 8; c < d; c += 512) {
+      float w[8], gv[8];
+      load8(xr + c, w);
+      load8(g + c, gv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) w[i] = (w[i] * r) * gv[i];
+      store8(orow + c, w);
+    }
   }
   if (lane == 0) slot_of[a] = pos;
 }

@@ -101,7 +101,7 @@ MoeWs carve_moe(Carve &cv, const triroute_cfg &c, int N) {
   const size_t ab = act_bytes(c);
   w.n2 = cv.take<uint8_t>(size_t(N) * c.top_k * c.d_model * ab);
   w.Hm = cv.take<uint8_t>(size_t(N) * c.top_k * c.d_ff * ab);
-  w.Y = cv.take<float>(size_t(N) * c.top_k * c.d_model);
+  w.Y = cv.take<float>(size_t(N) * c.top_k * c.d_model * tr::moe_ysplit(c, N));
   w.slot_of = cv.take<int32_t>(size_t(N) * c.top_k);
   return w;
 }

@@ -30,6 +30,7 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 struct MTile {
   int m0, n0, mvalid, e, p0;
+  int k0 = 0, yp = 0;  // K offset of a split product and its output plane
 };
 
 // Row tiles of the grouped problems: lane e - 1 of every wave holds expert
@@ -438,19 +439,26 @@ struct Moe2M {
   float *Y;  // rows in list order
   const int32_t *cnt;
   int E, d, dff;
+  int ksplit = 1;        // K halves (few-token path), each to its own plane of Y
+  int64_t yplane = 0;    // elements between planes
   static constexpr int out_cols(int BN) { return BN; }
   static constexpr bool GROUPED = true;
   __device__ int tiles(int BM, int ny, const GroupScan &gs) const { return gs.total * ny; }
   __device__ bool map(int bx, int by, int BM, int BN, MTile &t, const GroupScan &gs) const {
     if (!mmap_grouped(bx, BM, gs, t)) return false;
-    t.n0 = by * BN;
+    const int ncol = (d + BN - 1) / BN, kh = by / ncol;
+    t.n0 = (by - kh * ncol) * BN;
+    t.k0 = kh * (dff / ksplit);
+    t.yp = kh;
     return true;
   }
   __device__ const bf16 *a_base() const { return Hm; }
   __device__ const bf16 *b_base() const { return Wd; }
-  __device__ const bf16 *a_row(const MTile &t, int r) const { return Hm + int64_t(t.p0 + r) * dff; }
+  __device__ const bf16 *a_row(const MTile &t, int r) const {
+    return Hm + int64_t(t.p0 + r) * dff + t.k0;
+  }
   __device__ const bf16 *b_row(const MTile &t, int n) const {
-    return t.n0 + n < d ? Wd + (int64_t(t.e - 1) * d + t.n0 + n) * dff : nullptr;
+    return t.n0 + n < d ? Wd + (int64_t(t.e - 1) * d + t.n0 + n) * dff + t.k0 : nullptr;
   }
   // Four-wave kernel: in wave column wn, MFMA block ni, lane column c
   // holds output feature NI (16 wn + c) + ni of the tile, so each lane ends
@@ -484,7 +492,7 @@ struct Moe2M {
     for (int it = tid; it < BM * CC; it += NT) {
       const int r = it / CC, c8 = (it % CC) * 8;
       if (r >= t.mvalid || t.n0 + c8 >= d) continue;
-      float *y = Y + int64_t(t.p0 + r) * d + t.n0 + c8;
+      float *y = Y + t.yp * yplane + int64_t(t.p0 + r) * d + t.n0 + c8;
       const float *c = C + r * LDC + c8;
       *(float4 *)y = make_float4(c[0], c[1], c[2], c[3]);
       *(float4 *)(y + 4) = make_float4(c[4], c[5], c[6], c[7]);
@@ -1065,7 +1073,12 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
   p2.E = E;
   p2.d = d;
   p2.dff = dff;
-  if (small) return launch<Moe2M, 32, 64, 2, 1, 64, 4>(p2, dff, Nk / 32 + E, (d + 63) / 64, st);
+  if (small) {
+    p2.ksplit = moe_ysplit(cfg, N);
+    p2.yplane = int64_t(Nk) * d;
+    return launch<Moe2M, 32, 64, 2, 1, 64, 4>(p2, dff / p2.ksplit, Nk / 32 + E,
+                                              (d + 63) / 64 * p2.ksplit, st);
+  }
   const bool w4b = dff >= 128 && d % 192 == 0 && span32({{p2.Wd, wb}}, &alo) &&
                    span32({{p2.Hm, size_t(Nk) * dff * sizeof(bf16)}}, &alo);
   return w4b ? launch_w4<Moe2M, 256, 192>(p2, dff, Nk / 256 + E, d / 192, st)

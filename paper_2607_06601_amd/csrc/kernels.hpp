@@ -97,6 +97,12 @@ hipError_t launch_attn_mfma_prefill(const triroute_cfg &cfg, const CacheView &cv
 hipError_t launch_moe_norm_rows(const triroute_cfg &cfg, int N, const void *x, const void *g,
                                 const triroute_compaction &c, void *out, int32_t *slot_of,
                                 hipStream_t st);
+// Few assignments (decode, bf16): the down GEMM splits K in two halves, each
+// written to its own plane of Y (N k rows apart); the combine adds the planes
+// in order.  Returns the number of planes.
+inline int moe_ysplit(const triroute_cfg &c, int N) {
+  return c.act == TRIROUTE_BF16 && N * c.top_k <= 2048 && c.d_ff % 128 == 0 ? 2 : 1;
+}
 hipError_t launch_moe_combine(const triroute_cfg &cfg, int N, const void *xt, const float *Y,
                               const int32_t *slot_of, const int32_t *eidx, const float *egate,
                               void *xout, hipStream_t st);

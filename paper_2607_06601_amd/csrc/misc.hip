@@ -77,6 +77,7 @@ template <typename T>
 __global__ __launch_bounds__(256) void moe_combine_kernel(const T *__restrict__ xt,
                                                           const float *__restrict__ Y,
                                                           const int32_t *__restrict__ slot_of,
+                                                          int ysplit, int64_t yplane,
                                                           const int32_t *__restrict__ eidx,
                                                           const float *__restrict__ egate,
                                                           T *__restrict__ xout, int N, int d,
@@ -95,7 +96,14 @@ __global__ __launch_bounds__(256) void moe_combine_kernel(const T *__restrict__ 
       if (eidx[int64_t(i) * k + s] == 0) continue;
       const float gt = egate[int64_t(i) * k + s];
       float ys[8];
-      load8(Y + int64_t(slot_of[int64_t(i) * k + s]) * d + c, ys);
+      const float *yr = Y + int64_t(slot_of[int64_t(i) * k + s]) * d + c;
+      load8(yr, ys);
+      if (ysplit == 2) {  // the second K half's plane, added in order
+        float y2[8];
+        load8(yr + yplane, y2);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) ys[u] += y2[u];
+      }
 #pragma unroll
       for (int u = 0; u < 8; ++u) y[u] = fmaf(gt, ys[u], y[u]);
       any = true;
@@ -133,10 +141,10 @@ hipError_t launch_moe_combine(const triroute_cfg &cfg, int N, const void *xt, co
   if (blocks > 8192) blocks = 8192;
   if (cfg.act == TRIROUTE_BF16)
     moe_combine_kernel<bf16><<<dim3(unsigned(blocks)), 256, 0, st>>>(
-        (const bf16 *)xt, Y, slot_of, eidx, egate, (bf16 *)xout, N, cfg.d_model, cfg.top_k);
+        (const bf16 *)xt, Y, slot_of, moe_ysplit(cfg, N), int64_t(N) * cfg.top_k * cfg.d_model, eidx, egate, (bf16 *)xout, N, cfg.d_model, cfg.top_k);
   else
     moe_combine_kernel<float><<<dim3(unsigned(blocks)), 256, 0, st>>>(
-        (const float *)xt, Y, slot_of, eidx, egate, (float *)xout, N, cfg.d_model, cfg.top_k);
+        (const float *)xt, Y, slot_of, moe_ysplit(cfg, N), int64_t(N) * cfg.top_k * cfg.d_model, eidx, egate, (float *)xout, N, cfg.d_model, cfg.top_k);
   return hipGetLastError();
 }
 

@@ -208,11 +208,12 @@ def compact(mode, eidx, B, T, H, E, k):
 
 
 # ------------------------------------------------------------ attention
-def qkv(n1, L, pos):
+def qkv(n1, L, pos, act=None):
     """q = Wq n1, k = Wk n1, v = Wv n1 per head, RoPE on q and k at ``pos``;
-    outputs held in the activation dtype."""
+    outputs held in the activation dtype (``act``, default the workload's)."""
     cfg = L["cfg"]
-    H, Hkv, dh, act = cfg["H"], cfg["Hkv"], cfg["dh"], cfg["act"]
+    H, Hkv, dh = cfg["H"], cfg["Hkv"], cfg["dh"]
+    act = act or cfg["act"]
     n = len(n1)
     q = (n1 @ np.asarray(L["Wq"], np.float64).T).reshape(n, H, dh)
     k = (n1 @ np.asarray(L["Wk"], np.float64).T).reshape(n, Hkv, dh)
@@ -283,12 +284,13 @@ def oproj(x, o, Wo):
     return np.asarray(x, np.float64) + o.reshape(n, -1) @ np.asarray(Wo, np.float64).T
 
 
-def moe(xt, L, eidx, egate):
+def moe(xt, L, eidx, egate, act=None):
     """Second half of the block: x' = x~ + sum_{j in S, j != 0} g_j f_j(Norm x~)
     with SwiGLU experts f_j(u) = W_down,j (silu(W_gate,j u) * W_up,j u).
-    The null expert contributes nothing (Sec. 3.2 (B))."""
+    The null expert contributes nothing (Sec. 3.2 (B)).  n2 and the SwiGLU
+    product are held in ``act`` (default the workload's activation dtype)."""
     cfg = L["cfg"]
-    act = cfg["act"]
+    act = act or cfg["act"]
     n2 = to_native(rmsnorm(xt, L["g2"]), act)
     y = np.zeros_like(n2)
     k = eidx.shape[1]
@@ -308,16 +310,28 @@ def moe(xt, L, eidx, egate):
 
 
 # ------------------------------------------------------------ whole layer
-def layer_prefill(L, rows=None):
+def layer_prefill(L, rows=None, kv_in=None, xt_in=None, round_act=True):
     """Prefill of B fresh sequences of T tokens (cache empty beforehand).
 
     ``rows``: token indices whose attention / FFN outputs are wanted (all by
     default).  Routing and compaction are always computed for every token;
     K/V are computed and stored for every token of the sequences ``rows``
     touch.
+
+    Discretely forced evaluation (the comparison protocol for results that a
+    legitimate one-ulp difference upstream can move):
+      * ``kv_in``: {b: (k, v)} native-precision [T, Hkv, dh] keys (rotated) and
+        values of sequence b to quantize into the cache in place of the
+        oracle's own projections; the oracle's quantizer and dequantizer
+        still do all of the cache arithmetic;
+      * ``xt_in``: [len(rows), d] first-residual outputs to feed the expert
+        block in place of the oracle's own x~.
+    ``round_act=False`` holds every tensor handed between operators in fp64
+    instead of the activation dtype (the quantizer still works in fp32).
     """
     cfg = L["cfg"]
-    B, T, H, w, act = cfg["B"], cfg["T"], cfg["H"], cfg["w"], cfg["act"]
+    B, T, H, w = cfg["B"], cfg["T"], cfg["H"], cfg["w"]
+    act = cfg["act"] if round_act else "f64"
     N = B * T
     n1, za, ze, zb = router_logits(L)
     mode, bit, eidx, egate = decide(za, ze, zb, cfg["k"])
@@ -330,8 +344,9 @@ def layer_prefill(L, rows=None):
     for b in seqs:
         sl = slice(b * T, (b + 1) * T)
         pos = np.arange(T)
-        q, kn, vn = qkv(n1a[sl], L, pos)
-        khat, vhat, st = store_kv(kn, vn, bit[sl], cfg)
+        q, kn, vn = qkv(n1a[sl], L, pos, act)
+        kst, vst = (kn, vn) if kv_in is None else kv_in[b]
+        khat, vhat, st = store_kv(kst, vst, bit[sl], cfg)
         stored[b] = st
         want = [int(r) - b * T for r in rows if int(r) // T == b]
         o = attention_seq(q[want], np.asarray(want), khat, vhat,
@@ -341,41 +356,51 @@ def layer_prefill(L, rows=None):
         q_all[b], k_all[b], v_all[b] = q, kn, vn
     o = to_native(np.stack([o_rows[int(r)] for r in rows]), act)
     xt = to_native(oproj(L["x"][rows], o, L["Wo"]), act)
-    xout, n2, y = moe(xt, L, eidx[rows], egate[rows])
+    xin = xt if xt_in is None else np.asarray(xt_in, np.float64)
+    xout, n2, y = moe(xin, L, eidx[rows], egate[rows], act)
     return dict(rows=rows, n1=n1, za=za, ze=ze, zb=zb, mode=mode, bit=bit,
                 eidx=eidx, egate=egate, cmp=cmp, q=q_all, k=k_all, v=v_all,
                 stored=stored, o=o, xt=xt, n2=n2, y=y, xout=xout)
 
 
-def decode_cache_seq(cfg, s):
+def decode_cache_seq(cfg, s, context=None):
     """Read-back values of sequence ``s``'s pre-existing context (decode
-    workloads): the generator's native-precision K/V stored at the
-    generator's per-position widths."""
-    import gen
-    k, v = gen.context_kv(cfg, s)
-    bits = gen.context_bits(cfg, s)
+    workloads): native-precision K/V [ctx, Hkv, dh] and per-position widths
+    from ``context(s) -> (k, v, bits)`` (default: the generator's context),
+    stored through the quantizer."""
+    if context is None:
+        import gen
+        k, v = gen.context_kv(cfg, s)
+        bits = gen.context_bits(cfg, s)
+    else:
+        k, v, bits = context(s)
     khat, vhat, stored = store_kv(k, v, bits, cfg)
     return khat, vhat, stored, bits
 
 
-def layer_decode(L, seqs=None):
+def layer_decode(L, seqs=None, context=None, kv_in=None, xt_in=None, round_act=True):
     """One decode step: each sequence b gets one new token at position
     P = ctx; its K/V are appended at the routed width, then its query heads
-    attend over the read-back cache [0, P] (or its last w keys)."""
+    attend over the read-back cache [0, P] (or its last w keys).
+
+    ``context``: as in ``decode_cache_seq``.  ``kv_in`` ({s: (k, v)}, each
+    [1, Hkv, dh]), ``xt_in`` and ``round_act``: as in ``layer_prefill``."""
     cfg = L["cfg"]
-    B, H, w, act, ctx = cfg["B"], cfg["H"], cfg["w"], cfg["act"], cfg["ctx"]
+    B, H, w, ctx = cfg["B"], cfg["H"], cfg["w"], cfg["ctx"]
+    act = cfg["act"] if round_act else "f64"
     n1, za, ze, zb = router_logits(L)
     mode, bit, eidx, egate = decide(za, ze, zb, cfg["k"])
     cmp = compact(mode, eidx, B, 1, H, cfg["E"], cfg["k"])
     seqs = list(range(B)) if seqs is None else sorted(set(int(s) for s in seqs))
     rows = np.asarray(seqs)
     pos = np.full(len(rows), ctx)
-    q, kn, vn = qkv(to_native(n1[rows], act), L, pos)
+    q, kn, vn = qkv(to_native(n1[rows], act), L, pos, act)
     o = np.zeros((len(rows), H, cfg["dh"]))
     new_stored = {}
     for ri, s in enumerate(seqs):
-        khat, vhat, _, _ = decode_cache_seq(cfg, s)
-        kh1, vh1, st = store_kv(kn[ri:ri + 1], vn[ri:ri + 1], bit[s:s + 1], cfg)
+        khat, vhat, _, _ = decode_cache_seq(cfg, s, context)
+        kst, vst = (kn[ri:ri + 1], vn[ri:ri + 1]) if kv_in is None else kv_in[s]
+        kh1, vh1, st = store_kv(kst, vst, bit[s:s + 1], cfg)
         new_stored[s] = st
         khat = np.concatenate([khat, kh1], axis=0)
         vhat = np.concatenate([vhat, vh1], axis=0)
@@ -384,7 +409,8 @@ def layer_decode(L, seqs=None):
         del khat, vhat
     o = to_native(o, act)
     xt = to_native(oproj(L["x"][rows], o, L["Wo"]), act)
-    xout, n2, y = moe(xt, L, eidx[rows], egate[rows])
+    xin = xt if xt_in is None else np.asarray(xt_in, np.float64)
+    xout, n2, y = moe(xin, L, eidx[rows], egate[rows], act)
     return dict(rows=rows, n1=n1, za=za, ze=ze, zb=zb, mode=mode, bit=bit,
                 eidx=eidx, egate=egate, cmp=cmp, q=q, k=kn, v=vn,
                 stored=new_stored, o=o, xt=xt, n2=n2, y=y, xout=xout)

@@ -20,7 +20,7 @@ F32, BF16 = 0, 1
 SKIP, LOCAL, FULL = 0, 1, 2
 OP_ROUTER, OP_QKV, OP_KV_APPEND, OP_ATTN_PREFILL, OP_ATTN_DECODE, OP_MOE, \
     OP_LAYER_PREFILL, OP_LAYER_DECODE = range(8)
-CACHE_OVERFLOW = 1
+CACHE_OVERFLOW, CACHE_BAD_SEQ = 1, 2
 
 STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too small",
           -4: "cache capacity exceeded", -5: "HIP runtime error"}

@@ -471,7 +471,7 @@ int triroute_qkv(const triroute_cfg *cfg, int B, int T, const void *n1, const tr
   TRY(check_ws(*cfg, TRIROUTE_OP_QKV, B, T, ws, ws_bytes));
   Carve cv(ws);
   float *rope = carve_qkv(cv, *cfg, B * T);
-  CHECK_HIP(tr::launch_qkv(*cfg, B, T, n1, *w, pos0, nullptr, q, k, v, rope, false,
+  CHECK_HIP(tr::launch_qkv(*cfg, B, T, n1, *w, pos0, nullptr, B, q, k, v, rope, false,
                            (hipStream_t)stream),
             "qkv launch");
   return TRIROUTE_OK;
@@ -588,12 +588,13 @@ static int layer_impl(const triroute_cfg *cfg, int B, int T, bool decode, const 
     sc.used = scratch_at;
     RouterWs r = carve_router(sc, *cfg, N);
     float *rope = carve_qkv(sc, *cfg, N);
-    const tr::RopeJob job = tr::make_rope_job(*cfg, T, seq_len, seq_ids, rope);
+    const tr::RopeJob job = tr::make_rope_job(*cfg, T, seq_len, seq_ids, cache->n_seq, rope);
     CHECK_HIP(tr::launch_router(*cfg, N, x, psi, *rw, L.n1, L.mode, L.bit, L.eidx, L.egate, r.rinv,
                                 r.u, &job, st),
               "router launch");
     CHECK_HIP(tr::launch_compact(*cfg, B, T, L.mode, L.eidx, L.cmp, r.hist, st), "compaction");
-    CHECK_HIP(tr::launch_qkv(*cfg, B, T, L.n1, *dw, seq_len, seq_ids, L.q, L.k, L.v, rope, true, st),
+    CHECK_HIP(tr::launch_qkv(*cfg, B, T, L.n1, *dw, seq_len, seq_ids, cache->n_seq, L.q, L.k, L.v,
+                             rope, true, st),
               "qkv launch");
   }
   {

@@ -71,10 +71,30 @@ __device__ __forceinline__ void store8(float *p, const float *v) {
   *(float4 *)(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
 }
 
+// fp64 -> activation dtype as every tensor handed between operators is
+// rounded: to fp32 (RNE), then for bf16 to bf16 (RNE).
+__device__ __forceinline__ void store8(bf16 *p, const double *v) {
+  float f[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) f[i] = float(v[i]);
+  store8(p, f);
+}
+__device__ __forceinline__ void store8(float *p, const double *v) {
+  float f[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) f[i] = float(v[i]);
+  store8(p, f);
+}
+
 // --------------------------------------------------------- wave helpers
 constexpr int WAVE = 64;
 
 __device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, WAVE);
+  return v;
+}
+__device__ __forceinline__ double wave_sum(double v) {
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, WAVE);
   return v;

@@ -253,10 +253,11 @@ __global__ __launch_bounds__(256) void rope_table_kernel(int N, const RopeJob r)
 }
 
 RopeJob make_rope_job(const triroute_cfg &cfg, int Tq, const int32_t *pos_base,
-                      const int32_t *pos_idx, float *tab) {
+                      const int32_t *pos_idx, int n_base, float *tab) {
   RopeJob r;
   r.pos_base = pos_base;
   r.pos_idx = pos_idx;
+  r.n_base = n_base;
   r.Tq = Tq;
   r.hd = cfg.head_dim / 2;
   r.tab = (float2 *)tab;
@@ -293,10 +294,11 @@ static hipError_t qkv_t(const triroute_cfg &cfg, int B, int Tq, const void *n1,
 
 hipError_t launch_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
                       const triroute_dense_w &w, const int32_t *pos_base, const int32_t *pos_idx,
-                      void *q, void *k, void *v, float *rope, bool rope_ready, hipStream_t st) {
+                      int n_base, void *q, void *k, void *v, float *rope, bool rope_ready,
+                      hipStream_t st) {
   const int N = B * Tq;
   if (!rope_ready) {
-    const RopeJob r = make_rope_job(cfg, Tq, pos_base, pos_idx, rope);
+    const RopeJob r = make_rope_job(cfg, Tq, pos_base, pos_idx, n_base, rope);
     const int64_t n = int64_t(N) * r.hd;
     rope_table_kernel<<<dim3(unsigned((n + 255) / 256)), 256, 0, st>>>(N, r);
   }

@@ -10,21 +10,26 @@ hipError_t router_prepare();
 // trunk K split: ks chunks of kchunk inputs; the trunk partials take
 // ks * N * 128 floats of scratch
 void router_split(int N, int K, int &ks, int &kchunk);
-// Rotation table of rotate-half RoPE (paper Sec. 3.1): for token row i of a
-// [B, Tq] batch and pair j < d_h / 2, (cos, sin) of pos * theta^(-2j/d_h) at
-// pos = (pos_base ? pos_base[pos_idx ? pos_idx[b] : b] : 0) + t; the angle is
-// taken in fp64 and reduced to [-pi, pi] before an accurate fp32 sincos.
+// Rotation table of rotate-half RoPE (paper Sec. 4 Models): for token row i
+// of a [B, Tq] batch and pair j < d_h / 2, (cos, sin) of pos * theta^(-2j/d_h)
+// at pos = base + t, base = pos_base[s] with s = pos_idx ? pos_idx[b] : b when
+// 0 <= s < n_base, else 0 (a row naming no valid sequence is dropped by the
+// append, which flags it; its table entries only need to be finite); the
+// angle is taken in fp64 and reduced to [-pi, pi] before an accurate fp32
+// sincos.
 struct RopeJob {
   const int32_t *pos_base, *pos_idx;
+  int n_base;  // entries of pos_base
   int Tq, hd;
   float2 *tab;  // [N][hd]
   double inv_freq[64];
 };
 RopeJob make_rope_job(const triroute_cfg &cfg, int Tq, const int32_t *pos_base,
-                      const int32_t *pos_idx, float *tab);
+                      const int32_t *pos_idx, int n_base, float *tab);
 __device__ __forceinline__ float2 rope_entry(const RopeJob &r, int row, int j) {
   const int b = row / r.Tq, tt = row - b * r.Tq;
-  const int pos = (r.pos_base ? r.pos_base[r.pos_idx ? r.pos_idx[b] : b] : 0) + tt;
+  const int s = r.pos_idx ? r.pos_idx[b] : b;
+  const int pos = (r.pos_base && s >= 0 && s < r.n_base ? r.pos_base[s] : 0) + tt;
   const double ang = double(pos) * r.inv_freq[j];
   const double kq = rint(ang * 0.15915494309189535);
   double rr = fma(-kq, 6.283185307179586, ang);
@@ -59,12 +64,13 @@ hipError_t launch_kv_export(const triroute_cfg &cfg, const CacheView &cv, int se
                             int slot0, int count, void *kout, void *vout, uint16_t *ksz,
                             uint16_t *vsz, int32_t *pos_out, hipStream_t st);
 // gemm.hip
-// position of token (b, t) = (pos_base ? pos_base[pos_idx ? pos_idx[b] : b] : 0) + t;
+// position of token (b, t) as in RopeJob (pos_base has n_base entries);
 // rope: scratch of qkv_rope_floats(cfg, B * Tq) floats (the rotation table)
 size_t qkv_rope_floats(const triroute_cfg &cfg, int N);
 hipError_t launch_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
                       const triroute_dense_w &w, const int32_t *pos_base, const int32_t *pos_idx,
-                      void *q, void *k, void *v, float *rope, bool rope_ready, hipStream_t st);
+                      int n_base, void *q, void *k, void *v, float *rope, bool rope_ready,
+                      hipStream_t st);
 hipError_t launch_oproj(const triroute_cfg &cfg, int N, const void *x, const void *o,
                         const triroute_dense_w &w, void *xt, hipStream_t st);
 hipError_t launch_moe_gemms(const triroute_cfg &cfg, int N, const void *n2,

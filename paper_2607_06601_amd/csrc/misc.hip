@@ -11,7 +11,11 @@ namespace tr {
 
 // One wave per list entry pos (8 consecutive elements per lane access,
 // d % 64 == 0): token a / k of assignment a = rows[pos], normalised, to row
-// pos; slot_of[a] = pos.  Entries past the lists' total do nothing.
+// pos; slot_of[a] = pos.  Entries past the lists' total do nothing.  The
+// norm is evaluated in fp64 (sum of squares, scale, products) and rounded
+// once to the activation dtype, so n2 is the correctly rounded value of the
+// exact norm: a last-place difference in n2 would otherwise move the expert
+// output by far more than its own size.
 template <typename T>
 __global__ __launch_bounds__(256) void moe_norm_rows_kernel(
     const T *__restrict__ x, const T *__restrict__ g, const int32_t *__restrict__ rows,
@@ -25,7 +29,7 @@ __global__ __launch_bounds__(256) void moe_norm_rows_kernel(
   // rows of up to 1024 elements stay in registers between the two passes
   constexpr int RR = 2;
   float v[RR][8];
-  float ss = 0.f;
+  double ss = 0.0;
   if (d <= 512 * RR) {
 #pragma unroll
     for (int q = 0; q < RR; ++q) {
@@ -33,7 +37,7 @@ __global__ __launch_bounds__(256) void moe_norm_rows_kernel(
       if (c < d) {
         load8(xr + c, v[q]);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) ss = fmaf(v[q][i], v[q][i], ss);
+        for (int i = 0; i < 8; ++i) ss = fma(double(v[q][i]), double(v[q][i]), ss);
       }
     }
   } else {
@@ -41,11 +45,11 @@ __global__ __launch_bounds__(256) void moe_norm_rows_kernel(
       float w[8];
       load8(xr + c, w);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) ss = fmaf(w[i], w[i], ss);
+      for (int i = 0; i < 8; ++i) ss = fma(double(w[i]), double(w[i]), ss);
     }
   }
   ss = wave_sum(ss);
-  const float r = 1.0f / sqrtf(ss / float(d) + eps);
+  const double r = 1.0 / sqrt(ss / double(d) + double(eps));
   T *orow = out + int64_t(pos) * d;
   if (d <= 512 * RR) {
 #pragma unroll
@@ -53,20 +57,22 @@ __global__ __launch_bounds__(256) void moe_norm_rows_kernel(
       const int c = lane * 8 + 512 * q;
       if (c < d) {
         float gv[8];
+        double o[8];
         load8(g + c, gv);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) v[q][i] = (v[q][i] * r) * gv[i];
-        store8(orow + c, v[q]);
+        for (int i = 0; i < 8; ++i) o[i] = (double(v[q][i]) * r) * double(gv[i]);
+        store8(orow + c, o);
       }
     }
   } else {
     for (int c = lane * 8; c < d; c += 512) {
       float w[8], gv[8];
+      double o[8];
       load8(xr + c, w);
       load8(g + c, gv);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) w[i] = (w[i] * r) * gv[i];
-      store8(orow + c, w);
+      for (int i = 0; i < 8; ++i) o[i] = (double(w[i]) * r) * double(gv[i]);
+      store8(orow + c, o);
     }
   }
   if (lane == 0) slot_of[a] = pos;

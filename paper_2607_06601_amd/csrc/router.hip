@@ -1,7 +1,7 @@
 // Controller (paper Sec. 3.3 controller equation) and hard inference
 // decisions (Sec. 3.8), fp32 end to end.
 //
-//   rms_norm1   : r_i = 1/sqrt(mean(x_i^2) + eps); n1 = x r g1 (act out, for QKV)
+//   rms_norm1   : r_i = 1/sqrt(mean(x_i^2) + eps); n1 = x r g1 (act out, for QKV; fp64)
 //   trunk1      : partial W1 [x r g1 ; psi] over K chunks    fp32 MFMA, N x 128
 //   tail        : u = GELU(sum + b1), h = W2 u + b2, h^ = RMSNorm(h) gr,
 //                 z = W_{a,e,b} h^ + c, argmax / top-k decisions and gates
@@ -22,25 +22,34 @@ __global__ __launch_bounds__(256) void rms_norm1_kernel(const T *__restrict__ x,
   if (rj.tab)  // the token's rotation table entries (one lane per pair)
     for (int j = lane; j < rj.hd; j += 64) rj.tab[int64_t(row) * rj.hd + j] = rope_entry(rj, row, j);
   const T *xr = x + int64_t(row) * d;
+  // fp32 scale for the controller (fp32 end to end); fp64 for the n1 the
+  // projections read, rounded once to the activation dtype
   float ss = 0.f;
+  double sd = 0.0;
   for (int c = lane * 8; c < d; c += 512) {
     float v[8];
     load8(xr + c, v);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) ss = fmaf(v[i], v[i], ss);
+    for (int i = 0; i < 8; ++i) {
+      ss = fmaf(v[i], v[i], ss);
+      sd = fma(double(v[i]), double(v[i]), sd);
+    }
   }
   ss = wave_sum(ss);
   float r = 1.0f / sqrtf(ss / float(d) + eps);
   if (lane == 0) rinv[row] = r;
   if (n1) {
+    sd = wave_sum(sd);
+    const double rd = 1.0 / sqrt(sd / double(d) + double(eps));
     T *nr = n1 + int64_t(row) * d;
     for (int c = lane * 8; c < d; c += 512) {
       float v[8], gv[8];
+      double o[8];
       load8(xr + c, v);
       load8(g + c, gv);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = (v[i] * r) * gv[i];
-      store8(nr + c, v);
+      for (int i = 0; i < 8; ++i) o[i] = (double(v[i]) * rd) * double(gv[i]);
+      store8(nr + c, o);
     }
   }
 }

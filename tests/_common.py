@@ -13,29 +13,69 @@ from oracle.ties import enforce_margins
 BF16_ATOL, BF16_RTOL = 2e-3, 1e-2
 F32_RTOL = 1e-5
 
+# (test, tensor, max err/bound) of every tolerance check, printed in the
+# terminal summary (tests/conftest.py) so that a passing run shows its margins
+MARGINS = []
+
+# Largest x_out err/bound between the oracle with every inter-operator tensor
+# held in the activation dtype and the same oracle in fp64 throughout, per
+# workload, rounded up from test_oracle_pins.test_activation_rounding_spread
+# (which asserts the measured value stays below it).  Any implementation that
+# stores those tensors in bf16 lies within about this spread of the fp64
+# computation, so an unforced end-to-end comparison is held to 1 + 2x it.
+ROUNDING_SPREAD = {"tiny_f32_prefill": 0.05, "160m_bf16_prefill": 2.5,
+                   "410m_bf16_decode": 2.0, "1p3b_bf16_prefill": 8.0,
+                   "1p3b_bf16_decode": 4.0}
+
 
 def npy(t):
     return t.detach().float().cpu().numpy() if t.dtype in (torch.bfloat16, torch.float16) \
         else t.detach().cpu().numpy()
 
 
-def assert_close(gpu, ref, act, name=""):
+def bound_of(ref, act):
+    """Elementwise tolerance: bf16 |d| <= 2e-3 + 1e-2 |ref|; fp32
+    |d| <= 1e-5 (|ref| + rms(ref))."""
+    ref = np.asarray(ref, np.float64)
+    if act == "bf16":
+        return BF16_ATOL + BF16_RTOL * np.abs(ref)
+    rms = np.sqrt(np.mean(ref ** 2)) if ref.size else 0.0
+    return F32_RTOL * (np.abs(ref) + rms)
+
+
+def err_ratio(gpu, ref, act):
+    """max |gpu - ref| / bound (0 for empty inputs)."""
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if not ref.size:
+        return 0.0
+    return float((np.abs(gpu - ref) / bound_of(ref, act)).max())
+
+
+def note(name, ratio):
+    import os
+    MARGINS.append((os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0], name, ratio))
+
+
+def assert_close(gpu, ref, act, name="", factor=1.0):
+    """Elementwise tolerance check (``factor`` x the bound); records the margin."""
     gpu = np.asarray(gpu, np.float64)
     ref = np.asarray(ref, np.float64)
     assert gpu.shape == ref.shape, (name, gpu.shape, ref.shape)
+    if not ref.size:
+        return 0.0
     err = np.abs(gpu - ref)
-    if act == "bf16":
-        bound = BF16_ATOL + BF16_RTOL * np.abs(ref)
-    else:
-        rms = np.sqrt(np.mean(ref ** 2)) if ref.size else 0.0
-        bound = F32_RTOL * (np.abs(ref) + rms)
+    bound = factor * bound_of(ref, act)
+    ratio = float((err / bound).max())
+    note(name + (f" (x{factor:g} bound)" if factor != 1.0 else ""), ratio)
     bad = err > bound
     if bad.any():
         i = np.unravel_index(np.argmax(err - bound), err.shape)
         raise AssertionError(
-            f"{name}: {int(bad.sum())}/{bad.size} outside tolerance ({act}); worst at {i}: "
-            f"gpu {gpu[i]!r} ref {ref[i]!r}; max abs err {err.max():.3e}")
-    return float(err.max()) if err.size else 0.0
+            f"{name}: {int(bad.sum())}/{bad.size} outside {factor:g}x tolerance ({act}); worst at "
+            f"{i}: gpu {gpu[i]!r} ref {ref[i]!r}; max abs err {err.max():.3e}; "
+            f"max err/bound {ratio:.3f}")
+    return ratio
 
 
 def layer(name, seed=None, moe=True, act=None):

@@ -1,12 +1,30 @@
 """End-to-end parity of the composite layer calls against the CPU oracle.
 
-Full workload sizes run on the GPU exactly as the benchmark launches them;
-the oracle evaluates a sample of rows (or sequences) one by one.  Routing
-decisions are compared for every token, bit for bit.  KV codes inside the
-layer are compared only as a diagnostic: the K the GPU quantizes comes from
-its own bf16 projection, which can differ from the oracle's rounding of the
-fp64 projection in the last bit (the codes themselves are pinned bit-exact at
-the append boundary in test_gpu_stages)."""
+The GPU runs every workload at full size, launched as the benchmark launches
+it.  The comparison follows the protocol that makes every result well defined
+(paper Sec. 3.2 (C) quantizer, Sec. 3.8 hard decisions):
+
+1. routing decisions: bit exact for every token;
+2. q, k, v (the GPU's stored projections): within the tolerance of the
+   oracle's own projections;
+3. the GPU's cache: codes, fp16 scale/zero and positions bit exact against
+   the oracle's quantizer applied to the K/V tensor the GPU appended (its
+   own k, v), every token of every compared sequence; a decode workload's
+   whole pre-existing context bit exact against the oracle's quantizer of
+   the generator's context (identical inputs);
+4. discretely forced continuous outputs: the oracle attends over the cache
+   its own quantizer builds from that k, v (so both sides read the same
+   codes: a bf16 K that legitimately differs from the oracle's in its last
+   bit can move a code by a whole quantization step) and recomputes o and x~
+   in fp64 from the original inputs; its expert block takes the GPU's x~
+   (just verified within tolerance: both sides hold x~ in bf16 and may round
+   an element differently) and recomputes n2, the experts and x_out.  o, x~
+   and x_out are held to the stated tolerance;
+5. unforced: the GPU's x_out against the fully independent oracle, within
+   1 + 2 x the spread that bf16 storage of the inter-operator tensors alone
+   causes (measured on the CPU by test_activation_rounding_spread).
+
+Every max err/bound is recorded and printed in the terminal summary."""
 import numpy as np
 import pytest
 import torch
@@ -16,7 +34,7 @@ import oracle
 import paper_2607_06601_amd as tr
 from paper_2607_06601_amd.device import DeviceLayer, to_dev
 
-from _common import assert_close, layer, npy
+from _common import ROUNDING_SPREAD, assert_close, layer, note, npy
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -40,94 +58,65 @@ def _taps(cfg, N, act_t):
     return t, s
 
 
-LOOSE = 8.0   # bound multiplier for outputs downstream of a differing cache entry
-LOOSE_ROW = 3.0  # for x~ / x_out rows whose input differs from the oracle's in a bf16 bit
+def export_pool(c, cache, s, bi, n, act, Hkv, dh, G):
+    tdt = torch.bfloat16 if act == "bf16" else torch.float32
+    dt = torch.uint8 if bi < 3 else tdt
+    ko = torch.zeros(n, Hkv, dh, dtype=dt, device=DEV)
+    vo = torch.zeros_like(ko)
+    ks = torch.zeros(n, Hkv, dh // G, 2, dtype=torch.int16, device=DEV)
+    vs = torch.zeros_like(ks)
+    pos = torch.zeros(n, dtype=torch.int32, device=DEV)
+    tr.kv_export(c, cache, s, bi, 0, n, ko, vo, ks, vs, pos)
+    torch.cuda.synchronize()
+    return npy(ko), npy(vo), npy(ks), npy(vs), npy(pos)
 
 
-def _cache_diff(c, cache, cfg, r, seqs, only_last=False):
-    """Per sequence, a bool [n_positions, Hkv]: the quantized cache entry of
-    that token / kv head (codes or fp16 scale/zero, K or V) differs between
-    the GPU's cache and the oracle's.  Each side quantized its own K/V, which
-    may legitimately differ in the last bf16 bit (fp32 versus fp64
-    accumulation); such a bit can move a code.  16-bit entries are not
-    flagged: a last-bit difference there is covered by the tolerance."""
-    from test_gpu_stages import export_pool
+def _f16_bits(a):
+    return np.asarray(a).astype(np.int16).view(np.uint16)
+
+
+def check_pool(c, cache, cfg, s, bi, ent, positions, first=0):
+    """The slots [first, first + n) of pool (s, bi) hold, bit for bit, the
+    oracle's quantization `ent` (store_kv's entry for that width) of the
+    tokens at `positions`."""
     Hkv, dh, G, act = cfg["Hkv"], cfg["dh"], cfg["G"], cfg["act"]
-    out = {}
-    for s_ in seqs:
-        st = r["stored"][s_]
-        npos = 1 if only_last else cfg["T"]
-        d = np.zeros((npos, Hkv), bool)
-        plen = npy(cache.pool_len())[s_]
-        for bi, ent in st.items():
-            if bi == 3:
-                continue
-            n = len(ent["tokens"])
-            first = int(plen[bi]) - n            # the oracle's tokens are the pool's last n
-            ko, vo, ks, vs, _ = export_pool(c, cache, s_, bi, int(plen[bi]), act, Hkv, dh, G)
-            sl = slice(first, first + n)
-            kc, vc = npy(ko)[sl], npy(vo)[sl]
-            ksz = npy(ks)[sl].astype(np.int16).view(np.float16)
-            vsz = npy(vs)[sl].astype(np.int16).view(np.float16)
-            diff = (kc != ent["kc"]).any(-1) | (vc != ent["vc"]).any(-1)
-            diff |= (ksz[..., 0] != ent["ks"]).any(-1) | (ksz[..., 1] != ent["kz"]).any(-1)
-            diff |= (vsz[..., 0] != ent["vs"]).any(-1) | (vsz[..., 1] != ent["vz"]).any(-1)
-            idx = np.zeros(n, int) if only_last else ent["tokens"]
-            d[idx] |= diff
-        out[s_] = d
-    return out
+    n = len(ent["tokens"])
+    ko, vo, ks, vs, pos = export_pool(c, cache, s, bi, first + n, act, Hkv, dh, G)
+    sl = slice(first, first + n)
+    np.testing.assert_array_equal(pos[sl], positions)
+    if bi == 3:
+        np.testing.assert_array_equal(ko[sl].astype(np.float32), np.asarray(ent["kc"], np.float32))
+        np.testing.assert_array_equal(vo[sl].astype(np.float32), np.asarray(ent["vc"], np.float32))
+        return
+    np.testing.assert_array_equal(ko[sl], ent["kc"])
+    np.testing.assert_array_equal(vo[sl], ent["vc"])
+    np.testing.assert_array_equal(_f16_bits(ks[sl][..., 0]), ent["ks"].view(np.uint16))
+    np.testing.assert_array_equal(_f16_bits(ks[sl][..., 1]), ent["kz"].view(np.uint16))
+    np.testing.assert_array_equal(_f16_bits(vs[sl][..., 0]), ent["vs"].view(np.uint16))
+    np.testing.assert_array_equal(_f16_bits(vs[sl][..., 1]), ent["vz"].view(np.uint16))
 
 
-def _tainted(cfg, mode, rows, seq_of, qpos_of, diff, first_pos=0):
-    """(row, head) pairs whose key range holds a differing cache entry."""
-    H, Hkv, w = cfg["H"], cfg["Hkv"], cfg["w"]
-    grp = H // Hkv
-    taint = np.zeros((len(rows), H), bool)
-    for ri, row in enumerate(rows):
-        b, P = seq_of(row), qpos_of(row)
-        for h in range(H):
-            m = int(mode[row, h])
-            if m == 0:
-                continue
-            lo = max(0, P - w + 1) if m == 1 else 0
-            keys = diff[b][max(lo - first_pos, 0):P - first_pos + 1, h // grp]
-            taint[ri, h] = bool(keys.any())
-    return taint
+def _codes_differ(own, forced):
+    """Fraction of (token, kv head) cache entries whose codes or scale/zero
+    differ between the oracle's quantization of its own K/V and of the GPU's."""
+    tot = dif = 0
+    for bi, a in own.items():
+        if bi == 3:
+            continue
+        b = forced[bi]
+        d = (a["kc"] != b["kc"]).any(-1) | (a["vc"] != b["vc"]).any(-1)
+        for key in ("ks", "kz", "vs", "vz"):
+            d |= (a[key].view(np.uint16) != b[key].view(np.uint16)).any(-1)
+        dif += int(d.sum())
+        tot += d.size
+    return dif / max(tot, 1)
 
 
-def _assert_split(gpu, ref, taint_rows, act, name, loose=LOOSE):
-    """Strict tolerance on untainted entries, `loose` x tolerance on the rest."""
-    from _common import BF16_ATOL, BF16_RTOL
-    ok = ~taint_rows
-    if ok.any():
-        assert_close(gpu[ok], ref[ok], act, name)
-    if (~ok).any():
-        err = np.abs(gpu[~ok] - ref[~ok])
-        bound = loose * (BF16_ATOL + BF16_RTOL * np.abs(ref[~ok]))
-        assert (err <= bound).all(), f"{name} (tainted): max abs err {err.max():.3e}"
-
-
-def _row_bits_differ(gpu, ref, act):
-    """Rows where the GPU's stored activation differs from the oracle's
-    rounding of the same quantity in at least one element (both are correct
-    roundings of nearly equal values; the expert block amplifies such a bit,
-    see test_oracle_pins.test_expert_block_sensitivity_to_one_bit)."""
-    if act != "bf16":
-        return np.zeros(len(gpu), bool)
-    return (np.asarray(gpu, np.float32) != np.asarray(ref, np.float32)).any(axis=1)
-
-
-def _check_chain(t, xo, r, rows, taint, act):
-    H = taint.shape[1]
-    og = npy(t["o"])[rows]
-    _assert_split(og.reshape(len(rows), H, -1), r["o"].reshape(len(rows), H, -1), taint, act, "o")
-    trow = taint.any(axis=1)
-    xt_rows = trow | _row_bits_differ(og, r["o"].reshape(len(rows), -1), act)
-    _assert_split(npy(t["xt"])[rows], r["xt"], xt_rows, act, "xt", LOOSE_ROW)
-    xo_rows = xt_rows | _row_bits_differ(npy(t["xt"])[rows], r["xt"], act)
-    print(f"rows held to the {LOOSE_ROW}x bound: x~ {int(xt_rows.sum())}, x_out {int(xo_rows.sum())}"
-          f" of {len(rows)}")
-    _assert_split(npy(xo)[rows], r["xout"], xo_rows, act, "x_out", LOOSE_ROW)
+def _check_decisions(t, r):
+    np.testing.assert_array_equal(npy(t["mode"]), r["mode"])
+    np.testing.assert_array_equal(npy(t["bit"]), r["bit"])
+    np.testing.assert_array_equal(npy(t["eidx"]), r["eidx"])
+    np.testing.assert_allclose(npy(t["egate"]), r["egate"], rtol=2e-5, atol=1e-6)
 
 
 def run_prefill(L, D=None):
@@ -143,49 +132,59 @@ def run_prefill(L, D=None):
     tr.layer_prefill(c, B, T, D.x, D.psi, D.rw, D.dw, D.mw, cache, xo, ws, taps=s)
     torch.cuda.synchronize()
     assert cache.status() == 0
-    return xo, t, cache
+    return xo, t, cache, c
 
 
-def _check_decisions(t, r):
-    np.testing.assert_array_equal(npy(t["mode"]), r["mode"])
-    np.testing.assert_array_equal(npy(t["bit"]), r["bit"])
-    np.testing.assert_array_equal(npy(t["eidx"]), r["eidx"])
-    np.testing.assert_allclose(npy(t["egate"]), r["egate"], rtol=2e-5, atol=1e-6)
+# (workload, seed, sequences compared whole: None = all)
+PREFILL_CASES = [("tiny_f32_prefill", 0, None), ("160m_bf16_prefill", 1, None),
+                 ("1p3b_bf16_prefill", 104, "first_last")]
 
 
-@pytest.mark.parametrize("name,seed,nrows", [("tiny_f32_prefill", 0, None),
-                                             ("160m_bf16_prefill", 1, 40),
-                                             ("1p3b_bf16_prefill", 104, 24)])
-def test_layer_prefill(name, seed, nrows):
+@pytest.mark.parametrize("name,seed,which", PREFILL_CASES)
+def test_layer_prefill(name, seed, which):
     L = layer(name, seed)
     cfg = L["cfg"]
-    N = cfg["B"] * cfg["T"]
-    xo, t, cache = run_prefill(L)
-    if nrows is None:
-        rows = np.arange(N)
-    else:
-        rows = np.sort(gen.stream(seed, "rows").choice(N, nrows, replace=False))
-        rows[0], rows[-1] = 0, N - 1                   # first and last token of the batch
-        rows = np.unique(rows)
-    r = oracle.layer_prefill(L, rows)
-    _check_decisions(t, r)
-    act = cfg["act"]
-    T, H, dh = cfg["T"], cfg["H"], cfg["dh"]
-    D_cfg = DeviceLayer.cfg_only(L)
-    diff = _cache_diff(D_cfg, cache, cfg, r, sorted(r["stored"]))
-    frac = np.mean([d.mean() for d in diff.values()])
-    taint = _tainted(cfg, npy(t["mode"]), rows, lambda row: row // T, lambda row: row % T, diff)
-    print(f"{name}: quantized cache entries differing: {frac:.2e}; "
-          f"tainted (row, head) pairs: {int(taint.sum())}/{taint.size}")
-    assert frac < 1e-2
-    _check_chain(t, xo, r, rows, taint, act)
+    act, B, T, H, Hkv, dh = (cfg[x] for x in ("act", "B", "T", "H", "Hkv", "dh"))
+    xo, t, cache, c = run_prefill(L)
+    seqs = list(range(B)) if which is None else sorted({0, B - 1})
+    rows = np.concatenate([np.arange(b * T, (b + 1) * T) for b in seqs])
+    # 1-2: decisions for every token, projections of the compared sequences;
+    # the independent oracle's expert block on a sample of rows (step 5)
+    sample = rows if which is None else np.unique(np.concatenate(
+        [rows[:128], rows[-128:], gen.stream(seed, "rows").choice(rows, 256, replace=False)]))
+    r0 = oracle.layer_prefill(L, sample)
+    _check_decisions(t, r0)
+    gq, gk, gv = npy(t["q"]), npy(t["k"]), npy(t["v"])
+    kv_in = {}
+    for b in seqs:
+        sl = slice(b * T, (b + 1) * T)
+        assert_close(gq[sl], r0["q"][b].reshape(T, -1), act, "q")
+        assert_close(gk[sl], r0["k"][b].reshape(T, -1), act, "k")
+        assert_close(gv[sl], r0["v"][b].reshape(T, -1), act, "v")
+        kv_in[b] = (gk[sl].reshape(T, Hkv, dh), gv[sl].reshape(T, Hkv, dh))
+    # 3-4: the forced chain over every row of the compared sequences
+    gxt = npy(t["xt"])
+    r1 = oracle.layer_prefill(L, rows, kv_in=kv_in, xt_in=gxt[rows])
+    flips = []
+    for b in seqs:
+        for bi, ent in r1["stored"][b].items():
+            check_pool(c, cache, cfg, b, bi, ent, ent["tokens"])
+        flips.append(_codes_differ(r0["stored"][b], r1["stored"][b]))
+    note("cache entries moved by a last-bit K/V difference (fraction)", float(np.mean(flips)))
+    assert np.mean(flips) < 1e-2
+    assert_close(npy(t["o"])[rows], r1["o"].reshape(len(rows), -1), act, "o (forced codes)")
+    assert_close(gxt[rows], r1["xt"], act, "x~ (forced codes)")
+    assert_close(npy(xo)[rows], r1["xout"], act, "x_out (forced x~)")
+    # 5: unforced
+    f = 1.0 + 2.0 * ROUNDING_SPREAD[name]
+    assert_close(npy(xo)[sample], r0["xout"], act, "x_out (unforced)", factor=f)
 
 
 def test_layer_prefill_deterministic():
     L = layer("160m_bf16_prefill", 2)
     D = DeviceLayer(L)
-    a, _, _ = run_prefill(L, D)
-    b, _, _ = run_prefill(L, D)
+    a = run_prefill(L, D)[0]
+    b = run_prefill(L, D)[0]
     assert torch.equal(a, b)
 
 
@@ -194,13 +193,15 @@ def test_skip_and_null_tokens_keep_the_residual_on_device():
     H, E = L["cfg"]["H"], L["cfg"]["E"]
     L["ca"] = np.tile(np.array([50.0, -50.0, -50.0], np.float32), H)
     L["ce"] = np.array([50.0] + [-50.0] * E, np.float32)
-    xo, t, _ = run_prefill(L)
+    xo, t, _, _ = run_prefill(L)
     assert (npy(t["mode"]) == 0).all() and (npy(t["eidx"]) == 0).all()
     np.testing.assert_array_equal(npy(t["xt"]), L["x"])
     np.testing.assert_array_equal(npy(xo), L["x"])
 
 
 def fill_context(c, cache, cfg, act_t):
+    """The decode workload's pre-existing context, appended one whole
+    sequence per call (the benchmark's fill)."""
     ctx = cfg["ctx"]
     ws = tr.workspace(c, tr.OP_KV_APPEND, 1, ctx)
     for s in range(cfg["B"]):
@@ -212,13 +213,13 @@ def fill_context(c, cache, cfg, act_t):
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("name,nseq", [("410m_bf16_decode", 4), ("1p3b_bf16_decode", 3)])
+@pytest.mark.parametrize("name,nseq", [("410m_bf16_decode", 12), ("1p3b_bf16_decode", 4)])
 def test_layer_decode(name, nseq):
     L = layer(name)
     cfg = L["cfg"]
     D = DeviceLayer(L)
     c = D.cfg
-    B, ctx = cfg["B"], cfg["ctx"]
+    act, B, ctx, Hkv, dh = (cfg[x] for x in ("act", "B", "ctx", "Hkv", "dh"))
     cache = tr.KVCache(c, B, ctx + 16)
     fill_context(c, cache, cfg, D.act)
     assert cache.status() == 0
@@ -227,16 +228,34 @@ def test_layer_decode(name, nseq):
     tr.layer_decode(c, B, D.x, D.psi, D.rw, D.dw, D.mw, cache, xo,
                     tr.workspace(c, tr.OP_LAYER_DECODE, B, 1), taps=s)
     torch.cuda.synchronize()
+    assert cache.status() == 0
     np.testing.assert_array_equal(npy(cache.seq_len()), ctx + 1)
-    seqs = np.unique(np.concatenate([[0, B - 1], gen.stream(cfg["seed"], "seqs").choice(B, nseq)]))
-    r = oracle.layer_decode(L, seqs)
-    _check_decisions(t, r)
-    act = cfg["act"]
-    H, dh = cfg["H"], cfg["dh"]
-    diff = _cache_diff(c, cache, cfg, r, [int(x) for x in seqs], only_last=True)
-    taint = _tainted(cfg, npy(t["mode"]), [int(x) for x in seqs], lambda row: row,
-                     lambda row: ctx, diff, first_pos=ctx)
-    print(f"{name}: new tokens with a differing quantized cache entry: "
-          f"{sum(int(d.any()) for d in diff.values())}/{len(diff)}; "
-          f"tainted (seq, head) pairs: {int(taint.sum())}/{taint.size}")
-    _check_chain(t, xo, r, seqs, taint, act)
+    seqs = np.unique(np.concatenate(
+        [[0, B - 1], gen.stream(cfg["seed"], "seqs").choice(B, nseq, replace=False)]))
+    seqs = [int(x) for x in seqs]
+    r0 = oracle.layer_decode(L, seqs)
+    _check_decisions(t, r0)
+    gq, gk, gv = npy(t["q"])[seqs], npy(t["k"])[seqs], npy(t["v"])[seqs]
+    assert_close(gq, r0["q"].reshape(len(seqs), -1), act, "q")
+    assert_close(gk, r0["k"].reshape(len(seqs), -1), act, "k")
+    assert_close(gv, r0["v"].reshape(len(seqs), -1), act, "v")
+    kv_in = {s_: (gk[i].reshape(1, Hkv, dh), gv[i].reshape(1, Hkv, dh))
+             for i, s_ in enumerate(seqs)}
+    gxt = npy(t["xt"])[seqs]
+    r1 = oracle.layer_decode(L, seqs, kv_in=kv_in, xt_in=gxt)
+    bits_new = npy(t["bit"])
+    for s_ in seqs:
+        # the whole context fill, then the step's own token at the end of its pool
+        _, _, stored, bits = oracle.decode_cache_seq(cfg, s_)
+        for bi, ent in stored.items():
+            check_pool(c, cache, cfg, s_, bi, ent, ent["tokens"])
+        bi = int(bits_new[s_])
+        first = int((bits == bi).sum())
+        check_pool(c, cache, cfg, s_, bi, r1["stored"][s_][bi], [ctx], first=first)
+    note("new tokens whose cache entry a last-bit K/V difference moved (fraction)",
+         float(np.mean([_codes_differ(r0["stored"][s_], r1["stored"][s_]) for s_ in seqs])))
+    assert_close(npy(t["o"])[seqs], r1["o"].reshape(len(seqs), -1), act, "o (forced codes)")
+    assert_close(gxt, r1["xt"], act, "x~ (forced codes)")
+    assert_close(npy(xo)[seqs], r1["xout"], act, "x_out (forced x~)")
+    f = 1.0 + 2.0 * ROUNDING_SPREAD[name]
+    assert_close(npy(xo)[seqs], r0["xout"], act, "x_out (unforced)", factor=f)

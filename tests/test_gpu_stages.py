@@ -14,7 +14,7 @@ import paper_2607_06601_amd as tr
 from oracle import quant
 from paper_2607_06601_amd.device import DeviceLayer, cfg_from, to_dev
 
-from _common import assert_close, layer, npy, shape_of, torch_act
+from _common import assert_close, layer, note, npy, shape_of, torch_act
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -403,3 +403,181 @@ def test_kv_reset_and_reuse_overwrites_slots():
                 np.testing.assert_array_equal(npy(out).astype(np.float32), src[toks])
             else:
                 np.testing.assert_array_equal(npy(out), quant.quantize(src[toks], nb, G)[0])
+
+
+# ----------------------------------------- single-token appends (decode)
+@pytest.mark.parametrize("act,dh,G,Hkv", [("bf16", 64, 64, 4), ("bf16", 128, 64, 4),
+                                          ("bf16", 64, 32, 2), ("f32", 64, 32, 1)])
+def test_kv_append_one_token_rows_bit_exact(act, dh, G, Hkv):
+    """The decode append (one token per row, 2/4-bit V codes set in words
+    shared with earlier slots): 64 rows with different starting lengths,
+    then 40 one-token appends; every slot of every pool equals the oracle's
+    quantization of the token it holds (paper Sec. 3.2 (C))."""
+    B, steps = 64, 40
+    c = kv_cfg(act, dh, G, Hkv)
+    tdt = torch_act(act)
+    start = np.array([(7 * r) % 37 for r in range(B)])
+    total = start + steps
+    k, v = gen.kv_block(16, B * int(total.max()), Hkv, dh, act, std=0.9)
+    k = k.reshape(B, -1, Hkv, dh)
+    v = v.reshape(B, -1, Hkv, dh)
+    bits = gen.stream(16, "kvbits1").integers(0, 4, (B, int(total.max()))).astype(np.uint8)
+    cache = tr.KVCache(c, B + 2, int(total.max()) + 8)
+    seq_of = gen.stream(16, "seqperm").permutation(B + 2)[:B].astype(np.int32)
+    for r in range(B):          # starting lengths, one row per call
+        n = int(start[r])
+        if n == 0:
+            continue
+        tr.kv_append(c, cache, 1, n, to_dev(k[r, :n].reshape(n, -1), tdt),
+                     to_dev(v[r, :n].reshape(n, -1), tdt), to_dev(bits[r, :n], torch.uint8),
+                     tr.workspace(c, tr.OP_KV_APPEND, 1, n),
+                     seq_ids=to_dev(seq_of[r:r + 1], torch.int32))
+    sid = to_dev(seq_of, torch.int32)
+    ws = tr.workspace(c, tr.OP_KV_APPEND, B, 1)
+    for j in range(steps):      # one new token per row, at each row's own position
+        t_idx = start + j
+        kd = to_dev(k[np.arange(B), t_idx].reshape(B, -1), tdt)
+        vd = to_dev(v[np.arange(B), t_idx].reshape(B, -1), tdt)
+        bd = to_dev(bits[np.arange(B), t_idx], torch.uint8)
+        tr.kv_append(c, cache, B, 1, kd, vd, bd, ws, seq_ids=sid)
+    torch.cuda.synchronize()
+    assert cache.status() == 0
+    np.testing.assert_array_equal(npy(cache.seq_len())[seq_of], total)
+    for r in range(B):
+        s_ = int(seq_of[r])
+        n = int(total[r])
+        for bi, nb in enumerate(quant.BITS):
+            toks = np.flatnonzero(bits[r, :n] == bi)
+            assert int(npy(cache.pool_len())[s_, bi]) == len(toks)
+            if len(toks) == 0:
+                continue
+            ko, vo, ks, vs, pos = export_pool(c, cache, s_, bi, len(toks), act, Hkv, dh, G)
+            np.testing.assert_array_equal(npy(pos), toks)
+            for src, out, sz in ((k, ko, ks), (v, vo, vs)):
+                x = src[r, toks]
+                if nb == 16:
+                    np.testing.assert_array_equal(npy(out).astype(np.float32), x)
+                    continue
+                codes, s16, z16 = quant.quantize(x, nb, G)
+                np.testing.assert_array_equal(npy(out), codes)
+                szn = npy(sz)
+                np.testing.assert_array_equal(_f16(szn[..., 0]).view(np.uint16), s16.view(np.uint16))
+                np.testing.assert_array_equal(_f16(szn[..., 1]).view(np.uint16), z16.view(np.uint16))
+
+
+def test_layer_prefill_bad_sequence_id_is_flagged():
+    """A row naming a sequence outside the cache is dropped by the append,
+    sets TRIROUTE_CACHE_BAD_SEQ, and reads no position out of bounds: its
+    outputs stay finite and the other rows are unaffected."""
+    L = layer("tiny_f32_prefill", 0)
+    L["cfg"]["B"], L["cfg"]["T"] = 2, 64
+    L["x"] = np.concatenate([L["x"][:64], L["x"][64:128]])
+    D = DeviceLayer(L)
+    c = D.cfg
+    cache = tr.KVCache(c, 2, 64)
+    xo = torch.empty(128, L["cfg"]["d"], dtype=D.act, device=DEV)
+    ws = tr.workspace(c, tr.OP_LAYER_PREFILL, 2, 64)
+    sid = torch.tensor([0, 2], dtype=torch.int32, device=DEV)    # 2 == n_seq
+    tr.layer_prefill(c, 2, 64, D.x, D.psi, D.rw, D.dw, D.mw, cache, xo, ws, seq_ids=sid)
+    torch.cuda.synchronize()
+    assert cache.status() == tr.CACHE_BAD_SEQ
+    assert torch.isfinite(xo).all()
+    np.testing.assert_array_equal(npy(cache.seq_len()), [64, 0])
+
+
+# ----------------------------------------------- full-size expert block
+def _moe_case(L, n_tok, eidx, egate, tag):
+    """triroute_moe on a generator-made x~ with the given routing, every row
+    against the oracle's expert block (paper Sec. 3.2 (B) expert equation)."""
+    cfg = L["cfg"]
+    act, d, E, k = cfg["act"], cfg["d"], cfg["E"], cfg["k"]
+    D = DeviceLayer(L)
+    c = D.cfg
+    xt_in = gen.to_act(gen.normal(33, "xt_full", (n_tok, d)), act)
+    cm = oracle.compact(np.zeros((n_tok, 1), np.uint8), eidx, n_tok, 1, 1, E, k)
+    cmp = tr.CompactionBuffers(c, n_tok, 1)
+    cmp.exp_cnt.copy_(to_dev(cm["exp_cnt"], torch.int32))
+    cmp.exp_off.copy_(to_dev(cm["exp_off"], torch.int32))
+    if len(cm["exp_rows"]):
+        cmp.exp_rows[:len(cm["exp_rows"])].copy_(to_dev(cm["exp_rows"], torch.int32))
+    xo = torch.empty(n_tok, d, dtype=D.act, device=DEV)
+    tr.moe(c, n_tok, to_dev(xt_in, D.act), D.dw, D.mw, to_dev(eidx, torch.int32),
+           to_dev(egate.astype(np.float32), torch.float32), cmp.struct, xo,
+           tr.workspace(c, tr.OP_MOE, n_tok, 1))
+    torch.cuda.synchronize()
+    del D
+    ref, _, _ = oracle.moe(np.asarray(xt_in, np.float64), L, eidx,
+                           egate.astype(np.float32).astype(np.float64))
+    assert_close(npy(xo), ref, act, f"x_out ({tag})")
+    null_only = np.all(eidx == 0, axis=1)
+    np.testing.assert_array_equal(npy(xo)[null_only], xt_in[null_only])
+    return cm
+
+
+@pytest.mark.parametrize("name", ["160m_bf16_prefill", "1p3b_bf16_prefill"])
+def test_moe_and_oproj_full_size(name):
+    """The many-token grouped GEMMs and O-projection at the workload's own
+    token count (B*T = 16384, > 2048 assignments), every row."""
+    L = gen.make_layer(name)
+    cfg = L["cfg"]
+    act, H, dh, E, k = cfg["act"], cfg["H"], cfg["dh"], cfg["E"], cfg["k"]
+    N = cfg["B"] * cfg["T"]
+    D = DeviceLayer(L, moe=False)
+    o = gen.to_act(gen.normal(34, "o_full", (N, H * dh), 0.5), act)
+    xt = torch.empty(N, cfg["d"], dtype=D.act, device=DEV)
+    tr.oproj(D.cfg, N, D.x, to_dev(o, D.act), D.dw, xt)
+    torch.cuda.synchronize()
+    assert_close(npy(xt), oracle.oproj(L["x"], np.asarray(o, np.float64), L["Wo"]), act,
+                 "x~ (oproj, many-token)")
+    del D, xt
+    ze = gen.normal(35, "ze_full", (N, E + 1), 1.5).astype(np.float64)
+    _, _, eidx, egate = oracle.decide(np.zeros((N, 1, 3)), ze, np.zeros((N, 4)), k)
+    cm = _moe_case(L, N, eidx, egate, "uniform, many-token")
+    assert cm["exp_off"][-1] > 2048
+
+
+def _routing_with_counts(counts, n_both_null, N, k, seed):
+    """eidx [N, 2] / egate with exactly counts[e] assignments to expert e
+    (index 0: null slots outside the both-null tokens), n_both_null tokens
+    whose two slots are both null, ids ascending within a token, rows in a
+    seeded random order."""
+    assert k == 2
+    rest = N - n_both_null
+    ids = np.repeat(np.arange(len(counts)), counts)
+    assert len(ids) == 2 * rest and max(counts) <= rest
+    pairs = np.stack([ids[:rest], ids[rest:]], axis=1)       # sorted: distinct, ascending
+    pairs = np.concatenate([np.zeros((n_both_null, 2), np.int64), pairs])
+    g = gen.stream(seed, "perm")
+    pairs = pairs[g.permutation(N)].astype(np.int32)
+    w = g.random((N, 2)) + 0.05
+    egate = w / w.sum(axis=1, keepdims=True)
+    egate[pairs == 0] *= 0.5                                   # the null's share is dropped
+    return pairs, egate
+
+
+def test_moe_expert_count_edges():
+    """Expert lists of 0, 1, 255, 256, 257, 511 and 513 rows (tile edges of
+    the 256-row tiles), tokens with both slots null, > 2048 assignments."""
+    L = gen.make_layer("160m_bf16_prefill")
+    N, E = 1300, L["cfg"]["E"]
+    nb = 9
+    counts = [120, 0, 1, 255, 256, 257, 511, 513]
+    counts.append(2 * (N - nb) - sum(counts))
+    eidx, egate = _routing_with_counts(np.array(counts), nb, N, 2, 36)
+    cm = _moe_case(L, N, eidx, egate, "count edges")
+    np.testing.assert_array_equal(cm["exp_cnt"][1:], counts[1:])
+    assert (np.all(eidx == 0, axis=1)).sum() == nb
+
+
+def test_moe_skewed_prefill_scale():
+    """Skewed routing at prefill scale (1.3B shapes, 16384 tokens): two hot
+    experts take 30 % of the assignments each and the null 15 % (the
+    long-context decode workload's mix), stressing grouped-GEMM imbalance."""
+    L = gen.make_layer("1p3b_bf16_prefill")
+    N, E = 16384, L["cfg"]["E"]
+    t = gen.expert_targets(dict(E=E, experts="skewed"))
+    counts = np.floor(t * 2 * N).astype(np.int64)
+    counts[3] += 2 * N - counts.sum()
+    eidx, egate = _routing_with_counts(counts, 0, N, 2, 37)
+    cm = _moe_case(L, N, eidx, egate, "skewed 30/30/15")
+    note("hot expert rows", float(cm["exp_cnt"][1]))

@@ -324,6 +324,33 @@ int triroute_layer_decode(const triroute_cfg *cfg, int B, const int32_t *seq_ids
                           const triroute_layer_taps *taps, void *ws, size_t ws_bytes,
                           triroute_stream_t stream);
 
+/* ---- no-allocation variant ---------------------------------------------- */
+
+/* Bytes of the library's static device scratch (per GPU, held until the
+ * process ends). */
+#define TRIROUTE_STATIC_SCRATCH_BYTES ((size_t)16 << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): one decode
+ * step exactly as triroute_layer_decode (same kernels, same results), with
+ * its workspace taken from a static device array of
+ * TRIROUTE_STATIC_SCRATCH_BYTES that the library holds on each GPU it runs
+ * on, instead of a caller buffer.  The caller still passes every input and
+ * output.  A batch whose workspace (triroute_workspace_bytes(cfg,
+ * TRIROUTE_OP_LAYER_DECODE, B, 1, .)) exceeds that size is rejected with
+ * TRIROUTE_E_WORKSPACE before any launch (16 MiB holds 64 sequences of the
+ * 1.3B-class shape, 128 of the 410M-class one).  The call allocates nothing:
+ * the array's address on the current device is looked up once per device.
+ * Every call on a GPU shares that GPU's array, which keeps the last call's
+ * contents; nothing in it needs clearing (no step depends on what an
+ * earlier call left there), but calls that overlap on one GPU (several
+ * streams or threads) race on it and must be serialised by the caller. */
+int triroute_layer_decode_noalloc(const triroute_cfg *cfg, int B, const int32_t *seq_ids,
+                                  const void *x, const float *psi, const triroute_router_w *rw,
+                                  const triroute_dense_w *dw, const triroute_moe_w *mw,
+                                  const triroute_kv_cache *cache, void *x_out,
+                                  const triroute_layer_taps *taps, triroute_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

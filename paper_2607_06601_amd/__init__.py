@@ -78,7 +78,7 @@ EXPORTS = [
     "triroute_kv_reset_seq", "triroute_kv_status", "triroute_kv_seq_len_ptr",
     "triroute_kv_append", "triroute_kv_export", "triroute_router", "triroute_qkv",
     "triroute_attn_prefill", "triroute_attn_decode", "triroute_oproj", "triroute_moe",
-    "triroute_layer_prefill", "triroute_layer_decode",
+    "triroute_layer_prefill", "triroute_layer_decode", "triroute_layer_decode_noalloc",
 ]
 
 _lib = None
@@ -112,6 +112,7 @@ def lib():
             "triroute_moe": [P, i32, P, P, P, P, P, P, P, P, sz, P],
             "triroute_layer_prefill": [P, i32, i32, P, P, P, P, P, P, P, P, P, P, sz, P],
             "triroute_layer_decode": [P, i32, P, P, P, P, P, P, P, P, P, P, sz, P],
+            "triroute_layer_decode_noalloc": [P, i32, P, P, P, P, P, P, P, P, P, P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -277,6 +278,14 @@ def layer_decode(cfg, B, x, psi, rw, dw, mw, cache: KVCache, x_out, ws, taps=Non
         C.byref(cfg), B, _p(seq_ids), _p(x), _p(psi), C.byref(rw), C.byref(dw), C.byref(mw),
         cache.ref, _p(x_out), C.byref(taps) if taps is not None else None, _p(ws), ws.numel(),
         _stream(stream)))
+
+
+def layer_decode_noalloc(cfg, B, x, psi, rw, dw, mw, cache: KVCache, x_out, taps=None,
+                         seq_ids=None, stream=None):
+    """triroute_layer_decode with the library's static scratch (no workspace)."""
+    _check(lib().triroute_layer_decode_noalloc(
+        C.byref(cfg), B, _p(seq_ids), _p(x), _p(psi), C.byref(rw), C.byref(dw), C.byref(mw),
+        cache.ref, _p(x_out), C.byref(taps) if taps is not None else None, _stream(stream)))
 
 
 # ------------------------------------------------------ device-side buffers

@@ -42,6 +42,32 @@ int hip_fail(hipError_t e, const char *what) {
     if (!(cond)) return fail(code, __VA_ARGS__); \
   } while (0)
 
+// Static scratch of the no-allocation entry point: one copy per GPU, whose
+// device address is looked up once per device (the host-side name of the
+// array is not a device address).
+__device__ __align__(256) uint8_t scratch[TRIROUTE_STATIC_SCRATCH_BYTES];
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[MAX_DEVICES] = {};
+
+int static_scratch(void **out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= MAX_DEVICES)
+    return fail(TRIROUTE_E_UNSUPPORTED, "device %d beyond the %d the library tracks", dev,
+                MAX_DEVICES);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return TRIROUTE_OK;
+}
+
 int prepare_once() {
   static std::once_flag once;
   static hipError_t err = hipSuccess;
@@ -632,6 +658,23 @@ int triroute_layer_prefill(const triroute_cfg *cfg, int B, int T, const int32_t 
                            triroute_stream_t stream) {
   return layer_impl(cfg, B, T, false, seq_ids, x, psi, rw, dw, mw, cache, x_out, taps, ws, ws_bytes,
                     stream);
+}
+
+int triroute_layer_decode_noalloc(const triroute_cfg *cfg, int B, const int32_t *seq_ids,
+                                  const void *x, const float *psi, const triroute_router_w *rw,
+                                  const triroute_dense_w *dw, const triroute_moe_w *mw,
+                                  const triroute_kv_cache *cache, void *x_out,
+                                  const triroute_layer_taps *taps, triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  TRY(check_bt(B, 1));
+  const size_t need = op_bytes(*cfg, TRIROUTE_OP_LAYER_DECODE, B, 1);
+  REQUIRE(need <= TRIROUTE_STATIC_SCRATCH_BYTES, TRIROUTE_E_WORKSPACE,
+          "decode step of %d sequences needs %zu bytes of scratch > the static %zu", B, need,
+          (size_t)TRIROUTE_STATIC_SCRATCH_BYTES);
+  void *ws = nullptr;
+  TRY(static_scratch(&ws));
+  return layer_impl(cfg, B, 1, true, seq_ids, x, psi, rw, dw, mw, cache, x_out, taps, ws,
+                    TRIROUTE_STATIC_SCRATCH_BYTES, stream);
 }
 
 int triroute_layer_decode(const triroute_cfg *cfg, int B, const int32_t *seq_ids, const void *x,

@@ -2,24 +2,38 @@
 
 A step is one full routed-layer prefill (router, compaction, QKV + RoPE,
 KV quantize/append, attention, O-proj, second norm, expert grouped GEMM,
-combine) of the 160M-class workload: batch 8 x 2048 tokens, d 768, 12 x 64
-heads (3 kv heads), window 128, 8 SwiGLU experts (d_ff 2048) + null, top-2,
-KV group 64, bf16, seeded synthetic inputs and random-init weights.  Inputs
-are resident in HBM before timing; every step writes a fresh cache; the
-L2 / Infinity Cache is flushed before each timed step by reading a 1 GiB
-buffer (a read, so that no dirty lines are left whose write-back would land
-in the timed region).
+combine) of the 1.3B-class workload, the largest that the benchmark's
+configurations define: batch 4 x 4096 tokens, d 2048, 16 x 128 heads (4 kv
+heads), window 512, 16 SwiGLU experts (d_ff 5632) + null, top-2, KV group 64,
+bf16, seeded synthetic inputs and random-init weights.  Inputs are resident in
+HBM before timing; every step writes a fresh cache; L2 and the 256 MB
+Infinity Cache are flushed before each timed step by reading a 1 GiB buffer
+(a read, so that no dirty lines are left whose write-back would land in the
+timed region).  Each step is bracketed by HIP events on the launch stream.
 
-Also reported: the MoE sublayer's achieved bf16 MFMA rate (roofline), the
-410M-class decode step (64 sequences x 8192 context) and its decode
-attention's achieved HBM bandwidth, and the CPU oracle timed on a bounded
-sample on the host cores.
+Also reported, as extra keys of the one JSON line:
+  roofline      the MoE sublayer (triroute_moe) of the headline workload:
+                achieved bf16 MFMA rate of the algorithmic expert FLOPs
+  prefill_160m  the 160M-class prefill (8 x 2048) on seeds 1, 2, 3 and their
+                median, with its MoE sublayer
+  decode_410m / decode_1p3b
+                the decode steps (64 x 8192 and 32 x 32768 context) with the
+                decode attention's achieved HBM bandwidth; the same attention
+                with every head in full mode over the routed mixed-width cache
+                (bandwidth stress point); and the dense special case (all
+                heads full, every token 16-bit, one expert, k = 1) through the
+                same kernels, with routed / dense tokens/s and the cost-model
+                fractions of the routed step
+  dense_1p3b_prefill
+                the dense special case of the headline workload
+  cpu_baseline  the CPU oracle on a bounded sample of the headline workload
 """
 from __future__ import annotations
 
 import argparse
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -29,8 +43,10 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2516.6  # MI355X dense bf16 MFMA, TFLOP/s (256 CU x 2.4 GHz x 4096)
 
-PREFILL = "160m_bf16_prefill"
-DECODE = "410m_bf16_decode"
+HEADLINE = "1p3b_bf16_prefill"
+SMALL = "160m_bf16_prefill"
+DECODES = {"decode_410m": "410m_bf16_decode", "decode_1p3b": "1p3b_bf16_decode"}
+METRIC = "routed-layer tokens/s (prefill, decode); decode-attn HBM GB/s; MoE MFMA util"
 
 
 def parse():
@@ -39,13 +55,14 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--no-decode", action="store_true")
-    p.add_argument("--no-wide", action="store_true",
-                   help="leave out the 1.3B-class prefill and long-context decode legs")
-    p.add_argument("--only", choices=("prefill", "decode", "moe", "prefill_1p3b", "decode_1p3b"),
-                   default=None,
-                   help="profile one workload alone (prints its section only); 'moe' times "
-                        "the MoE sublayer and then runs a 256 MiB copy for counter calibration")
+    p.add_argument("--no-extra", action="store_true",
+                   help="the headline workload only (no 160M, decode or dense legs)")
+    p.add_argument("--only", default=None,
+                   choices=("prefill_1p3b", "prefill_160m", "moe_1p3b", "moe_160m",
+                            "decode_410m", "decode_1p3b", "attn_410m", "attn_1p3b"),
+                   help="profile one leg alone (prints its section only); moe_* time the "
+                        "MoE sublayer, attn_* the decode attention, and both then run a "
+                        "256 MiB copy for counter calibration")
     p.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "KERNEL_REGEX"),
                    default=None,
                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; csv output) "
@@ -65,80 +82,110 @@ class CacheFlush:
         self.buf.sum()
 
 
-def events(torch):
-    return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+class Ctx:
+    """Modules and shared objects of one benchmark run."""
+
+    def __init__(self, args):
+        import numpy as np
+        import torch
+
+        import gen
+        import paper_2607_06601_amd as tr
+        from paper_2607_06601_amd.device import DeviceLayer, to_dev
+        self.args, self.np, self.torch, self.gen, self.tr = args, np, torch, gen, tr
+        self.DeviceLayer, self.to_dev = DeviceLayer, to_dev
+        self.dev = "cuda"
+        self.flush = CacheFlush(torch, self.dev)
+        self._layer = (None, None)
+
+    def layer(self, name, seed=None):
+        """The generator's layer (the last one is kept: the headline, its
+        dense case and the CPU baseline share it; callers copy before they
+        change anything)."""
+        key = (name, seed)
+        if self._layer[0] != key:
+            self._layer = (None, None)
+            self._layer = (key, self.gen.make_layer(name, seed))
+        return self._layer[1]
+
+    def timed(self, fn, steps, before=None):
+        """Mean and per-step ms of `steps` calls of fn(i), each preceded by a
+        cache flush, bracketed by HIP events on the current stream."""
+        torch = self.torch
+        stream = torch.cuda.current_stream()
+        ev = []
+        torch.cuda.synchronize()
+        for i in range(steps):
+            if before:
+                before(i)
+            self.flush()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn(i)
+            e1.record(stream)
+            ev.append((e0, e1))
+        torch.cuda.synchronize()
+        ms = [a.elapsed_time(b) for a, b in ev]
+        return float(self.np.mean(ms)), ms
 
 
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the routed layer is "
-              "measured on a single MI355X in this build", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the routed layer is "
+              "measured on a single MI355X; how it would shard is described in DESIGN.md",
+              file=sys.stderr)
         sys.exit(2)
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc)
         return
-    import numpy as np
     import torch
-
-    import gen
-    import paper_2607_06601_amd as tr
-    from paper_2607_06601_amd.device import DeviceLayer, to_dev
-
     assert torch.cuda.is_available(), "bench.py needs the GPU"
-    tr.lib()
-    dev = "cuda"
-    stream = torch.cuda.current_stream()
-    flush = CacheFlush(torch, dev)
-    if args.only == "decode":
-        res = bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush, DECODE)
-        copy_calibration(torch)
-        print(json.dumps({"decode": res}), flush=True)
-        return
-    if args.only in ("prefill_1p3b", "decode_1p3b"):
-        res = run_wide(args, torch, np, gen, tr, DeviceLayer, to_dev, flush, args.only)
-        print(json.dumps({args.only: res}), flush=True)
+    cx = Ctx(args)
+    cx.tr.lib()
+    if args.only:
+        leg = args.only
+        if leg in ("prefill_1p3b", "moe_1p3b"):
+            r = bench_prefill(cx, HEADLINE, None, args.steps, args.warmup, moe_only=leg == "moe_1p3b")
+        elif leg in ("prefill_160m", "moe_160m"):
+            r = bench_prefill(cx, SMALL, 1, args.steps, args.warmup, moe_only=leg == "moe_160m")
+        else:
+            name = DECODES["decode_410m" if leg.endswith("410m") else "decode_1p3b"]
+            r = bench_decode(cx, name, args.steps, args.warmup, attn_only=leg.startswith("attn"))
+        if leg.startswith(("moe", "attn")):
+            copy_calibration(torch)
+        print(json.dumps({leg: r}), flush=True)
         return
 
-    res = bench_prefill(args, torch, np, gen, tr, DeviceLayer, flush, PREFILL, 1)
-    if args.only == "moe":
-        copy_calibration(torch)
-        print(json.dumps({"moe": res["roofline"]}), flush=True)
-        return
-    B, T, ms, step_ms, wall = (res[x] for x in ("B", "T", "ms", "step_ms", "wall"))
-    N = B * T
-    roofline = res["roofline"]
-
+    K, W = args.steps, args.warmup
+    head = bench_prefill(cx, HEADLINE, None, K, W)
+    N = head["B"] * head["T"]
+    cfg = cx.gen.CONFIGS[HEADLINE]
     out = {
-        "metric": "routed-layer tokens/s (prefill, decode); decode-attn HBM GB/s; MoE MFMA util",
-        "value": round(N / (ms * 1e-3), 1),
+        "metric": METRIC,
+        "value": round(N / (head["ms"] * 1e-3), 1),
         "unit": "tokens/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms, 4),
+        "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(head["ms"], 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic (seeded generator, random-init weights)",
-        "config": {"workload": "160M-class TriRoute layer prefill: batch 8 x seq 2048, d 768, "
-                               "12x64 heads (3 kv), window 128, 8 SwiGLU experts d_ff 2048 + "
-                               "null, top-2, KV group 64, bf16",
-                   "global_batch": B, "seq_len": T, "parallelism": "single GPU"},
-        "roofline": roofline,
-        "timing": {"per_step_ms_min": round(min(step_ms), 4),
-                   "per_step_ms_max": round(max(step_ms), 4),
-                   "wall_s_timed_loop": round(wall, 3), "cache_flush_per_step": "1 GiB read"},
+        "config": {"workload": "1.3B-class TriRoute " + describe(cfg),
+                   "global_batch": head["B"], "seq_len": head["T"],
+                   "parallelism": "single GPU"},
+        "roofline": head["roofline"],
+        "timing": {"per_step_ms_min": round(min(head["step_ms"]), 4),
+                   "per_step_ms_max": round(max(head["step_ms"]), 4),
+                   "cache_flush_per_step": "1 GiB read"},
     }
-
-    # ------------------------------------------------------------- decode
-    if not args.no_decode and args.only is None:
-        out["decode"] = bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush, DECODE)
-
-    # ---------------------------------- the 1.3B-class workloads (context)
-    if not args.no_wide and args.only is None:
-        for leg in ("prefill_1p3b", "decode_1p3b"):
-            out[leg] = run_wide(args, torch, np, gen, tr, DeviceLayer, to_dev, flush, leg)
-
-    # --------------------------------------------------------- CPU oracle
-    if not args.no_cpu_baseline and args.only is None:
-        out["cpu_baseline"] = cpu_baseline(np)
+    if not args.no_extra:
+        ks, ws = min(K, 10), min(W, 3)
+        out["prefill_160m"] = bench_small_seeds(cx, ks, ws)
+        for key, name in DECODES.items():
+            out[key] = bench_decode(cx, name, ks, ws)
+        out["dense_1p3b_prefill"] = bench_dense_prefill(cx, ks, ws, head)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cx.layer(HEADLINE))
     print(json.dumps(out), flush=True)
 
 
@@ -149,72 +196,117 @@ def describe(cfg):
     else:
         head = (f"decode step: {cfg['B']} sequences x 1 new token, context {cfg['ctx']} (bits "
                 + "/".join(f"{round(100 * f)}" for f in cfg["ctx_bits"]) + " % for 2/4/8/16)")
-    ex = "skewed" if cfg["experts"] == "skewed" else "uniform"
+    ex = {"skewed": "skewed", "uniform": "uniform"}.get(cfg["experts"], cfg["experts"])
     return (f"{head}, d {cfg['d']}, {cfg['H']}x{cfg['dh']} heads ({cfg['Hkv']} kv), window "
             f"{cfg['w']}, {cfg['E']} SwiGLU experts d_ff {cfg['d_ff']} + null, top-{cfg['k']} "
             f"({ex} routing), KV group {cfg['G']}, {cfg['act']}")
 
 
-def run_wide(args, torch, np, gen, tr, DeviceLayer, to_dev, flush, leg):
-    """The 1.3B-class prefill (step + MoE sublayer) or long-context decode
-    (step + decode attention), with at most 10 timed steps."""
-    import copy
-    a = copy.copy(args)
-    a.steps, a.warmup = min(args.steps, 10), min(args.warmup, 3)
-    if leg == "prefill_1p3b":
-        name = "1p3b_bf16_prefill"
-        r = bench_prefill(a, torch, np, gen, tr, DeviceLayer, flush, name, None)
-        N = r["B"] * r["T"]
-        return {"workload": "1.3B-class " + describe(gen.CONFIGS[name]),
-                "tokens_per_s": round(N / (r["ms"] * 1e-3), 1), "ms_per_step": round(r["ms"], 4),
-                "steps": a.steps, "moe": r["roofline"]}
-    return bench_decode(a, torch, np, gen, tr, DeviceLayer, to_dev, flush, "1p3b_bf16_decode")
+def dense_variant(L, np):
+    """The dense special case of a routed layer (the standard pre-norm
+    block): every head in full mode, every token 16-bit, one SwiGLU expert
+    (the first), k = 1, the null never chosen, forced through the router
+    biases; same shapes and weights otherwise."""
+    D = dict(L)
+    cfg = dict(L["cfg"], E=1, k=1, experts="dense")
+    if "ctx_bits" in cfg:
+        cfg["ctx_bits"] = (0.0, 0.0, 0.0, 1.0)
+    D["cfg"] = cfg
+    H = cfg["H"]
+    D["ca"] = np.tile(np.array([-50.0, -50.0, 50.0], np.float32), H)
+    D["cb"] = np.array([-50.0, -50.0, -50.0, 50.0], np.float32)
+    D["We"] = np.ascontiguousarray(L["We"][:2])
+    D["ce"] = np.array([-1.0e4, 50.0], np.float32)
+    for n in ("Wg", "Wu", "Wd"):
+        D[n] = L[n][:1]
+    return D
 
 
-def bench_prefill(args, torch, np, gen, tr, DeviceLayer, flush, name, seed):
+def bench_prefill(cx, name, seed, steps, warmup, moe_only=False, L=None):
     """Timed triroute_layer_prefill steps of one prefill workload, then its
     MoE sublayer alone on the same routed inputs."""
-    L = gen.make_layer(name, seed)
+    np, torch, tr = cx.np, cx.torch, cx.tr
+    if L is None:
+        L = cx.layer(name, seed)
     cfg = L["cfg"]
     B, T, d, k = (cfg[x] for x in ("B", "T", "d", "k"))
     N = B * T
-    D = DeviceLayer(L)
-    del L
+    D = cx.DeviceLayer(L)
     c = D.cfg
-    dev = "cuda"
-    stream = torch.cuda.current_stream()
     ws = tr.workspace(c, tr.OP_LAYER_PREFILL, B, T)
-    xo = torch.empty(N, d, dtype=D.act, device=dev)
-    caches = [tr.KVCache(c, B, T) for _ in range(args.steps)]
-    warm = tr.KVCache(c, B, T)
-    eidx_t = torch.empty(N, k, dtype=torch.int32, device=dev)
-    egate_t = torch.empty(N, k, dtype=torch.float32, device=dev)
-    xt_t = torch.empty(N, d, dtype=D.act, device=dev)
+    xo = torch.empty(N, d, dtype=D.act, device=cx.dev)
+    eidx_t = torch.empty(N, k, dtype=torch.int32, device=cx.dev)
+    egate_t = torch.empty(N, k, dtype=torch.float32, device=cx.dev)
+    xt_t = torch.empty(N, d, dtype=D.act, device=cx.dev)
     taps = tr.Taps(eidx=eidx_t.data_ptr(), egate=egate_t.data_ptr(), xt=xt_t.data_ptr())
-    for _ in range(args.warmup):
+    warm = tr.KVCache(c, B, T)
+    for _ in range(max(warmup, 1)):
         for s in range(B):
             warm.reset_seq(s)
         tr.layer_prefill(c, B, T, D.x, D.psi, D.rw, D.dw, D.mw, warm, xo, ws, taps=taps)
     torch.cuda.synchronize()
-    times = []
-    t_wall0 = time.perf_counter()
-    for i in range(args.steps):
-        flush()
-        e0, e1 = events(torch)
-        e0.record(stream)
-        tr.layer_prefill(c, B, T, D.x, D.psi, D.rw, D.dw, D.mw, caches[i], xo, ws, taps=taps)
-        e1.record(stream)
-        times.append((e0, e1))
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_wall0
-    step_ms = [a.elapsed_time(b) for a, b in times]
-    for cc in caches:
-        assert cc.status() == 0
-    del caches, warm
-    roofline = bench_moe(args, torch, np, tr, D, c, B, T, flush, eidx_t, egate_t, xt_t, xo,
-                         name)
-    return {"B": B, "T": T, "ms": float(np.mean(step_ms)), "step_ms": step_ms, "wall": wall,
-            "roofline": roofline}
+    res = {"B": B, "T": T}
+    if not moe_only:
+        caches = [tr.KVCache(c, B, T) for _ in range(steps)]
+        ms, step_ms = cx.timed(lambda i: tr.layer_prefill(c, B, T, D.x, D.psi, D.rw, D.dw, D.mw,
+                                                           caches[i], xo, ws, taps=taps), steps)
+        for cc in caches:
+            assert cc.status() == 0
+        del caches
+        res.update(ms=ms, step_ms=step_ms, tokens_per_s=round(N / (ms * 1e-3), 1))
+    del warm
+    res["roofline"] = bench_moe(cx, D, c, B, T, eidx_t, egate_t, xt_t, xo, name, steps)
+    return res
+
+
+def bench_moe(cx, D, c, B, T, eidx_t, egate_t, xt_t, xo, name, steps):
+    """The MoE sublayer (triroute_moe: rmsnorm2, grouped GEMM gate/up +
+    SwiGLU, grouped GEMM down, combine) alone on the routed inputs of the last
+    prefill step: achieved bf16 MFMA rate of the algorithmic expert FLOPs
+    (6 d d_ff per real assignment; norm and combine time included)."""
+    np, torch, tr = cx.np, cx.torch, cx.tr
+    d, dff = c.d_model, c.d_ff
+    N = B * T
+    n_real = int((eidx_t.cpu().numpy() != 0).sum())
+    moe_flops = 6.0 * d * dff * n_real
+    cmp = tr.CompactionBuffers(c, B, T)
+    n1 = torch.empty(N, d, dtype=D.act, device=cx.dev)
+    mode = torch.empty(N, c.n_heads, dtype=torch.uint8, device=cx.dev)
+    bit = torch.empty(N, dtype=torch.uint8, device=cx.dev)
+    tr.router(c, B, T, D.x, D.psi, D.rw, n1, mode, bit, eidx_t, egate_t, cmp.struct,
+              tr.workspace(c, tr.OP_ROUTER, B, T))
+    moe_ws = tr.workspace(c, tr.OP_MOE, N, 1)
+    for _ in range(3):
+        tr.moe(c, N, xt_t, D.dw, D.mw, eidx_t, egate_t, cmp.struct, xo, moe_ws)
+    ms, _ = cx.timed(lambda i: tr.moe(c, N, xt_t, D.dw, D.mw, eidx_t, egate_t, cmp.struct, xo,
+                                      moe_ws), steps)
+    tflops = moe_flops / (ms * 1e-3) / 1e12
+    prof = {HEADLINE: "moe_1p3b_prefill_traffic.txt", SMALL: "moe_160m_prefill_traffic.txt"}
+    return {"kernel": "triroute_moe (rmsnorm2, grouped GEMM gate/up + SwiGLU, grouped GEMM "
+                      "down, combine)",
+            "bound": "mfma", "achieved": round(tflops, 2),
+            "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+            "traffic": stored_traffic(prof.get(name), MOE_SOURCES),
+            "algorithmic": f"6*d*d_ff FLOP x {n_real} real assignments = "
+                           f"{moe_flops / 1e9:.1f} GFLOP per launch",
+            "avg_ms": round(ms, 4)}
+
+
+def bench_small_seeds(cx, steps, warmup):
+    """The 160M-class prefill on its three seeds; the median is the figure."""
+    per = {}
+    moe = None
+    for seed in cx.gen.CONFIGS[SMALL]["seeds"]:
+        r = bench_prefill(cx, SMALL, seed, steps, warmup)
+        per[str(seed)] = {"tokens_per_s": r["tokens_per_s"], "ms_per_step": round(r["ms"], 4),
+                          "moe_frac": r["roofline"]["frac"]}
+        if moe is None:
+            moe = r["roofline"]
+    tps = [v["tokens_per_s"] for v in per.values()]
+    return {"workload": "160M-class " + describe(cx.gen.CONFIGS[SMALL]),
+            "tokens_per_s_median": round(statistics.median(tps), 1), "seeds": per,
+            "steps": steps, "moe_seed1": moe}
 
 
 def source_digest(*names):
@@ -236,6 +328,8 @@ def stored_traffic(name, sources):
     """HBM bytes per launch from a committed counter summary under profiles/
     (FETCH_SIZE + WRITE_SIZE, scaled by the plain-copy calibration), or None
     when it is missing or was taken from other kernel sources."""
+    if not name:
+        return None
     path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
@@ -253,49 +347,6 @@ def stored_traffic(name, sources):
         return None
 
 
-def bench_moe(args, torch, np, tr, D, c, B, T, flush, eidx_t, egate_t, xt_t, xo, name):
-    """The MoE sublayer (triroute_moe: rmsnorm2, grouped GEMM gate/up + SwiGLU,
-    grouped GEMM down, combine) alone on the routed inputs of the last prefill
-    step: achieved bf16 MFMA rate of the expert FLOPs."""
-    dev = "cuda"
-    stream = torch.cuda.current_stream()
-    d, dff = c.d_model, c.d_ff
-    N = B * T
-    eidx_h = eidx_t.cpu().numpy()
-    n_real = int((eidx_h != 0).sum())
-    moe_flops = 6.0 * d * dff * n_real
-    cmp = tr.CompactionBuffers(c, B, T)
-    rw_ws = tr.workspace(c, tr.OP_ROUTER, B, T)
-    n1 = torch.empty(N, d, dtype=D.act, device=dev)
-    mode = torch.empty(N, c.n_heads, dtype=torch.uint8, device=dev)
-    bit = torch.empty(N, dtype=torch.uint8, device=dev)
-    tr.router(c, B, T, D.x, D.psi, D.rw, n1, mode, bit, eidx_t, egate_t, cmp.struct, rw_ws)
-    moe_ws = tr.workspace(c, tr.OP_MOE, N, 1)
-    for _ in range(3):
-        tr.moe(c, N, xt_t, D.dw, D.mw, eidx_t, egate_t, cmp.struct, xo, moe_ws)
-    moe_ms = []
-    for i in range(args.steps):
-        flush()
-        e0, e1 = events(torch)
-        e0.record(stream)
-        tr.moe(c, N, xt_t, D.dw, D.mw, eidx_t, egate_t, cmp.struct, xo, moe_ws)
-        e1.record(stream)
-        moe_ms.append((e0, e1))
-    torch.cuda.synchronize()
-    moe_avg = float(np.mean([a.elapsed_time(b) for a, b in moe_ms]))
-    moe_tflops = moe_flops / (moe_avg * 1e-3) / 1e12
-    return {"kernel": "triroute_moe (rmsnorm2, grouped GEMM gate/up + SwiGLU, grouped GEMM "
-                      "down, combine)",
-            "bound": "mfma", "achieved": round(moe_tflops, 2),
-            "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(moe_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
-            "traffic": (stored_traffic("moe_160m_prefill_traffic.txt", MOE_SOURCES)
-                        if name == PREFILL else None),
-            "algorithmic": f"6*d*d_ff FLOP x {n_real} real assignments = "
-                           f"{moe_flops / 1e9:.1f} GFLOP per launch",
-            "avg_ms": round(moe_avg, 4)}
-
-
 def copy_calibration(torch):
     """A plain device copy of 256 MiB: the reference reading for the FETCH_SIZE
     / WRITE_SIZE counters (kernel name contains 'copy' or 'elementwise')."""
@@ -308,16 +359,22 @@ def copy_calibration(torch):
     return n
 
 
+def slot_bytes(cfg):
+    """Packed K+V bytes of one cached token per kv head at each width,
+    fp16 scale/zero included (16-bit: the bf16 values only)."""
+    dh, G = cfg["dh"], cfg["G"]
+    return [2 * dh * b / 8 + (2 * (dh // G) * 4 if b < 16 else 0) for b in (2, 4, 8, 16)]
+
+
 def decode_attn_bytes(cfg, mode, bits_per_seq):
     """Algorithmic bytes the routed decode attention must read: per (sequence,
     kv head), the union of the key ranges its query heads need (full -> all
     P+1 keys, local -> last w, skip -> none) x packed K+V bytes incl. fp16
     scale/zero."""
     import numpy as np
-    H, Hkv, dh, G, w = cfg["H"], cfg["Hkv"], cfg["dh"], cfg["G"], cfg["w"]
+    H, Hkv, w = cfg["H"], cfg["Hkv"], cfg["w"]
     grp = H // Hkv
-    per_tok = np.array([2 * dh * b / 8 + (2 * (dh // G) * 4 if b < 16 else 0)
-                        for b in (2, 4, 8, 16)])
+    per_tok = np.array(slot_bytes(cfg))
     total = 0.0
     for s, bits in enumerate(bits_per_seq):
         P1 = len(bits)
@@ -329,76 +386,143 @@ def decode_attn_bytes(cfg, mode, bits_per_seq):
     return total
 
 
-def bench_decode(args, torch, np, gen, tr, DeviceLayer, to_dev, flush, name):
-    L = gen.make_layer(name)
-    cfg = L["cfg"]
-    B, ctx, d, H, k = cfg["B"], cfg["ctx"], cfg["d"], cfg["H"], cfg["k"]
-    D = DeviceLayer(L)
-    c = D.cfg
-    dev = "cuda"
-    stream = torch.cuda.current_stream()
-    cap = ctx + args.warmup + args.steps + 1
-    cache = tr.KVCache(c, B, cap)
-    ws_app = tr.workspace(c, tr.OP_KV_APPEND, 1, ctx)
+def decode_cost(cfg, mode, bits_per_seq, eidx):
+    """Cost-model terms of one decode step (paper Sec. 3.5 per-token costs,
+    App. A): attention MACs 2 d_h per head and key (local: the window's w
+    keys, full: all P + 1), KV memory 2 d_kv b bits per cached token, expert
+    MACs 3 d d_f per real assignment (reading R27)."""
+    import numpy as np
+    H, dh, w, d, dff = cfg["H"], cfg["dh"], cfg["w"], cfg["d"], cfg["d_ff"]
+    dkv = cfg["Hkv"] * dh
+    attn = kv = 0.0
+    for s, bits in enumerate(bits_per_seq):
+        P1 = len(bits)
+        for h in range(H):
+            m = int(mode[s, h])
+            attn += 2 * dh * (0 if m == 0 else min(P1, w) if m == 1 else P1)
+        kv += 2 * dkv * float(np.sum(np.array([2, 4, 8, 16])[bits]))
+    ffn = 3.0 * d * dff * float((eidx != 0).sum())
+    return {"attn_macs": attn, "kv_bits": kv, "ffn_macs": ffn}
+
+
+def fill_decode_cache(cx, c, cache, cfg, act_t, dense=False):
+    """The workload's pre-existing context: the generator's K/V at its
+    per-position widths (all 16-bit for the dense case)."""
+    np, torch, tr, gen = cx.np, cx.torch, cx.tr, cx.gen
+    ctx = cfg["ctx"]
+    ws = tr.workspace(c, tr.OP_KV_APPEND, 1, ctx)
     bits_all = []
-    for s in range(B):
+    for s in range(cfg["B"]):
         kk, vv = gen.context_kv(cfg, s)
-        bits = gen.context_bits(cfg, s)
+        bits = np.full(ctx, 3, np.uint8) if dense else gen.context_bits(cfg, s)
         bits_all.append(bits)
-        tr.kv_append(c, cache, 1, ctx, to_dev(kk.reshape(ctx, -1), D.act),
-                     to_dev(vv.reshape(ctx, -1), D.act), to_dev(bits, torch.uint8), ws_app,
-                     seq_ids=torch.tensor([s], dtype=torch.int32, device=dev))
+        tr.kv_append(c, cache, 1, ctx, cx.to_dev(kk.reshape(ctx, -1), act_t),
+                     cx.to_dev(vv.reshape(ctx, -1), act_t), cx.to_dev(bits, torch.uint8), ws,
+                     seq_ids=torch.tensor([s], dtype=torch.int32, device=cx.dev))
     torch.cuda.synchronize()
+    return bits_all
+
+
+def run_decode_steps(cx, L, steps, warmup, dense=False):
+    """Timed decode steps of one layer over a freshly filled cache; returns
+    the step time, the step's decisions and the cache."""
+    np, torch, tr = cx.np, cx.torch, cx.tr
+    cfg = L["cfg"]
+    B, d, H, k = cfg["B"], cfg["d"], cfg["H"], cfg["k"]
+    D = cx.DeviceLayer(L)
+    c = D.cfg
+    cache = tr.KVCache(c, B, cfg["ctx"] + warmup + steps + 1)
+    bits_all = fill_decode_cache(cx, c, cache, cfg, D.act, dense)
     ws = tr.workspace(c, tr.OP_LAYER_DECODE, B, 1)
-    xo = torch.empty(B, d, dtype=D.act, device=dev)
-    mode_t = torch.empty(B, H, dtype=torch.uint8, device=dev)
-    bit_t = torch.empty(B, dtype=torch.uint8, device=dev)
-    q_t = torch.empty(B, H * cfg["dh"], dtype=D.act, device=dev)
-    taps = tr.Taps(mode=mode_t.data_ptr(), bit=bit_t.data_ptr(), q=q_t.data_ptr())
-    for _ in range(args.warmup):
+    xo = torch.empty(B, d, dtype=D.act, device=cx.dev)
+    t = dict(mode=torch.empty(B, H, dtype=torch.uint8, device=cx.dev),
+             bit=torch.empty(B, dtype=torch.uint8, device=cx.dev),
+             eidx=torch.empty(B, k, dtype=torch.int32, device=cx.dev),
+             q=torch.empty(B, H * cfg["dh"], dtype=D.act, device=cx.dev))
+    taps = tr.Taps(**{n: x.data_ptr() for n, x in t.items()})
+    for _ in range(warmup):
         tr.layer_decode(c, B, D.x, D.psi, D.rw, D.dw, D.mw, cache, xo, ws, taps=taps)
-    times = []
-    for i in range(args.steps):
-        flush()
-        e0, e1 = events(torch)
-        e0.record(stream)
-        tr.layer_decode(c, B, D.x, D.psi, D.rw, D.dw, D.mw, cache, xo, ws, taps=taps)
-        e1.record(stream)
-        times.append((e0, e1))
-    torch.cuda.synchronize()
+    ms, _ = cx.timed(lambda i: tr.layer_decode(c, B, D.x, D.psi, D.rw, D.dw, D.mw, cache, xo, ws,
+                                               taps=taps), steps)
     assert cache.status() == 0
-    step_ms = float(np.mean([a.elapsed_time(b) for a, b in times]))
-    # decode attention alone over the cache as it now stands
-    mode = mode_t.cpu().numpy()
     seq_len = cache.seq_len().cpu().numpy()
-    # bit widths of every cached token, in position order, per sequence
-    extra = bit_t.cpu().numpy()
+    extra = t["bit"].cpu().numpy()
+    ctx = cfg["ctx"]
     bits_now = [np.concatenate([bits_all[s], np.full(seq_len[s] - ctx, extra[s], np.uint8)])
                 for s in range(B)]
-    nbytes = decode_attn_bytes(cfg, mode, bits_now)
-    o = torch.empty(B, H * cfg["dh"], dtype=D.act, device=dev)
-    aws = tr.workspace(c, tr.OP_ATTN_DECODE, B, 1)
+    return dict(ms=ms, D=D, c=c, cache=cache, t=t, bits=bits_now,
+                eidx=t["eidx"].cpu().numpy())
+
+
+def bench_attn(cx, r, cfg, mode_t, steps, label):
+    """The decode attention alone over the cache as it stands, with the
+    given per-head modes: achieved HBM bandwidth of the algorithmic bytes."""
+    tr, torch = cx.tr, cx.torch
+    B, H = cfg["B"], cfg["H"]
+    nbytes = decode_attn_bytes(cfg, mode_t.cpu().numpy(), r["bits"])
+    o = torch.empty(B, H * cfg["dh"], dtype=r["D"].act, device=cx.dev)
+    aws = tr.workspace(r["c"], tr.OP_ATTN_DECODE, B, 1)
     for _ in range(3):
-        tr.attn_decode(c, B, q_t, cache, mode_t, o, aws)
-    at = []
-    for i in range(args.steps):
-        flush()
-        e0, e1 = events(torch)
-        e0.record(stream)
-        tr.attn_decode(c, B, q_t, cache, mode_t, o, aws)
-        e1.record(stream)
-        at.append((e0, e1))
-    torch.cuda.synchronize()
-    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in at]))
-    gbs = nbytes / (attn_ms * 1e-3) / 1e9
-    cls = "410M" if name == DECODE else "1.3B"
-    return {"workload": f"{cls}-class " + describe(cfg),
-            "tokens_per_s": round(B / (step_ms * 1e-3), 1), "ms_per_step": round(step_ms, 4),
-            "attn": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                     "algorithmic_bytes": int(nbytes), "avg_ms": round(attn_ms, 4),
-                     "traffic": (stored_traffic("attn_decode_410m_traffic.txt",
-                                                 DECODE_ATTN_SOURCES) if name == DECODE else None)}}
+        tr.attn_decode(r["c"], B, r["t"]["q"], r["cache"], mode_t, o, aws)
+    ms, _ = cx.timed(lambda i: tr.attn_decode(r["c"], B, r["t"]["q"], r["cache"], mode_t, o,
+                                              aws), steps)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    prof = {"410m_bf16_decode": "attn_decode_410m_traffic.txt",
+            "1p3b_bf16_decode": "attn_decode_1p3b_traffic.txt"}
+    return {"modes": label, "bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": int(nbytes),
+            "avg_ms": round(ms, 4),
+            "traffic": (stored_traffic(prof.get(cfg["name"]), DECODE_ATTN_SOURCES)
+                        if label == "routed" else None)}
+
+
+def bench_decode(cx, name, steps, warmup, attn_only=False):
+    np, torch = cx.np, cx.torch
+    L = cx.gen.make_layer(name)
+    cfg = L["cfg"]
+    B = cfg["B"]
+    r = run_decode_steps(cx, L, steps, warmup)
+    cls = "410M" if name.startswith("410m") else "1.3B"
+    out = {"workload": f"{cls}-class " + describe(cfg),
+           "tokens_per_s": round(B / (r["ms"] * 1e-3), 1), "ms_per_step": round(r["ms"], 4),
+           "attn": bench_attn(cx, r, cfg, r["t"]["mode"], steps, "routed")}
+    if attn_only:
+        return out
+    full = torch.full_like(r["t"]["mode"], 2)
+    out["attn_all_full"] = bench_attn(cx, r, cfg, full, steps, "every head full (routed widths)")
+    routed_cost = decode_cost(cfg, r["t"]["mode"].cpu().numpy(), r["bits"], r["eidx"])
+    del r
+    torch.cuda.empty_cache()
+    # the dense special case through the same kernels
+    Ld = dense_variant(L, np)
+    del L
+    rd = run_decode_steps(cx, Ld, steps, warmup, dense=True)
+    dcfg = Ld["cfg"]
+    assert (rd["t"]["mode"].cpu().numpy() == 2).all() and (rd["eidx"] == 1).all()
+    dense_cost = decode_cost(dcfg, rd["t"]["mode"].cpu().numpy(), rd["bits"], rd["eidx"])
+    out["dense"] = {
+        "workload": "dense special case: every head full, every token 16-bit, one SwiGLU "
+                    "expert (d_ff %d), k = 1" % dcfg["d_ff"],
+        "tokens_per_s": round(B / (rd["ms"] * 1e-3), 1), "ms_per_step": round(rd["ms"], 4),
+        "attn": bench_attn(cx, rd, dcfg, rd["t"]["mode"], steps, "dense: all full, 16-bit")}
+    out["routed_over_dense_tokens_per_s"] = round(rd["ms"] / out["ms_per_step"], 3)
+    out["cost_model_routed_over_dense"] = {
+        key: round(routed_cost[key] / dense_cost[key], 4) for key in routed_cost}
+    del rd
+    torch.cuda.empty_cache()
+    return out
+
+
+def bench_dense_prefill(cx, steps, warmup, head):
+    """The dense special case of the headline workload through the same
+    kernels (NEXT to the routed headline figure)."""
+    Ld = dense_variant(cx.layer(HEADLINE), cx.np)
+    r = bench_prefill(cx, HEADLINE, None, steps, warmup, L=Ld)
+    N = r["B"] * r["T"]
+    return {"workload": "dense special case of the 1.3B-class prefill: every head full, every "
+                        "token 16-bit, one SwiGLU expert (d_ff 5632), k = 1",
+            "tokens_per_s": round(N / (r["ms"] * 1e-3), 1), "ms_per_step": round(r["ms"], 4),
+            "routed_over_dense_tokens_per_s": round(r["ms"] / head["ms"], 3)}
 
 
 def summarize_pmc(fetch_dir, write_dir, regex):
@@ -447,25 +571,38 @@ def summarize_pmc(fetch_dir, write_dir, regex):
     print(f"hbm_bytes_per_launch: {total:.0f}")
 
 
-def cpu_baseline(np):
-    """The CPU oracle (fp64 numpy) on the whole prefill workload (8 x 2048
-    tokens), on the host cores."""
-    import gen
+def cpu_baseline(L):
+    """The CPU oracle (fp64 numpy) on a bounded sample of the headline
+    workload `L`: its first sequence (4096 tokens) as a one-sequence prefill,
+    the whole layer, with BLAS threads set to every core of the affinity
+    mask."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
     import oracle
+    cores = len(os.sched_getaffinity(0))
+    model = "unknown"
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        threads = len(os.sched_getaffinity(0))
-    L = gen.make_layer(PREFILL, 1)
-    N = L["cfg"]["B"] * L["cfg"]["T"]
-    t0 = time.perf_counter()
-    oracle.layer_prefill(L)
-    dt = time.perf_counter() - t0
-    return {"value": round(N / dt, 2), "unit": "tokens/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"the whole prefill workload (8 x 2048 tokens) through the fp64 oracle, "
-                      f"{dt:.1f} s"}
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    L = dict(L)
+    T = L["cfg"]["T"]
+    L["cfg"] = dict(L["cfg"], B=1)
+    L["x"], L["psi"] = np.ascontiguousarray(L["x"][:T]), np.ascontiguousarray(L["psi"][:T])
+    with threadpool_limits(limits=cores):
+        t0 = time.perf_counter()
+        oracle.layer_prefill(L)
+        dt = time.perf_counter() - t0
+    return {"value": round(T / dt, 2), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "cpu_model": model,
+            "sample": f"the first 4096-token sequence of the 1.3B-class prefill workload as a "
+                      f"one-sequence layer (router, cache, attention, experts) through the "
+                      f"fp64 oracle, {dt:.1f} s"}
 
 
 if __name__ == "__main__":

@@ -511,6 +511,39 @@ __device__ __forceinline__ int xcd_tile(int L, int total) {
   return x * per + min(x, extra) + (L >> 3);
 }
 
+// Order of the tiles handed to one XCD.  The 32 CUs of an XCD run 32
+// consecutive tiles of its share at a time and stream their K loops in near
+// lockstep, so what that XCD's L2 must hold per K step is the union of their
+// operand slices.  Walking the tiles in bands of BAND_R row tiles (of one
+// expert, for grouped problems), each band in chunks of BAND_R x BAND_C
+// tiles with the row fastest, makes that union BAND_R A slices and BAND_C B
+// slices instead of one A slice and 32 B slices (the expert weights would
+// otherwise stream past the L2 once per row tile).
+constexpr int BAND_R = 16, BAND_C = 2;
+
+// Tile t of a rows x ny grid walked in bands -> (row tile i, column tile j).
+__device__ __forceinline__ void band_order(int t, int rows, int ny, int &i, int &j) {
+  const int band = t / (BAND_R * ny);
+  const int rem = t - band * BAND_R * ny;
+  const int rb = min(BAND_R, rows - band * BAND_R);  // rows of this band
+  const int chunk = rem / (rb * BAND_C);
+  const int idx = rem - chunk * rb * BAND_C;
+  i = band * BAND_R + idx % rb;
+  j = chunk * BAND_C + idx / rb;
+}
+
+// The same within each expert of a grouped problem: tile t lies in the
+// first expert whose tiles (row tiles x ny, in expert order) reach past it.
+__device__ __forceinline__ void grouped_band_order(int t, int ny, const GroupScan &gs, int &bx,
+                                                   int &by) {
+  const uint64_t m = __ballot(gs.incl * ny > t);
+  const int l = __ffsll((unsigned long long)m) - 1;
+  const int nt = __shfl(gs.nt, l, 64), first = __shfl(gs.incl, l, 64) - nt;
+  int i;
+  band_order(t - first * ny, nt, ny, i, by);
+  bx = first + i;
+}
+
 // LDS chunk (16 bytes) of chunk c of operand row r in a stage whose rows are
 // CPR chunks long: a XOR with the row's position in its 256-byte bank span
 // makes the 16 rows read by one 16-lane phase (same c) hit 16 distinct
@@ -742,7 +775,12 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
   auto tile = [&](int l) {  // a tile's fields are wave-uniform: kept in SGPRs
     MTile t;
     const int x = xcd_tile(l, total);
-    p.map(x / ny, x % ny, BM, BN, t, gs);  // every index below total maps to a tile
+    int bx, by;
+    if constexpr (P::GROUPED)
+      grouped_band_order(x, ny, gs, bx, by);
+    else
+      band_order(x, total / ny, ny, bx, by);
+    p.map(bx, by, BM, BN, t, gs);  // every index below total maps to a tile
     t.m0 = __builtin_amdgcn_readfirstlane(t.m0);
     t.n0 = __builtin_amdgcn_readfirstlane(t.n0);
     t.mvalid = __builtin_amdgcn_readfirstlane(t.mvalid);
@@ -1079,10 +1117,14 @@ hipError_t mfma_moe(const triroute_cfg &cfg, int N, const void *n2, const trirou
     return launch<Moe2M, 32, 64, 2, 1, 64, 4>(p2, dff / p2.ksplit, Nk / 32 + E,
                                               (d + 63) / 64 * p2.ksplit, st);
   }
-  const bool w4b = dff >= 128 && d % 192 == 0 && span32({{p2.Wd, wb}}, &alo) &&
+  const bool w4b = dff >= 128 && (d % 192 == 0 || d % 256 == 0) && span32({{p2.Wd, wb}}, &alo) &&
                    span32({{p2.Hm, size_t(Nk) * dff * sizeof(bf16)}}, &alo);
-  return w4b ? launch_w4<Moe2M, 256, 192>(p2, dff, Nk / 256 + E, d / 192, st)
-             : launch<Moe2M, 256, 128, 4, 2, 64, 3>(p2, dff, Nk / 256 + E, (d + 127) / 128, st);
+  if (w4b) {  // 192-wide tiles where they divide d (measured faster), else 256
+    const int mt = Nk / 256 + E;
+    if (d % 192 == 0) return launch_w4<Moe2M, 256, 192>(p2, dff, mt, d / 192, st);
+    return launch_w4<Moe2M, 256, 256>(p2, dff, mt, d / 256, st);
+  }
+  return launch<Moe2M, 256, 128, 4, 2, 64, 3>(p2, dff, Nk / 256 + E, (d + 127) / 128, st);
 }
 
 }  // namespace tr

@@ -133,9 +133,8 @@ MoeWs carve_moe(Carve &cv, const triroute_cfg &c, int N) {
 }
 tr::KvWs carve_kv(Carve &cv, const triroute_cfg &c, int B, int T) {
   tr::KvWs w;
-  w.slots = cv.take<int32_t>(size_t(B) * T);
   w.old_len = cv.take<int32_t>(size_t(B) * 4);
-  w.vstage = cv.take<uint8_t>(size_t(B) * T * c.n_kv_heads * c.head_dim);
+  (void)T;
   return w;
 }
 float *carve_attn_decode(Carve &cv, const triroute_cfg &c, int B) {

@@ -50,12 +50,9 @@ hipError_t launch_compact(const triroute_cfg &cfg, int B, int T, const uint8_t *
                           hipStream_t st);
 // kv.hip
 hipError_t launch_fill_u32(void *p, int64_t n_words, uint32_t v, hipStream_t st);
-// append scratch: slot of every token, each row's pool lengths before the
-// append, staged 2/4-bit V codes (one byte per element)
+// append scratch: each row's pool lengths before the append
 struct KvWs {
-  int32_t *slots;    // [B*T]
   int32_t *old_len;  // [B][4]
-  uint8_t *vstage;   // [B*T][H_kv][d_h]
 };
 hipError_t launch_kv_append(const triroute_cfg &cfg, const CacheView &cv, int B, int T,
                             const int32_t *seq_ids, const void *k, const void *v,

@@ -23,51 +23,52 @@ hipError_t launch_fill_u32(void *p, int64_t n_words, uint32_t v, hipStream_t st)
   return hipGetLastError();
 }
 
-// Per batch row: slots in each width pool, positions, new lengths.
-__global__ __launch_bounds__(256) void kv_slots_kernel(CacheView cv, int T,
-                                                       const int32_t *__restrict__ seq_ids,
-                                                       const uint8_t *__restrict__ bit,
-                                                       int32_t *__restrict__ slots,
-                                                       int32_t *__restrict__ old_len) {
-  __shared__ int wc[4][4];
+// Per batch row: the slot of each new token in its width pool (its rank
+// among the row's earlier tokens of that width, after the pool's current
+// length), its position in the pool's position array, the new lengths, and
+// the pool lengths before the append.  One block of 16 waves per row walks
+// the row's tokens 1024 at a time (ballot counts per wave, then per block).
+__global__ __launch_bounds__(1024) void kv_slots_kernel(CacheView cv, int T,
+                                                        const int32_t *__restrict__ seq_ids,
+                                                        const uint8_t *__restrict__ bit,
+                                                        int32_t *__restrict__ old_len) {
+  constexpr int NW = 16;
+  __shared__ int wc[4][NW];
   const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int s = seq_ids ? seq_ids[b] : b;
   if (s < 0 || s >= cv.n_seq) {
     if (tid == 0) atomicOr(cv.status, int(TRIROUTE_CACHE_BAD_SEQ));
     if (tid < 4) old_len[b * 4 + tid] = -1;
-    for (int t = tid; t < T; t += 256) slots[int64_t(b) * T + t] = -1;
     return;
   }
   const int len0 = cv.seq_len[s];
   if (len0 + T > cv.capacity) {
     if (tid == 0) atomicOr(cv.status, int(TRIROUTE_CACHE_OVERFLOW));
     if (tid < 4) old_len[b * 4 + tid] = -1;
-    for (int t = tid; t < T; t += 256) slots[int64_t(b) * T + t] = -1;
     return;
   }
   int run[4];
 #pragma unroll
   for (int bi = 0; bi < 4; ++bi) run[bi] = cv.pool_len[s * 4 + bi];
   if (tid < 4) old_len[b * 4 + tid] = run[tid];
-  for (int t0 = 0; t0 < T; t0 += 256) {
+  for (int t0 = 0; t0 < T; t0 += 64 * NW) {
     const int t = t0 + tid;
     const int bi = t < T ? int(bit[int64_t(b) * T + t]) : -1;
     uint64_t bal[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) bal[q] = __ballot(bi == q);
-    if (lane == 0)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) wc[q][w] = __popcll(bal[q]);
+    if (lane < 4) wc[lane][w] = __popcll(bal[lane]);
     __syncthreads();
     if (bi >= 0) {
       int slot = run[bi] + __popcll(bal[bi] & lanemask_lt());
       for (int ww = 0; ww < w; ++ww) slot += wc[bi][ww];
-      slots[int64_t(b) * T + t] = slot;
       cv.pos_of(s, bi)[slot] = len0 + t;
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) run[q] += wc[q][0] + wc[q][1] + wc[q][2] + wc[q][3];
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) run[q] += wc[q][ww];
     __syncthreads();
   }
   if (tid == 0) {
@@ -77,21 +78,22 @@ __global__ __launch_bounds__(256) void kv_slots_kernel(CacheView cv, int T,
   }
 }
 
-// One wave per (token, kv head): quantize K and V, write K codes (every
-// 32-bit word of a K record belongs to one slot), scales and 8/16-bit V
-// codes (byte and half-word stores); 2- and 4-bit V codes share words with
-// neighbouring slots and go to vstage, one byte per element, for
-// kv_vpack_kernel (single-token rows: in place, by word atomics).  The K
-// words of the token are assembled in LDS: each lane ORs its element into
-// its word, then one lane per word stores it.
+// One token per row (decode): one wave per (row, kv head), one channel per
+// lane and row of K and V (two on d_h 128): quantize (group min/max by lane
+// reductions), write K codes (every 32-bit word of a K record belongs to one
+// slot; the token's words are assembled in LDS, each lane ORs its element
+// into its word, then one lane per word stores it), scales and 8/16-bit V
+// codes (byte and half-word stores).  2- and 4-bit V codes share words with
+// slots appended earlier: the token's bits of each word are cleared and set
+// in place by word atomics (another row's token of the same word, if any,
+// touches other bits).
 template <typename T>
-__global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int N,
+__global__ __launch_bounds__(256) void kv_token_kernel(CacheView cv, int N,
                                                        const int32_t *__restrict__ seq_ids,
                                                        const T *__restrict__ kin,
                                                        const T *__restrict__ vin,
                                                        const uint8_t *__restrict__ bit,
-                                                       const int32_t *__restrict__ slots,
-                                                       uint8_t *__restrict__ vstage) {
+                                                       const int32_t *__restrict__ old_len) {
   __shared__ uint32_t kw[4][128];  // per wave: the token's K words (at most 4 dh bits... / 32)
   // the wave index, and all that follows from it, in scalar registers: the
   // per-(token, head) bookkeeping (divisions, addresses) runs on the scalar
@@ -99,12 +101,13 @@ __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int item = blockIdx.x * 4 + w;
   const int Hkv = cv.Hkv, dh = cv.dh, G = cv.G;
-  const int i = item / Hkv, g = item % Hkv;
-  const int slot = item < N * Hkv ? __builtin_amdgcn_readfirstlane(slots[i]) : -1;
-  if (slot < 0) return;  // wave-uniform: nothing of this wave touches LDS or a barrier
-  const int b = i / T_;
-  const int s = seq_ids ? __builtin_amdgcn_readfirstlane(seq_ids[b]) : b;
+  const int i = item / Hkv, g = item % Hkv;  // row i = token i
+  if (item >= N * Hkv) return;
   const int bi = __builtin_amdgcn_readfirstlane(int(bit[i]));
+  // the token's slot: its pool's length before the append (-1: row dropped)
+  const int slot = __builtin_amdgcn_readfirstlane(old_len[i * 4 + bi]);
+  if (slot < 0) return;  // wave-uniform: nothing of this wave touches LDS or a barrier
+  const int s = seq_ids ? __builtin_amdgcn_readfirstlane(seq_ids[i]) : i;
   const int bp = cv.bits(bi);
   const int tile = slot / cv.TS, st = slot % cv.TS;
   uint8_t *tp = cv.tile(s, bi, g, tile);
@@ -174,16 +177,9 @@ __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int
         q_word(q, bp, wd, bt);
         uint8_t *addr = vp + ln * (8 * bp) + wd * 4;
         if (bp <= 4) {
-          if (T_ == 1) {
-            // one new token per row: its bits of the shared word are cleared
-            // and set in place (another row's token of the same word, if
-            // any, touches other bits), and kv_vpack is not needed
-            const uint32_t m = ((1u << bp) - 1u) << bt;
-            atomicAnd((uint32_t *)addr, ~m);
-            atomicOr((uint32_t *)addr, e << bt);
-          } else {
-            vstage[(int64_t(i) * Hkv + g) * dh + c] = uint8_t(e);
-          }
+          const uint32_t m = ((1u << bp) - 1u) << bt;
+          atomicAnd((uint32_t *)addr, ~m);
+          atomicOr((uint32_t *)addr, e << bt);
         } else if (bp == 8)
           addr[bt >> 3] = uint8_t(e);
         else if (bp == 16)
@@ -204,55 +200,228 @@ __global__ __launch_bounds__(256) void kv_write_kernel(CacheView cv, int T_, int
   }
 }
 
-// 2- and 4-bit V words: one wave per (batch row, pool, kv head, 32-slot
-// step of the appended range).  A step's words hold only that step's slots,
-// so the wave owns them: lane l builds the words of its record l from the
-// staged codes of the new slots and keeps the bits of slots appended before.
-__global__ __launch_bounds__(256) void kv_vpack_kernel(CacheView cv, int B, int T, int JS,
-                                                       const int32_t *__restrict__ seq_ids,
-                                                       const int32_t *__restrict__ old_len,
-                                                       const uint8_t *__restrict__ vstage) {
-  const int lane = threadIdx.x & 63;
-  int u = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // scalar bookkeeping
+// Quantizer of one group of N values held by one lane (bit exact with the
+// CPU oracle, every step in IEEE fp32): codes, and the fp16 (scale, zero)
+// pair packed as scale | zero << 16.
+template <int BP, int N>
+__device__ __forceinline__ uint32_t quantize_group(const float *x, uint32_t *code) {
+  float mn = x[0], mx = x[0];
+#pragma unroll
+  for (int e = 1; e < N; ++e) {
+    mn = fminf(mn, x[e]);
+    mx = fmaxf(mx, x[e]);
+  }
+  const float levels = float((1 << BP) - 1);
+  const float s32 = __fdiv_rn(mx - mn, levels);
+  const _Float16 s16 = (_Float16)s32;
+  const _Float16 z16 = (_Float16)mn;
+  const float S = (float)s16, Z = (float)z16;
+#pragma unroll
+  for (int e = 0; e < N; ++e) {
+    float q = 0.f;
+    if (S != 0.f) q = fminf(fmaxf(rintf(__fdiv_rn(x[e] - Z, S)), 0.f), levels);
+    code[e] = uint32_t(q);
+  }
+  return uint32_t(*(const uint16_t *)&s16) | (uint32_t(*(const uint16_t *)&z16) << 16);
+}
+
+// One 32-slot step of one pool: see kv_step_kernel.  64 channels of one row
+// of one token per lane; `code` holds its 64 codes (or raw values).
+template <typename T, int DH, int G, int BP>
+__device__ __forceinline__ void kv_step(const CacheView &cv, int s, int bi, int g, int step,
+                                        int old, int nlen, int len0, int64_t row0,
+                                        const T *__restrict__ kin, const T *__restrict__ vin,
+                                        uint8_t *stage) {
+  constexpr bool Q = BP < 16;
+  constexpr int EB = Q ? 1 : BP / 8;  // staged bytes per V element
+  constexpr int TS = 4096 / DH, KS = DH / 32, CB = DH / 16, NG = DH / G;
+  constexpr int NIT = DH == 128 ? 2 : 1;  // 64-channel row pieces per lane
+  const int lane = threadIdx.x & 63, r = lane & 31, hf = lane >> 5;
+  const int Hkv = cv.Hkv;
+  const int sl = step * 32 + r;
+  const bool live = sl >= old && sl < nlen;
+  const int tile = (step * 32) / TS, kvs = ((step * 32) % TS) / 32;  // the step within its tile
+  uint8_t *tp = cv.tile(s, bi, g, tile);
+  const int st = sl % TS;
+  if (live) {
+    const int t = cv.pos_of(s, bi)[sl] - len0;  // the token at the slot's recorded position
+    const int64_t rowoff = ((row0 + t) * Hkv + g) * DH;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const bool isv = NIT == 2 ? it == 1 : hf == 1;
+      const int c0 = NIT == 2 ? 64 * hf : 0;
+      const T *src = (isv ? vin : kin) + rowoff + c0;
+      uint32_t code[64];
+      if constexpr (Q) {
+        float x[64];
+#pragma unroll
+        for (int e = 0; e < 64; e += 8) load8(src + e, x + e);
+        uint8_t *szb = tp + (isv ? cv.v_sz_off(bi) : cv.k_sz_off(bi));
+#pragma unroll
+        for (int gg = 0; gg < 64 / G; ++gg) {
+          const uint32_t sz = quantize_group<BP, G>(x + gg * G, code + gg * G);
+          *(uint32_t *)(szb + (st * NG + c0 / G + gg) * 4) = sz;
+        }
+      } else {
+        // the activation value verbatim (bf16 or fp32 bit patterns)
+        const uint4 *p4 = (const uint4 *)src;
+#pragma unroll
+        for (int x4 = 0; x4 < 64 * int(sizeof(T)) / 16; ++x4) {
+          const uint4 w = p4[x4];
+          const uint32_t wv[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+          for (int y = 0; y < 4; ++y) {
+            if constexpr (sizeof(T) == 2) {
+              code[8 * x4 + 2 * y] = wv[y] & 0xFFFFu;
+              code[8 * x4 + 2 * y + 1] = wv[y] >> 16;
+            } else {
+              code[4 * x4 + y] = wv[y];
+            }
+          }
+        }
+      }
+      if (!isv) {
+        // K: record o * 16 + st % 16 holds channel 32 ks + 8 o + j of the
+        // slot as element q = 8 f + j of field f = (st / 16) KS + ks; this
+        // lane's channels are fields f0 and f0 + 1 (ks = c0 / 32 + u),
+        // code index 32 u + 8 o + j
+        const int f0 = (st >> 4) * KS + (c0 >> 5);
+#pragma unroll
+        for (int o = 0; o < 4; ++o) {
+          uint8_t *rec = tp + (o * 16 + (st & 15)) * 8 * BP;
+          const uint32_t *c = code + 8 * o;
+          if constexpr (BP == 2) {  // one word holds fields f0 (bits 4 j) and f0 + 1 (4 j + 2)
+            uint32_t v = 0;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v |= (c[j] << (4 * j)) | (c[32 + j] << (4 * j + 2));
+            *(uint32_t *)(rec + 4 * (f0 >> 1)) = v;
+          } else if constexpr (BP == 4) {  // one word per field, element j at 8 (j % 4) + 4 (j / 4)
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              uint32_t v = 0;
+#pragma unroll
+              for (int j = 0; j < 8; ++j) v |= c[32 * u + j] << (8 * (j & 3) + 4 * (j >> 2));
+              *(uint32_t *)(rec + 4 * (f0 + u)) = v;
+            }
+          } else if constexpr (BP == 8) {  // byte q
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              uint2 v;
+              v.x = c[32 * u] | (c[32 * u + 1] << 8) | (c[32 * u + 2] << 16) | (c[32 * u + 3] << 24);
+              v.y = c[32 * u + 4] | (c[32 * u + 5] << 8) | (c[32 * u + 6] << 16) | (c[32 * u + 7] << 24);
+              *(uint2 *)(rec + 8 * (f0 + u)) = v;
+            }
+          } else if constexpr (BP == 16) {  // half-word q
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              uint4 v;
+              v.x = c[32 * u] | (c[32 * u + 1] << 16);
+              v.y = c[32 * u + 2] | (c[32 * u + 3] << 16);
+              v.z = c[32 * u + 4] | (c[32 * u + 5] << 16);
+              v.w = c[32 * u + 6] | (c[32 * u + 7] << 16);
+              *(uint4 *)(rec + 16 * (f0 + u)) = v;
+            }
+          } else {  // word q
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              *(uint4 *)(rec + 32 * (f0 + u)) = make_uint4(c[32 * u], c[32 * u + 1], c[32 * u + 2], c[32 * u + 3]);
+              *(uint4 *)(rec + 32 * (f0 + u) + 16) = make_uint4(c[32 * u + 4], c[32 * u + 5], c[32 * u + 6], c[32 * u + 7]);
+            }
+          }
+        }
+      } else {
+        // V codes to the wave's stage: [slot r][channel] in EB bytes
+#pragma unroll
+        for (int e = 0; e < 64; ++e) {
+          uint8_t *d = stage + (r * DH + c0 + e) * EB;
+          if constexpr (EB == 1) *d = uint8_t(code[e]);
+          else if constexpr (EB == 2) *(uint16_t *)d = uint16_t(code[e]);
+          else *(uint32_t *)d = code[e];
+        }
+      }
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the wave's stage writes are in
+  __builtin_amdgcn_wave_barrier();
+  // V: record l = lane holds channel 16 cb + l % 16 of slot
+  // 16 (j / 4) + 4 (l / 16) + j % 4 of the step as element q = 8 f + j of
+  // field f = kvs CB + cb; build every word of the step's fields, keeping
+  // the bits of slots appended before this call
+  constexpr int EPW = 32 / BP;  // elements per word
+  uint32_t *rec = (uint32_t *)(tp + cv.v_codes_off(bi) + lane * 8 * BP);
+  const uint32_t mask = BP == 32 ? 0xFFFFFFFFu : ((1u << BP) - 1u);
+#pragma unroll 4
+  for (int wd = kvs * CB * 8 / EPW; wd < (kvs + 1) * CB * 8 / EPW; ++wd) {
+    uint32_t word = 0, keep = 0;
+    bool mine = false;  // the word holds a slot of this call (else it is left alone)
+#pragma unroll
+    for (int e = 0; e < EPW; ++e) {
+      const int j = (wd * EPW + e) & 7;
+      const int slot = step * 32 + 16 * (j >> 2) + 4 * (lane >> 4) + (j & 3);
+      mine |= slot >= old && slot < nlen;
+    }
+    if (!mine) continue;
+#pragma unroll
+    for (int e = 0; e < EPW; ++e) {
+      const int q = wd * EPW + e, f = q >> 3, j = q & 7;
+      const int rs = 16 * (j >> 2) + 4 * (lane >> 4) + (j & 3);
+      const int ch = 16 * (f - kvs * CB) + (lane & 15);
+      int wq, bt;
+      q_word(q, BP, wq, bt);
+      const int slot = step * 32 + rs;
+      if (slot < old) {
+        keep |= mask << bt;
+      } else if (slot < nlen) {
+        const uint8_t *sp = stage + (rs * DH + ch) * EB;
+        const uint32_t cv_ = EB == 1 ? *sp : EB == 2 ? *(const uint16_t *)sp : *(const uint32_t *)sp;
+        word |= cv_ << bt;
+      }
+    }
+    rec[wd] = keep ? (rec[wd] & keep) | word : word;
+  }
+}
+
+// One wave per (batch row b, width pool bi, kv head g, 32-slot step j of the
+// slots this append gives pool bi): lanes 0..31 take the step's slots, one
+// token each (the token at the slot's recorded position); on d_h 128 lane
+// half hf handles channels 64 hf .. 64 hf + 63 of both K and V, on d_h 64
+// half 0 does K and half 1 does V.  A lane quantizes its 64 channels of a
+// row (one or two groups of G), stores its fp16 scale/zero pairs and its
+// slot's K words directly (every K word belongs to one slot), and stages its
+// V codes in LDS; then each lane assembles the V words of one record, which
+// hold codes of several slots, keeping the bits of slots appended before.
+// A step belongs to one wave, so no two waves write a word.
+template <typename T, int DH, int G>
+__global__ __launch_bounds__(256) void kv_step_kernel(CacheView cv, int B, int T_, int JS,
+                                                      const int32_t *__restrict__ seq_ids,
+                                                      const T *__restrict__ kin,
+                                                      const T *__restrict__ vin,
+                                                      const int32_t *__restrict__ old_len) {
+  __shared__ __align__(16) uint8_t stage_all[4][32 * DH * sizeof(T)];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  int u = __builtin_amdgcn_readfirstlane(int(blockIdx.x) * 4 + wave);
   const int j = u % JS;
   u /= JS;
   const int g = u % cv.Hkv;
   u /= cv.Hkv;
-  const int bi = u % 2, b = u / 2;
+  const int bi = u % 4, b = u / 4;
   if (b >= B) return;
-  const int s = seq_ids ? seq_ids[b] : b;
-  const int old = old_len[b * 4 + bi];
+  const int old = __builtin_amdgcn_readfirstlane(old_len[b * 4 + bi]);
   if (old < 0) return;  // row dropped (bad sequence or capacity)
-  const int nlen = cv.pool_len[s * 4 + bi];
+  const int s = seq_ids ? __builtin_amdgcn_readfirstlane(seq_ids[b]) : b;
+  const int nlen = __builtin_amdgcn_readfirstlane(cv.pool_len[s * 4 + bi]);
   const int step = old / 32 + j;
   if (step * 32 >= nlen) return;
-  const int bp = 2 << bi, dh = cv.dh, TS = cv.TS, CB = dh / 16;
-  const int len0 = cv.seq_len[s] - T;
-  const int32_t *pos = cv.pos_of(s, bi);
-  // token of each slot of the step (lanes 0..31), shuffled to the elements
-  const int sl = step * 32 + (lane & 31);
-  const int tok = (sl >= old && sl < nlen) ? b * T + (pos[sl] - len0) : -1;
-  const int tile = step * 32 / TS, kv = (step * 32 % TS) / 32;
-  uint32_t *rec = (uint32_t *)(cv.tile(s, bi, g, tile) + cv.v_codes_off(bi) + lane * 8 * bp);
-  const int per = 16 / bp;  // element pairs per word
-  const int w0 = kv * CB * 8 / (2 * per), w1 = (kv + 1) * CB * 8 / (2 * per);
-  for (int wd = w0; wd < w1; ++wd) {
-    uint32_t word = 0, keep = 0;
-    for (int h = 0; h < 2 * per; ++h) {
-      const int q = 2 * (wd * per + (h >> 1)) + (h & 1);
-      const int f = q >> 3, jj = q & 7;
-      const int sis = 16 * (jj >> 2) + 4 * (lane >> 4) + (jj & 3);  // slot within the step
-      const int ch = 16 * (f % CB) + (lane & 15);
-      int wq, bt;
-      q_word(q, bp, wq, bt);
-      const int slot = step * 32 + sis;
-      const int t = __shfl(tok, sis, 64);
-      if (slot < old)
-        keep |= ((1u << bp) - 1u) << bt;
-      else if (t >= 0)
-        word |= uint32_t(vstage[(int64_t(t) * cv.Hkv + g) * dh + ch]) << bt;
-    }
-    rec[wd] = keep ? (rec[wd] & keep) | word : word;
+  const int len0 = __builtin_amdgcn_readfirstlane(cv.seq_len[s]) - T_;
+  uint8_t *stage = stage_all[wave];
+  const int64_t row0 = int64_t(b) * T_;
+  switch (bi) {
+    case 0: kv_step<T, DH, G, 2>(cv, s, bi, g, step, old, nlen, len0, row0, kin, vin, stage); break;
+    case 1: kv_step<T, DH, G, 4>(cv, s, bi, g, step, old, nlen, len0, row0, kin, vin, stage); break;
+    case 2: kv_step<T, DH, G, 8>(cv, s, bi, g, step, old, nlen, len0, row0, kin, vin, stage); break;
+    default:
+      kv_step<T, DH, G, 8 * int(sizeof(T))>(cv, s, bi, g, step, old, nlen, len0, row0, kin, vin, stage);
+      break;
   }
 }
 
@@ -320,22 +489,39 @@ __global__ void kv_export_kernel(CacheView cv, int seq, int bi, int slot0, int c
 hipError_t launch_kv_append(const triroute_cfg &cfg, const CacheView &cv, int B, int T,
                             const int32_t *seq_ids, const void *k, const void *v,
                             const uint8_t *bit, const KvWs &ws, hipStream_t st) {
-  kv_slots_kernel<<<B, 256, 0, st>>>(cv, T, seq_ids, bit, ws.slots, ws.old_len);
-  const int N = B * T;
-  dim3 grid((N * cfg.n_kv_heads + 3) / 4);
-  if (cfg.act == TRIROUTE_BF16)
-    kv_write_kernel<bf16><<<grid, 256, 0, st>>>(cv, T, N, seq_ids, (const bf16 *)k,
-                                                (const bf16 *)v, bit, ws.slots, ws.vstage);
-  else
-    kv_write_kernel<float><<<grid, 256, 0, st>>>(cv, T, N, seq_ids, (const float *)k,
-                                                 (const float *)v, bit, ws.slots, ws.vstage);
+  kv_slots_kernel<<<B, 1024, 0, st>>>(cv, T, seq_ids, bit, ws.old_len);
+  if (T == 1) {  // one token per row: token-parallel kernel
+    const dim3 g1((B * cfg.n_kv_heads + 3) / 4);
+    if (cfg.act == TRIROUTE_BF16)
+      kv_token_kernel<bf16><<<g1, 256, 0, st>>>(cv, B, seq_ids, (const bf16 *)k, (const bf16 *)v,
+                                                bit, ws.old_len);
+    else
+      kv_token_kernel<float><<<g1, 256, 0, st>>>(cv, B, seq_ids, (const float *)k,
+                                                 (const float *)v, bit, ws.old_len);
+    return hipGetLastError();
+  }
   // 32-slot steps an append can touch in one pool: all T tokens, plus the
   // partly filled step it starts in
   const int JS = (T + 31) / 32 + 1;
-  const int64_t units = int64_t(B) * 2 * cfg.n_kv_heads * JS;
-  if (T > 1)  // single-token rows wrote their 2- and 4-bit V codes in place
-    kv_vpack_kernel<<<dim3(unsigned((units + 3) / 4)), 256, 0, st>>>(cv, B, T, JS, seq_ids,
-                                                                      ws.old_len, ws.vstage);
+  const int64_t units = int64_t(B) * 4 * cfg.n_kv_heads * JS;
+  const dim3 grid(unsigned((units + 3) / 4));
+  const int dh = cfg.head_dim, G = cfg.kv_group;
+#define KV_STEP(TT, DH_, G_) \
+  kv_step_kernel<TT, DH_, G_><<<grid, 256, 0, st>>>(cv, B, T, JS, seq_ids, (const TT *)k, (const TT *)v, ws.old_len)
+#define KV_STEP_T(TT)                                  \
+  do {                                                 \
+    if (dh == 64) {                                    \
+      if (G == 64) KV_STEP(TT, 64, 64); else KV_STEP(TT, 64, 32);    \
+    } else {                                           \
+      if (G == 64) KV_STEP(TT, 128, 64); else KV_STEP(TT, 128, 32);  \
+    }                                                  \
+  } while (0)
+  if (cfg.act == TRIROUTE_BF16)
+    KV_STEP_T(bf16);
+  else
+    KV_STEP_T(float);
+#undef KV_STEP_T
+#undef KV_STEP
   return hipGetLastError();
 }
 

@@ -310,7 +310,7 @@ def moe(xt, L, eidx, egate, act=None):
 
 
 # ------------------------------------------------------------ whole layer
-def layer_prefill(L, rows=None, kv_in=None, xt_in=None, round_act=True):
+def layer_prefill(L, rows=None, kv_in=None, xt_in=None, o_in=None, round_act=True):
     """Prefill of B fresh sequences of T tokens (cache empty beforehand).
 
     ``rows``: token indices whose attention / FFN outputs are wanted (all by
@@ -324,6 +324,9 @@ def layer_prefill(L, rows=None, kv_in=None, xt_in=None, round_act=True):
         values of sequence b to quantize into the cache in place of the
         oracle's own projections; the oracle's quantizer and dequantizer
         still do all of the cache arithmetic;
+      * ``o_in``: [len(rows), H * dh] attention outputs to feed the output
+        projection in place of the oracle's own o (the returned ``o`` stays the
+        oracle's);
       * ``xt_in``: [len(rows), d] first-residual outputs to feed the expert
         block in place of the oracle's own x~.
     ``round_act=False`` holds every tensor handed between operators in fp64
@@ -355,7 +358,8 @@ def layer_prefill(L, rows=None, kv_in=None, xt_in=None, round_act=True):
             o_rows[b * T + t] = o[ti]
         q_all[b], k_all[b], v_all[b] = q, kn, vn
     o = to_native(np.stack([o_rows[int(r)] for r in rows]), act)
-    xt = to_native(oproj(L["x"][rows], o, L["Wo"]), act)
+    oin = o if o_in is None else np.asarray(o_in, np.float64)
+    xt = to_native(oproj(L["x"][rows], oin, L["Wo"]), act)
     xin = xt if xt_in is None else np.asarray(xt_in, np.float64)
     xout, n2, y = moe(xin, L, eidx[rows], egate[rows], act)
     return dict(rows=rows, n1=n1, za=za, ze=ze, zb=zb, mode=mode, bit=bit,
@@ -378,13 +382,15 @@ def decode_cache_seq(cfg, s, context=None):
     return khat, vhat, stored, bits
 
 
-def layer_decode(L, seqs=None, context=None, kv_in=None, xt_in=None, round_act=True):
+def layer_decode(L, seqs=None, context=None, kv_in=None, xt_in=None, o_in=None,
+                 round_act=True):
     """One decode step: each sequence b gets one new token at position
     P = ctx; its K/V are appended at the routed width, then its query heads
     attend over the read-back cache [0, P] (or its last w keys).
 
     ``context``: as in ``decode_cache_seq``.  ``kv_in`` ({s: (k, v)}, each
-    [1, Hkv, dh]), ``xt_in`` and ``round_act``: as in ``layer_prefill``."""
+    [1, Hkv, dh]), ``o_in``, ``xt_in`` and ``round_act``: as in
+    ``layer_prefill``."""
     cfg = L["cfg"]
     B, H, w, ctx = cfg["B"], cfg["H"], cfg["w"], cfg["ctx"]
     act = cfg["act"] if round_act else "f64"
@@ -408,7 +414,8 @@ def layer_decode(L, seqs=None, context=None, kv_in=None, xt_in=None, round_act=T
                               mode[s:s + 1], w)[0]
         del khat, vhat
     o = to_native(o, act)
-    xt = to_native(oproj(L["x"][rows], o, L["Wo"]), act)
+    oin = o if o_in is None else np.asarray(o_in, np.float64)
+    xt = to_native(oproj(L["x"][rows], oin, L["Wo"]), act)
     xin = xt if xt_in is None else np.asarray(xt_in, np.float64)
     xout, n2, y = moe(xin, L, eidx[rows], egate[rows], act)
     return dict(rows=rows, n1=n1, za=za, ze=ze, zb=zb, mode=mode, bit=bit,

@@ -568,11 +568,17 @@ struct StreamGeo {
 
 // s_waitcnt vmcnt(n) for a run-time n, rounded down to a value the tree
 // covers (waiting for fewer outstanding transfers is always safe): exact
-// below 4, then multiples of 4 up to 24.
+// below 4, then multiples of 4 up to 24, then multiples of 8 up to 56.
 __device__ __forceinline__ void wait_vm_le(int n) {
   if (n >= 12) {
     if (n >= 20) {
-      if (n >= 24) wait_vm<24>(); else wait_vm<20>();
+      if (n >= 40) {
+        if (n >= 56) wait_vm<56>(); else if (n >= 48) wait_vm<48>(); else wait_vm<40>();
+      } else if (n >= 24) {
+        if (n >= 32) wait_vm<32>(); else wait_vm<24>();
+      } else {
+        wait_vm<20>();
+      }
     } else {
       if (n >= 16) wait_vm<16>(); else wait_vm<12>();
     }
@@ -622,18 +628,21 @@ struct Int4 {
 };
 
 // Stream this wave's tiles [w0[bi], w1[bi]) of the four pools, pools in
-// order, through its LDS ring (DEC_RING bytes at rptr / LDS address rbase)
-// used as a byte FIFO: tiles are placed back to back, wrapping to the ring
-// start when one does not fit before the end, and the wave keeps issuing
-// tiles, across pool boundaries, while free space allows.  The consumer
-// walks the pools in the same order with the pool index known at compile
-// time: each resident tile goes to fold(BI, t, lds_pointer), BI an
+// order, through its LDS ring (RING bytes at rptr / LDS address rbase) used
+// as a byte FIFO: tiles are placed back to back, wrapping to the ring start
+// when one does not fit before the end, and the wave keeps issuing tiles,
+// across pool boundaries, while free space allows.  With POS each tile is
+// followed in the ring by the key positions of its TS slots (int32).  The
+// consumer walks the pools in the same order with the pool index known at
+// compile time: each resident tile goes to fold(BI, t, lds_pointer), BI an
 // std::integral_constant.  On entry no other vector-memory load of the wave
 // may be in flight.
-template <int DH, int G, class Fold>
+template <int DH, int G, int RING = DEC_RING, bool POS = false, class Fold>
 __device__ __forceinline__ void stream_tiles(const CacheView &cv, int s, int g, Int4 w0, Int4 w1,
                                              const uint8_t *rptr, uint32_t rbase, Fold &&fold) {
   using SG = StreamGeo<DH, G>;
+  constexpr int PB = POS ? 4 * SG::TS : 0;  // position bytes behind a tile
+  static_assert(((1024 * 16 + PB + 255) & ~255) <= RING, "a 16-bit tile fits the ring");
   // The producer walks the concatenation of the four ranges with one index
   // kp; pool and tile follow from the range ends without branches.
   const int e1 = w1[0] - w0[0], e2 = e1 + w1[1] - w0[1], e3 = e2 + w1[2] - w0[2];
@@ -647,8 +656,8 @@ __device__ __forceinline__ void stream_tiles(const CacheView &cv, int s, int g, 
     while (kp < ktot) {
       const int pb = (kp >= e1) + (kp >= e2) + (kp >= e3);
       const int tb = (1024 << (pb + 1)) + (pb < 3 ? SG::tb(0) - 2048 : 0);
-      const int sz = (tb + 255) & ~255;
-      const int pos = phead + sz <= DEC_RING ? phead : 0;
+      const int sz = (tb + PB + 255) & ~255;
+      const int pos = phead + sz <= RING ? phead : 0;
       bool ok = true;
       if (nin > 0) {
         if (pfree < phead)
@@ -664,20 +673,24 @@ __device__ __forceinline__ void stream_tiles(const CacheView &cv, int s, int g, 
         case 2: issue_tile<DH, G, 2>(cv.tile(s, 2, g, pt), rbase + pos); break;
         default: issue_tile<DH, G, 3>(cv.tile(s, 3, g, pt), rbase + pos); break;
       }
+      if constexpr (POS) {
+        if ((threadIdx.x & 63) < SG::TS / 4)
+          dma16(cv.pos_of(s, pb) + pt * SG::TS + 4 * (threadIdx.x & 63), rbase + pos + tb);
+      }
       phead = pos + sz;
-      issued += (tb + 1023) >> 10;
+      issued += ((tb + 1023) >> 10) + (POS ? 1 : 0);
       ++nin;
       ++kp;
     }
   };
   auto pool = [&](auto BI) {
     constexpr int bi = decltype(BI)::value;
-    constexpr int sz = SG::foot(bi);
+    constexpr int sz = (SG::tb(bi) + PB + 255) & ~255;
     const int t1 = w1[bi];
     for (int t = w0[bi]; t < t1; ++t) {
       produce();
-      const int cpos = chead + sz <= DEC_RING ? chead : 0;  // the producer's placement rule
-      consumed += SG::ni(bi);
+      const int cpos = chead + sz <= RING ? chead : 0;  // the producer's placement rule
+      consumed += SG::ni(bi) + (POS ? 1 : 0);
       wait_vm_le(issued - consumed);
       fold(BI, t, rptr + cpos);
       chead = cpos + sz;
@@ -1146,23 +1159,486 @@ struct PrefillArgs {
   float scale2;
 };
 
-// Prefill: one block of 4 waves per (sequence, kv head, head quartet, mode,
-// query tile qt): wave i takes the qt-th 16 compacted queries of head
-// 4 quartet + i of the kv head.  Those queries sit at similar positions, so
-// the block streams the union of their key ranges from every pool once,
-// tile by tile, through a shared LDS ring (each tile with its slots' key
-// positions; direct-to-LDS transfers split over the waves, D - 1 tiles
-// ahead) and every wave folds every tile with its own position masks.
-constexpr int PF_WAVES = 4;
-constexpr int PF_D = 3;  // ring slots
+// Prefill: one block of two waves per (sequence, kv head, head quartet,
+// mode, query tile qt); wave w takes the qt-th 16 compacted queries of heads
+// 2w and 2w + 1 of the quartet: two 16-column blocks that share every K and
+// V operand, so each code field of a tile is converted once per two heads.
+// The quartet's queries sit at similar positions; the block streams the
+// union of their key ranges from every pool once, through an LDS byte FIFO
+// shared by the two waves (each tile followed by its slots' key positions;
+// the transfers split over the waves), and every wave masks per head and key
+// by position.  A head whose columns all miss a tile skips it.
+constexpr int PF_WAVES = 2;
+constexpr int PF_HEADS = 2;                    // heads per wave
+constexpr int PF_RING = 40 * 1024 - 512;       // four blocks (eight waves) per CU
+// Lazy rescale threshold (log2 units): P' = fp16(p * s_v) with p <= 2^PF_TAU
+// stays finite for value scales up to 65504 / 2^PF_TAU = 1023.
+constexpr float PF_TAU = 6.f;
+
+// v_max3_f32 / v_max_f32 on scores that are never NaN (fmaxf would first
+// quiet each operand).
+__device__ __forceinline__ float vmax3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+__device__ __forceinline__ float vmax(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+// max_rows without quieting
+__device__ __forceinline__ float vmax_rows(float x) {
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+  x = vmax(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+  const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+  return vmax(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
+}
+
+// fp16(a * s) with s the fp16 in bits 0..15 of sw, rounded once: into bits
+// 0..15 of a fresh word (mixlo; bits 16..31 left as they were) or into bits
+// 16..31 of w (mixhi; bits 0..15 kept).
+__device__ __forceinline__ uint32_t mul_f16_lo(float a, uint32_t sw) {
+  uint32_t r;
+  asm("v_fma_mixlo_f16 %0, %1, %2, 0 op_sel_hi:[0,1,0]" : "=v"(r) : "v"(a), "v"(sw));
+  return r;
+}
+__device__ __forceinline__ uint32_t mul_f16_hi(uint32_t w, float a, uint32_t sw) {
+  asm("v_fma_mixhi_f16 %0, %1, %2, 0 op_sel_hi:[0,1,0]" : "+v"(w) : "v"(a), "v"(sw));
+  return w;
+}
+
+// Lower bounds, in the sorted key positions of pool k % 4 of sequence s, of
+// key[k] for eight (pool, key) pairs at once: each round probes 64 evenly
+// spaced entries of every range still longer than 64, the eight loads in
+// flight together.  A key <= 0 has bound 0 (positions are >= 0).  Called by
+// the whole wave with wave-uniform arguments.
+__device__ __forceinline__ void lower_bounds8(const CacheView &cv, int s, const int *len,
+                                              const int *key, int *res) {
+  const int lane = threadIdx.x & 63;
+  int lo[8], hi[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    lo[k] = 0;
+    hi[k] = key[k] <= 0 ? 0 : len[k & 3];
+  }
+  for (;;) {
+    bool more = false;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) more |= hi[k] - lo[k] > 64;
+    if (!more) break;
+    int v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int span = hi[k] - lo[k];
+      v[k] = 0;
+      if (span > 64) v[k] = cv.pos_of(s, k & 3)[lo[k] + int(int64_t(span) * (lane + 1) / 64) - 1];
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int span = hi[k] - lo[k];
+      if (span > 64) {
+        const int c = __popcll(__ballot(v[k] < key[k]));  // probes 0 .. c-1 lie below the key
+        const int nlo = c > 0 ? lo[k] + int(int64_t(span) * c / 64) : lo[k];
+        const int nhi = c < 64 ? lo[k] + int(int64_t(span) * (c + 1) / 64) - 1 : hi[k];
+        lo[k] = nlo;
+        hi[k] = nhi;
+      }
+    }
+  }
+  int v[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int idx = lo[k] + lane;
+    v[k] = idx < hi[k] ? cv.pos_of(s, k & 3)[idx] : INT_MAX;
+  }
+#pragma unroll
+  for (int k = 0; k < 8; ++k) res[k] = lo[k] + __popcll(__ballot(v[k] < key[k]));
+}
+
+// What a lane needs of a resident prefill tile of width BP (bf16 layer: the
+// 16-bit pool holds bf16), read from LDS in two parts so that the K part is
+// dead before the V part is live: the K lane record, the fp16 scale/zero
+// words of the lane's slots and their key positions (INT_MAX past the pool
+// length); then the V lane record and its scale/zero words.
+template <int DH, int BP, int G>
+struct PfTile {
+  using Gm = Geo<DH>;
+  static constexpr int NG = DH / G;
+  static constexpr int W = PoolTraits<BP>::WORDS;
+  static constexpr bool Q = PoolTraits<BP>::QUANT;
+  static constexpr int KSZ = 1024 * BP, VSZ = 1024 * BP + Gm::TS * NG * 4;
+  static constexpr int TB = 1024 * BP + (Q ? 2 * Gm::TS * NG * 4 : 0);  // codes + scale/zero
+  union Rec {
+    u32x4 v[W / 4];
+    uint32_t w[W];
+  };
+
+  struct K {
+    Rec r;
+    uint32_t sz[Q ? Gm::NB : 1][4 * NG];  // [block][slot i * NG + g]
+    int key[Gm::NB][4];
+    int first, last;  // positions of the first and last slot (last INT_MAX past the length)
+  };
+  struct V {
+    Rec r;
+    uint32_t sz[Q ? Gm::KV : 1][2][4 * NG];  // [step][half][slot i * NG + g]
+  };
+
+  __device__ static __forceinline__ void load_k(K &k, const uint8_t *tp, int slot0, int klen) {
+    const int lane = threadIdx.x & 63, o4 = lane >> 4;
+    const u32x4 *kp = (const u32x4 *)(tp + lane * 8 * BP);
+#pragma unroll
+    for (int x = 0; x < W / 4; ++x) k.r.v[x] = kp[x];
+    if constexpr (Q) {
+      const u32x4 *ks = (const u32x4 *)(tp + KSZ);
+#pragma unroll
+      for (int blk = 0; blk < Gm::NB; ++blk)
+#pragma unroll
+        for (int x = 0; x < NG; ++x) {
+          const u32x4 t = ks[((blk * 16 + 4 * o4) * NG) / 4 + x];
+#pragma unroll
+          for (int y = 0; y < 4; ++y) k.sz[blk][4 * x + y] = t[y];
+        }
+    }
+    const int32_t *pp = (const int32_t *)(tp + TB);
+#pragma unroll
+    for (int blk = 0; blk < Gm::NB; ++blk) {
+      const u32x4 t = *(const u32x4 *)(pp + blk * 16 + 4 * o4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) k.key[blk][i] = int(t[i]);
+    }
+    k.first = __builtin_amdgcn_readfirstlane(pp[0]);
+    k.last = __builtin_amdgcn_readfirstlane(pp[Gm::TS - 1]);
+    if (slot0 + Gm::TS > klen) {  // the pool ends inside this tile
+      k.last = INT_MAX;
+#pragma unroll
+      for (int blk = 0; blk < Gm::NB; ++blk)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          k.key[blk][i] = slot0 + blk * 16 + 4 * o4 + i < klen ? k.key[blk][i] : INT_MAX;
+    }
+  }
+
+  __device__ static __forceinline__ void load_v(V &v, const uint8_t *tp) {
+    const int lane = threadIdx.x & 63, o4 = lane >> 4;
+    const u32x4 *vp = (const u32x4 *)(tp + 512 * BP + lane * 8 * BP);
+#pragma unroll
+    for (int x = 0; x < W / 4; ++x) v.r.v[x] = vp[x];
+    if constexpr (Q) {
+      const u32x4 *vs = (const u32x4 *)(tp + VSZ);
+#pragma unroll
+      for (int kv = 0; kv < Gm::KV; ++kv)
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+          for (int x = 0; x < NG; ++x) {
+            const u32x4 t = vs[((32 * kv + 16 * hb + 4 * o4) * NG) / 4 + x];
+#pragma unroll
+            for (int y = 0; y < 4; ++y) v.sz[kv][hb][4 * x + y] = t[y];
+          }
+    }
+  }
+};
+
+// How a head's 16 columns meet a tile: every key in every column's range
+// (PF_ALL), whole columns out (PF_COLS; `none` per lane), or per key
+// (PF_KEYS: key passes iff key - lo <= span, mod 2^32).
+enum { PF_ALL = 0, PF_COLS = 1, PF_KEYS = 2 };
+
+struct PfMask {
+  uint32_t lo, span;  // lo = 2^32 - 1 and span = 0 for a column without a query
+  int mode;
+  bool none;
+};
+
+// Scores of a whole tile for one head: S^T for the tile's 16-slot blocks
+// from the shared K operands, dequantised per group, masked; one
+// online-softmax update for the tile; leaves exp2(score - m) in p (block
+// blk, slot i at p[4 blk + i]).
+template <int DH, int BP, int G>
+__device__ __forceinline__ void pf_scores(SoftState<DH> &st, const typename PfTile<DH, BP, G>::K &tk,
+                                          const u32x4 (&kop)[Geo<DH>::NB][DH / 32],
+                                          const bf16x8 *qop, const float *qsum, float scale2,
+                                          const PfMask &mk, float (&p)[4 * Geo<DH>::NB]) {
+  constexpr int NB = Geo<DH>::NB, NX = 4 * NB;
+  constexpr int NG = DH / G, gks = G / 32, KS = DH / 32, CB = DH / 16;
+  constexpr bool QUANT = PoolTraits<BP>::QUANT;
+  const int lane = threadIdx.x & 63, o4 = lane >> 4;
+  float x[NX];
+#pragma unroll
+  for (int blk = 0; blk < NB; ++blk) {
+    f32x4 acc[NG];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      acc[ks / gks] =
+          __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_op(kop[blk][ks]), qop[ks], acc[ks / gks], 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float sv = 0.f;
+      if constexpr (QUANT) {
+#pragma unroll
+        for (int g = 0; g < NG; ++g) {
+          float S, Z;
+          unpack_sz(tk.sz[blk][i * NG + g], S, Z);
+          sv = fmaf(S, acc[g][i], sv);
+          sv = fmaf(Z, qsum[g], sv);
+        }
+      } else {
+#pragma unroll
+        for (int g = 0; g < NG; ++g) sv += acc[g][i];
+      }
+      x[4 * blk + i] = sv;
+    }
+  }
+  if (mk.mode == PF_KEYS) {
+#pragma unroll
+    for (int j = 0; j < NX; ++j)
+      x[j] = uint32_t(tk.key[j >> 2][j & 3]) - mk.lo <= mk.span ? x[j] : -INFINITY;
+  } else if (mk.mode == PF_COLS) {
+#pragma unroll
+    for (int j = 0; j < NX; ++j) x[j] = mk.none ? -INFINITY : x[j];
+  }
+  // scores are x * scale2 (log2 domain); the positive factor commutes with the max
+  float mt = vmax3(vmax3(x[0], x[1], x[2]), vmax3(x[3], x[4], x[5]), vmax(x[6], x[7]));
+#pragma unroll
+  for (int j = 8; j < NX; j += 8)
+    mt = vmax3(mt, vmax3(x[j], x[j + 1], x[j + 2]),
+               vmax3(vmax3(x[j + 3], x[j + 4], x[j + 5]), x[j + 6], x[j + 7]));
+  mt = vmax_rows(mt) * scale2;
+  // The running max moves only when some column's tile max exceeds it by
+  // more than PF_TAU: below that the stale max still bounds exp2(score - m)
+  // by 2^PF_TAU, and O, l and zc keep a common scale, so the quotient is
+  // unchanged.
+  if (__builtin_amdgcn_ballot_w64(mt > st.m + PF_TAU)) {
+    const float mnew = fmaxf(st.m, mt);
+    const float corr = __builtin_amdgcn_exp2f(st.m - mnew);
+    st.l *= corr;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) st.zc[g] *= corr;
+    st.m = mnew;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float ci = __shfl(corr, 4 * o4 + i, 64);
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) st.O[cb][i] *= ci;
+    }
+  }
+  const float nm = -st.m;
+  float ps = 0.f;
+#pragma unroll
+  for (int j = 0; j < NX; ++j) {
+    p[j] = __builtin_amdgcn_exp2f(fmaf(x[j], scale2, nm));
+    ps += p[j];
+  }
+  st.l += ps;
+}
+
+// P operands of one step for one head: P' = fp16(p * s_v) per group against
+// the fp16 codes (quantized pools; the zero term goes to zc), P = bf16(p)
+// against the stored bf16 (16-bit pool).
+template <int DH, int BP, int G>
+__device__ __forceinline__ void pf_pack(SoftState<DH> &st, const typename PfTile<DH, BP, G>::V &tv,
+                                        int kv, const float (&p)[4 * Geo<DH>::NB],
+                                        u32x4 (&pk)[DH / G]) {
+  constexpr int NG = DH / G;
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+#pragma unroll
+    for (int jp = 0; jp < 4; ++jp) {
+      const int j0 = 2 * jp, j1 = 2 * jp + 1;  // step slots: block 2 kv + (j >> 2), slot j & 3
+      const float p0 = p[8 * kv + j0], p1 = p[8 * kv + j1];
+      if constexpr (PoolTraits<BP>::QUANT) {
+        const uint32_t w0 = tv.sz[kv][j0 >> 2][(j0 & 3) * NG + g];
+        const uint32_t w1 = tv.sz[kv][j1 >> 2][(j1 & 3) * NG + g];
+        pk[g][jp] = mul_f16_hi(mul_f16_lo(p0, w0), p1, w1);
+        const uint16_t z0 = uint16_t(w0 >> 16), z1 = uint16_t(w1 >> 16);
+        st.zc[g] = fmaf(p0, float(*(const _Float16 *)&z0), st.zc[g]);
+        st.zc[g] = fmaf(p1, float(*(const _Float16 *)&z1), st.zc[g]);
+      } else {
+        pk[g][jp] = pk_bf16(p0, p1);
+      }
+    }
+  }
+}
+
+// Fold one resident tile (pool width BP, first slot slot0, pool length klen)
+// into the heads' states: the scores of every head from K operands converted
+// once, then per 32-slot step O += P' V with each V field converted once.
+template <int DH, int BP, int G>
+__device__ __forceinline__ void pf_tile(SoftState<DH> (&st)[PF_HEADS], const uint8_t *tp, int slot0,
+                                        int klen, const ColMask (&cm)[PF_HEADS],
+                                        const uint32_t (&mlo)[PF_HEADS],
+                                        const uint32_t (&mspan)[PF_HEADS],
+                                        const bool (&act)[PF_HEADS],
+                                        const bf16x8 (&qop)[PF_HEADS][DH / 32],
+                                        const float (&qsum)[PF_HEADS][DH / G], float scale2) {
+  using Gm = Geo<DH>;
+  using PT = PfTile<DH, BP, G>;
+  constexpr int KS = DH / 32, CB = DH / 16, NG = DH / G;
+  typename PT::K tk;
+  PT::load_k(tk, tp, slot0, klen);
+  PfMask mk[PF_HEADS];
+  bool run[PF_HEADS];
+#pragma unroll
+  for (int hq = 0; hq < PF_HEADS; ++hq) {
+    const bool none = cm[hq].lo > cm[hq].hi || tk.last < cm[hq].lo || tk.first > cm[hq].hi;
+    const bool all = tk.first >= cm[hq].lo && tk.last <= cm[hq].hi;
+    run[hq] = act[hq] && __builtin_amdgcn_ballot_w64(!none) != 0;
+    mk[hq].lo = mlo[hq];
+    mk[hq].span = mspan[hq];
+    mk[hq].none = none;
+    mk[hq].mode = __builtin_amdgcn_ballot_w64(!none && !all) ? PF_KEYS
+                  : __builtin_amdgcn_ballot_w64(none)        ? PF_COLS
+                                                             : PF_ALL;
+  }
+  float p[PF_HEADS][4 * Gm::NB];
+  {
+    u32x4 kop[Gm::NB][KS];
+#pragma unroll
+    for (int blk = 0; blk < Gm::NB; ++blk)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kop[blk][ks] = kfield<BP>(tk.r.w, blk * KS + ks);
+#pragma unroll
+    for (int hq = 0; hq < PF_HEADS; ++hq)
+      if (run[hq]) pf_scores<DH, BP, G>(st[hq], tk, kop, qop[hq], qsum[hq], scale2, mk[hq], p[hq]);
+  }
+  typename PT::V tv;
+  PT::load_v(tv, tp);
+#pragma unroll
+  for (int kv = 0; kv < Gm::KV; ++kv) {
+    u32x4 pk[PF_HEADS][NG];
+#pragma unroll
+    for (int hq = 0; hq < PF_HEADS; ++hq)
+      if (run[hq]) pf_pack<DH, BP, G>(st[hq], tv, kv, p[hq], pk[hq]);
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      const int g = (16 * cb) / G;
+      if constexpr (PT::Q) {
+        const f16x8 bv = vfield_h<BP>(tv.r.w, kv * CB + cb);
+#pragma unroll
+        for (int hq = 0; hq < PF_HEADS; ++hq)
+          if (run[hq])
+            st[hq].O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_h(pk[hq][g]), bv, st[hq].O[cb],
+                                                                  0, 0, 0);
+      } else {
+        const bf16x8 bv = field16(tv.r.w, kv * CB + cb);
+#pragma unroll
+        for (int hq = 0; hq < PF_HEADS; ++hq)
+          if (run[hq])
+            st[hq].O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_op(pk[hq][g]), bv,
+                                                                   st[hq].O[cb], 0, 0, 0);
+      }
+    }
+  }
+}
+
+// The block's tiles [w0[bi], w1[bi]) of the four pools, pools in order,
+// through one LDS byte FIFO (RING bytes at rptr / LDS address rbase) shared
+// by the NW waves: the placement rule of stream_tiles (each tile followed by
+// its slots' positions), transfer x of a tile (the positions last) issued by
+// wave x % NW.  Before a tile is folded each wave waits for its own
+// transfers of it and the block meets at a barrier, which also tells every
+// wave that all of them are done with the previous tile, whose space is
+// released only then.  A tile that found no room while the previous one was
+// resident (two wide tiles and the wrap rule) is issued after an extra
+// barrier that releases the previous tile first.  fold(BI, t, lds_pointer)
+// as in stream_tiles.  On entry no other vector-memory load of any wave may
+// be in flight.
+template <int DH, int G, int RING, int NW, class Fold>
+__device__ __forceinline__ void stream_tiles_block(const CacheView &cv, int s, int g, Int4 w0,
+                                                   Int4 w1, const uint8_t *rptr, uint32_t rbase,
+                                                   Fold &&fold) {
+  using SG = StreamGeo<DH, G>;
+  constexpr int PB = 4 * SG::TS;
+  static_assert(((1024 * 16 + PB + 255) & ~255) <= RING, "a 16-bit tile fits the ring");
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // transfers of a width-bi tile: ni(bi) code/scale blocks + 1 for the positions
+  auto own = [&](int bi) { return max(0, (SG::ni(bi) + 1 - wave + NW - 1) / NW); };
+  const int e1 = w1[0] - w0[0], e2 = e1 + w1[1] - w0[1], e3 = e2 + w1[2] - w0[2];
+  const int ktot = e3 + w1[3] - w0[3];
+  const int d0 = w0[0], d1 = w0[1] - e1, d2 = w0[2] - e2, d3 = w0[3] - e3;
+  int kp = 0;
+  int phead = 0, pfree = 0;  // ring end of the newest tile; start of the oldest resident tile
+  int nin = 0, issued = 0, consumed = 0;  // tiles resident or in flight; own transfers out / used
+  int chead = 0;                          // ring end of the last tile handed to fold
+  auto produce = [&]() {
+    while (kp < ktot) {
+      const int pb = (kp >= e1) + (kp >= e2) + (kp >= e3);
+      const int tb = (1024 << (pb + 1)) + (pb < 3 ? SG::tb(0) - 2048 : 0);
+      const int sz = (tb + PB + 255) & ~255;
+      const int pos = phead + sz <= RING ? phead : 0;
+      bool ok = true;
+      if (nin > 0) {
+        if (pfree < phead)
+          ok = pos == phead || sz <= pfree;
+        else
+          ok = pos == phead && phead + sz <= pfree;
+      }
+      if (!ok) break;
+      const int pt = kp + (pb == 0 ? d0 : pb == 1 ? d1 : pb == 2 ? d2 : d3);
+      const uint8_t *src = cv.tile(s, pb, g, pt);
+      const int ni = (tb + 1023) >> 10;
+      for (int x = wave; x < ni; x += NW)
+        if (x * 1024 + lane * 16 < tb) dma16(src + x * 1024 + lane * 16, rbase + pos + x * 1024);
+      if (ni % NW == wave && lane < SG::TS / 4)
+        dma16(cv.pos_of(s, pb) + pt * SG::TS + 4 * lane, rbase + pos + tb);
+      issued += own(pb);
+      phead = pos + sz;
+      ++nin;
+      ++kp;
+    }
+  };
+  produce();
+  int gi = 0;         // index of the tile being consumed in the concatenated ranges
+  bool held = false;  // the previous tile is still resident
+  auto release = [&]() {
+    if (held) {
+      --nin;
+      pfree = chead;
+      held = false;
+    }
+  };
+  auto pool = [&](auto BI) {
+    constexpr int bi = decltype(BI)::value;
+    constexpr int sz = (SG::tb(bi) + PB + 255) & ~255;
+    const int t1 = w1[bi];
+    for (int t = w0[bi]; t < t1; ++t) {
+      if (kp <= gi) {
+        // not issued yet: the previous tile left no room for it; once every
+        // wave is done with that tile the ring is empty and this one goes in
+        __syncthreads();
+        release();
+        produce();
+      }
+      const int cpos = chead + sz <= RING ? chead : 0;  // the producer's placement rule
+      consumed += own(bi);
+      wait_vm_le(issued - consumed);
+      __syncthreads();  // this tile is in from every wave; every wave is done with the previous
+      release();
+      produce();
+      fold(BI, t, rptr + cpos);
+      chead = cpos + sz;
+      held = true;
+      ++gi;
+    }
+  };
+  pool(std::integral_constant<int, 0>{});
+  pool(std::integral_constant<int, 1>{});
+  pool(std::integral_constant<int, 2>{});
+  pool(std::integral_constant<int, 3>{});
+}
 
 template <int DH, int G>
-__global__ __launch_bounds__(256, 3) void attn_prefill_mfma_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(64 * PF_WAVES) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_prefill_mfma_kernel(PrefillArgs a) {
   using SG = StreamGeo<DH, G>;
-  constexpr int TS = 4096 / DH;
-  constexpr int SLOT = (1024 * 16 + 4 * TS + 255) & ~255;  // widest tile + its positions
-  __shared__ __align__(1024) uint8_t ring[PF_D * SLOT];
-  __shared__ int bounds[4][3];  // per pool: first tile, end tile, length
+  constexpr int TS = SG::TS, KS = DH / 32, NG = DH / G;
+  __shared__ __align__(1024) uint8_t ring[PF_RING];
   const CacheView &cv = a.cv;
   const int lane = threadIdx.x & 63, n16 = lane & 15, o4 = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1180,10 +1656,10 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_mfma_kernel(PrefillArgs a
   const int s = a.seq_ids ? a.seq_ids[b] : b;
   if (s < 0 || s >= cv.n_seq) return;
   const int base = cv.seq_len[s] - a.T;
-  // union of the quartet's key ranges (every wave computes it; block-uniform)
+  // union of the quartet's key ranges (block-uniform: every wave computes it)
   int lo_u = INT_MAX, hi_u = -1;
-  for (int k = 0; k < PF_WAVES && quart * PF_WAVES + k < a.R; ++k) {
-    const int sg = (b * a.H + g * a.R + quart * PF_WAVES + k) * 2 + (m - 1);
+  for (int k = 0; k < PF_WAVES * PF_HEADS && quart * PF_WAVES * PF_HEADS + k < a.R; ++k) {
+    const int sg = (b * a.H + g * a.R + quart * PF_WAVES * PF_HEADS + k) * 2 + (m - 1);
     const int ck = a.cnt[sg];
     if (qt * 16 >= ck) continue;
     const int32_t *lk = a.idx + int64_t(sg) * a.T;
@@ -1191,107 +1667,80 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_mfma_kernel(PrefillArgs a
     lo_u = min(lo_u, m == TRIROUTE_LOCAL ? pmin - a.w + 1 : 0);
     hi_u = max(hi_u, pmax);
   }
+  // this wave's heads: query columns, position bounds, query operands
+  int count[PF_HEADS];
+  bool act[PF_HEADS];
+  ColMask cm[PF_HEADS];
+  uint32_t mlo[PF_HEADS], mspan[PF_HEADS];
+  bf16x8 qop[PF_HEADS][KS];
+  float qsum[PF_HEADS][NG];
+#pragma unroll
+  for (int hq = 0; hq < PF_HEADS; ++hq) {
+    const int hr = (quart * PF_WAVES + wave) * PF_HEADS + hq;
+    const int h = g * a.R + min(hr, a.R - 1);
+    const int seg = (b * a.H + h) * 2 + (m - 1);
+    count[hq] = hr < a.R ? a.cnt[seg] : 0;
+    act[hq] = qt * 16 < count[hq];  // wave-uniform
+    const int32_t *lst = a.idx + int64_t(seg) * a.T;
+    const int j = qt * 16 + n16;
+    const bool valid = act[hq] && j < count[hq];
+    const int t = valid ? lst[j] : 0;
+    const int P = base + t;
+    load_q<DH, G>(a.q + (int64_t(b * a.T + t) * a.H + h) * DH, valid, qop[hq], qsum[hq]);
+    cm[hq].lo = valid ? (m == TRIROUTE_LOCAL ? P - a.w + 1 : 0) : 1;
+    cm[hq].hi = valid ? P : 0;
+    mlo[hq] = valid ? uint32_t(cm[hq].lo) : 0xFFFFFFFFu;
+    mspan[hq] = valid ? uint32_t(cm[hq].hi - cm[hq].lo) : 0u;
+  }
   lo_u = __builtin_amdgcn_readfirstlane(lo_u);
   hi_u = __builtin_amdgcn_readfirstlane(hi_u);
   if (hi_u < 0) return;
-  {  // wave w finds the tile range of pool w
-    const int bi = wave;
-    const int len = cv.pool_len[s * 4 + bi];
-    const int32_t *pos = cv.pos_of(s, bi);
-    const int sa = lower_bound_pos(pos, len, lo_u);
-    const int sb = lower_bound_pos(pos, len, hi_u + 1);
-    if (lane == 0) {
-      bounds[bi][0] = sa < sb ? sa / TS : 0;
-      bounds[bi][1] = sa < sb ? (sb + TS - 1) / TS : 0;
-      bounds[bi][2] = len;
-    }
-  }
-  // this wave's queries
-  const int hr = quart * PF_WAVES + wave;
-  const int h = g * a.R + hr;
-  const int seg = (b * a.H + h) * 2 + (m - 1);
-  const int count = hr < a.R ? a.cnt[seg] : 0;
-  const bool wv = qt * 16 < count;  // wave-uniform
-  const int j = qt * 16 + n16;
-  const bool valid = wv && j < count;
-  const int32_t *lst = a.idx + int64_t(seg) * a.T;
-  const int t = valid ? lst[j] : (wv ? lst[count - 1] : 0);
-  const int P = base + t;
-  bf16x8 qop[DH / 32];
-  float qsum[DH / G];
-  load_q<DH, G>(a.q + (int64_t(b * a.T + t) * a.H + (hr < a.R ? h : 0)) * DH, valid, qop, qsum);
-  ColMask cm;
-  cm.lo = valid ? (m == TRIROUTE_LOCAL ? P - a.w + 1 : 0) : 1;
-  cm.hi = valid ? P : 0;
-  SoftState<DH> st;
-  state_init(st);
-  wait_vm<0>();  // from here on the only vector-memory traffic is the tile stream
-  __syncthreads();
-  Int4 w0, w1, lens;
-  int n = 0;
+  // tile ranges of the union in every pool
+  int len[4], key[8], res[8];
+#pragma unroll
   for (int bi = 0; bi < 4; ++bi) {
-    w0.set(bi, bounds[bi][0]);
-    w1.set(bi, bounds[bi][1]);
-    lens.set(bi, bounds[bi][2]);
-    n += bounds[bi][1] - bounds[bi][0];
+    len[bi] = cv.pool_len[s * 4 + bi];
+    key[bi] = lo_u;
+    key[4 + bi] = hi_u + 1;
   }
-  // transfers of a width-bi tile: ni(bi) code/scale blocks + 1 for the positions;
-  // transfer x is issued by wave x % PF_WAVES
-  auto own = [&](int bi) { return max(0, (SG::ni(bi) + 1 - wave + PF_WAVES - 1) / PF_WAVES); };
-  const uint32_t rbase = lds_addr(ring);
-  int pb = 0, pt = w0[0];  // next tile to issue
-  while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
-  int cb = pb, ct = pt;    // next tile to fold
-  int issued = 0, consumed = 0;  // this wave's transfers
-  auto issue = [&](int slot) {
-    const uint8_t *src = cv.tile(s, pb, g, pt);
-    const uint32_t dst = rbase + slot * SLOT;
-    const int tb = SG::tb(pb), ni = SG::ni(pb);
-    for (int x = wave; x < ni; x += PF_WAVES)
-      if (x * 1024 + lane * 16 < tb) dma16(src + x * 1024 + lane * 16, dst + x * 1024);
-    if (ni % PF_WAVES == wave && lane < TS / 4)
-      dma16(cv.pos_of(s, pb) + pt * TS + 4 * lane, dst + tb);
-    issued += own(pb);
-    ++pt;
-    while (pb < 4 && pt >= w1[pb]) { ++pb; if (pb < 4) pt = w0[pb]; }
-  };
-  for (int i = 0; i < PF_D - 1 && i < n; ++i) issue(i);
-  for (int i = 0; i < n; ++i) {
-    consumed += own(cb);
-    wait_vm_le(issued - consumed);
-    __syncthreads();  // tile i is in from every wave; slot (i - 1) % D is free
-    if (i + PF_D - 1 < n) issue((i + PF_D - 1) % PF_D);
-    if (wv) {
-      const uint8_t *tp = ring + (i % PF_D) * SLOT;
-      const int32_t *kp = (const int32_t *)(tp + SG::tb(cb));
-      switch (cb) {
-        case 0: { TileRegs<DH, 2, G, true> rg; rg.load(tp, cv, 0, ct * TS, kp, lens[0]);
-                  process_tile<DH, 2, G, true>(st, rg, ct * TS, cm, qop, qsum, a.scale2); } break;
-        case 1: { TileRegs<DH, 4, G, true> rg; rg.load(tp, cv, 1, ct * TS, kp, lens[1]);
-                  process_tile<DH, 4, G, true>(st, rg, ct * TS, cm, qop, qsum, a.scale2); } break;
-        case 2: { TileRegs<DH, 8, G, true> rg; rg.load(tp, cv, 2, ct * TS, kp, lens[2]);
-                  process_tile<DH, 8, G, true>(st, rg, ct * TS, cm, qop, qsum, a.scale2); } break;
-        default: { TileRegs<DH, 16, G, true> rg; rg.load(tp, cv, 3, ct * TS, kp, lens[3]);
-                   process_tile<DH, 16, G, true>(st, rg, ct * TS, cm, qop, qsum, a.scale2); } break;
-      }
-    }
-    ++ct;
-    while (cb < 4 && ct >= w1[cb]) { ++cb; if (cb < 4) ct = w0[cb]; }
+  lower_bounds8(cv, s, len, key, res);
+  Int4 w0, w1;
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi) {
+    const int sa = res[bi], sb = res[4 + bi];
+    w0.set(bi, sa < sb ? sa / TS : 0);
+    w1.set(bi, sa < sb ? (sb + TS - 1) / TS : 0);
   }
-  if (!wv) return;
-  state_finish<DH, G>(st);
+  SoftState<DH> st[PF_HEADS];
+#pragma unroll
+  for (int hq = 0; hq < PF_HEADS; ++hq) state_init(st[hq]);
+  wait_vm<0>();  // from here on the only vector-memory traffic is the tile stream
+  stream_tiles_block<DH, G, PF_RING, PF_WAVES>(
+      cv, s, g, w0, w1, ring, lds_addr(ring), [&](auto BI, int t, const uint8_t *tp) {
+        constexpr int bi = decltype(BI)::value;
+        pf_tile<DH, (2 << bi), G>(st, tp, t * TS, len[bi], cm, mlo, mspan, act, qop, qsum,
+                                  a.scale2);
+      });
   // normalise and write: lane (o4, n) holds column 4 o4 + i, channel n + 16 cb
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int col = 4 * o4 + i;
-    const float lc = __shfl(st.l, col, 64);
-    const int jj = qt * 16 + col;
-    if (jj >= count) continue;
-    const int tt = lst[jj];
-    const float inv = lc > 0.f ? 1.f / lc : 0.f;
-    bf16 *orow = a.o + (int64_t(b * a.T + tt) * a.H + h) * DH;
+  for (int hq = 0; hq < PF_HEADS; ++hq) {
+    if (!act[hq]) continue;
+    state_finish<DH, G>(st[hq]);
+    const int h = g * a.R + (quart * PF_WAVES + wave) * PF_HEADS + hq;
+    const int seg = (b * a.H + h) * 2 + (m - 1);
+    const int32_t *lst = a.idx + int64_t(seg) * a.T;
 #pragma unroll
-    for (int cbk = 0; cbk < DH / 16; ++cbk) orow[n16 + 16 * cbk] = f2bf(st.O[cbk][i] * inv);
+    for (int i = 0; i < 4; ++i) {
+      const int col = 4 * o4 + i;
+      const float lc = __shfl(st[hq].l, col, 64);
+      const int jj = qt * 16 + col;
+      if (jj >= count[hq]) continue;
+      const int tt = lst[jj];
+      const float inv = lc > 0.f ? 1.f / lc : 0.f;
+      bf16 *orow = a.o + (int64_t(b * a.T + tt) * a.H + h) * DH;
+#pragma unroll
+      for (int cbk = 0; cbk < DH / 16; ++cbk) orow[n16 + 16 * cbk] = f2bf(st[hq].O[cbk][i] * inv);
+    }
   }
 }
 
@@ -1358,7 +1807,7 @@ hipError_t launch_attn_mfma_prefill(const triroute_cfg &cfg, const CacheView &cv
   a.w = cfg.window;
   a.QT = (T + 15) / 16;
   a.Hkv = cfg.n_kv_heads;
-  a.NQ = (a.R + PF_WAVES - 1) / PF_WAVES;
+  a.NQ = (a.R + PF_WAVES * PF_HEADS - 1) / (PF_WAVES * PF_HEADS);
   a.scale2 = LOG2E / sqrtf(float(cfg.head_dim));
   const int64_t blocks = int64_t(B) * a.Hkv * a.NQ * 2 * a.QT;
   const dim3 grid{unsigned(blocks)};

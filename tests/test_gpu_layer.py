@@ -164,7 +164,7 @@ def test_layer_prefill(name, seed, which):
         kv_in[b] = (gk[sl].reshape(T, Hkv, dh), gv[sl].reshape(T, Hkv, dh))
     # 3-4: the forced chain over every row of the compared sequences
     gxt = npy(t["xt"])
-    r1 = oracle.layer_prefill(L, rows, kv_in=kv_in, xt_in=gxt[rows])
+    r1 = oracle.layer_prefill(L, rows, kv_in=kv_in, o_in=npy(t["o"])[rows], xt_in=gxt[rows])
     flips = []
     for b in seqs:
         for bi, ent in r1["stored"][b].items():
@@ -173,7 +173,7 @@ def test_layer_prefill(name, seed, which):
     note("cache entries moved by a last-bit K/V difference (fraction)", float(np.mean(flips)))
     assert np.mean(flips) < 1e-2
     assert_close(npy(t["o"])[rows], r1["o"].reshape(len(rows), -1), act, "o (forced codes)")
-    assert_close(gxt[rows], r1["xt"], act, "x~ (forced codes)")
+    assert_close(gxt[rows], r1["xt"], act, "x~ (forced o)")
     assert_close(npy(xo)[rows], r1["xout"], act, "x_out (forced x~)")
     # 5: unforced
     f = 1.0 + 2.0 * ROUNDING_SPREAD[name]
@@ -242,7 +242,7 @@ def test_layer_decode(name, nseq):
     kv_in = {s_: (gk[i].reshape(1, Hkv, dh), gv[i].reshape(1, Hkv, dh))
              for i, s_ in enumerate(seqs)}
     gxt = npy(t["xt"])[seqs]
-    r1 = oracle.layer_decode(L, seqs, kv_in=kv_in, xt_in=gxt)
+    r1 = oracle.layer_decode(L, seqs, kv_in=kv_in, o_in=npy(t["o"])[seqs], xt_in=gxt)
     bits_new = npy(t["bit"])
     for s_ in seqs:
         # the whole context fill, then the step's own token at the end of its pool
@@ -255,7 +255,7 @@ def test_layer_decode(name, nseq):
     note("new tokens whose cache entry a last-bit K/V difference moved (fraction)",
          float(np.mean([_codes_differ(r0["stored"][s_], r1["stored"][s_]) for s_ in seqs])))
     assert_close(npy(t["o"])[seqs], r1["o"].reshape(len(seqs), -1), act, "o (forced codes)")
-    assert_close(gxt, r1["xt"], act, "x~ (forced codes)")
+    assert_close(gxt, r1["xt"], act, "x~ (forced o)")
     assert_close(npy(xo)[seqs], r1["xout"], act, "x_out (forced x~)")
     f = 1.0 + 2.0 * ROUNDING_SPREAD[name]
     assert_close(npy(xo)[seqs], r0["xout"], act, "x_out (unforced)", factor=f)

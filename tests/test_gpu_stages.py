@@ -264,24 +264,28 @@ def _fill_cache(c, cache, kk, vv, bits, act, seq_ids=None):
                  seq_ids=None if seq_ids is None else to_dev(np.asarray(seq_ids, np.int32), torch.int32))
 
 
-ATTN_SHAPES = [  # (act, H, Hkv, dh, G, w, B, T)
-    ("f32", 4, 1, 64, 32, 32, 1, 128),
-    ("bf16", 12, 3, 64, 64, 48, 2, 150),
-    ("bf16", 16, 4, 128, 64, 40, 2, 97),
+ATTN_SHAPES = [  # (act, H, Hkv, dh, G, w, B, T, ctx): T queries after ctx cached tokens
+    ("f32", 4, 1, 64, 32, 32, 1, 128, 0),
+    ("bf16", 12, 3, 64, 64, 48, 2, 150, 0),
+    ("bf16", 16, 4, 128, 64, 40, 2, 97, 0),
+    ("bf16", 16, 2, 64, 32, 64, 2, 200, 300),    # 8 heads per kv head: two quartets
+    ("bf16", 6, 3, 128, 32, 50, 2, 120, 0),      # 2 heads per kv head: half quartets
+    ("bf16", 16, 4, 128, 64, 100, 3, 160, 1000),  # long cached context
 ]
 
 
-@pytest.mark.parametrize("act,H,Hkv,dh,G,w,B,T", ATTN_SHAPES)
-def test_attention_prefill(act, H, Hkv, dh, G, w, B, T):
+@pytest.mark.parametrize("act,H,Hkv,dh,G,w,B,T,ctx", ATTN_SHAPES)
+def test_attention_prefill(act, H, Hkv, dh, G, w, B, T, ctx):
     c = tr.make_cfg(256, H, Hkv, dh, w, 4, 1, 512, G, act)
     std = 0.6
-    kk, vv = gen.kv_block(21, B * T, Hkv, dh, act, std)
-    kk, vv = kk.reshape(B, T, Hkv, dh), vv.reshape(B, T, Hkv, dh)
+    P = ctx + T
+    kk, vv = gen.kv_block(21, B * P, Hkv, dh, act, std)
+    kk, vv = kk.reshape(B, P, Hkv, dh), vv.reshape(B, P, Hkv, dh)
     qq = gen.to_act(gen.normal(21, "attn_q", (B, T, H, dh), std), act)
     rng = gen.stream(21, "attn_modes")
     modes = rng.choice(3, size=(B * T, H), p=[0.25, 0.45, 0.30]).astype(np.uint8)
-    bits = rng.integers(0, 4, (B, T)).astype(np.uint8)
-    cache = tr.KVCache(c, B, T + 8)
+    bits = rng.integers(0, 4, (B, P)).astype(np.uint8)
+    cache = tr.KVCache(c, B, P + 8)
     _fill_cache(c, cache, kk, vv, bits, act)
     cm = oracle.compact(modes, np.zeros((B * T, 1), np.int32), B, T, H, 4, 1)
     cmp = tr.CompactionBuffers(c, B, T)
@@ -297,7 +301,7 @@ def test_attention_prefill(act, H, Hkv, dh, G, w, B, T):
     cfgd = dict(G=G)
     for b in range(B):
         khat, vhat, _ = oracle.layer.store_kv(kk[b], vv[b], bits[b], cfgd)
-        ref = oracle.attention_seq(np.asarray(qq[b], np.float64), np.arange(T), khat, vhat,
+        ref = oracle.attention_seq(np.asarray(qq[b], np.float64), ctx + np.arange(T), khat, vhat,
                                    modes[b * T:(b + 1) * T], w)
         assert_close(og[b], ref, act, f"o[b={b}]")
 

@@ -1537,6 +1537,25 @@ __device__ __forceinline__ void pf_tile(SoftState<DH> (&st)[PF_HEADS], const uin
   }
 }
 
+// This wave's share of the transfers of one tile of pool BI (codes and
+// scale/zero from src, then the TS key positions from ps) into LDS address
+// dst: transfer x goes to wave x % NW.
+template <int DH, int G, int BI, int NW>
+__device__ __forceinline__ void issue_tile_split(const uint8_t *src, const int32_t *ps, uint32_t dst,
+                                                 int wave) {
+  using SG = StreamGeo<DH, G>;
+  constexpr int TB = SG::tb(BI), NI = SG::ni(BI);
+  const int lane = threadIdx.x & 63;
+  const uint32_t off = lane * 16;
+#pragma unroll
+  for (int j = 0; j < NI; ++j) {
+    if (j % NW != wave) continue;
+    if ((j + 1) * 1024 <= TB || off < uint32_t(TB - j * 1024))
+      dma16_s(src + j * 1024, off, dst + j * 1024);
+  }
+  if (NI % NW == wave && lane < SG::TS / 4) dma16(ps + 4 * lane, dst + TB);
+}
+
 // The block's tiles [w0[bi], w1[bi]) of the four pools, pools in order,
 // through one LDS byte FIFO (RING bytes at rptr / LDS address rbase) shared
 // by the NW waves: the placement rule of stream_tiles (each tile followed by
@@ -1582,12 +1601,13 @@ __device__ __forceinline__ void stream_tiles_block(const CacheView &cv, int s, i
       }
       if (!ok) break;
       const int pt = kp + (pb == 0 ? d0 : pb == 1 ? d1 : pb == 2 ? d2 : d3);
-      const uint8_t *src = cv.tile(s, pb, g, pt);
-      const int ni = (tb + 1023) >> 10;
-      for (int x = wave; x < ni; x += NW)
-        if (x * 1024 + lane * 16 < tb) dma16(src + x * 1024 + lane * 16, rbase + pos + x * 1024);
-      if (ni % NW == wave && lane < SG::TS / 4)
-        dma16(cv.pos_of(s, pb) + pt * SG::TS + 4 * lane, rbase + pos + tb);
+      const int32_t *ps = cv.pos_of(s, pb) + pt * SG::TS;
+      switch (pb) {  // compile-time pool: no run-time indexing of the cache view's arrays
+        case 0: issue_tile_split<DH, G, 0, NW>(cv.tile(s, 0, g, pt), ps, rbase + pos, wave); break;
+        case 1: issue_tile_split<DH, G, 1, NW>(cv.tile(s, 1, g, pt), ps, rbase + pos, wave); break;
+        case 2: issue_tile_split<DH, G, 2, NW>(cv.tile(s, 2, g, pt), ps, rbase + pos, wave); break;
+        default: issue_tile_split<DH, G, 3, NW>(cv.tile(s, 3, g, pt), ps, rbase + pos, wave); break;
+      }
       issued += own(pb);
       phead = pos + sz;
       ++nin;

@@ -202,26 +202,6 @@ def describe(cfg):
             f"({ex} routing), KV group {cfg['G']}, {cfg['act']}")
 
 
-def dense_variant(L, np):
-    """The dense special case of a routed layer (the standard pre-norm
-    block): every head in full mode, every token 16-bit, one SwiGLU expert
-    (the first), k = 1, the null never chosen, forced through the router
-    biases; same shapes and weights otherwise."""
-    D = dict(L)
-    cfg = dict(L["cfg"], E=1, k=1, experts="dense")
-    if "ctx_bits" in cfg:
-        cfg["ctx_bits"] = (0.0, 0.0, 0.0, 1.0)
-    D["cfg"] = cfg
-    H = cfg["H"]
-    D["ca"] = np.tile(np.array([-50.0, -50.0, 50.0], np.float32), H)
-    D["cb"] = np.array([-50.0, -50.0, -50.0, 50.0], np.float32)
-    D["We"] = np.ascontiguousarray(L["We"][:2])
-    D["ce"] = np.array([-1.0e4, 50.0], np.float32)
-    for n in ("Wg", "Wu", "Wd"):
-        D[n] = L[n][:1]
-    return D
-
-
 def bench_prefill(cx, name, seed, steps, warmup, moe_only=False, L=None):
     """Timed triroute_layer_prefill steps of one prefill workload, then its
     MoE sublayer alone on the same routed inputs."""
@@ -494,7 +474,7 @@ def bench_decode(cx, name, steps, warmup, attn_only=False):
     del r
     torch.cuda.empty_cache()
     # the dense special case through the same kernels
-    Ld = dense_variant(L, np)
+    Ld = cx.gen.dense_variant(L)
     del L
     rd = run_decode_steps(cx, Ld, steps, warmup, dense=True)
     dcfg = Ld["cfg"]
@@ -516,7 +496,7 @@ def bench_decode(cx, name, steps, warmup, attn_only=False):
 def bench_dense_prefill(cx, steps, warmup, head):
     """The dense special case of the headline workload through the same
     kernels (NEXT to the routed headline figure)."""
-    Ld = dense_variant(cx.layer(HEADLINE), cx.np)
+    Ld = cx.gen.dense_variant(cx.layer(HEADLINE))
     r = bench_prefill(cx, HEADLINE, None, steps, warmup, L=Ld)
     N = r["B"] * r["T"]
     return {"workload": "dense special case of the 1.3B-class prefill: every head full, every "

@@ -183,6 +183,27 @@ def make_layer(name: str, seed: int | None = None, *, act: str | None = None,
     return L
 
 
+def dense_variant(L: dict) -> dict:
+    """The dense special case of a routed layer (the standard pre-norm
+    block): every head in full mode, every token 16-bit, one SwiGLU expert
+    (the first), k = 1, the null never chosen, forced through the router
+    biases; same shapes and weights otherwise.  Decode workloads' contexts
+    become all 16-bit."""
+    D = dict(L)
+    cfg = dict(L["cfg"], E=1, k=1, experts="dense")
+    if "ctx_bits" in cfg:
+        cfg["ctx_bits"] = (0.0, 0.0, 0.0, 1.0)
+    D["cfg"] = cfg
+    H = cfg["H"]
+    D["ca"] = np.tile(np.array([-50.0, -50.0, 50.0], np.float32), H)
+    D["cb"] = np.array([-50.0, -50.0, -50.0, 50.0], np.float32)
+    D["We"] = np.ascontiguousarray(L["We"][:2])
+    D["ce"] = np.array([-1.0e4, 50.0], np.float32)
+    for n in ("Wg", "Wu", "Wd"):
+        D[n] = L[n][:1]
+    return D
+
+
 def moe_weights(cfg: dict):
     """SwiGLU expert weights: gate/up [E, d_ff, d], down [E, d, d_ff]."""
     E, d, dff, seed, act = cfg["E"], cfg["d"], cfg["d_ff"], cfg["seed"], cfg["act"]

@@ -12,6 +12,7 @@ invariants the paper states.  Values beyond those pins (the exact numbers of a
 trained layer) are "parity unpinned": the paper prints no worked example.
 """
 from . import quant  # noqa: F401
+from . import cost  # noqa: F401
 from .layer import (  # noqa: F401
     MODE_SKIP, MODE_LOCAL, MODE_FULL, BITS,
     rmsnorm, gelu, silu, softmax, rope,

@@ -135,14 +135,21 @@ def run_prefill(L, D=None):
     return xo, t, cache, c
 
 
-# (workload, seed, sequences compared whole: None = all)
-PREFILL_CASES = [("tiny_f32_prefill", 0, None), ("160m_bf16_prefill", 1, None),
-                 ("1p3b_bf16_prefill", 104, "first_last")]
+# (workload, seed, sequences compared whole: None = all, variant); "dense" =
+# the dense special case (every head full, every token 16-bit, one expert,
+# k = 1) through the same kernels
+PREFILL_CASES = [("tiny_f32_prefill", 0, None, None), ("160m_bf16_prefill", 1, None, None),
+                 ("1p3b_bf16_prefill", 104, "first_last", None),
+                 ("1p3b_bf16_prefill", 104, "first_last", "dense")]
 
 
-@pytest.mark.parametrize("name,seed,which", PREFILL_CASES)
-def test_layer_prefill(name, seed, which):
-    L = layer(name, seed)
+def _variant(L, variant):
+    return gen.dense_variant(L) if variant == "dense" else L
+
+
+@pytest.mark.parametrize("name,seed,which,variant", PREFILL_CASES)
+def test_layer_prefill(name, seed, which, variant):
+    L = _variant(layer(name, seed), variant)
     cfg = L["cfg"]
     act, B, T, H, Hkv, dh = (cfg[x] for x in ("act", "B", "T", "H", "Hkv", "dh"))
     xo, t, cache, c = run_prefill(L)
@@ -154,6 +161,9 @@ def test_layer_prefill(name, seed, which):
         [rows[:128], rows[-128:], gen.stream(seed, "rows").choice(rows, 256, replace=False)]))
     r0 = oracle.layer_prefill(L, sample)
     _check_decisions(t, r0)
+    if variant == "dense":
+        assert (r0["mode"] == oracle.MODE_FULL).all() and (r0["bit"] == 3).all()
+        assert (r0["eidx"] == 1).all()
     gq, gk, gv = npy(t["q"]), npy(t["k"]), npy(t["v"])
     kv_in = {}
     for b in seqs:
@@ -176,7 +186,7 @@ def test_layer_prefill(name, seed, which):
     assert_close(gxt[rows], r1["xt"], act, "x~ (forced o)")
     assert_close(npy(xo)[rows], r1["xout"], act, "x_out (forced x~)")
     # 5: unforced
-    f = 1.0 + 2.0 * ROUNDING_SPREAD[name]
+    f = 1.0 + 2.0 * ROUNDING_SPREAD[name if variant is None else f"{name}/{variant}"]
     assert_close(npy(xo)[sample], r0["xout"], act, "x_out (unforced)", factor=f)
 
 
@@ -213,9 +223,11 @@ def fill_context(c, cache, cfg, act_t):
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("name,nseq", [("410m_bf16_decode", 12), ("1p3b_bf16_decode", 4)])
-def test_layer_decode(name, nseq):
-    L = layer(name)
+@pytest.mark.parametrize("name,nseq,variant", [("410m_bf16_decode", 12, None),
+                                               ("1p3b_bf16_decode", 4, None),
+                                               ("1p3b_bf16_decode", 2, "dense")])
+def test_layer_decode(name, nseq, variant):
+    L = _variant(layer(name), variant)
     cfg = L["cfg"]
     D = DeviceLayer(L)
     c = D.cfg
@@ -235,6 +247,9 @@ def test_layer_decode(name, nseq):
     seqs = [int(x) for x in seqs]
     r0 = oracle.layer_decode(L, seqs)
     _check_decisions(t, r0)
+    if variant == "dense":
+        assert (r0["mode"] == oracle.MODE_FULL).all() and (r0["bit"] == 3).all()
+        assert (r0["eidx"] == 1).all()
     gq, gk, gv = npy(t["q"])[seqs], npy(t["k"])[seqs], npy(t["v"])[seqs]
     assert_close(gq, r0["q"].reshape(len(seqs), -1), act, "q")
     assert_close(gk, r0["k"].reshape(len(seqs), -1), act, "k")
@@ -257,5 +272,5 @@ def test_layer_decode(name, nseq):
     assert_close(npy(t["o"])[seqs], r1["o"].reshape(len(seqs), -1), act, "o (forced codes)")
     assert_close(gxt, r1["xt"], act, "x~ (forced o)")
     assert_close(npy(xo)[seqs], r1["xout"], act, "x_out (forced x~)")
-    f = 1.0 + 2.0 * ROUNDING_SPREAD[name]
+    f = 1.0 + 2.0 * ROUNDING_SPREAD[name if variant is None else f"{name}/{variant}"]
     assert_close(npy(xo)[seqs], r0["xout"], act, "x_out (unforced)", factor=f)

@@ -441,7 +441,8 @@ def test_decode_step_equals_prefill_row(name, T, positions):
 
 # ----------------------------------------------- storage rounding (R28)
 @pytest.mark.parametrize("name", ["tiny_f32_prefill", "160m_bf16_prefill", "410m_bf16_decode",
-                                  "1p3b_bf16_prefill", "1p3b_bf16_decode"])
+                                  "1p3b_bf16_prefill", "1p3b_bf16_decode",
+                                  "1p3b_bf16_prefill/dense", "1p3b_bf16_decode/dense"])
 def test_activation_rounding_spread(name):
     """How far holding the tensors passed between operators in the
     activation dtype (the bf16 model of Sec. 4 Training) moves the layer's
@@ -450,7 +451,10 @@ def test_activation_rounding_spread(name):
     is not discretely forced uses this spread, so it must stay below the
     table the GPU tests read."""
     from _common import ROUNDING_SPREAD, err_ratio
-    L = gen.make_layer(name)
+    base, _, variant = name.partition("/")
+    L = gen.make_layer(base)
+    if variant == "dense":
+        L = gen.dense_variant(L)
     cfg = L["cfg"]
     if cfg["kind"] == "prefill":
         T = cfg["T"]

@@ -222,7 +222,7 @@ int triroute_kv_reset_seq(const triroute_cfg *cfg, const triroute_kv_cache *cach
 /* Synchronises `stream` and copies the cache status word to *status (host). */
 int triroute_kv_status(const triroute_kv_cache *cache, int32_t *status, triroute_stream_t stream);
 
-/* Row a4 (Sec. 3.2 (C)): quantize and append T new tokens to each of B cache
+/* Sec. 3.2 (C) KV bit-width axis: quantize and append T new tokens to each of B cache
  * sequences.  Row b goes to sequence seq_ids[b] (seq_ids NULL: b); its tokens
  * take positions seq_len, seq_len + 1, ... in order, and token (b, t) lands in
  * the pool of width bit[b*T + t] at the next free slot.
@@ -247,7 +247,7 @@ int triroute_kv_export(const triroute_cfg *cfg, const triroute_kv_cache *cache, 
 
 /* ---- per-stage calls ------------------------------------------------------ */
 
-/* Rows a1 + a2 (Sec. 3.3 controller equation, Sec. 3.8 hard decisions):
+/* Sec. 3.3 controller equation, Sec. 3.8 hard decisions:
  *   n1 = RMSNorm(x; g1) (fp32 inside, act out), u = GELU(W1 [n1; psi] + b1),
  *   h = W2 u + b2, h^ = RMSNorm(h; gr), z^a = Wa h^ + ca, z^e = We h^ + ce,
  *   z^b = Wb h^ + cb;  mode[i,h] = argmax_m z^a[h,m] (first maximum),
@@ -261,7 +261,8 @@ int triroute_router(const triroute_cfg *cfg, int B, int T, const void *x, const 
                     int32_t *eidx, float *egate, const triroute_compaction *cmp, void *ws,
                     size_t ws_bytes, triroute_stream_t stream);
 
-/* Row a3: q = Wq n1, k = Wk n1, v = Wv n1 with rotate-half RoPE on q and k
+/* Sec. 3.1 pre-norm block (the attention projections of Norm(x)) with Sec. 4
+ * Models' RoPE: q = Wq n1, k = Wk n1, v = Wv n1 with rotate-half RoPE on q and k
  * at position pos0[b] + t (pos0 NULL: t); pos0 may point into a cache's
  * sequence lengths (see triroute_kv_seq_len_ptr).
  *   n1 act [B*T, d]; q act [B*T, H*dh]; k, v act [B*T, Hkv*dh].
@@ -274,7 +275,7 @@ int triroute_qkv(const triroute_cfg *cfg, int B, int T, const void *n1,
 /* Device pointer to the int32 [n_seq] sequence lengths of a cache. */
 const int32_t *triroute_kv_seq_len_ptr(const triroute_kv_cache *cache);
 
-/* Row a6 (Sec. 3.2 (A)): attention of B*T new queries whose K/V were just
+/* Sec. 3.2 (A) attention-resolution axis: attention of B*T new queries whose K/V were just
  * appended (the T tokens of row b occupy the last T positions of sequence
  * seq_ids[b]).  Query head h of token (b, t) at position P reads kv head
  * h / (H / Hkv): skip -> zeros, local -> keys [P - w + 1, P], full -> [0, P],
@@ -285,18 +286,21 @@ int triroute_attn_prefill(const triroute_cfg *cfg, int B, int T, const int32_t *
                           const triroute_compaction *cmp, void *o, void *ws, size_t ws_bytes,
                           triroute_stream_t stream);
 
-/* Row a7: as triroute_attn_prefill for one new query per sequence (T = 1),
+/* Sec. 3.2 (A) for the Sec. 3.8 left-to-right decode: as triroute_attn_prefill
+ * for one new query per sequence (T = 1),
  * split over KV chunks with a log-sum-exp combine.
  *   q act [B, H*dh]; mode u8 [B, H]; o act [B, H*dh]. */
 int triroute_attn_decode(const triroute_cfg *cfg, int B, const int32_t *seq_ids, const void *q,
                          const triroute_kv_cache *cache, const uint8_t *mode, void *o, void *ws,
                          size_t ws_bytes, triroute_stream_t stream);
 
-/* Row a8 (first residual): xt = x + Wo concat_h(o).  x, xt act [N, d]. */
+/* Sec. 3.1 pre-norm block, first residual: xt = x + Wo concat_h(o).
+ * x, xt act [N, d]. */
 int triroute_oproj(const triroute_cfg *cfg, int n_tok, const void *x, const void *o,
                    const triroute_dense_w *w, void *xt, triroute_stream_t stream);
 
-/* Rows a8 (second norm) + a9 (Sec. 3.2 (B)): n2 = RMSNorm(xt; g2),
+/* Sec. 3.1 second half of the block with the Sec. 3.2 (B) expert axis:
+ * n2 = RMSNorm(xt; g2),
  * x_out = xt + sum over slots with eidx != 0 of egate * f_eidx(n2).
  * Null slots are never computed.  eidx/egate/cmp as produced by
  * triroute_router for the same n_tok = B*T tokens. */

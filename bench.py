@@ -184,6 +184,7 @@ def main():
         for key, name in DECODES.items():
             out[key] = bench_decode(cx, name, ks, ws)
         out["dense_1p3b_prefill"] = bench_dense_prefill(cx, ks, ws, head)
+        out["granularity_1p3b_prefill"] = bench_granularity(cx, ks, ws, head)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cx.layer(HEADLINE))
     print(json.dumps(out), flush=True)
@@ -503,6 +504,22 @@ def bench_dense_prefill(cx, steps, warmup, head):
                         "token 16-bit, one SwiGLU expert (d_ff 5632), k = 1",
             "tokens_per_s": round(N / (r["ms"] * 1e-3), 1), "ms_per_step": round(r["ms"], 4),
             "routed_over_dense_tokens_per_s": round(r["ms"] / head["ms"], 3)}
+
+
+def bench_granularity(cx, steps, warmup, head):
+    """The headline prefill with one attention decision per token and per
+    kv-head group instead of per head (the granularity variants) through the
+    same kernels."""
+    base = cx.layer(HEADLINE)
+    out = {}
+    for label, groups in (("per_token", 1), ("per_kv_group", base["cfg"]["Hkv"])):
+        L = cx.gen.granularity_variant(base, groups)
+        r = bench_prefill(cx, HEADLINE, None, steps, warmup, L=L)
+        N = r["B"] * r["T"]
+        out[label] = {"attn_groups": groups, "tokens_per_s": round(N / (r["ms"] * 1e-3), 1),
+                      "ms_per_step": round(r["ms"], 4),
+                      "over_per_head_tokens_per_s": round(head["ms"] / r["ms"], 3)}
+    return out
 
 
 def summarize_pmc(fetch_dir, write_dir, regex):

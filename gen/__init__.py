@@ -204,6 +204,24 @@ def dense_variant(L: dict) -> dict:
     return D
 
 
+def granularity_variant(L: dict, groups: int) -> dict:
+    """The layer with ``groups`` attention decisions per token instead of one
+    per head (groups = 1: a single per-token decision; groups = H_kv: one
+    per kv-head group): group a keeps the attention-head rows and biases of
+    its first head a H / groups, so its decision is the one that head made
+    in the per-head layer.  Same weights and inputs otherwise."""
+    cfg = dict(L["cfg"])
+    H = cfg["H"]
+    assert H % groups == 0
+    D = dict(L)
+    D["cfg"] = dict(cfg, attn_groups=groups)
+    first = np.arange(groups) * (H // groups)
+    rows = (3 * first[:, None] + np.arange(3)[None, :]).reshape(-1)
+    D["Wa"] = np.ascontiguousarray(L["Wa"][rows])
+    D["ca"] = np.ascontiguousarray(L["ca"][rows])
+    return D
+
+
 def moe_weights(cfg: dict):
     """SwiGLU expert weights: gate/up [E, d_ff, d], down [E, d, d_ff]."""
     E, d, dff, seed, act = cfg["E"], cfg["d"], cfg["d_ff"], cfg["seed"], cfg["act"]

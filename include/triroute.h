@@ -74,7 +74,8 @@ enum triroute_mode { TRIROUTE_SKIP = 0, TRIROUTE_LOCAL = 1, TRIROUTE_FULL = 2 };
  * at most 16 query heads per kv head; kv_group in {32, 64} dividing
  * head_dim; d_router == 128; d_psi <= 32 and a multiple of 4 (W1 rows stay
  * 16-byte aligned); 1 <= top_k <= n_experts + 1 <= 64;
- * d_model and d_ff multiples of 64; 3 * n_heads + n_experts + 5 <= 112;
+ * d_model and d_ff multiples of 64; 3 * A + n_experts + 5 <= 112 (A = attn_groups,
+ * n_heads if 0, a divisor of n_heads);
  * rms_eps > 0. */
 typedef struct triroute_cfg {
   int32_t d_model;
@@ -91,6 +92,12 @@ typedef struct triroute_cfg {
   int32_t act;       /* enum triroute_dtype */
   float rms_eps;     /* all three RMSNorms */
   float rope_theta;  /* rotate-half RoPE base */
+  /* Attention decisions per token (Sec. 3.2 (A): per head or per head group;
+   * the Sec. 5 ablation of a single per-token decision): the attention head
+   * has 3 * attn_groups logits and query head h takes the decision of group
+   * h / (n_heads / attn_groups).  0 means n_heads (one decision per head);
+   * otherwise it must divide n_heads. */
+  int32_t attn_groups;
 } triroute_cfg;
 
 /* Controller weights, fp32 (Sec. 3.3 controller equation; trunk = two-layer
@@ -100,7 +107,8 @@ typedef struct triroute_cfg {
  *   W1 [d_r, d+d_psi] b1 [d_r]      trunk layer 1 (input [n1 ; psi])
  *   W2 [d_r, d_r]     b2 [d_r]      trunk layer 2
  *   gr [d_r]          RMSNorm gain of h
- *   Wa [3H, d_r]      ca [3H]       attention head, logits [H, 3]
+ *   Wa [3A, d_r]      ca [3A]       attention head, logits [A, 3] for the A =
+ *                                   attn_groups (n_heads if 0) decision groups
  *   We [E+1, d_r]     ce [E+1]      expert head (index 0 = null)
  *   Wb [4, d_r]       cb [4]        bit head */
 typedef struct triroute_router_w {

@@ -103,7 +103,9 @@ def to_native(a, act):
 def router_logits(L, tokens=None):
     """Controller equation (Sec. 3.3) on tokens ``tokens`` (all by default).
 
-    Returns n1 (the shared first norm), z^a [n, H, 3], z^e [n, E+1], z^b [n, 4].
+    Returns n1 (the shared first norm), z^a [n, A, 3], z^e [n, E+1], z^b [n, 4]
+    with A attention decisions per token (``cfg["attn_groups"]``, default H:
+    one per head; Sec. 3.2 (A) routes per head or per head group).
     Whitening and the gradient-balance scale are frozen at inference and are
     already folded into (W, c).
     """
@@ -116,7 +118,7 @@ def router_logits(L, tokens=None):
     h = u @ np.asarray(L["W2"], np.float64).T + L["b2"]
     hh = rmsnorm(h, L["gr"])
     za = (hh @ np.asarray(L["Wa"], np.float64).T + L["ca"]).reshape(
-        len(x), cfg["H"], 3)
+        len(x), cfg.get("attn_groups") or cfg["H"], 3)
     ze = hh @ np.asarray(L["We"], np.float64).T + L["ce"]
     zb = hh @ np.asarray(L["Wb"], np.float64).T + L["cb"]
     return n1, za, ze, zb
@@ -130,14 +132,18 @@ def _argmax_first(row):
     return best
 
 
-def decide(za, ze, zb, k):
+def decide(za, ze, zb, k, H=None):
     """Hard inference decisions (Sec. 3.8, Sec. 3.2 (A)-(C)).
 
-    mode[i, h] = argmax over (skip, local, full); bit[i] = argmax over
-    (2, 4, 8, 16) as index 0..3; S_i = the k most probable options of
+    mode[i, h] = argmax over (skip, local, full) of the logits of h's
+    decision group (za [N, A, 3]: query heads h with h // (H / A) == a share
+    group a; A = H, the default, is one decision per head); bit[i] = argmax
+    over (2, 4, 8, 16) as index 0..3; S_i = the k most probable options of
     softmax(z^e) (index 0 = null), gates p_j / sum_{S_i} p.
     """
-    N, H, _ = za.shape
+    N, A, _ = za.shape
+    H = A if H is None else H
+    assert H % A == 0
     mode = np.zeros((N, H), np.uint8)
     bit = np.zeros(N, np.uint8)
     eidx = np.zeros((N, k), np.int32)
@@ -145,7 +151,7 @@ def decide(za, ze, zb, k):
     p = softmax(ze, axis=-1)
     for i in range(N):
         for h in range(H):
-            mode[i, h] = _argmax_first(za[i, h])
+            mode[i, h] = _argmax_first(za[i, h // (H // A)])
         bit[i] = _argmax_first(zb[i])
         # larger probability first, lower index on ties
         order = sorted(range(p.shape[1]), key=lambda j: (-p[i, j], j))
@@ -337,7 +343,7 @@ def layer_prefill(L, rows=None, kv_in=None, xt_in=None, o_in=None, round_act=Tru
     act = cfg["act"] if round_act else "f64"
     N = B * T
     n1, za, ze, zb = router_logits(L)
-    mode, bit, eidx, egate = decide(za, ze, zb, cfg["k"])
+    mode, bit, eidx, egate = decide(za, ze, zb, cfg["k"], cfg["H"])
     cmp = compact(mode, eidx, B, T, H, cfg["E"], cfg["k"])
     rows = np.arange(N) if rows is None else np.asarray(sorted(set(rows)))
     seqs = sorted(set(int(r) // T for r in rows))
@@ -395,7 +401,7 @@ def layer_decode(L, seqs=None, context=None, kv_in=None, xt_in=None, o_in=None,
     B, H, w, ctx = cfg["B"], cfg["H"], cfg["w"], cfg["ctx"]
     act = cfg["act"] if round_act else "f64"
     n1, za, ze, zb = router_logits(L)
-    mode, bit, eidx, egate = decide(za, ze, zb, cfg["k"])
+    mode, bit, eidx, egate = decide(za, ze, zb, cfg["k"], cfg["H"])
     cmp = compact(mode, eidx, B, 1, H, cfg["E"], cfg["k"])
     seqs = list(range(B)) if seqs is None else sorted(set(int(s) for s in seqs))
     rows = np.asarray(seqs)

@@ -37,7 +37,7 @@ class Cfg(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "d_model", "n_heads", "n_kv_heads", "head_dim", "window", "n_experts", "top_k",
         "d_ff", "kv_group", "d_psi", "d_router", "act")] + [
-        ("rms_eps", C.c_float), ("rope_theta", C.c_float)]
+        ("rms_eps", C.c_float), ("rope_theta", C.c_float), ("attn_groups", C.c_int32)]
 
 
 class RouterW(C.Structure):
@@ -152,10 +152,11 @@ def act_dtype(cfg: Cfg):
 
 
 def make_cfg(d_model, n_heads, n_kv_heads, head_dim, window, n_experts, top_k, d_ff,
-             kv_group, act, d_psi=8, d_router=128, rms_eps=1e-6, rope_theta=1e4) -> Cfg:
+             kv_group, act, d_psi=8, d_router=128, rms_eps=1e-6, rope_theta=1e4,
+             attn_groups=0) -> Cfg:
     return Cfg(d_model, n_heads, n_kv_heads, head_dim, window, n_experts, top_k, d_ff,
                kv_group, d_psi, d_router, BF16 if act in ("bf16", BF16) else F32,
-               rms_eps, rope_theta)
+               rms_eps, rope_theta, attn_groups)
 
 
 def validate(cfg: Cfg) -> int:

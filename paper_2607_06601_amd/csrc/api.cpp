@@ -221,8 +221,11 @@ int check_cfg(const triroute_cfg *c) {
   REQUIRE(c->d_psi <= 32 && c->d_psi % 4 == 0, TRIROUTE_E_UNSUPPORTED,
           "d_psi %d: must be a multiple of 4, at most 32", c->d_psi);
   REQUIRE(c->n_experts + 1 <= 64, TRIROUTE_E_UNSUPPORTED, "n_experts + 1 > 64");
-  REQUIRE(3 * c->n_heads + c->n_experts + 5 <= 112, TRIROUTE_E_UNSUPPORTED,
-          "router head count 3H + E + 5 > 112");
+  REQUIRE(c->attn_groups >= 0 && (c->attn_groups == 0 || c->n_heads % c->attn_groups == 0),
+          TRIROUTE_E_INVALID, "attn_groups (%d) must be 0 or divide n_heads (%d)", c->attn_groups,
+          c->n_heads);
+  REQUIRE(3 * tr::attn_groups(*c) + c->n_experts + 5 <= 112, TRIROUTE_E_UNSUPPORTED,
+          "router head count 3A + E + 5 > 112");
   REQUIRE(c->d_model % 64 == 0 && c->d_ff % 64 == 0, TRIROUTE_E_UNSUPPORTED,
           "d_model and d_ff must be multiples of 64");
   return TRIROUTE_OK;

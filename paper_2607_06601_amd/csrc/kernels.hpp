@@ -5,6 +5,10 @@
 
 namespace tr {
 
+// Attention decisions per token (cfg.attn_groups, 0 = one per head).
+inline int attn_groups(const triroute_cfg &c) { return c.attn_groups > 0 ? c.attn_groups : c.n_heads; }
+
+
 // router.hip
 hipError_t router_prepare();
 // trunk K split: ks chunks of kchunk inputs; the trunk partials take

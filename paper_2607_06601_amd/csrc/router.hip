@@ -181,7 +181,7 @@ __global__ __launch_bounds__(512) void router_tail_kernel(
     const float *__restrict__ Wa, const float *__restrict__ ca, const float *__restrict__ We,
     const float *__restrict__ ce, const float *__restrict__ Wb, const float *__restrict__ cb,
     uint8_t *__restrict__ mode, uint8_t *__restrict__ bit, int32_t *__restrict__ eidx,
-    float *__restrict__ egate, int N, int H, int E1, int k, float eps) {
+    float *__restrict__ egate, int N, int H, int A, int E1, int k, float eps) {
   constexpr int TB = RT_TB, DR = RT_DR, LD = RT_LD;
   extern __shared__ __align__(16) float rt_lds[];
   float(*W2s)[LD] = (float(*)[LD])rt_lds;              // [128][LD]
@@ -190,7 +190,7 @@ __global__ __launch_bounds__(512) void router_tail_kernel(
   const int g = threadIdx.x >> 8, tid = threadIdx.x & 255, lane = tid & 63, wave = tid >> 6;
   float(*Us)[LD] = (float(*)[LD])(rt_lds + (DR + RT_NZ + 2 * TB * g) * LD);
   float(*Zs)[LD] = (float(*)[LD])(rt_lds + (DR + RT_NZ + 2 * TB * g + TB) * LD);
-  const int NZ = 3 * H + E1 + 4;
+  const int NZ = 3 * A + E1 + 4;
   for (int i = threadIdx.x; i < DR * DR / 4; i += 512) {
     const int r = i / (DR / 4), c4 = (i % (DR / 4)) * 4;
     const float4 v = *(const float4 *)(W2 + r * DR + c4);
@@ -198,8 +198,8 @@ __global__ __launch_bounds__(512) void router_tail_kernel(
   }
   for (int i = threadIdx.x; i < NZ * DR / 4; i += 512) {
     const int z = i / (DR / 4), c4 = (i % (DR / 4)) * 4;
-    const float *wz = z < 3 * H ? Wa + z * DR
-                      : z < 3 * H + E1 ? We + (z - 3 * H) * DR : Wb + (z - 3 * H - E1) * DR;
+    const float *wz = z < 3 * A ? Wa + z * DR
+                      : z < 3 * A + E1 ? We + (z - 3 * A) * DR : Wb + (z - 3 * A - E1) * DR;
     const float4 v = *(const float4 *)(wz + c4);
     Wzs[z][c4] = v.x; Wzs[z][c4 + 1] = v.y; Wzs[z][c4 + 2] = v.z; Wzs[z][c4 + 3] = v.w;
   }
@@ -310,17 +310,18 @@ __global__ __launch_bounds__(512) void router_tail_kernel(
       zacc[(kk >> 2) & 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(
           Us[lane & 15][kk + (lane >> 4)], Wzs[zr][kk + (lane >> 4)], zacc[(kk >> 2) & 1], 0, 0, 0);
     if (z < NZ) {
-      const float bias = z < 3 * H ? ca[z] : z < 3 * H + E1 ? ce[z - 3 * H] : cb[z - 3 * H - E1];
+      const float bias = z < 3 * A ? ca[z] : z < 3 * A + E1 ? ce[z - 3 * A] : cb[z - 3 * A - E1];
 #pragma unroll
       for (int r = 0; r < 4; ++r) Zs[4 * (lane >> 4) + r][z] = (zacc[0][r] + zacc[1][r]) + bias;
     }
   }
   __syncthreads();
   // modes: one thread per (token, head); argmax, first maximum on ties
+  const int HA = H / A;  // heads per decision group
   for (int it = tid; it < TB * H; it += 256) {
     const int tt = it / H, hh = it - tt * H;
     if (t0 + tt >= N) continue;
-    const float *za = Zs[tt] + 3 * hh;
+    const float *za = Zs[tt] + 3 * (hh / HA);
     int best = 0;
     if (za[1] > za[best]) best = 1;
     if (za[2] > za[best]) best = 2;
@@ -333,7 +334,7 @@ __global__ __launch_bounds__(512) void router_tail_kernel(
     if (t >= N) break;  // wave-uniform
     const float *z = Zs[tt];
     if (lane == 0) {
-      const float *zb = z + 3 * H + E1;
+      const float *zb = z + 3 * A + E1;
       int bb = 0;
       for (int j = 1; j < 4; ++j)
         if (zb[j] > zb[bb]) bb = j;
@@ -341,7 +342,7 @@ __global__ __launch_bounds__(512) void router_tail_kernel(
     }
     // top-k by logit (softmax is monotone), ties to the lower id; the gate
     // renormalises over the selected set, null included
-    const float zj = lane < E1 ? z[3 * H + lane] : -INFINITY;
+    const float zj = lane < E1 ? z[3 * A + lane] : -INFINITY;
     const float zmax = seg_max(zj, 64);
     uint64_t taken = 0;
     float tot = 0.f;
@@ -376,14 +377,14 @@ __global__ __launch_bounds__(256) void router_tail_tok_kernel(
     const float *__restrict__ Wa, const float *__restrict__ ca, const float *__restrict__ We,
     const float *__restrict__ ce, const float *__restrict__ Wb, const float *__restrict__ cb,
     uint8_t *__restrict__ mode, uint8_t *__restrict__ bit, int32_t *__restrict__ eidx,
-    float *__restrict__ egate, int N, int H, int E1, int k, float eps) {
+    float *__restrict__ egate, int N, int H, int A, int E1, int k, float eps) {
   constexpr int DR = RT_DR;
   __shared__ __align__(16) float vs[4][2][DR];  // per wave: u, then h^; z
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int t = blockIdx.x * 4 + wave;
   if (t >= N) return;  // wave-uniform; no barrier below
   float *us = vs[wave][0], *zs = vs[wave][1];
-  const int NZ = 3 * H + E1 + 4;
+  const int NZ = 3 * A + E1 + 4;
   // u = GELU(sum of the KS trunk partials + b1), chunks summed in order
   float p0[RT1_MAXKS], p1[RT1_MAXKS];
 #pragma unroll
@@ -425,8 +426,8 @@ __global__ __launch_bounds__(256) void router_tail_tok_kernel(
   __builtin_amdgcn_wave_barrier();
   // z = [Wa; We; Wb] h^ + [ca; ce; cb]: lane j owns logits j and j + 64
   for (int z = lane; z < NZ; z += 64) {
-    const float *wz = z < 3 * H ? Wa + z * DR : z < 3 * H + E1 ? We + (z - 3 * H) * DR
-                                                                : Wb + (z - 3 * H - E1) * DR;
+    const float *wz = z < 3 * A ? Wa + z * DR : z < 3 * A + E1 ? We + (z - 3 * A) * DR
+                                                                : Wb + (z - 3 * A - E1) * DR;
     float acc = 0.f;
 #pragma unroll 8
     for (int c4 = 0; c4 < DR / 4; ++c4) {
@@ -434,27 +435,28 @@ __global__ __launch_bounds__(256) void router_tail_tok_kernel(
       const float4 u = *(const float4 *)(us + 4 * c4);
       acc = fmaf(x.x, u.x, acc); acc = fmaf(x.y, u.y, acc); acc = fmaf(x.z, u.z, acc); acc = fmaf(x.w, u.w, acc);
     }
-    const float bias = z < 3 * H ? ca[z] : z < 3 * H + E1 ? ce[z - 3 * H] : cb[z - 3 * H - E1];
+    const float bias = z < 3 * A ? ca[z] : z < 3 * A + E1 ? ce[z - 3 * A] : cb[z - 3 * A - E1];
     zs[z] = acc + bias;
   }
   __builtin_amdgcn_wave_barrier();
   // modes: lane h takes head h; argmax, first maximum on ties
+  const int HA = H / A;  // heads per decision group
   for (int hh = lane; hh < H; hh += 64) {
-    const float *za = zs + 3 * hh;
+    const float *za = zs + 3 * (hh / HA);
     int best = 0;
     if (za[1] > za[best]) best = 1;
     if (za[2] > za[best]) best = 2;
     mode[int64_t(t) * H + hh] = uint8_t(best);
   }
   if (lane == 0) {
-    const float *zb = zs + 3 * H + E1;
+    const float *zb = zs + 3 * A + E1;
     int bb = 0;
     for (int j = 1; j < 4; ++j)
       if (zb[j] > zb[bb]) bb = j;
     bit[t] = uint8_t(bb);
   }
   // top-k by logit, ties to the lower id; gates renormalised over the set
-  const float zj = lane < E1 ? zs[3 * H + lane] : -INFINITY;
+  const float zj = lane < E1 ? zs[3 * A + lane] : -INFINITY;
   const float zmax = seg_max(zj, 64);
   uint64_t taken = 0;
   float tot = 0.f;
@@ -498,7 +500,7 @@ hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const fl
   if (N <= 256 && ks <= RT1_MAXKS) {  // few tokens: one wave per token
     router_tail_tok_kernel<<<dim3((N + 3) / 4), 256, 0, st>>>(
         u, ks, w.b1, w.W2, w.b2, w.gr, w.Wa, w.ca, w.We, w.ce, w.Wb, w.cb, mode, bit, eidx, egate,
-        N, cfg.n_heads, cfg.n_experts + 1, cfg.top_k, cfg.rms_eps);
+        N, cfg.n_heads, attn_groups(cfg), cfg.n_experts + 1, cfg.top_k, cfg.rms_eps);
     return hipGetLastError();
   }
   // one block per CU at most (the weights fill most of its LDS), each
@@ -506,7 +508,7 @@ hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const fl
   const int pairs = ((N + RT_TB - 1) / RT_TB + 1) / 2;
   router_tail_kernel<<<dim3(pairs < 256 ? pairs : 256), 512, RT_LDS, st>>>(
       u, ks, w.b1, w.W2, w.b2, w.gr, w.Wa, w.ca, w.We, w.ce, w.Wb, w.cb, mode, bit, eidx, egate, N,
-      cfg.n_heads, cfg.n_experts + 1, cfg.top_k, cfg.rms_eps);
+      cfg.n_heads, attn_groups(cfg), cfg.n_experts + 1, cfg.top_k, cfg.rms_eps);
   return hipGetLastError();
 }
 

@@ -12,9 +12,10 @@ from . import (BF16, Cfg, DenseW, MoeW, RouterW, make_cfg)
 
 def cfg_from(shape: dict, act: str | None = None) -> Cfg:
     """Build a triroute_cfg from a workload shape dict (d, H, Hkv, dh, w, E, k,
-    d_ff, G, act)."""
+    d_ff, G, act; optional attn_groups)."""
     return make_cfg(shape["d"], shape["H"], shape["Hkv"], shape["dh"], shape["w"],
-                    shape["E"], shape["k"], shape["d_ff"], shape["G"], act or shape["act"])
+                    shape["E"], shape["k"], shape["d_ff"], shape["G"], act or shape["act"],
+                    attn_groups=shape.get("attn_groups", 0) or 0)
 
 
 def to_dev(a, dtype, device="cuda"):

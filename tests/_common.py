@@ -28,7 +28,9 @@ ROUNDING_SPREAD = {"tiny_f32_prefill": 0.05, "160m_bf16_prefill": 2.5,
                    "1p3b_bf16_decode": 4.0,
                    # the dense special case of the 1.3B workloads (every head full,
                    # every token 16-bit, one expert)
-                   "1p3b_bf16_prefill/dense": 6.0, "1p3b_bf16_decode/dense": 6.0}
+                   "1p3b_bf16_prefill/dense": 6.0, "1p3b_bf16_decode/dense": 6.0,
+                   # one attention decision per token / per kv-head group
+                   "160m_bf16_prefill/per_token": 3.5, "410m_bf16_decode/per_group": 2.0}
 
 
 def npy(t):

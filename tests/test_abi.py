@@ -36,7 +36,8 @@ def test_library_exports_every_declared_symbol():
 @pytest.mark.parametrize("field,value,code", [
     ("head_dim", 96, -2), ("kv_group", 48, -2), ("n_kv_heads", 5, -1), ("top_k", 10, -1),
     ("act", 7, -1), ("d_router", 64, -2), ("rms_eps", 0.0, -1), ("d_model", 100, -2),
-    ("n_heads", 0, -1), ("d_psi", 6, -2), ("d_psi", 36, -2)])
+    ("n_heads", 0, -1), ("d_psi", 6, -2), ("d_psi", 36, -2), ("attn_groups", 5, -1),
+    ("attn_groups", -1, -1)])
 def test_validate_rejects(field, value, code):
     assert tr.validate(cfg160(**{field: value})) == code
     assert tr.lib().triroute_last_error()
@@ -47,6 +48,8 @@ def test_validate_accepts_every_workload():
     from paper_2607_06601_amd.device import cfg_from
     for name, shape in gen.CONFIGS.items():
         assert tr.validate(cfg_from(shape)) == 0, name
+        for groups in (1, shape["Hkv"]):  # per-token and per-kv-group decisions
+            assert tr.validate(cfg_from(dict(shape, attn_groups=groups))) == 0, (name, groups)
 
 
 def test_workspace_and_cache_sizes():

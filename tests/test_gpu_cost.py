@@ -85,7 +85,7 @@ def test_prefill_executed_equals_accounted(name, seed):
                      tr.workspace(c, tr.OP_LAYER_PREFILL, B, T), taps=s)
     torch.cuda.synchronize()
     _, za, ze, zb = oracle.router_logits(L)
-    mode, bit, eidx, _ = oracle.decide(za, ze, zb, cfg["k"])
+    mode, bit, eidx, _ = oracle.decide(za, ze, zb, cfg["k"], cfg["H"])
     qpos = np.tile(np.arange(T), B)
     acc = cost.cost_terms(cfg, mode, bit, eidx, qpos)
     caches = {}
@@ -113,7 +113,7 @@ def test_decode_executed_equals_accounted():
                     tr.workspace(c, tr.OP_LAYER_DECODE, B, 1), taps=s)
     torch.cuda.synchronize()
     _, za, ze, zb = oracle.router_logits(L)
-    mode, bit, eidx, _ = oracle.decide(za, ze, zb, cfg["k"])
+    mode, bit, eidx, _ = oracle.decide(za, ze, zb, cfg["k"], cfg["H"])
     # the step's cost: its new tokens, each reading the context plus itself;
     # the KV term counts the step's own token (the context was stored before)
     qpos = np.full(B, ctx)

@@ -140,11 +140,20 @@ def run_prefill(L, D=None):
 # k = 1) through the same kernels
 PREFILL_CASES = [("tiny_f32_prefill", 0, None, None), ("160m_bf16_prefill", 1, None, None),
                  ("1p3b_bf16_prefill", 104, "first_last", None),
-                 ("1p3b_bf16_prefill", 104, "first_last", "dense")]
+                 ("1p3b_bf16_prefill", 104, "first_last", "dense"),
+                 ("160m_bf16_prefill", 1, "first_last", "per_token")]
 
 
 def _variant(L, variant):
-    return gen.dense_variant(L) if variant == "dense" else L
+    """dense: the dense special case; per_token / per_group: one attention
+    decision per token / per kv-head group (the granularity variants)."""
+    if variant == "dense":
+        return gen.dense_variant(L)
+    if variant == "per_token":
+        return gen.granularity_variant(L, 1)
+    if variant == "per_group":
+        return gen.granularity_variant(L, L["cfg"]["Hkv"])
+    return L
 
 
 @pytest.mark.parametrize("name,seed,which,variant", PREFILL_CASES)
@@ -225,7 +234,8 @@ def fill_context(c, cache, cfg, act_t):
 
 @pytest.mark.parametrize("name,nseq,variant", [("410m_bf16_decode", 12, None),
                                                ("1p3b_bf16_decode", 4, None),
-                                               ("1p3b_bf16_decode", 2, "dense")])
+                                               ("1p3b_bf16_decode", 2, "dense"),
+                                               ("410m_bf16_decode", 6, "per_group")])
 def test_layer_decode(name, nseq, variant):
     L = _variant(layer(name), variant)
     cfg = L["cfg"]

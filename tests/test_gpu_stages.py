@@ -47,16 +47,24 @@ def run_router(L):
     return dict(n1=n1, mode=mode, bit=bit, eidx=eidx, egate=egate, cmp=cmp)
 
 
-@pytest.mark.parametrize("name,seed", [
-    ("tiny_f32_prefill", 0), ("160m_bf16_prefill", 1), ("410m_bf16_decode", 103),
-    ("1p3b_bf16_prefill", 104), ("1p3b_bf16_decode", 105)])
-def test_router_and_compaction_bit_exact(name, seed):
+@pytest.mark.parametrize("name,seed,groups", [
+    ("tiny_f32_prefill", 0, None), ("160m_bf16_prefill", 1, None), ("410m_bf16_decode", 103, None),
+    ("1p3b_bf16_prefill", 104, None), ("1p3b_bf16_decode", 105, None),
+    # attention decisions per token / per kv-head group instead of per head
+    ("160m_bf16_prefill", 1, 1), ("1p3b_bf16_decode", 105, 4)])
+def test_router_and_compaction_bit_exact(name, seed, groups):
     L = layer(name, seed, moe=False)
+    if groups is not None:
+        L = gen.granularity_variant(L, groups)
     cfg = L["cfg"]
     B, T, H, E, k = cfg["B"], cfg["T"], cfg["H"], cfg["E"], cfg["k"]
     g = run_router(L)
     n1, za, ze, zb = oracle.router_logits(L)
-    mode, bit, eidx, egate = oracle.decide(za, ze, zb, k)
+    mode, bit, eidx, egate = oracle.decide(za, ze, zb, k, H)
+    if groups is not None:
+        R = H // groups
+        assert all((mode[:, a * R:(a + 1) * R] == mode[:, a * R:a * R + 1]).all()
+                   for a in range(groups))
     np.testing.assert_array_equal(npy(g["mode"]), mode)
     np.testing.assert_array_equal(npy(g["bit"]), bit)
     np.testing.assert_array_equal(npy(g["eidx"]), eidx)

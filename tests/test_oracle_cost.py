@@ -67,6 +67,6 @@ def test_dense_variant_decisions_cost_the_dense_reference():
     one expert for every token, so its accounted cost is App. A's reference."""
     L = gen.dense_variant(gen.make_layer("tiny_f32_prefill", act="f64"))
     n1, za, ze, zb = oracle.router_logits(L)
-    mode, bit, eidx, egate = oracle.decide(za, ze, zb, L["cfg"]["k"])
+    mode, bit, eidx, egate = oracle.decide(za, ze, zb, L["cfg"]["k"], L["cfg"]["H"])
     qpos = np.arange(L["cfg"]["T"])
     assert cost.cost_terms(L["cfg"], mode, bit, eidx, qpos) == cost.dense_reference(L["cfg"], qpos)

@@ -442,7 +442,8 @@ def test_decode_step_equals_prefill_row(name, T, positions):
 # ----------------------------------------------- storage rounding (R28)
 @pytest.mark.parametrize("name", ["tiny_f32_prefill", "160m_bf16_prefill", "410m_bf16_decode",
                                   "1p3b_bf16_prefill", "1p3b_bf16_decode",
-                                  "1p3b_bf16_prefill/dense", "1p3b_bf16_decode/dense"])
+                                  "1p3b_bf16_prefill/dense", "1p3b_bf16_decode/dense",
+                                  "160m_bf16_prefill/per_token", "410m_bf16_decode/per_group"])
 def test_activation_rounding_spread(name):
     """How far holding the tensors passed between operators in the
     activation dtype (the bf16 model of Sec. 4 Training) moves the layer's
@@ -455,6 +456,10 @@ def test_activation_rounding_spread(name):
     L = gen.make_layer(base)
     if variant == "dense":
         L = gen.dense_variant(L)
+    elif variant == "per_token":
+        L = gen.granularity_variant(L, 1)
+    elif variant == "per_group":
+        L = gen.granularity_variant(L, L["cfg"]["Hkv"])
     cfg = L["cfg"]
     if cfg["kind"] == "prefill":
         T = cfg["T"]
@@ -475,3 +480,30 @@ def test_activation_rounding_spread(name):
     assert s["xout"] <= ROUNDING_SPREAD[name]
     if act == "f32":
         assert max(s.values()) < 0.05   # fp32 storage is far inside the fp32 tolerance
+
+
+# ------------------------------------------------- decision granularity
+@pytest.mark.parametrize("groups", [1, 2, 4])
+def test_attention_decision_groups(groups):
+    """One attention decision per head group (Sec. 3.2 (A)) or per token (the
+    Sec. 5 granularity ablation): every head of a group takes the decision
+    its group's first head makes in the per-head layer, and groups = H is
+    the per-head layer itself."""
+    L = gen.make_layer("tiny_f32_prefill", act="f64")
+    H, k = L["cfg"]["H"], L["cfg"]["k"]
+    _, za, ze, zb = oracle.router_logits(L)
+    mode_h, bit_h, eidx_h, _ = oracle.decide(za, ze, zb, k, H)
+    V = gen.granularity_variant(L, groups)
+    _, za_g, ze_g, zb_g = oracle.router_logits(V)
+    assert za_g.shape[1] == groups
+    mode_g, bit_g, eidx_g, _ = oracle.decide(za_g, ze_g, zb_g, k, H)
+    R = H // groups
+    for h in range(H):
+        np.testing.assert_array_equal(mode_g[:, h], mode_h[:, (h // R) * R])
+    np.testing.assert_array_equal(bit_g, bit_h)
+    np.testing.assert_array_equal(eidx_g, eidx_h)
+    if groups == H:
+        np.testing.assert_array_equal(mode_g, mode_h)
+    # a group-level mode change moves every head of the group together
+    assert all(len(set(mode_g[i, a * R:(a + 1) * R])) == 1
+               for i in range(len(mode_g)) for a in range(groups))

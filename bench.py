@@ -59,7 +59,8 @@ def parse():
                    help="the headline workload only (no 160M, decode or dense legs)")
     p.add_argument("--only", default=None,
                    choices=("prefill_1p3b", "prefill_160m", "moe_1p3b", "moe_160m",
-                            "decode_410m", "decode_1p3b", "attn_410m", "attn_1p3b"),
+                            "decode_410m", "decode_1p3b", "attn_410m", "attn_1p3b",
+                            "stack_410m"),
                    help="profile one leg alone (prints its section only); moe_* time the "
                         "MoE sublayer, attn_* the decode attention, and both then run a "
                         "256 MiB copy for counter calibration")
@@ -150,6 +151,8 @@ def main():
             r = bench_prefill(cx, HEADLINE, None, args.steps, args.warmup, moe_only=leg == "moe_1p3b")
         elif leg in ("prefill_160m", "moe_160m"):
             r = bench_prefill(cx, SMALL, 1, args.steps, args.warmup, moe_only=leg == "moe_160m")
+        elif leg == "stack_410m":
+            r = bench_stack(cx, args.steps, args.warmup, None)
         else:
             name = DECODES["decode_410m" if leg.endswith("410m") else "decode_1p3b"]
             r = bench_decode(cx, name, args.steps, args.warmup, attn_only=leg.startswith("attn"))
@@ -183,6 +186,7 @@ def main():
         out["prefill_160m"] = bench_small_seeds(cx, ks, ws)
         for key, name in DECODES.items():
             out[key] = bench_decode(cx, name, ks, ws)
+        out["stack_410m_decode"] = bench_stack(cx, ks, ws, out["decode_410m"]["ms_per_step"])
         out["dense_1p3b_prefill"] = bench_dense_prefill(cx, ks, ws, head)
         out["granularity_1p3b_prefill"] = bench_granularity(cx, ks, ws, head)
     if not args.no_cpu_baseline:
@@ -433,6 +437,49 @@ def run_decode_steps(cx, L, steps, warmup, dense=False):
                 for s in range(B)]
     return dict(ms=ms, D=D, c=c, cache=cache, t=t, bits=bits_now,
                 eidx=t["eidx"].cpu().numpy())
+
+
+STACK_LAYERS = 8
+
+
+def bench_stack(cx, steps, warmup, single_ms):
+    """One decode step through a stack of STACK_LAYERS routed layers of the
+    410M-class decode workload (triroute_stack_decode: the next layer's side
+    features from the previous layer's decisions on the device), every layer
+    over its own cache holding the workload's context (the same K/V values
+    and widths in every layer)."""
+    np, torch, tr = cx.np, cx.torch, cx.tr
+    name = "410m_bf16_decode"
+    Ls = cx.gen.make_stack(name, STACK_LAYERS)
+    cfg = Ls[0]["cfg"]
+    B, d = cfg["B"], cfg["d"]
+    Ds = [cx.DeviceLayer(L) for L in Ls]
+    c = Ds[0].cfg
+    caches = [tr.KVCache(c, B, cfg["ctx"] + warmup + steps + 1) for _ in Ds]
+    ctx = cfg["ctx"]
+    aws = tr.workspace(c, tr.OP_KV_APPEND, 1, ctx)
+    for sq in range(B):
+        kk, vv = cx.gen.context_kv(cfg, sq)
+        k_t = cx.to_dev(kk.reshape(ctx, -1), Ds[0].act)
+        v_t = cx.to_dev(vv.reshape(ctx, -1), Ds[0].act)
+        b_t = cx.to_dev(cx.gen.context_bits(cfg, sq), torch.uint8)
+        sid = torch.tensor([sq], dtype=torch.int32, device=cx.dev)
+        for cache in caches:
+            tr.kv_append(c, cache, 1, ctx, k_t, v_t, b_t, aws, seq_ids=sid)
+    torch.cuda.synchronize()
+    ws = tr.workspace(c, tr.OP_STACK_DECODE, B, 1)
+    xo = torch.empty(B, d, dtype=Ds[0].act, device=cx.dev)
+    layers = [(D.rw, D.dw, D.mw) for D in Ds]
+    run = lambda i: tr.stack_decode(c, B, Ds[0].x, Ds[0].psi, layers, caches, xo, ws)
+    for _ in range(warmup):
+        run(0)
+    ms, _ = cx.timed(run, steps)
+    assert all(ca.status() == 0 for ca in caches)
+    return {"workload": f"{STACK_LAYERS}-layer stack of the 410M-class decode step (64 sequences, "
+                        "context 8192 per layer), one decode step through every layer",
+            "layers": STACK_LAYERS, "tokens_per_s": round(B / (ms * 1e-3), 1),
+            "ms_per_step": round(ms, 4), "ms_per_layer": round(ms / STACK_LAYERS, 4),
+            "single_layer_ms": None if single_ms is None else round(single_ms, 4)}
 
 
 def bench_attn(cx, r, cfg, mode_t, steps, label):

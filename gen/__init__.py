@@ -222,6 +222,21 @@ def granularity_variant(L: dict, groups: int) -> dict:
     return D
 
 
+def make_stack(name: str, n_layers: int, seed: int | None = None) -> list:
+    """n_layers routed layers of workload ``name`` for a decode stack: layer 0
+    is ``make_layer(name, seed)`` (its x and psi are the stack's inputs);
+    layer l > 0 draws its weights and its cached context from the seed
+    seed + 7919 l and takes layer 0's calibrated router biases."""
+    L0 = make_layer(name, seed)
+    out = [L0]
+    for l in range(1, n_layers):
+        Ll = make_layer(name, L0["cfg"]["seed"] + 7919 * l, biases={})
+        for b in ("ca", "ce", "cb"):
+            Ll[b] = L0[b].copy()
+        out.append(Ll)
+    return out
+
+
 def moe_weights(cfg: dict):
     """SwiGLU expert weights: gate/up [E, d_ff, d], down [E, d, d_ff]."""
     E, d, dff, seed, act = cfg["E"], cfg["d"], cfg["d_ff"], cfg["seed"], cfg["act"]

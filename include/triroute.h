@@ -201,7 +201,8 @@ enum triroute_op {
   TRIROUTE_OP_ATTN_DECODE = 4,
   TRIROUTE_OP_MOE = 5,
   TRIROUTE_OP_LAYER_PREFILL = 6,
-  TRIROUTE_OP_LAYER_DECODE = 7
+  TRIROUTE_OP_LAYER_DECODE = 7,
+  TRIROUTE_OP_STACK_DECODE = 8
 };
 
 /* ---- configuration, errors, sizes ---------------------------------------- */
@@ -334,6 +335,35 @@ int triroute_layer_decode(const triroute_cfg *cfg, int B, const int32_t *seq_ids
                           const triroute_dense_w *dw, const triroute_moe_w *mw,
                           const triroute_kv_cache *cache, void *x_out,
                           const triroute_layer_taps *taps, void *ws, size_t ws_bytes,
+                          triroute_stream_t stream);
+
+/* ---- a stack of routed layers ------------------------------------------- */
+
+/* The weights of one routed layer. */
+typedef struct triroute_layer_w {
+  triroute_router_w router;
+  triroute_dense_w dense;
+  triroute_moe_w moe;
+} triroute_layer_w;
+
+/* One decode step of B sequences through n_layers routed layers (Sec. 3.8:
+ * one left-to-right pass, per-token decisions taken layer by layer on the
+ * device, no host synchronisation), layer l reading and appending to its own
+ * cache caches[l].  Layer 0 takes the caller's side features psi; layer
+ * l > 0 takes them with the last four replaced by layer l - 1's decisions
+ * of the same token (Sec. 3.3 counts the previous layer's decisions among
+ * the side features),
+ *   psi'[d_psi - 4] = heads in full mode / H,  psi'[d_psi - 3] = heads in
+ *   local mode / H,  psi'[d_psi - 2] = width index / 3,  psi'[d_psi - 1] =
+ *   real (non-null) expert slots / k
+ * (fp32, exact quotients of small integers).  Layer l's output is layer
+ * l + 1's input; the last layer's goes to x_out.  Requires d_psi >= 4.
+ *   layers, caches: host arrays of n_layers entries (1 <= n_layers <= 256);
+ *   x, x_out act [B, d]; psi f32 [B, d_psi];
+ *   ws: triroute_workspace_bytes(cfg, TRIROUTE_OP_STACK_DECODE, B, 1) bytes. */
+int triroute_stack_decode(const triroute_cfg *cfg, int n_layers, int B, const int32_t *seq_ids,
+                          const void *x, const float *psi, const triroute_layer_w *layers,
+                          const triroute_kv_cache *caches, void *x_out, void *ws, size_t ws_bytes,
                           triroute_stream_t stream);
 
 /* ---- no-allocation variant ---------------------------------------------- */

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libtriroute.so")
 F32, BF16 = 0, 1
 SKIP, LOCAL, FULL = 0, 1, 2
 OP_ROUTER, OP_QKV, OP_KV_APPEND, OP_ATTN_PREFILL, OP_ATTN_DECODE, OP_MOE, \
-    OP_LAYER_PREFILL, OP_LAYER_DECODE = range(8)
+    OP_LAYER_PREFILL, OP_LAYER_DECODE, OP_STACK_DECODE = range(9)
 CACHE_OVERFLOW, CACHE_BAD_SEQ = 1, 2
 
 STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too small",
@@ -53,6 +53,10 @@ class MoeW(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in ("Wgate", "Wup", "Wdown")]
 
 
+class LayerW(C.Structure):
+    _fields_ = [("router", RouterW), ("dense", DenseW), ("moe", MoeW)]
+
+
 class Compaction(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in
                 ("attn_cnt", "attn_idx", "exp_cnt", "exp_off", "exp_rows")]
@@ -79,6 +83,7 @@ EXPORTS = [
     "triroute_kv_append", "triroute_kv_export", "triroute_router", "triroute_qkv",
     "triroute_attn_prefill", "triroute_attn_decode", "triroute_oproj", "triroute_moe",
     "triroute_layer_prefill", "triroute_layer_decode", "triroute_layer_decode_noalloc",
+    "triroute_stack_decode",
 ]
 
 _lib = None
@@ -113,6 +118,7 @@ def lib():
             "triroute_layer_prefill": [P, i32, i32, P, P, P, P, P, P, P, P, P, P, sz, P],
             "triroute_layer_decode": [P, i32, P, P, P, P, P, P, P, P, P, P, sz, P],
             "triroute_layer_decode_noalloc": [P, i32, P, P, P, P, P, P, P, P, P, P],
+            "triroute_stack_decode": [P, i32, i32, P, P, P, P, P, P, P, sz, P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -287,6 +293,17 @@ def layer_decode_noalloc(cfg, B, x, psi, rw, dw, mw, cache: KVCache, x_out, taps
     _check(lib().triroute_layer_decode_noalloc(
         C.byref(cfg), B, _p(seq_ids), _p(x), _p(psi), C.byref(rw), C.byref(dw), C.byref(mw),
         cache.ref, _p(x_out), C.byref(taps) if taps is not None else None, _stream(stream)))
+
+
+def stack_decode(cfg, B, x, psi, layers, caches, x_out, ws, seq_ids=None, stream=None):
+    """One decode step through len(layers) routed layers; ``layers`` is a list
+    of (RouterW, DenseW, MoeW), ``caches`` one KVCache per layer."""
+    n = len(layers)
+    lw = (LayerW * n)(*[LayerW(r, d, m) for r, d, m in layers])
+    cs = (type(caches[0].desc) * n)(*[c.desc for c in caches])
+    _check(lib().triroute_stack_decode(
+        C.byref(cfg), n, B, _p(seq_ids), _p(x), _p(psi), lw, cs, _p(x_out), _p(ws), ws.numel(),
+        _stream(stream)))
 
 
 # ------------------------------------------------------ device-side buffers

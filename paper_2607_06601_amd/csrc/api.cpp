@@ -167,6 +167,28 @@ float *carve_qkv(Carve &cv, const triroute_cfg &c, int N) {
   return cv.take<float>(tr::qkv_rope_floats(c, N));
 }
 
+// A stack's own buffers, ahead of the layer workspace: the activations
+// handed between layers (two, used in turn), the next layer's side features
+// and the decisions of the layer just run.
+struct StackBufs {
+  void *xa, *xb;
+  float *psi;
+  uint8_t *mode, *bit;
+  int32_t *eidx;
+};
+
+StackBufs carve_stack(Carve &cv, const triroute_cfg &c, int B) {
+  const size_t ab = act_bytes(c);
+  StackBufs S;
+  S.xa = cv.take<uint8_t>(size_t(B) * c.d_model * ab);
+  S.xb = cv.take<uint8_t>(size_t(B) * c.d_model * ab);
+  S.psi = cv.take<float>(size_t(B) * c.d_psi);
+  S.mode = cv.take<uint8_t>(size_t(B) * c.n_heads);
+  S.bit = cv.take<uint8_t>(B);
+  S.eidx = cv.take<int32_t>(size_t(B) * c.top_k);
+  return S;
+}
+
 size_t op_bytes(const triroute_cfg &c, int op, int B, int T) {
   Carve cv(nullptr);
   const int N = B * T;
@@ -190,6 +212,9 @@ size_t op_bytes(const triroute_cfg &c, int op, int B, int T) {
       s = std::max(s, op_bytes(c, TRIROUTE_OP_MOE, B, T));
       return cv.used + s;
     }
+    case TRIROUTE_OP_STACK_DECODE:
+      carve_stack(cv, c, B);
+      return cv.used + op_bytes(c, TRIROUTE_OP_LAYER_DECODE, B, 1);
     default: return 0;
   }
   return cv.used;
@@ -370,7 +395,7 @@ int triroute_workspace_bytes(const triroute_cfg *cfg, int op, int B, int T, size
   TRY(check_cfg(cfg));
   TRY(check_bt(B, T));
   REQUIRE(bytes, TRIROUTE_E_INVALID, "bytes is NULL");
-  REQUIRE(op >= TRIROUTE_OP_ROUTER && op <= TRIROUTE_OP_LAYER_DECODE, TRIROUTE_E_INVALID,
+  REQUIRE(op >= TRIROUTE_OP_ROUTER && op <= TRIROUTE_OP_STACK_DECODE, TRIROUTE_E_INVALID,
           "unknown op %d", op);
   *bytes = op_bytes(*cfg, op, B, T);
   return TRIROUTE_OK;
@@ -686,6 +711,40 @@ int triroute_layer_decode(const triroute_cfg *cfg, int B, const int32_t *seq_ids
                           triroute_stream_t stream) {
   return layer_impl(cfg, B, 1, true, seq_ids, x, psi, rw, dw, mw, cache, x_out, taps, ws, ws_bytes,
                     stream);
+}
+
+int triroute_stack_decode(const triroute_cfg *cfg, int n_layers, int B, const int32_t *seq_ids,
+                          const void *x, const float *psi, const triroute_layer_w *layers,
+                          const triroute_kv_cache *caches, void *x_out, void *ws, size_t ws_bytes,
+                          triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  REQUIRE(n_layers >= 1 && n_layers <= 256, TRIROUTE_E_INVALID, "n_layers (%d) must be in [1, 256]",
+          n_layers);
+  REQUIRE(layers && caches && x && psi && x_out, TRIROUTE_E_INVALID, "NULL argument");
+  REQUIRE(cfg->d_psi >= 4, TRIROUTE_E_INVALID,
+          "a stack needs d_psi >= 4 (the previous layer's decisions)");
+  TRY(check_bt(B, 1));
+  TRY(check_aligned({x, x_out, psi}));
+  TRY(check_ws(*cfg, TRIROUTE_OP_STACK_DECODE, B, 1, ws, ws_bytes));
+  Carve cv(ws);
+  const StackBufs S = carve_stack(cv, *cfg, B);
+  void *lws = (uint8_t *)ws + cv.used;
+  const size_t lbytes = ws_bytes - cv.used;
+  hipStream_t st = (hipStream_t)stream;
+  triroute_layer_taps taps{};
+  taps.mode = S.mode;
+  taps.bit = S.bit;
+  taps.eidx = S.eidx;
+  const void *xin = x;
+  for (int l = 0; l < n_layers; ++l) {
+    void *xo = l == n_layers - 1 ? x_out : (l % 2 == 0 ? S.xa : S.xb);
+    TRY(layer_impl(cfg, B, 1, true, seq_ids, xin, l == 0 ? psi : S.psi, &layers[l].router,
+                   &layers[l].dense, &layers[l].moe, &caches[l], xo, &taps, lws, lbytes, stream));
+    if (l + 1 < n_layers)
+      CHECK_HIP(tr::launch_psi_next(*cfg, B, psi, S.mode, S.bit, S.eidx, S.psi, st), "psi launch");
+    xin = xo;
+  }
+  return TRIROUTE_OK;
 }
 
 }  // extern "C"

@@ -110,6 +110,8 @@ hipError_t launch_moe_norm_rows(const triroute_cfg &cfg, int N, const void *x, c
 inline int moe_ysplit(const triroute_cfg &c, int N) {
   return c.act == TRIROUTE_BF16 && N * c.top_k <= 2048 && c.d_ff % 128 == 0 ? 2 : 1;
 }
+hipError_t launch_psi_next(const triroute_cfg &cfg, int N, const float *psi, const uint8_t *mode,
+                           const uint8_t *bit, const int32_t *eidx, float *out, hipStream_t st);
 hipError_t launch_moe_combine(const triroute_cfg &cfg, int N, const void *xt, const float *Y,
                               const int32_t *slot_of, const int32_t *eidx, const float *egate,
                               void *xout, hipStream_t st);

@@ -154,4 +154,39 @@ hipError_t launch_moe_combine(const triroute_cfg &cfg, int N, const void *xt, co
   return hipGetLastError();
 }
 
+// Side features of the next layer of a stack (Sec. 3.3: the previous
+// layer's decisions among them): the caller's features with the last four
+// replaced by this token's decisions in the layer just run, as exact fp32
+// quotients: full heads / H, local heads / H, width index / 3, real expert
+// slots / k.  One thread per token.
+__global__ __launch_bounds__(256) void psi_next_kernel(const float *__restrict__ psi,
+                                                       const uint8_t *__restrict__ mode,
+                                                       const uint8_t *__restrict__ bit,
+                                                       const int32_t *__restrict__ eidx,
+                                                       float *__restrict__ out, int N, int dpsi,
+                                                       int H, int k) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= N) return;
+  for (int j = 0; j < dpsi - 4; ++j) out[int64_t(t) * dpsi + j] = psi[int64_t(t) * dpsi + j];
+  int full = 0, local = 0, real = 0;
+  for (int h = 0; h < H; ++h) {
+    const int m = mode[int64_t(t) * H + h];
+    full += m == TRIROUTE_FULL;
+    local += m == TRIROUTE_LOCAL;
+  }
+  for (int j = 0; j < k; ++j) real += eidx[int64_t(t) * k + j] != 0;
+  float *o = out + int64_t(t) * dpsi + dpsi - 4;
+  o[0] = float(full) / float(H);
+  o[1] = float(local) / float(H);
+  o[2] = float(bit[t]) / 3.0f;
+  o[3] = float(real) / float(k);
+}
+
+hipError_t launch_psi_next(const triroute_cfg &cfg, int N, const float *psi, const uint8_t *mode,
+                           const uint8_t *bit, const int32_t *eidx, float *out, hipStream_t st) {
+  psi_next_kernel<<<dim3((N + 255) / 256), 256, 0, st>>>(psi, mode, bit, eidx, out, N, cfg.d_psi,
+                                                         cfg.n_heads, cfg.top_k);
+  return hipGetLastError();
+}
+
 }  // namespace tr

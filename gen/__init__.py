@@ -237,6 +237,49 @@ def make_stack(name: str, n_layers: int, seed: int | None = None) -> list:
     return out
 
 
+def gumbel(seed, name, shape, *index):
+    """Gumbel(0, 1) draws (numpy's inverse-CDF sampler), rounded to fp32."""
+    return stream(seed, name, *index).gumbel(0.0, 1.0, shape).astype(np.float32)
+
+
+def token_positions(cfg: dict) -> np.ndarray:
+    """0-based position of every token of a workload: t within its sequence
+    (prefill), the context length (decode)."""
+    if cfg["kind"] == "prefill":
+        return np.tile(np.arange(cfg["T"], dtype=np.int32), cfg["B"]) + np.int32(
+            cfg.get("ctx", 0))
+    return np.full(cfg["B"], cfg["ctx"], np.int32)
+
+
+def relax_inputs(L: dict, *, tau_a: float = 1.3, tau_b: float = 0.8,
+                 white: bool = True) -> dict:
+    """Inputs of the training-time relaxed controller forward of layer ``L``:
+    i.i.d. Gumbel(0, 1) noise per attention decision group (3 options) and
+    per token for the bit head (4 options); per-axis running whitening
+    statistics (mean ~ N(0, 0.1^2), standard deviation ~ U(0.7, 1.3); axis
+    order attention, experts, bits); mid-anneal temperatures (the paper
+    anneals from 2.0 to 0.5); loss weights, cost targets and dual state."""
+    cfg = L["cfg"]
+    seed, N = cfg["seed"], len(L["x"])
+    A = cfg.get("attn_groups") or cfg["H"]
+    R = dict(g_attn=gumbel(seed, "g_attn", (N, A, 3)), g_bits=gumbel(seed, "g_bits", (N, 4)),
+             white_mu=None, white_sd=None, white_eps=1e-5, tau_a=tau_a, tau_b=tau_b,
+             pos=token_positions(cfg), zeta=0.5, alpha=1e-2, beta=1e-3, gamma=0.1,
+             c_target=(0.5, 0.4), dual=(0.3, 0.7, 0.55, 0.45), dual_lr=0.05, dual_ema=0.1)
+    if white:
+        R["white_mu"] = normal(seed, "white_mu", (3, D_ROUTER), 0.1)
+        R["white_sd"] = (np.float32(0.7) + np.float32(0.6) * stream(seed, "white_sd").random(
+            (3, D_ROUTER), dtype=np.float32)).astype(np.float32)
+    return R
+
+
+def resample_gumbel_row(seed: int, name: str, token: int, attempt: int, shape) -> np.ndarray:
+    """Fresh Gumbel noise for one token's decisions (used to move a relaxed
+    decision off a tie)."""
+    return stream(seed, name + "_resample", token, attempt).gumbel(0.0, 1.0, shape).astype(
+        np.float32)
+
+
 def moe_weights(cfg: dict):
     """SwiGLU expert weights: gate/up [E, d_ff, d], down [E, d, d_ff]."""
     E, d, dff, seed, act = cfg["E"], cfg["d"], cfg["d_ff"], cfg["seed"], cfg["act"]

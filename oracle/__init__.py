@@ -14,6 +14,7 @@ trained layer) are "parity unpinned": the paper prints no worked example.
 from . import quant  # noqa: F401
 from . import cost  # noqa: F401
 from . import stack  # noqa: F401
+from . import relax  # noqa: F401
 from .layer import (  # noqa: F401
     MODE_SKIP, MODE_LOCAL, MODE_FULL, BITS,
     rmsnorm, gelu, silu, softmax, rope,

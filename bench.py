@@ -60,7 +60,7 @@ def parse():
     p.add_argument("--only", default=None,
                    choices=("prefill_1p3b", "prefill_160m", "moe_1p3b", "moe_160m",
                             "decode_410m", "decode_1p3b", "attn_410m", "attn_1p3b",
-                            "stack_410m"),
+                            "stack_410m", "relaxed_1p3b"),
                    help="profile one leg alone (prints its section only); moe_* time the "
                         "MoE sublayer, attn_* the decode attention, and both then run a "
                         "256 MiB copy for counter calibration")
@@ -153,6 +153,8 @@ def main():
             r = bench_prefill(cx, SMALL, 1, args.steps, args.warmup, moe_only=leg == "moe_160m")
         elif leg == "stack_410m":
             r = bench_stack(cx, args.steps, args.warmup, None)
+        elif leg == "relaxed_1p3b":
+            r = bench_relaxed(cx, args.steps, args.warmup)
         else:
             name = DECODES["decode_410m" if leg.endswith("410m") else "decode_1p3b"]
             r = bench_decode(cx, name, args.steps, args.warmup, attn_only=leg.startswith("attn"))
@@ -189,6 +191,7 @@ def main():
         out["stack_410m_decode"] = bench_stack(cx, ks, ws, out["decode_410m"]["ms_per_step"])
         out["dense_1p3b_prefill"] = bench_dense_prefill(cx, ks, ws, head)
         out["granularity_1p3b_prefill"] = bench_granularity(cx, ks, ws, head)
+        out["relaxed_1p3b_router"] = bench_relaxed(cx, ks, ws)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cx.layer(HEADLINE))
     print(json.dumps(out), flush=True)
@@ -567,6 +570,63 @@ def bench_granularity(cx, steps, warmup, head):
                       "ms_per_step": round(r["ms"], 4),
                       "over_per_head_tokens_per_s": round(head["ms"] / r["ms"], 3)}
     return out
+
+
+def bench_relaxed(cx, steps, warmup):
+    """The training-time relaxed controller forward (whitening, ST-Gumbel,
+    expected costs, losses, dual step, compaction) on the headline prefill's
+    tokens, beside the inference controller (triroute_router) on the same
+    tokens."""
+    torch, tr, np = cx.torch, cx.tr, cx.np
+    L = cx.layer(HEADLINE)
+    cfg = L["cfg"]
+    B, T, H, E, k = cfg["B"], cfg["T"], cfg["H"], cfg["E"], cfg["k"]
+    N = B * T
+    R = cx.gen.relax_inputs(L)
+    D = cx.DeviceLayer(L, moe=False)
+    c = D.cfg
+    dev, f32 = cx.dev, torch.float32
+    t = {n: cx.to_dev(R[n], f32) for n in ("g_attn", "g_bits", "white_mu", "white_sd")}
+    t["pos"] = cx.to_dev(R["pos"], torch.int32)
+    t["dual"] = cx.to_dev(np.asarray(R["dual"]), torch.float64)
+    p = tr.RelaxParams(g_attn=t["g_attn"].data_ptr(), g_bits=t["g_bits"].data_ptr(),
+                       pos=t["pos"].data_ptr(), white_mu=t["white_mu"].data_ptr(),
+                       white_sd=t["white_sd"].data_ptr(), white_eps=R["white_eps"],
+                       tau_a=R["tau_a"], tau_b=R["tau_b"], zeta=R["zeta"], alpha=R["alpha"],
+                       beta=R["beta"], gamma=R["gamma"], dual=t["dual"].data_ptr(),
+                       dual_lr=R["dual_lr"], dual_ema=R["dual_ema"])
+    p.c_target[0], p.c_target[1] = R["c_target"]
+    o = [torch.empty(N, H, 3, dtype=f32, device=dev), torch.empty(N, 4, dtype=f32, device=dev),
+         torch.empty(N, dtype=f32, device=dev), torch.empty(N, dtype=f32, device=dev),
+         torch.empty(tr.RELAX_NSTAT, dtype=torch.float64, device=dev)]
+    out = tr.RelaxOut(*(x.data_ptr() for x in o), None, None, None, None, None)
+    n1 = torch.empty(N, cfg["d"], dtype=D.act, device=dev)
+    mode = torch.empty(N, H, dtype=torch.uint8, device=dev)
+    bit = torch.empty(N, dtype=torch.uint8, device=dev)
+    eidx = torch.empty(N, k, dtype=torch.int32, device=dev)
+    egate = torch.empty(N, k, dtype=f32, device=dev)
+    cmp = tr.CompactionBuffers(c, B, T)
+    ws_r = tr.workspace(c, tr.OP_ROUTER_RELAXED, B, T)
+    ws_i = tr.workspace(c, tr.OP_ROUTER, B, T)
+
+    def relaxed(_):
+        tr.router_relaxed(c, B, T, D.x, D.psi, D.rw, p, n1, mode, bit, eidx, egate, cmp.struct,
+                          out, ws_r)
+
+    def inference(_):
+        tr.router(c, B, T, D.x, D.psi, D.rw, n1, mode, bit, eidx, egate, cmp.struct, ws_i)
+
+    for i in range(warmup):
+        relaxed(i)
+        inference(i)
+    ms_r, _ = cx.timed(relaxed, steps)
+    ms_i, _ = cx.timed(inference, steps)
+    return {"workload": f"relaxed controller forward on the 1.3B-class prefill tokens ({B} x {T}): "
+                        "per-axis whitening, ST-Gumbel (attention per head, bits), top-k experts, "
+                        "expected costs, balance / z / entropy losses, dual step, compaction",
+            "tokens_per_s": round(N / (ms_r * 1e-3), 1), "ms_per_call": round(ms_r, 4),
+            "inference_router_ms": round(ms_i, 4),
+            "relaxed_over_inference_ms": round(ms_r / ms_i, 3)}
 
 
 def summarize_pmc(fetch_dir, write_dir, regex):

@@ -202,7 +202,8 @@ enum triroute_op {
   TRIROUTE_OP_MOE = 5,
   TRIROUTE_OP_LAYER_PREFILL = 6,
   TRIROUTE_OP_LAYER_DECODE = 7,
-  TRIROUTE_OP_STACK_DECODE = 8
+  TRIROUTE_OP_STACK_DECODE = 8,
+  TRIROUTE_OP_ROUTER_RELAXED = 9
 };
 
 /* ---- configuration, errors, sizes ---------------------------------------- */
@@ -365,6 +366,90 @@ int triroute_stack_decode(const triroute_cfg *cfg, int n_layers, int B, const in
                           const void *x, const float *psi, const triroute_layer_w *layers,
                           const triroute_kv_cache *caches, void *x_out, void *ws, size_t ws_bytes,
                           triroute_stream_t stream);
+
+/* ---- training-time relaxed controller forward ----------------------------- */
+
+/* Inputs of the relaxed forward (Sec. 3.4-3.7, Algorithm 1).  Pointers are
+ * device memory; N = B * T tokens, A = attention decision groups. */
+typedef struct triroute_relax_params {
+  const float *g_attn;   /* [N, A, 3] Gumbel(0, 1) noise of the attention choices */
+  const float *g_bits;   /* [N, 4] Gumbel(0, 1) noise of the bit choice */
+  const int32_t *pos;    /* [N] 0-based position of each token in its sequence */
+  const float *white_mu; /* [3, d_r] per-axis running means (attention, experts, bits), or NULL */
+  const float *white_sd; /* [3, d_r] per-axis running standard deviations; NULL with white_mu */
+  float white_eps;       /* Sec. 3.6 whitening epsilon; sd + eps must be nonzero */
+  float tau_a, tau_b;    /* ST-Gumbel temperatures of the attention and bit heads, > 0 */
+  float zeta;            /* entropy floor: a fraction of log |O| */
+  float alpha, beta, gamma; /* weights of L_bal, L_z and L_ent (Sec. 3.7 total loss) */
+  float c_target[2];     /* C*_flops, C*_mem */
+  double *dual;          /* [4] lambda_flops, lambda_mem, EMA of C-bar_flops, C-bar_mem, or
+                          * NULL (lambda = 0); updated in place when dual_ema > 0 */
+  float dual_lr, dual_ema; /* rho_lambda and the EMA momentum m */
+} triroute_relax_params;
+
+/* Layout of triroute_relax_out.stats (fp64); the three axes in the order
+ * attention, experts, bits. */
+enum triroute_relax_stat {
+  TRIROUTE_RS_LBAL = 0,     /* [3] Switch balance loss |O| sum_o f_o P_o */
+  TRIROUTE_RS_LZ = 3,       /* [3] router z-loss, mean of (log sum_o exp z_o)^2 */
+  TRIROUTE_RS_LENT = 6,     /* [3] entropy floor [zeta log |O| - H(P)]_+ */
+  TRIROUTE_RS_ENTROPY = 9,  /* [3] H(P) of the mean soft probabilities */
+  TRIROUTE_RS_CBAR = 12,    /* [2] C-bar_flops, C-bar_mem: cost / dense cost */
+  TRIROUTE_RS_COST = 14,    /* [2] summed expected costs (MACs, bits) */
+  TRIROUTE_RS_DENSE = 16,   /* [2] summed dense costs of the same tokens */
+  TRIROUTE_RS_REG = 18,     /* the regulariser: sum of alpha L_bal + beta L_z + gamma L_ent
+                             * over the axes + sum_r lambda_r (C-bar_r - C*_r) */
+  TRIROUTE_RS_F_ATTN = 19,  /* [3] hard-choice fractions of the attention axis */
+  TRIROUTE_RS_P_ATTN = 22,  /* [3] mean soft probabilities of the attention axis */
+  TRIROUTE_RS_F_BITS = 25,  /* [4] */
+  TRIROUTE_RS_P_BITS = 29,  /* [4] */
+  TRIROUTE_RELAX_NSTAT = 33
+};
+
+/* Outputs of the relaxed forward beyond the hard decisions (device). */
+typedef struct triroute_relax_out {
+  float *y_attn;     /* [N, A, 3] soft samples of the attention choice */
+  float *y_bits;     /* [N, 4] soft samples of the bit choice */
+  float *c_flops;    /* [N] expected attention-read plus expert MACs of each token */
+  float *c_mem;      /* [N] expected KV bits of each token */
+  double *stats;     /* [TRIROUTE_RELAX_NSTAT] */
+  float *p_exp;      /* [N, E+1] softmax(z^e), or NULL */
+  double *usage_exp; /* [2, E+1] f_o then P_o of the expert axis, or NULL */
+  float *h_mean;     /* [d_r] batch mean of h^ (before whitening), or NULL */
+  float *h_var;      /* [d_r] batch (population) variance of h^, or NULL */
+  float *z;          /* [N, 3A + E + 5] head logits after whitening, or NULL */
+} triroute_relax_out;
+
+/* One layer's relaxed controller forward at training time (Algorithm 1
+ * steps 1-3, 5, 6; the backward pass is not part of the library):
+ *   h^ as in triroute_router; each head reads its own whitening
+ *   (h^ - mu) / (sd + eps) (Sec. 3.6; folded into that head's weights on
+ *   the device, W' = W / (sd + eps), c' = c - W' mu);
+ *   attention and bits (Sec. 3.4): soft sample y~ = softmax((z + g) / tau),
+ *   hard choice argmax (z + g) (first maximum), broadcast to the heads of a
+ *   decision group in `mode`; experts: the inference top-k and gates;
+ *   costs (Sec. 3.5): c_flops = sum_h sum_m y~^a_m 2 d_h keys_m(t) +
+ *   3 d d_f sum over the real experts of S_t of their gates (the null costs
+ *   nothing), keys_local = min(P + 1, w), keys_full = P + 1; c_mem =
+ *   sum_b y~^b_b 2 d_kv b; dense reference H 2 d_h (P + 1) + 3 d d_f and
+ *   2 d_kv 16 per token, C-bar = summed cost / summed dense cost;
+ *   losses (Sec. 3.6) per axis: f_o hard-choice fractions (attention over
+ *   (token, group) rows, experts over the N k assignments), P_o mean of
+ *   softmax(z), L_bal = |O| sum f P, L_z = mean (logsumexp z)^2,
+ *   L_ent = [zeta log |O| - H(P)]_+; the regulariser of Sec. 3.7 with the
+ *   multipliers in `dual` as given; then, when dual_ema > 0, the dual step
+ *   ema <- (1 - m) ema + m C-bar, lambda <- max(0, lambda + rho (ema - C*)).
+ * Then the compaction of the hard decisions, as triroute_router.  Batch
+ * statistics are reduced in a fixed order (deterministic).
+ *   x act [B*T, d], psi f32 [B*T, d_psi]; n1, mode, bit, eidx, egate, cmp as
+ *   in triroute_router; ws: triroute_workspace_bytes(cfg,
+ *   TRIROUTE_OP_ROUTER_RELAXED, B, T) bytes. */
+int triroute_router_relaxed(const triroute_cfg *cfg, int B, int T, const void *x,
+                            const float *psi, const triroute_router_w *w,
+                            const triroute_relax_params *p, void *n1, uint8_t *mode,
+                            uint8_t *bit, int32_t *eidx, float *egate,
+                            const triroute_compaction *cmp, const triroute_relax_out *out,
+                            void *ws, size_t ws_bytes, triroute_stream_t stream);
 
 /* ---- no-allocation variant ---------------------------------------------- */
 

@@ -19,7 +19,10 @@ LIB_PATH = os.path.join(_HERE, "libtriroute.so")
 F32, BF16 = 0, 1
 SKIP, LOCAL, FULL = 0, 1, 2
 OP_ROUTER, OP_QKV, OP_KV_APPEND, OP_ATTN_PREFILL, OP_ATTN_DECODE, OP_MOE, \
-    OP_LAYER_PREFILL, OP_LAYER_DECODE, OP_STACK_DECODE = range(9)
+    OP_LAYER_PREFILL, OP_LAYER_DECODE, OP_STACK_DECODE, OP_ROUTER_RELAXED = range(10)
+# fp64 fields of RelaxOut.stats (axes in the order attention, experts, bits)
+RS_LBAL, RS_LZ, RS_LENT, RS_ENTROPY, RS_CBAR, RS_COST, RS_DENSE, RS_REG = 0, 3, 6, 9, 12, 14, 16, 18
+RS_F_ATTN, RS_P_ATTN, RS_F_BITS, RS_P_BITS, RELAX_NSTAT = 19, 22, 25, 29, 33
 CACHE_OVERFLOW, CACHE_BAD_SEQ = 1, 2
 
 STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too small",
@@ -76,6 +79,21 @@ class Taps(C.Structure):
                 ("n1", "mode", "bit", "eidx", "egate", "q", "k", "v", "o", "xt")]
 
 
+class RelaxParams(C.Structure):
+    _fields_ = [("g_attn", C.c_void_p), ("g_bits", C.c_void_p), ("pos", C.c_void_p),
+                ("white_mu", C.c_void_p), ("white_sd", C.c_void_p), ("white_eps", C.c_float),
+                ("tau_a", C.c_float), ("tau_b", C.c_float), ("zeta", C.c_float),
+                ("alpha", C.c_float), ("beta", C.c_float), ("gamma", C.c_float),
+                ("c_target", C.c_float * 2), ("dual", C.c_void_p), ("dual_lr", C.c_float),
+                ("dual_ema", C.c_float)]
+
+
+class RelaxOut(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in
+                ("y_attn", "y_bits", "c_flops", "c_mem", "stats", "p_exp", "usage_exp",
+                 "h_mean", "h_var", "z")]
+
+
 EXPORTS = [
     "triroute_validate", "triroute_status_string", "triroute_last_error",
     "triroute_workspace_bytes", "triroute_kv_cache_bytes", "triroute_kv_cache_init",
@@ -83,7 +101,7 @@ EXPORTS = [
     "triroute_kv_append", "triroute_kv_export", "triroute_router", "triroute_qkv",
     "triroute_attn_prefill", "triroute_attn_decode", "triroute_oproj", "triroute_moe",
     "triroute_layer_prefill", "triroute_layer_decode", "triroute_layer_decode_noalloc",
-    "triroute_stack_decode",
+    "triroute_stack_decode", "triroute_router_relaxed",
 ]
 
 _lib = None
@@ -119,6 +137,7 @@ def lib():
             "triroute_layer_decode": [P, i32, P, P, P, P, P, P, P, P, P, P, sz, P],
             "triroute_layer_decode_noalloc": [P, i32, P, P, P, P, P, P, P, P, P, P],
             "triroute_stack_decode": [P, i32, i32, P, P, P, P, P, P, P, sz, P],
+            "triroute_router_relaxed": [P, i32, i32, P, P, P, P, P, P, P, P, P, P, P, P, sz, P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -239,6 +258,15 @@ def router(cfg, B, T, x, psi, rw: RouterW, n1, mode, bit, eidx, egate, cmp: Comp
     _check(lib().triroute_router(C.byref(cfg), B, T, _p(x), _p(psi), C.byref(rw), _p(n1),
                                  _p(mode), _p(bit), _p(eidx), _p(egate), C.byref(cmp), _p(ws),
                                  ws.numel(), _stream(stream)))
+
+
+def router_relaxed(cfg, B, T, x, psi, rw: RouterW, params: RelaxParams, n1, mode, bit, eidx,
+                   egate, cmp: Compaction, out: RelaxOut, ws, stream=None):
+    """Training-time relaxed controller forward (triroute_router_relaxed)."""
+    _check(lib().triroute_router_relaxed(C.byref(cfg), B, T, _p(x), _p(psi), C.byref(rw),
+                                         C.byref(params), _p(n1), _p(mode), _p(bit), _p(eidx),
+                                         _p(egate), C.byref(cmp), C.byref(out), _p(ws),
+                                         ws.numel(), _stream(stream)))
 
 
 def qkv(cfg, B, T, n1, dw: DenseW, q, k, v, ws, pos0=None, stream=None):

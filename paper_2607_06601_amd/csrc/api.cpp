@@ -189,6 +189,23 @@ StackBufs carve_stack(Carve &cv, const triroute_cfg &c, int B) {
   return S;
 }
 
+// The relaxed controller forward's scratch beyond the router's: the folded
+// head weights, the tail's logits and h^, and the rows of partial sums.
+struct RelaxWs {
+  float *Wf, *cf, *z, *h;
+  double *part;
+};
+RelaxWs carve_relax(Carve &cv, const triroute_cfg &c, int N) {
+  const int NZ = 3 * tr::attn_groups(c) + c.n_experts + 5;
+  RelaxWs w;
+  w.Wf = cv.take<float>(size_t(NZ) * 128);
+  w.cf = cv.take<float>(NZ);
+  w.z = cv.take<float>(size_t(N) * NZ);
+  w.h = cv.take<float>(size_t(N) * 128);
+  w.part = cv.take<double>(tr::relax_part_doubles());
+  return w;
+}
+
 size_t op_bytes(const triroute_cfg &c, int op, int B, int T) {
   Carve cv(nullptr);
   const int N = B * T;
@@ -215,6 +232,10 @@ size_t op_bytes(const triroute_cfg &c, int op, int B, int T) {
     case TRIROUTE_OP_STACK_DECODE:
       carve_stack(cv, c, B);
       return cv.used + op_bytes(c, TRIROUTE_OP_LAYER_DECODE, B, 1);
+    case TRIROUTE_OP_ROUTER_RELAXED:
+      carve_router(cv, c, N);
+      carve_relax(cv, c, N);
+      break;
     default: return 0;
   }
   return cv.used;
@@ -395,7 +416,7 @@ int triroute_workspace_bytes(const triroute_cfg *cfg, int op, int B, int T, size
   TRY(check_cfg(cfg));
   TRY(check_bt(B, T));
   REQUIRE(bytes, TRIROUTE_E_INVALID, "bytes is NULL");
-  REQUIRE(op >= TRIROUTE_OP_ROUTER && op <= TRIROUTE_OP_STACK_DECODE, TRIROUTE_E_INVALID,
+  REQUIRE(op >= TRIROUTE_OP_ROUTER && op <= TRIROUTE_OP_ROUTER_RELAXED, TRIROUTE_E_INVALID,
           "unknown op %d", op);
   *bytes = op_bytes(*cfg, op, B, T);
   return TRIROUTE_OK;
@@ -510,6 +531,76 @@ int triroute_router(const triroute_cfg *cfg, int B, int T, const void *x, const 
   CHECK_HIP(tr::launch_router(*cfg, B * T, x, psi, *w, n1, mode, bit, eidx, egate, rw.rinv, rw.u,
                               nullptr, st),
             "router launch");
+  CHECK_HIP(tr::launch_compact(*cfg, B, T, mode, eidx, *cmp, rw.hist, st), "compaction launch");
+  return TRIROUTE_OK;
+}
+
+int triroute_router_relaxed(const triroute_cfg *cfg, int B, int T, const void *x,
+                            const float *psi, const triroute_router_w *w,
+                            const triroute_relax_params *p, void *n1, uint8_t *mode,
+                            uint8_t *bit, int32_t *eidx, float *egate,
+                            const triroute_compaction *cmp, const triroute_relax_out *out,
+                            void *ws, size_t ws_bytes, triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  TRY(check_bt(B, T));
+  REQUIRE(x && (psi || cfg->d_psi == 0) && w && p && n1 && mode && bit && eidx && egate && cmp &&
+              out,
+          TRIROUTE_E_INVALID, "NULL argument");
+  REQUIRE(w->g1 && w->W1 && w->b1 && w->W2 && w->b2 && w->gr && w->Wa && w->ca && w->We &&
+              w->ce && w->Wb && w->cb,
+          TRIROUTE_E_INVALID, "NULL router weight");
+  REQUIRE(cmp->attn_cnt && cmp->attn_idx && cmp->exp_cnt && cmp->exp_off && cmp->exp_rows,
+          TRIROUTE_E_INVALID, "NULL compaction array");
+  REQUIRE(p->g_attn && p->g_bits && p->pos, TRIROUTE_E_INVALID, "NULL noise or position array");
+  REQUIRE(!p->white_mu == !p->white_sd, TRIROUTE_E_INVALID,
+          "white_mu and white_sd must both be given or both be NULL");
+  REQUIRE(isfinite(p->tau_a) && isfinite(p->tau_b) && p->tau_a > 0.f && p->tau_b > 0.f,
+          TRIROUTE_E_INVALID, "temperatures must be finite and positive (%g, %g)", p->tau_a,
+          p->tau_b);
+  REQUIRE(isfinite(p->white_eps) && isfinite(p->zeta) && isfinite(p->alpha) &&
+              isfinite(p->beta) && isfinite(p->gamma) && isfinite(p->c_target[0]) &&
+              isfinite(p->c_target[1]) && isfinite(p->dual_lr) && isfinite(p->dual_ema),
+          TRIROUTE_E_INVALID, "a relaxation parameter is not finite");
+  REQUIRE(p->dual_ema >= 0.f && p->dual_ema <= 1.f, TRIROUTE_E_INVALID,
+          "dual_ema (%g) outside [0, 1]", p->dual_ema);
+  REQUIRE(out->y_attn && out->y_bits && out->c_flops && out->c_mem && out->stats,
+          TRIROUTE_E_INVALID, "NULL relaxed output");
+  TRY(check_aligned({x, n1, w->g1, w->W1, w->W2, w->Wa, w->We, w->Wb}));
+  TRY(check_ws(*cfg, TRIROUTE_OP_ROUTER_RELAXED, B, T, ws, ws_bytes));
+  TRY(prepare_once());
+  const int N = B * T, A = tr::attn_groups(*cfg), E1 = cfg->n_experts + 1;
+  Carve cv(ws);
+  RouterWs rw = carve_router(cv, *cfg, N);
+  RelaxWs xw = carve_relax(cv, *cfg, N);
+  hipStream_t st = (hipStream_t)stream;
+  triroute_router_w wf = *w;
+  if (p->white_mu) {
+    CHECK_HIP(tr::launch_white_fold(*cfg, *w, p->white_mu, p->white_sd, p->white_eps, xw.Wf,
+                                    xw.cf, st),
+              "whitening fold launch");
+    wf.Wa = xw.Wf;
+    wf.We = xw.Wf + size_t(3 * A) * 128;
+    wf.Wb = xw.Wf + size_t(3 * A + E1) * 128;
+    wf.ca = xw.cf;
+    wf.ce = xw.cf + 3 * A;
+    wf.cb = xw.cf + 3 * A + E1;
+  }
+  tr::TailTap tap;
+  tap.h = xw.h;
+  tap.z = out->z ? out->z : xw.z;
+  CHECK_HIP(tr::launch_router(*cfg, N, x, psi, wf, n1, mode, bit, eidx, egate, rw.rinv, rw.u,
+                              nullptr, st, tap),
+            "router launch");
+  tr::RelaxJob j;
+  j.z = tap.z; j.h = tap.h; j.g_attn = p->g_attn; j.g_bits = p->g_bits; j.pos = p->pos;
+  j.eidx = eidx; j.egate = egate; j.mode = mode; j.bit = bit;
+  j.y_attn = out->y_attn; j.y_bits = out->y_bits; j.p_exp = out->p_exp;
+  j.c_flops = out->c_flops; j.c_mem = out->c_mem; j.part = xw.part; j.dual = p->dual;
+  j.stats = out->stats; j.usage_exp = out->usage_exp; j.h_mean = out->h_mean; j.h_var = out->h_var;
+  j.tau_a = p->tau_a; j.tau_b = p->tau_b; j.zeta = p->zeta; j.alpha = p->alpha;
+  j.beta = p->beta; j.gamma = p->gamma; j.target_f = p->c_target[0]; j.target_m = p->c_target[1];
+  j.dual_lr = p->dual_lr; j.dual_ema = p->dual_ema;
+  CHECK_HIP(tr::launch_relax(*cfg, N, j, st), "relaxed forward launch");
   CHECK_HIP(tr::launch_compact(*cfg, B, T, mode, eidx, *cmp, rw.hist, st), "compaction launch");
   return TRIROUTE_OK;
 }

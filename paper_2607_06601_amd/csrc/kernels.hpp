@@ -42,11 +42,16 @@ __device__ __forceinline__ float2 rope_entry(const RopeJob &r, int row, int j) {
   sincosf(float(rr), &sn, &cs);
   return make_float2(cs, sn);
 }
+// Optional copies of the controller tail's intermediates: h^ [N, 128] and
+// the head logits z [N, 3 A + E + 5] (either may be NULL).
+struct TailTap {
+  float *h = nullptr, *z = nullptr;
+};
 // rope (optional): the first RMSNorm also writes that rotation table
 hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const float *psi,
                          const triroute_router_w &w, void *n1, uint8_t *mode, uint8_t *bit,
                          int32_t *eidx, float *egate, float *rinv, float *u, const RopeJob *rope,
-                         hipStream_t st);
+                         hipStream_t st, TailTap tap = TailTap{});
 // compact.hip
 int compact_hist_ints(int N, int k, int E1);
 hipError_t launch_compact(const triroute_cfg &cfg, int B, int T, const uint8_t *mode,
@@ -115,5 +120,25 @@ hipError_t launch_psi_next(const triroute_cfg &cfg, int N, const float *psi, con
 hipError_t launch_moe_combine(const triroute_cfg &cfg, int N, const void *xt, const float *Y,
                               const int32_t *slot_of, const int32_t *eidx, const float *egate,
                               void *xout, hipStream_t st);
+
+// relax.hip: the relaxed controller forward around the router kernels
+struct RelaxJob {
+  const float *z, *h;  // the tail's logits and h^
+  const float *g_attn, *g_bits;
+  const int32_t *pos, *eidx;
+  const float *egate;
+  uint8_t *mode, *bit;
+  float *y_attn, *y_bits, *p_exp, *c_flops, *c_mem;
+  double *part;  // relax_part_doubles() of scratch
+  double *dual, *stats, *usage_exp;
+  float *h_mean, *h_var;
+  float tau_a, tau_b;
+  double zeta, alpha, beta, gamma, target_f, target_m, dual_lr, dual_ema;
+};
+size_t relax_part_doubles();
+// whitening folded into the head weights: Wf [3A + E + 5][128], cf [3A + E + 5]
+hipError_t launch_white_fold(const triroute_cfg &cfg, const triroute_router_w &w, const float *mu,
+                             const float *sd, float eps, float *Wf, float *cf, hipStream_t st);
+hipError_t launch_relax(const triroute_cfg &cfg, int N, const RelaxJob &j, hipStream_t st);
 
 }  // namespace tr

@@ -181,7 +181,7 @@ __global__ __launch_bounds__(512) void router_tail_kernel(
     const float *__restrict__ Wa, const float *__restrict__ ca, const float *__restrict__ We,
     const float *__restrict__ ce, const float *__restrict__ Wb, const float *__restrict__ cb,
     uint8_t *__restrict__ mode, uint8_t *__restrict__ bit, int32_t *__restrict__ eidx,
-    float *__restrict__ egate, int N, int H, int A, int E1, int k, float eps) {
+    float *__restrict__ egate, int N, int H, int A, int E1, int k, float eps, TailTap tap) {
   constexpr int TB = RT_TB, DR = RT_DR, LD = RT_LD;
   extern __shared__ __align__(16) float rt_lds[];
   float(*W2s)[LD] = (float(*)[LD])rt_lds;              // [128][LD]
@@ -298,6 +298,11 @@ __global__ __launch_bounds__(512) void router_tail_kernel(
       const float r = 1.0f / sqrtf(ss[j] / float(DR) + eps);
       Us[wave + 4 * j][lane] = (av[j] * r) * gr[lane];
       Us[wave + 4 * j][lane + 64] = (bv[j] * r) * gr[lane + 64];
+      const int tj = t0 + wave + 4 * j;
+      if (tap.h && tj < N) {
+        tap.h[int64_t(tj) * DR + lane] = Us[wave + 4 * j][lane];
+        tap.h[int64_t(tj) * DR + lane + 64] = Us[wave + 4 * j][lane + 64];
+      }
     }
   }
   __syncthreads();
@@ -316,6 +321,11 @@ __global__ __launch_bounds__(512) void router_tail_kernel(
     }
   }
   __syncthreads();
+  if (tap.z)
+    for (int it = tid; it < TB * NZ; it += 256) {
+      const int tt = it / NZ, z = it - tt * NZ;
+      if (t0 + tt < N) tap.z[int64_t(t0 + tt) * NZ + z] = Zs[tt][z];
+    }
   // modes: one thread per (token, head); argmax, first maximum on ties
   const int HA = H / A;  // heads per decision group
   for (int it = tid; it < TB * H; it += 256) {
@@ -377,7 +387,7 @@ __global__ __launch_bounds__(256) void router_tail_tok_kernel(
     const float *__restrict__ Wa, const float *__restrict__ ca, const float *__restrict__ We,
     const float *__restrict__ ce, const float *__restrict__ Wb, const float *__restrict__ cb,
     uint8_t *__restrict__ mode, uint8_t *__restrict__ bit, int32_t *__restrict__ eidx,
-    float *__restrict__ egate, int N, int H, int A, int E1, int k, float eps) {
+    float *__restrict__ egate, int N, int H, int A, int E1, int k, float eps, TailTap tap) {
   constexpr int DR = RT_DR;
   __shared__ __align__(16) float vs[4][2][DR];  // per wave: u, then h^; z
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -423,6 +433,10 @@ __global__ __launch_bounds__(256) void router_tail_tok_kernel(
   __builtin_amdgcn_wave_barrier();  // every lane is done reading u
   us[lane] = (h0 * r) * gr[lane];
   us[lane + 64] = (h1 * r) * gr[lane + 64];
+  if (tap.h) {
+    tap.h[int64_t(t) * DR + lane] = us[lane];
+    tap.h[int64_t(t) * DR + lane + 64] = us[lane + 64];
+  }
   __builtin_amdgcn_wave_barrier();
   // z = [Wa; We; Wb] h^ + [ca; ce; cb]: lane j owns logits j and j + 64
   for (int z = lane; z < NZ; z += 64) {
@@ -437,6 +451,7 @@ __global__ __launch_bounds__(256) void router_tail_tok_kernel(
     }
     const float bias = z < 3 * A ? ca[z] : z < 3 * A + E1 ? ce[z - 3 * A] : cb[z - 3 * A - E1];
     zs[z] = acc + bias;
+    if (tap.z) tap.z[int64_t(t) * NZ + z] = zs[z];
   }
   __builtin_amdgcn_wave_barrier();
   // modes: lane h takes head h; argmax, first maximum on ties
@@ -478,7 +493,7 @@ __global__ __launch_bounds__(256) void router_tail_tok_kernel(
 hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const float *psi,
                          const triroute_router_w &w, void *n1, uint8_t *mode, uint8_t *bit,
                          int32_t *eidx, float *egate, float *rinv, float *u, const RopeJob *rope,
-                         hipStream_t st) {
+                         hipStream_t st, TailTap tap) {
   RopeJob rj{};
   if (rope) rj = *rope;
   const int d = cfg.d_model;
@@ -500,7 +515,7 @@ hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const fl
   if (N <= 256 && ks <= RT1_MAXKS) {  // few tokens: one wave per token
     router_tail_tok_kernel<<<dim3((N + 3) / 4), 256, 0, st>>>(
         u, ks, w.b1, w.W2, w.b2, w.gr, w.Wa, w.ca, w.We, w.ce, w.Wb, w.cb, mode, bit, eidx, egate,
-        N, cfg.n_heads, attn_groups(cfg), cfg.n_experts + 1, cfg.top_k, cfg.rms_eps);
+        N, cfg.n_heads, attn_groups(cfg), cfg.n_experts + 1, cfg.top_k, cfg.rms_eps, tap);
     return hipGetLastError();
   }
   // one block per CU at most (the weights fill most of its LDS), each
@@ -508,7 +523,7 @@ hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const fl
   const int pairs = ((N + RT_TB - 1) / RT_TB + 1) / 2;
   router_tail_kernel<<<dim3(pairs < 256 ? pairs : 256), 512, RT_LDS, st>>>(
       u, ks, w.b1, w.W2, w.b2, w.gr, w.Wa, w.ca, w.We, w.ce, w.Wb, w.cb, mode, bit, eidx, egate, N,
-      cfg.n_heads, attn_groups(cfg), cfg.n_experts + 1, cfg.top_k, cfg.rms_eps);
+      cfg.n_heads, attn_groups(cfg), cfg.n_experts + 1, cfg.top_k, cfg.rms_eps, tap);
   return hipGetLastError();
 }
 

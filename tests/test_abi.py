@@ -97,3 +97,36 @@ def test_bad_calls_return_codes_without_launching():
     # unknown op
     assert lib.triroute_workspace_bytes(C.byref(c), 42, 1, 1, C.byref(n)) == -1
     assert lib.triroute_status_string(-3) == b"workspace too small"
+
+
+def test_relaxed_router_rejects_bad_parameters():
+    """triroute_router_relaxed checks its relaxation parameters on the host
+    (Sec. 3.4 temperatures, whitening statistics given together, the dual
+    EMA momentum in [0, 1]) before anything is launched."""
+    lib = tr.lib()
+    c = cfg160()
+    fake = 1 << 40
+    rw = tr.RouterW(*([fake] * 12))
+    cmp = tr.Compaction(*([fake] * 5))
+    out = tr.RelaxOut(fake, fake, fake, fake, fake, None, None, None, None, None)
+
+    def call(ws_bytes=1 << 40, **over):
+        p = tr.RelaxParams(g_attn=fake, g_bits=fake, pos=fake, white_mu=fake, white_sd=fake,
+                           white_eps=1e-5, tau_a=1.0, tau_b=1.0, zeta=0.5, alpha=0.01,
+                           beta=0.001, gamma=0.1, dual=None, dual_lr=0.05, dual_ema=0.1)
+        for k, v in over.items():
+            setattr(p, k, v)
+        return lib.triroute_router_relaxed(C.byref(c), 8, 2048, fake, fake, C.byref(rw),
+                                           C.byref(p), fake, fake, fake, fake, fake,
+                                           C.byref(cmp), C.byref(out), fake, ws_bytes, None)
+    assert call(tau_a=0.0) == -1 and b"temperature" in lib.triroute_last_error()
+    assert call(tau_b=float("inf")) == -1
+    assert call(white_sd=None) == -1 and b"white_mu" in lib.triroute_last_error()
+    assert call(g_bits=None) == -1
+    assert call(dual_ema=1.5) == -1 and b"dual_ema" in lib.triroute_last_error()
+    assert call(zeta=float("nan")) == -1
+    assert call(ws_bytes=1024) == -3
+    n = C.c_size_t()
+    assert lib.triroute_workspace_bytes(C.byref(c), tr.OP_ROUTER_RELAXED, 8, 2048, C.byref(n)) == 0
+    # beyond the router's scratch: the logits and h^ of every token
+    assert n.value > tr.workspace_bytes(c, tr.OP_ROUTER, 8, 2048) + 8 * 2048 * (3 * 12 + 9 + 4 + 128) * 4

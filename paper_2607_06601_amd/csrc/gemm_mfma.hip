@@ -154,11 +154,18 @@ struct QkvM {
     jw = dh == 64 ? 0 : 32 * wn;
   }
   __device__ uint32_t a_off(const MTile &t, int r) const { return uint32_t(t.m0 + r) * uint32_t(2 * d); }
+  // 256-column tiles (d_h 128 only): wave column wn holds the tile's head
+  // wn, lane column c pairs j = 4 c + (ni >> 1), first halves in even ni.
   template <int NI>
   __device__ uint32_t b_off_w4(const MTile &t, int wn, int ni, int c) const {
     int hcol, jw;
-    w4_head(t, wn, hcol, jw);
-    const int gc = hcol + jw + 2 * c + (ni >> 1) + (ni & 1) * (dh >> 1);
+    if constexpr (NI == 8) {
+      hcol = t.n0 + 128 * wn;
+      jw = 0;
+    } else {
+      w4_head(t, wn, hcol, jw);
+    }
+    const int gc = hcol + jw + (NI / 2) * c + (ni >> 1) + (ni & 1) * (dh >> 1);
     // (arithmetic on the field values: a select of fields by a lane-varying
     // condition becomes a per-lane load from the kernel arguments)
     const uint32_t base = wq_o + uint32_t(gc >= Hd) * (wk_o - wq_o) + uint32_t(gc >= HKd) * (wv_o - wk_o);
@@ -166,6 +173,78 @@ struct QkvM {
   }
   template <int MI, int NI>
   __device__ void store_w4(const MTile &t, const f32x4_t (&acc)[MI][NI], int wm, int wn, int lane) const {
+    if constexpr (NI == 8)
+      store_w4_wide(t, acc, wm, wn, lane);
+    else
+      store_w4_narrow(t, acc, wm, wn, lane);
+  }
+  // 256-column tiles: each lane holds both halves of pairs j .. j + 3 of
+  // head wn; the rotation entries of a row block mi are loaded one block
+  // ahead of their use.
+  template <int MI, int NI>
+  __device__ void store_w4_wide(const MTile &t, const f32x4_t (&acc)[MI][NI], int wm, int wn,
+                                int lane) const {
+    const int hcol = t.n0 + 128 * wn;
+    if (hcol >= Ncols) return;
+    const int Hd = H * dh, Kd = Hkv * dh, hd = dh >> 1;
+    bf16 *out = q;
+    int ld = Hd, col = hcol;
+    bool rot = true;
+    if (hcol >= Hd + Kd) {
+      out = v; ld = Kd; col = hcol - Hd - Kd; rot = false;
+    } else if (hcol >= Hd) {
+      out = k; ld = Kd; col = hcol - Hd;
+    }
+    const int j = 4 * (lane & 15);
+    auto row_of = [&](int mi, int i) { return wm * MI * 16 + mi * 16 + 4 * (lane >> 4) + i; };
+    auto load_cs = [&](int mi, float4 (&cs)[4][2]) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = row_of(mi, i);
+        const float4 *tb = (const float4 *)(rope + int64_t(t.m0 + (r < t.mvalid ? r : 0)) * hd + j);
+        cs[i][0] = tb[0];
+        cs[i][1] = tb[1];
+      }
+    };
+    float4 cur[4][2], nxt[4][2];
+    if (rot) load_cs(0, cur);
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi) {
+      if (rot && mi + 1 < MI) load_cs(mi + 1, nxt);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = row_of(mi, i);
+        float y1[4], y2[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float a1 = acc[mi][2 * u][i], a2 = acc[mi][2 * u + 1][i];
+          y1[u] = a1;
+          y2[u] = a2;
+          if (rot) {
+            const float4 c4 = cur[i][u >> 1];  // (cos, sin) of pairs j + 2 (u / 2), + 1
+            const float cs = (u & 1) ? c4.z : c4.x, sn = (u & 1) ? c4.w : c4.y;
+            y1[u] = a1 * cs - a2 * sn;
+            y2[u] = a1 * sn + a2 * cs;
+          }
+        }
+        if (r < t.mvalid) {
+          bf16 *o = out + int64_t(t.m0 + r) * ld + col + j;
+          *(uint2 *)o = make_uint2(pk_bf16(y1[0], y1[1]), pk_bf16(y1[2], y1[3]));
+          *(uint2 *)(o + hd) = make_uint2(pk_bf16(y2[0], y2[1]), pk_bf16(y2[2], y2[3]));
+        }
+      }
+      if (rot && mi + 1 < MI) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          cur[i][0] = nxt[i][0];
+          cur[i][1] = nxt[i][1];
+        }
+      }
+    }
+  }
+  template <int MI, int NI>
+  __device__ void store_w4_narrow(const MTile &t, const f32x4_t (&acc)[MI][NI], int wm, int wn,
+                                  int lane) const {
     static_assert(NI == 4, "two pairs per lane");
     int hcol, jw;
     w4_head(t, wn, hcol, jw);
@@ -1046,6 +1125,10 @@ hipError_t mfma_qkv(const triroute_cfg &cfg, int B, int Tq, const void *n1,
     p.wq_o = uint32_t((const uint8_t *)p.Wq - (const uint8_t *)p.Wlo);
     p.wk_o = uint32_t((const uint8_t *)p.Wk - (const uint8_t *)p.Wlo) - uint32_t(p.Hd) * pitch;
     p.wv_o = uint32_t((const uint8_t *)p.Wv - (const uint8_t *)p.Wlo) - uint32_t(p.HKd) * pitch;
+    // d_h 128: one head per wave column on 256-column tiles (long K steps,
+    // one barrier each), where the columns divide into them
+    if (p.dh == 128 && p.Ncols % 256 == 0)
+      return launch_w4<QkvM, 256, 256>(p, cfg.d_model, (p.N + 255) / 256, p.Ncols / 256, st);
     return launch_w4<QkvM, 256, 128>(p, cfg.d_model, (p.N + 255) / 256, p.Ncols / 128, st);
   }
   return launch<QkvM, 256, 128, 4, 2, 64, 3>(p, cfg.d_model, (p.N + 255) / 256, (p.Ncols + 127) / 128, st);

@@ -15,6 +15,7 @@ from . import quant  # noqa: F401
 from . import cost  # noqa: F401
 from . import stack  # noqa: F401
 from . import relax  # noqa: F401
+from . import relax_grad  # noqa: F401
 from .layer import (  # noqa: F401
     MODE_SKIP, MODE_LOCAL, MODE_FULL, BITS,
     rmsnorm, gelu, silu, softmax, rope,

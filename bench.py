@@ -574,9 +574,9 @@ def bench_granularity(cx, steps, warmup, head):
 
 def bench_relaxed(cx, steps, warmup):
     """The training-time relaxed controller forward (whitening, ST-Gumbel,
-    expected costs, losses, dual step, compaction) on the headline prefill's
-    tokens, beside the inference controller (triroute_router) on the same
-    tokens."""
+    expected costs, losses, dual step, compaction) and its backward pass on
+    the headline prefill's tokens, beside the inference controller
+    (triroute_router) on the same tokens."""
     torch, tr, np = cx.torch, cx.tr, cx.np
     L = cx.layer(HEADLINE)
     cfg = L["cfg"]
@@ -616,17 +616,45 @@ def bench_relaxed(cx, steps, warmup):
     def inference(_):
         tr.router(c, B, T, D.x, D.psi, D.rw, n1, mode, bit, eidx, egate, cmp.struct, ws_i)
 
+    # the backward pass on the same tokens: upstream gradients of the soft
+    # samples and gates drawn N(0, 1), balance factors stepped each call
+    o.append(torch.empty(2, E + 1, dtype=torch.float64, device=dev))
+    out.usage_exp = o[-1].data_ptr()
+    A = H
+    up = [cx.to_dev(cx.gen.normal(9, n, shp), f32) for n, shp in
+          (("bwd_ga", (N, A, 3)), ("bwd_gb", (N, 4)), ("bwd_gg", (N, k)))]
+    lam = cx.to_dev(np.asarray(R["dual"][:2]), torch.float64)
+    rho = torch.ones(3, dtype=torch.float64, device=dev)
+    gin = tr.RelaxGradIn(g_attn=up[0].data_ptr(), g_bits=up[1].data_ptr(), g_gate=up[2].data_ptr(),
+                         lambda_=lam.data_ptr(), rho=rho.data_ptr(), rho_m=0.01)
+    shapes = dict(dW1=(128, cfg["d"] + 8), db1=(128,), dW2=(128, 128), db2=(128,), dgr=(128,),
+                  dWa=(3 * H, 128), dca=(3 * H,), dWe=(E + 1, 128), dce=(E + 1,), dWb=(4, 128),
+                  dcb=(4,), dg1=(cfg["d"],), dx=(N, cfg["d"]), dpsi=(N, 8))
+    gt = {n: torch.empty(shp, dtype=f32, device=dev) for n, shp in shapes.items()}
+    gout = tr.RelaxGradOut(**{n: v.data_ptr() for n, v in gt.items()})
+    ws_b = tr.workspace(c, tr.OP_ROUTER_RELAXED_BACKWARD, B, T)
+
+    def backward(_):
+        tr.router_relaxed_backward(c, B, T, D.x, D.psi, D.rw, p, out, eidx, egate, gin, gout, ws_b)
+
     for i in range(warmup):
         relaxed(i)
         inference(i)
+    relaxed(0)
+    for i in range(warmup):
+        backward(i)
     ms_r, _ = cx.timed(relaxed, steps)
     ms_i, _ = cx.timed(inference, steps)
+    relaxed(0)
+    ms_b, _ = cx.timed(backward, steps)
     return {"workload": f"relaxed controller forward on the 1.3B-class prefill tokens ({B} x {T}): "
                         "per-axis whitening, ST-Gumbel (attention per head, bits), top-k experts, "
                         "expected costs, balance / z / entropy losses, dual step, compaction",
             "tokens_per_s": round(N / (ms_r * 1e-3), 1), "ms_per_call": round(ms_r, 4),
             "inference_router_ms": round(ms_i, 4),
-            "relaxed_over_inference_ms": round(ms_r / ms_i, 3)}
+            "relaxed_over_inference_ms": round(ms_r / ms_i, 3),
+            "backward_ms_per_call": round(ms_b, 4),
+            "backward_tokens_per_s": round(N / (ms_b * 1e-3), 1)}
 
 
 def summarize_pmc(fetch_dir, write_dir, regex):

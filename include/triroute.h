@@ -203,7 +203,8 @@ enum triroute_op {
   TRIROUTE_OP_LAYER_PREFILL = 6,
   TRIROUTE_OP_LAYER_DECODE = 7,
   TRIROUTE_OP_STACK_DECODE = 8,
-  TRIROUTE_OP_ROUTER_RELAXED = 9
+  TRIROUTE_OP_ROUTER_RELAXED = 9,
+  TRIROUTE_OP_ROUTER_RELAXED_BACKWARD = 10
 };
 
 /* ---- configuration, errors, sizes ---------------------------------------- */
@@ -450,6 +451,57 @@ int triroute_router_relaxed(const triroute_cfg *cfg, int B, int T, const void *x
                             uint8_t *bit, int32_t *eidx, float *egate,
                             const triroute_compaction *cmp, const triroute_relax_out *out,
                             void *ws, size_t ws_bytes, triroute_stream_t stream);
+
+/* Upstream gradients and balance state of the relaxed backward (device). */
+typedef struct triroute_relax_grad_in {
+  const float *g_attn;   /* [N, A, 3] dL/dy~^a: the language-model gradient the straight-through
+                          * estimator hands from the hard attention choice to its soft sample */
+  const float *g_bits;   /* [N, 4] dL/dy~^b */
+  const float *g_gate;   /* [N, k] dL/dp-bar of the selected slots (from the expert combine) */
+  const double *lambda;  /* [2] the multipliers of the forward's regulariser, or NULL (0) */
+  double *rho;           /* [3] gradient-balance factors (attention, experts, bits), in and out,
+                          * or NULL (1, no update) */
+  float rho_m;           /* EMA momentum of rho; 0 leaves rho as is */
+} triroute_relax_grad_in;
+
+/* Gradients of the relaxed backward (device fp32, overwritten): one per
+ * router weight, shaped like it (see triroute_router_w), and of the inputs:
+ * dx [N, d], dpsi [N, d_psi] (the controller path only: the attention
+ * sublayer's share of n1's gradient is the caller's).  lm_norm [3] (fp64,
+ * may be NULL): per axis the norm of the language-model part of the logit
+ * gradient before balancing. */
+typedef struct triroute_relax_grad_out {
+  float *dW1, *db1, *dW2, *db2, *dgr;
+  float *dWa, *dca, *dWe, *dce, *dWb, *dcb;
+  float *dg1, *dx, *dpsi;
+  double *lm_norm;
+} triroute_relax_grad_out;
+
+/* Backward pass of triroute_router_relaxed (Algorithm 1 step 7 for the
+ * controller; Sec. 3.4-3.7).  Differentiates the soft outputs the rest of the
+ * layer consumes and the regulariser, with the hard choices, the usage
+ * fractions f_o, the whitening statistics and the multipliers held constant:
+ *   attention / bits: dz = (1 / tau) y~ (G - <y~, G>) with G = g_attn / rho
+ *   (language-model part) plus lambda_r / C_dense^r times the option costs
+ *   of Sec. 3.5; experts: dz_j = p-bar_j (G_j - <p-bar, G>) on the selected
+ *   slots with G = g_gate / rho plus lambda_flops / C_dense^flops 3 d d_f on
+ *   the real experts; each axis adds the gradients of alpha L_bal + beta L_z
+ *   + gamma L_ent (the floor only when it is active); then the chain through
+ *   the whitened heads, RMSNorm(h; gr), W2, the GELU, W1 and Norm(x; g1).
+ *   rho, when given, is used as passed and then set to (1 - rho_m) rho +
+ *   rho_m ||language-model part||.
+ * x, psi, w, p as given to the forward (the trunk is recomputed; its logits
+ * equal the forward's); fwd: the forward's outputs, of which y_attn,
+ * y_bits, stats and usage_exp are read (usage_exp must have been
+ * requested); eidx, egate: the forward's expert choices.
+ * ws: triroute_workspace_bytes(cfg, TRIROUTE_OP_ROUTER_RELAXED_BACKWARD, B, T). */
+int triroute_router_relaxed_backward(const triroute_cfg *cfg, int B, int T, const void *x,
+                                     const float *psi, const triroute_router_w *w,
+                                     const triroute_relax_params *p,
+                                     const triroute_relax_out *fwd, const int32_t *eidx,
+                                     const float *egate, const triroute_relax_grad_in *gin,
+                                     const triroute_relax_grad_out *gout, void *ws,
+                                     size_t ws_bytes, triroute_stream_t stream);
 
 /* ---- no-allocation variant ---------------------------------------------- */
 

@@ -19,7 +19,8 @@ LIB_PATH = os.path.join(_HERE, "libtriroute.so")
 F32, BF16 = 0, 1
 SKIP, LOCAL, FULL = 0, 1, 2
 OP_ROUTER, OP_QKV, OP_KV_APPEND, OP_ATTN_PREFILL, OP_ATTN_DECODE, OP_MOE, \
-    OP_LAYER_PREFILL, OP_LAYER_DECODE, OP_STACK_DECODE, OP_ROUTER_RELAXED = range(10)
+    OP_LAYER_PREFILL, OP_LAYER_DECODE, OP_STACK_DECODE, OP_ROUTER_RELAXED, \
+    OP_ROUTER_RELAXED_BACKWARD = range(11)
 # fp64 fields of RelaxOut.stats (axes in the order attention, experts, bits)
 RS_LBAL, RS_LZ, RS_LENT, RS_ENTROPY, RS_CBAR, RS_COST, RS_DENSE, RS_REG = 0, 3, 6, 9, 12, 14, 16, 18
 RS_F_ATTN, RS_P_ATTN, RS_F_BITS, RS_P_BITS, RELAX_NSTAT = 19, 22, 25, 29, 33
@@ -94,6 +95,17 @@ class RelaxOut(C.Structure):
                  "h_mean", "h_var", "z")]
 
 
+class RelaxGradIn(C.Structure):
+    _fields_ = [("g_attn", C.c_void_p), ("g_bits", C.c_void_p), ("g_gate", C.c_void_p),
+                ("lambda_", C.c_void_p), ("rho", C.c_void_p), ("rho_m", C.c_float)]
+
+
+class RelaxGradOut(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in
+                ("dW1", "db1", "dW2", "db2", "dgr", "dWa", "dca", "dWe", "dce", "dWb", "dcb",
+                 "dg1", "dx", "dpsi", "lm_norm")]
+
+
 EXPORTS = [
     "triroute_validate", "triroute_status_string", "triroute_last_error",
     "triroute_workspace_bytes", "triroute_kv_cache_bytes", "triroute_kv_cache_init",
@@ -101,7 +113,7 @@ EXPORTS = [
     "triroute_kv_append", "triroute_kv_export", "triroute_router", "triroute_qkv",
     "triroute_attn_prefill", "triroute_attn_decode", "triroute_oproj", "triroute_moe",
     "triroute_layer_prefill", "triroute_layer_decode", "triroute_layer_decode_noalloc",
-    "triroute_stack_decode", "triroute_router_relaxed",
+    "triroute_stack_decode", "triroute_router_relaxed", "triroute_router_relaxed_backward",
 ]
 
 _lib = None
@@ -138,6 +150,7 @@ def lib():
             "triroute_layer_decode_noalloc": [P, i32, P, P, P, P, P, P, P, P, P, P],
             "triroute_stack_decode": [P, i32, i32, P, P, P, P, P, P, P, sz, P],
             "triroute_router_relaxed": [P, i32, i32, P, P, P, P, P, P, P, P, P, P, P, P, sz, P],
+            "triroute_router_relaxed_backward": [P, i32, i32, P, P, P, P, P, P, P, P, P, P, sz, P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -267,6 +280,15 @@ def router_relaxed(cfg, B, T, x, psi, rw: RouterW, params: RelaxParams, n1, mode
                                          C.byref(params), _p(n1), _p(mode), _p(bit), _p(eidx),
                                          _p(egate), C.byref(cmp), C.byref(out), _p(ws),
                                          ws.numel(), _stream(stream)))
+
+
+def router_relaxed_backward(cfg, B, T, x, psi, rw: RouterW, params: RelaxParams,
+                            fwd: RelaxOut, eidx, egate, gin: RelaxGradIn, gout: RelaxGradOut, ws,
+                            stream=None):
+    """Backward pass of the relaxed controller (triroute_router_relaxed_backward)."""
+    _check(lib().triroute_router_relaxed_backward(
+        C.byref(cfg), B, T, _p(x), _p(psi), C.byref(rw), C.byref(params), C.byref(fwd), _p(eidx),
+        _p(egate), C.byref(gin), C.byref(gout), _p(ws), ws.numel(), _stream(stream)))
 
 
 def qkv(cfg, B, T, n1, dw: DenseW, q, k, v, ws, pos0=None, stream=None):

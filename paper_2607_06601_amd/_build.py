@@ -19,7 +19,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libtriroute.so")
 
 SOURCES = ["api.cpp", "router.hip", "compact.hip", "kv.hip", "gemm.hip", "gemm_mfma.hip", "attn_valu.hip",
-           "attn_mfma.hip", "misc.hip", "relax.hip"]
+           "attn_mfma.hip", "misc.hip", "relax.hip", "relax_grad.hip"]
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -206,6 +206,42 @@ RelaxWs carve_relax(Carve &cv, const triroute_cfg &c, int N) {
   return w;
 }
 
+// The relaxed backward's scratch beyond the forward's: taps of the
+// recomputed trunk, the recomputed tail's decisions (discarded), the
+// per-token gradients, [n1; psi] and its gradient, and the gram partials.
+struct RelaxBwdWs {
+  float *a1, *hpre, *dz, *dh, *da1, *u, *tgr, *lmsq, *s, *ds, *part, *G, *dc;
+  double *lmsq_sum;
+  void *n1;
+  uint8_t *mode, *bit;
+  int32_t *eidx;
+  float *egate;
+};
+RelaxBwdWs carve_relax_bwd(Carve &cv, const triroute_cfg &c, int N) {
+  const int NZ = 3 * tr::attn_groups(c) + c.n_experts + 5, K1 = c.d_model + c.d_psi;
+  RelaxBwdWs w;
+  w.a1 = cv.take<float>(size_t(N) * 128);
+  w.hpre = cv.take<float>(size_t(N) * 128);
+  w.dz = cv.take<float>(size_t(N) * NZ);
+  w.dh = cv.take<float>(size_t(N) * 128);
+  w.da1 = cv.take<float>(size_t(N) * 128);
+  w.u = cv.take<float>(size_t(N) * 128);
+  w.tgr = cv.take<float>(size_t(N) * 128);
+  w.lmsq = cv.take<float>(size_t(N) * 4);
+  w.s = cv.take<float>(size_t(N) * K1);
+  w.ds = cv.take<float>(size_t(N) * K1);
+  w.part = cv.take<float>(tr::relax_grad_part_floats(c, N));
+  w.G = cv.take<float>(size_t(NZ) * 128);
+  w.dc = cv.take<float>(NZ);
+  w.lmsq_sum = cv.take<double>(4);
+  w.n1 = cv.take<uint8_t>(size_t(N) * c.d_model * act_bytes(c));
+  w.mode = cv.take<uint8_t>(size_t(N) * c.n_heads);
+  w.bit = cv.take<uint8_t>(N);
+  w.eidx = cv.take<int32_t>(size_t(N) * c.top_k);
+  w.egate = cv.take<float>(size_t(N) * c.top_k);
+  return w;
+}
+
 size_t op_bytes(const triroute_cfg &c, int op, int B, int T) {
   Carve cv(nullptr);
   const int N = B * T;
@@ -235,6 +271,11 @@ size_t op_bytes(const triroute_cfg &c, int op, int B, int T) {
     case TRIROUTE_OP_ROUTER_RELAXED:
       carve_router(cv, c, N);
       carve_relax(cv, c, N);
+      break;
+    case TRIROUTE_OP_ROUTER_RELAXED_BACKWARD:
+      carve_router(cv, c, N);
+      carve_relax(cv, c, N);
+      carve_relax_bwd(cv, c, N);
       break;
     default: return 0;
   }
@@ -416,7 +457,7 @@ int triroute_workspace_bytes(const triroute_cfg *cfg, int op, int B, int T, size
   TRY(check_cfg(cfg));
   TRY(check_bt(B, T));
   REQUIRE(bytes, TRIROUTE_E_INVALID, "bytes is NULL");
-  REQUIRE(op >= TRIROUTE_OP_ROUTER && op <= TRIROUTE_OP_ROUTER_RELAXED, TRIROUTE_E_INVALID,
+  REQUIRE(op >= TRIROUTE_OP_ROUTER && op <= TRIROUTE_OP_ROUTER_RELAXED_BACKWARD, TRIROUTE_E_INVALID,
           "unknown op %d", op);
   *bytes = op_bytes(*cfg, op, B, T);
   return TRIROUTE_OK;
@@ -602,6 +643,95 @@ int triroute_router_relaxed(const triroute_cfg *cfg, int B, int T, const void *x
   j.dual_lr = p->dual_lr; j.dual_ema = p->dual_ema;
   CHECK_HIP(tr::launch_relax(*cfg, N, j, st), "relaxed forward launch");
   CHECK_HIP(tr::launch_compact(*cfg, B, T, mode, eidx, *cmp, rw.hist, st), "compaction launch");
+  return TRIROUTE_OK;
+}
+
+int triroute_router_relaxed_backward(const triroute_cfg *cfg, int B, int T, const void *x,
+                                     const float *psi, const triroute_router_w *w,
+                                     const triroute_relax_params *p,
+                                     const triroute_relax_out *fwd, const int32_t *eidx,
+                                     const float *egate, const triroute_relax_grad_in *gin,
+                                     const triroute_relax_grad_out *go, void *ws,
+                                     size_t ws_bytes, triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  TRY(check_bt(B, T));
+  REQUIRE(x && (psi || cfg->d_psi == 0) && w && p && fwd && eidx && egate && gin && go,
+          TRIROUTE_E_INVALID, "NULL argument");
+  REQUIRE(w->g1 && w->W1 && w->b1 && w->W2 && w->b2 && w->gr && w->Wa && w->ca && w->We &&
+              w->ce && w->Wb && w->cb,
+          TRIROUTE_E_INVALID, "NULL router weight");
+  REQUIRE(p->pos, TRIROUTE_E_INVALID, "NULL position array");
+  REQUIRE(!p->white_mu == !p->white_sd, TRIROUTE_E_INVALID,
+          "white_mu and white_sd must both be given or both be NULL");
+  REQUIRE(isfinite(p->tau_a) && isfinite(p->tau_b) && p->tau_a > 0.f && p->tau_b > 0.f,
+          TRIROUTE_E_INVALID, "temperatures must be finite and positive (%g, %g)", p->tau_a,
+          p->tau_b);
+  REQUIRE(isfinite(p->white_eps) && isfinite(p->zeta) && isfinite(p->alpha) &&
+              isfinite(p->beta) && isfinite(p->gamma),
+          TRIROUTE_E_INVALID, "a relaxation parameter is not finite");
+  REQUIRE(fwd->y_attn && fwd->y_bits && fwd->stats && fwd->usage_exp, TRIROUTE_E_INVALID,
+          "the backward reads the forward's y_attn, y_bits, stats and usage_exp");
+  REQUIRE(gin->g_attn && gin->g_bits && gin->g_gate, TRIROUTE_E_INVALID, "NULL upstream gradient");
+  REQUIRE(isfinite(gin->rho_m) && gin->rho_m >= 0.f && gin->rho_m <= 1.f, TRIROUTE_E_INVALID,
+          "rho_m (%g) outside [0, 1]", gin->rho_m);
+  REQUIRE(go->dW1 && go->db1 && go->dW2 && go->db2 && go->dgr && go->dWa && go->dca && go->dWe &&
+              go->dce && go->dWb && go->dcb && go->dg1 && go->dx && (go->dpsi || cfg->d_psi == 0),
+          TRIROUTE_E_INVALID, "NULL gradient output");
+  TRY(check_aligned({x, w->g1, w->W1, w->W2, w->Wa, w->We, w->Wb, go->dx}));
+  TRY(check_ws(*cfg, TRIROUTE_OP_ROUTER_RELAXED_BACKWARD, B, T, ws, ws_bytes));
+  TRY(prepare_once());
+  const int N = B * T, A = tr::attn_groups(*cfg), E1 = cfg->n_experts + 1;
+  Carve cv(ws);
+  RouterWs rw = carve_router(cv, *cfg, N);
+  RelaxWs xw = carve_relax(cv, *cfg, N);
+  RelaxBwdWs bw = carve_relax_bwd(cv, *cfg, N);
+  hipStream_t st = (hipStream_t)stream;
+  // the head weights as the forward applied them, [Wa; We; Wb] in one array
+  triroute_router_w wf = *w;
+  if (p->white_mu) {
+    CHECK_HIP(tr::launch_white_fold(*cfg, *w, p->white_mu, p->white_sd, p->white_eps, xw.Wf,
+                                    xw.cf, st),
+              "whitening fold launch");
+    wf.Wa = xw.Wf;
+    wf.We = xw.Wf + size_t(3 * A) * 128;
+    wf.Wb = xw.Wf + size_t(3 * A + E1) * 128;
+    wf.ca = xw.cf;
+    wf.ce = xw.cf + 3 * A;
+    wf.cb = xw.cf + 3 * A + E1;
+  } else {
+    CHECK_HIP(hipMemcpyAsync(xw.Wf, w->Wa, size_t(3 * A) * 128 * 4, hipMemcpyDeviceToDevice, st),
+              "head weight copy");
+    CHECK_HIP(hipMemcpyAsync(xw.Wf + size_t(3 * A) * 128, w->We, size_t(E1) * 128 * 4,
+                             hipMemcpyDeviceToDevice, st),
+              "head weight copy");
+    CHECK_HIP(hipMemcpyAsync(xw.Wf + size_t(3 * A + E1) * 128, w->Wb, size_t(4) * 128 * 4,
+                             hipMemcpyDeviceToDevice, st),
+              "head weight copy");
+  }
+  tr::TailTap tap;
+  tap.h = xw.h;
+  tap.z = xw.z;
+  tap.a1 = bw.a1;
+  tap.hpre = bw.hpre;
+  CHECK_HIP(tr::launch_router(*cfg, N, x, psi, wf, bw.n1, bw.mode, bw.bit, bw.eidx, bw.egate,
+                              rw.rinv, rw.u, nullptr, st, tap),
+            "router launch");
+  tr::RelaxBwdJob j;
+  j.z = xw.z; j.hh = xw.h; j.a1 = bw.a1; j.hpre = bw.hpre;
+  j.y_attn = fwd->y_attn; j.y_bits = fwd->y_bits; j.egate = egate; j.eidx = eidx; j.pos = p->pos;
+  j.g_attn = gin->g_attn; j.g_bits = gin->g_bits; j.g_gate = gin->g_gate;
+  j.stats = fwd->stats; j.usage = fwd->usage_exp; j.lambda = gin->lambda;
+  j.rho_io = gin->rho; j.rho_m = gin->rho_m;
+  j.tau_a = p->tau_a; j.tau_b = p->tau_b; j.zeta = p->zeta; j.alpha = p->alpha; j.beta = p->beta;
+  j.gamma = p->gamma;
+  j.dz = bw.dz; j.dh = bw.dh; j.da1 = bw.da1; j.u = bw.u; j.tgr = bw.tgr; j.lmsq = bw.lmsq;
+  j.s = bw.s; j.ds = bw.ds; j.part = bw.part; j.G = bw.G; j.dc = bw.dc; j.lmsq_sum = bw.lmsq_sum;
+  j.out = tr::RelaxGradOut{go->dW1, go->db1, go->dW2, go->db2, go->dgr, go->dWa, go->dca,
+                           go->dWe, go->dce, go->dWb, go->dcb, go->dg1, go->dx, go->dpsi,
+                           go->lm_norm};
+  CHECK_HIP(tr::launch_relax_backward(*cfg, N, x, psi, *w, xw.Wf, p->white_mu, p->white_sd,
+                                      p->white_eps, j, st),
+            "relaxed backward launch");
   return TRIROUTE_OK;
 }
 

@@ -42,10 +42,11 @@ __device__ __forceinline__ float2 rope_entry(const RopeJob &r, int row, int j) {
   sincosf(float(rr), &sn, &cs);
   return make_float2(cs, sn);
 }
-// Optional copies of the controller tail's intermediates: h^ [N, 128] and
-// the head logits z [N, 3 A + E + 5] (either may be NULL).
+// Optional copies of the controller tail's intermediates (any may be NULL):
+// h^ [N, 128], the head logits z [N, 3 A + E + 5], the trunk's pre-GELU
+// a1 = W1 [n1; psi] + b1 [N, 128] and h = W2 u + b2 before its norm [N, 128].
 struct TailTap {
-  float *h = nullptr, *z = nullptr;
+  float *h = nullptr, *z = nullptr, *a1 = nullptr, *hpre = nullptr;
 };
 // rope (optional): the first RMSNorm also writes that rotation table
 hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const float *psi,
@@ -141,4 +142,30 @@ hipError_t launch_white_fold(const triroute_cfg &cfg, const triroute_router_w &w
                              const float *sd, float eps, float *Wf, float *cf, hipStream_t st);
 hipError_t launch_relax(const triroute_cfg &cfg, int N, const RelaxJob &j, hipStream_t st);
 
+// relax_grad.hip: the relaxed controller's backward pass
+struct RelaxGradOut {
+  float *dW1, *db1, *dW2, *db2, *dgr, *dWa, *dca, *dWe, *dce, *dWb, *dcb, *dg1, *dx, *dpsi;
+  double *lm_norm;
+};
+struct RelaxBwdJob {
+  const float *z, *hh, *a1, *hpre;  // taps of the recomputed trunk and tail
+  const float *y_attn, *y_bits, *egate;
+  const int32_t *eidx, *pos;
+  const float *g_attn, *g_bits, *g_gate;
+  const double *stats, *usage, *lambda;
+  double *rho_io;  // [3] or NULL
+  float rho_m;
+  float tau_a, tau_b, zeta, alpha, beta, gamma;
+  // scratch
+  float *dz, *dh, *da1, *u, *tgr, *lmsq, *s, *ds, *part, *G, *dc;
+  double *lmsq_sum;
+  RelaxGradOut out;
+};
+size_t relax_grad_part_floats(const triroute_cfg &cfg, int N);
+// Wf: the head weights [3A + E + 5][128] as the forward applied them (folded
+// with the whitening, or the plain ones); mu / sd NULL: no whitening
+hipError_t launch_relax_backward(const triroute_cfg &cfg, int N, const void *x, const float *psi,
+                                 const triroute_router_w &w, const float *Wf,
+                                 const float *white_mu, const float *white_sd, float white_eps,
+                                 const RelaxBwdJob &j, hipStream_t st);
 }  // namespace tr

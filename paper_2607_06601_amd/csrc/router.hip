@@ -253,6 +253,7 @@ __global__ __launch_bounds__(512) void router_tail_kernel(
       float y = 0.f;
       if (t0 + t < N) {
         y = sacc[e] + b1[c];
+        if (tap.a1) tap.a1[int64_t(t0 + t) * DR + c] = y;
         y = 0.5f * y * (1.0f + erff(y * 0.70710678118654752f));
       }
       Us[t][c] = y;
@@ -278,7 +279,12 @@ __global__ __launch_bounds__(512) void router_tail_kernel(
   for (int j = 0; j < 2; ++j) {
     const int n = 32 * wave + 16 * j + (lane & 15);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) Us[4 * (lane >> 4) + r][n] = (hacc[j][0][r] + hacc[j][1][r]) + b2[n];
+    for (int r = 0; r < 4; ++r) {
+      const float hv = (hacc[j][0][r] + hacc[j][1][r]) + b2[n];
+      Us[4 * (lane >> 4) + r][n] = hv;
+      const int tr_ = t0 + 4 * (lane >> 4) + r;
+      if (tap.hpre && tr_ < N) tap.hpre[int64_t(tr_) * DR + n] = hv;
+    }
   }
   __syncthreads();
   {
@@ -412,6 +418,10 @@ __global__ __launch_bounds__(256) void router_tail_tok_kernel(
     }
   a0 += b1[lane];
   a1 += b1[lane + 64];
+  if (tap.a1) {
+    tap.a1[int64_t(t) * DR + lane] = a0;
+    tap.a1[int64_t(t) * DR + lane + 64] = a1;
+  }
   us[lane] = 0.5f * a0 * (1.0f + erff(a0 * 0.70710678118654752f));
   us[lane + 64] = 0.5f * a1 * (1.0f + erff(a1 * 0.70710678118654752f));
   __builtin_amdgcn_wave_barrier();
@@ -427,6 +437,10 @@ __global__ __launch_bounds__(256) void router_tail_tok_kernel(
   }
   h0 += b2[lane];
   h1 += b2[lane + 64];
+  if (tap.hpre) {
+    tap.hpre[int64_t(t) * DR + lane] = h0;
+    tap.hpre[int64_t(t) * DR + lane + 64] = h1;
+  }
   // h^ = RMSNorm(h) gr
   const float ss = seg_sum(h0 * h0 + h1 * h1, 64);
   const float r = 1.0f / sqrtf(ss / float(DR) + eps);

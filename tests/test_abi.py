@@ -130,3 +130,31 @@ def test_relaxed_router_rejects_bad_parameters():
     assert lib.triroute_workspace_bytes(C.byref(c), tr.OP_ROUTER_RELAXED, 8, 2048, C.byref(n)) == 0
     # beyond the router's scratch: the logits and h^ of every token
     assert n.value > tr.workspace_bytes(c, tr.OP_ROUTER, 8, 2048) + 8 * 2048 * (3 * 12 + 9 + 4 + 128) * 4
+
+
+def test_relaxed_backward_rejects_bad_arguments():
+    """triroute_router_relaxed_backward needs the forward's statistics and
+    usage, the upstream gradients and a momentum in [0, 1]; checked on the
+    host before any launch."""
+    lib = tr.lib()
+    c = cfg160()
+    fake = 1 << 40
+    rw = tr.RouterW(*([fake] * 12))
+    p = tr.RelaxParams(pos=fake, tau_a=1.0, tau_b=1.0, zeta=0.5, alpha=0.01, beta=0.001,
+                       gamma=0.1)
+    go = tr.RelaxGradOut(*([fake] * 14), None)
+
+    def call(fwd_usage=fake, g_gate=fake, rho_m=0.1, ws_bytes=1 << 40, dx=fake):
+        fwd = tr.RelaxOut(y_attn=fake, y_bits=fake, stats=fake, usage_exp=fwd_usage)
+        gin = tr.RelaxGradIn(g_attn=fake, g_bits=fake, g_gate=g_gate, rho_m=rho_m)
+        go.dx = dx
+        return lib.triroute_router_relaxed_backward(C.byref(c), 8, 2048, fake, fake, C.byref(rw),
+                                                    C.byref(p), C.byref(fwd), fake, fake,
+                                                    C.byref(gin), C.byref(go), fake, ws_bytes, None)
+    assert call(fwd_usage=None) == -1 and b"usage_exp" in lib.triroute_last_error()
+    assert call(g_gate=None) == -1 and b"upstream" in lib.triroute_last_error()
+    assert call(rho_m=2.0) == -1 and b"rho_m" in lib.triroute_last_error()
+    assert call(dx=fake + 4) == -1 and b"aligned" in lib.triroute_last_error()
+    assert call(ws_bytes=1024) == -3
+    assert tr.workspace_bytes(c, tr.OP_ROUTER_RELAXED_BACKWARD, 8, 2048) > \
+        tr.workspace_bytes(c, tr.OP_ROUTER_RELAXED, 8, 2048)

@@ -19,7 +19,7 @@ from oracle import relax
 from oracle.ties import enforce_relaxed_margins
 from paper_2607_06601_amd.device import DeviceLayer, to_dev
 
-from _common import assert_close, layer, note, npy
+from _common import assert_close, err_ratio, layer, note, npy
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -181,3 +181,95 @@ def test_relaxed_forward_is_deterministic_and_noise_free_limit():
     np.testing.assert_array_equal(a["mode"], mode)
     np.testing.assert_array_equal(a["bit"], bit)
     np.testing.assert_array_equal(a["eidx"], eidx)
+
+
+# ------------------------------------------------------------------ backward
+from oracle import relax_grad  # noqa: E402
+
+GRAD_KEYS = [("dW1", "W1"), ("db1", "b1"), ("dW2", "W2"), ("db2", "b2"), ("dgr", "gr"),
+             ("dWa", "Wa"), ("dca", "ca"), ("dWe", "We"), ("dce", "ce"), ("dWb", "Wb"),
+             ("dcb", "cb"), ("dg1", "g1")]
+
+
+def run_relaxed_backward(L, R, g, up, rho, rho_m):
+    cfg = L["cfg"]
+    D = DeviceLayer(L, moe=False)
+    c = D.cfg
+    B, T = cfg["B"], cfg["T"]
+    N = B * T
+    f32 = dict(dtype=torch.float32, device=DEV)
+    t = dict(pos=to_dev(R["pos"], torch.int32))
+    if R["white_mu"] is not None:
+        t["mu"] = to_dev(R["white_mu"], torch.float32)
+        t["sd"] = to_dev(R["white_sd"], torch.float32)
+    p = tr.RelaxParams(pos=t["pos"].data_ptr(), white_mu=t["mu"].data_ptr() if "mu" in t else None,
+                       white_sd=t["sd"].data_ptr() if "sd" in t else None,
+                       white_eps=R["white_eps"], tau_a=R["tau_a"], tau_b=R["tau_b"],
+                       zeta=R["zeta"], alpha=R["alpha"], beta=R["beta"], gamma=R["gamma"])
+    fw = {n: to_dev(g[n], torch.float32) for n in ("y_attn", "y_bits")}
+    fw["stats"] = to_dev(g["stats"], torch.float64)
+    fw["usage_exp"] = to_dev(g["usage_exp"], torch.float64)
+    fwd = tr.RelaxOut(y_attn=fw["y_attn"].data_ptr(), y_bits=fw["y_bits"].data_ptr(),
+                      stats=fw["stats"].data_ptr(), usage_exp=fw["usage_exp"].data_ptr())
+    eidx = to_dev(g["eidx"], torch.int32)
+    egate = to_dev(g["egate"], torch.float32)
+    u = {n: to_dev(up[n], torch.float32) for n in ("g_ya", "g_yb", "g_gate")}
+    lam = None if R.get("dual") is None else to_dev(np.asarray(R["dual"][:2]), torch.float64)
+    rho_t = to_dev(np.asarray(rho, np.float64), torch.float64)
+    gin = tr.RelaxGradIn(g_attn=u["g_ya"].data_ptr(), g_bits=u["g_yb"].data_ptr(),
+                         g_gate=u["g_gate"].data_ptr(), lambda_=lam.data_ptr() if lam is not None else None,
+                         rho=rho_t.data_ptr(), rho_m=rho_m)
+    out = {n: torch.full(np.shape(L[w]), float("nan"), **f32) for n, w in GRAD_KEYS}
+    out["dx"] = torch.full((N, cfg["d"]), float("nan"), **f32)
+    out["dpsi"] = torch.full((N, 8), float("nan"), **f32)
+    out["lm_norm"] = torch.zeros(3, dtype=torch.float64, device=DEV)
+    go = tr.RelaxGradOut(**{n: v.data_ptr() for n, v in out.items()})
+    ws = tr.workspace(c, tr.OP_ROUTER_RELAXED_BACKWARD, B, T)
+    tr.router_relaxed_backward(c, B, T, D.x, D.psi, D.rw, p, fwd, eidx, egate, gin, go, ws)
+    torch.cuda.synchronize()
+    res = {n: npy(v) for n, v in out.items()}
+    res["rho"] = npy(rho_t)
+    return res
+
+
+BWD_CASES = [  # (workload, groups, whitening, k override, zeta)
+    ("tiny_f32_prefill", None, True, 2, 0.5),
+    ("160m_bf16_prefill", None, True, None, 1.0),
+    ("1p3b_bf16_decode", 4, False, None, 0.5),
+]
+
+
+@pytest.mark.parametrize("name,groups,white,k,zeta", BWD_CASES)
+def test_relaxed_backward_matches_oracle(name, groups, white, k, zeta):
+    L = layer(name, moe=False)
+    if k is not None:
+        L["cfg"] = dict(L["cfg"], k=k)
+    if groups is not None:
+        L = gen.granularity_variant(L, groups)
+    R = gen.relax_inputs(L, white=white)
+    R["zeta"] = zeta
+    enforce_relaxed_margins(L, R)
+    print(f"relaxed backward {name} groups={groups} white={white} k={L['cfg']['k']}", flush=True)
+    g = run_relaxed(L, R)
+    ref = relax.relaxed_forward(L, R)
+    np.testing.assert_array_equal(g["eidx"], ref["S"])
+    N, A = ref["za"].shape[:2]
+    kk = L["cfg"]["k"]
+    up = dict(g_ya=gen.normal(9, "bwd_ga", (N, A, 3)), g_yb=gen.normal(9, "bwd_gb", (N, 4)),
+              g_gate=gen.normal(9, "bwd_gg", (N, kk)))
+    rho, rho_m = (1.5, 0.8, 2.5), 0.1
+    gb = run_relaxed_backward(L, R, g, up, rho, rho_m)
+    want = relax_grad.relaxed_backward(L, R, ref, {n: np.asarray(v, np.float64) for n, v in up.items()},
+                                       rho=rho, rho_m=rho_m)
+    names = [n for n, _ in GRAD_KEYS] + ["dx", "dpsi"]
+    for n in names:  # every ratio first, so that one failure shows them all
+        print(f"  {n}: max err/bound {err_ratio(gb[n], want[n], 'f32') / GRAD_FACTOR:.3f}", flush=True)
+    for n in names:
+        assert_close(gb[n], want[n], "f32", n, factor=GRAD_FACTOR)
+    np.testing.assert_allclose(gb["lm_norm"], want["lm_norm"], rtol=1e-4)
+    np.testing.assert_allclose(gb["rho"], want["rho"], rtol=1e-4)
+
+
+# fp32 gradients summed over up to 16384 tokens in chunks of 128 (fp32 within
+# a chunk, fp64 across): the tolerance is the fp32 bound times this factor
+GRAD_FACTOR = 1.0

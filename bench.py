@@ -411,15 +411,33 @@ def fill_decode_cache(cx, c, cache, cfg, act_t, dense=False):
     return bits_all
 
 
-def run_decode_steps(cx, L, steps, warmup, dense=False):
-    """Timed decode steps of one layer over a freshly filled cache; returns
-    the step time, the step's decisions and the cache."""
+PAGE_TILES = 8
+
+
+def decode_pages(cx, cfg, extra, slack=4):
+    """Pages per width of a paged cache that holds the workload's context and
+    `extra` more tokens a sequence."""
+    per = PAGE_TILES * (4096 // cfg["dh"])
+    need = [slack] * 4
+    for s in range(cfg["B"]):
+        cnt = cx.np.bincount(cx.gen.context_bits(cfg, s), minlength=4)
+        for bi in range(4):
+            need[bi] += -(-(int(cnt[bi]) + extra) // per)
+    return need
+
+
+def run_decode_steps(cx, L, steps, warmup, dense=False, paged=False):
+    """Timed decode steps of one layer over a freshly filled cache (contiguous
+    pools, or a paged cache); returns the step time, the step's decisions and
+    the cache."""
     np, torch, tr = cx.np, cx.torch, cx.tr
     cfg = L["cfg"]
     B, d, H, k = cfg["B"], cfg["d"], cfg["H"], cfg["k"]
     D = cx.DeviceLayer(L)
     c = D.cfg
-    cache = tr.KVCache(c, B, cfg["ctx"] + warmup + steps + 1)
+    cap = cfg["ctx"] + warmup + steps + 1
+    pages = (PAGE_TILES, decode_pages(cx, cfg, warmup + steps + 1)) if paged else None
+    cache = tr.KVCache(c, B, cap, pages=pages)
     bits_all = fill_decode_cache(cx, c, cache, cfg, D.act, dense)
     ws = tr.workspace(c, tr.OP_LAYER_DECODE, B, 1)
     xo = torch.empty(B, d, dtype=D.act, device=cx.dev)
@@ -522,7 +540,18 @@ def bench_decode(cx, name, steps, warmup, attn_only=False):
     full = torch.full_like(r["t"]["mode"], 2)
     out["attn_all_full"] = bench_attn(cx, r, cfg, full, steps, "every head full (routed widths)")
     routed_cost = decode_cost(cfg, r["t"]["mode"].cpu().numpy(), r["bits"], r["eidx"])
+    cont_mib = r["cache"].nbytes / 2 ** 20
     del r
+    torch.cuda.empty_cache()
+    # the same steps over a paged cache (pages of PAGE_TILES tiles per width)
+    rp = run_decode_steps(cx, L, steps, warmup, paged=True)
+    out["paged"] = {"page_tiles": PAGE_TILES,
+                    "cache_mib": round(rp["cache"].nbytes / 2 ** 20, 1),
+                    "contiguous_cache_mib": round(cont_mib, 1),
+                    "tokens_per_s": round(B / (rp["ms"] * 1e-3), 1),
+                    "ms_per_step": round(rp["ms"], 4),
+                    "paged_over_contiguous_ms": round(rp["ms"] / out["ms_per_step"], 3)}
+    del rp
     torch.cuda.empty_cache()
     # the dense special case through the same kernels
     Ld = cx.gen.dense_variant(L)

@@ -178,6 +178,20 @@ typedef struct triroute_kv_cache {
   int64_t off_pool[4];    /* first tile of width bi */
   int64_t tile_bytes[4];  /* bytes per tile of width bi */
   int64_t total_bytes;
+  /* Paged caches only (page_tiles > 0, see triroute_kv_paged_cache_init):
+   * width bi's tiles and slot positions live in a pool of n_pages[bi] pages
+   * of page_tiles tiles (every kv head) and page_tiles * tile_slots
+   * positions; sequence s's pool of width bi is the list of pages
+   * page_table[(s * 4 + bi) * max_pages + j], j < alloc[s * 4 + bi]; the
+   * free pages of width bi are free_list[bi][0 .. free_top[bi]). */
+  int32_t page_tiles;     /* 0: contiguous pools of `capacity` slots per sequence and width */
+  int32_t max_pages;      /* page-table entries per (sequence, width) */
+  int32_t n_pages[4];
+  int64_t off_alloc;      /* int32 [n_seq][4] */
+  int64_t off_page_table; /* int32 [n_seq][4][max_pages] */
+  int64_t off_free_top;   /* int32 [4] */
+  int64_t off_free_list[4]; /* int32 [n_pages[bi]] */
+  int64_t off_pos_pool[4];  /* int32 [n_pages[bi]][page_tiles * tile_slots] */
 } triroute_kv_cache;
 
 /* Optional taps of the composite calls: where to also leave intermediates
@@ -228,6 +242,25 @@ int triroute_kv_cache_init(const triroute_cfg *cfg, triroute_kv_cache *cache, vo
                            size_t bytes, int n_seq, int capacity, triroute_stream_t stream);
 /* Empties sequence `seq` (its length and pool lengths) on `stream`; later
  * appends overwrite every bit of the slots they take. */
+/* Paged mixed-width cache (the layout above with page_tiles > 0): instead of
+ * every sequence reserving `capacity` slots in each of the four width pools,
+ * width bi has a pool of n_pages[bi] pages of page_tiles tiles shared by all
+ * sequences, and an append takes pages from it as a sequence's pool of that
+ * width grows (device-side, no host synchronisation).  capacity still
+ * bounds one sequence's length.  An append row whose pages cannot be had
+ * (the width's pool is exhausted, or several rows asked at once for the last
+ * pages) is dropped and flags TRIROUTE_CACHE_OVERFLOW; pages it already took
+ * for other widths stay with its sequence.  triroute_kv_reset_seq returns a
+ * sequence's pages.  Every other call takes paged and contiguous caches alike
+ * and computes the same results.  page_tiles >= 1; n_pages[bi] >= 0. */
+int triroute_kv_paged_cache_bytes(const triroute_cfg *cfg, int n_seq, int capacity,
+                                  int page_tiles, const int32_t n_pages[4], size_t *bytes);
+int triroute_kv_paged_cache_init(const triroute_cfg *cfg, triroute_kv_cache *cache, void *base,
+                                 size_t bytes, int n_seq, int capacity, int page_tiles,
+                                 const int32_t n_pages[4], triroute_stream_t stream);
+/* Free pages per width of a paged cache (synchronises the stream). */
+int triroute_kv_free_pages(const triroute_kv_cache *cache, int32_t free_pages[4],
+                           triroute_stream_t stream);
 int triroute_kv_reset_seq(const triroute_cfg *cfg, const triroute_kv_cache *cache, int seq,
                           triroute_stream_t stream);
 /* Synchronises `stream` and copies the cache status word to *status (host). */

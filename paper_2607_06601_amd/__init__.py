@@ -72,7 +72,10 @@ class KVCacheDesc(C.Structure):
                 ("off_status", C.c_int64), ("off_seq_len", C.c_int64),
                 ("off_pool_len", C.c_int64), ("off_pos", C.c_int64),
                 ("off_pool", C.c_int64 * 4), ("tile_bytes", C.c_int64 * 4),
-                ("total_bytes", C.c_int64)]
+                ("total_bytes", C.c_int64), ("page_tiles", C.c_int32), ("max_pages", C.c_int32),
+                ("n_pages", C.c_int32 * 4), ("off_alloc", C.c_int64),
+                ("off_page_table", C.c_int64), ("off_free_top", C.c_int64),
+                ("off_free_list", C.c_int64 * 4), ("off_pos_pool", C.c_int64 * 4)]
 
 
 class Taps(C.Structure):
@@ -114,6 +117,7 @@ EXPORTS = [
     "triroute_attn_prefill", "triroute_attn_decode", "triroute_oproj", "triroute_moe",
     "triroute_layer_prefill", "triroute_layer_decode", "triroute_layer_decode_noalloc",
     "triroute_stack_decode", "triroute_router_relaxed", "triroute_router_relaxed_backward",
+    "triroute_kv_paged_cache_bytes", "triroute_kv_paged_cache_init", "triroute_kv_free_pages",
 ]
 
 _lib = None
@@ -134,6 +138,9 @@ def lib():
             "triroute_workspace_bytes": [P, i32, i32, i32, C.POINTER(sz)],
             "triroute_kv_cache_bytes": [P, i32, i32, C.POINTER(sz)],
             "triroute_kv_cache_init": [P, P, P, sz, i32, i32, P],
+            "triroute_kv_paged_cache_bytes": [P, i32, i32, i32, P, C.POINTER(sz)],
+            "triroute_kv_paged_cache_init": [P, P, P, sz, i32, i32, i32, P, P],
+            "triroute_kv_free_pages": [P, P, P],
             "triroute_kv_reset_seq": [P, P, i32, P],
             "triroute_kv_status": [P, C.POINTER(C.c_int32), P],
             "triroute_kv_seq_len_ptr": [P],
@@ -214,18 +221,36 @@ def workspace(cfg: Cfg, op: int, B: int, T: int, device="cuda"):
 
 # ------------------------------------------------------------------ cache
 class KVCache:
-    """A device allocation laid out by triroute_kv_cache_init."""
+    """A device allocation laid out by triroute_kv_cache_init, or, with
+    ``pages=(page_tiles, [n_pages per width])``, by triroute_kv_paged_cache_init."""
 
-    def __init__(self, cfg: Cfg, n_seq: int, capacity: int, device="cuda", stream=None):
+    def __init__(self, cfg: Cfg, n_seq: int, capacity: int, device="cuda", stream=None,
+                 pages=None):
         n = C.c_size_t()
-        _check(lib().triroute_kv_cache_bytes(C.byref(cfg), n_seq, capacity, C.byref(n)))
         self.cfg = cfg
+        self.desc = KVCacheDesc()
+        if pages is None:
+            _check(lib().triroute_kv_cache_bytes(C.byref(cfg), n_seq, capacity, C.byref(n)))
+        else:
+            pt, npg = pages
+            self._np = (C.c_int32 * 4)(*npg)
+            _check(lib().triroute_kv_paged_cache_bytes(C.byref(cfg), n_seq, capacity, pt, self._np,
+                                                       C.byref(n)))
         self.nbytes = n.value
         self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
-        self.desc = KVCacheDesc()
-        _check(lib().triroute_kv_cache_init(C.byref(cfg), C.byref(self.desc),
-                                            self.buf.data_ptr(), self.nbytes, n_seq,
-                                            capacity, _stream(stream)))
+        if pages is None:
+            _check(lib().triroute_kv_cache_init(C.byref(cfg), C.byref(self.desc),
+                                                self.buf.data_ptr(), self.nbytes, n_seq,
+                                                capacity, _stream(stream)))
+        else:
+            _check(lib().triroute_kv_paged_cache_init(C.byref(cfg), C.byref(self.desc),
+                                                      self.buf.data_ptr(), self.nbytes, n_seq,
+                                                      capacity, pt, self._np, _stream(stream)))
+
+    def free_pages(self, stream=None):
+        out = (C.c_int32 * 4)()
+        _check(lib().triroute_kv_free_pages(self.ref, out, _stream(stream)))
+        return list(out)
 
     @property
     def ref(self):

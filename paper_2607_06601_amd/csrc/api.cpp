@@ -386,6 +386,61 @@ void layout_cache(const triroute_cfg &c, int n_seq, int capacity, triroute_kv_ca
   kc->total_bytes = off;
 }
 
+// Paged layout: the header words, per-sequence lengths, held-page counts and
+// page tables, the free stacks, then per width its positions and its tiles
+// (page p of width bi: tiles (p Hkv + g) page_tiles + i).
+void layout_paged(const triroute_cfg &c, int n_seq, int capacity, int PT, const int32_t np[4],
+                  triroute_kv_cache *kc) {
+  memset(kc, 0, sizeof *kc);
+  const int dh = c.head_dim, G = c.kv_group, ab = act_bytes(c);
+  const int TS = 4096 / dh;
+  kc->n_seq = n_seq;
+  kc->capacity = capacity;
+  kc->tile_slots = TS;
+  kc->n_tiles = (capacity + TS - 1) / TS;
+  kc->page_tiles = PT;
+  kc->max_pages = (kc->n_tiles + PT - 1) / PT;
+  size_t off = 0;
+  kc->off_status = off;
+  off += 256;
+  kc->off_seq_len = off;
+  off += align256(size_t(n_seq) * 4);
+  kc->off_pool_len = off;
+  off += align256(size_t(n_seq) * 16);
+  kc->off_alloc = off;
+  off += align256(size_t(n_seq) * 16);
+  kc->off_page_table = off;
+  off += align256(size_t(n_seq) * 4 * kc->max_pages * 4);
+  kc->off_free_top = off;
+  off += 256;
+  for (int bi = 0; bi < 4; ++bi) {
+    kc->n_pages[bi] = np[bi];
+    kc->off_free_list[bi] = off;
+    off += align256(size_t(np[bi]) * 4);
+    kc->off_pos_pool[bi] = off;
+    off += align256(size_t(np[bi]) * PT * TS * 4);
+  }
+  kc->off_pos = kc->off_pos_pool[0];
+  for (int bi = 0; bi < 4; ++bi) {
+    const int bp = tr::pool_bits(bi, ab);
+    kc->tile_bytes[bi] = align256(size_t(1024) * bp + (bi < 3 ? size_t(2) * TS * (dh / G) * 4 : 0));
+    kc->off_pool[bi] = off;
+    off += size_t(np[bi]) * c.n_kv_heads * PT * kc->tile_bytes[bi];
+  }
+  kc->total_bytes = off;
+}
+
+int check_paged_args(int n_seq, int capacity, int PT, const int32_t *np) {
+  REQUIRE(n_seq >= 1 && capacity >= 1, TRIROUTE_E_INVALID, "n_seq and capacity must be >= 1");
+  REQUIRE(int64_t(capacity) <= (int64_t(1) << 28), TRIROUTE_E_UNSUPPORTED, "capacity too large");
+  REQUIRE(PT >= 1 && PT <= (1 << 16), TRIROUTE_E_INVALID, "page_tiles %d outside [1, 65536]", PT);
+  REQUIRE(np, TRIROUTE_E_INVALID, "n_pages is NULL");
+  for (int bi = 0; bi < 4; ++bi)
+    REQUIRE(np[bi] >= 0 && np[bi] <= (1 << 28), TRIROUTE_E_INVALID,
+            "n_pages[%d] = %d outside [0, 2^28]", bi, np[bi]);
+  return TRIROUTE_OK;
+}
+
 hipError_t run_attn_prefill(const triroute_cfg &c, const triroute_kv_cache &kc, int B, int T,
                             const int32_t *seq_ids, const void *q, const triroute_compaction &cmp,
                             void *o, hipStream_t st) {
@@ -426,6 +481,19 @@ CacheView make_view(const triroute_cfg &c, const triroute_kv_cache &k) {
   for (int i = 0; i < 4; ++i) {
     v.off_pool[i] = k.off_pool[i];
     v.tile_bytes[i] = k.tile_bytes[i];
+  }
+  v.PT = k.page_tiles;
+  v.max_pages = k.max_pages;
+  v.page_table = v.alloc = v.free_top = nullptr;
+  for (int i = 0; i < 4; ++i) v.free_list[i] = v.pos_pool[i] = nullptr;
+  if (k.page_tiles > 0) {
+    v.page_table = (int32_t *)(v.base + k.off_page_table);
+    v.alloc = (int32_t *)(v.base + k.off_alloc);
+    v.free_top = (int32_t *)(v.base + k.off_free_top);
+    for (int i = 0; i < 4; ++i) {
+      v.free_list[i] = (int32_t *)(v.base + k.off_free_list[i]);
+      v.pos_pool[i] = (int32_t *)(v.base + k.off_pos_pool[i]);
+    }
   }
   return v;
 }
@@ -490,14 +558,63 @@ int triroute_kv_cache_init(const triroute_cfg *cfg, triroute_kv_cache *cache, vo
   return TRIROUTE_OK;
 }
 
+int triroute_kv_paged_cache_bytes(const triroute_cfg *cfg, int n_seq, int capacity,
+                                  int page_tiles, const int32_t n_pages[4], size_t *bytes) {
+  TRY(check_cfg(cfg));
+  REQUIRE(bytes, TRIROUTE_E_INVALID, "bytes is NULL");
+  TRY(check_paged_args(n_seq, capacity, page_tiles, n_pages));
+  triroute_kv_cache kc;
+  layout_paged(*cfg, n_seq, capacity, page_tiles, n_pages, &kc);
+  *bytes = kc.total_bytes;
+  return TRIROUTE_OK;
+}
+
+int triroute_kv_paged_cache_init(const triroute_cfg *cfg, triroute_kv_cache *cache, void *base,
+                                 size_t bytes, int n_seq, int capacity, int page_tiles,
+                                 const int32_t n_pages[4], triroute_stream_t stream) {
+  TRY(check_cfg(cfg));
+  REQUIRE(cache && base, TRIROUTE_E_INVALID, "cache or base is NULL");
+  REQUIRE((uintptr_t(base) & 255) == 0, TRIROUTE_E_INVALID, "cache base must be 256-byte aligned");
+  TRY(check_paged_args(n_seq, capacity, page_tiles, n_pages));
+  triroute_kv_cache kc;
+  layout_paged(*cfg, n_seq, capacity, page_tiles, n_pages, &kc);
+  REQUIRE(bytes >= size_t(kc.total_bytes), TRIROUTE_E_CAPACITY,
+          "cache allocation %zu bytes < %lld needed", bytes, (long long)kc.total_bytes);
+  kc.base = base;
+  hipStream_t st = (hipStream_t)stream;
+  // everything is cleared, as for the contiguous layout: the attention
+  // kernels read whole tiles, and the slots past a pool's length must hold
+  // finite values (their weights are zero); then the free stacks get every
+  // page.  A page returned by a reset keeps finite values from its appends.
+  CHECK_HIP(tr::launch_fill_u32(base, kc.total_bytes / 4, 0u, st), "cache clear");
+  CHECK_HIP(tr::launch_kv_paged_init(tr::make_view(*cfg, kc), kc.n_pages, st), "page stacks");
+  *cache = kc;
+  return TRIROUTE_OK;
+}
+
+int triroute_kv_free_pages(const triroute_kv_cache *cache, int32_t free_pages[4],
+                           triroute_stream_t stream) {
+  REQUIRE(cache && cache->base && free_pages, TRIROUTE_E_INVALID, "NULL argument");
+  REQUIRE(cache->page_tiles > 0, TRIROUTE_E_INVALID, "the cache is not paged");
+  CHECK_HIP(hipStreamSynchronize((hipStream_t)stream), "stream sync");
+  CHECK_HIP(hipMemcpy(free_pages, (uint8_t *)cache->base + cache->off_free_top, 16,
+                      hipMemcpyDeviceToHost),
+            "free page read");
+  return TRIROUTE_OK;
+}
+
 int triroute_kv_reset_seq(const triroute_cfg *cfg, const triroute_kv_cache *cache, int seq,
                           triroute_stream_t stream) {
   TRY(check_cfg(cfg));
   REQUIRE(cache && cache->base, TRIROUTE_E_INVALID, "cache is NULL");
   REQUIRE(seq >= 0 && seq < cache->n_seq, TRIROUTE_E_INVALID, "seq %d out of range", seq);
+  hipStream_t st = (hipStream_t)stream;
+  if (cache->page_tiles > 0) {  // its pages go back to the free stacks
+    CHECK_HIP(tr::launch_kv_paged_reset(tr::make_view(*cfg, *cache), seq, st), "reset");
+    return TRIROUTE_OK;
+  }
   // Appends overwrite every bit a slot owns, so emptying a sequence only
   // needs its lengths cleared.
-  hipStream_t st = (hipStream_t)stream;
   uint8_t *b = (uint8_t *)cache->base;
   CHECK_HIP(tr::launch_fill_u32(b + cache->off_seq_len + 4 * size_t(seq), 1, 0u, st), "reset");
   CHECK_HIP(tr::launch_fill_u32(b + cache->off_pool_len + 16 * size_t(seq), 4, 0u, st), "reset");

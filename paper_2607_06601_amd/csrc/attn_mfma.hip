@@ -436,13 +436,13 @@ __device__ __forceinline__ void process_tile(SoftState<DH> &st,
 // the whole wave: each round probes 64 evenly spaced entries and narrows the
 // range 64-fold, so a 32k-entry pool takes two rounds of parallel loads.
 // Must be called by all 64 lanes with wave-uniform arguments.
-__device__ __forceinline__ int lower_bound_pos(const int32_t *pos, int len, int p) {
+__device__ __forceinline__ int lower_bound_pos(const CacheView &cv, int s, int bi, int len, int p) {
   const int lane = threadIdx.x & 63;
   int lo = 0, hi = len;  // the answer lies in [lo, hi]
   while (hi - lo > 64) {
     const int span = hi - lo;
     const int idx = lo + int(int64_t(span) * (lane + 1) / 64) - 1;
-    const uint64_t below = __ballot(pos[idx] < p);
+    const uint64_t below = __ballot(cv.pos_at(s, bi, idx) < p);
     const int c = __popcll(below);  // probes 0 .. c-1 lie below p
     const int nlo = c > 0 ? lo + int(int64_t(span) * c / 64) : lo;
     const int nhi = c < 64 ? lo + int(int64_t(span) * (c + 1) / 64) - 1 : hi;
@@ -450,7 +450,7 @@ __device__ __forceinline__ int lower_bound_pos(const int32_t *pos, int len, int 
     hi = nhi;
   }
   const int idx = lo + lane;
-  const uint64_t below = __ballot(idx < hi && pos[idx] < p);
+  const uint64_t below = __ballot(idx < hi && cv.pos_at(s, bi, idx) < p);
   return lo + __popcll(below);
 }
 
@@ -675,7 +675,7 @@ __device__ __forceinline__ void stream_tiles(const CacheView &cv, int s, int g, 
       }
       if constexpr (POS) {
         if ((threadIdx.x & 63) < SG::TS / 4)
-          dma16(cv.pos_of(s, pb) + pt * SG::TS + 4 * (threadIdx.x & 63), rbase + pos + tb);
+          dma16(cv.pos_tile(s, pb, pt) + 4 * (threadIdx.x & 63), rbase + pos + tb);
       }
       phead = pos + sz;
       issued += ((tb + 1023) >> 10) + (POS ? 1 : 0);
@@ -1002,7 +1002,7 @@ __global__ __launch_bounds__(512, 1) void attn_decode_kernel(DecodeArgs a) {
     const int P = cv.seq_len[s] - 1;
     const int len = cv.pool_len[s * 4 + bi];
     // the window start matters only to local heads
-    const int lb = any_local ? lower_bound_pos(cv.pos_of(s, bi), len, P - a.w + 1) : 0;
+    const int lb = any_local ? lower_bound_pos(cv, s, bi, len, P - a.w + 1) : 0;
     if (lane == 0) {
       bounds[bi][0] = lb;
       bounds[bi][1] = len;
@@ -1234,7 +1234,7 @@ __device__ __forceinline__ void lower_bounds8(const CacheView &cv, int s, const 
     for (int k = 0; k < 8; ++k) {
       const int span = hi[k] - lo[k];
       v[k] = 0;
-      if (span > 64) v[k] = cv.pos_of(s, k & 3)[lo[k] + int(int64_t(span) * (lane + 1) / 64) - 1];
+      if (span > 64) v[k] = cv.pos_at(s, k & 3, lo[k] + int(int64_t(span) * (lane + 1) / 64) - 1);
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
@@ -1252,7 +1252,7 @@ __device__ __forceinline__ void lower_bounds8(const CacheView &cv, int s, const 
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
     const int idx = lo[k] + lane;
-    v[k] = idx < hi[k] ? cv.pos_of(s, k & 3)[idx] : INT_MAX;
+    v[k] = idx < hi[k] ? cv.pos_at(s, k & 3, idx) : INT_MAX;
   }
 #pragma unroll
   for (int k = 0; k < 8; ++k) res[k] = lo[k] + __popcll(__ballot(v[k] < key[k]));
@@ -1601,7 +1601,7 @@ __device__ __forceinline__ void stream_tiles_block(const CacheView &cv, int s, i
       }
       if (!ok) break;
       const int pt = kp + (pb == 0 ? d0 : pb == 1 ? d1 : pb == 2 ? d2 : d3);
-      const int32_t *ps = cv.pos_of(s, pb) + pt * SG::TS;
+      const int32_t *ps = cv.pos_tile(s, pb, pt);
       switch (pb) {  // compile-time pool: no run-time indexing of the cache view's arrays
         case 0: issue_tile_split<DH, G, 0, NW>(cv.tile(s, 0, g, pt), ps, rbase + pos, wave); break;
         case 1: issue_tile_split<DH, G, 1, NW>(cv.tile(s, 1, g, pt), ps, rbase + pos, wave); break;

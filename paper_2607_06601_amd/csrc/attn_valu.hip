@@ -10,11 +10,10 @@ namespace tr {
 // First slot of pool (s, bi) whose position is >= p (positions ascend).
 __device__ __forceinline__ int pool_lower_bound(const CacheView &cv, int s, int bi, int len,
                                                 int p) {
-  const int32_t *pos = cv.pos_of(s, bi);
   int lo = 0, hi = len;
   while (lo < hi) {
     const int mid = (lo + hi) >> 1;
-    if (pos[mid] < p)
+    if (cv.pos_at(s, bi, mid) < p)
       lo = mid + 1;
     else
       hi = mid;

@@ -215,12 +215,28 @@ struct CacheView {
   int n_seq, capacity, TS, n_tiles;
   int Hkv, dh, G, act_bytes;
   int64_t off_pool[4], tile_bytes[4];
+  // paged caches (PT > 0): pool (s, bi) is a list of pages of PT tiles (all
+  // kv heads) taken from width bi's page pool; page j of it is
+  // page_table[(s * 4 + bi) * max_pages + j]
+  int PT, max_pages;
+  int32_t *page_table, *alloc, *free_top;
+  int32_t *free_list[4], *pos_pool[4];
 
-  // positions of pool (s, bi): one int32 per slot, n_tiles * TS slots per pool
-  __device__ __forceinline__ int32_t *pos_of(int s, int bi) const {
-    return pos + (int64_t(s) * 4 + bi) * (int64_t(n_tiles) * TS);
+  __device__ __forceinline__ int page(int s, int bi, int j) const {
+    return page_table[(int64_t(s) * 4 + bi) * max_pages + j];
+  }
+  // positions of the TS slots of tile t of pool (s, bi) (one int32 per slot)
+  __device__ __forceinline__ int32_t *pos_tile(int s, int bi, int t) const {
+    if (PT) return pos_pool[bi] + (int64_t(page(s, bi, t / PT)) * PT + t % PT) * TS;
+    return pos + ((int64_t(s) * 4 + bi) * n_tiles + t) * TS;
+  }
+  __device__ __forceinline__ int32_t &pos_at(int s, int bi, int slot) const {
+    return pos_tile(s, bi, slot / TS)[slot % TS];
   }
   __device__ __forceinline__ uint8_t *tile(int s, int bi, int g, int t) const {
+    if (PT)
+      return base + off_pool[bi] +
+             ((int64_t(page(s, bi, t / PT)) * Hkv + g) * PT + t % PT) * tile_bytes[bi];
     return base + off_pool[bi] + ((int64_t(s) * Hkv + g) * n_tiles + t) * tile_bytes[bi];
   }
   __device__ __forceinline__ int bits(int bi) const { return pool_bits(bi, act_bytes); }

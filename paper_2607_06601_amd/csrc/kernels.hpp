@@ -64,6 +64,9 @@ hipError_t launch_fill_u32(void *p, int64_t n_words, uint32_t v, hipStream_t st)
 struct KvWs {
   int32_t *old_len;  // [B][4]
 };
+// paged caches: fill the free stacks with every page; return a sequence's pages
+hipError_t launch_kv_paged_init(const CacheView &cv, const int32_t n_pages[4], hipStream_t st);
+hipError_t launch_kv_paged_reset(const CacheView &cv, int seq, hipStream_t st);
 hipError_t launch_kv_append(const triroute_cfg &cfg, const CacheView &cv, int B, int T,
                             const int32_t *seq_ids, const void *k, const void *v,
                             const uint8_t *bit, const KvWs &ws, hipStream_t st);

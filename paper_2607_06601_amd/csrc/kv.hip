@@ -51,6 +51,48 @@ __global__ __launch_bounds__(1024) void kv_slots_kernel(CacheView cv, int T,
   int run[4];
 #pragma unroll
   for (int bi = 0; bi < 4; ++bi) run[bi] = cv.pool_len[s * 4 + bi];
+  if (cv.PT) {
+    // paged: count the row's tokens per width, then take the pages the
+    // pools grow into from the free stacks (thread bi for width bi)
+    __shared__ int cnt_s[4], fail_s;
+    if (tid < 4) cnt_s[tid] = 0;
+    if (tid == 0) fail_s = 0;
+    __syncthreads();
+    for (int t0 = 0; t0 < T; t0 += 64 * NW) {
+      const int t = t0 + tid;
+      const int bi = t < T ? int(bit[int64_t(b) * T + t]) : -1;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint64_t bq = __ballot(bi == q);
+        if (lane == 0 && bq) atomicAdd(&cnt_s[q], __popcll(bq));  // a count: order does not matter
+      }
+    }
+    __syncthreads();
+    if (tid < 4) {
+      const int bi = tid, per = cv.PT * cv.TS;
+      const int need = (run[bi] + cnt_s[bi] + per - 1) / per;
+      int32_t *held = cv.alloc + s * 4 + bi;
+      const int have = *held;
+      if (need > have) {
+        const int k = need - have;
+        const int top = atomicSub(cv.free_top + bi, k);
+        if (need > cv.max_pages || top - k < 0) {
+          atomicAdd(cv.free_top + bi, k);  // give the claim back
+          atomicOr(&fail_s, 1);
+        } else {
+          for (int q = 0; q < k; ++q)
+            cv.page_table[(int64_t(s) * 4 + bi) * cv.max_pages + have + q] = cv.free_list[bi][top - k + q];
+          *held = need;
+        }
+      }
+    }
+    __syncthreads();
+    if (fail_s) {
+      if (tid == 0) atomicOr(cv.status, int(TRIROUTE_CACHE_OVERFLOW));
+      if (tid < 4) old_len[b * 4 + tid] = -1;
+      return;
+    }
+  }
   if (tid < 4) old_len[b * 4 + tid] = run[tid];
   for (int t0 = 0; t0 < T; t0 += 64 * NW) {
     const int t = t0 + tid;
@@ -63,7 +105,7 @@ __global__ __launch_bounds__(1024) void kv_slots_kernel(CacheView cv, int T,
     if (bi >= 0) {
       int slot = run[bi] + __popcll(bal[bi] & lanemask_lt());
       for (int ww = 0; ww < w; ++ww) slot += wc[bi][ww];
-      cv.pos_of(s, bi)[slot] = len0 + t;
+      cv.pos_at(s, bi, slot) = len0 + t;
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q)
@@ -244,7 +286,7 @@ __device__ __forceinline__ void kv_step(const CacheView &cv, int s, int bi, int 
   uint8_t *tp = cv.tile(s, bi, g, tile);
   const int st = sl % TS;
   if (live) {
-    const int t = cv.pos_of(s, bi)[sl] - len0;  // the token at the slot's recorded position
+    const int t = cv.pos_at(s, bi, sl) - len0;  // the token at the slot's recorded position
     const int64_t rowoff = ((row0 + t) * Hkv + g) * DH;
 #pragma unroll
     for (int it = 0; it < NIT; ++it) {
@@ -482,8 +524,49 @@ __global__ void kv_export_kernel(CacheView cv, int seq, int bi, int slot0, int c
       ((uint32_t *)vout)[idx] = ve;
     }
     if (pos_out && c == 0 && g == 0)
-      pos_out[r] = live ? cv.pos_of(seq, bi)[slot] : 0;
+      pos_out[r] = live ? cv.pos_at(seq, bi, slot) : 0;
   }
+}
+
+__global__ __launch_bounds__(256) void kv_paged_init_kernel(CacheView cv, int n0, int n1, int n2,
+                                                             int n3) {
+  const int np[4] = {n0, n1, n2, n3};
+  const int bi = blockIdx.y;
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < np[bi]; i += gridDim.x * 256)
+    cv.free_list[bi][i] = i;
+  if (blockIdx.x == 0 && threadIdx.x == 0) cv.free_top[bi] = np[bi];
+}
+
+hipError_t launch_kv_paged_init(const CacheView &cv, const int32_t n_pages[4], hipStream_t st) {
+  int mx = 1;
+  for (int bi = 0; bi < 4; ++bi) mx = n_pages[bi] > mx ? n_pages[bi] : mx;
+  const int bx = (mx + 255) / 256 < 1024 ? (mx + 255) / 256 : 1024;
+  kv_paged_init_kernel<<<dim3(bx, 4), 256, 0, st>>>(cv, n_pages[0], n_pages[1], n_pages[2],
+                                                    n_pages[3]);
+  return hipGetLastError();
+}
+
+// Return sequence seq's pages to the free stacks and empty it (one wave per
+// width: lane q pushes pages q, q + 64, ...).
+__global__ __launch_bounds__(256) void kv_paged_reset_kernel(CacheView cv, int seq) {
+  const int bi = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  int32_t *held = cv.alloc + seq * 4 + bi;
+  const int k = *held;
+  int top = 0;
+  if (lane == 0 && k > 0) top = atomicAdd(cv.free_top + bi, k);
+  top = __shfl(top, 0, 64);
+  for (int q = lane; q < k; q += 64)
+    cv.free_list[bi][top + q] = cv.page_table[(int64_t(seq) * 4 + bi) * cv.max_pages + q];
+  if (lane == 0) {
+    *held = 0;
+    cv.pool_len[seq * 4 + bi] = 0;
+    if (bi == 0) cv.seq_len[seq] = 0;
+  }
+}
+
+hipError_t launch_kv_paged_reset(const CacheView &cv, int seq, hipStream_t st) {
+  kv_paged_reset_kernel<<<dim3(1), 256, 0, st>>>(cv, seq);
+  return hipGetLastError();
 }
 
 hipError_t launch_kv_append(const triroute_cfg &cfg, const CacheView &cv, int B, int T,

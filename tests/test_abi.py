@@ -158,3 +158,26 @@ def test_relaxed_backward_rejects_bad_arguments():
     assert call(ws_bytes=1024) == -3
     assert tr.workspace_bytes(c, tr.OP_ROUTER_RELAXED_BACKWARD, 8, 2048) > \
         tr.workspace_bytes(c, tr.OP_ROUTER_RELAXED, 8, 2048)
+
+
+def test_paged_cache_sizes_and_rejections():
+    """A paged cache sized for the pages the workload's widths need is far
+    smaller than one that reserves the capacity in every width pool; bad
+    page arguments are refused on the host."""
+    lib = tr.lib()
+    c = tr.make_cfg(2048, 16, 4, 128, 1024, 16, 2, 5632, 64, "bf16")
+    n = C.c_size_t()
+    pages = (C.c_int32 * 4)(740, 215, 4, 110)  # 32 sequences of 32768 slots at 70/20/0/10 %
+    assert lib.triroute_kv_paged_cache_bytes(C.byref(c), 32, 32784, 32, pages, C.byref(n)) == 0
+    paged = n.value
+    assert lib.triroute_kv_cache_bytes(C.byref(c), 32, 32784, C.byref(n)) == 0
+    assert paged < n.value / 6
+    bad = (C.c_int32 * 4)(1, -1, 1, 1)
+    assert lib.triroute_kv_paged_cache_bytes(C.byref(c), 32, 32784, 32, bad, C.byref(n)) == -1
+    assert lib.triroute_kv_paged_cache_bytes(C.byref(c), 32, 32784, 0, pages, C.byref(n)) == -1
+    assert lib.triroute_kv_paged_cache_bytes(C.byref(c), 32, 32784, 32, None, C.byref(n)) == -1
+    desc = tr.KVCacheDesc()
+    desc.base = 1 << 40
+    out = (C.c_int32 * 4)()
+    assert lib.triroute_kv_free_pages(C.byref(desc), out, None) == -1  # not paged
+    assert b"not paged" in lib.triroute_last_error()

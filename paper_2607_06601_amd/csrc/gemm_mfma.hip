@@ -822,24 +822,22 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
   constexpr int NF = MI + NI;             // fragment reads per K slice
   constexpr int NM = MI * NI;             // MFMAs per K slice
   static_assert(STAGE % (1024 * NW) == 0 && (TN % 64 == 0 || P::DIRECT_W4), "whole transfers, 64-column slices");
-  // slice 1 schedule: 16 MFMAs, the barrier, then a transfer every DMA_GAP
-  // MFMAs and the next slice's reads from MFMA RS on
-  // K step schedule.  Long steps (NM = 64: 128 MFMAs per wave) take one
-  // barrier, 16 MFMAs into slice 1: it frees the buffer of stage kt and
-  // publishes stage kt + 1; the transfers of stage kt + 2 follow one every
-  // GAP1 MFMAs.  Shorter steps cannot cover the transfer latency that way
-  // and take two: the first, after MFMA B1J of slice 0 (its reads of set 1
-  // are in), frees the buffer; the transfers go out one every GAP MFMAs
-  // until MFMA RS of slice 1, where the second barrier publishes stage
-  // kt + 1 (at most this step's IPW transfers still out) for the reads of
-  // set 0, so stage kt + 2 has from slice 0 of step kt to slice 1 of kt + 1.
-  constexpr bool TWO = NM < 64;
-  constexpr int RS = NM - NF < 32 ? NM - NF : 32;
-  constexpr int GAP1 = (NM - 17) / (IPW - 1) < 3 ? (NM - 17) / (IPW - 1) : 3;
+  // K step schedule, two barriers: the first, after MFMA B1J of slice 0
+  // (every wave's reads of set 1, the last reads of stage kt, are in), frees
+  // the buffer of stage kt; the transfers of stage kt + 2 go out one every GAP
+  // MFMAs from there until MFMA RS of slice 1, where the second barrier
+  // publishes stage kt + 1 (at most this step's IPW transfers still out) for
+  // the reads of set 0.  A transfer thus has from slice 0 of step kt to
+  // slice 1 of step kt + 1 to land.  (One barrier 16 MFMAs into slice 1, with
+  // the transfers after it, left the last ones under 90 MFMAs to land, and a
+  // cache-missing transfer stalled the wave at that barrier; spacing the
+  // transfers closer than 5 MFMAs slowed the MFMA issue.)
+  constexpr int RS = NM - NF < 48 ? NM - NF : 48;
   constexpr int B1J = NF + 4;
   constexpr int NSLOT = (NM - 1 - B1J) + RS;  // slice 0 after B1J, then slice 1 before RS
-  constexpr int GAP = NSLOT / IPW < 4 ? NSLOT / IPW : 4;
-  static_assert(B1J < NM && RS >= 16 && (TWO ? GAP >= 1 : GAP1 >= 1), "room for the reads and transfers");
+  constexpr int GAP = NSLOT / IPW < 5 ? NSLOT / IPW : 5;
+  static_assert(B1J < NM && RS >= 16 && RS + NF <= NM && GAP >= 1 && GAP * (IPW - 1) < NSLOT,
+                "room for the reads and transfers");
   static_assert(P::DIRECT_W4, "results are written from the accumulators");
   __shared__ __align__(1024) uint8_t smem[2 * STAGE];
   // Persistent: block b takes tiles b, b + gridDim.x, ... (one block per CU).
@@ -969,7 +967,7 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
         }
       };
       // slice 0: MFMAs on set 0, the reads of slice 1 into set 1 after the
-      // first NF of them (TWO: the first barrier after MFMA B1J)
+      // first NF of them, the first barrier after MFMA B1J
 #pragma unroll
       for (int j = 0; j < NM; ++j) {
         if constexpr (FIRST)
@@ -977,35 +975,22 @@ __global__ __launch_bounds__(256, 1) void gemm_w4_kernel(P p, int K, int ny) {
         else
           mma(0, j);
         if (j < NF) read_piece(1, buf, j);
-        if constexpr (TWO) {
-          if (j == B1J) __syncthreads();  // every wave's reads of stage kt are in
-          if (j > B1J) dma_slot(j - B1J - 1);
-        }
+        if (j == B1J) __syncthreads();  // every wave's reads of stage kt are in
+        if (j > B1J) dma_slot(j - B1J - 1);
       }
       // slice 1: MFMAs on set 1, the barrier, then the reads of stage
       // kt + 1, slice 0, into set 0 (unused in the last step: the registers
       // are free while the results are written, and read again after)
 #pragma unroll
       for (int j = 0; j < NM; ++j) {
-        if constexpr (TWO) {
-          if (j == RS) {
-            // stage kt + 1 has landed: loads complete in issue order and only
-            // stage kt + 2 may be out (stores in between do not matter)
-            wait_vm<IPW>();
-            __syncthreads();  // ... in every wave's part
-          }
-        } else {
-          if (j == 16) {
-            wait_vm<0>();
-            __syncthreads();  // buffer buf is free, stage kt + 1 is in
-          }
+        if (j == RS) {
+          // stage kt + 1 has landed: loads complete in issue order and only
+          // stage kt + 2 may be out (stores in between do not matter)
+          wait_vm<IPW>();
+          __syncthreads();  // ... in every wave's part
         }
         mma(1, j);
-        if constexpr (TWO) {
-          if (j < RS) dma_slot(NM - 1 - B1J + j);
-        } else {
-          if (j >= 16 && (j - 16) % GAP1 == 0 && (j - 16) / GAP1 < IPW) dma_slot((j - 16) / GAP1 * GAP);
-        }
+        if (j < RS) dma_slot(NM - 1 - B1J + j);
         if (j >= RS && j - RS < NF) read_piece(0, buf ^ 1, j - RS);
       }
     };

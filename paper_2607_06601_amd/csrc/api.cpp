@@ -914,7 +914,7 @@ static int moe_impl(const triroute_cfg *cfg, int n_tok, const void *xt, const tr
                     const triroute_moe_w *w, const int32_t *eidx, const float *egate,
                     const triroute_compaction *cmp, void *x_out, Carve &cv, hipStream_t st) {
   MoeWs m = carve_moe(cv, *cfg, n_tok);
-  CHECK_HIP(tr::launch_moe_norm_rows(*cfg, n_tok, xt, dw->g2, *cmp, m.n2, m.slot_of, st),
+  CHECK_HIP(tr::launch_moe_norm_rows(*cfg, n_tok, xt, dw->g2, *cmp, eidx, m.n2, m.slot_of, st),
             "moe_norm_rows launch");
   CHECK_HIP(tr::launch_moe_gemms(*cfg, n_tok, m.n2, *w, *cmp, m.Hm, m.Y, st), "moe gemm launch");
   CHECK_HIP(tr::launch_moe_combine(*cfg, n_tok, xt, m.Y, m.slot_of, eidx, egate, x_out, st),

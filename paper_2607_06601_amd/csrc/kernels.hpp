@@ -111,8 +111,8 @@ hipError_t launch_attn_mfma_prefill(const triroute_cfg &cfg, const CacheView &cv
                                     const triroute_compaction &c, void *o, hipStream_t st);
 // misc.hip
 hipError_t launch_moe_norm_rows(const triroute_cfg &cfg, int N, const void *x, const void *g,
-                                const triroute_compaction &c, void *out, int32_t *slot_of,
-                                hipStream_t st);
+                                const triroute_compaction &c, const int32_t *eidx, void *out,
+                                int32_t *slot_of, hipStream_t st);
 // Few assignments (decode, bf16): the down GEMM splits K in two halves, each
 // written to its own plane of Y (N k rows apart); the combine adds the planes
 // in order.  Returns the number of planes.

@@ -3,41 +3,48 @@
 // Slots are summed in slot order (deterministic); a token whose every slot is
 // the null expert gets x_out = xt exactly.  The expert GEMMs take n2 and give
 // Y in list order (one row per entry of the expert lists, lists back to
-// back), so the normalisation writes the rows of each list entry and records
-// where each assignment's row went.
+// back), so the normalisation first records where each assignment's row
+// goes and then writes every token's normalised row to those rows.
 #include "kernels.hpp"
 
 namespace tr {
 
-// One wave per list entry pos (8 consecutive elements per lane access,
-// d % 64 == 0): token a / k of assignment a = rows[pos], normalised, to row
-// pos; slot_of[a] = pos.  Entries past the lists' total do nothing.  The
+// List row of every real assignment: slot_of[rows[pos]] = pos for each
+// entry pos of the expert lists (one thread per entry).
+__global__ __launch_bounds__(256) void moe_slot_of_kernel(const int32_t *__restrict__ rows,
+                                                          const int32_t *__restrict__ off, int E,
+                                                          int Nk, int32_t *__restrict__ slot_of) {
+  const int pos = blockIdx.x * 256 + threadIdx.x;
+  if (pos < Nk && pos < off[E]) slot_of[rows[pos]] = pos;  // off[E]: end of the last list
+}
+
+// One wave per token i (8 consecutive elements per lane access,
+// d % 64 == 0): the row is read once (kept in registers when
+// d <= 512 RR, read again for the products otherwise), normalised, and
+// written to the list row of each of the token's real assignments.  The
 // norm is evaluated in fp64 (sum of squares, scale, products) and rounded
 // once to the activation dtype, so n2 is the correctly rounded value of the
 // exact norm: a last-place difference in n2 would otherwise move the expert
 // output by far more than its own size.
-template <typename T>
-__global__ __launch_bounds__(256) void moe_norm_rows_kernel(
-    const T *__restrict__ x, const T *__restrict__ g, const int32_t *__restrict__ rows,
-    const int32_t *__restrict__ off, int E, int k, int Nk, T *__restrict__ out,
-    int32_t *__restrict__ slot_of, int d, float eps) {
-  const int pos = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
+template <typename T, int RR>
+__global__ __launch_bounds__(256) void moe_norm_tok_kernel(
+    const T *__restrict__ x, const T *__restrict__ g, const int32_t *__restrict__ eidx,
+    const int32_t *__restrict__ slot_of, int N, int k, T *__restrict__ out, int d, float eps) {
+  const int i = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
   const int lane = threadIdx.x & 63;
-  if (pos >= Nk || pos >= off[E]) return;  // off[E]: end of the last list
-  const int a = rows[pos];
-  const T *xr = x + int64_t(a / k) * d;
-  // rows of up to 1024 elements stay in registers between the two passes
-  constexpr int RR = 2;
-  float v[RR][8];
+  if (i >= N) return;
+  const T *xr = x + int64_t(i) * d;
+  const int32_t *ei = eidx + int64_t(i) * k, *so = slot_of + int64_t(i) * k;
+  float v[RR > 0 ? RR : 1][8];
   double ss = 0.0;
-  if (d <= 512 * RR) {
+  if constexpr (RR > 0) {
 #pragma unroll
     for (int q = 0; q < RR; ++q) {
       const int c = lane * 8 + 512 * q;
       if (c < d) {
         load8(xr + c, v[q]);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) ss = fma(double(v[q][i]), double(v[q][i]), ss);
+        for (int j = 0; j < 8; ++j) ss = fma(double(v[q][j]), double(v[q][j]), ss);
       }
     }
   } else {
@@ -45,37 +52,34 @@ __global__ __launch_bounds__(256) void moe_norm_rows_kernel(
       float w[8];
       load8(xr + c, w);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) ss = fma(double(w[i]), double(w[i]), ss);
+      for (int j = 0; j < 8; ++j) ss = fma(double(w[j]), double(w[j]), ss);
     }
   }
   ss = wave_sum(ss);
   const double r = 1.0 / sqrt(ss / double(d) + double(eps));
-  T *orow = out + int64_t(pos) * d;
-  if (d <= 512 * RR) {
+  // products of the 8 elements at c, rounded, to every real assignment's row
+  auto emit = [&](int c, const float *w) {
+    float gv[8];
+    double o[8];
+    load8(g + c, gv);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[j] = (double(w[j]) * r) * double(gv[j]);
+    for (int s = 0; s < k; ++s)
+      if (ei[s] != 0) store8(out + int64_t(so[s]) * d + c, o);
+  };
+  if constexpr (RR > 0) {
 #pragma unroll
     for (int q = 0; q < RR; ++q) {
       const int c = lane * 8 + 512 * q;
-      if (c < d) {
-        float gv[8];
-        double o[8];
-        load8(g + c, gv);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) o[i] = (double(v[q][i]) * r) * double(gv[i]);
-        store8(orow + c, o);
-      }
+      if (c < d) emit(c, v[q]);
     }
   } else {
     for (int c = lane * 8; c < d; c += 512) {
-      float w[8], gv[8];
-      double o[8];
+      float w[8];
       load8(xr + c, w);
-      load8(g + c, gv);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o[i] = (double(w[i]) * r) * double(gv[i]);
-      store8(orow + c, o);
+      emit(c, w);
     }
   }
-  if (lane == 0) slot_of[a] = pos;
 }
 
 // One thread per 8 consecutive features of a token.
@@ -123,19 +127,26 @@ __global__ __launch_bounds__(256) void moe_combine_kernel(const T *__restrict__ 
 }
 
 hipError_t launch_moe_norm_rows(const triroute_cfg &cfg, int N, const void *x, const void *g,
-                                const triroute_compaction &c, void *out, int32_t *slot_of,
-                                hipStream_t st) {
-  const int k = cfg.top_k, Nk = N * k, E = cfg.n_experts;
-  dim3 grid((Nk + 3) / 4);
-  if (cfg.act == TRIROUTE_BF16)
-    moe_norm_rows_kernel<bf16><<<grid, 256, 0, st>>>((const bf16 *)x, (const bf16 *)g, c.exp_rows,
-                                                     c.exp_off, E, k, Nk, (bf16 *)out, slot_of,
-                                                     cfg.d_model, cfg.rms_eps);
-  else
-    moe_norm_rows_kernel<float><<<grid, 256, 0, st>>>((const float *)x, (const float *)g,
-                                                      c.exp_rows, c.exp_off, E, k, Nk,
-                                                      (float *)out, slot_of, cfg.d_model,
-                                                      cfg.rms_eps);
+                                const triroute_compaction &c, const int32_t *eidx, void *out,
+                                int32_t *slot_of, hipStream_t st) {
+  const int k = cfg.top_k, Nk = N * k, E = cfg.n_experts, d = cfg.d_model;
+  if (Nk > 0) moe_slot_of_kernel<<<(Nk + 255) / 256, 256, 0, st>>>(c.exp_rows, c.exp_off, E, Nk, slot_of);
+  const dim3 grid((N + 3) / 4);
+  auto run = [&](auto tag, auto rr) {
+    using T = decltype(tag);
+    moe_norm_tok_kernel<T, decltype(rr)::value><<<grid, 256, 0, st>>>(
+        (const T *)x, (const T *)g, eidx, slot_of, N, k, (T *)out, d, cfg.rms_eps);
+  };
+  auto by_width = [&](auto tag) {
+    if (d <= 512) run(tag, std::integral_constant<int, 1>{});
+    else if (d <= 1024) run(tag, std::integral_constant<int, 2>{});
+    else if (d <= 2048) run(tag, std::integral_constant<int, 4>{});
+    else run(tag, std::integral_constant<int, 0>{});
+  };
+  if (N > 0) {
+    if (cfg.act == TRIROUTE_BF16) by_width(bf16{});
+    else by_width(float{});
+  }
   return hipGetLastError();
 }
 

@@ -3,11 +3,81 @@
 // Slots are summed in slot order (deterministic); a token whose every slot is
 // the null expert gets x_out = xt exactly.  The expert GEMMs take n2 and give
 // Y in list order (one row per entry of the expert lists, lists back to
-// back), so the normalisation first records where each assignment's row
-// goes and then writes every token's normalised row to those rows.
+// back), so the normalisation writes each token's normalised row to the list
+// rows of its assignments and records where each assignment's row went.
 #include "kernels.hpp"
 
 namespace tr {
+
+// Few tokens (decode): one wave per list entry pos (8 consecutive elements
+// per lane access, d % 64 == 0): token a / k of assignment a = rows[pos],
+// normalised, to row pos; slot_of[a] = pos (one launch instead of two; the
+// same arithmetic as moe_norm_tok, so the same n2).  Entries past the lists' total do nothing.  The
+// norm is evaluated in fp64 (sum of squares, scale, products) and rounded
+// once to the activation dtype, so n2 is the correctly rounded value of the
+// exact norm: a last-place difference in n2 would otherwise move the expert
+// output by far more than its own size.
+template <typename T>
+__global__ __launch_bounds__(256) void moe_norm_rows_kernel(
+    const T *__restrict__ x, const T *__restrict__ g, const int32_t *__restrict__ rows,
+    const int32_t *__restrict__ off, int E, int k, int Nk, T *__restrict__ out,
+    int32_t *__restrict__ slot_of, int d, float eps) {
+  const int pos = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
+  const int lane = threadIdx.x & 63;
+  if (pos >= Nk || pos >= off[E]) return;  // off[E]: end of the last list
+  const int a = rows[pos];
+  const T *xr = x + int64_t(a / k) * d;
+  // rows of up to 1024 elements stay in registers between the two passes
+  constexpr int RR = 2;
+  float v[RR][8];
+  double ss = 0.0;
+  if (d <= 512 * RR) {
+#pragma unroll
+    for (int q = 0; q < RR; ++q) {
+      const int c = lane * 8 + 512 * q;
+      if (c < d) {
+        load8(xr + c, v[q]);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) ss = fma(double(v[q][i]), double(v[q][i]), ss);
+      }
+    }
+  } else {
+    for (int c = lane * 8; c < d; c += 512) {
+      float w[8];
+      load8(xr + c, w);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ss = fma(double(w[i]), double(w[i]), ss);
+    }
+  }
+  ss = wave_sum(ss);
+  const double r = 1.0 / sqrt(ss / double(d) + double(eps));
+  T *orow = out + int64_t(pos) * d;
+  if (d <= 512 * RR) {
+#pragma unroll
+    for (int q = 0; q < RR; ++q) {
+      const int c = lane * 8 + 512 * q;
+      if (c < d) {
+        float gv[8];
+        double o[8];
+        load8(g + c, gv);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[i] = (double(v[q][i]) * r) * double(gv[i]);
+        store8(orow + c, o);
+      }
+    }
+  } else {
+    for (int c = lane * 8; c < d; c += 512) {
+      float w[8], gv[8];
+      double o[8];
+      load8(xr + c, w);
+      load8(g + c, gv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] = (double(w[i]) * r) * double(gv[i]);
+      store8(orow + c, o);
+    }
+  }
+  if (lane == 0) slot_of[a] = pos;
+}
 
 // List row of every real assignment: slot_of[rows[pos]] = pos for each
 // entry pos of the expert lists (one thread per entry).
@@ -130,7 +200,20 @@ hipError_t launch_moe_norm_rows(const triroute_cfg &cfg, int N, const void *x, c
                                 const triroute_compaction &c, const int32_t *eidx, void *out,
                                 int32_t *slot_of, hipStream_t st) {
   const int k = cfg.top_k, Nk = N * k, E = cfg.n_experts, d = cfg.d_model;
-  if (Nk > 0) moe_slot_of_kernel<<<(Nk + 255) / 256, 256, 0, st>>>(c.exp_rows, c.exp_off, E, Nk, slot_of);
+  if (Nk <= 2048) {  // few tokens: the launch costs more than normalising a row twice
+    if (Nk == 0) return hipSuccess;
+    const dim3 g1((Nk + 3) / 4);
+    if (cfg.act == TRIROUTE_BF16)
+      moe_norm_rows_kernel<bf16><<<g1, 256, 0, st>>>((const bf16 *)x, (const bf16 *)g, c.exp_rows,
+                                                     c.exp_off, E, k, Nk, (bf16 *)out, slot_of, d,
+                                                     cfg.rms_eps);
+    else
+      moe_norm_rows_kernel<float><<<g1, 256, 0, st>>>((const float *)x, (const float *)g,
+                                                      c.exp_rows, c.exp_off, E, k, Nk,
+                                                      (float *)out, slot_of, d, cfg.rms_eps);
+    return hipGetLastError();
+  }
+  moe_slot_of_kernel<<<(Nk + 255) / 256, 256, 0, st>>>(c.exp_rows, c.exp_off, E, Nk, slot_of);
   const dim3 grid((N + 3) / 4);
   auto run = [&](auto tag, auto rr) {
     using T = decltype(tag);
@@ -143,10 +226,8 @@ hipError_t launch_moe_norm_rows(const triroute_cfg &cfg, int N, const void *x, c
     else if (d <= 2048) run(tag, std::integral_constant<int, 4>{});
     else run(tag, std::integral_constant<int, 0>{});
   };
-  if (N > 0) {
-    if (cfg.act == TRIROUTE_BF16) by_width(bf16{});
-    else by_width(float{});
-  }
+  if (cfg.act == TRIROUTE_BF16) by_width(bf16{});
+  else by_width(float{});
   return hipGetLastError();
 }
 

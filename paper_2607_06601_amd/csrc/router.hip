@@ -380,14 +380,16 @@ __global__ __launch_bounds__(512) void router_tail_kernel(
   }
 }
 
-// The same tail for few tokens (decode): one wave per token, so every
-// token's chain runs on its own SIMD instead of 16 tokens sharing one block.
-// The weights are read from global memory (cache-resident: every wave reads
-// the same 120 KB); all trunk chunks are loaded at once.  The products are
-// summed in a different order than the MFMA tail (fp32 either way; the
-// decisions do not depend on it above the routing margin).
-constexpr int RT1_MAXKS = 32;
-__global__ __launch_bounds__(256) void router_tail_tok_kernel(
+// The same tail for few tokens (decode), one 256-thread block per token, so
+// that each step's weight reads are all in flight at once instead of a wave
+// walking whole rows: thread j < 128 sums the trunk partials of column j (in
+// chunk order, then b1); two threads per row of W2 (64 columns each) and
+// four per logit row (32 columns each), their partial sums added by lane
+// shuffles (every thread of a row ends with the same value).  fp32 either
+// way; the products are summed in a different order than the MFMA tail, and
+// the decisions do not depend on it above the routing margin.
+constexpr int RTB_MAXKS = 48;
+__global__ __launch_bounds__(256) void router_tail_blk_kernel(
     const float *__restrict__ upart, int KS, const float *__restrict__ b1,
     const float *__restrict__ W2, const float *__restrict__ b2, const float *__restrict__ gr,
     const float *__restrict__ Wa, const float *__restrict__ ca, const float *__restrict__ We,
@@ -395,81 +397,83 @@ __global__ __launch_bounds__(256) void router_tail_tok_kernel(
     uint8_t *__restrict__ mode, uint8_t *__restrict__ bit, int32_t *__restrict__ eidx,
     float *__restrict__ egate, int N, int H, int A, int E1, int k, float eps, TailTap tap) {
   constexpr int DR = RT_DR;
-  __shared__ __align__(16) float vs[4][2][DR];  // per wave: u, then h^; z
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int t = blockIdx.x * 4 + wave;
-  if (t >= N) return;  // wave-uniform; no barrier below
-  float *us = vs[wave][0], *zs = vs[wave][1];
+  __shared__ __align__(16) float us[DR], hs[DR], zs[RT_NZ];
+  __shared__ float red[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t = blockIdx.x;  // grid = N
   const int NZ = 3 * A + E1 + 4;
-  // u = GELU(sum of the KS trunk partials + b1), chunks summed in order
-  float p0[RT1_MAXKS], p1[RT1_MAXKS];
+  // u = GELU(sum of the KS trunk partials + b1)
+  if (tid < DR) {
+    float p[RTB_MAXKS];
 #pragma unroll
-  for (int s = 0; s < RT1_MAXKS; ++s)
-    if (s < KS) {
-      p0[s] = upart[(int64_t(s) * N + t) * DR + lane];
-      p1[s] = upart[(int64_t(s) * N + t) * DR + lane + 64];
-    }
-  float a0 = 0.f, a1 = 0.f;
+    for (int s = 0; s < RTB_MAXKS; ++s)
+      if (s < KS) p[s] = upart[(int64_t(s) * N + t) * DR + tid];
+    float a = 0.f;
 #pragma unroll
-  for (int s = 0; s < RT1_MAXKS; ++s)
-    if (s < KS) {
-      a0 += p0[s];
-      a1 += p1[s];
-    }
-  a0 += b1[lane];
-  a1 += b1[lane + 64];
-  if (tap.a1) {
-    tap.a1[int64_t(t) * DR + lane] = a0;
-    tap.a1[int64_t(t) * DR + lane + 64] = a1;
+    for (int s = 0; s < RTB_MAXKS; ++s)
+      if (s < KS) a += p[s];
+    a += b1[tid];
+    if (tap.a1) tap.a1[int64_t(t) * DR + tid] = a;
+    us[tid] = 0.5f * a * (1.0f + erff(a * 0.70710678118654752f));
   }
-  us[lane] = 0.5f * a0 * (1.0f + erff(a0 * 0.70710678118654752f));
-  us[lane + 64] = 0.5f * a1 * (1.0f + erff(a1 * 0.70710678118654752f));
-  __builtin_amdgcn_wave_barrier();
-  // h = W2 u + b2: lane n owns rows n and n + 64
-  float h0 = 0.f, h1 = 0.f;
-  const float4 *w0 = (const float4 *)(W2 + lane * DR), *w1 = (const float4 *)(W2 + (lane + 64) * DR);
-#pragma unroll 8
-  for (int c4 = 0; c4 < DR / 4; ++c4) {
-    const float4 x = w0[c4], y = w1[c4];
-    const float4 u = *(const float4 *)(us + 4 * c4);
-    h0 = fmaf(x.x, u.x, h0); h0 = fmaf(x.y, u.y, h0); h0 = fmaf(x.z, u.z, h0); h0 = fmaf(x.w, u.w, h0);
-    h1 = fmaf(y.x, u.x, h1); h1 = fmaf(y.y, u.y, h1); h1 = fmaf(y.z, u.z, h1); h1 = fmaf(y.w, u.w, h1);
-  }
-  h0 += b2[lane];
-  h1 += b2[lane + 64];
-  if (tap.hpre) {
-    tap.hpre[int64_t(t) * DR + lane] = h0;
-    tap.hpre[int64_t(t) * DR + lane + 64] = h1;
-  }
-  // h^ = RMSNorm(h) gr
-  const float ss = seg_sum(h0 * h0 + h1 * h1, 64);
-  const float r = 1.0f / sqrtf(ss / float(DR) + eps);
-  __builtin_amdgcn_wave_barrier();  // every lane is done reading u
-  us[lane] = (h0 * r) * gr[lane];
-  us[lane + 64] = (h1 * r) * gr[lane + 64];
-  if (tap.h) {
-    tap.h[int64_t(t) * DR + lane] = us[lane];
-    tap.h[int64_t(t) * DR + lane + 64] = us[lane + 64];
-  }
-  __builtin_amdgcn_wave_barrier();
-  // z = [Wa; We; Wb] h^ + [ca; ce; cb]: lane j owns logits j and j + 64
-  for (int z = lane; z < NZ; z += 64) {
-    const float *wz = z < 3 * A ? Wa + z * DR : z < 3 * A + E1 ? We + (z - 3 * A) * DR
-                                                                : Wb + (z - 3 * A - E1) * DR;
+  __syncthreads();
+  // h = W2 u + b2, row r = tid / 2; h^ = RMSNorm(h) gr
+  {
+    const int r = tid >> 1, c0 = (tid & 1) * (DR / 2);
+    const float4 *w = (const float4 *)(W2 + r * DR + c0);
+    float4 x[DR / 8];
+#pragma unroll
+    for (int i = 0; i < DR / 8; ++i) x[i] = w[i];
     float acc = 0.f;
-#pragma unroll 8
-    for (int c4 = 0; c4 < DR / 4; ++c4) {
-      const float4 x = ((const float4 *)wz)[c4];
-      const float4 u = *(const float4 *)(us + 4 * c4);
-      acc = fmaf(x.x, u.x, acc); acc = fmaf(x.y, u.y, acc); acc = fmaf(x.z, u.z, acc); acc = fmaf(x.w, u.w, acc);
+#pragma unroll
+    for (int i = 0; i < DR / 8; ++i) {
+      const float4 u = *(const float4 *)(us + c0 + 4 * i);
+      acc = fmaf(x[i].x, u.x, acc); acc = fmaf(x[i].y, u.y, acc);
+      acc = fmaf(x[i].z, u.z, acc); acc = fmaf(x[i].w, u.w, acc);
     }
-    const float bias = z < 3 * A ? ca[z] : z < 3 * A + E1 ? ce[z - 3 * A] : cb[z - 3 * A - E1];
-    zs[z] = acc + bias;
-    if (tap.z) tap.z[int64_t(t) * NZ + z] = zs[z];
+    acc += __shfl_xor(acc, 1, 64);
+    const float h = acc + b2[r];
+    const float ssw = seg_sum((tid & 1) ? 0.f : h * h, 64);  // the wave's 32 rows
+    if (lane == 0) red[wave] = ssw;
+    __syncthreads();
+    const float ss = (red[0] + red[1]) + (red[2] + red[3]);
+    const float rr = 1.0f / sqrtf(ss / float(DR) + eps);
+    const float hn = (h * rr) * gr[r];
+    if ((tid & 1) == 0) {
+      hs[r] = hn;
+      if (tap.hpre) tap.hpre[int64_t(t) * DR + r] = h;
+      if (tap.h) tap.h[int64_t(t) * DR + r] = hn;
+    }
   }
-  __builtin_amdgcn_wave_barrier();
-  // modes: lane h takes head h; argmax, first maximum on ties
-  const int HA = H / A;  // heads per decision group
+  __syncthreads();
+  // z = [Wa; We; Wb] h^ + [ca; ce; cb], logit row z0 + tid / 4
+  for (int z0 = 0; z0 < NZ; z0 += 64) {
+    const int z = z0 + (tid >> 2), c0 = (tid & 3) * (DR / 4);
+    float acc = 0.f;
+    if (z < NZ) {
+      const float *wz = z < 3 * A ? Wa + z * DR : z < 3 * A + E1 ? We + (z - 3 * A) * DR
+                                                                  : Wb + (z - 3 * A - E1) * DR;
+      float4 x[DR / 16];
+#pragma unroll
+      for (int i = 0; i < DR / 16; ++i) x[i] = ((const float4 *)(wz + c0))[i];
+#pragma unroll
+      for (int i = 0; i < DR / 16; ++i) {
+        const float4 u = *(const float4 *)(hs + c0 + 4 * i);
+        acc = fmaf(x[i].x, u.x, acc); acc = fmaf(x[i].y, u.y, acc);
+        acc = fmaf(x[i].z, u.z, acc); acc = fmaf(x[i].w, u.w, acc);
+      }
+    }
+    acc += __shfl_xor(acc, 1, 64);
+    acc += __shfl_xor(acc, 2, 64);
+    if (z < NZ && (tid & 3) == 0) {
+      const float bias = z < 3 * A ? ca[z] : z < 3 * A + E1 ? ce[z - 3 * A] : cb[z - 3 * A - E1];
+      zs[z] = acc + bias;
+      if (tap.z) tap.z[int64_t(t) * NZ + z] = zs[z];
+    }
+  }
+  __syncthreads();
+  if (wave != 0) return;  // decisions by the first wave (no barrier below)
+  const int HA = H / A;
   for (int hh = lane; hh < H; hh += 64) {
     const float *za = zs + 3 * (hh / HA);
     int best = 0;
@@ -484,7 +488,6 @@ __global__ __launch_bounds__(256) void router_tail_tok_kernel(
       if (zb[j] > zb[bb]) bb = j;
     bit[t] = uint8_t(bb);
   }
-  // top-k by logit, ties to the lower id; gates renormalised over the set
   const float zj = lane < E1 ? zs[3 * A + lane] : -INFINITY;
   const float zmax = seg_max(zj, 64);
   uint64_t taken = 0;
@@ -526,8 +529,8 @@ hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const fl
     trunk1_kernel<float><<<g2, 256, 0, st>>>((const float *)x, rinv, w.g1, psi, w.W1, u, N, d,
                                              cfg.d_psi, kchunk);
   }
-  if (N <= 256 && ks <= RT1_MAXKS) {  // few tokens: one wave per token
-    router_tail_tok_kernel<<<dim3((N + 3) / 4), 256, 0, st>>>(
+  if (N <= 256 && ks <= RTB_MAXKS) {  // few tokens: one block per token
+    router_tail_blk_kernel<<<dim3(N), 256, 0, st>>>(
         u, ks, w.b1, w.W2, w.b2, w.gr, w.Wa, w.ca, w.We, w.ce, w.Wb, w.cb, mode, bit, eidx, egate,
         N, cfg.n_heads, attn_groups(cfg), cfg.n_experts + 1, cfg.top_k, cfg.rms_eps, tap);
     return hipGetLastError();

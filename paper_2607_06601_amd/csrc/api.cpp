@@ -983,7 +983,9 @@ static int layer_impl(const triroute_cfg *cfg, int B, int T, bool decode, const 
     CHECK_HIP(tr::launch_router(*cfg, N, x, psi, *rw, L.n1, L.mode, L.bit, L.eidx, L.egate, r.rinv,
                                 r.u, &job, st),
               "router launch");
-    CHECK_HIP(tr::launch_compact(*cfg, B, T, L.mode, L.eidx, L.cmp, r.hist, st), "compaction");
+    // decode attention reads the modes themselves: no attention lists
+    CHECK_HIP(tr::launch_compact(*cfg, B, T, L.mode, L.eidx, L.cmp, r.hist, st, !decode),
+              "compaction");
     CHECK_HIP(tr::launch_qkv(*cfg, B, T, L.n1, *dw, seq_len, seq_ids, cache->n_seq, L.q, L.k, L.v,
                              rope, true, st),
               "qkv launch");

@@ -116,13 +116,60 @@ __global__ __launch_bounds__(256) void compact_scatter_kernel(const int32_t *__r
   }
 }
 
+// Few assignments (one chunk) and no attention lists (decode): the expert
+// lists by one block in one launch, histogram, offsets and the same stable
+// scatter as the two kernels above (so the same lists).
+__global__ __launch_bounds__(256) void compact_experts_one_kernel(const int32_t *__restrict__ eidx,
+                                                                  int E1, int Nk,
+                                                                  int32_t *__restrict__ rows,
+                                                                  int32_t *__restrict__ exp_cnt,
+                                                                  int32_t *__restrict__ exp_off) {
+  __shared__ int lh[64], run[64];
+  __shared__ int wc[4][64];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  if (tid < E1) lh[tid] = 0;  // E1 <= 64
+  __syncthreads();
+  for (int a = tid; a < Nk; a += 256) atomicAdd(&lh[eidx[a]], 1);
+  __syncthreads();
+  if (tid < E1) {
+    int start = 0;  // lists of experts 1 .. tid - 1 come first
+    for (int ee = 1; ee < tid; ++ee) start += lh[ee];
+    run[tid] = start;
+    exp_cnt[tid] = lh[tid];
+    exp_off[tid] = tid == 0 ? 0 : start + lh[tid];
+  }
+  __syncthreads();
+  for (int sub = 0; sub < Nk; sub += 256) {  // block-uniform bound: every barrier is reached
+    const int a = sub + tid;
+    const int e = a < Nk ? eidx[a] : -1;
+    int rank = 0;
+    for (int ee = 1; ee < E1; ++ee) {
+      const uint64_t bal = __ballot(e == ee);
+      if (e == ee) rank = __popcll(bal & lanemask_lt());
+      if (lane == 0) wc[w][ee] = __popcll(bal);
+    }
+    __syncthreads();
+    if (e >= 1) {
+      int pos = run[e] + rank;
+      for (int ww = 0; ww < w; ++ww) pos += wc[ww][e];
+      rows[pos] = a;
+    }
+    __syncthreads();
+    if (tid >= 1 && tid < E1) run[tid] += wc[0][tid] + wc[1][tid] + wc[2][tid] + wc[3][tid];
+    __syncthreads();
+  }
+}
 int compact_hist_ints(int N, int k, int E1) { return ((N * k + CHUNK - 1) / CHUNK) * E1; }
 
 hipError_t launch_compact(const triroute_cfg &cfg, int B, int T, const uint8_t *mode,
                           const int32_t *eidx, const triroute_compaction &c, int32_t *hist,
-                          hipStream_t st) {
+                          hipStream_t st, bool attn_lists) {
   const int H = cfg.n_heads, E1 = cfg.n_experts + 1, Nk = B * T * cfg.top_k;
   const int nbe = (Nk + CHUNK - 1) / CHUNK;
+  if (!attn_lists && nbe == 1) {
+    compact_experts_one_kernel<<<1, 256, 0, st>>>(eidx, E1, Nk, c.exp_rows, c.exp_cnt, c.exp_off);
+    return hipGetLastError();
+  }
   compact_count_kernel<<<B * H + nbe, 256, 0, st>>>(mode, eidx, B, T, H, E1, Nk, c.attn_cnt,
                                                     c.attn_idx, hist);
   compact_scatter_kernel<<<nbe, 256, 0, st>>>(eidx, hist, nbe, E1, Nk, c.exp_rows, c.exp_cnt,

@@ -55,9 +55,11 @@ hipError_t launch_router(const triroute_cfg &cfg, int N, const void *x, const fl
                          hipStream_t st, TailTap tap = TailTap{});
 // compact.hip
 int compact_hist_ints(int N, int k, int E1);
+// attn_lists false: the attention lists are not wanted (decode reads the
+// modes themselves) and are left untouched.
 hipError_t launch_compact(const triroute_cfg &cfg, int B, int T, const uint8_t *mode,
                           const int32_t *eidx, const triroute_compaction &c, int32_t *hist,
-                          hipStream_t st);
+                          hipStream_t st, bool attn_lists = true);
 // kv.hip
 hipError_t launch_fill_u32(void *p, int64_t n_words, uint32_t v, hipStream_t st);
 // append scratch: each row's pool lengths before the append

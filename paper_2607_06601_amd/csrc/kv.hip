@@ -120,125 +120,170 @@ __global__ __launch_bounds__(1024) void kv_slots_kernel(CacheView cv, int T,
   }
 }
 
-// One token per row (decode): one wave per (row, kv head), one channel per
-// lane and row of K and V (two on d_h 128): quantize (group min/max by lane
-// reductions), write K codes (every 32-bit word of a K record belongs to one
-// slot; the token's words are assembled in LDS, each lane ORs its element
-// into its word, then one lane per word stores it), scales and 8/16-bit V
-// codes (byte and half-word stores).  2- and 4-bit V codes share words with
-// slots appended earlier: the token's bits of each word are cleared and set
-// in place by word atomics (another row's token of the same word, if any,
-// touches other bits).
+// One token per row (decode).  The slot of a row's token (sequence s, width
+// bi), in one thread:
+// the checks and the page take of kv_slots_kernel for a single token; the
+// token's position, the new pool and sequence lengths.  Returns the slot
+// (-1: row dropped, status flagged).
+__device__ int kv_slot1(const CacheView &cv, int s, int bi) {
+  if (s < 0 || s >= cv.n_seq) {
+    atomicOr(cv.status, int(TRIROUTE_CACHE_BAD_SEQ));
+    return -1;
+  }
+  const int len0 = cv.seq_len[s];
+  if (len0 + 1 > cv.capacity) {
+    atomicOr(cv.status, int(TRIROUTE_CACHE_OVERFLOW));
+    return -1;
+  }
+  const int run = cv.pool_len[s * 4 + bi];
+  if (cv.PT) {  // paged: the page the pool grows into, from the free stack
+    const int per = cv.PT * cv.TS;
+    const int need = (run + 1 + per - 1) / per;
+    int32_t *held = cv.alloc + s * 4 + bi;
+    const int have = *held;
+    if (need > have) {
+      const int k = need - have;
+      const int top = atomicSub(cv.free_top + bi, k);
+      if (need > cv.max_pages || top - k < 0) {
+        atomicAdd(cv.free_top + bi, k);  // give the claim back
+        atomicOr(cv.status, int(TRIROUTE_CACHE_OVERFLOW));
+        return -1;
+      }
+      for (int q = 0; q < k; ++q)
+        cv.page_table[(int64_t(s) * 4 + bi) * cv.max_pages + have + q] = cv.free_list[bi][top - k + q];
+      *held = need;
+    }
+  }
+  cv.pos_at(s, bi, run) = len0;
+  cv.pool_len[s * 4 + bi] = run + 1;
+  cv.seq_len[s] = len0 + 1;
+  return run;
+}
+
+// One token per row (decode), one launch: one block per row; thread 0 takes
+// the slot (kv_slot1), then wave w writes kv heads w, w + 4, ...: one
+// channel per lane and row of K and V (two on d_h 128): quantize (group
+// min/max by lane reductions), write K codes (every 32-bit word of a K
+// record belongs to one slot; the token's words are assembled in LDS, each
+// lane ORs its element into its word, then one lane per word stores it),
+// scales and 8/16-bit V codes (byte and half-word stores).  2- and 4-bit V
+// codes share words with slots appended earlier: the token's bits of each
+// word are cleared and set in place by word atomics (another row's token of
+// the same word, if any, touches other bits).
 template <typename T>
-__global__ __launch_bounds__(256) void kv_token_kernel(CacheView cv, int N,
+__global__ __launch_bounds__(256) void kv_token_kernel(CacheView cv,
                                                        const int32_t *__restrict__ seq_ids,
                                                        const T *__restrict__ kin,
                                                        const T *__restrict__ vin,
-                                                       const uint8_t *__restrict__ bit,
-                                                       const int32_t *__restrict__ old_len) {
-  __shared__ uint32_t kw[4][128];  // per wave: the token's K words (at most 4 dh bits... / 32)
-  // the wave index, and all that follows from it, in scalar registers: the
-  // per-(token, head) bookkeeping (divisions, addresses) runs on the scalar
-  // unit and the branches on the width are scalar branches
+                                                       const uint8_t *__restrict__ bit) {
+  __shared__ uint32_t kws[4][128];  // per wave: the token's K words (at most 4 dh bits / 32)
+  __shared__ int slot_s;
+  const int i = blockIdx.x;  // row i = token i
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int item = blockIdx.x * 4 + w;
-  const int Hkv = cv.Hkv, dh = cv.dh, G = cv.G;
-  const int i = item / Hkv, g = item % Hkv;  // row i = token i
-  if (item >= N * Hkv) return;
   const int bi = __builtin_amdgcn_readfirstlane(int(bit[i]));
-  // the token's slot: its pool's length before the append (-1: row dropped)
-  const int slot = __builtin_amdgcn_readfirstlane(old_len[i * 4 + bi]);
-  if (slot < 0) return;  // wave-uniform: nothing of this wave touches LDS or a barrier
   const int s = seq_ids ? __builtin_amdgcn_readfirstlane(seq_ids[i]) : i;
-  const int bp = cv.bits(bi);
-  const int tile = slot / cv.TS, st = slot % cv.TS;
-  uint8_t *tp = cv.tile(s, bi, g, tile);
-  const int NR = dh >> 6;  // channels per lane: lane + 64 r
-  // both rows first, so that the two loads are in flight together
-  T kr[2], vr[2];
-  const int64_t row = int64_t(i) * Hkv * dh + g * dh;
+  if (threadIdx.x == 0) slot_s = kv_slot1(cv, s, bi);
+  __syncthreads();
+  const int slot = __builtin_amdgcn_readfirstlane(slot_s);
+  if (slot < 0) return;  // block-uniform: no barrier below
+  uint32_t *kwv = kws[w];
+  const int Hkv = cv.Hkv, dh = cv.dh, G = cv.G;
+  // the wave's kv heads; the scalar bookkeeping (divisions, addresses) runs
+  // on the scalar unit and the branches on the width are scalar branches
+  for (int g = w; g < Hkv; g += 4) {
+    // the wave's own LDS words of the previous head are read: order first
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    __builtin_amdgcn_wave_barrier();
+    const int bp = cv.bits(bi);
+    const int tile = slot / cv.TS, st = slot % cv.TS;
+    uint8_t *tp = cv.tile(s, bi, g, tile);
+    const int NR = dh >> 6;  // channels per lane: lane + 64 r
+    // both rows first, so that the two loads are in flight together
+    T kr[2], vr[2];
+    const int64_t row = int64_t(i) * Hkv * dh + g * dh;
 #pragma unroll
-  for (int r = 0; r < 2; ++r)
-    if (r < NR) {
-      kr[r] = kin[row + lane + 64 * r];
-      vr[r] = vin[row + lane + 64 * r];
-    }
-  const int KS = dh >> 5;
-  const int blk = st >> 4, n = st & 15;
-  const int per = bp == 32 ? 1 : 32 / bp;                 // elements per word
-  const int q0 = blk * KS * 8, nq = KS * 8;                // this token's elements per record
-  const int wpr = (nq + per - 1) / per;                    // its words per record
-  const int nw = 4 * wpr;                                  // K words of the token
-  for (int x = lane; x < nw; x += 64) kw[w][x] = 0u;
-  uint8_t *vp = tp + cv.v_codes_off(bi);
+    for (int r = 0; r < 2; ++r)
+      if (r < NR) {
+        kr[r] = kin[row + lane + 64 * r];
+        vr[r] = vin[row + lane + 64 * r];
+      }
+    const int KS = dh >> 5;
+    const int blk = st >> 4, n = st & 15;
+    const int per = bp == 32 ? 1 : 32 / bp;                 // elements per word
+    const int q0 = blk * KS * 8, nq = KS * 8;                // this token's elements per record
+    const int wpr = (nq + per - 1) / per;                    // its words per record
+    const int nw = 4 * wpr;                                  // K words of the token
+    for (int x = lane; x < nw; x += 64) kwv[x] = 0u;
+    uint8_t *vp = tp + cv.v_codes_off(bi);
 #pragma unroll
-  for (int kvsel = 0; kvsel < 2; ++kvsel) {
+    for (int kvsel = 0; kvsel < 2; ++kvsel) {
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      if (r >= NR) break;
-      const int c = lane + 64 * r;
-      const T raw = kvsel ? vr[r] : kr[r];
-      const float x = Act<T>::cvt(raw);
-      uint32_t e;
-      if (bi == 3) {
-        if (sizeof(T) == 2)
-          e = uint32_t(*(const uint16_t *)&raw);
-        else
-          e = __float_as_uint(x);
-      } else {
-        const int seg = G < 64 ? G : 64;
-        const float mn = seg_min(x, seg), mx = seg_max(x, seg);
-        const float levels = float((1 << bp) - 1);
-        const float s32 = __fdiv_rn(mx - mn, levels);
-        const _Float16 s16 = (_Float16)s32;
-        const _Float16 z16 = (_Float16)mn;
-        const float S = (float)s16, Z = (float)z16;
-        float q = 0.f;
-        if (S != 0.f) q = fminf(fmaxf(rintf(__fdiv_rn(x - Z, S)), 0.f), levels);
-        e = uint32_t(q);
-        if ((lane & (seg - 1)) == 0) {
-          const int grp = c / G;
-          const int off = (kvsel ? cv.v_sz_off(bi) : cv.k_sz_off(bi)) + (st * (dh / G) + grp) * 4;
-          const uint32_t pk = uint32_t(*(const uint16_t *)&s16) | (uint32_t(*(const uint16_t *)&z16) << 16);
-          *(uint32_t *)(tp + off) = pk;
+      for (int r = 0; r < 2; ++r) {
+        if (r >= NR) break;
+        const int c = lane + 64 * r;
+        const T raw = kvsel ? vr[r] : kr[r];
+        const float x = Act<T>::cvt(raw);
+        uint32_t e;
+        if (bi == 3) {
+          if (sizeof(T) == 2)
+            e = uint32_t(*(const uint16_t *)&raw);
+          else
+            e = __float_as_uint(x);
+        } else {
+          const int seg = G < 64 ? G : 64;
+          const float mn = seg_min(x, seg), mx = seg_max(x, seg);
+          const float levels = float((1 << bp) - 1);
+          const float s32 = __fdiv_rn(mx - mn, levels);
+          const _Float16 s16 = (_Float16)s32;
+          const _Float16 z16 = (_Float16)mn;
+          const float S = (float)s16, Z = (float)z16;
+          float q = 0.f;
+          if (S != 0.f) q = fminf(fmaxf(rintf(__fdiv_rn(x - Z, S)), 0.f), levels);
+          e = uint32_t(q);
+          if ((lane & (seg - 1)) == 0) {
+            const int grp = c / G;
+            const int off = (kvsel ? cv.v_sz_off(bi) : cv.k_sz_off(bi)) + (st * (dh / G) + grp) * 4;
+            const uint32_t pk = uint32_t(*(const uint16_t *)&s16) | (uint32_t(*(const uint16_t *)&z16) << 16);
+            *(uint32_t *)(tp + off) = pk;
+          }
+        }
+        if (kvsel == 0) {
+          // K element (slot st, channel c): record o, element q = f * 8 + j
+          const int ks = c >> 5, o = (c >> 3) & 3, j = c & 7;
+          const int q = (blk * KS + ks) * 8 + j;
+          int wd, bt;
+          q_word(q, bp, wd, bt);
+          if (bp == 32)
+            kwv[o * wpr + (wd - q0)] = e;
+          else
+            atomicOr(&kwv[o * wpr + (wd - q0 / per)], e << bt);
+        } else {
+          int ln, q, wd, bt;
+          v_place(st, c, dh, ln, q);
+          q_word(q, bp, wd, bt);
+          uint8_t *addr = vp + ln * (8 * bp) + wd * 4;
+          if (bp <= 4) {
+            const uint32_t m = ((1u << bp) - 1u) << bt;
+            atomicAnd((uint32_t *)addr, ~m);
+            atomicOr((uint32_t *)addr, e << bt);
+          } else if (bp == 8)
+            addr[bt >> 3] = uint8_t(e);
+          else if (bp == 16)
+            *(uint16_t *)(addr + (bt >> 3)) = uint16_t(e);
+          else
+            *(uint32_t *)addr = e;
         }
       }
-      if (kvsel == 0) {
-        // K element (slot st, channel c): record o, element q = f * 8 + j
-        const int ks = c >> 5, o = (c >> 3) & 3, j = c & 7;
-        const int q = (blk * KS + ks) * 8 + j;
-        int wd, bt;
-        q_word(q, bp, wd, bt);
-        if (bp == 32)
-          kw[w][o * wpr + (wd - q0)] = e;
-        else
-          atomicOr(&kw[w][o * wpr + (wd - q0 / per)], e << bt);
-      } else {
-        int ln, q, wd, bt;
-        v_place(st, c, dh, ln, q);
-        q_word(q, bp, wd, bt);
-        uint8_t *addr = vp + ln * (8 * bp) + wd * 4;
-        if (bp <= 4) {
-          const uint32_t m = ((1u << bp) - 1u) << bt;
-          atomicAnd((uint32_t *)addr, ~m);
-          atomicOr((uint32_t *)addr, e << bt);
-        } else if (bp == 8)
-          addr[bt >> 3] = uint8_t(e);
-        else if (bp == 16)
-          *(uint16_t *)(addr + (bt >> 3)) = uint16_t(e);
-        else
-          *(uint32_t *)addr = e;
-      }
     }
-  }
-  // the wave's own LDS words: order its ORs before its reads (no other wave
-  // touches them, so no block barrier)
-  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
-  __builtin_amdgcn_wave_barrier();
-  for (int x = lane; x < nw; x += 64) {
-    const int o = x / wpr, wr = x % wpr;
-    const int wd = q0 / per + wr;
-    *(uint32_t *)(tp + (o * 16 + n) * (8 * bp) + wd * 4) = kw[w][x];
+    // the wave's own LDS words: order its ORs before its reads (no other wave
+    // touches them, so no block barrier)
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    __builtin_amdgcn_wave_barrier();
+    for (int x = lane; x < nw; x += 64) {
+      const int o = x / wpr, wr = x % wpr;
+      const int wd = q0 / per + wr;
+      *(uint32_t *)(tp + (o * 16 + n) * (8 * bp) + wd * 4) = kwv[x];
+    }
   }
 }
 
@@ -572,17 +617,15 @@ hipError_t launch_kv_paged_reset(const CacheView &cv, int seq, hipStream_t st) {
 hipError_t launch_kv_append(const triroute_cfg &cfg, const CacheView &cv, int B, int T,
                             const int32_t *seq_ids, const void *k, const void *v,
                             const uint8_t *bit, const KvWs &ws, hipStream_t st) {
-  kv_slots_kernel<<<B, 1024, 0, st>>>(cv, T, seq_ids, bit, ws.old_len);
-  if (T == 1) {  // one token per row: token-parallel kernel
-    const dim3 g1((B * cfg.n_kv_heads + 3) / 4);
+  if (T == 1) {  // one token per row: slot and codes in one launch
     if (cfg.act == TRIROUTE_BF16)
-      kv_token_kernel<bf16><<<g1, 256, 0, st>>>(cv, B, seq_ids, (const bf16 *)k, (const bf16 *)v,
-                                                bit, ws.old_len);
+      kv_token_kernel<bf16><<<B, 256, 0, st>>>(cv, seq_ids, (const bf16 *)k, (const bf16 *)v, bit);
     else
-      kv_token_kernel<float><<<g1, 256, 0, st>>>(cv, B, seq_ids, (const float *)k,
-                                                 (const float *)v, bit, ws.old_len);
+      kv_token_kernel<float><<<B, 256, 0, st>>>(cv, seq_ids, (const float *)k, (const float *)v,
+                                                bit);
     return hipGetLastError();
   }
+  kv_slots_kernel<<<B, 1024, 0, st>>>(cv, T, seq_ids, bit, ws.old_len);
   // 32-slot steps an append can touch in one pool: all T tokens, plus the
   // partly filled step it starts in
   const int JS = (T + 31) / 32 + 1;

@@ -284,3 +284,61 @@ def test_layer_decode(name, nseq, variant):
     assert_close(npy(xo)[seqs], r1["xout"], act, "x_out (forced x~)")
     f = 1.0 + 2.0 * ROUNDING_SPREAD[name if variant is None else f"{name}/{variant}"]
     assert_close(npy(xo)[seqs], r0["xout"], act, "x_out (unforced)", factor=f)
+
+
+def test_layer_decode_wide_batch_rows_repeat():
+    """320 decode rows: the 64 sequences of the 410M workload five times over
+    (row b + 64 j holds row b's inputs and its own copy of b's context), so
+    the step routes 640 expert assignments (the decode compaction's one-block
+    scatter runs several rounds), appends 320 rows in one launch and takes
+    the tile form of the router tail.  Every copy of a row must give the
+    bit-identical result; against the 64-row step (one-block router tail)
+    the decisions, q, the attention output and x~ are bit-identical, and
+    x_out may differ only where the two tails' fp32 gates round a bf16
+    element differently (one bf16 step)."""
+    L = layer("410m_bf16_decode")
+    cfg = L["cfg"]
+    D = DeviceLayer(L)
+    c = D.cfg
+    B, ctx, R = cfg["B"], cfg["ctx"], 5
+    BW = B * R
+    runs = {}
+    for nb in (B, BW):
+        cache = tr.KVCache(c, nb, ctx + 16)
+        ws = tr.workspace(c, tr.OP_KV_APPEND, 1, ctx)
+        for s in range(B):
+            k, v = gen.context_kv(cfg, s)
+            bits = to_dev(gen.context_bits(cfg, s), torch.uint8)
+            kd, vd = to_dev(k.reshape(ctx, -1), D.act), to_dev(v.reshape(ctx, -1), D.act)
+            for j in range(nb // B):
+                tr.kv_append(c, cache, 1, ctx, kd, vd, bits, ws,
+                             seq_ids=torch.tensor([s + B * j], dtype=torch.int32, device=DEV))
+        torch.cuda.synchronize()
+        assert cache.status() == 0
+        x = D.x.repeat(nb // B, 1)
+        psi = D.psi.repeat(nb // B, 1)
+        xo = torch.empty(nb, cfg["d"], dtype=D.act, device=DEV)
+        t, s_ = _taps(cfg, nb, D.act)
+        print(f"decode step of {nb} rows ({nb * cfg['k']} expert assignments)", flush=True)
+        tr.layer_decode(c, nb, x, psi, D.rw, D.dw, D.mw, cache, xo,
+                        tr.workspace(c, tr.OP_LAYER_DECODE, nb, 1), taps=s_)
+        torch.cuda.synchronize()
+        assert cache.status() == 0
+        t["xout"] = xo
+        runs[nb] = t
+        del cache
+    w, n = runs[BW], runs[B]
+    for key in ("mode", "bit", "eidx", "egate", "q", "o", "xt", "xout"):
+        for j in range(1, R):
+            assert torch.equal(w[key][B * j:B * (j + 1)], w[key][:B]), (key, j)
+    for key in ("mode", "bit", "eidx", "q", "o", "xt"):
+        assert torch.equal(w[key][:B], n[key]), key
+    ga, gb = w["egate"][:B].double(), n["egate"].double()
+    note("wide decode: max rel gate difference against the 64-row step",
+         float(((ga - gb).abs() / gb.abs().clamp_min(1e-30)).max()))
+    assert torch.allclose(ga, gb, rtol=1e-5, atol=0)
+    xa, xb = w["xout"][:B].double(), n["xout"].double()
+    diff = (xa - xb).abs()
+    note("wide decode: x_out elements differing from the 64-row step (fraction)",
+         float((diff > 0).double().mean()))
+    assert bool((diff <= 2.0 ** -7 * torch.maximum(xa.abs(), xb.abs())).all())

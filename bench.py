@@ -135,7 +135,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the routed layer is "
-              "measured on a single MI355X; how it would shard is described in DESIGN.md",
+              "measured on a single MI355X",
               file=sys.stderr)
         sys.exit(2)
     if args.summarize_pmc:

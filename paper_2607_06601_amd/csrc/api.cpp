@@ -442,10 +442,10 @@ int check_paged_args(int n_seq, int capacity, int PT, const int32_t *np) {
 }
 
 hipError_t run_attn_prefill(const triroute_cfg &c, const triroute_kv_cache &kc, int B, int T,
-                            const int32_t *seq_ids, const void *q, const triroute_compaction &cmp,
-                            void *o, hipStream_t st) {
-  const int64_t words = int64_t(B) * T * c.n_heads * c.head_dim * act_bytes(c) / 4;
-  hipError_t e = tr::launch_fill_u32(o, words, 0u, st);
+                            const int32_t *seq_ids, const void *q, const uint8_t *mode,
+                            const triroute_compaction &cmp, void *o, hipStream_t st) {
+  // the rows no attention block writes: skipped heads, dropped rows
+  hipError_t e = tr::launch_attn_zero_rows(c, B, T, mode, seq_ids, kc.n_seq, o, st);
   if (e != hipSuccess) return e;
   const tr::CacheView v = tr::make_view(c, kc);
   return c.act == TRIROUTE_BF16 ? tr::launch_attn_mfma_prefill(c, v, B, T, seq_ids, q, cmp, o, st)
@@ -879,7 +879,7 @@ int triroute_attn_prefill(const triroute_cfg *cfg, int B, int T, const int32_t *
           "NULL argument");
   TRY(check_aligned({q, o}));
   TRY(check_ws(*cfg, TRIROUTE_OP_ATTN_PREFILL, B, T, ws, ws_bytes));
-  CHECK_HIP(run_attn_prefill(*cfg, *cache, B, T, seq_ids, q, *cmp, o, (hipStream_t)stream),
+  CHECK_HIP(run_attn_prefill(*cfg, *cache, B, T, seq_ids, q, mode, *cmp, o, (hipStream_t)stream),
             "attn_prefill launch");
   return TRIROUTE_OK;
 }
@@ -1005,7 +1005,7 @@ static int layer_impl(const triroute_cfg *cfg, int B, int T, bool decode, const 
     CHECK_HIP(run_attn_decode(*cfg, *cache, B, seq_ids, L.q, L.mode, L.o, part, st),
               "attn_decode launch");
   } else {
-    CHECK_HIP(run_attn_prefill(*cfg, *cache, B, T, seq_ids, L.q, L.cmp, L.o, st),
+    CHECK_HIP(run_attn_prefill(*cfg, *cache, B, T, seq_ids, L.q, L.mode, L.cmp, L.o, st),
               "attn_prefill launch");
   }
   CHECK_HIP(tr::launch_oproj(*cfg, N, x, L.o, *dw, L.xt, st), "oproj launch");

@@ -121,6 +121,10 @@ hipError_t launch_moe_norm_rows(const triroute_cfg &cfg, int N, const void *x, c
 inline int moe_ysplit(const triroute_cfg &c, int N) {
   return c.act == TRIROUTE_BF16 && N * c.top_k <= 2048 && c.d_ff % 128 == 0 ? 2 : 1;
 }
+// zero the prefill attention rows no attention block writes (skipped heads,
+// rows of sequence ids outside [0, n_seq))
+hipError_t launch_attn_zero_rows(const triroute_cfg &cfg, int B, int T, const uint8_t *mode,
+                                 const int32_t *seq_ids, int n_seq, void *o, hipStream_t st);
 hipError_t launch_psi_next(const triroute_cfg &cfg, int N, const float *psi, const uint8_t *mode,
                            const uint8_t *bit, const int32_t *eidx, float *out, hipStream_t st);
 hipError_t launch_moe_combine(const triroute_cfg &cfg, int N, const void *xt, const float *Y,

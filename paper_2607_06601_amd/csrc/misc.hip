@@ -246,6 +246,39 @@ hipError_t launch_moe_combine(const triroute_cfg &cfg, int N, const void *xt, co
   return hipGetLastError();
 }
 
+// The attention output rows the prefill kernels leave unwritten, zeroed:
+// skipped heads (any mode but local or full), and every head of a row whose
+// sequence id lies outside the cache (that row is dropped and flagged).  One
+// thread per (token, head) row, writing its 16-byte chunks only when the row
+// needs zeros; rows of attended heads are not touched.
+__global__ __launch_bounds__(256) void attn_zero_rows_kernel(uint4 *__restrict__ o,
+                                                             const uint8_t *__restrict__ mode,
+                                                             const int32_t *__restrict__ seq_ids,
+                                                             int n_seq, uint32_t row_tokens,
+                                                             int chunks, uint32_t pairs) {
+  const uint32_t pair = blockIdx.x * 256u + threadIdx.x;  // token * H + head (< 2^31, host)
+  if (pair >= pairs) return;
+  const int b = int(pair / row_tokens);  // row_tokens = H T pairs per batch row
+  const int s = seq_ids ? seq_ids[b] : b;
+  const int m = mode[pair];  // anything but local or full is in no attention list
+  if ((m != TRIROUTE_LOCAL && m != TRIROUTE_FULL) || s < 0 || s >= n_seq) {
+    uint4 *row = o + size_t(pair) * chunks;
+    for (int c = 0; c < chunks; ++c) row[c] = make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
+hipError_t launch_attn_zero_rows(const triroute_cfg &cfg, int B, int T, const uint8_t *mode,
+                                 const int32_t *seq_ids, int n_seq, void *o, hipStream_t st) {
+  const int chunks = cfg.head_dim * (cfg.act == TRIROUTE_BF16 ? 2 : 4) / 16;
+  const int64_t pairs = int64_t(B) * T * cfg.n_heads;
+  if (pairs <= 0) return hipSuccess;
+  if (pairs >= (int64_t(1) << 31)) return launch_fill_u32(o, pairs * chunks * 4, 0u, st);  // every row
+  attn_zero_rows_kernel<<<dim3(unsigned((pairs + 255) / 256)), 256, 0, st>>>(
+      (uint4 *)o, mode, seq_ids, n_seq, uint32_t(cfg.n_heads) * uint32_t(T), chunks,
+      uint32_t(pairs));
+  return hipGetLastError();
+}
+
 // Side features of the next layer of a stack (Sec. 3.3: the previous
 // layer's decisions among them): the caller's features with the last four
 // replaced by this token's decisions in the layer just run, as exact fp32

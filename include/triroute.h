@@ -323,7 +323,9 @@ const int32_t *triroute_kv_seq_len_ptr(const triroute_kv_cache *cache);
  * appended (the T tokens of row b occupy the last T positions of sequence
  * seq_ids[b]).  Query head h of token (b, t) at position P reads kv head
  * h / (H / Hkv): skip -> zeros, local -> keys [P - w + 1, P], full -> [0, P],
- * softmax(q k^T / sqrt(dh)) v over the dequantized cache.
+ * softmax(q k^T / sqrt(dh)) v over the dequantized cache.  Rows of a
+ * sequence id outside [0, n_seq), and heads whose mode byte is neither
+ * local nor full, are written as zeros.
  *   q act [B*T, H*dh]; mode u8 [B*T, H]; cmp from triroute_router; o act [B*T, H*dh]. */
 int triroute_attn_prefill(const triroute_cfg *cfg, int B, int T, const int32_t *seq_ids,
                           const void *q, const triroute_kv_cache *cache, const uint8_t *mode,
